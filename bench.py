@@ -1,0 +1,202 @@
+"""FrameFT adapter hot-path benchmark (one GPU).
+
+A step is the whole adapter hot path over one batch: forward (y_a) then
+backward (dX and dC on the support) of one adapted layer, inputs already in
+HBM.  Default workload: Llama-2-7B q_proj (4096 x 4096, frames k = 64,
+rho = 64 on both sides, 10,000 coefficients) on 8 x 512 = 4096 bf16 tokens.
+
+Prints ONE JSON line.  `roofline` describes the dominant kernel (the one with
+the longest average duration) as algorithmic HBM bytes per launch divided by
+its average duration, measured with HIP events recorded around that kernel on
+its stream during the timed steps.  `cpu_baseline` times the fp64 oracle on
+this machine's host on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E peak, GB/s
+METRIC = "FrameFT adapter fwd+bwd tokens/s @Llama-7B shapes; % of HBM roofline"
+CSRC = os.path.join(ROOT, "paper_2608_26430_amd", "csrc")
+
+
+def kernel_hash() -> str:
+    """Hash of every library source: identifies the kernels a profile or counter file belongs to."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(T, n, m, nnz, esz):
+    """Bytes each kernel must move at minimum (activations once, coefficients once)."""
+    fwd = T * esz * (n + m) + 4 * nnz                  # read x, write y_a; read c
+    bwd = T * esz * (m + 2 * n) + 4 * nnz              # read g, read x, write dX; read c
+    red = 4 * nnz                                       # write dC
+    return fwd, bwd, red
+
+
+def cpu_baseline(wl, ad, data, budget_s=12.0):
+    """fp64 oracle fwd+bwd on the first S tokens of the same workload, single-threaded."""
+    from threadpoolctl import threadpool_limits
+    from oracle import frameft_oracle as O
+    t0 = time.perf_counter()
+    P_in = O.tight_fusion_frame(ad.k_in, ad.rho_in, ad.d_in)
+    P_out = P_in if (ad.k_out, ad.rho_out, ad.d_out) == (ad.k_in, ad.rho_in, ad.d_in) else \
+        O.tight_fusion_frame(ad.k_out, ad.rho_out, ad.d_out)
+    setup = time.perf_counter() - t0
+    S, elapsed = 16, 0.0
+    with threadpool_limits(limits=1):
+        while True:
+            S = min(S, wl.tokens)
+            t0 = time.perf_counter()
+            O.adapter_fwd(P_in, P_out, data.rows, data.cols, data.vals, data.scale, data.X[:S])
+            O.adapter_bwd(P_in, P_out, data.rows, data.cols, data.vals, data.scale, data.X[:S], data.G[:S])
+            elapsed = time.perf_counter() - t0
+            if elapsed >= budget_s / 3 or S == wl.tokens:
+                break
+            S = int(S * max(2.0, min(8.0, (budget_s / 3) / max(elapsed, 1e-3))))
+    return {"value": round(S / elapsed, 2), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {S} of {wl.tokens} tokens, fp64 scipy-sparse oracle fwd+bwd (dX, dC), "
+                      f"1 thread, frame construction ({setup:.1f} s) excluded",
+            "seconds": round(elapsed, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="cfg2_llama7b_qproj")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (the adapter shards "
+              "over tokens with one dC all-reduce, see the design notes); run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_26430_amd as ff
+    from paper_2608_26430_amd import inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    wl = inputs.WORKLOADS[args.workload]
+    ad = wl.adapters[0]
+    data = inputs.adapter_data(wl, ad)
+    T, n, m, nnz = wl.tokens, ad.d_in, ad.d_out, ad.nnz
+    esz = 2 if wl.dtype == "bf16" else 4
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+
+    t0 = time.perf_counter()
+    f_in = ff.framegen(n, ad.k_in, ad.rho_in)
+    f_out = f_in if (m, ad.k_out, ad.rho_out) == (n, ad.k_in, ad.rho_in) else ff.framegen(m, ad.k_out, ad.rho_out)
+    plan = ff.plan_create(f_in, f_out, data.rows, data.cols, max_tokens=T)
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t0
+
+    X = torch.from_numpy(data.X).to(dev, tdt)
+    G = torch.from_numpy(data.G).to(dev, tdt)
+    c = torch.from_numpy(data.vals).to(dev)
+    Y = torch.empty((T, m), dtype=tdt, device=dev)
+    dX = torch.empty((T, n), dtype=tdt, device=dev)
+    dC = torch.empty((nnz,), dtype=torch.float32, device=dev)
+
+    def step(evs=None):
+        if evs is not None:
+            ff.binding.time_next_kernel(evs[0], evs[1])
+        ff.adapter_fwd(plan, X, c, data.scale, Y=Y)
+        if evs is not None:
+            ff.binding.time_next_kernel(evs[2], evs[3])
+        ff.adapter_bwd(plan, X, G, c, data.scale, dX=dX, dC=dC)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: K whole steps, no per-kernel events (step time)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3
+    ms_per_step = start.elapsed_time(stop) / args.steps
+
+    # per-kernel durations: the same steps with events around the fused kernels
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    fwd_us = 1e3 * float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    bwd_us = 1e3 * float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+
+    b_fwd, b_bwd, b_red = algorithmic_bytes(T, n, m, nnz, esz)
+    if bwd_us >= fwd_us:
+        dom, dom_us, dom_bytes = "bwd_kernel", bwd_us, b_bwd
+    else:
+        dom, dom_us, dom_bytes = "fwd_kernel", fwd_us, b_fwd
+    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
+    traffic = None
+    tfile = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
+    if os.path.exists(tfile):
+        tr = json.load(open(tfile))
+        if tr.get("kernel_hash") == kernel_hash() and dom in tr.get("bytes_per_launch", {}):
+            traffic = tr["bytes_per_launch"][dom]
+    step_bytes = b_fwd + b_bwd + b_red
+    value = T / (ms_per_step * 1e-3)
+
+    # context: the frozen W0 GEMM of this layer through the vendor BLAS (not part of the step)
+    W0 = torch.randn((m, n), device=dev, dtype=tdt)
+    for _ in range(3):
+        torch.matmul(X, W0.t())
+    torch.cuda.synchronize()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record()
+    for _ in range(10):
+        torch.matmul(X, W0.t())
+    g1.record()
+    torch.cuda.synchronize()
+    gemm_us = 1e3 * g0.elapsed_time(g1) / 10
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {ad.name} {n}->{m}, frames (k={ad.k_in}, rho={ad.rho_in}) -> "
+                               f"(k={ad.k_out}, rho={ad.rho_out}), nnz={nnz}, {T} tokens, fwd+bwd(dX,dC)",
+                   "tokens": T, "d_in": n, "d_out": m, "nnz": nnz},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": dom_bytes, "avg_us": round(dom_us, 3)},
+        "step_roofline": {"bytes_per_step": step_bytes, "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9
+                                                                       / HBM_PEAK_GBS, 4),
+                          "fwd_kernel_us": round(fwd_us, 3), "bwd_kernel_us": round(bwd_us, 3)},
+        "context": {"w0_gemm_us": round(gemm_us, 2), "setup_s": round(setup_s, 3),
+                    "wall_ms_timed": round(wall_ms, 3),
+                    "tile_tokens": plan.tile_tokens(wl.dtype), "kernel_hash": kernel_hash()},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, ad, data)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,148 @@
+// Internal declarations of libframeft: frame and plan objects, the device
+// descriptors handed to kernels, and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "../../include/frameft.h"
+
+namespace ff {
+
+// Padding (elements) after each 2k-wide frame block inside an LDS token row,
+// so that the 16 rows of an MFMA fragment do not start on the same LDS bank.
+constexpr int kBlockPad = 8;
+// Largest LDS allocation of one workgroup on gfx950.
+constexpr int kMaxLdsBytes = 160 * 1024;
+// Upper bound on tokens per workgroup tile.
+constexpr int kMaxTileTokens = 64;
+// Threads per workgroup of the fused forward / backward kernels.
+constexpr int kFusedThreads = 512;
+
+// Device form of a frame: the 2k x 2k block B (every diagonal block of P is B
+// when k*rho = d) as MFMA fragments for analysis (P^T) and synthesis (P).
+struct FrameDev {
+  int d;      // real dimension
+  int W;      // block width 2k
+  int nblk;   // number of blocks rho/2
+  int MT;     // 16-row output tiles, ceil(W/16)
+  int KT;     // bf16 contraction steps of 32, ceil(W/32)
+  int KT4;    // fp32 contraction steps of 16, ceil(W/16)
+  const void* fa16;  // analysis   fragments, bf16x8 [MT][KT][64]
+  const void* fs16;  // synthesis  fragments, bf16x8 [MT][KT][64]
+  const void* fa32;  // analysis   fragments, f32x4  [MT][KT4][64]
+  const void* fs32;  // synthesis  fragments, f32x4  [MT][KT4][64]
+  const float* B32;  // B, W x W row-major fp32: B[u][c], u = local coordinate, c = local coefficient
+};
+
+// Device tables of a plan.  "LDS offset" means an element offset inside one
+// token row of an LDS tile laid out block by block (block stride W + kBlockPad).
+struct PlanDev {
+  // v = C z: one slot per row of C (block order), slots sorted by row length.
+  const int* fwd_slot_off;   // LDS offset of the slot's row in the v tile
+  const int* fwd_ptr;        // slot -> [ptr[s], ptr[s+1]) entries
+  const int2* fwd_ent;       // (LDS offset of the column in the z tile, user index e)
+  int fwd_nslots;
+  // q = C^T u: one slot per column of C, sorted by column length.
+  const int* bwd_slot_off;   // LDS offset of the slot's column in the q tile
+  const int* bwd_ptr;
+  const int2* bwd_ent;       // (LDS offset of the row in the u tile, user index e)
+  int bwd_nslots;
+  // dC: per user entry e, (LDS offset of row in u tile, LDS offset of column in z tile).
+  const int2* sdd;
+  // merge: entries bucketed by (output block R, input block S), bucket = R*nblk_in + S.
+  const int* mrg_ptr;
+  const int4* mrg_ent;       // (local row a', local column b', user index e, 0)
+  int mrg_max_bucket;
+  int nnz;
+};
+
+// Entry streams of the 128-wide fused kernels: per pair of adjacent 128-wide
+// blocks, `len` rows of 64 lane slots starting at stream row `off`.
+struct FastPlanDev {
+  int enabled = 0;
+  const int* fwd_off = nullptr;   // v = C z, per output pair
+  const int* fwd_len = nullptr;
+  const uint2* fwd_st = nullptr;
+  const int* bwd_off = nullptr;   // q = C^T u, per input pair
+  const int* bwd_len = nullptr;
+  const uint2* bwd_st = nullptr;
+  const int* sdd_off = nullptr;   // dC, per input pair
+  const int* sdd_len = nullptr;
+  const uint2* sdd_st = nullptr;
+  int sdd_slots = 0;              // 64 * total dC stream rows
+};
+
+}  // namespace ff
+
+struct ff_frame {
+  std::atomic<int> refs{1};
+  int64_t d = 0, k = 0, rho = 0;
+  int device = 0;
+  std::vector<double> B;   // W x W fp64 block on the host
+  bool transpose_is_sign_flip = false;   // B^T == D B D exactly, D = diag((-1)^i)
+  void* dev_mem = nullptr;
+  ff::FrameDev dev{};
+};
+
+struct ff_plan {
+  ff_frame* fin = nullptr;
+  ff_frame* fout = nullptr;
+  int64_t nnz = 0, max_tokens = 0, max_batch = 1;
+  int device = 0;
+  int ldb_in = 0, ldb_out = 0;     // LDS block strides (elements)
+  int ldt_in[2] = {0, 0};          // LDS token strides of the input-side tile, [FF_F32], [FF_BF16]
+  int ldt_out[2] = {0, 0};
+  int tile_tokens[2] = {0, 0};     // tokens per fused-kernel tile
+  size_t lds_bytes[2] = {0, 0};
+  int64_t max_tiles = 0;           // tiles of the largest call, per adapter
+  float* partial = nullptr;        // dC partial sums, [batch][tile][nnz]
+  size_t workspace_bytes = 0;
+  void* dev_mem = nullptr;
+  ff::PlanDev dev{};
+  ff::FastPlanDev fast{};
+};
+
+namespace ff {
+
+// Error reporting (capi.cpp): remember a message for ff_last_error and return s.
+ff_status fail(ff_status s, const char* fmt, ...);
+void clear_error();
+
+// One-shot kernel timing events armed by ff_time_next_kernel.
+void take_timing_events(hipEvent_t* start, hipEvent_t* stop);
+
+// Launchers (kernels.hip).  Arguments are validated by the caller.
+struct ActPtrs {          // one tensor: either a single pointer or a device array of pointers
+  const void* one;
+  const void* const* many;
+};
+
+hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx,
+                      const float* c, const float* const* cs, float scale, float beta,
+                      ActPtrs Y, int64_t ldy, hipStream_t s);
+hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx,
+                      ActPtrs G, int64_t ldg, const float* c, const float* const* cs, float scale,
+                      float beta_dx, ActPtrs dX, int64_t lddx, bool want_dx, int accumulate_dc,
+                      float* dC, float* const* dCs, bool want_dc, hipStream_t s);
+hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf16, float beta,
+                        void* W, int64_t ldw, hipStream_t s);
+// Set the per-kernel dynamic LDS limits once per process.
+hipError_t configure_kernels();
+
+// 128-wide fused path (kernels_w128.hip).
+hipError_t configure_fast128();
+size_t fast128_lds_bytes(int nblk);
+hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, const float* c,
+                         const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, hipStream_t s);
+hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G, int64_t ldg,
+                         const float* c, const float* const* cs, float scale, float beta_dx, ActPtrs dX,
+                         int64_t lddx, bool want_dx, int accumulate_dc, float* dC, float* const* dCs, bool want_dc,
+                         hipStream_t s);
+constexpr int kFastTileTokens = 8;
+
+}  // namespace ff

@@ -1,0 +1,323 @@
+// Frame generation (Algorithm 1, step 2): the real (k, rho, d) tight fusion
+// frame of Sec. 3.2, built on the host in fp64 and placed on the device as
+// MFMA fragments of its diagonal block.
+//
+// Construction (appendix "Fusion Frames Construction: an example"):
+//   1. Spectral Tetris: a unit-norm tight frame F of d_c = d/2 vectors in
+//      C^{rho_c}, rho_c = rho/2.  Each row must reach squared norm d_c/rho_c;
+//      it is filled with ones while a whole unit is missing, and a leftover x in
+//      (0,1) is placed by the 2x2 block T(x) = [[sqrt(x/2), sqrt(x/2)],
+//      [sqrt((2-x)/2), -sqrt((2-x)/2)]] whose lower row starts the next row.
+//      Norms are kept as integer multiples of 1/rho_c, so every comparison is
+//      exact.
+//   2. Modulation: vector (i, r) = row r of F times (e^{2 pi i i j / k})_j,
+//      scaled by 1/sqrt(k) (Parseval normalisation).
+//   3. Real extension x + iy -> [[x, -y], [y, x]].
+// Column order is canonical: i*rho + 2r + s.
+//
+// When k*rho = d every row of F is k consecutive ones, so P is block diagonal
+// with rho/2 identical square blocks B (2k x 2k): B[2 tau + t][2 i + s] is the
+// entry of column (i, r, s) at real row 2(r k + tau) + t.  The device works on
+// B alone.
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <utility>
+
+#include "ff_internal.h"
+
+namespace {
+
+struct TetrisEntry {
+  int64_t r;   // row of F
+  int64_t j;   // column of F
+  double v;
+};
+
+// Spectral Tetris F (rho_c x d_c) as a list of nonzeros in column order.
+ff_status spectral_tetris(int64_t rho_c, int64_t d_c, std::vector<TetrisEntry>& F) {
+  if (rho_c < 1 || d_c < rho_c)
+    return ff::fail(FF_ENOTFF, "Spectral Tetris needs d/2 >= rho/2 >= 1 (rho_c=%lld, d_c=%lld)",
+                    (long long)rho_c, (long long)d_c);
+  F.clear();
+  const int64_t unit = rho_c;      // one unit of squared norm, in units of 1/rho_c
+  const int64_t target = d_c;      // squared row norm d_c/rho_c, in units of 1/rho_c
+  int64_t col = 0, carried = 0;
+  for (int64_t r = 0; r < rho_c; ++r) {
+    int64_t missing = target - carried;
+    if (missing < 0)
+      return ff::fail(FF_ENOTFF, "Spectral Tetris: row %lld overfilled", (long long)r);
+    while (missing >= unit) {
+      if (col >= d_c) return ff::fail(FF_ENOTFF, "Spectral Tetris ran out of columns");
+      F.push_back({r, col, 1.0});
+      ++col;
+      missing -= unit;
+    }
+    if (missing > 0) {
+      if (r + 1 >= rho_c || col + 2 > d_c)
+        return ff::fail(FF_ENOTFF, "Spectral Tetris: leftover norm in the last row");
+      // x = missing/rho_c; entries sqrt(x/2) and sqrt((2-x)/2), each ratio rounded once.
+      const double a = std::sqrt((double)missing / (double)(2 * rho_c));
+      const double b = std::sqrt((double)(2 * unit - missing) / (double)(2 * rho_c));
+      F.push_back({r, col, a});
+      F.push_back({r + 1, col, b});
+      F.push_back({r, col + 1, a});
+      F.push_back({r + 1, col + 1, -b});
+      col += 2;
+      carried = 2 * unit - missing;
+    } else {
+      carried = 0;
+    }
+  }
+  if (col != d_c) return ff::fail(FF_ENOTFF, "Spectral Tetris filled %lld of %lld columns",
+                                  (long long)col, (long long)d_c);
+  return FF_OK;
+}
+
+// Tightness of the modulated frame: F's columns j != j' with j = j' (mod k)
+// must be orthogonal (the roots-of-unity sum removes every other pair).
+ff_status check_tight(const std::vector<TetrisEntry>& F, int64_t k) {
+  std::map<int64_t, std::vector<std::pair<int64_t, double>>> by_row;
+  for (const auto& e : F) by_row[e.r].push_back({e.j, e.v});
+  std::map<std::pair<int64_t, int64_t>, double> ip;
+  for (const auto& kv : by_row) {
+    const auto& cols = kv.second;
+    for (size_t a = 0; a < cols.size(); ++a)
+      for (size_t b = a + 1; b < cols.size(); ++b)
+        if ((cols[a].first - cols[b].first) % k == 0)
+          ip[{cols[a].first, cols[b].first}] += cols[a].second * cols[b].second;
+  }
+  for (const auto& kv : ip)
+    if (std::fabs(kv.second) > 1e-12)
+      return ff::fail(FF_ENOTFF, "columns %lld and %lld of F are not orthogonal: not a tight frame",
+                      (long long)kv.first.first, (long long)kv.first.second);
+  return FF_OK;
+}
+
+// Nonzeros of real column c (canonical index) of P: (real row, value).
+void real_column(const std::vector<std::vector<std::pair<int64_t, double>>>& Frows, int64_t k,
+                 int64_t rho, int64_t c, std::vector<std::pair<int64_t, double>>& out) {
+  out.clear();
+  const int64_t i = c / rho, rem = c % rho, r = rem / 2, s = rem % 2;
+  const double sqrt_k = std::sqrt((double)k);
+  for (const auto& jv : Frows[r]) {
+    const int64_t j = jv.first;
+    const int64_t m = (i * j) % k;                    // exponent reduced mod k
+    const double theta = (2.0 * M_PI * (double)m) / (double)k;
+    const double re = (jv.second * std::cos(theta)) / sqrt_k;
+    const double im = (jv.second * std::sin(theta)) / sqrt_k;
+    if (s == 0) {          // [Re; Im]
+      out.push_back({2 * j, re});
+      out.push_back({2 * j + 1, im});
+    } else {               // [-Im; Re]
+      out.push_back({2 * j, -im});
+      out.push_back({2 * j + 1, re});
+    }
+  }
+}
+
+ff_status build_host(int64_t d, int64_t k, int64_t rho,
+                     std::vector<std::vector<std::pair<int64_t, double>>>& Frows) {
+  if (d < 2 || rho < 2 || k < 1 || (d % 2) || (rho % 2))
+    return ff::fail(FF_EINVAL, "need k >= 1 and even d, rho >= 2 (d=%lld, k=%lld, rho=%lld)",
+                    (long long)d, (long long)k, (long long)rho);
+  if (d > (int64_t)1 << 24 || k * rho > (int64_t)1 << 26)
+    return ff::fail(FF_EINVAL, "frame too large");
+  std::vector<TetrisEntry> F;
+  ff_status st = spectral_tetris(rho / 2, d / 2, F);
+  if (st != FF_OK) return st;
+  st = check_tight(F, k);
+  if (st != FF_OK) return st;
+  Frows.assign(rho / 2, {});
+  for (const auto& e : F) Frows[e.r].push_back({e.j, e.v});
+  return FF_OK;
+}
+
+uint16_t bf16_rne(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;   // NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+}  // namespace
+
+extern "C" ff_status ff_tff_host(int64_t d, int64_t k, int64_t rho, int64_t col0, int64_t ncols,
+                                 double* out) {
+  ff::clear_error();
+  if (!out) return ff::fail(FF_EINVAL, "out is NULL");
+  std::vector<std::vector<std::pair<int64_t, double>>> Frows;
+  ff_status st = build_host(d, k, rho, Frows);
+  if (st != FF_OK) return st;
+  if (col0 < 0 || ncols < 0 || col0 + ncols > k * rho)
+    return ff::fail(FF_EINVAL, "column range [%lld, %lld) outside [0, %lld)", (long long)col0,
+                    (long long)(col0 + ncols), (long long)(k * rho));
+  std::memset(out, 0, sizeof(double) * (size_t)d * (size_t)ncols);
+  std::vector<std::pair<int64_t, double>> colv;
+  for (int64_t c = 0; c < ncols; ++c) {
+    real_column(Frows, k, rho, col0 + c, colv);
+    for (const auto& rv : colv) out[rv.first * ncols + c] = rv.second;
+  }
+  return FF_OK;
+}
+
+extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** out) {
+  ff::clear_error();
+  if (!out) return ff::fail(FF_EINVAL, "out is NULL");
+  *out = nullptr;
+  std::vector<std::vector<std::pair<int64_t, double>>> Frows;
+  ff_status st = build_host(d, k, rho, Frows);
+  if (st != FF_OK) return st;
+  if (k * rho != d)
+    return ff::fail(FF_EUNSUPPORTED, "GPU path needs k*rho == d (k=%lld, rho=%lld, d=%lld)",
+                    (long long)k, (long long)rho, (long long)d);
+  const int64_t W = 2 * k;
+  if (W % 8 != 0)
+    return ff::fail(FF_EUNSUPPORTED, "GPU path needs 2k to be a multiple of 8 (k=%lld)", (long long)k);
+  if (W > 2048) return ff::fail(FF_EUNSUPPORTED, "frame block 2k=%lld too wide", (long long)W);
+
+  // Extract the diagonal block and confirm that P is block diagonal with identical blocks.
+  std::vector<double> B((size_t)(W * W), 0.0);
+  std::vector<std::pair<int64_t, double>> colv;
+  for (int64_t c = 0; c < k * rho; ++c) {
+    const int64_t i = c / rho, rem = c % rho, r = rem / 2, s = rem % 2;
+    const int64_t lc = 2 * i + s;
+    real_column(Frows, k, rho, c, colv);
+    for (const auto& rv : colv) {
+      const int64_t u = rv.first - r * W;
+      if (u < 0 || u >= W)
+        return ff::fail(FF_EUNSUPPORTED, "frame is not block diagonal (column %lld)", (long long)c);
+      if (r == 0) {
+        B[u * W + lc] = rv.second;
+      } else if (B[u * W + lc] != rv.second) {
+        return ff::fail(FF_EUNSUPPORTED, "frame blocks differ (column %lld)", (long long)c);
+      }
+    }
+  }
+
+  // The realified DFT block satisfies B^T = D B D (D flips odd coordinates); the 128-wide
+  // kernels rely on it to apply P^T with the fragments of P.  Checked exactly here.
+  bool sign_flip = true;
+  for (int64_t r = 0; r < W && sign_flip; ++r)
+    for (int64_t c = 0; c < W; ++c)
+      if (B[c * W + r] != (((r + c) & 1) ? -B[r * W + c] : B[r * W + c])) {
+        sign_flip = false;
+        break;
+      }
+
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ff::fail(FF_EDEVICE, "no HIP device");
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return ff::fail(FF_EDEVICE, "no HIP device");
+
+  ff::FrameDev fd{};
+  fd.d = (int)d;
+  fd.W = (int)W;
+  fd.nblk = (int)(rho / 2);
+  fd.MT = (int)((W + 15) / 16);
+  fd.KT = (int)((W + 31) / 32);
+  fd.KT4 = (int)((W + 15) / 16);
+  const size_t n16 = (size_t)fd.MT * fd.KT * 64 * 8;     // bf16 elements per fragment set
+  const size_t n32 = (size_t)fd.MT * fd.KT4 * 64 * 4;    // fp32 elements per fragment set
+  std::vector<uint16_t> fa16(n16, 0), fs16(n16, 0);
+  std::vector<float> fa32(n32, 0.f), fs32(n32, 0.f), B32((size_t)(W * W));
+  // analysis computes out[c] = sum_u B[u][c] in[u]  (matrix M_a[o][i] = B[i][o]);
+  // synthesis computes out[u] = sum_c B[u][c] in[c] (matrix M_s[o][i] = B[o][i]).
+  auto Ma = [&](int64_t o, int64_t i) { return (o < W && i < W) ? B[i * W + o] : 0.0; };
+  auto Ms = [&](int64_t o, int64_t i) { return (o < W && i < W) ? B[o * W + i] : 0.0; };
+  for (int mt = 0; mt < fd.MT; ++mt)
+    for (int lane = 0; lane < 64; ++lane) {
+      const int64_t o = 16 * mt + (lane & 15), q = lane >> 4;
+      for (int ks = 0; ks < fd.KT; ++ks)
+        for (int j = 0; j < 8; ++j) {
+          const size_t idx = (((size_t)mt * fd.KT + ks) * 64 + lane) * 8 + j;
+          const int64_t i = 32 * ks + 8 * q + j;
+          fa16[idx] = bf16_rne((float)Ma(o, i));
+          fs16[idx] = bf16_rne((float)Ms(o, i));
+        }
+      for (int ks = 0; ks < fd.KT4; ++ks)
+        for (int j = 0; j < 4; ++j) {
+          const size_t idx = (((size_t)mt * fd.KT4 + ks) * 64 + lane) * 4 + j;
+          const int64_t i = 16 * ks + 4 * q + j;
+          fa32[idx] = (float)Ma(o, i);
+          fs32[idx] = (float)Ms(o, i);
+        }
+    }
+  for (size_t e = 0; e < B32.size(); ++e) B32[e] = (float)B[e];
+
+  const size_t b16 = n16 * 2, b32 = n32 * 4, bB = B32.size() * 4;
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t total = 2 * up(b16) + 2 * up(b32) + up(bB);
+  void* mem = nullptr;
+  if (hipMalloc(&mem, total) != hipSuccess) {
+    (void)hipGetLastError();
+    return ff::fail(FF_ENOMEM, "hipMalloc of %zu bytes for frame failed", total);
+  }
+  char* p = (char*)mem;
+  size_t off = 0;
+  auto put = [&](const void* src, size_t bytes) -> const void* {
+    void* dst = p + off;
+    off += up(bytes);
+    return hipMemcpy(dst, src, bytes, hipMemcpyHostToDevice) == hipSuccess ? dst : nullptr;
+  };
+  fd.fa16 = put(fa16.data(), b16);
+  fd.fs16 = put(fs16.data(), b16);
+  fd.fa32 = put(fa32.data(), b32);
+  fd.fs32 = put(fs32.data(), b32);
+  fd.B32 = (const float*)put(B32.data(), bB);
+  if (!fd.fa16 || !fd.fs16 || !fd.fa32 || !fd.fs32 || !fd.B32) {
+    (void)hipFree(mem);
+    return ff::fail(FF_EDEVICE, "copying frame to the device failed");
+  }
+  if (ff::configure_kernels() != hipSuccess || ff::configure_fast128() != hipSuccess) {
+    (void)hipFree(mem);
+    return ff::fail(FF_EDEVICE, "configuring kernels failed");
+  }
+  ff_frame* f = new ff_frame();
+  f->d = d;
+  f->k = k;
+  f->rho = rho;
+  f->device = dev;
+  f->B = std::move(B);
+  f->transpose_is_sign_flip = sign_flip;
+  f->dev_mem = mem;
+  f->dev = fd;
+  *out = f;
+  return FF_OK;
+}
+
+extern "C" ff_status ff_frame_export(const ff_frame* f, int64_t col0, int64_t ncols, double* out) {
+  ff::clear_error();
+  if (!f || !out) return ff::fail(FF_EINVAL, "NULL argument");
+  const int64_t d = f->d, k = f->k, rho = f->rho, W = 2 * k;
+  if (col0 < 0 || ncols < 0 || col0 + ncols > k * rho)
+    return ff::fail(FF_EINVAL, "column range outside [0, %lld)", (long long)(k * rho));
+  std::vector<float> B32((size_t)(W * W));
+  if (hipMemcpy(B32.data(), f->dev.B32, B32.size() * 4, hipMemcpyDeviceToHost) != hipSuccess)
+    return ff::fail(FF_EDEVICE, "reading the frame back failed");
+  std::memset(out, 0, sizeof(double) * (size_t)d * (size_t)ncols);
+  for (int64_t cc = 0; cc < ncols; ++cc) {
+    const int64_t c = col0 + cc;
+    const int64_t i = c / rho, rem = c % rho, r = rem / 2, s = rem % 2;
+    for (int64_t u = 0; u < W; ++u) out[(r * W + u) * ncols + cc] = (double)B32[u * W + 2 * i + s];
+  }
+  return FF_OK;
+}
+
+extern "C" ff_status ff_frame_info(const ff_frame* f, int64_t* d, int64_t* k, int64_t* rho) {
+  ff::clear_error();
+  if (!f) return ff::fail(FF_EINVAL, "frame is NULL");
+  if (d) *d = f->d;
+  if (k) *k = f->k;
+  if (rho) *rho = f->rho;
+  return FF_OK;
+}
+
+extern "C" void ff_frame_destroy(ff_frame* f) {
+  if (!f) return;
+  if (f->refs.fetch_sub(1) == 1) {
+    if (f->dev_mem) (void)hipFree(f->dev_mem);
+    delete f;
+  }
+}

@@ -1,0 +1,544 @@
+// HIP kernels of the FrameFT adapter hot path for gfx950 (MI355X).
+//
+// With k*rho = d the frame P is block diagonal with identical 2k x 2k blocks
+// B, so applying P^T (analysis, Sec. 2.1) or P (synthesis) to one token is a
+// dense 2k x 2k product per block: over a tile of tokens it is one GEMM whose
+// rows are (token, block) pairs.  Those products run on MFMA
+// (v_mfma_f32_16x16x32_bf16 for bf16 activations, v_mfma_f32_16x16x4_f32 for
+// fp32), with the frame block as the A operand (fragments prepared by
+// ff_framegen) and 16 activation rows as the B operand.  The sparse
+// coefficient products (v = C z forward, q = C^T u and the support-restricted
+// dC = s sum_t u_t z_t^T backward, Appendix A) run on the vector ALUs from
+// LDS, where one tile's coefficient vectors are kept whole because the
+// support of C is uniformly random.
+//
+// Kernels:
+//   fwd_kernel    x -> z = P_in^T x (LDS) -> v = C z (LDS) -> y = beta y + s P_out v
+//   bwd_kernel    g -> u = P_out^T g (LDS), x -> z = P_in^T x (LDS)
+//                 -> dC partial per tile: sum_t u[a_e] z[b_e]
+//                 -> q = C^T u (LDS, over z) -> dX = beta dX + s P_in q
+//   dc_reduce     dC[e] = [dC[e] +] s * sum_tiles partial[tile][e]   (fixed order)
+//   merge_kernel  W = beta W + s P_out C P_in^T, per (output block, input block)
+//                 tile as a sum of rank-1 products of block columns.
+#include <algorithm>
+
+#include "ff_internal.h"
+
+namespace ff {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16;
+
+__device__ __forceinline__ float bf2f(u16 h) { return __uint_as_float((unsigned)h << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ u16 f2bf(float f) {
+  unsigned u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (u16)(u >> 16);
+}
+
+template <bool BF16>
+struct Act;
+
+template <>
+struct Act<true> {
+  using E = u16;
+  static __device__ __forceinline__ float ld(const E* p) { return bf2f(*p); }
+  static __device__ __forceinline__ void st(E* p, float v) { *p = f2bf(v); }
+  static __device__ __forceinline__ f32x4 ld4(const E* p) {
+    const uint2 w = *reinterpret_cast<const uint2*>(p);
+    return f32x4{bf2f((u16)(w.x & 0xffff)), bf2f((u16)(w.x >> 16)), bf2f((u16)(w.y & 0xffff)),
+                 bf2f((u16)(w.y >> 16))};
+  }
+  static __device__ __forceinline__ void st4(E* p, f32x4 v) {
+    uint2 w;
+    w.x = (unsigned)f2bf(v[0]) | ((unsigned)f2bf(v[1]) << 16);
+    w.y = (unsigned)f2bf(v[2]) | ((unsigned)f2bf(v[3]) << 16);
+    *reinterpret_cast<uint2*>(p) = w;
+  }
+};
+
+template <>
+struct Act<false> {
+  using E = float;
+  static __device__ __forceinline__ float ld(const E* p) { return *p; }
+  static __device__ __forceinline__ void st(E* p, float v) { *p = v; }
+  static __device__ __forceinline__ f32x4 ld4(const E* p) { return *reinterpret_cast<const f32x4*>(p); }
+  static __device__ __forceinline__ void st4(E* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+};
+
+// Output tiles (16 outputs each) computed per pass over the contraction.
+constexpr int kCH = 8;
+
+// acc[c] (lane's 4 outputs 16*(mt0+c) + 4*(lane>>4) + j of the lane's row) =
+// sum_i M[o][i] * in[i], where M is the frame block in analysis or synthesis
+// orientation and `in` points at the lane's activation row (2k values).
+template <bool BF16>
+__device__ __forceinline__ void apply_chunk(const FrameDev& f, bool synth, int mt0,
+                                            const typename Act<BF16>::E* in, bool valid, int lane,
+                                            f32x4 (&acc)[kCH]) {
+  const int q = lane >> 4;
+#pragma unroll
+  for (int c = 0; c < kCH; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (BF16) {
+    const bf16x8* fr = reinterpret_cast<const bf16x8*>(synth ? f.fs16 : f.fa16);
+    for (int ks = 0; ks < f.KT; ++ks) {
+      const int i0 = ks * 32 + q * 8;
+      bf16x8 b = {};
+      if (valid && i0 < f.W) b = *reinterpret_cast<const bf16x8*>(in + i0);
+#pragma unroll
+      for (int c = 0; c < kCH; ++c) {
+        const int mt = mt0 + c;
+        if (mt < f.MT) {
+          const bf16x8 a = fr[((size_t)mt * f.KT + ks) * 64 + lane];
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[c], 0, 0, 0);
+        }
+      }
+    }
+  } else {
+    const f32x4* fr = reinterpret_cast<const f32x4*>(synth ? f.fs32 : f.fa32);
+    for (int ks = 0; ks < f.KT4; ++ks) {
+      const int i0 = ks * 16 + q * 4;
+      f32x4 b = {0.f, 0.f, 0.f, 0.f};
+      if (valid && i0 < f.W) b = *reinterpret_cast<const f32x4*>(in + i0);
+#pragma unroll
+      for (int c = 0; c < kCH; ++c) {
+        const int mt = mt0 + c;
+        if (mt < f.MT) {
+          const f32x4 a = fr[((size_t)mt * f.KT4 + ks) * 64 + lane];
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc[c], 0, 0, 0);
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], acc[c], 0, 0, 0);
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], acc[c], 0, 0, 0);
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], acc[c], 0, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+// Apply the frame block to every (token, block) row of a tile.  Row r is
+// token t = r / nblk, block b = r % nblk; its input starts at
+// src + t*src_ld + b*src_bs.  epi(t, b, o, acc) consumes outputs o..o+3.
+template <bool BF16, class Epi>
+__device__ __forceinline__ void frame_apply(const FrameDev& f, bool synth, int nrows,
+                                            const typename Act<BF16>::E* src, long src_ld, int src_bs,
+                                            Epi epi) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int q = lane >> 4;
+  for (int g = wave; g * 16 < nrows; g += nw) {
+    const int row = g * 16 + (lane & 15);
+    const bool valid = row < nrows;
+    const int rr = valid ? row : 0;
+    const int t = rr / f.nblk, b = rr - t * f.nblk;
+    const typename Act<BF16>::E* in = src + (long)t * src_ld + (long)b * src_bs;
+    for (int mt0 = 0; mt0 < f.MT; mt0 += kCH) {
+      f32x4 acc[kCH];
+      apply_chunk<BF16>(f, synth, mt0, in, valid, lane, acc);
+      if (valid) {
+#pragma unroll
+        for (int c = 0; c < kCH; ++c) {
+          const int o = 16 * (mt0 + c) + 4 * q;
+          if (o < f.W) epi(t, b, o, acc[c]);
+        }
+      }
+    }
+  }
+}
+
+struct FwdArgs {
+  FrameDev fin, fout;
+  int T, tt, ldt_in, ldt_out, ldb_in, ldb_out;
+  const void* X;
+  const void* const* Xs;
+  long ldx;
+  void* Y;
+  void* const* Ys;
+  long ldy;
+  const float* c;
+  const float* const* cs;
+  float scale, beta;
+  const int* slot_off;
+  const int* ptr;
+  const int2* ent;
+  int nslots;
+};
+
+template <bool BF16>
+__global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
+  using A = Act<BF16>;
+  using E = typename A::E;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  E* zt = reinterpret_cast<E*>(smem);           // tt x ldt_in   z = P_in^T x
+  E* vt = zt + (size_t)a.tt * a.ldt_in;         // tt x ldt_out  v = C z
+  const int bi = blockIdx.y;
+  const E* X = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X);
+  E* Y = reinterpret_cast<E*>(a.Ys ? a.Ys[bi] : a.Y);
+  const float* cv = a.cs ? a.cs[bi] : a.c;
+  const int t0 = blockIdx.x * a.tt;
+  const int nt = min(a.tt, a.T - t0);
+  X += (long)t0 * a.ldx;
+  Y += (long)t0 * a.ldy;
+
+  // analysis: z = P_in^T x for every (token, input block)
+  frame_apply<BF16>(a.fin, false, nt * a.fin.nblk, X, a.ldx, a.fin.W,
+                    [&](int t, int b, int o, f32x4 v) { A::st4(zt + t * a.ldt_in + b * a.ldb_in + o, v); });
+  __syncthreads();
+
+  // coefficients: v[a] = sum_{e in row a} c_e z[b_e]; lanes of one slot take consecutive tokens
+  for (int it = threadIdx.x; it < a.nslots * nt; it += blockDim.x) {
+    const int slot = it / nt, t = it - slot * nt;
+    const int beg = a.ptr[slot], end = a.ptr[slot + 1];
+    const E* zr = zt + t * a.ldt_in;
+    float acc = 0.f;
+    for (int j = beg; j < end; ++j) {
+      const int2 en = a.ent[j];
+      acc = fmaf(cv[en.y], A::ld(zr + en.x), acc);
+    }
+    A::st(vt + t * a.ldt_out + a.slot_off[slot], acc);
+  }
+  __syncthreads();
+
+  // synthesis and epilogue: y = beta y + s P_out v
+  const float s = a.scale, beta = a.beta;
+  frame_apply<BF16>(a.fout, true, nt * a.fout.nblk, vt, a.ldt_out, a.ldb_out,
+                    [&](int t, int b, int o, f32x4 v) {
+                      E* yp = Y + (long)t * a.ldy + b * a.fout.W + o;
+                      f32x4 r = v * s;
+                      if (beta != 0.f) r += beta * A::ld4(yp);
+                      A::st4(yp, r);
+                    });
+}
+
+struct BwdArgs {
+  FrameDev fin, fout;
+  int T, tt, ldt_in, ldt_out, ldb_in, ldb_out;
+  const void* X;
+  const void* const* Xs;
+  long ldx;
+  const void* G;
+  const void* const* Gs;
+  long ldg;
+  void* dX;
+  void* const* dXs;
+  long lddx;
+  const float* c;
+  const float* const* cs;
+  float scale, beta;
+  int want_dx, want_dc;
+  // q = C^T u tables
+  const int* slot_off;
+  const int* ptr;
+  const int2* ent;
+  int nslots;
+  // dC tables and partial sums [batch][tile][nnz]
+  const int2* sdd;
+  int nnz;
+  float* partial;
+  long ntiles;
+};
+
+template <bool BF16>
+__global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
+  using A = Act<BF16>;
+  using E = typename A::E;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  E* ut = reinterpret_cast<E*>(smem);           // tt x ldt_out  u = P_out^T g
+  E* zt = ut + (size_t)a.tt * a.ldt_out;        // tt x ldt_in   z = P_in^T x, later q = C^T u
+  const int bi = blockIdx.y;
+  const int t0 = blockIdx.x * a.tt;
+  const int nt = min(a.tt, a.T - t0);
+  const E* G = reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G) + (long)t0 * a.ldg;
+
+  frame_apply<BF16>(a.fout, false, nt * a.fout.nblk, G, a.ldg, a.fout.W,
+                    [&](int t, int b, int o, f32x4 v) { A::st4(ut + t * a.ldt_out + b * a.ldb_out + o, v); });
+  if (a.want_dc) {
+    const E* X = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx;
+    frame_apply<BF16>(a.fin, false, nt * a.fin.nblk, X, a.ldx, a.fin.W,
+                      [&](int t, int b, int o, f32x4 v) { A::st4(zt + t * a.ldt_in + b * a.ldb_in + o, v); });
+  }
+  __syncthreads();
+
+  if (a.want_dc) {
+    // this tile's share of dC_e / s = sum_t u_t[row_e] z_t[col_e]
+    float* part = a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.nnz;
+    for (int e = threadIdx.x; e < a.nnz; e += blockDim.x) {
+      const int2 o = a.sdd[e];
+      float acc = 0.f;
+      for (int t = 0; t < nt; ++t) acc = fmaf(A::ld(ut + t * a.ldt_out + o.x), A::ld(zt + t * a.ldt_in + o.y), acc);
+      part[e] = acc;
+    }
+    if (!a.want_dx) return;
+    __syncthreads();
+  }
+
+  // q[b] = sum_{e in column b} c_e u[a_e], written over z
+  const float* cv = a.cs ? a.cs[bi] : a.c;
+  for (int it = threadIdx.x; it < a.nslots * nt; it += blockDim.x) {
+    const int slot = it / nt, t = it - slot * nt;
+    const int beg = a.ptr[slot], end = a.ptr[slot + 1];
+    const E* ur = ut + t * a.ldt_out;
+    float acc = 0.f;
+    for (int j = beg; j < end; ++j) {
+      const int2 en = a.ent[j];
+      acc = fmaf(cv[en.y], A::ld(ur + en.x), acc);
+    }
+    A::st(zt + t * a.ldt_in + a.slot_off[slot], acc);
+  }
+  __syncthreads();
+
+  E* dX = reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX) + (long)t0 * a.lddx;
+  const float s = a.scale, beta = a.beta;
+  frame_apply<BF16>(a.fin, true, nt * a.fin.nblk, zt, a.ldt_in, a.ldb_in, [&](int t, int b, int o, f32x4 v) {
+    E* p = dX + (long)t * a.lddx + b * a.fin.W + o;
+    f32x4 r = v * s;
+    if (beta != 0.f) r += beta * A::ld4(p);
+    A::st4(p, r);
+  });
+}
+
+__global__ void __launch_bounds__(256) dc_reduce(const float* __restrict__ partial, long ntiles, int nnz,
+                                                 float scale, int accumulate, float* dC, float* const* dCs) {
+  const int bi = blockIdx.y;
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= nnz) return;
+  const float* p = partial + (long)bi * ntiles * nnz + e;
+  float sum = 0.f;
+  for (long t = 0; t < ntiles; ++t) sum += p[t * nnz];
+  float* out = dCs ? dCs[bi] : dC;
+  const float v = scale * sum;
+  out[e] = accumulate ? out[e] + v : v;
+}
+
+struct MergeArgs {
+  const float* Bm;   // output-frame block, W_m x W_m
+  const float* Bn;   // input-frame block,  W_n x W_n
+  int Wm, Wn, nblk_in, rows_per_wg, nsub, chunk;
+  const int* ptr;
+  const int4* ent;
+  const float* c;
+  float scale, beta;
+  void* W;
+  long ldw;
+};
+
+constexpr int kMergeThreads = 256;
+constexpr int kMergeEPT = 8;   // output elements per thread
+
+template <bool BF16W>
+__global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int OR = a.rows_per_wg;
+  float* cb = reinterpret_cast<float*>(smem);    // chunk x OR : s * c_e * B_m[u][a'_e]
+  float* bn = cb + a.chunk * OR;                 // chunk x W_n: B_n[p][b'_e]
+  const int sub = blockIdx.x % a.nsub;
+  const int tile = blockIdx.x / a.nsub;          // R * nblk_in + S
+  const int R = tile / a.nblk_in, S = tile - R * a.nblk_in;
+  const int u0 = sub * OR;
+  const int rows = min(OR, a.Wm - u0);
+  const int nel = rows * a.Wn;
+  int eo[kMergeEPT], ep[kMergeEPT];
+  float acc[kMergeEPT];
+#pragma unroll
+  for (int k = 0; k < kMergeEPT; ++k) {
+    const int idx = threadIdx.x + k * kMergeThreads;
+    eo[k] = idx < nel ? idx / a.Wn : -1;
+    ep[k] = idx < nel ? idx - eo[k] * a.Wn : 0;
+    acc[k] = 0.f;
+  }
+  const int beg = a.ptr[tile], end = a.ptr[tile + 1];
+  for (int c0 = beg; c0 < end; c0 += a.chunk) {
+    const int nch = min(a.chunk, end - c0);
+    for (int x = threadIdx.x; x < nch * OR; x += kMergeThreads) {
+      const int e = x / OR, u = x - e * OR;
+      const int4 en = a.ent[c0 + e];
+      cb[e * OR + u] = (u < rows) ? a.scale * a.c[en.z] * a.Bm[(u0 + u) * a.Wm + en.x] : 0.f;
+    }
+    for (int x = threadIdx.x; x < nch * a.Wn; x += kMergeThreads) {
+      const int e = x / a.Wn, p = x - e * a.Wn;
+      bn[e * a.Wn + p] = a.Bn[p * a.Wn + a.ent[c0 + e].y];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kMergeEPT; ++k) {
+      if (eo[k] >= 0) {
+        float s = acc[k];
+        for (int e = 0; e < nch; ++e) s = fmaf(cb[e * OR + eo[k]], bn[e * a.Wn + ep[k]], s);
+        acc[k] = s;
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int k = 0; k < kMergeEPT; ++k) {
+    if (eo[k] < 0) continue;
+    const long off = (long)(R * a.Wm + u0 + eo[k]) * a.ldw + (long)S * a.Wn + ep[k];
+    if constexpr (BF16W) {
+      u16* w = reinterpret_cast<u16*>(a.W) + off;
+      const float v = a.beta != 0.f ? a.beta * bf2f(*w) + acc[k] : acc[k];
+      *w = f2bf(v);
+    } else {
+      float* w = reinterpret_cast<float*>(a.W) + off;
+      *w = a.beta != 0.f ? a.beta * *w + acc[k] : acc[k];
+    }
+  }
+}
+
+void record(hipEvent_t ev, hipStream_t s) {
+  if (ev) (void)hipEventRecord(ev, s);
+}
+
+}  // namespace
+
+hipError_t configure_kernels() {
+  static hipError_t once = [] {
+    hipError_t e = hipSuccess;
+    auto set = [&](const void* fn) {
+      hipError_t r = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
+      if (r != hipSuccess) e = r;
+    };
+    set(reinterpret_cast<const void*>(&fwd_kernel<true>));
+    set(reinterpret_cast<const void*>(&fwd_kernel<false>));
+    set(reinterpret_cast<const void*>(&bwd_kernel<true>));
+    set(reinterpret_cast<const void*>(&bwd_kernel<false>));
+    set(reinterpret_cast<const void*>(&merge_kernel<true>));
+    set(reinterpret_cast<const void*>(&merge_kernel<false>));
+    return e;
+  }();
+  return once;
+}
+
+hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx, const float* c,
+                      const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, hipStream_t s) {
+  if (bf16 && p->fast.enabled) return launch_fwd128(p, count, T, X, ldx, c, cs, scale, beta, Y, ldy, s);
+  FwdArgs a{};
+  a.fin = p->fin->dev;
+  a.fout = p->fout->dev;
+  a.T = T;
+  a.tt = p->tile_tokens[bf16];
+  a.ldt_in = p->ldt_in[bf16];
+  a.ldt_out = p->ldt_out[bf16];
+  a.ldb_in = p->ldb_in;
+  a.ldb_out = p->ldb_out;
+  a.X = X.one;
+  a.Xs = X.many;
+  a.ldx = (long)ldx;
+  a.Y = const_cast<void*>(Y.one);
+  a.Ys = const_cast<void* const*>(Y.many);
+  a.ldy = (long)ldy;
+  a.c = c;
+  a.cs = cs;
+  a.scale = scale;
+  a.beta = beta;
+  a.slot_off = p->dev.fwd_slot_off;
+  a.ptr = p->dev.fwd_ptr;
+  a.ent = p->dev.fwd_ent;
+  a.nslots = p->dev.fwd_nslots;
+  const dim3 grid((unsigned)((T + a.tt - 1) / a.tt), (unsigned)count);
+  hipEvent_t e0, e1;
+  take_timing_events(&e0, &e1);
+  record(e0, s);
+  if (bf16)
+    hipLaunchKernelGGL(fwd_kernel<true>, grid, dim3(kFusedThreads), p->lds_bytes[1], s, a);
+  else
+    hipLaunchKernelGGL(fwd_kernel<false>, grid, dim3(kFusedThreads), p->lds_bytes[0], s, a);
+  record(e1, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G,
+                      int64_t ldg, const float* c, const float* const* cs, float scale, float beta_dx,
+                      ActPtrs dX, int64_t lddx, bool want_dx, int accumulate_dc, float* dC, float* const* dCs,
+                      bool want_dc, hipStream_t s) {
+  if (bf16 && p->fast.enabled)
+    return launch_bwd128(p, count, T, X, ldx, G, ldg, c, cs, scale, beta_dx, dX, lddx, want_dx, accumulate_dc, dC, dCs,
+                         want_dc, s);
+  BwdArgs a{};
+  a.fin = p->fin->dev;
+  a.fout = p->fout->dev;
+  a.T = T;
+  a.tt = p->tile_tokens[bf16];
+  a.ldt_in = p->ldt_in[bf16];
+  a.ldt_out = p->ldt_out[bf16];
+  a.ldb_in = p->ldb_in;
+  a.ldb_out = p->ldb_out;
+  a.X = X.one;
+  a.Xs = X.many;
+  a.ldx = (long)ldx;
+  a.G = G.one;
+  a.Gs = G.many;
+  a.ldg = (long)ldg;
+  a.dX = const_cast<void*>(dX.one);
+  a.dXs = const_cast<void* const*>(dX.many);
+  a.lddx = (long)lddx;
+  a.c = c;
+  a.cs = cs;
+  a.scale = scale;
+  a.beta = beta_dx;
+  a.want_dx = want_dx;
+  a.want_dc = want_dc;
+  a.slot_off = p->dev.bwd_slot_off;
+  a.ptr = p->dev.bwd_ptr;
+  a.ent = p->dev.bwd_ent;
+  a.nslots = p->dev.bwd_nslots;
+  a.sdd = p->dev.sdd;
+  a.nnz = p->dev.nnz;
+  a.partial = p->partial;
+  const long ntiles = (T + a.tt - 1) / a.tt;
+  a.ntiles = ntiles;
+  hipEvent_t e0, e1;
+  take_timing_events(&e0, &e1);
+  if (T > 0 && (want_dx || want_dc)) {
+    const dim3 grid((unsigned)ntiles, (unsigned)count);
+    record(e0, s);
+    if (bf16)
+      hipLaunchKernelGGL(bwd_kernel<true>, grid, dim3(kFusedThreads), p->lds_bytes[1], s, a);
+    else
+      hipLaunchKernelGGL(bwd_kernel<false>, grid, dim3(kFusedThreads), p->lds_bytes[0], s, a);
+    record(e1, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (want_dc) {
+    const dim3 grid((unsigned)((a.nnz + 255) / 256), (unsigned)count);
+    hipLaunchKernelGGL(dc_reduce, grid, dim3(256), 0, s, p->partial, ntiles, a.nnz, scale, accumulate_dc, dC,
+                       dCs);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf16, float beta, void* W,
+                        int64_t ldw, hipStream_t s) {
+  MergeArgs a{};
+  a.Bm = p->fout->dev.B32;
+  a.Bn = p->fin->dev.B32;
+  a.Wm = p->fout->dev.W;
+  a.Wn = p->fin->dev.W;
+  a.nblk_in = p->fin->dev.nblk;
+  a.rows_per_wg = std::max(1, std::min(a.Wm, kMergeThreads * kMergeEPT / a.Wn));
+  a.nsub = (a.Wm + a.rows_per_wg - 1) / a.rows_per_wg;
+  a.chunk = std::max(1, std::min(32, (int)(65536 / ((a.rows_per_wg + a.Wn) * sizeof(float)))));
+  a.ptr = p->dev.mrg_ptr;
+  a.ent = p->dev.mrg_ent;
+  a.c = c;
+  a.scale = scale;
+  a.beta = beta;
+  a.W = W;
+  a.ldw = (long)ldw;
+  const size_t lds = (size_t)a.chunk * (a.rows_per_wg + a.Wn) * sizeof(float);
+  const long nwg = (long)p->fout->dev.nblk * p->fin->dev.nblk * a.nsub;
+  hipEvent_t e0, e1;
+  take_timing_events(&e0, &e1);
+  record(e0, s);
+  if (w_bf16)
+    hipLaunchKernelGGL(merge_kernel<true>, dim3((unsigned)nwg), dim3(kMergeThreads), lds, s, a);
+  else
+    hipLaunchKernelGGL(merge_kernel<false>, dim3((unsigned)nwg), dim3(kMergeThreads), lds, s, a);
+  record(e1, s);
+  return hipGetLastError();
+}
+
+}  // namespace ff

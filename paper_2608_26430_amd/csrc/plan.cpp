@@ -1,0 +1,341 @@
+// Plan: the coefficient support G of Algorithm 1 (steps 3-4), shared by every
+// layer that uses the same frames (Sec. 3.3), turned into device index tables
+// for the fused kernels, plus the dC workspace.
+//
+// Canonical coefficient index c = i*rho + 2r + s (subspace i, frame-block r,
+// real part s) lives in frame block r at local position 2i + s.  Kernels keep
+// one token's coefficients in LDS block by block with block stride W + pad,
+// so every table stores LDS element offsets r*(W + pad) + 2i + s directly.
+#include <algorithm>
+#include <cstring>
+#include <memory>
+#include <numeric>
+
+#include "ff_internal.h"
+
+namespace {
+
+struct Loc {
+  int blk;
+  int local;
+};
+
+Loc locate(int64_t c, int64_t rho) {
+  const int64_t i = c / rho, rem = c % rho;
+  return {(int)(rem / 2), (int)(2 * i + rem % 2)};
+}
+
+// Token stride of an LDS tile (elements): whole blocks plus a pad chosen so
+// that consecutive token rows start 16 bytes apart modulo 128 bytes, which
+// spreads the per-token accesses of the sparse phases over different banks.
+int token_stride(int nblk, int ldb, int esz) {
+  const int base = nblk * ldb;                 // multiple of 8 elements
+  const int period = 128 / esz, want = 16 / esz;
+  int pad = ((want - base) % period + period) % period;
+  return base + pad;
+}
+
+// Row swizzle inside a 128-row block of the 128-wide kernels' coefficient arrays.
+int swz128(int blk, int o) { return o ^ ((o >> 2) & 4) ^ ((blk & 1) << 1); }
+
+constexpr uint32_t kStreamValid = 1u << 25, kStreamEnd = 1u << 24;
+
+// Lane-interleaved stream for one pair of blocks: destination row r (0..255) collects
+// rows[r] = (source row, user index e) entries.  Rows go whole to the least-loaded of 64
+// lanes (longest first); slot k of lane l is stream element k*64 + l.  Returns the number
+// of stream rows appended.
+int balanced_stream(const std::vector<std::vector<std::pair<uint32_t, int>>>& rows,
+                    const std::vector<uint32_t>& dst, std::vector<uint2>& st) {
+  std::vector<int> order;
+  for (int r = 0; r < (int)rows.size(); ++r)
+    if (!rows[r].empty()) order.push_back(r);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return rows[a].size() > rows[b].size(); });
+  std::vector<int> load(64, 0);
+  std::vector<std::vector<int>> lane_rows(64);
+  for (int r : order) {
+    const int l = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    lane_rows[l].push_back(r);
+    load[l] += (int)rows[r].size();
+  }
+  const int len = *std::max_element(load.begin(), load.end());
+  const size_t base = st.size();
+  st.resize(base + (size_t)len * 64, make_uint2(0u, 0u));
+  for (int l = 0; l < 64; ++l) {
+    int k = 0;
+    for (int r : lane_rows[l])
+      for (size_t i = 0; i < rows[r].size(); ++i, ++k) {
+        const bool last = i + 1 == rows[r].size();
+        st[base + (size_t)k * 64 + l] = make_uint2(rows[r][i].first | (dst[r] << 16) | kStreamValid |
+                                                       (last ? kStreamEnd : 0u),
+                                                   (unsigned)rows[r][i].second);
+      }
+  }
+  return len;
+}
+
+}  // namespace
+
+extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out, int64_t nnz,
+                                    const int32_t* rows, const int32_t* cols, int64_t max_tokens,
+                                    int64_t max_batch, ff_plan** out) {
+  ff::clear_error();
+  if (!out) return ff::fail(FF_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!f_in || !f_out) return ff::fail(FF_EINVAL, "frame is NULL");
+  if (f_in->device != f_out->device) return ff::fail(FF_EINVAL, "frames live on different devices");
+  const int64_t n = f_in->d, m = f_out->d;          // k*rho == d on the GPU path
+  if (nnz < 0 || nnz > m * n || nnz > ((int64_t)1 << 30))
+    return ff::fail(FF_EINVAL, "nnz=%lld out of range", (long long)nnz);
+  if (nnz > 0 && (!rows || !cols)) return ff::fail(FF_EINVAL, "rows/cols is NULL");
+  if (max_tokens < 0 || max_tokens > ((int64_t)1 << 31) - 1)
+    return ff::fail(FF_EINVAL, "max_tokens=%lld out of range", (long long)max_tokens);
+  if (max_batch < 1 || max_batch > 65535)
+    return ff::fail(FF_EINVAL, "max_batch=%lld out of range", (long long)max_batch);
+  for (int64_t e = 0; e < nnz; ++e)
+    if (rows[e] < 0 || rows[e] >= m || cols[e] < 0 || cols[e] >= n)
+      return ff::fail(FF_EINVAL, "support entry %lld = (%d, %d) outside %lld x %lld", (long long)e,
+                      rows[e], cols[e], (long long)m, (long long)n);
+  {
+    std::vector<int64_t> key((size_t)nnz);
+    for (int64_t e = 0; e < nnz; ++e) key[e] = (int64_t)rows[e] * n + cols[e];
+    std::sort(key.begin(), key.end());
+    for (int64_t e = 1; e < nnz; ++e)
+      if (key[e] == key[e - 1])
+        return ff::fail(FF_EINVAL, "duplicate support entry (%lld, %lld)", (long long)(key[e] / n),
+                        (long long)(key[e] % n));
+  }
+
+  const ff::FrameDev& FI = f_in->dev;
+  const ff::FrameDev& FO = f_out->dev;
+  std::unique_ptr<ff_plan> p(new ff_plan());
+  p->fin = const_cast<ff_frame*>(f_in);
+  p->fout = const_cast<ff_frame*>(f_out);
+  p->nnz = nnz;
+  p->max_tokens = max_tokens;
+  p->max_batch = max_batch;
+  p->device = f_in->device;
+  p->ldb_in = FI.W + ff::kBlockPad;
+  p->ldb_out = FO.W + ff::kBlockPad;
+  for (int dt = 0; dt < 2; ++dt) {
+    const int esz = dt == FF_BF16 ? 2 : 4;
+    p->ldt_in[dt] = token_stride(FI.nblk, p->ldb_in, esz);
+    p->ldt_out[dt] = token_stride(FO.nblk, p->ldb_out, esz);
+    const int64_t per_token = (int64_t)(p->ldt_in[dt] + p->ldt_out[dt]) * esz;
+    int64_t tt = ff::kMaxLdsBytes / per_token;
+    if (tt < 1)
+      return ff::fail(FF_EUNSUPPORTED, "one token of %lld + %lld coefficients exceeds LDS", (long long)n,
+                      (long long)m);
+    tt = std::min<int64_t>(tt, ff::kMaxTileTokens);
+    p->tile_tokens[dt] = (int)tt;
+    p->lds_bytes[dt] = (size_t)(tt * per_token);
+    p->max_tiles = std::max<int64_t>(p->max_tiles, (max_tokens + tt - 1) / tt);
+  }
+
+  // ---------------- host tables
+  std::vector<Loc> rloc((size_t)nnz), cloc((size_t)nnz);
+  for (int64_t e = 0; e < nnz; ++e) {
+    rloc[e] = locate(rows[e], f_out->rho);
+    cloc[e] = locate(cols[e], f_in->rho);
+  }
+  auto off_out = [&](const Loc& l) { return l.blk * p->ldb_out + l.local; };
+  auto off_in = [&](const Loc& l) { return l.blk * p->ldb_in + l.local; };
+
+  // forward CSR over all m rows, slots sorted by row length (longest first)
+  std::vector<int> rcount((size_t)m, 0), ccount((size_t)n, 0);
+  for (int64_t e = 0; e < nnz; ++e) {
+    rcount[rows[e]]++;
+    ccount[cols[e]]++;
+  }
+  auto build_slots = [](const std::vector<int>& count, std::vector<int>& order) {
+    order.resize(count.size());
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return count[a] > count[b]; });
+  };
+  std::vector<int> rorder, corder;
+  build_slots(rcount, rorder);
+  build_slots(ccount, corder);
+  std::vector<int> rslot_of((size_t)m), cslot_of((size_t)n);
+  for (int64_t s = 0; s < m; ++s) rslot_of[rorder[s]] = (int)s;
+  for (int64_t s = 0; s < n; ++s) cslot_of[corder[s]] = (int)s;
+
+  std::vector<int> fwd_ptr((size_t)m + 1, 0), bwd_ptr((size_t)n + 1, 0);
+  for (int64_t s = 0; s < m; ++s) fwd_ptr[s + 1] = fwd_ptr[s] + rcount[rorder[s]];
+  for (int64_t s = 0; s < n; ++s) bwd_ptr[s + 1] = bwd_ptr[s] + ccount[corder[s]];
+  std::vector<int> fwd_slot_off((size_t)m), bwd_slot_off((size_t)n);
+  for (int64_t s = 0; s < m; ++s) fwd_slot_off[s] = off_out(locate(rorder[s], f_out->rho));
+  for (int64_t s = 0; s < n; ++s) bwd_slot_off[s] = off_in(locate(corder[s], f_in->rho));
+  std::vector<int2> fwd_ent((size_t)std::max<int64_t>(nnz, 1)), bwd_ent((size_t)std::max<int64_t>(nnz, 1)),
+      sdd((size_t)std::max<int64_t>(nnz, 1));
+  {
+    std::vector<int> fpos(fwd_ptr.begin(), fwd_ptr.end() - 1), bpos(bwd_ptr.begin(), bwd_ptr.end() - 1);
+    // entries in order of their column (forward) / row (backward) for locality
+    std::vector<int64_t> byc((size_t)nnz), byr((size_t)nnz);
+    std::iota(byc.begin(), byc.end(), 0);
+    std::iota(byr.begin(), byr.end(), 0);
+    std::stable_sort(byc.begin(), byc.end(), [&](int64_t a, int64_t b) { return cols[a] < cols[b]; });
+    std::stable_sort(byr.begin(), byr.end(), [&](int64_t a, int64_t b) { return rows[a] < rows[b]; });
+    for (int64_t e : byc) fwd_ent[fpos[rslot_of[rows[e]]]++] = make_int2(off_in(cloc[e]), (int)e);
+    for (int64_t e : byr) bwd_ent[bpos[cslot_of[cols[e]]]++] = make_int2(off_out(rloc[e]), (int)e);
+    for (int64_t e = 0; e < nnz; ++e) sdd[e] = make_int2(off_out(rloc[e]), off_in(cloc[e]));
+  }
+  // merge buckets (R, S)
+  const int64_t nb = (int64_t)FO.nblk * FI.nblk;
+  std::vector<int> mrg_ptr((size_t)nb + 1, 0);
+  for (int64_t e = 0; e < nnz; ++e) mrg_ptr[(int64_t)rloc[e].blk * FI.nblk + cloc[e].blk + 1]++;
+  int max_bucket = 0;
+  for (int64_t b = 0; b < nb; ++b) {
+    max_bucket = std::max(max_bucket, mrg_ptr[b + 1]);
+    mrg_ptr[b + 1] += mrg_ptr[b];
+  }
+  std::vector<int4> mrg_ent((size_t)std::max<int64_t>(nnz, 1));
+  {
+    std::vector<int> pos(mrg_ptr.begin(), mrg_ptr.end() - 1);
+    for (int64_t e = 0; e < nnz; ++e) {
+      const int64_t b = (int64_t)rloc[e].blk * FI.nblk + cloc[e].blk;
+      mrg_ent[pos[b]++] = make_int4(rloc[e].local, cloc[e].local, (int)e, 0);
+    }
+  }
+
+  // ---------------- 128-wide fused path: balanced entry streams per pair of blocks
+  const bool fast = FI.W == 128 && FO.W == 128 && FI.nblk % 2 == 0 && FO.nblk % 2 == 0 &&
+                    f_in->transpose_is_sign_flip && f_out->transpose_is_sign_flip && f_in->B == f_out->B &&
+                    n < 65536 && m < 65536 &&
+                    ff::fast128_lds_bytes(std::max(FI.nblk, FO.nblk)) <= (size_t)ff::kMaxLdsBytes;
+  std::vector<int> f_off, f_len, b_off, b_len, s_off, s_len;
+  std::vector<uint2> f_st, b_st, s_st;
+  if (fast) {
+    auto zrow = [&](const Loc& l) { return (uint32_t)(l.blk * 128 + swz128(l.blk, l.local)); };
+    auto trow = [&](const Loc& l) { return (uint32_t)((l.blk & 1) * 128 + swz128(l.blk, l.local)); };
+    const int npo = FO.nblk / 2, npi = FI.nblk / 2;
+    std::vector<std::vector<std::vector<std::pair<uint32_t, int>>>> frows(npo), brows(npi);
+    std::vector<std::vector<uint32_t>> fdst(npo, std::vector<uint32_t>(256)), bdst(npi, std::vector<uint32_t>(256));
+    for (auto& v : frows) v.assign(256, {});
+    for (auto& v : brows) v.assign(256, {});
+    for (int pp = 0; pp < npo; ++pp)
+      for (int r = 0; r < 256; ++r) fdst[pp][r] = (uint32_t)((r >> 7) * 128 + swz128(r >> 7, r & 127));
+    for (int pp = 0; pp < npi; ++pp)
+      for (int r = 0; r < 256; ++r) bdst[pp][r] = (uint32_t)((r >> 7) * 128 + swz128(r >> 7, r & 127));
+    std::vector<std::vector<std::pair<uint32_t, int>>> sent(npi);
+    for (int64_t e = 0; e < nnz; ++e) {
+      const Loc& a = rloc[e];
+      const Loc& b = cloc[e];
+      frows[a.blk / 2][(a.blk & 1) * 128 + a.local].push_back({zrow(b), (int)e});
+      brows[b.blk / 2][(b.blk & 1) * 128 + b.local].push_back({zrow(a), (int)e});
+      sent[b.blk / 2].push_back({zrow(a) | (trow(b) << 16), (int)e});
+    }
+    for (int pp = 0; pp < npo; ++pp) {
+      f_off.push_back((int)(f_st.size() / 64));
+      f_len.push_back(balanced_stream(frows[pp], fdst[pp], f_st));
+    }
+    for (int pp = 0; pp < npi; ++pp) {
+      b_off.push_back((int)(b_st.size() / 64));
+      b_len.push_back(balanced_stream(brows[pp], bdst[pp], b_st));
+      s_off.push_back((int)(s_st.size() / 64));
+      const int rows64 = (int)((sent[pp].size() + 63) / 64);
+      s_len.push_back(rows64);
+      const size_t base = s_st.size();
+      s_st.resize(base + (size_t)rows64 * 64, make_uint2(0u, 0u));
+      for (size_t i = 0; i < sent[pp].size(); ++i)
+        s_st[base + i] = make_uint2(sent[pp][i].first | kStreamValid, (unsigned)sent[pp][i].second);
+    }
+  }
+  const int64_t fast_tiles = fast ? (max_tokens + ff::kFastTileTokens - 1) / ff::kFastTileTokens : 0;
+
+  // ---------------- device memory: one allocation for every table and the workspace
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t partial_elems = std::max((size_t)max_batch * (size_t)p->max_tiles * (size_t)nnz,
+                                        (size_t)max_batch * (size_t)fast_tiles * s_st.size());
+  struct Blob {
+    const void* src;
+    size_t bytes;
+  };
+  const std::vector<Blob> blobs = {
+      {fwd_slot_off.data(), m * sizeof(int)},      {fwd_ptr.data(), (m + 1) * sizeof(int)},
+      {fwd_ent.data(), fwd_ent.size() * sizeof(int2)}, {bwd_slot_off.data(), n * sizeof(int)},
+      {bwd_ptr.data(), (n + 1) * sizeof(int)},      {bwd_ent.data(), bwd_ent.size() * sizeof(int2)},
+      {sdd.data(), sdd.size() * sizeof(int2)},       {mrg_ptr.data(), (nb + 1) * sizeof(int)},
+      {mrg_ent.data(), mrg_ent.size() * sizeof(int4)},
+      {f_off.data(), f_off.size() * sizeof(int)},     {f_len.data(), f_len.size() * sizeof(int)},
+      {f_st.data(), f_st.size() * sizeof(uint2)},     {b_off.data(), b_off.size() * sizeof(int)},
+      {b_len.data(), b_len.size() * sizeof(int)},     {b_st.data(), b_st.size() * sizeof(uint2)},
+      {s_off.data(), s_off.size() * sizeof(int)},     {s_len.data(), s_len.size() * sizeof(int)},
+      {s_st.data(), s_st.size() * sizeof(uint2)},
+      {nullptr, std::max<size_t>(partial_elems, 1) * sizeof(float)}};
+  size_t total = 0;
+  for (const Blob& b : blobs) total += up(b.bytes);
+  int cur = 0;
+  if (hipGetDevice(&cur) != hipSuccess || cur != p->device)
+    return ff::fail(FF_EDEVICE, "current device differs from the frames' device");
+  void* mem = nullptr;
+  if (hipMalloc(&mem, total) != hipSuccess) {
+    (void)hipGetLastError();
+    return ff::fail(FF_ENOMEM, "hipMalloc of %zu bytes for the plan failed", total);
+  }
+  std::vector<void*> where;
+  {
+    size_t off = 0;
+    for (const Blob& b : blobs) {
+      void* dst = (char*)mem + off;
+      off += up(b.bytes);
+      if (b.src && b.bytes && hipMemcpy(dst, b.src, b.bytes, hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(mem);
+        return ff::fail(FF_EDEVICE, "copying plan tables to the device failed");
+      }
+      where.push_back(dst);
+    }
+  }
+  ff::PlanDev& pd = p->dev;
+  pd.fwd_slot_off = (const int*)where[0];
+  pd.fwd_ptr = (const int*)where[1];
+  pd.fwd_ent = (const int2*)where[2];
+  pd.fwd_nslots = (int)m;
+  pd.bwd_slot_off = (const int*)where[3];
+  pd.bwd_ptr = (const int*)where[4];
+  pd.bwd_ent = (const int2*)where[5];
+  pd.bwd_nslots = (int)n;
+  pd.sdd = (const int2*)where[6];
+  pd.mrg_ptr = (const int*)where[7];
+  pd.mrg_ent = (const int4*)where[8];
+  pd.mrg_max_bucket = max_bucket;
+  pd.nnz = (int)nnz;
+  ff::FastPlanDev& fp = p->fast;
+  fp.enabled = fast ? 1 : 0;
+  fp.fwd_off = (const int*)where[9];
+  fp.fwd_len = (const int*)where[10];
+  fp.fwd_st = (const uint2*)where[11];
+  fp.bwd_off = (const int*)where[12];
+  fp.bwd_len = (const int*)where[13];
+  fp.bwd_st = (const uint2*)where[14];
+  fp.sdd_off = (const int*)where[15];
+  fp.sdd_len = (const int*)where[16];
+  fp.sdd_st = (const uint2*)where[17];
+  fp.sdd_slots = (int)s_st.size();
+  p->partial = (float*)where[18];
+  p->dev_mem = mem;
+  p->workspace_bytes = total;
+  p->fin->refs.fetch_add(1);
+  p->fout->refs.fetch_add(1);
+  *out = p.release();
+  return FF_OK;
+}
+
+extern "C" void ff_plan_destroy(ff_plan* p) {
+  if (!p) return;
+  if (p->dev_mem) (void)hipFree(p->dev_mem);
+  ff_frame_destroy(p->fin);
+  ff_frame_destroy(p->fout);
+  delete p;
+}
+
+extern "C" ff_status ff_plan_query(const ff_plan* p, int key, int64_t* value) {
+  ff::clear_error();
+  if (!p || !value) return ff::fail(FF_EINVAL, "NULL argument");
+  switch (key) {
+    case FF_Q_TOKENS_PER_TILE_F32: *value = p->tile_tokens[FF_F32]; return FF_OK;
+    case FF_Q_TOKENS_PER_TILE_BF16: *value = p->tile_tokens[FF_BF16]; return FF_OK;
+    case FF_Q_WORKSPACE_BYTES: *value = (int64_t)p->workspace_bytes; return FF_OK;
+    case FF_Q_NNZ: *value = p->nnz; return FF_OK;
+    case FF_Q_FAST128: *value = p->fast.enabled; return FF_OK;
+    default: return ff::fail(FF_EINVAL, "unknown query key %d", key);
+  }
+}

@@ -1,0 +1,49 @@
+"""Helpers shared by the GPU parity tests (no method arithmetic here)."""
+import functools
+
+import numpy as np
+
+from oracle import frameft_oracle as O
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}   # normwise relative error bounds for fp32 / bf16 activations
+
+
+@functools.lru_cache(maxsize=None)
+def oracle_frame(k, rho, d):
+    return O.tight_fusion_frame(k, rho, d)
+
+
+def to_np(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def rel(got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(ref)
+    num = np.linalg.norm(got - ref)
+    return float(num / den) if den > 0 else float(num)
+
+
+def torch_act(a, dtype, device):
+    """Host fp32 array (bf16-valued when dtype == 'bf16') -> device tensor, exactly."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(device=device, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32)
+
+
+def bf16_ulp(x):
+    """Spacing of bf16 numbers at |x| (x finite, fp64 array)."""
+    ax = np.maximum(np.abs(x), np.finfo(np.float32).tiny)
+    e = np.floor(np.log2(ax))
+    return np.exp2(e - 7)
+
+
+def merged_bf16_ok(got, W0, dW):
+    """bf16 merge check: within one bf16 ulp of RNE(W0 + dW), widened by the fp32 rounding of
+    W0 + dW (2^-22 (|W0| + |dW|)), which matters only where the two nearly cancel."""
+    from paper_2608_26430_amd import inputs
+    exact = W0.astype(np.float64) + dW
+    want = inputs.bf16_round(exact.astype(np.float32)).astype(np.float64)
+    bound = bf16_ulp(want) + 2.0 ** -22 * (np.abs(W0) + np.abs(dW)) + 1e-30
+    return bool(np.all(np.abs(np.asarray(got, dtype=np.float64) - want) <= bound))

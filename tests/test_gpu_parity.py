@@ -1,0 +1,237 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Tolerances (normwise relative error per output tensor): 1e-5 for fp32
+activations, 2e-2 for bf16 activations with fp32 accumulation.  The merge is
+fp32 arithmetic: 1e-5 for the dense delta; merged into a bf16 weight, the result
+is within one bf16 ulp of the correctly rounded W0 + dW, widened by the fp32
+rounding of the sum (visible only where W0 and dW nearly cancel).
+"""
+import numpy as np
+import pytest
+
+from oracle import frameft_oracle as O
+from paper_2608_26430_amd import inputs
+from tests.parity_util import TOL, merged_bf16_ok, oracle_frame, rel, to_np, torch_act
+
+torch = pytest.importorskip("torch")
+import paper_2608_26430_amd as ff  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+    return torch.device("cuda:0")
+
+
+@pytest.mark.parametrize("d,k,rho", [(256, 16, 16), (4096, 64, 64), (768, 12, 64), (2304, 36, 64),
+                                     (2752, 172, 16), (3584, 224, 16), (64, 4, 16)])
+def test_framegen_matches_oracle(dev, d, k, rho):
+    f = ff.framegen(d, k, rho)
+    ref = oracle_frame(k, rho, d)
+    cols = sorted(set([0, 1, rho - 1, rho, k * rho - 1] + list(np.random.default_rng(d).integers(0, k * rho, 24))))
+    got = np.concatenate([f.export(c, 1) for c in cols], axis=1)
+    np.testing.assert_allclose(got, ref[:, cols].toarray(), rtol=0, atol=3e-7)
+
+
+# (n, rho_in, m, rho_out, nnz, T): block widths 2k of 8, 16, 24, 32, 72, 128, 344 and 448,
+# ragged token counts, a single token, an empty and a fully dense coefficient matrix.
+SHAPES = [
+    (256, 16, 256, 16, 512, 64),
+    (256, 16, 256, 16, 512, 1),
+    (256, 16, 512, 32, 700, 100),
+    (768, 64, 2304, 64, 3000, 37),
+    (1024, 16, 256, 16, 2000, 19),
+    (2752, 16, 1024, 16, 4000, 9),
+    (3584, 16, 256, 32, 5000, 5),
+    (64, 16, 64, 16, 4096, 23),
+    (256, 16, 256, 16, 0, 10),
+    # both blocks 128 wide: the fused 128-wide kernels serve bf16
+    (4096, 64, 4096, 64, 10000, 13),
+    (1024, 16, 2048, 32, 3000, 1),
+    (2048, 32, 1024, 16, 5000, 29),
+    (1024, 16, 1024, 16, 0, 9),
+]
+
+
+def _problem(shape, dtype, seed):
+    n, rn, m, rm, nnz, T = shape
+    g = inputs.rng(seed)
+    rows, cols = inputs.support(g, m, n, nnz)
+    vals = inputs.gaussian(g, (nnz,), std=0.02)
+    X = inputs.gaussian(g, (T, n), dtype=dtype)
+    G = inputs.gaussian(g, (T, m), dtype=dtype)
+    return rows, cols, vals, X, G
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "n%d_m%d_nnz%d_T%d" % (s[0], s[2], s[4], s[5]))
+def test_small_parity(dev, shape, dtype):
+    n, rn, m, rm, nnz, T = shape
+    rows, cols, vals, X, G = _problem(shape, dtype, seed=n * 7 + m + nnz + T)
+    s = 0.173
+    P_in, P_out = oracle_frame(n // rn, rn, n), oracle_frame(m // rm, rm, m)
+    f_in, f_out = ff.framegen(n, n // rn, rn), ff.framegen(m, m // rm, rm)
+    plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T)
+    assert plan.fast128 == (n // rn == 64 and m // rm == 64 and (n // 128) % 2 == 0 and (m // 128) % 2 == 0)
+    tol = TOL[dtype]
+    Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
+    c = torch.from_numpy(vals).to(dev)
+
+    # forward, overwrite and accumulate into an existing Y
+    y_ref = O.adapter_fwd(P_in, P_out, rows, cols, vals, s, X)
+    Y = ff.adapter_fwd(plan, Xd, c, s)
+    Y0 = inputs.gaussian(inputs.rng(3), (T, m), dtype=dtype)
+    Yb = ff.adapter_fwd(plan, Xd, c, s, Y=torch_act(Y0, dtype, dev), beta=0.75)
+    # backward: overwrite, then accumulate
+    dx_ref, dc_ref = O.adapter_bwd(P_in, P_out, rows, cols, vals, s, X, G)
+    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s)
+    dX0 = inputs.gaussian(inputs.rng(4), (T, n), dtype=dtype)
+    dC0 = inputs.gaussian(inputs.rng(5), (nnz,))
+    dXb, dCb = ff.adapter_bwd(plan, Xd, Gd, c, s, dX=torch_act(dX0, dtype, dev), beta_dx=-1.5,
+                              dC=torch.from_numpy(dC0.copy()).to(dev), accumulate_dc=True)
+    _, dC2 = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dx=False)
+    # merge: dense delta into fp32, and in place into a bf16 weight
+    dw_ref = O.merge_delta(P_in, P_out, rows, cols, vals, s)
+    Wd = ff.merge_delta(plan, c, s, torch.full((m, n), float("nan"), device=dev), beta=0.0)
+    W0 = inputs.weight(inputs.rng(6), m, n, "bf16")
+    Wb = ff.merge_delta(plan, c, s, torch_act(W0, "bf16", dev), beta=1.0)
+    torch.cuda.synchronize()
+
+    if nnz == 0:
+        assert np.all(to_np(Y) == 0) and np.all(to_np(dX) == 0) and np.all(to_np(Wd) == 0)
+        assert dC.numel() == 0
+        return
+    assert rel(to_np(Y), y_ref) <= tol
+    assert rel(to_np(Yb), 0.75 * Y0 + y_ref) <= tol
+    assert rel(to_np(dX), dx_ref) <= tol
+    assert rel(to_np(dC), dc_ref) <= tol
+    assert rel(to_np(dXb), -1.5 * dX0 + dx_ref) <= tol
+    assert rel(to_np(dCb), dC0 + dc_ref) <= tol
+    assert torch.equal(dC, dC2), "dC is not deterministic"
+    assert rel(to_np(Wd), dw_ref) <= 1e-5
+    assert merged_bf16_ok(to_np(Wb), W0, dw_ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_batched_matches_single_calls(dev, dtype):
+    n, m, nnz, T, count = 4096, 4096, 4000, 21, 3
+    g = inputs.rng(77)
+    rows, cols = inputs.support(g, m, n, nnz)
+    f = ff.framegen(4096, 64, 64)
+    plan = ff.plan_create(f, f, rows, cols, max_tokens=T, max_batch=count)
+    P = oracle_frame(64, 64, 4096)
+    s = 0.05
+    vals = [inputs.gaussian(g, (nnz,), std=0.02) for _ in range(count)]
+    Xs = [inputs.gaussian(g, (T, n), dtype=dtype) for _ in range(count)]
+    Gs = [inputs.gaussian(g, (T, m), dtype=dtype) for _ in range(count)]
+    Xd = [torch_act(x, dtype, dev) for x in Xs]
+    Gd = [torch_act(x, dtype, dev) for x in Gs]
+    cd = [torch.from_numpy(v).to(dev) for v in vals]
+    Yd = [torch.empty((T, m), dtype=Xd[0].dtype, device=dev) for _ in range(count)]
+    dXd = [torch.empty((T, n), dtype=Xd[0].dtype, device=dev) for _ in range(count)]
+    dCd = [torch.empty((nnz,), device=dev) for _ in range(count)]
+    ff.adapter_fwd_batched(plan, Xd, cd, s, Yd)
+    ff.adapter_bwd_batched(plan, Xd, Gd, cd, s, dXd, dCd)
+    torch.cuda.synchronize()
+    tol = TOL[dtype]
+    for i in range(count):
+        y_ref = O.adapter_fwd(P, P, rows, cols, vals[i], s, Xs[i])
+        dx_ref, dc_ref = O.adapter_bwd(P, P, rows, cols, vals[i], s, Xs[i], Gs[i])
+        assert rel(to_np(Yd[i]), y_ref) <= tol
+        assert rel(to_np(dXd[i]), dx_ref) <= tol
+        assert rel(to_np(dCd[i]), dc_ref) <= tol
+
+
+def test_empty_batch_is_noop_and_zeroes_dc(dev):
+    n = m = 256
+    rows, cols, vals, X, G = _problem((n, 16, m, 16, 100, 4), "f32", 1)
+    f = ff.framegen(256, 16, 16)
+    plan = ff.plan_create(f, f, rows, cols, max_tokens=4)
+    c = torch.from_numpy(vals).to(dev)
+    Xe = torch.zeros((0, n), device=dev)
+    Ge = torch.zeros((0, m), device=dev)
+    Y = ff.adapter_fwd(plan, Xe, c, 1.0)
+    dC = torch.full((100,), 7.0, device=dev)
+    dX, dC = ff.adapter_bwd(plan, Xe, Ge, c, 1.0, dC=dC)
+    torch.cuda.synchronize()
+    assert Y.shape == (0, m) and dX.shape == (0, n)
+    assert torch.all(dC == 0)
+
+
+def test_argument_errors_write_nothing(dev):
+    f = ff.framegen(256, 16, 16)
+    rows, cols, vals, X, G = _problem((256, 16, 256, 16, 50, 8), "f32", 2)
+    with pytest.raises(ff.FrameFTError) as ei:
+        ff.plan_create(f, f, np.array([1, 1]), np.array([2, 2]), max_tokens=8)
+    assert ei.value.name == "FF_EINVAL"
+    with pytest.raises(ff.FrameFTError):
+        ff.plan_create(f, f, np.array([256]), np.array([0]), max_tokens=8)
+    plan = ff.plan_create(f, f, rows, cols, max_tokens=8)
+    c = torch.from_numpy(vals).to(dev)
+    Y = torch.full((9, 256), 3.0, device=dev)
+    with pytest.raises(ff.FrameFTError) as ei:       # T above max_tokens
+        ff.adapter_fwd(plan, torch.zeros((9, 256), device=dev), c, 1.0, Y=Y)
+    assert ei.value.name == "FF_EINVAL"
+    Xb = torch.zeros((8, 256), device=dev, dtype=torch.bfloat16)
+    Yb = torch.full((8, 256), 3.0, device=dev, dtype=torch.bfloat16)
+    with pytest.raises(ff.FrameFTError):              # misaligned view
+        ff.adapter_fwd(plan, Xb[:, 1:], c, 1.0, Y=Yb[:, 1:])
+    torch.cuda.synchronize()
+    assert torch.all(Y == 3.0) and torch.all(Yb == 3.0)
+
+
+# ------------------------------------------------------------------ full-size configurations
+
+def _sample_tokens(T, k, seed):
+    g = np.random.default_rng(seed)
+    extra = g.choice(T, size=min(k, T), replace=False)
+    return np.unique(np.concatenate([[0, 1, T // 2, T - 1], extra]))
+
+
+def _full_size_check(dev, wl_name, adapter_index=0, n_tok=48, n_nnz=384, n_rows=6):
+    wl = inputs.WORKLOADS[wl_name]
+    ad = wl.adapters[adapter_index]
+    data = inputs.adapter_data(wl, ad, seed=wl.seed + adapter_index)
+    T, dtype = wl.tokens, wl.dtype
+    P_in = oracle_frame(ad.k_in, ad.rho_in, ad.d_in)
+    P_out = oracle_frame(ad.k_out, ad.rho_out, ad.d_out)
+    f_in = ff.framegen(ad.d_in, ad.k_in, ad.rho_in)
+    f_out = ff.framegen(ad.d_out, ad.k_out, ad.rho_out)
+    plan = ff.plan_create(f_in, f_out, data.rows, data.cols, max_tokens=T)
+    Xd, Gd = torch_act(data.X, dtype, dev), torch_act(data.G, dtype, dev)
+    c = torch.from_numpy(data.vals).to(dev)
+    Y = ff.adapter_fwd(plan, Xd, c, data.scale)
+    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, data.scale)
+    W0 = inputs.weight(inputs.rng(wl.seed + 99), ad.d_out, ad.d_in, "bf16")
+    Wb = ff.merge_delta(plan, c, data.scale, torch_act(W0, "bf16", dev), beta=1.0)
+    Wd = ff.merge_delta(plan, c, data.scale, torch.empty((ad.d_out, ad.d_in), device=dev), beta=0.0)
+    torch.cuda.synchronize()
+    tol = TOL[dtype]
+    tok = _sample_tokens(T, n_tok, wl.seed)
+    y_ref = O.adapter_fwd(P_in, P_out, data.rows, data.cols, data.vals, data.scale, data.X[tok])
+    dx_ref, _ = O.adapter_bwd(P_in, P_out, data.rows, data.cols, data.vals, data.scale, data.X[tok],
+                              data.G[tok])
+    assert rel(to_np(Y[tok]), y_ref) <= tol
+    assert rel(to_np(dX[tok]), dx_ref) <= tol
+    ent = np.random.default_rng(wl.seed + 1).choice(ad.nnz, size=min(n_nnz, ad.nnz), replace=False)
+    dc_ref = O.coeff_grad_entries(P_in, P_out, data.rows[ent], data.cols[ent], data.scale, data.X, data.G)
+    assert rel(to_np(dC)[ent], dc_ref) <= tol
+    r = np.unique(np.concatenate([[0, ad.d_out - 1], np.random.default_rng(wl.seed + 2).integers(0, ad.d_out, n_rows)]))
+    dw_ref = O.merge_delta_rows(P_in, P_out, data.rows, data.cols, data.vals, data.scale, r)
+    assert rel(to_np(Wd[r]), dw_ref) <= 1e-5
+    assert merged_bf16_ok(to_np(Wb[r]), W0[r], dw_ref)
+    # the frames are orthogonal, so ||dW||_F = |s| ||C||_F for the whole matrix
+    nrm = float(torch.linalg.vector_norm(Wd.double()))
+    assert abs(nrm - abs(data.scale) * np.linalg.norm(data.vals.astype(np.float64))) <= 1e-5 * nrm
+
+
+def test_cfg1_full(dev):
+    _full_size_check(dev, "cfg1_256_fp32", n_tok=64, n_nnz=512, n_rows=256)
+
+
+def test_cfg2_llama7b_qproj_full(dev):
+    _full_size_check(dev, "cfg2_llama7b_qproj")

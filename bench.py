@@ -110,7 +110,7 @@ def main():
 
     X = torch.from_numpy(data.X).to(dev, tdt)
     G = torch.from_numpy(data.G).to(dev, tdt)
-    c = torch.from_numpy(data.vals).to(dev)
+    c = torch.from_numpy(np.ascontiguousarray(data.vals[plan.order])).to(dev)   # plan order
     Y = torch.empty((T, m), dtype=tdt, device=dev)
     dX = torch.empty((T, n), dtype=tdt, device=dev)
     dC = torch.empty((nnz,), dtype=torch.float32, device=dev)

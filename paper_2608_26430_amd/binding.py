@@ -56,6 +56,7 @@ def _load():
         "ff_plan_create": (i32, [vp, vp, i64, vp, vp, i64, i64, ctypes.POINTER(vp)]),
         "ff_plan_destroy": (None, [vp]),
         "ff_plan_query": (i32, [vp, i32, ctypes.POINTER(i64)]),
+        "ff_plan_order": (i32, [vp, ctypes.POINTER(i64)]),
         "ff_adapter_fwd": (i32, [vp, i64, i32, vp, i64, vp, f32, f32, vp, i64, vp]),
         "ff_adapter_bwd": (i32, [vp, i64, i32, vp, i64, vp, i64, vp, f32, f32, vp, i64, i32, vp, vp]),
         "ff_merge_delta": (i32, [vp, vp, f32, i32, f32, vp, i64, vp]),
@@ -151,6 +152,7 @@ class Plan:
         self.n, self.m = f_in.d, f_out.d
         self.nnz = int(rows.size)
         self.max_tokens, self.max_batch = max_tokens, max_batch
+        self._order = None
 
     @property
     def handle(self):
@@ -172,6 +174,16 @@ class Plan:
     def fast128(self) -> bool:
         """True when bf16 calls run the fused kernels for 128-wide frame blocks."""
         return bool(self.query(4))
+
+    @property
+    def order(self) -> np.ndarray:
+        """user index of each plan-ordered coefficient: c_plan = c_user[order],
+        dC_user[order] = dC_plan."""
+        if self._order is None:
+            o = np.empty(self.nnz, dtype=np.int64)
+            _check(_load().ff_plan_order(self._h, o.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))))
+            self._order = o
+        return self._order
 
     def close(self):
         if self._h:

@@ -65,16 +65,14 @@ struct PlanDev {
 // blocks, `len` rows of 64 lane slots starting at stream row `off`.
 struct FastPlanDev {
   int enabled = 0;
-  const int* fwd_off = nullptr;   // v = C z, per output pair
+  const int* fwd_off = nullptr;       // v = C z, per output pair
   const int* fwd_len = nullptr;
-  const uint2* fwd_st = nullptr;
-  const int* bwd_off = nullptr;   // q = C^T u, per input pair
+  const uint32_t* fwd_st = nullptr;   // slot words
+  const int2* fwd_ri = nullptr;       // per stream row: (plan index of lane 0, occupied lanes)
+  const int* bwd_off = nullptr;       // dC and q = C^T u, per input pair
   const int* bwd_len = nullptr;
-  const uint2* bwd_st = nullptr;
-  const int* sdd_off = nullptr;   // dC, per input pair
-  const int* sdd_len = nullptr;
-  const uint2* sdd_st = nullptr;
-  int sdd_slots = 0;              // 64 * total dC stream rows
+  const uint2* bwd_st = nullptr;      // (slot word, plan index)
+  int bwd_slots = 0;                  // 64 * backward stream rows = dC partials per tile
 };
 
 }  // namespace ff
@@ -85,6 +83,7 @@ struct ff_frame {
   int device = 0;
   std::vector<double> B;   // W x W fp64 block on the host
   bool transpose_is_sign_flip = false;   // B^T == D B D exactly, D = diag((-1)^i)
+  bool half_shift_sign = false;          // B[u + W/2][c] == (-1)^(c/2) B[u][c]
   void* dev_mem = nullptr;
   ff::FrameDev dev{};
 };
@@ -105,6 +104,7 @@ struct ff_plan {
   void* dev_mem = nullptr;
   ff::PlanDev dev{};
   ff::FastPlanDev fast{};
+  std::vector<int64_t> user_order;  // user index of each plan-ordered coefficient
 };
 
 namespace ff {

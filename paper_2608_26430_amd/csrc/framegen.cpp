@@ -206,6 +206,20 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
         break;
       }
 
+  // The modulation by roots of unity makes the lower half of the block the upper half with
+  // the odd complex columns negated: B[u + W/2][c] = (-1)^(c/2) B[u][c] (the row-wise radix-2
+  // symmetry of the DFT).  The 128-wide kernels hold only the upper half.  Checked to within
+  // the rounding of the cosines, far below bf16 resolution.
+  bool half_shift = W % 4 == 0;
+  for (int64_t u = 0; u < W / 2 && half_shift; ++u)
+    for (int64_t c = 0; c < W; ++c) {
+      const double top = B[u * W + c], bot = B[(u + W / 2) * W + c];
+      if (std::fabs(bot - (((c >> 1) & 1) ? -top : top)) > 1e-12) {
+        half_shift = false;
+        break;
+      }
+    }
+
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return ff::fail(FF_EDEVICE, "no HIP device");
   int ndev = 0;
@@ -281,6 +295,7 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   f->device = dev;
   f->B = std::move(B);
   f->transpose_is_sign_flip = sign_flip;
+  f->half_shift_sign = half_shift;
   f->dev_mem = mem;
   f->dev = fd;
   *out = f;

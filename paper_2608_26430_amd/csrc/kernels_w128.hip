@@ -10,22 +10,28 @@
 // (8 consecutive coefficients of one token, four tokens' lanes per row) hit
 // distinct banks.
 //
-// Frame products.  The block B (synthesis) is held in 128 VGPRs by every wave
-// for the whole kernel.  Analysis needs B^T; for these frames B^T = D B D with
+// Frame products.  Only the upper half of the block B (synthesis) is held in
+// registers (64 VGPRs per wave, staged once per workgroup through LDS): the
+// lower half is the upper half applied to the input with its odd complex
+// components negated, B[u + 64][c] = (-1)^(c/2) B[u][c], the row-wise radix-2
+// symmetry of the DFT.  Analysis needs B^T; for these frames B^T = D B D with
 // D = diag(+1, -1, +1, ...) (the realified DFT is symmetric up to the sign of
-// its sine terms), so analysis flips the sign of odd inputs and odd outputs and
-// reuses the same fragments.  One v_mfma_f32_16x16x32_bf16 column group is 16
-// (token, block) pairs: the tile's 8 tokens times a pair of adjacent blocks.
+// its sine terms), so analysis negates odd inputs and odd outputs and reuses
+// the same fragments.  All sign changes are XORs on the packed bf16 operand.
+// One v_mfma_f32_16x16x32_bf16 column group is 16 (token, block) pairs: 8
+// tokens times a pair of blocks.
 //
 // Sparse products.  After the shared coefficient array is complete, each wave
-// streams over its own block pairs with a private 4 KB LDS tile: it builds the
-// pair's 256 coefficients of v = C z (forward) or q = C^T u (backward) from a
-// load-balanced, lane-interleaved entry stream prepared by the plan (each lane
-// owns whole rows; entries of a row are consecutive), then applies the frame
-// block and writes the activations.  The backward also forms this tile's
-// share of dC_e = sum_t u_t[a_e] z_t[b_e] with v_dot2_f32_bf16 over token pairs
-// and stores it as a partial sum; a second kernel reduces partials in a fixed
-// order.
+// streams over its own block pairs with a private 4 KB LDS tile.  The plan's
+// entry streams are load-balanced and lane-interleaved (a lane owns whole rows
+// of C for v = C z, whole columns for q = C^T u), and the coefficient vector is
+// in the plan's order, which is the forward stream's order: forward slots read
+// their coefficients with coalesced loads that do not wait for the entries.
+// The next pair's stream chunk is loaded while the current pair is synthesised.
+// The backward runs one stream per input pair twice: first for this tile's
+// share of dC_e = sum_t u_t[a_e] z_t[b_e] (v_dot2_f32_bf16 over token pairs),
+// then for q = C^T u; partial dC sums go to a workspace reduced in a fixed
+// order by a second kernel.
 #include "ff_internal.h"
 
 namespace ff {
@@ -34,9 +40,11 @@ namespace {
 constexpr int kW = 128;   // block width
 constexpr int kTT = 8;    // tokens per tile
 constexpr int kMT = 8;    // 16-row output tiles per block
+constexpr int kHT = kMT / 2;   // 16-row tiles of the upper half (held in registers)
 constexpr int kKT = 4;    // 32-wide contraction steps per block
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
+constexpr int kCh = 16;   // stream slots per lane held in registers at once
 
 constexpr unsigned kValid = 1u << 25, kEnd = 1u << 24;
 
@@ -64,60 +72,74 @@ __device__ __forceinline__ u16 to_bf(float a) { return __builtin_bit_cast(u16, (
 __device__ __forceinline__ void wave_lds_fence() { __asm__ volatile("" ::: "memory"); }
 
 struct Frag {
-  bf16x8 f[kMT][kKT];
+  bf16x8 f[kHT][kKT];
 };
 
-__device__ __forceinline__ void load_frag(const void* fs16, int lane, Frag& F) {
-  const bf16x8* src = reinterpret_cast<const bf16x8*>(fs16);
+// Stage the 16 KB of upper-half synthesis fragments through LDS (once per workgroup) and load
+// this wave's copy.  `stage` must be free LDS of that size; it may be reused after return.
+// The fragment array is ordered [row tile][contraction step][lane], so the upper half is its
+// first half.
+__device__ __forceinline__ void load_frag(const void* fs16, u32x4* stage, int lane, Frag& F) {
+  const u32x4* src = reinterpret_cast<const u32x4*>(fs16);
+  for (int i = threadIdx.x; i < kHT * kKT * 64; i += kThreads) stage[i] = src[i];
+  __syncthreads();
 #pragma unroll
-  for (int mt = 0; mt < kMT; ++mt)
+  for (int mt = 0; mt < kHT; ++mt)
 #pragma unroll
-    for (int ks = 0; ks < kKT; ++ks) F.f[mt][ks] = src[(mt * kKT + ks) * 64 + lane];
+    for (int ks = 0; ks < kKT; ++ks) F.f[mt][ks] = __builtin_bit_cast(bf16x8, stage[(mt * kKT + ks) * 64 + lane]);
+  __syncthreads();
 }
 
-// acc[mt] = sum_ks F[mt][ks] * b[ks]
-__device__ __forceinline__ void mfma_block(const Frag& F, const u32x4 (&b)[kKT], f32x4 (&acc)[kMT]) {
+// acc[mt] = sum_ks B[mt][ks] * b[ks] for the 8 row tiles of the block; rows 64..127 use the
+// upper-half fragments on the input with its odd complex components negated.  With flip
+// (analysis) odd real inputs are negated first.  A lane's 8 inputs of a contraction step are
+// real indices 32 ks + 8 q + j: odd j is the high half of each word, odd complex index is
+// words 1 and 3.
+__device__ __forceinline__ void mfma_block(const Frag& F, const u32x4 (&b)[kKT], f32x4 (&acc)[kMT], bool flip) {
+  const unsigned d = flip ? 0x80000000u : 0u;
+  const u32x4 m_top = {d, d, d, d};
+  const u32x4 m_bot = {d, d ^ 0x80008000u, d, d ^ 0x80008000u};
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ks = 0; ks < kKT; ++ks) {
-    const bf16x8 bk = __builtin_bit_cast(bf16x8, b[ks]);
+    const bf16x8 bt = __builtin_bit_cast(bf16x8, b[ks] ^ m_top);
+    const bf16x8 bb = __builtin_bit_cast(bf16x8, b[ks] ^ m_bot);
 #pragma unroll
-    for (int mt = 0; mt < kMT; ++mt) acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.f[mt][ks], bk, acc[mt], 0, 0, 0);
+    for (int mt = 0; mt < kHT; ++mt) {
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.f[mt][ks], bt, acc[mt], 0, 0, 0);
+      acc[mt + kHT] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.f[mt][ks], bb, acc[mt + kHT], 0, 0, 0);
+    }
   }
 }
 
 // Activation fragments of one column group: lane (token t, block bs of the pair, quarter q)
-// reads 8 consecutive inputs per contraction step from a row-major token matrix.
-__device__ __forceinline__ void load_act(const u16* rows, long ld, int nt, int blk0, int lane, bool flip,
-                                         u32x4 (&b)[kKT]) {
-  const int n = lane & 15, t = n & 7, bs = n >> 3, q = lane >> 4;
-  if (t < nt) {
-    const u16* p = rows + (long)t * ld + (blk0 + bs) * kW + 8 * q;
+// reads 8 consecutive inputs per contraction step from a row-major token matrix.  The loads
+// are unconditional (tokens past the tile's end re-read its last token) and nothing touches
+// the registers until mfma_block, so they stay in flight; store_coef zeroes those columns and
+// store_act skips them.
+__device__ __forceinline__ void load_act(const u16* rows, long ld, int nt, int blk0, int lane, u32x4 (&b)[kKT]) {
+  const int n = lane & 15, t = min(n & 7, nt - 1), bs = n >> 3, q = lane >> 4;
+  const u16* p = rows + (long)t * ld + (blk0 + bs) * kW + 8 * q;
 #pragma unroll
-    for (int ks = 0; ks < kKT; ++ks) b[ks] = *reinterpret_cast<const u32x4*>(p + 32 * ks);
-    if (flip) {
-#pragma unroll
-      for (int ks = 0; ks < kKT; ++ks) b[ks] ^= 0x80000000u;   // negate odd coordinates
-    }
-  } else {
-#pragma unroll
-    for (int ks = 0; ks < kKT; ++ks) b[ks] = u32x4{0u, 0u, 0u, 0u};
-  }
+  for (int ks = 0; ks < kKT; ++ks) b[ks] = *reinterpret_cast<const u32x4*>(p + 32 * ks);
 }
 
 // Write an analysis result (odd outputs negated) into a coefficient-major LDS array whose
-// block `blk0 + bs` starts at row (blk0 + bs - row_blk0) * 128.
-__device__ __forceinline__ void store_coef(u16* lds, int blk0, int row_blk0, int lane, const f32x4 (&acc)[kMT]) {
+// block `blk0 + bs` starts at row (blk0 + bs - row_blk0) * 128.  Columns of tokens past the
+// tile's end are written as zeros.
+__device__ __forceinline__ void store_coef(u16* lds, int blk0, int row_blk0, int nt, int lane,
+                                           const f32x4 (&acc)[kMT]) {
   const int n = lane & 15, t = n & 7, bs = n >> 3, q = lane >> 4;
   const int blk = blk0 + bs;
+  const float keep = t < nt ? 1.f : 0.f;
   u16* base = lds + (long)(blk - row_blk0) * kW * kTT + t;
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int o = 16 * mt + 4 * q + j;
-      const float v = (j & 1) ? -acc[mt][j] : acc[mt][j];
+      const float v = (j & 1) ? -keep * acc[mt][j] : keep * acc[mt][j];
       base[swz(blk, o) * kTT] = to_bf(v);
     }
 }
@@ -160,35 +182,112 @@ __device__ __forceinline__ void store_act(u16* rows, long ld, int nt, int blk0, 
   }
 }
 
-// v[row][t] = sum_{e in row} c_e * src[row_e][t] over a lane-interleaved stream; rows are written
-// into `tile` when their last entry is seen.  The tile is zeroed first (rows without entries).
-__device__ __forceinline__ void spmm_stream(const uint2* __restrict__ st, int len, const float* __restrict__ cv,
-                                            const u16* src, u16* tile, int lane) {
+__device__ __forceinline__ void zero_tile(u16* tile, int lane) {
   u32x4* tz = reinterpret_cast<u32x4*>(tile);
   wave_lds_fence();
 #pragma unroll
   for (int i = 0; i < 4; ++i) tz[lane + 64 * i] = u32x4{0u, 0u, 0u, 0u};
   wave_lds_fence();
-  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int k = 0; k < len; ++k) {
-    const uint2 en = st[(long)k * 64 + lane];
-    if (en.x & kValid) {
-      const float c = cv[en.y];
-      const u32x4 zv = *reinterpret_cast<const u32x4*>(src + (en.x & 0xffffu) * kTT);
+}
+
+// a[0..7] += c * (8 bf16 tokens of source row); at the end of a row, write it to the tile.
+__device__ __forceinline__ void accum_row(unsigned e, float c, const u16* src, u16* tile, float (&a)[8]) {
+  const u32x4 zv = *reinterpret_cast<const u32x4*>(src + (e & 0xffffu) * kTT);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        a[2 * i] = fmaf(c, lo_bf(zv[i]), a[2 * i]);
-        a[2 * i + 1] = fmaf(c, hi_bf(zv[i]), a[2 * i + 1]);
-      }
-      if (en.x & kEnd) {
-        tz[(en.x >> 16) & 0xffu] = u32x4{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(a[4], a[5]),
-                                          pack_bf2(a[6], a[7])};
+  for (int j = 0; j < 4; ++j) {
+    const unsigned w = zv[j];
+    a[2 * j] = fmaf(c, lo_bf(w), a[2 * j]);
+    a[2 * j + 1] = fmaf(c, hi_bf(w), a[2 * j + 1]);
+  }
+  if (e & kEnd) {
+    reinterpret_cast<u32x4*>(tile)[(e >> 16) & 0xffu] =
+        u32x4{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(a[4], a[5]), pack_bf2(a[6], a[7])};
 #pragma unroll
-        for (int i = 0; i < 8; ++i) a[i] = 0.f;
-      }
+    for (int j = 0; j < 8; ++j) a[j] = 0.f;
+  }
+}
+
+// ---------------------------------------------------------------- forward stream chunks
+
+struct FwdChunk {
+  unsigned en[kCh];
+  float cc[kCh];
+};
+
+// Load slots k0 .. k0+kCh-1 of a forward stream: entries and their coefficients, which sit at
+// plan index rowinfo.x + lane; loads are clamped to real rows/lanes and masked when used.
+__device__ __forceinline__ void fwd_load(const unsigned* __restrict__ st, const int2* __restrict__ ri, int off,
+                                         int len, int k0, const float* __restrict__ cv, int lane, FwdChunk& ch) {
+#pragma unroll
+  for (int i = 0; i < kCh; ++i) {
+    const int r = off + min(k0 + i, len - 1);
+    const int2 info = ri[r];
+    ch.en[i] = st[(long)r * 64 + lane];
+    ch.cc[i] = cv[info.x + min(lane, info.y - 1)];
+  }
+}
+
+__device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int len, int k0, const u16* zL, u16* tile,
+                                            float (&a)[8]) {
+#pragma unroll
+  for (int i = 0; i < kCh; ++i) {
+    if (k0 + i < len) {   // uniform
+      const unsigned e = ch.en[i];
+      accum_row(e, (e & kValid) ? ch.cc[i] : 0.f, zL, tile, a);
     }
   }
-  wave_lds_fence();
+}
+
+// ---------------------------------------------------------------- backward stream chunks
+
+struct BwdChunk {
+  uint2 en[kCh];
+  float cc[kCh];
+};
+
+__device__ __forceinline__ void bwd_load_entries(const uint2* __restrict__ st, int len, int k0, int lane,
+                                                 BwdChunk& ch) {
+#pragma unroll
+  for (int i = 0; i < kCh; ++i) ch.en[i] = st[(long)min(k0 + i, len - 1) * 64 + lane];
+}
+
+// Coefficients of the loaded entries (empty slots read entry 0 and are masked when used).
+__device__ __forceinline__ void bwd_load_coeffs(const float* __restrict__ cv, BwdChunk& ch) {
+#pragma unroll
+  for (int i = 0; i < kCh; ++i) ch.cc[i] = cv[ch.en[i].y];
+}
+
+// This tile's share of dC / s for the chunk's slots, written to part (one float per slot).
+__device__ __forceinline__ void bwd_sddmm(const BwdChunk& ch, int len, int k0, const u16* uL, const u16* tile,
+                                          float* __restrict__ part, int lane) {
+#pragma unroll
+  for (int i = 0; i < kCh; ++i) {
+    if (k0 + i < len) {   // uniform
+      const unsigned e = ch.en[i].x;
+      const u32x4 uv = *reinterpret_cast<const u32x4*>(uL + (e & 0xffffu) * kTT);
+      const u32x4 zv = *reinterpret_cast<const u32x4*>(tile + ((e >> 16) & 0xffu) * kTT);
+      float s = 0.f;
+  #pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        // copy the elements out first: bit-casting a vector element expression directly reads
+        // element 0 with this compiler
+        const unsigned uw = uv[j], zw = zv[j];
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, uw), __builtin_bit_cast(bf16x2, zw), s, false);
+      }
+      part[(long)(k0 + i) * 64 + lane] = (e & kValid) ? s : 0.f;
+    }
+  }
+}
+
+__device__ __forceinline__ void bwd_spmm(const BwdChunk& ch, int len, int k0, const u16* uL, u16* tile,
+                                         float (&a)[8]) {
+#pragma unroll
+  for (int i = 0; i < kCh; ++i) {
+    if (k0 + i < len) {   // uniform
+      const unsigned e = ch.en[i].x;
+      accum_row(e, (e & kValid) ? ch.cc[i] : 0.f, uL, tile, a);
+    }
+  }
 }
 
 struct FastArgs {
@@ -209,45 +308,77 @@ struct FastArgs {
   int want_dx, want_dc;
   const int* off;     // per pair: first stream row
   const int* len;     // per pair: stream rows
-  const uint2* st;
-  const int* soff;    // dC streams (backward)
-  const int* slen;
-  const uint2* sst;
-  int slots;          // dC slots per tile
+  const unsigned* fst;
+  const int2* fri;
+  const uint2* bst;
+  int slots;          // dC partials per tile
   float* partial;     // [batch][tile][slots]
   long ntiles;
 };
 
+// Analysis of every pair of blocks of a tile into a coefficient-major LDS array, two pairs'
+// inputs in flight per wave.
+__device__ __forceinline__ void analysis_phase(const Frag& F, const u16* rows, long ld, int nt, int np, int wave,
+                                               int lane, u16* lds) {
+  u32x4 bA[kKT], bB[kKT];
+  if (wave < np) load_act(rows, ld, nt, 2 * wave, lane, bA);
+  if (wave + kWaves < np) load_act(rows, ld, nt, 2 * (wave + kWaves), lane, bB);
+  for (int p = wave; p < np; p += 2 * kWaves) {
+    {
+      f32x4 acc[kMT];
+      mfma_block(F, bA, acc, true);
+      store_coef(lds, 2 * p, 0, nt, lane, acc);
+    }
+    if (p + 2 * kWaves < np) load_act(rows, ld, nt, 2 * (p + 2 * kWaves), lane, bA);
+    if (p + kWaves < np) {
+      f32x4 acc[kMT];
+      mfma_block(F, bB, acc, true);
+      store_coef(lds, 2 * (p + kWaves), 0, nt, lane, acc);
+      if (p + 3 * kWaves < np) load_act(rows, ld, nt, 2 * (p + 3 * kWaves), lane, bB);
+    }
+  }
+}
+
 __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   u16* zL = reinterpret_cast<u16*>(smem);                          // n rows x 8 tokens
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   u16* tile = zL + (long)a.nblk_in * kW * kTT + wave * (2 * kW * kTT);
   const int bi = blockIdx.y;
   const int t0 = blockIdx.x * kTT, nt = min(kTT, a.T - t0);
   const u16* X = reinterpret_cast<const u16*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx;
   u16* Y = reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy;
   const float* cv = a.cs ? a.cs[bi] : a.c;
+  const int npo = a.nblk_out / 2;
+
+  // first stream chunk of this wave's first output pair, in flight during the analysis
+  FwdChunk ch;
+  if (wave < npo && a.len[wave] > 0) fwd_load(a.fst, a.fri, a.off[wave], a.len[wave], 0, cv, lane, ch);
 
   Frag F;
-  load_frag(a.frag, lane, F);
-  // z = P_in^T x for the tile, one pair of blocks per step
-  for (int p = wave; p < a.nblk_in / 2; p += kWaves) {
-    u32x4 b[kKT];
-    f32x4 acc[kMT];
-    load_act(X, a.ldx, nt, 2 * p, lane, true, b);
-    mfma_block(F, b, acc);
-    store_coef(zL, 2 * p, 0, lane, acc);
-  }
+  load_frag(a.frag, reinterpret_cast<u32x4*>(smem), lane, F);
+  analysis_phase(F, X, a.ldx, nt, a.nblk_in / 2, wave, lane, zL);
   __syncthreads();
-  // per output pair: v = C z into the wave's tile, then y = beta y + s P_out v
-  for (int p = wave; p < a.nblk_out / 2; p += kWaves) {
-    spmm_stream(a.st + (long)a.off[p] * 64, a.len[p], cv, zL, tile, lane);
+
+  for (int p = wave; p < npo; p += kWaves) {
+    // v = C z for this pair into the tile
+    const int off = a.off[p], len = a.len[p];
+    zero_tile(tile, lane);
+    float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < len; k0 += kCh) {
+      if (k0 > 0) fwd_load(a.fst, a.fri, off, len, k0, cv, lane, ch);
+      fwd_compute(ch, len, k0, zL, tile, acc8);
+    }
+    wave_lds_fence();
+    // next pair's first chunk flies during this pair's synthesis
+    const int pn = p + kWaves;
+    if (pn < npo && a.len[pn] > 0) fwd_load(a.fst, a.fri, a.off[pn], a.len[pn], 0, cv, lane, ch);
+    // y = beta y + s P_out v
     u32x4 b[kKT];
     f32x4 acc[kMT];
     load_tile_act(tile, lane, b);
     wave_lds_fence();
-    mfma_block(F, b, acc);
+    mfma_block(F, b, acc, false);
     store_act(Y, a.ldy, nt, 2 * p, lane, acc, a.scale, a.beta);
   }
 }
@@ -255,7 +386,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a) {
 __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   u16* uL = reinterpret_cast<u16*>(smem);                          // m rows x 8 tokens
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   u16* tile = uL + (long)a.nblk_out * kW * kTT + wave * (2 * kW * kTT);
   const int bi = blockIdx.y;
   const int t0 = blockIdx.x * kTT, nt = min(kTT, a.T - t0);
@@ -264,65 +395,74 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a) {
   u16* dX = a.want_dx ? reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy : nullptr;
   const float* cv = a.cs ? a.cs[bi] : a.c;
   float* part = a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.slots;
+  const int npi = a.nblk_in / 2;
+
+  // this wave's first input pair: stream entries and x in flight during the analysis of g
+  BwdChunk ch;
+  u32x4 bx[kKT];
+  if (wave < npi) {
+    if (a.len[wave] > 0) bwd_load_entries(a.bst + (long)a.off[wave] * 64, a.len[wave], 0, lane, ch);
+    if (a.want_dc) load_act(X, a.ldx, nt, 2 * wave, lane, bx);
+  }
 
   Frag F;
-  load_frag(a.frag, lane, F);
-  // u = P_out^T g for the tile
-  for (int p = wave; p < a.nblk_out / 2; p += kWaves) {
-    u32x4 b[kKT];
-    f32x4 acc[kMT];
-    load_act(G, a.ldg, nt, 2 * p, lane, true, b);
-    mfma_block(F, b, acc);
-    store_coef(uL, 2 * p, 0, lane, acc);
-  }
+  load_frag(a.frag, reinterpret_cast<u32x4*>(smem), lane, F);
+  analysis_phase(F, G, a.ldg, nt, a.nblk_out / 2, wave, lane, uL);
   __syncthreads();
-  for (int p = wave; p < a.nblk_in / 2; p += kWaves) {
+
+  for (int p = wave; p < npi; p += kWaves) {
+    const int len = a.len[p];
+    const uint2* st = a.bst + (long)a.off[p] * 64;
+    if (a.want_dx && len > 0) bwd_load_coeffs(cv, ch);
     if (a.want_dc) {
-      // z = P_in^T x for this pair of input blocks, then this tile's share of dC
-      u32x4 b[kKT];
+      // z = P_in^T x for this pair, then this tile's share of dC
       f32x4 acc[kMT];
-      load_act(X, a.ldx, nt, 2 * p, lane, true, b);
-      mfma_block(F, b, acc);
-      store_coef(tile, 2 * p, 2 * p, lane, acc);
+      mfma_block(F, bx, acc, true);
+      store_coef(tile, 2 * p, 2 * p, nt, lane, acc);
       wave_lds_fence();
-      const uint2* st = a.sst + (long)a.soff[p] * 64;
-      float* pp = part + (long)a.soff[p] * 64;
-      for (int k = 0; k < a.slen[p]; ++k) {
-        const uint2 en = st[(long)k * 64 + lane];
-        float s = 0.f;
-        if (en.x & kValid) {
-          const u32x4 uv = *reinterpret_cast<const u32x4*>(uL + (en.x & 0xffffu) * kTT);
-          const u32x4 zv = *reinterpret_cast<const u32x4*>(tile + ((en.x >> 16) & 0xffu) * kTT);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            // copy the elements out first: bit-casting a vector element expression directly
-            // reads element 0 with this compiler
-            const unsigned uw = uv[i], zw = zv[i];
-            s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, uw), __builtin_bit_cast(bf16x2, zw), s,
-                                                false);
-          }
-        }
-        pp[(long)k * 64 + lane] = s;
+      if (p + kWaves < npi) load_act(X, a.ldx, nt, 2 * (p + kWaves), lane, bx);
+      float* pp = part + (long)a.off[p] * 64;
+      for (int k0 = 0; k0 < len; k0 += kCh) {
+        if (k0 > 0) bwd_load_entries(st, len, k0, lane, ch);
+        bwd_sddmm(ch, len, k0, uL, tile, pp, lane);
       }
       wave_lds_fence();
+      if (a.want_dx && len > kCh) {   // the stream is reread for q
+        bwd_load_entries(st, len, 0, lane, ch);
+        bwd_load_coeffs(cv, ch);
+      }
     }
     if (a.want_dx) {
       // q = C^T u for this pair, then dX = beta dX + s P_in q
-      spmm_stream(a.st + (long)a.off[p] * 64, a.len[p], cv, uL, tile, lane);
+      zero_tile(tile, lane);
+      float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      for (int k0 = 0; k0 < len; k0 += kCh) {
+        if (k0 > 0) {
+          bwd_load_entries(st, len, k0, lane, ch);
+          bwd_load_coeffs(cv, ch);
+        }
+        bwd_spmm(ch, len, k0, uL, tile, acc8);
+      }
+      wave_lds_fence();
+    }
+    const int pn = p + kWaves;
+    if (pn < npi && a.len[pn] > 0) bwd_load_entries(a.bst + (long)a.off[pn] * 64, a.len[pn], 0, lane, ch);
+    if (a.want_dx) {
       u32x4 b[kKT];
       f32x4 acc[kMT];
       load_tile_act(tile, lane, b);
       wave_lds_fence();
-      mfma_block(F, b, acc);
+      mfma_block(F, b, acc, false);
       store_act(dX, a.ldy, nt, 2 * p, lane, acc, a.scale, a.beta);
     }
   }
 }
 
-// dC[e] = [dC[e] +] s * sum_tiles partial[tile][slot] for every valid slot of the dC streams.
-// Eight waves split the tiles; their sums are combined in a fixed order.
+// dC[j] = [dC[j] +] s * sum_tiles partial[tile][slot] for every valid slot of the backward
+// streams (j = the slot's plan index).  Eight waves split the tiles; their sums are combined
+// in a fixed order.
 __global__ void __launch_bounds__(512) reduce128(const float* __restrict__ partial, long ntiles, int slots,
-                                                 const uint2* __restrict__ sst, float scale, int accumulate,
+                                                 const uint2* __restrict__ bst, float scale, int accumulate,
                                                  float* dC, float* const* dCs) {
   __shared__ float red[8][64];
   const int bi = blockIdx.y;
@@ -331,7 +471,16 @@ __global__ void __launch_bounds__(512) reduce128(const float* __restrict__ parti
   float s = 0.f;
   if (slot < slots) {
     const float* p = partial + (long)bi * ntiles * slots + slot;
-    for (long t = w; t < ntiles; t += 8) s += p[t * slots];
+    float s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    long t = w;
+    for (; t + 24 < ntiles; t += 32) {
+      s += p[t * slots];
+      s1 += p[(t + 8) * slots];
+      s2 += p[(t + 16) * slots];
+      s3 += p[(t + 24) * slots];
+    }
+    for (; t < ntiles; t += 8) s += p[t * slots];
+    s = (s + s1) + (s2 + s3);
   }
   red[w][lane] = s;
   __syncthreads();
@@ -339,7 +488,7 @@ __global__ void __launch_bounds__(512) reduce128(const float* __restrict__ parti
     float tot = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) tot += red[i][lane];
-    const uint2 en = sst[slot];
+    const uint2 en = bst[slot];
     if (en.x & kValid) {
       float* out = dCs ? dCs[bi] : dC;
       const float v = scale * tot;
@@ -366,7 +515,13 @@ hipError_t configure_fast128() {
   return once;
 }
 
-size_t fast128_lds_bytes(int nblk) { return (size_t)nblk * kW * kTT * 2 + (size_t)kWaves * 2 * kW * kTT * 2; }
+// The coefficient array (nblk 128-row blocks of 16 bytes) plus one 4 KB tile per wave; at least
+// the 16 KB of fragments staged at kernel start.
+size_t fast128_lds_bytes(int nblk) {
+  const size_t b = (size_t)nblk * kW * kTT * 2 + (size_t)kWaves * 2 * kW * kTT * 2;
+  const size_t frag = (size_t)kHT * kKT * 64 * 16;
+  return b < frag ? frag : b;
+}
 
 hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, const float* c,
                          const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, hipStream_t s) {
@@ -387,7 +542,8 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   a.beta = beta;
   a.off = p->fast.fwd_off;
   a.len = p->fast.fwd_len;
-  a.st = p->fast.fwd_st;
+  a.fst = p->fast.fwd_st;
+  a.fri = p->fast.fwd_ri;
   const dim3 grid((unsigned)((T + kTT - 1) / kTT), (unsigned)count);
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
@@ -423,11 +579,8 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   a.want_dc = want_dc;
   a.off = p->fast.bwd_off;
   a.len = p->fast.bwd_len;
-  a.st = p->fast.bwd_st;
-  a.soff = p->fast.sdd_off;
-  a.slen = p->fast.sdd_len;
-  a.sst = p->fast.sdd_st;
-  a.slots = p->fast.sdd_slots;
+  a.bst = p->fast.bwd_st;
+  a.slots = p->fast.bwd_slots;
   a.partial = p->partial;
   const long ntiles = (T + kTT - 1) / kTT;
   a.ntiles = ntiles;
@@ -443,7 +596,7 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   }
   if (want_dc) {
     const dim3 grid((unsigned)((a.slots + 63) / 64), (unsigned)count);
-    hipLaunchKernelGGL(reduce128, grid, dim3(512), 0, s, p->partial, ntiles, a.slots, a.sst, scale, accumulate_dc, dC,
+    hipLaunchKernelGGL(reduce128, grid, dim3(512), 0, s, p->partial, ntiles, a.slots, a.bst, scale, accumulate_dc, dC,
                        dCs);
   }
   return hipGetLastError();

@@ -40,37 +40,28 @@ int swz128(int blk, int o) { return o ^ ((o >> 2) & 4) ^ ((blk & 1) << 1); }
 
 constexpr uint32_t kStreamValid = 1u << 25, kStreamEnd = 1u << 24;
 
-// Lane-interleaved stream for one pair of blocks: destination row r (0..255) collects
-// rows[r] = (source row, user index e) entries.  Rows go whole to the least-loaded of 64
-// lanes (longest first); slot k of lane l is stream element k*64 + l.  Returns the number
-// of stream rows appended.
-int balanced_stream(const std::vector<std::vector<std::pair<uint32_t, int>>>& rows,
-                    const std::vector<uint32_t>& dst, std::vector<uint2>& st) {
+// Rows of one pair of blocks assigned whole to 64 lanes, longest first, each to the least
+// loaded lane; lanes are then renumbered by decreasing load, so in every stream row the
+// occupied slots are a prefix of the lanes.  Returns, per lane, its rows in order.
+std::vector<std::vector<int>> assign_lanes(const std::vector<int>& row_size, int& len) {
   std::vector<int> order;
-  for (int r = 0; r < (int)rows.size(); ++r)
-    if (!rows[r].empty()) order.push_back(r);
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return rows[a].size() > rows[b].size(); });
+  for (int r = 0; r < (int)row_size.size(); ++r)
+    if (row_size[r] > 0) order.push_back(r);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return row_size[a] > row_size[b]; });
   std::vector<int> load(64, 0);
   std::vector<std::vector<int>> lane_rows(64);
   for (int r : order) {
     const int l = (int)(std::min_element(load.begin(), load.end()) - load.begin());
     lane_rows[l].push_back(r);
-    load[l] += (int)rows[r].size();
+    load[l] += row_size[r];
   }
-  const int len = *std::max_element(load.begin(), load.end());
-  const size_t base = st.size();
-  st.resize(base + (size_t)len * 64, make_uint2(0u, 0u));
-  for (int l = 0; l < 64; ++l) {
-    int k = 0;
-    for (int r : lane_rows[l])
-      for (size_t i = 0; i < rows[r].size(); ++i, ++k) {
-        const bool last = i + 1 == rows[r].size();
-        st[base + (size_t)k * 64 + l] = make_uint2(rows[r][i].first | (dst[r] << 16) | kStreamValid |
-                                                       (last ? kStreamEnd : 0u),
-                                                   (unsigned)rows[r][i].second);
-      }
-  }
-  return len;
+  std::vector<int> lanes(64);
+  std::iota(lanes.begin(), lanes.end(), 0);
+  std::stable_sort(lanes.begin(), lanes.end(), [&](int a, int b) { return load[a] > load[b]; });
+  std::vector<std::vector<int>> out(64);
+  for (int l = 0; l < 64; ++l) out[l] = lane_rows[lanes[l]];
+  len = load[lanes[0]];
+  return out;
 }
 
 }  // namespace
@@ -197,54 +188,105 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   }
 
   // ---------------- 128-wide fused path: balanced entry streams per pair of blocks
+  // Forward stream (v = C z), one per pair of output blocks: slot word = source row of z
+  // (16 bits) | destination row of the pair tile (8 bits) | end-of-row | valid.  The plan
+  // order of the coefficients is the order of the valid forward slots (pair, stream row,
+  // lane), so slot (row, lane) reads coefficient rowinfo[row].x + lane.
+  // Backward stream (dC and q = C^T u), one per pair of input blocks, grouped by column
+  // of C: (source row of u | tile row of the column | end-of-column | valid, plan index).
   const bool fast = FI.W == 128 && FO.W == 128 && FI.nblk % 2 == 0 && FO.nblk % 2 == 0 &&
-                    f_in->transpose_is_sign_flip && f_out->transpose_is_sign_flip && f_in->B == f_out->B &&
+                    f_in->transpose_is_sign_flip && f_in->half_shift_sign && f_in->B == f_out->B &&
                     n < 65536 && m < 65536 &&
                     ff::fast128_lds_bytes(std::max(FI.nblk, FO.nblk)) <= (size_t)ff::kMaxLdsBytes;
-  std::vector<int> f_off, f_len, b_off, b_len, s_off, s_len;
-  std::vector<uint2> f_st, b_st, s_st;
+  std::vector<int> f_off, f_len, b_off, b_len;
+  std::vector<uint32_t> f_st;
+  std::vector<int2> f_ri;
+  std::vector<uint2> b_st;
+  std::vector<int> plan_of_user((size_t)nnz), user_of_plan((size_t)nnz);
   if (fast) {
-    auto zrow = [&](const Loc& l) { return (uint32_t)(l.blk * 128 + swz128(l.blk, l.local)); };
+    auto lrow = [&](const Loc& l) { return (uint32_t)(l.blk * 128 + swz128(l.blk, l.local)); };
     auto trow = [&](const Loc& l) { return (uint32_t)((l.blk & 1) * 128 + swz128(l.blk, l.local)); };
     const int npo = FO.nblk / 2, npi = FI.nblk / 2;
-    std::vector<std::vector<std::vector<std::pair<uint32_t, int>>>> frows(npo), brows(npi);
-    std::vector<std::vector<uint32_t>> fdst(npo, std::vector<uint32_t>(256)), bdst(npi, std::vector<uint32_t>(256));
-    for (auto& v : frows) v.assign(256, {});
-    for (auto& v : brows) v.assign(256, {});
-    for (int pp = 0; pp < npo; ++pp)
-      for (int r = 0; r < 256; ++r) fdst[pp][r] = (uint32_t)((r >> 7) * 128 + swz128(r >> 7, r & 127));
-    for (int pp = 0; pp < npi; ++pp)
-      for (int r = 0; r < 256; ++r) bdst[pp][r] = (uint32_t)((r >> 7) * 128 + swz128(r >> 7, r & 127));
-    std::vector<std::vector<std::pair<uint32_t, int>>> sent(npi);
+    // entries of each destination row r = (block parity)*128 + local of a pair
+    std::vector<std::vector<std::vector<int>>> frows(npo, std::vector<std::vector<int>>(256)),
+        brows(npi, std::vector<std::vector<int>>(256));
     for (int64_t e = 0; e < nnz; ++e) {
-      const Loc& a = rloc[e];
-      const Loc& b = cloc[e];
-      frows[a.blk / 2][(a.blk & 1) * 128 + a.local].push_back({zrow(b), (int)e});
-      brows[b.blk / 2][(b.blk & 1) * 128 + b.local].push_back({zrow(a), (int)e});
-      sent[b.blk / 2].push_back({zrow(a) | (trow(b) << 16), (int)e});
+      frows[rloc[e].blk / 2][(rloc[e].blk & 1) * 128 + rloc[e].local].push_back((int)e);
+      brows[cloc[e].blk / 2][(cloc[e].blk & 1) * 128 + cloc[e].local].push_back((int)e);
     }
+    int next_plan = 0;
     for (int pp = 0; pp < npo; ++pp) {
-      f_off.push_back((int)(f_st.size() / 64));
-      f_len.push_back(balanced_stream(frows[pp], fdst[pp], f_st));
+      std::vector<int> sz(256);
+      for (int r = 0; r < 256; ++r) sz[r] = (int)frows[pp][r].size();
+      int len = 0;
+      const auto lanes = assign_lanes(sz, len);
+      f_off.push_back((int)f_ri.size());
+      f_len.push_back(len);
+      const size_t base = f_st.size();
+      f_st.resize(base + (size_t)len * 64, 0u);
+      std::vector<std::vector<int>> slot_e(64);         // entries of each lane in slot order
+      for (int l = 0; l < 64; ++l)
+        for (int r : lanes[l])
+          for (size_t i = 0; i < frows[pp][r].size(); ++i) {
+            const int e = frows[pp][r][i];
+            const bool last = i + 1 == frows[pp][r].size();
+            const uint32_t dst = (uint32_t)((r >> 7) * 128 + swz128(r >> 7, r & 127));
+            f_st[base + slot_e[l].size() * 64 + l] =
+                lrow(cloc[e]) | (dst << 16) | kStreamValid | (last ? kStreamEnd : 0u);
+            slot_e[l].push_back(e);
+          }
+      for (int k = 0; k < len; ++k) {
+        int cnt = 0;
+        while (cnt < 64 && (int)slot_e[cnt].size() > k) ++cnt;
+        f_ri.push_back(make_int2(next_plan, cnt));
+        for (int l = 0; l < cnt; ++l) {
+          user_of_plan[next_plan + l] = slot_e[l][k];
+          plan_of_user[slot_e[l][k]] = next_plan + l;
+        }
+        next_plan += cnt;
+      }
     }
     for (int pp = 0; pp < npi; ++pp) {
+      std::vector<int> sz(256);
+      for (int r = 0; r < 256; ++r) sz[r] = (int)brows[pp][r].size();
+      int len = 0;
+      const auto lanes = assign_lanes(sz, len);
       b_off.push_back((int)(b_st.size() / 64));
-      b_len.push_back(balanced_stream(brows[pp], bdst[pp], b_st));
-      s_off.push_back((int)(s_st.size() / 64));
-      const int rows64 = (int)((sent[pp].size() + 63) / 64);
-      s_len.push_back(rows64);
-      const size_t base = s_st.size();
-      s_st.resize(base + (size_t)rows64 * 64, make_uint2(0u, 0u));
-      for (size_t i = 0; i < sent[pp].size(); ++i)
-        s_st[base + i] = make_uint2(sent[pp][i].first | kStreamValid, (unsigned)sent[pp][i].second);
+      b_len.push_back(len);
+      const size_t base = b_st.size();
+      b_st.resize(base + (size_t)len * 64, make_uint2(0u, 0u));
+      for (int l = 0; l < 64; ++l) {
+        int k = 0;
+        for (int r : lanes[l])
+          for (size_t i = 0; i < brows[pp][r].size(); ++i, ++k) {
+            const int e = brows[pp][r][i];
+            const bool last = i + 1 == brows[pp][r].size();
+            b_st[base + (size_t)k * 64 + l] = make_uint2(
+                lrow(rloc[e]) | (trow(cloc[e]) << 16) | kStreamValid | (last ? kStreamEnd : 0u),
+                (unsigned)plan_of_user[e]);
+          }
+      }
     }
+  } else {
+    std::iota(plan_of_user.begin(), plan_of_user.end(), 0);
+    std::iota(user_of_plan.begin(), user_of_plan.end(), 0);
   }
+  // the generic kernels index coefficients in plan order too
+  for (auto& en : fwd_ent) en.y = nnz ? plan_of_user[en.y] : 0;
+  for (auto& en : bwd_ent) en.y = nnz ? plan_of_user[en.y] : 0;
+  for (auto& en : mrg_ent) en.z = nnz ? plan_of_user[en.z] : 0;
+  {
+    std::vector<int2> sdd_plan(sdd.size());
+    for (int64_t e = 0; e < nnz; ++e) sdd_plan[plan_of_user[e]] = sdd[e];
+    if (nnz) sdd = sdd_plan;
+  }
+  p->user_order.assign(user_of_plan.begin(), user_of_plan.end());
   const int64_t fast_tiles = fast ? (max_tokens + ff::kFastTileTokens - 1) / ff::kFastTileTokens : 0;
 
   // ---------------- device memory: one allocation for every table and the workspace
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t partial_elems = std::max((size_t)max_batch * (size_t)p->max_tiles * (size_t)nnz,
-                                        (size_t)max_batch * (size_t)fast_tiles * s_st.size());
+                                        (size_t)max_batch * (size_t)fast_tiles * b_st.size());
   struct Blob {
     const void* src;
     size_t bytes;
@@ -256,10 +298,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       {sdd.data(), sdd.size() * sizeof(int2)},       {mrg_ptr.data(), (nb + 1) * sizeof(int)},
       {mrg_ent.data(), mrg_ent.size() * sizeof(int4)},
       {f_off.data(), f_off.size() * sizeof(int)},     {f_len.data(), f_len.size() * sizeof(int)},
-      {f_st.data(), f_st.size() * sizeof(uint2)},     {b_off.data(), b_off.size() * sizeof(int)},
-      {b_len.data(), b_len.size() * sizeof(int)},     {b_st.data(), b_st.size() * sizeof(uint2)},
-      {s_off.data(), s_off.size() * sizeof(int)},     {s_len.data(), s_len.size() * sizeof(int)},
-      {s_st.data(), s_st.size() * sizeof(uint2)},
+      {f_st.data(), f_st.size() * sizeof(uint32_t)},  {f_ri.data(), f_ri.size() * sizeof(int2)},
+      {b_off.data(), b_off.size() * sizeof(int)},     {b_len.data(), b_len.size() * sizeof(int)},
+      {b_st.data(), b_st.size() * sizeof(uint2)},
       {nullptr, std::max<size_t>(partial_elems, 1) * sizeof(float)}};
   size_t total = 0;
   for (const Blob& b : blobs) total += up(b.bytes);
@@ -302,15 +343,13 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   fp.enabled = fast ? 1 : 0;
   fp.fwd_off = (const int*)where[9];
   fp.fwd_len = (const int*)where[10];
-  fp.fwd_st = (const uint2*)where[11];
-  fp.bwd_off = (const int*)where[12];
-  fp.bwd_len = (const int*)where[13];
-  fp.bwd_st = (const uint2*)where[14];
-  fp.sdd_off = (const int*)where[15];
-  fp.sdd_len = (const int*)where[16];
-  fp.sdd_st = (const uint2*)where[17];
-  fp.sdd_slots = (int)s_st.size();
-  p->partial = (float*)where[18];
+  fp.fwd_st = (const uint32_t*)where[11];
+  fp.fwd_ri = (const int2*)where[12];
+  fp.bwd_off = (const int*)where[13];
+  fp.bwd_len = (const int*)where[14];
+  fp.bwd_st = (const uint2*)where[15];
+  fp.bwd_slots = (int)b_st.size();
+  p->partial = (float*)where[16];
   p->dev_mem = mem;
   p->workspace_bytes = total;
   p->fin->refs.fetch_add(1);
@@ -325,6 +364,13 @@ extern "C" void ff_plan_destroy(ff_plan* p) {
   ff_frame_destroy(p->fin);
   ff_frame_destroy(p->fout);
   delete p;
+}
+
+extern "C" ff_status ff_plan_order(const ff_plan* p, int64_t* user_index) {
+  ff::clear_error();
+  if (!p || (!user_index && p->nnz > 0)) return ff::fail(FF_EINVAL, "NULL argument");
+  for (int64_t j = 0; j < p->nnz; ++j) user_index[j] = p->user_order[j];
+  return FF_OK;
 }
 
 extern "C" ff_status ff_plan_query(const ff_plan* p, int key, int64_t* value) {

@@ -47,3 +47,16 @@ def merged_bf16_ok(got, W0, dW):
     want = inputs.bf16_round(exact.astype(np.float32)).astype(np.float64)
     bound = bf16_ulp(want) + 2.0 ** -22 * (np.abs(W0) + np.abs(dW)) + 1e-30
     return bool(np.all(np.abs(np.asarray(got, dtype=np.float64) - want) <= bound))
+
+
+def plan_c(plan, vals, device):
+    """User-order coefficient values -> device fp32 tensor in the plan's order."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(vals, dtype=np.float32)[plan.order])).to(device)
+
+
+def user_dc(plan, dC):
+    """Plan-order dC (device tensor) -> fp64 host array in user order."""
+    out = np.empty(plan.nnz, dtype=np.float64)
+    out[plan.order] = to_np(dC)
+    return out

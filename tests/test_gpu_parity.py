@@ -11,7 +11,7 @@ import pytest
 
 from oracle import frameft_oracle as O
 from paper_2608_26430_amd import inputs
-from tests.parity_util import TOL, merged_bf16_ok, oracle_frame, rel, to_np, torch_act
+from tests.parity_util import TOL, merged_bf16_ok, oracle_frame, plan_c, rel, to_np, torch_act, user_dc
 
 torch = pytest.importorskip("torch")
 import paper_2608_26430_amd as ff  # noqa: E402
@@ -79,7 +79,9 @@ def test_small_parity(dev, shape, dtype):
     assert plan.fast128 == (n // rn == 64 and m // rm == 64 and (n // 128) % 2 == 0 and (m // 128) % 2 == 0)
     tol = TOL[dtype]
     Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
-    c = torch.from_numpy(vals).to(dev)
+    c = plan_c(plan, vals, dev)
+    order = plan.order
+    assert np.array_equal(np.sort(order), np.arange(nnz))
 
     # forward, overwrite and accumulate into an existing Y
     y_ref = O.adapter_fwd(P_in, P_out, rows, cols, vals, s, X)
@@ -90,9 +92,9 @@ def test_small_parity(dev, shape, dtype):
     dx_ref, dc_ref = O.adapter_bwd(P_in, P_out, rows, cols, vals, s, X, G)
     dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s)
     dX0 = inputs.gaussian(inputs.rng(4), (T, n), dtype=dtype)
-    dC0 = inputs.gaussian(inputs.rng(5), (nnz,))
+    dC0 = inputs.gaussian(inputs.rng(5), (nnz,)).astype(np.float32)
     dXb, dCb = ff.adapter_bwd(plan, Xd, Gd, c, s, dX=torch_act(dX0, dtype, dev), beta_dx=-1.5,
-                              dC=torch.from_numpy(dC0.copy()).to(dev), accumulate_dc=True)
+                              dC=plan_c(plan, dC0, dev), accumulate_dc=True)
     _, dC2 = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dx=False)
     # merge: dense delta into fp32, and in place into a bf16 weight
     dw_ref = O.merge_delta(P_in, P_out, rows, cols, vals, s)
@@ -108,9 +110,9 @@ def test_small_parity(dev, shape, dtype):
     assert rel(to_np(Y), y_ref) <= tol
     assert rel(to_np(Yb), 0.75 * Y0 + y_ref) <= tol
     assert rel(to_np(dX), dx_ref) <= tol
-    assert rel(to_np(dC), dc_ref) <= tol
+    assert rel(user_dc(plan, dC), dc_ref) <= tol
     assert rel(to_np(dXb), -1.5 * dX0 + dx_ref) <= tol
-    assert rel(to_np(dCb), dC0 + dc_ref) <= tol
+    assert rel(user_dc(plan, dCb), dC0 + dc_ref) <= tol
     assert torch.equal(dC, dC2), "dC is not deterministic"
     assert rel(to_np(Wd), dw_ref) <= 1e-5
     assert merged_bf16_ok(to_np(Wb), W0, dw_ref)
@@ -130,7 +132,7 @@ def test_batched_matches_single_calls(dev, dtype):
     Gs = [inputs.gaussian(g, (T, m), dtype=dtype) for _ in range(count)]
     Xd = [torch_act(x, dtype, dev) for x in Xs]
     Gd = [torch_act(x, dtype, dev) for x in Gs]
-    cd = [torch.from_numpy(v).to(dev) for v in vals]
+    cd = [plan_c(plan, v, dev) for v in vals]
     Yd = [torch.empty((T, m), dtype=Xd[0].dtype, device=dev) for _ in range(count)]
     dXd = [torch.empty((T, n), dtype=Xd[0].dtype, device=dev) for _ in range(count)]
     dCd = [torch.empty((nnz,), device=dev) for _ in range(count)]
@@ -143,7 +145,7 @@ def test_batched_matches_single_calls(dev, dtype):
         dx_ref, dc_ref = O.adapter_bwd(P, P, rows, cols, vals[i], s, Xs[i], Gs[i])
         assert rel(to_np(Yd[i]), y_ref) <= tol
         assert rel(to_np(dXd[i]), dx_ref) <= tol
-        assert rel(to_np(dCd[i]), dc_ref) <= tol
+        assert rel(user_dc(plan, dCd[i]), dc_ref) <= tol
 
 
 def test_empty_batch_is_noop_and_zeroes_dc(dev):
@@ -151,7 +153,7 @@ def test_empty_batch_is_noop_and_zeroes_dc(dev):
     rows, cols, vals, X, G = _problem((n, 16, m, 16, 100, 4), "f32", 1)
     f = ff.framegen(256, 16, 16)
     plan = ff.plan_create(f, f, rows, cols, max_tokens=4)
-    c = torch.from_numpy(vals).to(dev)
+    c = plan_c(plan, vals, dev)
     Xe = torch.zeros((0, n), device=dev)
     Ge = torch.zeros((0, m), device=dev)
     Y = ff.adapter_fwd(plan, Xe, c, 1.0)
@@ -171,7 +173,7 @@ def test_argument_errors_write_nothing(dev):
     with pytest.raises(ff.FrameFTError):
         ff.plan_create(f, f, np.array([256]), np.array([0]), max_tokens=8)
     plan = ff.plan_create(f, f, rows, cols, max_tokens=8)
-    c = torch.from_numpy(vals).to(dev)
+    c = plan_c(plan, vals, dev)
     Y = torch.full((9, 256), 3.0, device=dev)
     with pytest.raises(ff.FrameFTError) as ei:       # T above max_tokens
         ff.adapter_fwd(plan, torch.zeros((9, 256), device=dev), c, 1.0, Y=Y)
@@ -203,7 +205,7 @@ def _full_size_check(dev, wl_name, adapter_index=0, n_tok=48, n_nnz=384, n_rows=
     f_out = ff.framegen(ad.d_out, ad.k_out, ad.rho_out)
     plan = ff.plan_create(f_in, f_out, data.rows, data.cols, max_tokens=T)
     Xd, Gd = torch_act(data.X, dtype, dev), torch_act(data.G, dtype, dev)
-    c = torch.from_numpy(data.vals).to(dev)
+    c = plan_c(plan, data.vals, dev)
     Y = ff.adapter_fwd(plan, Xd, c, data.scale)
     dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, data.scale)
     W0 = inputs.weight(inputs.rng(wl.seed + 99), ad.d_out, ad.d_in, "bf16")
@@ -219,7 +221,7 @@ def _full_size_check(dev, wl_name, adapter_index=0, n_tok=48, n_nnz=384, n_rows=
     assert rel(to_np(dX[tok]), dx_ref) <= tol
     ent = np.random.default_rng(wl.seed + 1).choice(ad.nnz, size=min(n_nnz, ad.nnz), replace=False)
     dc_ref = O.coeff_grad_entries(P_in, P_out, data.rows[ent], data.cols[ent], data.scale, data.X, data.G)
-    assert rel(to_np(dC)[ent], dc_ref) <= tol
+    assert rel(user_dc(plan, dC)[ent], dc_ref) <= tol
     r = np.unique(np.concatenate([[0, ad.d_out - 1], np.random.default_rng(wl.seed + 2).integers(0, ad.d_out, n_rows)]))
     dw_ref = O.merge_delta_rows(P_in, P_out, data.rows, data.cols, data.vals, data.scale, r)
     assert rel(to_np(Wd[r]), dw_ref) <= 1e-5

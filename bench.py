@@ -110,10 +110,10 @@ def main():
 
     X = torch.from_numpy(data.X).to(dev, tdt)
     G = torch.from_numpy(data.G).to(dev, tdt)
-    c = torch.from_numpy(np.ascontiguousarray(data.vals[plan.order])).to(dev)   # plan order
+    c = torch.from_numpy(plan.to_plan(data.vals)).to(dev)      # plan layout (padded)
     Y = torch.empty((T, m), dtype=tdt, device=dev)
     dX = torch.empty((T, n), dtype=tdt, device=dev)
-    dC = torch.empty((nnz,), dtype=torch.float32, device=dev)
+    dC = torch.empty((plan.coef_slots,), dtype=torch.float32, device=dev)
 
     def step(evs=None):
         if evs is not None:

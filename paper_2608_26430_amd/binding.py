@@ -176,14 +176,37 @@ class Plan:
         return bool(self.query(4))
 
     @property
+    def coef_slots(self) -> int:
+        """Length L of every c / dC array of this plan (nnz plus padding slots)."""
+        return self.query(5)
+
+    @property
     def order(self) -> np.ndarray:
-        """user index of each plan-ordered coefficient: c_plan = c_user[order],
-        dC_user[order] = dC_plan."""
+        """User index of the support entry in each coefficient slot, -1 for padding:
+        c_plan[j] = c_user[order[j]] where order[j] >= 0, dC_user[order[j]] = dC_plan[j]."""
         if self._order is None:
-            o = np.empty(self.nnz, dtype=np.int64)
+            o = np.empty(self.coef_slots, dtype=np.int64)
             _check(_load().ff_plan_order(self._h, o.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))))
             self._order = o
         return self._order
+
+    def to_plan(self, c_user) -> np.ndarray:
+        """Host user-order coefficients (nnz) -> plan layout (L, fp32, zero padding)."""
+        c_user = np.asarray(c_user)
+        o = self.order
+        out = np.zeros(o.size, dtype=np.float32)
+        keep = o >= 0
+        out[keep] = c_user[o[keep]]
+        return out
+
+    def to_user(self, c_plan) -> np.ndarray:
+        """Host plan-layout array (L) -> user order (nnz)."""
+        c_plan = np.asarray(c_plan)
+        o = self.order
+        out = np.empty(self.nnz, dtype=c_plan.dtype)
+        keep = o >= 0
+        out[o[keep]] = c_plan[keep]
+        return out
 
     def close(self):
         if self._h:
@@ -223,10 +246,12 @@ def _mat(t, name):
     return t.data_ptr(), t.stride(0)
 
 
-def _vec(t, name):
+def _vec(t, name, length=None):
     torch = _torch()
     if t.dtype != torch.float32 or not t.is_contiguous() or not t.is_cuda:
         raise ValueError(f"{name} must be a contiguous fp32 device tensor")
+    if length is not None and t.numel() != length:
+        raise ValueError(f"{name} must hold the plan's {length} coefficient slots (Plan.coef_slots)")
     return t.data_ptr()
 
 
@@ -248,8 +273,8 @@ def adapter_fwd(plan: Plan, X, c_vals, scale: float, Y=None, beta: float = 0.0, 
     yp, ldy = _mat(Y, "Y")
     if Y.dtype != X.dtype or Y.shape[0] != T:
         raise ValueError("Y must match X in dtype and token count")
-    _check(_load().ff_adapter_fwd(plan.handle, T, _act_code(X), xp, ldx, _vec(c_vals, "c_vals"), scale, beta,
-                                  yp, ldy, _stream(stream)))
+    _check(_load().ff_adapter_fwd(plan.handle, T, _act_code(X), xp, ldx, _vec(c_vals, "c_vals", plan.coef_slots), scale,
+                                  beta, yp, ldy, _stream(stream)))
     return Y
 
 
@@ -266,13 +291,14 @@ def adapter_bwd(plan: Plan, X, G, c_vals, scale: float, dX=None, dC=None, beta_d
     if want_dc and dC is None:
         if accumulate_dc:
             raise ValueError("accumulate_dc needs an existing dC")
-        dC = torch.empty((plan.nnz,), dtype=torch.float32, device=G.device)
+        dC = torch.empty((plan.coef_slots,), dtype=torch.float32, device=G.device)
     gp, ldg = _mat(G, "G")
     xp, ldx = _mat(X, "X") if X is not None else (None, plan.n)
     dxp, lddx = _mat(dX, "dX") if want_dx else (None, plan.n)
-    dcp = _vec(dC, "dC") if want_dc else None
+    dcp = _vec(dC, "dC", plan.coef_slots) if want_dc else None
     _check(_load().ff_adapter_bwd(plan.handle, T, act, xp, ldx, gp, ldg,
-                                  _vec(c_vals, "c_vals") if c_vals is not None else None, scale, beta_dx,
+                                  _vec(c_vals, "c_vals", plan.coef_slots) if c_vals is not None else None,
+                                  scale, beta_dx,
                                   dxp, lddx, int(accumulate_dc), dcp, _stream(stream)))
     return (dX if want_dx else None), (dC if want_dc else None)
 
@@ -284,7 +310,7 @@ def merge_delta(plan: Plan, c_vals, scale: float, W, beta: float = 1.0, stream=N
     if W.dtype not in (torch.float32, torch.bfloat16) or tuple(W.shape) != (plan.m, plan.n):
         raise ValueError("W must be m x n fp32 or bf16")
     code = FF_BF16 if W.dtype == torch.bfloat16 else FF_F32
-    _check(_load().ff_merge_delta(plan.handle, _vec(c_vals, "c_vals"), scale, code, beta, wp, ldw,
+    _check(_load().ff_merge_delta(plan.handle, _vec(c_vals, "c_vals", plan.coef_slots), scale, code, beta, wp, ldw,
                                   _stream(stream)))
     return W
 

@@ -106,7 +106,7 @@ ff_status ff_adapter_fwd(const ff_plan* p, int64_t T, int act, const void* X, in
   if (T == 0) return FF_OK;
   if ((st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
   if ((st = check_act("Y", Y, ldy, p->fout->d, act)) != FF_OK) return st;
-  if (p->nnz > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
+  if (p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
   return launched(ff::launch_fwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, c_vals, nullptr, scale,
                                  beta, {Y, nullptr}, ldy, (hipStream_t)stream),
                   "forward launch");
@@ -119,7 +119,7 @@ ff_status ff_adapter_bwd(const ff_plan* p, int64_t T, int act, const void* X, in
   ff::clear_error();
   ff_status st = check_common(p, T, act, 1);
   if (st != FF_OK) return st;
-  const bool want_dx = dX != nullptr, want_dc = dC != nullptr && p->nnz > 0;
+  const bool want_dx = dX != nullptr, want_dc = dC != nullptr && p->coef_slots > 0;
   if (dC && ((uintptr_t)dC % 4)) return ff::fail(FF_EINVAL, "dC is not 4-byte aligned");
   if (T == 0) {
     if (!want_dc || accumulate_dc) return FF_OK;       // empty sum: dC = 0 unless accumulating
@@ -128,7 +128,7 @@ ff_status ff_adapter_bwd(const ff_plan* p, int64_t T, int act, const void* X, in
     if ((st = check_act("G", G, ldg, p->fout->d, act)) != FF_OK) return st;
     if (want_dc && (st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
     if (want_dx && (st = check_act("dX", dX, lddx, p->fin->d, act)) != FF_OK) return st;
-    if (want_dx && p->nnz > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
+    if (want_dx && p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
   }
   return launched(ff::launch_bwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, {G, nullptr}, ldg, c_vals,
                                  nullptr, scale, beta_dx, {dX, nullptr}, lddx, want_dx, accumulate_dc, dC,
@@ -145,7 +145,7 @@ ff_status ff_merge_delta(const ff_plan* p, const float* c_vals, float scale, int
   if (!W) return ff::fail(FF_EINVAL, "W is NULL");
   if (ldw < p->fin->d) return ff::fail(FF_EINVAL, "ldw < n");
   if ((uintptr_t)W % (w_dtype == FF_BF16 ? 2 : 4)) return ff::fail(FF_EINVAL, "W is misaligned");
-  if (p->nnz > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
+  if (p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
   return launched(ff::launch_merge(p, c_vals, scale, w_dtype == FF_BF16, beta, W, ldw, (hipStream_t)stream),
                   "merge launch");
 }
@@ -175,13 +175,13 @@ ff_status ff_adapter_bwd_batched(const ff_plan* p, int64_t count, int64_t T, int
   ff::clear_error();
   ff_status st = check_common(p, T, act, count);
   if (st != FF_OK) return st;
-  const bool want_dx = dX != nullptr, want_dc = dC != nullptr && p->nnz > 0;
+  const bool want_dx = dX != nullptr, want_dc = dC != nullptr && p->coef_slots > 0;
   if (T == 0 && (!want_dc || accumulate_dc)) return FF_OK;
   if (T > 0) {
     if (!want_dx && !want_dc) return FF_OK;
     if (!G) return ff::fail(FF_EINVAL, "G pointer array is NULL");
     if (want_dc && !X) return ff::fail(FF_EINVAL, "X pointer array is NULL");
-    if (want_dx && !c_vals && p->nnz > 0) return ff::fail(FF_EINVAL, "c_vals pointer array is NULL");
+    if (want_dx && !c_vals && p->coef_slots > 0) return ff::fail(FF_EINVAL, "c_vals pointer array is NULL");
     const int64_t mult = act == FF_BF16 ? 8 : 4;
     if (ldg < p->fout->d || ldg % mult) return ff::fail(FF_EINVAL, "bad ldg");
     if (want_dc && (ldx < p->fin->d || ldx % mult)) return ff::fail(FF_EINVAL, "bad ldx");

@@ -9,7 +9,7 @@
 #include <cstdint>
 #include <vector>
 
-#include "../../include/frameft.h"
+#include "frameft.h"
 
 namespace ff {
 
@@ -53,24 +53,23 @@ struct PlanDev {
   const int2* bwd_ent;       // (LDS offset of the row in the u tile, user index e)
   int bwd_nslots;
   // dC: per user entry e, (LDS offset of row in u tile, LDS offset of column in z tile).
-  const int2* sdd;
+  const int2* sdd;           // per coefficient slot; (-1, -1) for padding slots
   // merge: entries bucketed by (output block R, input block S), bucket = R*nblk_in + S.
   const int* mrg_ptr;
   const int4* mrg_ent;       // (local row a', local column b', user index e, 0)
   int mrg_max_bucket;
-  int nnz;
+  int nnz;                   // coefficient slots (nnz plus padding)
 };
 
 // Entry streams of the 128-wide fused kernels: per pair of adjacent 128-wide
 // blocks, `len` rows of 64 lane slots starting at stream row `off`.
 struct FastPlanDev {
   int enabled = 0;
-  const int* fwd_off = nullptr;       // v = C z, per output pair
-  const int* fwd_len = nullptr;
-  const uint32_t* fwd_st = nullptr;   // slot words
-  const int2* fwd_ri = nullptr;       // per stream row: (plan index of lane 0, occupied lanes)
-  const int* bwd_off = nullptr;       // dC and q = C^T u, per input pair
-  const int* bwd_len = nullptr;
+  const int2* fwd_pl = nullptr;       // v = C z, per output pair: (first stream row, rows)
+  const uint32_t* fwd_st = nullptr;   // slot words; slot (row r, lane l) is coefficient slot 64 r + l
+  const int* pad = nullptr;           // coefficient slots that hold no entry
+  int npad = 0;
+  const int2* bwd_pl = nullptr;       // dC and q = C^T u, per input pair: (first stream row, rows)
   const uint2* bwd_st = nullptr;      // (slot word, plan index)
   int bwd_slots = 0;                  // 64 * backward stream rows = dC partials per tile
 };
@@ -92,6 +91,7 @@ struct ff_plan {
   ff_frame* fin = nullptr;
   ff_frame* fout = nullptr;
   int64_t nnz = 0, max_tokens = 0, max_batch = 1;
+  int64_t coef_slots = 0;          // length of c_vals / dC arrays: nnz plus padding slots
   int device = 0;
   int ldb_in = 0, ldb_out = 0;     // LDS block strides (elements)
   int ldt_in[2] = {0, 0};          // LDS token strides of the input-side tile, [FF_F32], [FF_BF16]
@@ -99,12 +99,12 @@ struct ff_plan {
   int tile_tokens[2] = {0, 0};     // tokens per fused-kernel tile
   size_t lds_bytes[2] = {0, 0};
   int64_t max_tiles = 0;           // tiles of the largest call, per adapter
-  float* partial = nullptr;        // dC partial sums, [batch][tile][nnz]
+  float* partial = nullptr;        // dC partial sums per tile (layout depends on the kernels)
   size_t workspace_bytes = 0;
   void* dev_mem = nullptr;
   ff::PlanDev dev{};
   ff::FastPlanDev fast{};
-  std::vector<int64_t> user_order;  // user index of each plan-ordered coefficient
+  std::vector<int64_t> user_order;  // user index of each coefficient slot, -1 for padding
 };
 
 namespace ff {
@@ -137,6 +137,8 @@ hipError_t configure_kernels();
 // 128-wide fused path (kernels_w128.hip).
 hipError_t configure_fast128();
 size_t fast128_lds_bytes(int nblk);
+// Floats per tile of the fused backward's dC workspace for a plan with `bwd_slots` slots.
+size_t fast128_partial_floats(size_t bwd_slots);
 hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, const float* c,
                          const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, hipStream_t s);
 hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G, int64_t ldg,
@@ -144,5 +146,13 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
                          int64_t lddx, bool want_dx, int accumulate_dc, float* dC, float* const* dCs, bool want_dc,
                          hipStream_t s);
 constexpr int kFastTileTokens = 8;
+
+// Slot words of the 128-wide kernels' entry streams: the byte offset of the source row in the
+// LDS coefficient array (rows of 16 bytes, unswizzled), the destination row in the pair tile
+// (swizzled, 0..255), end-of-row and valid flags.
+constexpr uint32_t kSlotSrcMask = 0xFFFFFu;        // bits 0..19
+constexpr int kSlotDstShift = 20;                   // bits 20..27
+constexpr uint32_t kSlotEnd = 1u << 28;
+constexpr uint32_t kSlotValid = 1u << 31;
 
 }  // namespace ff

@@ -17,7 +17,7 @@
 //   bwd_kernel    g -> u = P_out^T g (LDS), x -> z = P_in^T x (LDS)
 //                 -> dC partial per tile: sum_t u[a_e] z[b_e]
 //                 -> q = C^T u (LDS, over z) -> dX = beta dX + s P_in q
-//   dc_reduce     dC[e] = [dC[e] +] s * sum_tiles partial[tile][e]   (fixed order)
+//   dc_reduce     dC[j] = [dC[j] +] s * sum_tiles partial[tile][j]   (fixed order, per coefficient slot)
 //   merge_kernel  W = beta W + s P_out C P_in^T, per (output block, input block)
 //                 tile as a sum of rank-1 products of block columns.
 #include <algorithm>
@@ -234,7 +234,7 @@ struct BwdArgs {
   const int* ptr;
   const int2* ent;
   int nslots;
-  // dC tables and partial sums [batch][tile][nnz]
+  // dC tables and partial sums [batch][tile][coefficient slot]
   const int2* sdd;
   int nnz;
   float* partial;
@@ -268,7 +268,8 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
     for (int e = threadIdx.x; e < a.nnz; e += blockDim.x) {
       const int2 o = a.sdd[e];
       float acc = 0.f;
-      for (int t = 0; t < nt; ++t) acc = fmaf(A::ld(ut + t * a.ldt_out + o.x), A::ld(zt + t * a.ldt_in + o.y), acc);
+      if (o.x >= 0)   // padding slots hold no entry
+        for (int t = 0; t < nt; ++t) acc = fmaf(A::ld(ut + t * a.ldt_out + o.x), A::ld(zt + t * a.ldt_in + o.y), acc);
       part[e] = acc;
     }
     if (!a.want_dx) return;

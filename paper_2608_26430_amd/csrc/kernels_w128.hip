@@ -5,10 +5,16 @@
 // Layout.  A workgroup owns a tile of 8 tokens.  The coefficients of one side
 // (z = P_in^T x forward, u = P_out^T g backward) live in LDS coefficient-major:
 // row c holds the 8 tokens' bf16 values (16 bytes), so every sparse access of
-// C's random support is one 16-byte LDS read covering the whole tile.  Rows are
-// XOR-swizzled inside each 128-row block so that the MFMA-side reads and writes
-// (8 consecutive coefficients of one token, four tokens' lanes per row) hit
-// distinct banks.
+// C's random support is one 16-byte LDS read covering the whole tile.  The
+// analysis that fills these arrays runs the MFMA with its operands swapped, so
+// that each lane ends up with four tokens of one coefficient and writes them
+// with a single 8-byte store.  The per-wave pair tiles, which the synthesis
+// reads as MFMA operands (8 consecutive coefficients of one token), are
+// XOR-swizzled inside each 128-row block so that those reads hit distinct
+// banks.  In a partial tile (fewer than 8 tokens left) the missing
+// token columns repeat the last token: every result they produce equals that
+// token's and is written to that token's row, so no store needs a lane mask;
+// only the dC products mask them out.
 //
 // Frame products.  Only the upper half of the block B (synthesis) is held in
 // registers (64 VGPRs per wave, staged once per workgroup through LDS): the
@@ -24,14 +30,29 @@
 // Sparse products.  After the shared coefficient array is complete, each wave
 // streams over its own block pairs with a private 4 KB LDS tile.  The plan's
 // entry streams are load-balanced and lane-interleaved (a lane owns whole rows
-// of C for v = C z, whole columns for q = C^T u), and the coefficient vector is
-// in the plan's order, which is the forward stream's order: forward slots read
-// their coefficients with coalesced loads that do not wait for the entries.
-// The next pair's stream chunk is loaded while the current pair is synthesised.
-// The backward runs one stream per input pair twice: first for this tile's
-// share of dC_e = sum_t u_t[a_e] z_t[b_e] (v_dot2_f32_bf16 over token pairs),
-// then for q = C^T u; partial dC sums go to a workspace reduced in a fixed
-// order by a second kernel.
+// of C for v = C z, whole columns for q = C^T u), every stream has at least one
+// row, and the coefficient vector is laid out like the forward stream (slot
+// (row r, lane l) is coefficient 64 r + l), so forward slots read their
+// coefficients with coalesced loads that do not wait for the entries.  A
+// chunk's LDS reads are all issued before its sums and its row writes, so one
+// LDS latency is paid per chunk rather than per slot.  The sparse products
+// multiply bf16 values by the coefficient rounded to bf16 with
+// v_dot2_f32_bf16 against (c, 0) and (0, c), which takes each token straight
+// from its packed pair, and accumulate in fp32.  The backward runs one
+// stream per input pair twice: first for this tile's share of
+// dC_e = sum_t u_t[a_e] z_t[b_e] (v_dot2_f32_bf16 over token pairs), then for
+// q = C^T u; partial dC sums go to a workspace reduced in a fixed order by a
+// second kernel.
+//
+// Memory-latency discipline.  The vector memory counter is in order and counts
+// stores as well as loads, so waiting for a load also waits for every store
+// issued before it, and a load that only some paths issue forces the compiler
+// into full waits.  Hence: every prefetch is issued on every path (out-of-range
+// pairs are clamped to a valid one and the result discarded), partial-sum
+// stores of slots past a stream's end go to a scratch row instead of being
+// skipped, the rare long-stream paths end with an explicit full wait, the
+// output options are template parameters rather than branches, and the loads a
+// pair needs are issued before the previous pair's stores.
 #include "ff_internal.h"
 
 namespace ff {
@@ -44,15 +65,29 @@ constexpr int kHT = kMT / 2;   // 16-row tiles of the upper half (held in regist
 constexpr int kKT = 4;    // 32-wide contraction steps per block
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kCh = 16;   // stream slots per lane held in registers at once
+constexpr int kCh = 12;   // stream slots per lane held in registers at once
 
-constexpr unsigned kValid = 1u << 25, kEnd = 1u << 24;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned short u16;
+
+// Global-memory views of generic pointers.  Pointers read from device arrays (the batched
+// entry points) carry no address space, and loads through them would be emitted as flat
+// loads, which the compiler must fence with full waits; every global access goes through
+// these casts so that it is a global load or store.
+#define FF_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ const FF_GLOBAL T* gld(const T* p) {
+  return (const FF_GLOBAL T*)p;
+}
+template <typename T>
+__device__ __forceinline__ FF_GLOBAL T* gst(T* p) {
+  return (FF_GLOBAL T*)p;
+}
 
 __device__ __forceinline__ int swz(int blk, int o) { return o ^ ((o >> 2) & 4) ^ ((blk & 1) << 1); }
 
@@ -66,22 +101,41 @@ __device__ __forceinline__ unsigned pack_bf2(float a, float b) {
 
 __device__ __forceinline__ u16 to_bf(float a) { return __builtin_bit_cast(u16, (__bf16)a); }
 
+// s_waitcnt vmcnt(0), other counters untouched: ends a rare path with no vector memory
+// operation of it still in flight.
+__device__ __forceinline__ void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Ordering point between phases that hand data through a wave's private LDS tile:
 // LDS instructions of one wave execute in order, so only the compiler must not move
 // accesses across it.
 __device__ __forceinline__ void wave_lds_fence() { __asm__ volatile("" ::: "memory"); }
 
+// A scheduling barrier: no instruction moves across it.  Placed after each group of
+// prefetch loads, it keeps them where they are written (the scheduler would otherwise move
+// them down next to their use, or hoist the arithmetic that consumes the previous prefetch
+// above the work that was meant to hide its latency).
+__device__ __forceinline__ void issue_point() { __builtin_amdgcn_sched_barrier(0); }
+
 struct Frag {
   bf16x8 f[kHT][kKT];
 };
 
-// Stage the 16 KB of upper-half synthesis fragments through LDS (once per workgroup) and load
-// this wave's copy.  `stage` must be free LDS of that size; it may be reused after return.
-// The fragment array is ordered [row tile][contraction step][lane], so the upper half is its
-// first half.
-__device__ __forceinline__ void load_frag(const void* fs16, u32x4* stage, int lane, Frag& F) {
-  const u32x4* src = reinterpret_cast<const u32x4*>(fs16);
-  for (int i = threadIdx.x; i < kHT * kKT * 64; i += kThreads) stage[i] = src[i];
+// The 16 KB of upper-half synthesis fragments are fetched by the whole workgroup (4 x 16 B
+// per thread, issued before anything else the kernel loads), staged through LDS and read back
+// by every wave.  The fragment array is ordered [row tile][contraction step][lane], so the
+// upper half is its first half.
+constexpr int kFragPerThread = kHT * kKT * 64 / kThreads;
+
+__device__ __forceinline__ void frag_fetch(const void* fs16, u32x4 (&r)[kFragPerThread]) {
+  const FF_GLOBAL u32x4* src = gld(reinterpret_cast<const u32x4*>(fs16));
+#pragma unroll
+  for (int j = 0; j < kFragPerThread; ++j) r[j] = src[threadIdx.x + j * kThreads];
+}
+
+// `stage` must be free LDS of 16 KB; it may be reused after return.
+__device__ __forceinline__ void frag_stage(const u32x4 (&r)[kFragPerThread], u32x4* stage, int lane, Frag& F) {
+#pragma unroll
+  for (int j = 0; j < kFragPerThread; ++j) stage[threadIdx.x + j * kThreads] = r[j];
   __syncthreads();
 #pragma unroll
   for (int mt = 0; mt < kHT; ++mt)
@@ -90,20 +144,17 @@ __device__ __forceinline__ void load_frag(const void* fs16, u32x4* stage, int la
   __syncthreads();
 }
 
-// acc[mt] = sum_ks B[mt][ks] * b[ks] for the 8 row tiles of the block; rows 64..127 use the
-// upper-half fragments on the input with its odd complex components negated.  With flip
-// (analysis) odd real inputs are negated first.  A lane's 8 inputs of a contraction step are
-// real indices 32 ks + 8 q + j: odd j is the high half of each word, odd complex index is
-// words 1 and 3.
-__device__ __forceinline__ void mfma_block(const Frag& F, const u32x4 (&b)[kKT], f32x4 (&acc)[kMT], bool flip) {
-  const unsigned d = flip ? 0x80000000u : 0u;
-  const u32x4 m_top = {d, d, d, d};
-  const u32x4 m_bot = {d, d ^ 0x80008000u, d, d ^ 0x80008000u};
+// Synthesis: acc[mt] = sum_ks B[mt][ks] * b[ks] for the 8 row tiles of the block; rows
+// 64..127 use the upper-half fragments on the input with its odd complex components negated.
+// A lane's 8 inputs of a contraction step are real indices 32 ks + 8 q + j: odd j is the high
+// half of each word, odd complex index is words 1 and 3.
+__device__ __forceinline__ void mfma_block(const Frag& F, const u32x4 (&b)[kKT], f32x4 (&acc)[kMT]) {
+  const u32x4 m_bot = {0u, 0x80008000u, 0u, 0x80008000u};
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ks = 0; ks < kKT; ++ks) {
-    const bf16x8 bt = __builtin_bit_cast(bf16x8, b[ks] ^ m_top);
+    const bf16x8 bt = __builtin_bit_cast(bf16x8, b[ks]);
     const bf16x8 bb = __builtin_bit_cast(bf16x8, b[ks] ^ m_bot);
 #pragma unroll
     for (int mt = 0; mt < kHT; ++mt) {
@@ -113,35 +164,51 @@ __device__ __forceinline__ void mfma_block(const Frag& F, const u32x4 (&b)[kKT],
   }
 }
 
-// Activation fragments of one column group: lane (token t, block bs of the pair, quarter q)
-// reads 8 consecutive inputs per contraction step from a row-major token matrix.  The loads
-// are unconditional (tokens past the tile's end re-read its last token) and nothing touches
-// the registers until mfma_block, so they stay in flight; store_coef zeroes those columns and
-// store_act skips them.
-__device__ __forceinline__ void load_act(const u16* rows, long ld, int nt, int blk0, int lane, u32x4 (&b)[kKT]) {
-  const int n = lane & 15, t = min(n & 7, nt - 1), bs = n >> 3, q = lane >> 4;
-  const u16* p = rows + (long)t * ld + (blk0 + bs) * kW + 8 * q;
+// Analysis with the operands swapped: D^T = X^T B^T, so lane (q, n) ends up holding
+// coefficient 16 mt + n (mt < 4: upper half of the block, mt >= 4: lower half) of block
+// (q >> 1) of the pair for tokens 4 (q & 1) .. 4 (q & 1) + 3.  Odd real inputs are negated
+// (B^T = D B D); `km` zeroes the activation columns of tokens past the tile's end where they
+// must not contribute.
+__device__ __forceinline__ void mfma_block_t(const Frag& F, const u32x4 (&b)[kKT], f32x4 (&acc)[kMT], unsigned km) {
+  const unsigned d = 0x80000000u;
+  const u32x4 m_top = {d, d, d, d};
+  const u32x4 m_bot = {d, d ^ 0x80008000u, d, d ^ 0x80008000u};
 #pragma unroll
-  for (int ks = 0; ks < kKT; ++ks) b[ks] = *reinterpret_cast<const u32x4*>(p + 32 * ks);
+  for (int mt = 0; mt < kMT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < kKT; ++ks) {
+    const u32x4 bk = b[ks] & km;
+    const bf16x8 bt = __builtin_bit_cast(bf16x8, bk ^ m_top);
+    const bf16x8 bb = __builtin_bit_cast(bf16x8, bk ^ m_bot);
+#pragma unroll
+    for (int mt = 0; mt < kHT; ++mt) {
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bt, F.f[mt][ks], acc[mt], 0, 0, 0);
+      acc[mt + kHT] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bb, F.f[mt][ks], acc[mt + kHT], 0, 0, 0);
+    }
+  }
 }
 
-// Write an analysis result (odd outputs negated) into a coefficient-major LDS array whose
-// block `blk0 + bs` starts at row (blk0 + bs - row_blk0) * 128.  Columns of tokens past the
-// tile's end are written as zeros.
-__device__ __forceinline__ void store_coef(u16* lds, int blk0, int row_blk0, int nt, int lane,
-                                           const f32x4 (&acc)[kMT]) {
-  const int n = lane & 15, t = n & 7, bs = n >> 3, q = lane >> 4;
-  const int blk = blk0 + bs;
-  const float keep = t < nt ? 1.f : 0.f;
-  u16* base = lds + (long)(blk - row_blk0) * kW * kTT + t;
+// Store the result of mfma_block_t into a coefficient-major LDS array (odd coefficients
+// negated: sgn = 0x80008000 on lanes with odd n), one 8-byte write per row tile.  `row_even` /
+// `row_odd` are this lane's byte offsets for even / odd row tiles (equal unless the array is
+// swizzled); row tile mt adds 256 mt bytes.
+__device__ __forceinline__ void store_coef_t(unsigned char* lds, unsigned row_even, unsigned row_odd,
+                                             const f32x4 (&acc)[kMT], unsigned sgn) {
 #pragma unroll
-  for (int mt = 0; mt < kMT; ++mt)
+  for (int mt = 0; mt < kMT; ++mt) {
+    const unsigned w0 = pack_bf2(acc[mt][0], acc[mt][1]) ^ sgn, w1 = pack_bf2(acc[mt][2], acc[mt][3]) ^ sgn;
+    *reinterpret_cast<u32x2*>(lds + ((mt & 1) ? row_odd : row_even) + 256 * mt) = u32x2{w0, w1};
+  }
+}
+
+// Activation fragments of one column group: lane (token t, block bs of the pair, quarter q)
+// reads 8 consecutive inputs per contraction step from a row-major token matrix.  Token
+// columns past the tile's end read its last token.
+__device__ __forceinline__ void load_act(const u16* rows, long ld, int nt, int blk0, int lane, u32x4 (&b)[kKT]) {
+  const int n = lane & 15, t = min(n & 7, nt - 1), bs = n >> 3, q = lane >> 4;
+  const FF_GLOBAL u32x4* p = gld(reinterpret_cast<const u32x4*>(rows + (long)t * ld + (blk0 + bs) * kW + 8 * q));
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int o = 16 * mt + 4 * q + j;
-      const float v = (j & 1) ? -keep * acc[mt][j] : keep * acc[mt][j];
-      base[swz(blk, o) * kTT] = to_bf(v);
-    }
+  for (int ks = 0; ks < kKT; ++ks) b[ks] = p[4 * ks];
 }
 
 // Gather the synthesis operand of the pair tile (rows bs*128 + swz(bs, o), 8 tokens per row).
@@ -161,28 +228,32 @@ __device__ __forceinline__ void load_tile_act(const u16* tile, int lane, u32x4 (
   }
 }
 
-// y[t][(blk0+bs)*128 + o] = scale * acc (+ beta * y)
+// y[t][(blk0+bs)*128 + o] = scale * acc (+ beta * y).  Token columns past the tile's end hold
+// the last token's values and write them to its row again.
+template <bool BETA>
 __device__ __forceinline__ void store_act(u16* rows, long ld, int nt, int blk0, int lane, const f32x4 (&acc)[kMT],
                                           float scale, float beta) {
-  const int n = lane & 15, t = n & 7, bs = n >> 3, q = lane >> 4;
-  if (t >= nt) return;
-  u16* p = rows + (long)t * ld + (blk0 + bs) * kW + 4 * q;
+  const int n = lane & 15, t = min(n & 7, nt - 1), bs = n >> 3, q = lane >> 4;
+  FF_GLOBAL u32x2* p = gst(reinterpret_cast<u32x2*>(rows + (long)t * ld + (blk0 + bs) * kW + 4 * q));
+  u32x2 old[kMT];
+  if (BETA) {
+#pragma unroll
+    for (int mt = 0; mt < kMT; ++mt) old[mt] = p[4 * mt];
+  }
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt) {
     f32x4 r = acc[mt] * scale;
-    uint2* dst = reinterpret_cast<uint2*>(p + 16 * mt);
-    if (beta != 0.f) {
-      const uint2 old = *dst;
-      r[0] += beta * lo_bf(old.x);
-      r[1] += beta * hi_bf(old.x);
-      r[2] += beta * lo_bf(old.y);
-      r[3] += beta * hi_bf(old.y);
+    if (BETA) {
+      r[0] += beta * lo_bf(old[mt].x);
+      r[1] += beta * hi_bf(old[mt].x);
+      r[2] += beta * lo_bf(old[mt].y);
+      r[3] += beta * hi_bf(old[mt].y);
     }
-    *dst = make_uint2(pack_bf2(r[0], r[1]), pack_bf2(r[2], r[3]));
+    p[4 * mt] = u32x2{pack_bf2(r[0], r[1]), pack_bf2(r[2], r[3])};
   }
 }
 
-__device__ __forceinline__ void zero_tile(u16* tile, int lane) {
+__device__ __forceinline__ void zero_tile(unsigned char* tile, int lane) {
   u32x4* tz = reinterpret_cast<u32x4*>(tile);
   wave_lds_fence();
 #pragma unroll
@@ -190,17 +261,37 @@ __device__ __forceinline__ void zero_tile(u16* tile, int lane) {
   wave_lds_fence();
 }
 
-// a[0..7] += c * (8 bf16 tokens of source row); at the end of a row, write it to the tile.
-__device__ __forceinline__ void accum_row(unsigned e, float c, const u16* src, u16* tile, float (&a)[8]) {
-  const u32x4 zv = *reinterpret_cast<const u32x4*>(src + (e & 0xffffu) * kTT);
+__device__ __forceinline__ u32x4 lds_at(const unsigned char* base, unsigned byte_off) {
+  return *reinterpret_cast<const u32x4*>(base + byte_off);
+}
+
+__device__ __forceinline__ unsigned tile_off(unsigned e) { return ((e >> kSlotDstShift) & 0xffu) * 16u; }
+
+// The coefficient of a slot as the two multiplier words of v_dot2_f32_bf16, (c, 0) and (0, c),
+// both zero for a slot that holds no entry (the valid flag is the sign bit of the slot word).
+__device__ __forceinline__ void coef_words(unsigned e, float c, unsigned& ce, unsigned& co) {
+  ce = pack_bf2(c, 0.f) & (unsigned)((int)e >> 31);
+  co = ce << 16;
+}
+
+__device__ __forceinline__ float dot2(unsigned a, unsigned b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
+}
+
+// a[t] += c z[t] for the 8 tokens of one source row; at the end of a row of the product, write
+// it to the tile row named by the slot word and restart.
+__device__ __forceinline__ void accum_row(unsigned e, unsigned ce, unsigned co, const u32x4 zv, unsigned char* tile,
+                                          float (&a)[8]) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
+    // copy the element out first: bit-casting a vector element expression directly reads
+    // element 0 with this compiler
     const unsigned w = zv[j];
-    a[2 * j] = fmaf(c, lo_bf(w), a[2 * j]);
-    a[2 * j + 1] = fmaf(c, hi_bf(w), a[2 * j + 1]);
+    a[2 * j] = dot2(w, ce, a[2 * j]);
+    a[2 * j + 1] = dot2(w, co, a[2 * j + 1]);
   }
-  if (e & kEnd) {
-    reinterpret_cast<u32x4*>(tile)[(e >> 16) & 0xffu] =
+  if (e & kSlotEnd) {
+    *reinterpret_cast<u32x4*>(tile + tile_off(e)) =
         u32x4{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(a[4], a[5]), pack_bf2(a[6], a[7])};
 #pragma unroll
     for (int j = 0; j < 8; ++j) a[j] = 0.f;
@@ -214,78 +305,105 @@ struct FwdChunk {
   float cc[kCh];
 };
 
-// Load slots k0 .. k0+kCh-1 of a forward stream: entries and their coefficients, which sit at
-// plan index rowinfo.x + lane; loads are clamped to real rows/lanes and masked when used.
-__device__ __forceinline__ void fwd_load(const unsigned* __restrict__ st, const int2* __restrict__ ri, int off,
-                                         int len, int k0, const float* __restrict__ cv, int lane, FwdChunk& ch) {
+// Load slots k0 .. k0+kCh-1 of a forward stream (its rows start at `off`, len >= 1): slot words
+// and their coefficients.  Rows past the stream's end re-read its last row and are dropped in
+// fwd_compute.
+__device__ __forceinline__ void fwd_load(const unsigned* __restrict__ st, int off, int len, int k0,
+                                         const float* __restrict__ cv, int lane, FwdChunk& ch) {
 #pragma unroll
   for (int i = 0; i < kCh; ++i) {
-    const int r = off + min(k0 + i, len - 1);
-    const int2 info = ri[r];
-    ch.en[i] = st[(long)r * 64 + lane];
-    ch.cc[i] = cv[info.x + min(lane, info.y - 1)];
+    const long slot = (long)(off + min(k0 + i, len - 1)) * 64 + lane;
+    ch.en[i] = gld(st)[slot];
+    ch.cc[i] = gld(cv)[slot];
   }
 }
 
-__device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int len, int k0, const u16* zL, u16* tile,
+// The first n (1 <= n <= kCh, uniform) slots of a loaded chunk; all kCh LDS rows are read first.
+__device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int n, const unsigned char* zL, unsigned char* tile,
                                             float (&a)[8]) {
+  u32x4 zv[kCh];
+#pragma unroll
+  for (int i = 0; i < kCh; ++i) zv[i] = lds_at(zL, ch.en[i] & kSlotSrcMask);
 #pragma unroll
   for (int i = 0; i < kCh; ++i) {
-    if (k0 + i < len) {   // uniform
-      const unsigned e = ch.en[i];
-      accum_row(e, (e & kValid) ? ch.cc[i] : 0.f, zL, tile, a);
+    if (i < n) {   // uniform
+      unsigned ce, co;
+      coef_words(ch.en[i], ch.cc[i], ce, co);
+      accum_row(ch.en[i], ce, co, zv[i], tile, a);
     }
   }
 }
 
 // ---------------------------------------------------------------- backward stream chunks
 
-struct BwdChunk {
-  uint2 en[kCh];
-  float cc[kCh];
+struct BwdEntries {
+  u32x2 en[kCh];   // (slot word, coefficient slot)
 };
 
+// Rows past the stream's end (len >= 1) re-read its last row; bwd_word drops them.
 __device__ __forceinline__ void bwd_load_entries(const uint2* __restrict__ st, int len, int k0, int lane,
-                                                 BwdChunk& ch) {
+                                                 BwdEntries& ch) {
 #pragma unroll
-  for (int i = 0; i < kCh; ++i) ch.en[i] = st[(long)min(k0 + i, len - 1) * 64 + lane];
+  for (int i = 0; i < kCh; ++i)
+    ch.en[i] = gld(reinterpret_cast<const u32x2*>(st))[(long)min(k0 + i, len - 1) * 64 + lane];
 }
 
-// Coefficients of the loaded entries (empty slots read entry 0 and are masked when used).
-__device__ __forceinline__ void bwd_load_coeffs(const float* __restrict__ cv, BwdChunk& ch) {
+// Coefficients of the loaded entries (padding slots read a coefficient that is masked at use).
+__device__ __forceinline__ void bwd_load_coeffs(const float* __restrict__ cv, const BwdEntries& ch,
+                                                float (&cc)[kCh]) {
 #pragma unroll
-  for (int i = 0; i < kCh; ++i) ch.cc[i] = cv[ch.en[i].y];
+  for (int i = 0; i < kCh; ++i) cc[i] = gld(cv)[ch.en[i].y];
 }
 
-// This tile's share of dC / s for the chunk's slots, written to part (one float per slot).
-__device__ __forceinline__ void bwd_sddmm(const BwdChunk& ch, int len, int k0, const u16* uL, const u16* tile,
-                                          float* __restrict__ part, int lane) {
+// This tile's share of dC / s for the first n (uniform) slots of a chunk, written to part (one
+// float per slot of this pair's stream, k0 = the chunk's first stream row; slots past the
+// stream's end write to the scratch row `trash`), in batches of kSb slots to bound the
+// registers held by LDS reads.
+constexpr int kSb = 4;
+__device__ __forceinline__ void bwd_sddmm(const BwdEntries& ch, int n, int k0, const unsigned char* uL,
+                                          const unsigned char* tile, float* __restrict__ part,
+                                          float* __restrict__ trash, int lane) {
 #pragma unroll
-  for (int i = 0; i < kCh; ++i) {
-    if (k0 + i < len) {   // uniform
-      const unsigned e = ch.en[i].x;
-      const u32x4 uv = *reinterpret_cast<const u32x4*>(uL + (e & 0xffffu) * kTT);
-      const u32x4 zv = *reinterpret_cast<const u32x4*>(tile + ((e >> 16) & 0xffu) * kTT);
+  for (int h = 0; h < kCh / kSb; ++h) {
+    u32x4 uv[kSb], zv[kSb];
+#pragma unroll
+    for (int i = 0; i < kSb; ++i) {
+      const unsigned e = ch.en[h * kSb + i].x;
+      uv[i] = lds_at(uL, e & kSlotSrcMask);
+      zv[i] = lds_at(tile, tile_off(e));
+    }
+#pragma unroll
+    for (int i = 0; i < kSb; ++i) {
+      const int k = h * kSb + i;
+      const unsigned e = ch.en[k].x;
       float s = 0.f;
-  #pragma unroll
+#pragma unroll
       for (int j = 0; j < 4; ++j) {
-        // copy the elements out first: bit-casting a vector element expression directly reads
-        // element 0 with this compiler
-        const unsigned uw = uv[j], zw = zv[j];
-        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, uw), __builtin_bit_cast(bf16x2, zw), s, false);
+        const unsigned uw = uv[i][j], zw = zv[i][j];
+        s = dot2(uw, zw, s);
       }
-      part[(long)(k0 + i) * 64 + lane] = (e & kValid) ? s : 0.f;
+      float* dst = k < n ? part + (long)(k0 + k) * 64 + lane : trash + lane;
+      *gst(dst) = (int)e < 0 ? s : 0.f;
     }
   }
 }
 
-__device__ __forceinline__ void bwd_spmm(const BwdChunk& ch, int len, int k0, const u16* uL, u16* tile,
-                                         float (&a)[8]) {
+__device__ __forceinline__ void bwd_spmm(const BwdEntries& ch, const float (&cc)[kCh], int n, const unsigned char* uL,
+                                         unsigned char* tile, float (&a)[8]) {
+  constexpr int kH = kCh / 2;
 #pragma unroll
-  for (int i = 0; i < kCh; ++i) {
-    if (k0 + i < len) {   // uniform
-      const unsigned e = ch.en[i].x;
-      accum_row(e, (e & kValid) ? ch.cc[i] : 0.f, uL, tile, a);
+  for (int h = 0; h < 2; ++h) {
+    u32x4 uv[kH];
+#pragma unroll
+    for (int i = 0; i < kH; ++i) uv[i] = lds_at(uL, ch.en[h * kH + i].x & kSlotSrcMask);
+#pragma unroll
+    for (int i = 0; i < kH; ++i) {
+      if (h * kH + i < n) {   // uniform
+        const unsigned e = ch.en[h * kH + i].x;
+        unsigned ce, co;
+        coef_words(e, cc[h * kH + i], ce, co);
+        accum_row(e, ce, co, uv[i], tile, a);
+      }
     }
   }
 }
@@ -305,194 +423,286 @@ struct FastArgs {
   const float* c;
   const float* const* cs;
   float scale, beta;
-  int want_dx, want_dc;
-  const int* off;     // per pair: first stream row
-  const int* len;     // per pair: stream rows
-  const unsigned* fst;
-  const int2* fri;
-  const uint2* bst;
   int slots;          // dC partials per tile
-  float* partial;     // [batch][tile][slots]
+  int pstride;        // floats per tile in the partial workspace: slots + one scratch row
+  float* partial;     // [batch][tile][pstride]
   long ntiles;
 };
 
 // Analysis of every pair of blocks of a tile into a coefficient-major LDS array, two pairs'
-// inputs in flight per wave.
+// inputs in flight per wave.  Every load is issued and consumed on every path (a pair index
+// past the end is clamped to the last pair and only its LDS store is skipped), so the compiler
+// neither sinks a prefetch to its use nor falls back to full waits.
 __device__ __forceinline__ void analysis_phase(const Frag& F, const u16* rows, long ld, int nt, int np, int wave,
-                                               int lane, u16* lds) {
+                                               int lane, unsigned char* lds) {
+  const int last = np - 1;
+  const int n = lane & 15, q = lane >> 4;
+  const unsigned off = ((q >> 1) * kW + n) * 16 + 8 * (q & 1);   // this lane's row of pair 0
+  const unsigned sgn = (n & 1) ? 0x80008000u : 0u;               // odd coefficients negated
+  constexpr unsigned kPairBytes = 2 * kW * kTT * 2;
   u32x4 bA[kKT], bB[kKT];
-  if (wave < np) load_act(rows, ld, nt, 2 * wave, lane, bA);
-  if (wave + kWaves < np) load_act(rows, ld, nt, 2 * (wave + kWaves), lane, bB);
+  load_act(rows, ld, nt, 2 * min(wave, last), lane, bA);
+  issue_point();
+  load_act(rows, ld, nt, 2 * min(wave + kWaves, last), lane, bB);
+  issue_point();
   for (int p = wave; p < np; p += 2 * kWaves) {
     {
       f32x4 acc[kMT];
-      mfma_block(F, bA, acc, true);
-      store_coef(lds, 2 * p, 0, nt, lane, acc);
+      mfma_block_t(F, bA, acc, ~0u);
+      store_coef_t(lds + p * kPairBytes, off, off, acc, sgn);
     }
-    if (p + 2 * kWaves < np) load_act(rows, ld, nt, 2 * (p + 2 * kWaves), lane, bA);
-    if (p + kWaves < np) {
+    load_act(rows, ld, nt, 2 * min(p + 2 * kWaves, last), lane, bA);
+    issue_point();
+    {
       f32x4 acc[kMT];
-      mfma_block(F, bB, acc, true);
-      store_coef(lds, 2 * (p + kWaves), 0, nt, lane, acc);
-      if (p + 3 * kWaves < np) load_act(rows, ld, nt, 2 * (p + 3 * kWaves), lane, bB);
+      mfma_block_t(F, bB, acc, ~0u);
+      if (p + kWaves < np) store_coef_t(lds + (p + kWaves) * kPairBytes, off, off, acc, sgn);
     }
+    load_act(rows, ld, nt, 2 * min(p + 3 * kWaves, last), lane, bB);
+    issue_point();
   }
 }
 
-__global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a) {
+// The stream tables are separate restrict-qualified arguments: the kernel never writes them,
+// so their wave-uniform reads become scalar loads, which do not wait for vector stores.
+template <bool BETA>
+__global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int2* __restrict__ pl,
+                                                      const unsigned* __restrict__ fst) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  u16* zL = reinterpret_cast<u16*>(smem);                          // n rows x 8 tokens
+  unsigned char* zL = smem;                                        // n rows x 8 tokens x 2 bytes
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  u16* tile = zL + (long)a.nblk_in * kW * kTT + wave * (2 * kW * kTT);
+  unsigned char* tile = zL + (long)a.nblk_in * kW * kTT * 2 + wave * (2 * kW * kTT * 2);
   const int bi = blockIdx.y;
   const int t0 = blockIdx.x * kTT, nt = min(kTT, a.T - t0);
   const u16* X = reinterpret_cast<const u16*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx;
   u16* Y = reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy;
   const float* cv = a.cs ? a.cs[bi] : a.c;
-  const int npo = a.nblk_out / 2;
+  const int npo = a.nblk_out / 2, lastp = npo - 1;
 
+  u32x4 fr[kFragPerThread];
+  frag_fetch(a.frag, fr);
+  issue_point();
   // first stream chunk of this wave's first output pair, in flight during the analysis
+  int2 q = pl[min(wave, lastp)];
   FwdChunk ch;
-  if (wave < npo && a.len[wave] > 0) fwd_load(a.fst, a.fri, a.off[wave], a.len[wave], 0, cv, lane, ch);
+  fwd_load(fst, q.x, q.y, 0, cv, lane, ch);
+  issue_point();
 
   Frag F;
-  load_frag(a.frag, reinterpret_cast<u32x4*>(smem), lane, F);
+  frag_stage(fr, reinterpret_cast<u32x4*>(smem), lane, F);
   analysis_phase(F, X, a.ldx, nt, a.nblk_in / 2, wave, lane, zL);
   __syncthreads();
 
-  for (int p = wave; p < npo; p += kWaves) {
+  // One output pair: its chunk is in `cur`; the next pair's chunk is loaded into `nxt` first,
+  // a whole pair ahead of its use.  The loop runs two pairs per iteration with the buffers'
+  // roles swapped, so no chunk is ever copied between registers.
+  auto pair = [&](int p, FwdChunk& cur, FwdChunk& nxt) {
+    const int2 qn = pl[min(p + kWaves, lastp)];
+    fwd_load(fst, qn.x, qn.y, 0, cv, lane, nxt);
+    issue_point();
     // v = C z for this pair into the tile
-    const int off = a.off[p], len = a.len[p];
+    const int off = q.x, len = q.y;
     zero_tile(tile, lane);
     float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < len; k0 += kCh) {
-      if (k0 > 0) fwd_load(a.fst, a.fri, off, len, k0, cv, lane, ch);
-      fwd_compute(ch, len, k0, zL, tile, acc8);
+    fwd_compute(cur, min(kCh, len), zL, tile, acc8);
+    if (len > kCh) {   // long stream
+      for (int k0 = kCh; k0 < len; k0 += kCh) {
+        fwd_load(fst, off, len, k0, cv, lane, cur);
+        fwd_compute(cur, min(kCh, len - k0), zL, tile, acc8);
+      }
+      vm_wait_all();
     }
     wave_lds_fence();
-    // next pair's first chunk flies during this pair's synthesis
-    const int pn = p + kWaves;
-    if (pn < npo && a.len[pn] > 0) fwd_load(a.fst, a.fri, a.off[pn], a.len[pn], 0, cv, lane, ch);
     // y = beta y + s P_out v
     u32x4 b[kKT];
     f32x4 acc[kMT];
-    load_tile_act(tile, lane, b);
+    load_tile_act(reinterpret_cast<const u16*>(tile), lane, b);
     wave_lds_fence();
-    mfma_block(F, b, acc, false);
-    store_act(Y, a.ldy, nt, 2 * p, lane, acc, a.scale, a.beta);
+    mfma_block(F, b, acc);
+    store_act<BETA>(Y, a.ldy, nt, 2 * p, lane, acc, a.scale, a.beta);
+    q = qn;
+  };
+  FwdChunk ch2;
+  for (int p = wave; p < npo; p += 2 * kWaves) {
+    pair(p, ch, ch2);
+    if (p + kWaves < npo) pair(p + kWaves, ch2, ch);
   }
 }
 
-__global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a) {
+template <bool DX, bool DC, bool BETA>
+__global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __restrict__ pl,
+                                                      const uint2* __restrict__ bst) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  u16* uL = reinterpret_cast<u16*>(smem);                          // m rows x 8 tokens
+  unsigned char* uL = smem;                                        // m rows x 8 tokens x 2 bytes
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  u16* tile = uL + (long)a.nblk_out * kW * kTT + wave * (2 * kW * kTT);
+  unsigned char* tile = uL + (long)a.nblk_out * kW * kTT * 2 + wave * (2 * kW * kTT * 2);
   const int bi = blockIdx.y;
   const int t0 = blockIdx.x * kTT, nt = min(kTT, a.T - t0);
   const u16* G = reinterpret_cast<const u16*>(a.Gs ? a.Gs[bi] : a.G) + (long)t0 * a.ldg;
-  const u16* X = a.want_dc ? reinterpret_cast<const u16*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx : nullptr;
-  u16* dX = a.want_dx ? reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy : nullptr;
-  const float* cv = a.cs ? a.cs[bi] : a.c;
-  float* part = a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.slots;
-  const int npi = a.nblk_in / 2;
+  const u16* X = DC ? reinterpret_cast<const u16*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx : nullptr;
+  u16* dX = DX ? reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy : nullptr;
+  const float* cv = DX ? (a.cs ? a.cs[bi] : a.c) : nullptr;
+  float* part = DC ? a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.pstride : nullptr;
+  float* trash = DC ? part + a.slots : nullptr;
+  // dC sums only over the tile's tokens: activation columns past its end are zeroed
+  const unsigned km = (lane & 7) < nt ? ~0u : 0u;
+  // this lane's rows of the swizzled pair tile for the analysis of x (even / odd row tiles)
+  const int ln = lane & 15, lq = lane >> 4, lbs = lq >> 1;
+  const unsigned zrow_even = (lbs * kW + (ln ^ (2 * lbs))) * 16 + 8 * (lq & 1);
+  const unsigned zrow_odd = (lbs * kW + (ln ^ 4 ^ (2 * lbs))) * 16 + 8 * (lq & 1);
+  const unsigned zsgn = (ln & 1) ? 0x80008000u : 0u;
+  const int npi = a.nblk_in / 2, lastp = npi - 1;
 
+  u32x4 fr[kFragPerThread];
+  frag_fetch(a.frag, fr);
+  issue_point();
   // this wave's first input pair: stream entries and x in flight during the analysis of g
-  BwdChunk ch;
+  int2 q = pl[min(wave, lastp)];
+  BwdEntries ch;
+  bwd_load_entries(bst + (long)q.x * 64, q.y, 0, lane, ch);
   u32x4 bx[kKT];
-  if (wave < npi) {
-    if (a.len[wave] > 0) bwd_load_entries(a.bst + (long)a.off[wave] * 64, a.len[wave], 0, lane, ch);
-    if (a.want_dc) load_act(X, a.ldx, nt, 2 * wave, lane, bx);
-  }
+  if (DC) load_act(X, a.ldx, nt, 2 * min(wave, lastp), lane, bx);
+  issue_point();
 
   Frag F;
-  load_frag(a.frag, reinterpret_cast<u32x4*>(smem), lane, F);
+  frag_stage(fr, reinterpret_cast<u32x4*>(smem), lane, F);
   analysis_phase(F, G, a.ldg, nt, a.nblk_out / 2, wave, lane, uL);
   __syncthreads();
 
-  for (int p = wave; p < npi; p += kWaves) {
-    const int len = a.len[p];
-    const uint2* st = a.bst + (long)a.off[p] * 64;
-    if (a.want_dx && len > 0) bwd_load_coeffs(cv, ch);
-    if (a.want_dc) {
-      // z = P_in^T x for this pair, then this tile's share of dC
-      f32x4 acc[kMT];
-      mfma_block(F, bx, acc, true);
-      store_coef(tile, 2 * p, 2 * p, nt, lane, acc);
-      wave_lds_fence();
-      if (p + kWaves < npi) load_act(X, a.ldx, nt, 2 * (p + kWaves), lane, bx);
-      float* pp = part + (long)a.off[p] * 64;
-      for (int k0 = 0; k0 < len; k0 += kCh) {
-        if (k0 > 0) bwd_load_entries(st, len, k0, lane, ch);
-        bwd_sddmm(ch, len, k0, uL, tile, pp, lane);
+  // Two passes over this wave's input pairs, so that each holds few registers: dC, then dX.
+  if (DC) {
+    // one input pair; the next pair's entries are loaded into `nxt` a whole pair ahead of
+    // their use, two pairs per iteration with the buffers' roles swapped
+    auto pair = [&](int p, BwdEntries& ch, BwdEntries& chn) {
+      const int len = q.y;
+      const uint2* st = bst + (long)q.x * 64;
+      const int2 qn = pl[min(p + kWaves, lastp)];
+      bwd_load_entries(bst + (long)qn.x * 64, qn.y, 0, lane, chn);
+      issue_point();
+      // z = P_in^T x for this pair (tile columns past the tile's end zeroed), then this
+      // tile's share of dC
+      {
+        f32x4 acc[kMT];
+        mfma_block_t(F, bx, acc, km);
+        store_coef_t(tile, zrow_even, zrow_odd, acc, zsgn);
       }
       wave_lds_fence();
-      if (a.want_dx && len > kCh) {   // the stream is reread for q
-        bwd_load_entries(st, len, 0, lane, ch);
-        bwd_load_coeffs(cv, ch);
+      load_act(X, a.ldx, nt, 2 * min(p + kWaves, lastp), lane, bx);
+      issue_point();
+      float* pp = part + (long)q.x * 64;
+      bwd_sddmm(ch, min(kCh, len), 0, uL, tile, pp, trash, lane);
+      if (len > kCh) {   // long stream
+        for (int k0 = kCh; k0 < len; k0 += kCh) {
+          BwdEntries ck;
+          bwd_load_entries(st, len, k0, lane, ck);
+          bwd_sddmm(ck, min(kCh, len - k0), k0, uL, tile, pp, trash, lane);
+        }
+        vm_wait_all();
       }
+      wave_lds_fence();
+      q = qn;
+    };
+    BwdEntries ch2;
+    for (int p = wave; p < npi; p += 2 * kWaves) {
+      pair(p, ch, ch2);
+      if (p + kWaves < npi) pair(p + kWaves, ch2, ch);
     }
-    if (a.want_dx) {
+    if (DX) {   // restart at this wave's first pair
+      q = pl[min(wave, lastp)];
+      bwd_load_entries(bst + (long)q.x * 64, q.y, 0, lane, ch);
+    }
+  }
+  if (DX) {
+    float cc[kCh], cc2[kCh];
+    bwd_load_coeffs(cv, ch, cc);
+    // one input pair; the next pair's entries are loaded at its start and their coefficients
+    // before its stores, two pairs per iteration with the buffers' roles swapped
+    auto pair = [&](int p, BwdEntries& ch, float (&cc)[kCh], BwdEntries& chn, float (&ccn)[kCh]) {
+      const int len = q.y;
+      const uint2* st = bst + (long)q.x * 64;
+      const int2 qn = pl[min(p + kWaves, lastp)];
+      bwd_load_entries(bst + (long)qn.x * 64, qn.y, 0, lane, chn);
+      issue_point();
       // q = C^T u for this pair, then dX = beta dX + s P_in q
       zero_tile(tile, lane);
       float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      for (int k0 = 0; k0 < len; k0 += kCh) {
-        if (k0 > 0) {
-          bwd_load_entries(st, len, k0, lane, ch);
-          bwd_load_coeffs(cv, ch);
+      bwd_spmm(ch, cc, min(kCh, len), uL, tile, acc8);
+      if (len > kCh) {   // long stream
+        for (int k0 = kCh; k0 < len; k0 += kCh) {
+          BwdEntries ck;
+          float ckc[kCh];
+          bwd_load_entries(st, len, k0, lane, ck);
+          bwd_load_coeffs(cv, ck, ckc);
+          bwd_spmm(ck, ckc, min(kCh, len - k0), uL, tile, acc8);
         }
-        bwd_spmm(ch, len, k0, uL, tile, acc8);
+        vm_wait_all();
       }
       wave_lds_fence();
-    }
-    const int pn = p + kWaves;
-    if (pn < npi && a.len[pn] > 0) bwd_load_entries(a.bst + (long)a.off[pn] * 64, a.len[pn], 0, lane, ch);
-    if (a.want_dx) {
       u32x4 b[kKT];
       f32x4 acc[kMT];
-      load_tile_act(tile, lane, b);
+      load_tile_act(reinterpret_cast<const u16*>(tile), lane, b);
       wave_lds_fence();
-      mfma_block(F, b, acc, false);
-      store_act(dX, a.ldy, nt, 2 * p, lane, acc, a.scale, a.beta);
+      mfma_block(F, b, acc);
+      bwd_load_coeffs(cv, chn, ccn);   // the next pair's coefficients, before this pair's stores
+      issue_point();
+      store_act<BETA>(dX, a.ldy, nt, 2 * p, lane, acc, a.scale, a.beta);
+      q = qn;
+    };
+    BwdEntries ch2;
+    for (int p = wave; p < npi; p += 2 * kWaves) {
+      pair(p, ch, cc, ch2, cc2);
+      if (p + kWaves < npi) pair(p + kWaves, ch2, cc2, ch, cc);
     }
   }
 }
 
 // dC[j] = [dC[j] +] s * sum_tiles partial[tile][slot] for every valid slot of the backward
-// streams (j = the slot's plan index).  Eight waves split the tiles; their sums are combined
-// in a fixed order.
-__global__ void __launch_bounds__(512) reduce128(const float* __restrict__ partial, long ntiles, int slots,
-                                                 const uint2* __restrict__ bst, float scale, int accumulate,
-                                                 float* dC, float* const* dCs) {
-  __shared__ float red[8][64];
+// streams (j = the slot's coefficient slot).  A workgroup owns 64 backward slots; each of its
+// 16 waves sums 1/16 of the tiles with all loads of a pass in flight, and the 16 sums are
+// combined in a fixed order.  Blocks past the reduction blocks zero the padding slots of dC
+// (overwrite mode only).
+constexpr int kRedWaves = 16;
+constexpr int kRedBatch = 8;
+
+__global__ void __launch_bounds__(64 * kRedWaves) reduce128(const float* __restrict__ partial, long ntiles,
+                                                            int slots, int pstride, const uint2* __restrict__ bst,
+                                                            float scale, int accumulate, float* dC,
+                                                            float* const* dCs, const int* __restrict__ pad,
+                                                            int npad, int nred) {
+  __shared__ float red[kRedWaves][64];
   const int bi = blockIdx.y;
+  float* out = dCs ? dCs[bi] : dC;
+  if ((int)blockIdx.x >= nred) {
+    const int i = ((int)blockIdx.x - nred) * 64 * kRedWaves + (int)threadIdx.x;
+    if (i < npad) gst(out)[gld(pad)[i]] = 0.f;
+    return;
+  }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int slot = blockIdx.x * 64 + lane;
   float s = 0.f;
   if (slot < slots) {
-    const float* p = partial + (long)bi * ntiles * slots + slot;
-    float s1 = 0.f, s2 = 0.f, s3 = 0.f;
-    long t = w;
-    for (; t + 24 < ntiles; t += 32) {
-      s += p[t * slots];
-      s1 += p[(t + 8) * slots];
-      s2 += p[(t + 16) * slots];
-      s3 += p[(t + 24) * slots];
+    const float* p = partial + (long)bi * ntiles * pstride + slot;
+    for (long t0 = w; t0 < ntiles; t0 += (long)kRedWaves * kRedBatch) {
+      float v[kRedBatch];
+#pragma unroll
+      for (int j = 0; j < kRedBatch; ++j) {
+        const long t = t0 + (long)j * kRedWaves;
+        v[j] = t < ntiles ? gld(p)[t * pstride] : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < kRedBatch; ++j) s += v[j];
     }
-    for (; t < ntiles; t += 8) s += p[t * slots];
-    s = (s + s1) + (s2 + s3);
   }
   red[w][lane] = s;
   __syncthreads();
   if (w == 0 && slot < slots) {
     float tot = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) tot += red[i][lane];
-    const uint2 en = bst[slot];
-    if (en.x & kValid) {
-      float* out = dCs ? dCs[bi] : dC;
+    for (int i = 0; i < kRedWaves; ++i) tot += red[i][lane];
+    const u32x2 en = gld(reinterpret_cast<const u32x2*>(bst))[slot];
+    if ((int)en.x < 0) {   // valid slot
       const float v = scale * tot;
-      out[en.y] = accumulate ? out[en.y] + v : v;
+      gst(out)[en.y] = accumulate ? gld(out)[en.y] + v : v;
     }
   }
 }
@@ -501,15 +711,26 @@ void rec(hipEvent_t ev, hipStream_t s) {
   if (ev) (void)hipEventRecord(ev, s);
 }
 
+template <typename K>
+hipError_t allow_lds(K* kernel) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                             kMaxLdsBytes);
+}
+
 }  // namespace
 
 hipError_t configure_fast128() {
   static hipError_t once = [] {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fwd128),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
-    if (e == hipSuccess)
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bwd128), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              kMaxLdsBytes);
+    hipError_t e = hipSuccess;
+    const hipError_t r[] = {allow_lds(&fwd128<false>),
+                            allow_lds(&fwd128<true>),
+                            allow_lds(&bwd128<true, true, false>),
+                            allow_lds(&bwd128<true, true, true>),
+                            allow_lds(&bwd128<true, false, false>),
+                            allow_lds(&bwd128<true, false, true>),
+                            allow_lds(&bwd128<false, true, false>)};
+    for (hipError_t x : r)
+      if (x != hipSuccess) e = x;
     return e;
   }();
   return once;
@@ -522,6 +743,8 @@ size_t fast128_lds_bytes(int nblk) {
   const size_t frag = (size_t)kHT * kKT * 64 * 16;
   return b < frag ? frag : b;
 }
+
+size_t fast128_partial_floats(size_t bwd_slots) { return bwd_slots + 64; }
 
 hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, const float* c,
                          const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, hipStream_t s) {
@@ -540,15 +763,15 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   a.cs = cs;
   a.scale = scale;
   a.beta = beta;
-  a.off = p->fast.fwd_off;
-  a.len = p->fast.fwd_len;
-  a.fst = p->fast.fwd_st;
-  a.fri = p->fast.fwd_ri;
   const dim3 grid((unsigned)((T + kTT - 1) / kTT), (unsigned)count);
+  const size_t lds = fast128_lds_bytes(a.nblk_in);
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
   rec(e0, s);
-  hipLaunchKernelGGL(fwd128, grid, dim3(kThreads), fast128_lds_bytes(a.nblk_in), s, a);
+  if (beta != 0.f)
+    hipLaunchKernelGGL(fwd128<true>, grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st);
+  else
+    hipLaunchKernelGGL(fwd128<false>, grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st);
   rec(e1, s);
   return hipGetLastError();
 }
@@ -575,12 +798,8 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   a.cs = cs;
   a.scale = scale;
   a.beta = beta_dx;
-  a.want_dx = want_dx;
-  a.want_dc = want_dc;
-  a.off = p->fast.bwd_off;
-  a.len = p->fast.bwd_len;
-  a.bst = p->fast.bwd_st;
   a.slots = p->fast.bwd_slots;
+  a.pstride = (int)fast128_partial_floats((size_t)a.slots);
   a.partial = p->partial;
   const long ntiles = (T + kTT - 1) / kTT;
   a.ntiles = ntiles;
@@ -588,16 +807,34 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   take_timing_events(&e0, &e1);
   if (T > 0 && (want_dx || want_dc)) {
     const dim3 grid((unsigned)ntiles, (unsigned)count);
+    const size_t lds = fast128_lds_bytes(a.nblk_out);
+    const int2* pl = p->fast.bwd_pl;
+    const uint2* st = p->fast.bwd_st;
+    const bool beta = beta_dx != 0.f;
     rec(e0, s);
-    hipLaunchKernelGGL(bwd128, grid, dim3(kThreads), fast128_lds_bytes(a.nblk_out), s, a);
+    if (want_dx && want_dc && beta)
+      hipLaunchKernelGGL((bwd128<true, true, true>), grid, dim3(kThreads), lds, s, a, pl, st);
+    else if (want_dx && want_dc)
+      hipLaunchKernelGGL((bwd128<true, true, false>), grid, dim3(kThreads), lds, s, a, pl, st);
+    else if (want_dx && beta)
+      hipLaunchKernelGGL((bwd128<true, false, true>), grid, dim3(kThreads), lds, s, a, pl, st);
+    else if (want_dx)
+      hipLaunchKernelGGL((bwd128<true, false, false>), grid, dim3(kThreads), lds, s, a, pl, st);
+    else
+      hipLaunchKernelGGL((bwd128<false, true, false>), grid, dim3(kThreads), lds, s, a, pl, st);
     rec(e1, s);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   if (want_dc) {
-    const dim3 grid((unsigned)((a.slots + 63) / 64), (unsigned)count);
-    hipLaunchKernelGGL(reduce128, grid, dim3(512), 0, s, p->partial, ntiles, a.slots, a.bst, scale, accumulate_dc, dC,
-                       dCs);
+    const int nred = (a.slots + 63) / 64;
+    const int npad = accumulate_dc ? 0 : p->fast.npad;
+    const int nzero = (npad + 64 * kRedWaves - 1) / (64 * kRedWaves);
+    if (nred + nzero > 0) {
+      const dim3 grid((unsigned)(nred + nzero), (unsigned)count);
+      hipLaunchKernelGGL(reduce128, grid, dim3(64 * kRedWaves), 0, s, p->partial, ntiles, a.slots, a.pstride,
+                         p->fast.bwd_st, scale, accumulate_dc, dC, dCs, p->fast.pad, npad, nred);
+    }
   }
   return hipGetLastError();
 }

@@ -35,10 +35,8 @@ int token_stride(int nblk, int ldb, int esz) {
   return base + pad;
 }
 
-// Row swizzle inside a 128-row block of the 128-wide kernels' coefficient arrays.
+// Row swizzle inside a 128-row block of the 128-wide kernels' pair tiles.
 int swz128(int blk, int o) { return o ^ ((o >> 2) & 4) ^ ((blk & 1) << 1); }
-
-constexpr uint32_t kStreamValid = 1u << 25, kStreamEnd = 1u << 24;
 
 // Rows of one pair of blocks assigned whole to 64 lanes, longest first, each to the least
 // loaded lane; lanes are then renumbered by decreasing load, so in every stream row the
@@ -188,23 +186,27 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   }
 
   // ---------------- 128-wide fused path: balanced entry streams per pair of blocks
-  // Forward stream (v = C z), one per pair of output blocks: slot word = source row of z
-  // (16 bits) | destination row of the pair tile (8 bits) | end-of-row | valid.  The plan
-  // order of the coefficients is the order of the valid forward slots (pair, stream row,
-  // lane), so slot (row, lane) reads coefficient rowinfo[row].x + lane.
+  // Forward stream (v = C z), one per pair of output blocks: slot word = byte offset of the
+  // source row of z | destination row of the pair tile | end-of-row | valid.  The plan's
+  // coefficient layout is this stream's slot layout: the coefficient of slot (stream row r,
+  // lane l) is c[64 r + l], so forward slots read coefficients without an index; slots that
+  // hold no entry are padding.
   // Backward stream (dC and q = C^T u), one per pair of input blocks, grouped by column
-  // of C: (source row of u | tile row of the column | end-of-column | valid, plan index).
+  // of C: (byte offset of the source row of u | tile row of the column | end-of-column | valid,
+  // coefficient slot).
   const bool fast = FI.W == 128 && FO.W == 128 && FI.nblk % 2 == 0 && FO.nblk % 2 == 0 &&
                     f_in->transpose_is_sign_flip && f_in->half_shift_sign && f_in->B == f_out->B &&
                     n < 65536 && m < 65536 &&
                     ff::fast128_lds_bytes(std::max(FI.nblk, FO.nblk)) <= (size_t)ff::kMaxLdsBytes;
-  std::vector<int> f_off, f_len, b_off, b_len;
+  std::vector<int2> f_pl, b_pl;   // per pair: (first stream row, stream rows)
+  std::vector<int> pad_slots;
   std::vector<uint32_t> f_st;
-  std::vector<int2> f_ri;
   std::vector<uint2> b_st;
-  std::vector<int> plan_of_user((size_t)nnz), user_of_plan((size_t)nnz);
+  std::vector<int> slot_of_user((size_t)nnz);
+  std::vector<int64_t> user_of_slot;
   if (fast) {
-    auto lrow = [&](const Loc& l) { return (uint32_t)(l.blk * 128 + swz128(l.blk, l.local)); };
+    // byte offset of a coefficient's row in the LDS array of a whole side, and its row in a pair tile
+    auto lsrc = [&](const Loc& l) { return (uint32_t)(l.blk * 128 + l.local) * 16u; };
     auto trow = [&](const Loc& l) { return (uint32_t)((l.blk & 1) * 128 + swz128(l.blk, l.local)); };
     const int npo = FO.nblk / 2, npi = FI.nblk / 2;
     // entries of each destination row r = (block parity)*128 + local of a pair
@@ -214,45 +216,39 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       frows[rloc[e].blk / 2][(rloc[e].blk & 1) * 128 + rloc[e].local].push_back((int)e);
       brows[cloc[e].blk / 2][(cloc[e].blk & 1) * 128 + cloc[e].local].push_back((int)e);
     }
-    int next_plan = 0;
     for (int pp = 0; pp < npo; ++pp) {
       std::vector<int> sz(256);
       for (int r = 0; r < 256; ++r) sz[r] = (int)frows[pp][r].size();
       int len = 0;
       const auto lanes = assign_lanes(sz, len);
-      f_off.push_back((int)f_ri.size());
-      f_len.push_back(len);
-      const size_t base = f_st.size();
-      f_st.resize(base + (size_t)len * 64, 0u);
-      std::vector<std::vector<int>> slot_e(64);         // entries of each lane in slot order
-      for (int l = 0; l < 64; ++l)
+      len = std::max(len, 1);   // every stream has a row, so prefetches never need a guard
+      const size_t row0 = f_st.size() / 64;
+      f_pl.push_back(make_int2((int)row0, len));
+      f_st.resize(f_st.size() + (size_t)len * 64, 0u);
+      user_of_slot.resize(f_st.size(), -1);
+      for (int l = 0; l < 64; ++l) {
+        size_t k = 0;
         for (int r : lanes[l])
-          for (size_t i = 0; i < frows[pp][r].size(); ++i) {
+          for (size_t i = 0; i < frows[pp][r].size(); ++i, ++k) {
             const int e = frows[pp][r][i];
             const bool last = i + 1 == frows[pp][r].size();
             const uint32_t dst = (uint32_t)((r >> 7) * 128 + swz128(r >> 7, r & 127));
-            f_st[base + slot_e[l].size() * 64 + l] =
-                lrow(cloc[e]) | (dst << 16) | kStreamValid | (last ? kStreamEnd : 0u);
-            slot_e[l].push_back(e);
+            const size_t slot = (row0 + k) * 64 + (size_t)l;
+            f_st[slot] = lsrc(cloc[e]) | (dst << ff::kSlotDstShift) | ff::kSlotValid | (last ? ff::kSlotEnd : 0u);
+            user_of_slot[slot] = e;
+            slot_of_user[e] = (int)slot;
           }
-      for (int k = 0; k < len; ++k) {
-        int cnt = 0;
-        while (cnt < 64 && (int)slot_e[cnt].size() > k) ++cnt;
-        f_ri.push_back(make_int2(next_plan, cnt));
-        for (int l = 0; l < cnt; ++l) {
-          user_of_plan[next_plan + l] = slot_e[l][k];
-          plan_of_user[slot_e[l][k]] = next_plan + l;
-        }
-        next_plan += cnt;
       }
     }
+    for (size_t j = 0; j < user_of_slot.size(); ++j)
+      if (user_of_slot[j] < 0) pad_slots.push_back((int)j);
     for (int pp = 0; pp < npi; ++pp) {
       std::vector<int> sz(256);
       for (int r = 0; r < 256; ++r) sz[r] = (int)brows[pp][r].size();
       int len = 0;
       const auto lanes = assign_lanes(sz, len);
-      b_off.push_back((int)(b_st.size() / 64));
-      b_len.push_back(len);
+      len = std::max(len, 1);
+      b_pl.push_back(make_int2((int)(b_st.size() / 64), len));
       const size_t base = b_st.size();
       b_st.resize(base + (size_t)len * 64, make_uint2(0u, 0u));
       for (int l = 0; l < 64; ++l) {
@@ -262,31 +258,36 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
             const int e = brows[pp][r][i];
             const bool last = i + 1 == brows[pp][r].size();
             b_st[base + (size_t)k * 64 + l] = make_uint2(
-                lrow(rloc[e]) | (trow(cloc[e]) << 16) | kStreamValid | (last ? kStreamEnd : 0u),
-                (unsigned)plan_of_user[e]);
+                lsrc(rloc[e]) | (trow(cloc[e]) << ff::kSlotDstShift) | ff::kSlotValid | (last ? ff::kSlotEnd : 0u),
+                (unsigned)slot_of_user[e]);
           }
       }
     }
   } else {
-    std::iota(plan_of_user.begin(), plan_of_user.end(), 0);
-    std::iota(user_of_plan.begin(), user_of_plan.end(), 0);
+    std::iota(slot_of_user.begin(), slot_of_user.end(), 0);
+    user_of_slot.resize((size_t)nnz);
+    std::iota(user_of_slot.begin(), user_of_slot.end(), 0);
   }
-  // the generic kernels index coefficients in plan order too
-  for (auto& en : fwd_ent) en.y = nnz ? plan_of_user[en.y] : 0;
-  for (auto& en : bwd_ent) en.y = nnz ? plan_of_user[en.y] : 0;
-  for (auto& en : mrg_ent) en.z = nnz ? plan_of_user[en.z] : 0;
+  const int64_t nslot = (int64_t)user_of_slot.size();   // coefficient slots (>= nnz)
+  // the generic kernels index coefficients by slot too; padding slots of the dC table are
+  // marked (-1, -1) and produce zeros
+  for (auto& en : fwd_ent) en.y = nnz ? slot_of_user[en.y] : 0;
+  for (auto& en : bwd_ent) en.y = nnz ? slot_of_user[en.y] : 0;
+  for (auto& en : mrg_ent) en.z = nnz ? slot_of_user[en.z] : 0;
   {
-    std::vector<int2> sdd_plan(sdd.size());
-    for (int64_t e = 0; e < nnz; ++e) sdd_plan[plan_of_user[e]] = sdd[e];
-    if (nnz) sdd = sdd_plan;
+    std::vector<int2> sdd_slot((size_t)std::max<int64_t>(nslot, 1), make_int2(-1, -1));
+    for (int64_t e = 0; e < nnz; ++e) sdd_slot[slot_of_user[e]] = sdd[e];
+    sdd = std::move(sdd_slot);
   }
-  p->user_order.assign(user_of_plan.begin(), user_of_plan.end());
+  p->user_order = std::move(user_of_slot);
+  p->coef_slots = nslot;
   const int64_t fast_tiles = fast ? (max_tokens + ff::kFastTileTokens - 1) / ff::kFastTileTokens : 0;
 
   // ---------------- device memory: one allocation for every table and the workspace
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t partial_elems = std::max((size_t)max_batch * (size_t)p->max_tiles * (size_t)nnz,
-                                        (size_t)max_batch * (size_t)fast_tiles * b_st.size());
+  const size_t partial_elems = std::max((size_t)max_batch * (size_t)p->max_tiles * (size_t)nslot,
+                                        (size_t)max_batch * (size_t)fast_tiles *
+                                            (fast ? ff::fast128_partial_floats(b_st.size()) : 0));
   struct Blob {
     const void* src;
     size_t bytes;
@@ -297,9 +298,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       {bwd_ptr.data(), (n + 1) * sizeof(int)},      {bwd_ent.data(), bwd_ent.size() * sizeof(int2)},
       {sdd.data(), sdd.size() * sizeof(int2)},       {mrg_ptr.data(), (nb + 1) * sizeof(int)},
       {mrg_ent.data(), mrg_ent.size() * sizeof(int4)},
-      {f_off.data(), f_off.size() * sizeof(int)},     {f_len.data(), f_len.size() * sizeof(int)},
-      {f_st.data(), f_st.size() * sizeof(uint32_t)},  {f_ri.data(), f_ri.size() * sizeof(int2)},
-      {b_off.data(), b_off.size() * sizeof(int)},     {b_len.data(), b_len.size() * sizeof(int)},
+      {f_pl.data(), f_pl.size() * sizeof(int2)},      {b_pl.data(), b_pl.size() * sizeof(int2)},
+      {f_st.data(), f_st.size() * sizeof(uint32_t)},  {pad_slots.data(), pad_slots.size() * sizeof(int)},
       {b_st.data(), b_st.size() * sizeof(uint2)},
       {nullptr, std::max<size_t>(partial_elems, 1) * sizeof(float)}};
   size_t total = 0;
@@ -338,18 +338,17 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   pd.mrg_ptr = (const int*)where[7];
   pd.mrg_ent = (const int4*)where[8];
   pd.mrg_max_bucket = max_bucket;
-  pd.nnz = (int)nnz;
+  pd.nnz = (int)nslot;
   ff::FastPlanDev& fp = p->fast;
   fp.enabled = fast ? 1 : 0;
-  fp.fwd_off = (const int*)where[9];
-  fp.fwd_len = (const int*)where[10];
+  fp.fwd_pl = (const int2*)where[9];
+  fp.bwd_pl = (const int2*)where[10];
   fp.fwd_st = (const uint32_t*)where[11];
-  fp.fwd_ri = (const int2*)where[12];
-  fp.bwd_off = (const int*)where[13];
-  fp.bwd_len = (const int*)where[14];
-  fp.bwd_st = (const uint2*)where[15];
+  fp.pad = (const int*)where[12];
+  fp.npad = (int)pad_slots.size();
+  fp.bwd_st = (const uint2*)where[13];
   fp.bwd_slots = (int)b_st.size();
-  p->partial = (float*)where[16];
+  p->partial = (float*)where[14];
   p->dev_mem = mem;
   p->workspace_bytes = total;
   p->fin->refs.fetch_add(1);
@@ -368,8 +367,8 @@ extern "C" void ff_plan_destroy(ff_plan* p) {
 
 extern "C" ff_status ff_plan_order(const ff_plan* p, int64_t* user_index) {
   ff::clear_error();
-  if (!p || (!user_index && p->nnz > 0)) return ff::fail(FF_EINVAL, "NULL argument");
-  for (int64_t j = 0; j < p->nnz; ++j) user_index[j] = p->user_order[j];
+  if (!p || (!user_index && p->coef_slots > 0)) return ff::fail(FF_EINVAL, "NULL argument");
+  for (int64_t j = 0; j < p->coef_slots; ++j) user_index[j] = p->user_order[j];
   return FF_OK;
 }
 
@@ -382,6 +381,7 @@ extern "C" ff_status ff_plan_query(const ff_plan* p, int key, int64_t* value) {
     case FF_Q_WORKSPACE_BYTES: *value = (int64_t)p->workspace_bytes; return FF_OK;
     case FF_Q_NNZ: *value = p->nnz; return FF_OK;
     case FF_Q_FAST128: *value = p->fast.enabled; return FF_OK;
+    case FF_Q_COEF_SLOTS: *value = p->coef_slots; return FF_OK;
     default: return ff::fail(FF_EINVAL, "unknown query key %d", key);
   }
 }

@@ -50,13 +50,13 @@ def merged_bf16_ok(got, W0, dW):
 
 
 def plan_c(plan, vals, device):
-    """User-order coefficient values -> device fp32 tensor in the plan's order."""
+    """User-order coefficient values -> device fp32 tensor in the plan's slot layout."""
     import torch
-    return torch.from_numpy(np.ascontiguousarray(np.asarray(vals, dtype=np.float32)[plan.order])).to(device)
+    return torch.from_numpy(plan.to_plan(vals)).to(device)
 
 
 def user_dc(plan, dC):
-    """Plan-order dC (device tensor) -> fp64 host array in user order."""
-    out = np.empty(plan.nnz, dtype=np.float64)
-    out[plan.order] = to_np(dC)
-    return out
+    """Plan-layout dC (device tensor) -> fp64 host array in user order; padding slots must be 0."""
+    d = to_np(dC)
+    assert np.all(d[plan.order < 0] == 0), "padding slots of dC are not zero"
+    return plan.to_user(d)

@@ -81,7 +81,8 @@ def test_small_parity(dev, shape, dtype):
     Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
     c = plan_c(plan, vals, dev)
     order = plan.order
-    assert np.array_equal(np.sort(order), np.arange(nnz))
+    assert np.array_equal(np.sort(order[order >= 0]), np.arange(nnz))
+    assert plan.coef_slots == order.size >= nnz
 
     # forward, overwrite and accumulate into an existing Y
     y_ref = O.adapter_fwd(P_in, P_out, rows, cols, vals, s, X)
@@ -90,11 +91,13 @@ def test_small_parity(dev, shape, dtype):
     Yb = ff.adapter_fwd(plan, Xd, c, s, Y=torch_act(Y0, dtype, dev), beta=0.75)
     # backward: overwrite, then accumulate
     dx_ref, dc_ref = O.adapter_bwd(P_in, P_out, rows, cols, vals, s, X, G)
-    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s)
+    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s, dC=torch.full((plan.coef_slots,), float("nan"), device=dev))
     dX0 = inputs.gaussian(inputs.rng(4), (T, n), dtype=dtype)
     dC0 = inputs.gaussian(inputs.rng(5), (nnz,)).astype(np.float32)
+    dC_init = plan.to_plan(dC0)
+    dC_init[order < 0] = 5.0            # accumulating calls leave padding slots alone
     dXb, dCb = ff.adapter_bwd(plan, Xd, Gd, c, s, dX=torch_act(dX0, dtype, dev), beta_dx=-1.5,
-                              dC=plan_c(plan, dC0, dev), accumulate_dc=True)
+                              dC=torch.from_numpy(dC_init).to(dev), accumulate_dc=True)
     _, dC2 = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dx=False)
     # merge: dense delta into fp32, and in place into a bf16 weight
     dw_ref = O.merge_delta(P_in, P_out, rows, cols, vals, s)
@@ -105,14 +108,15 @@ def test_small_parity(dev, shape, dtype):
 
     if nnz == 0:
         assert np.all(to_np(Y) == 0) and np.all(to_np(dX) == 0) and np.all(to_np(Wd) == 0)
-        assert dC.numel() == 0
+        assert dC.numel() == plan.coef_slots and np.all(to_np(dC) == 0)   # padding only
         return
     assert rel(to_np(Y), y_ref) <= tol
     assert rel(to_np(Yb), 0.75 * Y0 + y_ref) <= tol
     assert rel(to_np(dX), dx_ref) <= tol
     assert rel(user_dc(plan, dC), dc_ref) <= tol
     assert rel(to_np(dXb), -1.5 * dX0 + dx_ref) <= tol
-    assert rel(user_dc(plan, dCb), dC0 + dc_ref) <= tol
+    assert np.all(to_np(dCb)[order < 0] == 5.0)
+    assert rel(plan.to_user(to_np(dCb)), dC0 + dc_ref) <= tol
     assert torch.equal(dC, dC2), "dC is not deterministic"
     assert rel(to_np(Wd), dw_ref) <= 1e-5
     assert merged_bf16_ok(to_np(Wb), W0, dw_ref)
@@ -135,7 +139,7 @@ def test_batched_matches_single_calls(dev, dtype):
     cd = [plan_c(plan, v, dev) for v in vals]
     Yd = [torch.empty((T, m), dtype=Xd[0].dtype, device=dev) for _ in range(count)]
     dXd = [torch.empty((T, n), dtype=Xd[0].dtype, device=dev) for _ in range(count)]
-    dCd = [torch.empty((nnz,), device=dev) for _ in range(count)]
+    dCd = [torch.full((plan.coef_slots,), float("nan"), device=dev) for _ in range(count)]
     ff.adapter_fwd_batched(plan, Xd, cd, s, Yd)
     ff.adapter_bwd_batched(plan, Xd, Gd, cd, s, dXd, dCd)
     torch.cuda.synchronize()
@@ -157,7 +161,7 @@ def test_empty_batch_is_noop_and_zeroes_dc(dev):
     Xe = torch.zeros((0, n), device=dev)
     Ge = torch.zeros((0, m), device=dev)
     Y = ff.adapter_fwd(plan, Xe, c, 1.0)
-    dC = torch.full((100,), 7.0, device=dev)
+    dC = torch.full((plan.coef_slots,), 7.0, device=dev)
     dX, dC = ff.adapter_bwd(plan, Xe, Ge, c, 1.0, dC=dC)
     torch.cuda.synchronize()
     assert Y.shape == (0, m) and dX.shape == (0, n)

@@ -107,6 +107,7 @@ ff_status ff_adapter_fwd(const ff_plan* p, int64_t T, int act, const void* X, in
   if ((st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
   if ((st = check_act("Y", Y, ldy, p->fout->d, act)) != FF_OK) return st;
   if (p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
+  if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
   return launched(ff::launch_fwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, c_vals, nullptr, scale,
                                  beta, {Y, nullptr}, ldy, (hipStream_t)stream),
                   "forward launch");
@@ -129,6 +130,7 @@ ff_status ff_adapter_bwd(const ff_plan* p, int64_t T, int act, const void* X, in
     if (want_dc && (st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
     if (want_dx && (st = check_act("dX", dX, lddx, p->fin->d, act)) != FF_OK) return st;
     if (want_dx && p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
+    if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
   }
   return launched(ff::launch_bwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, {G, nullptr}, ldg, c_vals,
                                  nullptr, scale, beta_dx, {dX, nullptr}, lddx, want_dx, accumulate_dc, dC,
@@ -146,6 +148,7 @@ ff_status ff_merge_delta(const ff_plan* p, const float* c_vals, float scale, int
   if (ldw < p->fin->d) return ff::fail(FF_EINVAL, "ldw < n");
   if ((uintptr_t)W % (w_dtype == FF_BF16 ? 2 : 4)) return ff::fail(FF_EINVAL, "W is misaligned");
   if (p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
+  if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
   return launched(ff::launch_merge(p, c_vals, scale, w_dtype == FF_BF16, beta, W, ldw, (hipStream_t)stream),
                   "merge launch");
 }

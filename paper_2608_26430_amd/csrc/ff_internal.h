@@ -72,6 +72,9 @@ struct FastPlanDev {
   const int2* bwd_pl = nullptr;       // dC and q = C^T u, per input pair: (first stream row, rows)
   const uint2* bwd_st = nullptr;      // (slot word, plan index)
   int bwd_slots = 0;                  // 64 * backward stream rows = dC partials per tile
+  float* coef_bwd = nullptr;          // [batch][bwd_slots + 256]: c in backward slot order
+  const int* bwd_pos = nullptr;       // per coefficient slot: its backward slot (padding: bwd_slots)
+  int coef_slots = 0;
 };
 
 }  // namespace ff
@@ -147,12 +150,16 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
                          hipStream_t s);
 constexpr int kFastTileTokens = 8;
 
-// Slot words of the 128-wide kernels' entry streams: the byte offset of the source row in the
-// LDS coefficient array (rows of 16 bytes, unswizzled), the destination row in the pair tile
-// (swizzled, 0..255), end-of-row and valid flags.
-constexpr uint32_t kSlotSrcMask = 0xFFFFFu;        // bits 0..19
-constexpr int kSlotDstShift = 20;                   // bits 20..27
-constexpr uint32_t kSlotEnd = 1u << 28;
-constexpr uint32_t kSlotValid = 1u << 31;
+// Slot words of the 128-wide kernels' entry streams: end-of-row flag (bit 0), valid flag
+// (bit 1), the byte offset of the source row in the LDS coefficient array (rows of 16 bytes,
+// unswizzled; bits 4..19) and the byte offset of the destination row in the pair tile (swizzled
+// row * 16; bits 20..31).  Stream row r, lane l of a pair whose rows start at `off` (a multiple
+// of 4) is slot 64 off + 256 (r / 4) + 4 l + r % 4: each lane's four consecutive rows are
+// contiguous, so a wave loads them with one 16-byte load per lane.
+constexpr uint32_t kSlotEnd = 1u;
+constexpr uint32_t kSlotValid = 2u;
+constexpr uint32_t kSlotSrcMask = 0xFFFF0u;
+constexpr int kSlotDstShift = 20;
+inline int64_t fast_slot(int64_t off, int64_t r, int64_t l) { return 64 * off + 256 * (r >> 2) + 4 * l + (r & 3); }
 
 }  // namespace ff

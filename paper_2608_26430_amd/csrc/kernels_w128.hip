@@ -228,11 +228,11 @@ __device__ __forceinline__ void load_tile_act(const u16* tile, int lane, u32x4 (
   }
 }
 
-// y[t][(blk0+bs)*128 + o] = scale * acc (+ beta * y).  Token columns past the tile's end hold
-// the last token's values and write them to its row again.
+// y[t][(blk0+bs)*128 + o] = acc (+ beta * y); the scale s is already in the coefficients.  Token
+// columns past the tile's end hold the last token's values and write them to its row again.
 template <bool BETA>
 __device__ __forceinline__ void store_act(u16* rows, long ld, int nt, int blk0, int lane, const f32x4 (&acc)[kMT],
-                                          float scale, float beta) {
+                                          float beta) {
   const int n = lane & 15, t = min(n & 7, nt - 1), bs = n >> 3, q = lane >> 4;
   FF_GLOBAL u32x2* p = gst(reinterpret_cast<u32x2*>(rows + (long)t * ld + (blk0 + bs) * kW + 4 * q));
   u32x2 old[kMT];
@@ -242,7 +242,7 @@ __device__ __forceinline__ void store_act(u16* rows, long ld, int nt, int blk0, 
   }
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt) {
-    f32x4 r = acc[mt] * scale;
+    f32x4 r = acc[mt];
     if (BETA) {
       r[0] += beta * lo_bf(old[mt].x);
       r[1] += beta * hi_bf(old[mt].x);
@@ -265,12 +265,13 @@ __device__ __forceinline__ u32x4 lds_at(const unsigned char* base, unsigned byte
   return *reinterpret_cast<const u32x4*>(base + byte_off);
 }
 
-__device__ __forceinline__ unsigned tile_off(unsigned e) { return ((e >> kSlotDstShift) & 0xffu) * 16u; }
+__device__ __forceinline__ unsigned tile_off(unsigned e) { return e >> kSlotDstShift; }
 
-// The coefficient of a slot as the two multiplier words of v_dot2_f32_bf16, (c, 0) and (0, c),
-// both zero for a slot that holds no entry (the valid flag is the sign bit of the slot word).
-__device__ __forceinline__ void coef_words(unsigned e, float c, unsigned& ce, unsigned& co) {
-  ce = pack_bf2(c, 0.f) & (unsigned)((int)e >> 31);
+// The scaled coefficient of a slot as the two multiplier words of v_dot2_f32_bf16, (s c, 0) and
+// (0, s c).  Slots that hold no entry come after a lane's last row end in every stream, so
+// whatever they accumulate is never written and needs no mask.
+__device__ __forceinline__ void coef_words(float c, float scale, unsigned& ce, unsigned& co) {
+  ce = pack_bf2(c * scale, 0.f);
   co = ce << 16;
 }
 
@@ -305,22 +306,27 @@ struct FwdChunk {
   float cc[kCh];
 };
 
-// Load slots k0 .. k0+kCh-1 of a forward stream (its rows start at `off`, len >= 1): slot words
-// and their coefficients.  Rows past the stream's end re-read its last row and are dropped in
-// fwd_compute.
+// Load rows k0 .. k0+kCh-1 (k0 a multiple of 4) of a forward stream whose rows start at `off`
+// (len >= 4, a multiple of 4): slot words and their coefficients, four rows per 16-byte load.
+// Row groups past the stream's end re-read its last group and are skipped by fwd_compute.
 __device__ __forceinline__ void fwd_load(const unsigned* __restrict__ st, int off, int len, int k0,
                                          const float* __restrict__ cv, int lane, FwdChunk& ch) {
 #pragma unroll
-  for (int i = 0; i < kCh; ++i) {
-    const long slot = (long)(off + min(k0 + i, len - 1)) * 64 + lane;
-    ch.en[i] = gld(st)[slot];
-    ch.cc[i] = gld(cv)[slot];
+  for (int g = 0; g < kCh / 4; ++g) {
+    const long base = 64L * off + 256L * min(k0 / 4 + g, len / 4 - 1) + 4 * lane;
+    const u32x4 w = gld(reinterpret_cast<const u32x4*>(st + base))[0];
+    const f32x4 c = gld(reinterpret_cast<const f32x4*>(cv + base))[0];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      ch.en[4 * g + j] = w[j];
+      ch.cc[4 * g + j] = c[j];
+    }
   }
 }
 
-// The first n (1 <= n <= kCh, uniform) slots of a loaded chunk; all kCh LDS rows are read first.
-__device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int n, const unsigned char* zL, unsigned char* tile,
-                                            float (&a)[8]) {
+// The first n (uniform, a multiple of 4) slots of a loaded chunk; all kCh LDS rows are read first.
+__device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int n, float scale, const unsigned char* zL,
+                                            unsigned char* tile, float (&a)[8]) {
   u32x4 zv[kCh];
 #pragma unroll
   for (int i = 0; i < kCh; ++i) zv[i] = lds_at(zL, ch.en[i] & kSlotSrcMask);
@@ -328,7 +334,7 @@ __device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int n, const uns
   for (int i = 0; i < kCh; ++i) {
     if (i < n) {   // uniform
       unsigned ce, co;
-      coef_words(ch.en[i], ch.cc[i], ce, co);
+      coef_words(ch.cc[i], scale, ce, co);
       accum_row(ch.en[i], ce, co, zv[i], tile, a);
     }
   }
@@ -340,56 +346,71 @@ struct BwdEntries {
   u32x2 en[kCh];   // (slot word, coefficient slot)
 };
 
-// Rows past the stream's end (len >= 1) re-read its last row; bwd_word drops them.
+// Rows k0 .. k0+kCh-1 of a backward stream (`st` = its first row, len a multiple of 4), four
+// rows (32 bytes) per lane in two 16-byte loads; groups past the end re-read the last group.
 __device__ __forceinline__ void bwd_load_entries(const uint2* __restrict__ st, int len, int k0, int lane,
                                                  BwdEntries& ch) {
 #pragma unroll
-  for (int i = 0; i < kCh; ++i)
-    ch.en[i] = gld(reinterpret_cast<const u32x2*>(st))[(long)min(k0 + i, len - 1) * 64 + lane];
+  for (int g = 0; g < kCh / 4; ++g) {
+    const long base = 256L * min(k0 / 4 + g, len / 4 - 1) + 4 * lane;
+    const FF_GLOBAL u32x4* p = gld(reinterpret_cast<const u32x4*>(st + base));
+    const u32x4 lo = p[0], hi = p[1];
+    ch.en[4 * g + 0] = u32x2{lo[0], lo[1]};
+    ch.en[4 * g + 1] = u32x2{lo[2], lo[3]};
+    ch.en[4 * g + 2] = u32x2{hi[0], hi[1]};
+    ch.en[4 * g + 3] = u32x2{hi[2], hi[3]};
+  }
 }
 
-// Coefficients of the loaded entries (padding slots read a coefficient that is masked at use).
-__device__ __forceinline__ void bwd_load_coeffs(const float* __restrict__ cv, const BwdEntries& ch,
+// Coefficients of the same rows from the copy gathered into backward slot order (`cb` = the
+// pair's first slot), one 16-byte load per 4-row group.
+__device__ __forceinline__ void bwd_load_coeffs(const float* __restrict__ cb, int len, int k0, int lane,
                                                 float (&cc)[kCh]) {
 #pragma unroll
-  for (int i = 0; i < kCh; ++i) cc[i] = gld(cv)[ch.en[i].y];
+  for (int g = 0; g < kCh / 4; ++g) {
+    const f32x4 c = gld(reinterpret_cast<const f32x4*>(cb + 256L * min(k0 / 4 + g, len / 4 - 1) + 4 * lane))[0];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cc[4 * g + j] = c[j];
+  }
 }
 
-// This tile's share of dC / s for the first n (uniform) slots of a chunk, written to part (one
-// float per slot of this pair's stream, k0 = the chunk's first stream row; slots past the
-// stream's end write to the scratch row `trash`), in batches of kSb slots to bound the
-// registers held by LDS reads.
-constexpr int kSb = 4;
+// This tile's share of dC / s for the rows of a chunk, written per 4-row group with one 16-byte
+// store per lane to part (the pair's slots, k0 = the chunk's first stream row); groups past the
+// stream's end (n = rows of the chunk inside it, a multiple of 4) write to the scratch row
+// `trash`.  Padding slots write values the reduction never reads.
 __device__ __forceinline__ void bwd_sddmm(const BwdEntries& ch, int n, int k0, const unsigned char* uL,
                                           const unsigned char* tile, float* __restrict__ part,
                                           float* __restrict__ trash, int lane) {
 #pragma unroll
-  for (int h = 0; h < kCh / kSb; ++h) {
-    u32x4 uv[kSb], zv[kSb];
+  for (int g = 0; g < kCh / 4; ++g) {
+    f32x4 s4;
 #pragma unroll
-    for (int i = 0; i < kSb; ++i) {
-      const unsigned e = ch.en[h * kSb + i].x;
-      uv[i] = lds_at(uL, e & kSlotSrcMask);
-      zv[i] = lds_at(tile, tile_off(e));
-    }
+    for (int h = 0; h < 4; h += 2) {   // two slots' rows in flight at a time
+      u32x4 uv[2], zv[2];
 #pragma unroll
-    for (int i = 0; i < kSb; ++i) {
-      const int k = h * kSb + i;
-      const unsigned e = ch.en[k].x;
-      float s = 0.f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const unsigned uw = uv[i][j], zw = zv[i][j];
-        s = dot2(uw, zw, s);
+      for (int i = 0; i < 2; ++i) {
+        const unsigned e = ch.en[4 * g + h + i].x;
+        uv[i] = lds_at(uL, e & kSlotSrcMask);
+        zv[i] = lds_at(tile, tile_off(e));
       }
-      float* dst = k < n ? part + (long)(k0 + k) * 64 + lane : trash + lane;
-      *gst(dst) = (int)e < 0 ? s : 0.f;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        float s = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const unsigned uw = uv[i][j], zw = zv[i][j];
+          s = dot2(uw, zw, s);
+        }
+        s4[h + i] = s;
+      }
     }
+    float* dst = 4 * g < n ? part + 256L * (k0 / 4 + g) + 4 * lane : trash + 4 * lane;
+    *gst(reinterpret_cast<f32x4*>(dst)) = s4;
   }
 }
 
-__device__ __forceinline__ void bwd_spmm(const BwdEntries& ch, const float (&cc)[kCh], int n, const unsigned char* uL,
-                                         unsigned char* tile, float (&a)[8]) {
+__device__ __forceinline__ void bwd_spmm(const BwdEntries& ch, const float (&cc)[kCh], int n, float scale,
+                                         const unsigned char* uL, unsigned char* tile, float (&a)[8]) {
   constexpr int kH = kCh / 2;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -399,10 +420,9 @@ __device__ __forceinline__ void bwd_spmm(const BwdEntries& ch, const float (&cc)
 #pragma unroll
     for (int i = 0; i < kH; ++i) {
       if (h * kH + i < n) {   // uniform
-        const unsigned e = ch.en[h * kH + i].x;
         unsigned ce, co;
-        coef_words(e, cc[h * kH + i], ce, co);
-        accum_row(e, ce, co, uv[i], tile, a);
+        coef_words(cc[h * kH + i], scale, ce, co);
+        accum_row(ch.en[h * kH + i].x, ce, co, uv[i], tile, a);
       }
     }
   }
@@ -422,9 +442,10 @@ struct FastArgs {
   long ldy;
   const float* c;
   const float* const* cs;
+  const float* cb;    // backward: coefficients in backward slot order, [batch][slots + 256]
   float scale, beta;
   int slots;          // dC partials per tile
-  int pstride;        // floats per tile in the partial workspace: slots + one scratch row
+  int pstride;        // floats per tile in the partial workspace: slots + a scratch row group
   float* partial;     // [batch][tile][pstride]
   long ntiles;
 };
@@ -504,11 +525,11 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int2* __
     const int off = q.x, len = q.y;
     zero_tile(tile, lane);
     float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    fwd_compute(cur, min(kCh, len), zL, tile, acc8);
+    fwd_compute(cur, min(kCh, len), a.scale, zL, tile, acc8);
     if (len > kCh) {   // long stream
       for (int k0 = kCh; k0 < len; k0 += kCh) {
         fwd_load(fst, off, len, k0, cv, lane, cur);
-        fwd_compute(cur, min(kCh, len - k0), zL, tile, acc8);
+        fwd_compute(cur, min(kCh, len - k0), a.scale, zL, tile, acc8);
       }
       vm_wait_all();
     }
@@ -519,7 +540,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int2* __
     load_tile_act(reinterpret_cast<const u16*>(tile), lane, b);
     wave_lds_fence();
     mfma_block(F, b, acc);
-    store_act<BETA>(Y, a.ldy, nt, 2 * p, lane, acc, a.scale, a.beta);
+    store_act<BETA>(Y, a.ldy, nt, 2 * p, lane, acc, a.beta);
     q = qn;
   };
   FwdChunk ch2;
@@ -541,7 +562,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
   const u16* G = reinterpret_cast<const u16*>(a.Gs ? a.Gs[bi] : a.G) + (long)t0 * a.ldg;
   const u16* X = DC ? reinterpret_cast<const u16*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx : nullptr;
   u16* dX = DX ? reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy : nullptr;
-  const float* cv = DX ? (a.cs ? a.cs[bi] : a.c) : nullptr;
+  const float* cbw = DX ? a.cb + (long)bi * (a.slots + 256) : nullptr;
   float* part = DC ? a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.pstride : nullptr;
   float* trash = DC ? part + a.slots : nullptr;
   // dC sums only over the tile's tokens: activation columns past its end are zeroed
@@ -614,26 +635,28 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
   }
   if (DX) {
     float cc[kCh], cc2[kCh];
-    bwd_load_coeffs(cv, ch, cc);
-    // one input pair; the next pair's entries are loaded at its start and their coefficients
-    // before its stores, two pairs per iteration with the buffers' roles swapped
+    bwd_load_coeffs(cbw + (long)q.x * 64, q.y, 0, lane, cc);
+    // one input pair; the next pair's entries and coefficients are loaded at its start, two
+    // pairs per iteration with the buffers' roles swapped
     auto pair = [&](int p, BwdEntries& ch, float (&cc)[kCh], BwdEntries& chn, float (&ccn)[kCh]) {
       const int len = q.y;
       const uint2* st = bst + (long)q.x * 64;
+      const float* cbp = cbw + (long)q.x * 64;
       const int2 qn = pl[min(p + kWaves, lastp)];
       bwd_load_entries(bst + (long)qn.x * 64, qn.y, 0, lane, chn);
+      bwd_load_coeffs(cbw + (long)qn.x * 64, qn.y, 0, lane, ccn);
       issue_point();
       // q = C^T u for this pair, then dX = beta dX + s P_in q
       zero_tile(tile, lane);
       float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      bwd_spmm(ch, cc, min(kCh, len), uL, tile, acc8);
+      bwd_spmm(ch, cc, min(kCh, len), a.scale, uL, tile, acc8);
       if (len > kCh) {   // long stream
         for (int k0 = kCh; k0 < len; k0 += kCh) {
           BwdEntries ck;
           float ckc[kCh];
           bwd_load_entries(st, len, k0, lane, ck);
-          bwd_load_coeffs(cv, ck, ckc);
-          bwd_spmm(ck, ckc, min(kCh, len - k0), uL, tile, acc8);
+          bwd_load_coeffs(cbp, len, k0, lane, ckc);
+          bwd_spmm(ck, ckc, min(kCh, len - k0), a.scale, uL, tile, acc8);
         }
         vm_wait_all();
       }
@@ -643,9 +666,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
       load_tile_act(reinterpret_cast<const u16*>(tile), lane, b);
       wave_lds_fence();
       mfma_block(F, b, acc);
-      bwd_load_coeffs(cv, chn, ccn);   // the next pair's coefficients, before this pair's stores
-      issue_point();
-      store_act<BETA>(dX, a.ldy, nt, 2 * p, lane, acc, a.scale, a.beta);
+      store_act<BETA>(dX, a.ldy, nt, 2 * p, lane, acc, a.beta);
       q = qn;
     };
     BwdEntries ch2;
@@ -654,6 +675,19 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
       if (p + kWaves < npi) pair(p + kWaves, ch2, cc2, ch, cc);
     }
   }
+}
+
+// cb[batch][pos[j]] = c[batch][j]: the backward's coefficients scattered into its own stream
+// order (one coalesced load per coefficient, no dependent load), so that it loads them like the
+// forward does.  Padding slots go to a scratch slot past the backward slots.
+__global__ void __launch_bounds__(256) scatter_bwd_coef(const float* c, const float* const* cs,
+                                                        const int* __restrict__ pos, int nslot, int cstride,
+                                                        float* cb) {
+  const int bi = blockIdx.y;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= nslot) return;
+  const float* cv = cs ? cs[bi] : c;
+  gst(cb)[(long)bi * cstride + gld(pos)[j]] = gld(cv)[j];
 }
 
 // dC[j] = [dC[j] +] s * sum_tiles partial[tile][slot] for every valid slot of the backward
@@ -700,7 +734,7 @@ __global__ void __launch_bounds__(64 * kRedWaves) reduce128(const float* __restr
 #pragma unroll
     for (int i = 0; i < kRedWaves; ++i) tot += red[i][lane];
     const u32x2 en = gld(reinterpret_cast<const u32x2*>(bst))[slot];
-    if ((int)en.x < 0) {   // valid slot
+    if (en.x & kSlotValid) {
       const float v = scale * tot;
       gst(out)[en.y] = accumulate ? gld(out)[en.y] + v : v;
     }
@@ -744,7 +778,7 @@ size_t fast128_lds_bytes(int nblk) {
   return b < frag ? frag : b;
 }
 
-size_t fast128_partial_floats(size_t bwd_slots) { return bwd_slots + 64; }
+size_t fast128_partial_floats(size_t bwd_slots) { return bwd_slots + 256; }
 
 hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, const float* c,
                          const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, hipStream_t s) {
@@ -801,10 +835,17 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   a.slots = p->fast.bwd_slots;
   a.pstride = (int)fast128_partial_floats((size_t)a.slots);
   a.partial = p->partial;
+  a.cb = p->fast.coef_bwd;
   const long ntiles = (T + kTT - 1) / kTT;
   a.ntiles = ntiles;
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
+  if (T > 0 && want_dx) {
+    const int nslot = p->fast.coef_slots;
+    const dim3 g((unsigned)((nslot + 255) / 256), (unsigned)count);
+    hipLaunchKernelGGL(scatter_bwd_coef, g, dim3(256), 0, s, c, cs, p->fast.bwd_pos, nslot, a.slots + 256,
+                       p->fast.coef_bwd);
+  }
   if (T > 0 && (want_dx || want_dc)) {
     const dim3 grid((unsigned)ntiles, (unsigned)count);
     const size_t lds = fast128_lds_bytes(a.nblk_out);

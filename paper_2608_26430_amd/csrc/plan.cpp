@@ -186,11 +186,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   }
 
   // ---------------- 128-wide fused path: balanced entry streams per pair of blocks
-  // Forward stream (v = C z), one per pair of output blocks: slot word = byte offset of the
-  // source row of z | destination row of the pair tile | end-of-row | valid.  The plan's
-  // coefficient layout is this stream's slot layout: the coefficient of slot (stream row r,
-  // lane l) is c[64 r + l], so forward slots read coefficients without an index; slots that
-  // hold no entry are padding.
+  // Forward stream (v = C z), one per pair of output blocks, slot words as described with
+  // kSlotEnd in ff_internal.h.  The plan's coefficient layout is this stream's slot layout, so
+  // forward slots read coefficients without an index; slots that hold no entry are padding.
   // Backward stream (dC and q = C^T u), one per pair of input blocks, grouped by column
   // of C: (byte offset of the source row of u | tile row of the column | end-of-column | valid,
   // coefficient slot).
@@ -202,7 +200,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   std::vector<int> pad_slots;
   std::vector<uint32_t> f_st;
   std::vector<uint2> b_st;
-  std::vector<int> slot_of_user((size_t)nnz);
+  std::vector<int> slot_of_user((size_t)nnz), bwd_slot_of_user;
   std::vector<int64_t> user_of_slot;
   if (fast) {
     // byte offset of a coefficient's row in the LDS array of a whole side, and its row in a pair tile
@@ -221,20 +219,20 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       for (int r = 0; r < 256; ++r) sz[r] = (int)frows[pp][r].size();
       int len = 0;
       const auto lanes = assign_lanes(sz, len);
-      len = std::max(len, 1);   // every stream has a row, so prefetches never need a guard
+      len = std::max((len + 3) / 4 * 4, 4);   // whole 4-row groups; every stream has one
       const size_t row0 = f_st.size() / 64;
       f_pl.push_back(make_int2((int)row0, len));
       f_st.resize(f_st.size() + (size_t)len * 64, 0u);
       user_of_slot.resize(f_st.size(), -1);
       for (int l = 0; l < 64; ++l) {
-        size_t k = 0;
+        int k = 0;
         for (int r : lanes[l])
           for (size_t i = 0; i < frows[pp][r].size(); ++i, ++k) {
             const int e = frows[pp][r][i];
             const bool last = i + 1 == frows[pp][r].size();
             const uint32_t dst = (uint32_t)((r >> 7) * 128 + swz128(r >> 7, r & 127));
-            const size_t slot = (row0 + k) * 64 + (size_t)l;
-            f_st[slot] = lsrc(cloc[e]) | (dst << ff::kSlotDstShift) | ff::kSlotValid | (last ? ff::kSlotEnd : 0u);
+            const size_t slot = (size_t)ff::fast_slot((int64_t)row0, k, l);
+            f_st[slot] = lsrc(cloc[e]) | (dst * 16u << ff::kSlotDstShift) | ff::kSlotValid | (last ? ff::kSlotEnd : 0u);
             user_of_slot[slot] = e;
             slot_of_user[e] = (int)slot;
           }
@@ -242,23 +240,26 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     }
     for (size_t j = 0; j < user_of_slot.size(); ++j)
       if (user_of_slot[j] < 0) pad_slots.push_back((int)j);
+    bwd_slot_of_user.assign((size_t)nnz, 0);
     for (int pp = 0; pp < npi; ++pp) {
       std::vector<int> sz(256);
       for (int r = 0; r < 256; ++r) sz[r] = (int)brows[pp][r].size();
       int len = 0;
       const auto lanes = assign_lanes(sz, len);
-      len = std::max(len, 1);
-      b_pl.push_back(make_int2((int)(b_st.size() / 64), len));
-      const size_t base = b_st.size();
-      b_st.resize(base + (size_t)len * 64, make_uint2(0u, 0u));
+      len = std::max((len + 3) / 4 * 4, 4);
+      const int64_t row0 = (int64_t)(b_st.size() / 64);
+      b_pl.push_back(make_int2((int)row0, len));
+      b_st.resize(b_st.size() + (size_t)len * 64, make_uint2(0u, 0u));
       for (int l = 0; l < 64; ++l) {
         int k = 0;
         for (int r : lanes[l])
           for (size_t i = 0; i < brows[pp][r].size(); ++i, ++k) {
             const int e = brows[pp][r][i];
             const bool last = i + 1 == brows[pp][r].size();
-            b_st[base + (size_t)k * 64 + l] = make_uint2(
-                lsrc(rloc[e]) | (trow(cloc[e]) << ff::kSlotDstShift) | ff::kSlotValid | (last ? ff::kSlotEnd : 0u),
+            bwd_slot_of_user[e] = (int)ff::fast_slot(row0, k, l);
+            b_st[(size_t)ff::fast_slot(row0, k, l)] = make_uint2(
+                lsrc(rloc[e]) | (trow(cloc[e]) * 16u << ff::kSlotDstShift) | ff::kSlotValid |
+                    (last ? ff::kSlotEnd : 0u),
                 (unsigned)slot_of_user[e]);
           }
       }
@@ -269,6 +270,14 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     std::iota(user_of_slot.begin(), user_of_slot.end(), 0);
   }
   const int64_t nslot = (int64_t)user_of_slot.size();   // coefficient slots (>= nnz)
+  // for the 128-wide backward: the backward slot of every coefficient slot (padding slots go
+  // to the scratch slot just past the backward slots)
+  std::vector<int> bwd_pos;
+  if (fast) {
+    bwd_pos.resize((size_t)nslot);
+    for (int64_t j = 0; j < nslot; ++j)
+      bwd_pos[j] = user_of_slot[j] >= 0 ? bwd_slot_of_user[user_of_slot[j]] : (int)b_st.size();
+  }
   // the generic kernels index coefficients by slot too; padding slots of the dC table are
   // marked (-1, -1) and produce zeros
   for (auto& en : fwd_ent) en.y = nnz ? slot_of_user[en.y] : 0;
@@ -301,7 +310,10 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       {f_pl.data(), f_pl.size() * sizeof(int2)},      {b_pl.data(), b_pl.size() * sizeof(int2)},
       {f_st.data(), f_st.size() * sizeof(uint32_t)},  {pad_slots.data(), pad_slots.size() * sizeof(int)},
       {b_st.data(), b_st.size() * sizeof(uint2)},
-      {nullptr, std::max<size_t>(partial_elems, 1) * sizeof(float)}};
+      {nullptr, std::max<size_t>(partial_elems, 1) * sizeof(float)},
+      // the backward's coefficients in its stream's slot order, per adapter (+ a scratch group)
+      {nullptr, std::max<size_t>((size_t)max_batch * (b_st.size() + 256), 1) * sizeof(float)},
+      {bwd_pos.data(), bwd_pos.size() * sizeof(int)}};
   size_t total = 0;
   for (const Blob& b : blobs) total += up(b.bytes);
   int cur = 0;
@@ -349,6 +361,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   fp.bwd_st = (const uint2*)where[13];
   fp.bwd_slots = (int)b_st.size();
   p->partial = (float*)where[14];
+  fp.coef_bwd = (float*)where[15];
+  fp.bwd_pos = (const int*)where[16];
+  fp.coef_slots = (int)nslot;
   p->dev_mem = mem;
   p->workspace_bytes = total;
   p->fin->refs.fetch_add(1);

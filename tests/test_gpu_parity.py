@@ -241,3 +241,62 @@ def test_cfg1_full(dev):
 
 def test_cfg2_llama7b_qproj_full(dev):
     _full_size_check(dev, "cfg2_llama7b_qproj")
+
+
+def test_cfg3_llama7b_mlp_up_full(dev):
+    _full_size_check(dev, "cfg3_llama7b_mlp", adapter_index=0, n_tok=24, n_nnz=256, n_rows=4)
+
+
+def test_cfg3_llama7b_mlp_down_full(dev):
+    _full_size_check(dev, "cfg3_llama7b_mlp", adapter_index=1, n_tok=24, n_nnz=256, n_rows=4)
+
+
+def test_cfg5_llama70b_down_full(dev):
+    _full_size_check(dev, "cfg5_llama70b_down", n_tok=12, n_nnz=192, n_rows=3)
+
+
+def test_cfg5_vitb16_qkv_full(dev):
+    _full_size_check(dev, "cfg5_vitb16_qkv", n_tok=48, n_nnz=384, n_rows=8)
+
+
+@pytest.mark.parametrize("group", [("q_proj", "k_proj", "v_proj", "o_proj"), ("gate_proj", "up_proj"),
+                                   ("down_proj",)])
+def test_cfg4_stack_batched_full(dev, group):
+    """The 32-layer stack: one plan per projection shape (support shared across layers and
+    projections), one batched call over layers {0, 31} x the group's projections at full
+    per-adapter size (2048 tokens); every adapter checked on sampled tokens and entries."""
+    wl = inputs.WORKLOADS["cfg4_llama7b_stack"]
+    ads = [a for a in wl.adapters if a.name in group]
+    ad0 = ads[0]
+    layers = (0, wl.layers - 1)
+    datas = [inputs.adapter_data(wl, ad, seed=wl.seed + 1000 * layer + 10 * i, support_seed=wl.seed + 10 * i)
+             for layer in layers for i, ad in enumerate(ads)]
+    # one support per group (the first adapter's draw), shared by every layer and projection
+    rows, cols = datas[0].rows, datas[0].cols
+    T, dtype = wl.tokens, wl.dtype
+    f_in = ff.framegen(ad0.d_in, ad0.k_in, ad0.rho_in)
+    f_out = ff.framegen(ad0.d_out, ad0.k_out, ad0.rho_out)
+    count = len(datas)
+    plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T, max_batch=count)
+    Xd = [torch_act(d.X, dtype, dev) for d in datas]
+    Gd = [torch_act(d.G, dtype, dev) for d in datas]
+    cd = [plan_c(plan, d.vals, dev) for d in datas]
+    Yd = [torch.empty((T, ad0.d_out), dtype=Xd[0].dtype, device=dev) for _ in datas]
+    dXd = [torch.empty((T, ad0.d_in), dtype=Xd[0].dtype, device=dev) for _ in datas]
+    dCd = [torch.full((plan.coef_slots,), float("nan"), device=dev) for _ in datas]
+    s = datas[0].scale
+    ff.adapter_fwd_batched(plan, Xd, cd, s, Yd)
+    ff.adapter_bwd_batched(plan, Xd, Gd, cd, s, dXd, dCd)
+    torch.cuda.synchronize()
+    P_in = oracle_frame(ad0.k_in, ad0.rho_in, ad0.d_in)
+    P_out = oracle_frame(ad0.k_out, ad0.rho_out, ad0.d_out)
+    tol = TOL[dtype]
+    for i, d in enumerate(datas):
+        tok = _sample_tokens(T, 16, wl.seed + i)
+        y_ref = O.adapter_fwd(P_in, P_out, rows, cols, d.vals, s, d.X[tok])
+        dx_ref, _ = O.adapter_bwd(P_in, P_out, rows, cols, d.vals, s, d.X[tok], d.G[tok])
+        assert rel(to_np(Yd[i][tok]), y_ref) <= tol
+        assert rel(to_np(dXd[i][tok]), dx_ref) <= tol
+        ent = np.random.default_rng(wl.seed + i).choice(len(rows), size=128, replace=False)
+        dc_ref = O.coeff_grad_entries(P_in, P_out, rows[ent], cols[ent], s, d.X, d.G)
+        assert rel(user_dc(plan, dCd[i])[ent], dc_ref) <= tol

@@ -151,9 +151,9 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
 constexpr int kFastTileTokens = 8;
 
 // Slot words of the 128-wide kernels' entry streams: end-of-row flag (bit 0), valid flag
-// (bit 1), the byte offset of the source row in the LDS coefficient array (rows of 16 bytes,
-// unswizzled; bits 4..19) and the byte offset of the destination row in the pair tile (swizzled
-// row * 16; bits 20..31).  Stream row r, lane l of a pair whose rows start at `off` (a multiple
+// (bit 1), the byte offset of the source row in the LDS coefficient array (rows of 16 bytes;
+// bits 4..19) and the byte offset of the destination in the pair tile (rows of 32 bytes, one
+// per coefficient, holding both blocks' 8 tokens; bits 20..31).  Stream row r, lane l of a pair whose rows start at `off` (a multiple
 // of 4) is slot 64 off + 256 (r / 4) + 4 l + r % 4: each lane's four consecutive rows are
 // contiguous, so a wave loads them with one 16-byte load per lane.
 constexpr uint32_t kSlotEnd = 1u;

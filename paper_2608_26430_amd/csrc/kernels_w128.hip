@@ -74,6 +74,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned short u16;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 // Global-memory views of generic pointers.  Pointers read from device arrays (the batched
 // entry points) carry no address space, and loads through them would be emitted as flat
@@ -88,8 +89,6 @@ template <typename T>
 __device__ __forceinline__ FF_GLOBAL T* gst(T* p) {
   return (FF_GLOBAL T*)p;
 }
-
-__device__ __forceinline__ int swz(int blk, int o) { return o ^ ((o >> 2) & 4) ^ ((blk & 1) << 1); }
 
 __device__ __forceinline__ float lo_bf(unsigned w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf(unsigned w) { return __uint_as_float(w & 0xffff0000u); }
@@ -188,16 +187,38 @@ __device__ __forceinline__ void mfma_block_t(const Frag& F, const u32x4 (&b)[kKT
   }
 }
 
-// Store the result of mfma_block_t into a coefficient-major LDS array (odd coefficients
-// negated: sgn = 0x80008000 on lanes with odd n), one 8-byte write per row tile.  `row_even` /
-// `row_odd` are this lane's byte offsets for even / odd row tiles (equal unless the array is
-// swizzled); row tile mt adds 256 mt bytes.
-__device__ __forceinline__ void store_coef_t(unsigned char* lds, unsigned row_even, unsigned row_odd,
-                                             const f32x4 (&acc)[kMT], unsigned sgn) {
+// Store the result of mfma_block_t into a coefficient-major LDS array of 16-byte rows (odd
+// coefficients negated: sgn = 0x80008000 on lanes with odd n), one 8-byte write per row tile at
+// `row` (this lane's byte offset in row tile 0) + 256 mt.
+__device__ __forceinline__ void store_coef_t(unsigned char* lds, unsigned row, const f32x4 (&acc)[kMT],
+                                             unsigned sgn) {
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt) {
     const unsigned w0 = pack_bf2(acc[mt][0], acc[mt][1]) ^ sgn, w1 = pack_bf2(acc[mt][2], acc[mt][3]) ^ sgn;
-    *reinterpret_cast<u32x2*>(lds + ((mt & 1) ? row_odd : row_even) + 256 * mt) = u32x2{w0, w1};
+    *reinterpret_cast<u32x2*>(lds + row + 256 * mt) = u32x2{w0, w1};
+  }
+}
+
+// Pair tile: 128 rows of 32 bytes, one per coefficient k of the block width, each holding the
+// 8 tokens of both blocks.  Within 32 coefficients the rows are ordered by (bit 2, bits 3..4,
+// bits 0..1) of k, so that one transposed read of the synthesis operand covers 512 contiguous
+// bytes, and rows with bit 2 of k set hold block 1 in their first half.  Byte offset of this
+// lane's 8 bytes of row tile 0 of mfma_block_t's result (lane: coefficient n of quarter q, whose
+// 4 tokens are half q & 1 of block q >> 1), and the offset that row tile mt adds.
+__device__ __forceinline__ unsigned tile_lane_off(int lane) {
+  const int n = lane & 15, q = lane >> 4, b2 = (n >> 2) & 1;
+  return 512 * b2 + 128 * (n >> 3) + 32 * (n & 3) + 8 * (q ^ (2 * b2));
+}
+__device__ __forceinline__ constexpr unsigned tile_mt_off(int mt) { return 1024 * (mt >> 1) + 256 * (mt & 1); }
+
+// Store the result of mfma_block_t into the pair tile (odd coefficients negated as in
+// store_coef_t); 32 lanes of one write cover 256 distinct bytes.
+__device__ __forceinline__ void store_tile_t(unsigned char* tile, unsigned off, const f32x4 (&acc)[kMT],
+                                             unsigned sgn) {
+#pragma unroll
+  for (int mt = 0; mt < kMT; ++mt) {
+    const unsigned w0 = pack_bf2(acc[mt][0], acc[mt][1]) ^ sgn, w1 = pack_bf2(acc[mt][2], acc[mt][3]) ^ sgn;
+    *reinterpret_cast<u32x2*>(tile + off + tile_mt_off(mt)) = u32x2{w0, w1};
   }
 }
 
@@ -211,20 +232,23 @@ __device__ __forceinline__ void load_act(const u16* rows, long ld, int nt, int b
   for (int ks = 0; ks < kKT; ++ks) b[ks] = p[4 * ks];
 }
 
-// Gather the synthesis operand of the pair tile (rows bs*128 + swz(bs, o), 8 tokens per row).
-__device__ __forceinline__ void load_tile_act(const u16* tile, int lane, u32x4 (&b)[kKT]) {
-  const int n = lane & 15, t = n & 7, bs = n >> 3, q = lane >> 4;
-  const u16* base = tile + bs * kW * kTT + t;
+// The synthesis operand from the pair tile by transposed LDS reads (ds_read_b64_tr_b16): in each
+// 16-lane group the lanes' 8-byte chunks form 4 rows of 16 bf16 values and lane i receives
+// value i of each row.  Lane (column n = 8 bs + t, quarter q) thus receives token t of block bs
+// at 4 consecutive coefficients per read; read h of step ks covers coefficients
+// 32 ks + 8 q + 4 h + (0..3), the 16 tile rows starting at row 32 ks + 16 h, whose halves are
+// swapped when h = 1.
+__device__ __forceinline__ void load_tile_act(const unsigned char* tile, int lane, u32x4 (&b)[kKT]) {
 #pragma unroll
   for (int ks = 0; ks < kKT; ++ks) {
-    unsigned w[4];
+    u32x2 v[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int o = 32 * ks + 8 * q + 2 * i;
-      const unsigned e0 = base[swz(bs, o) * kTT], e1 = base[swz(bs, o + 1) * kTT];
-      w[i] = e0 | (e1 << 16);
+    for (int h = 0; h < 2; ++h) {
+      auto* p = (__attribute__((address_space(3))) i16x4*)(const_cast<unsigned char*>(tile) +
+                                                           (32 * ks + 16 * h) * 32 + 8 * (lane ^ (2 * h)));
+      v[h] = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(p));
     }
-    b[ks] = u32x4{w[0], w[1], w[2], w[3]};
+    b[ks] = u32x4{v[0].x, v[0].y, v[1].x, v[1].y};
   }
 }
 
@@ -470,14 +494,14 @@ __device__ __forceinline__ void analysis_phase(const Frag& F, const u16* rows, l
     {
       f32x4 acc[kMT];
       mfma_block_t(F, bA, acc, ~0u);
-      store_coef_t(lds + p * kPairBytes, off, off, acc, sgn);
+      store_coef_t(lds + p * kPairBytes, off, acc, sgn);
     }
     load_act(rows, ld, nt, 2 * min(p + 2 * kWaves, last), lane, bA);
     issue_point();
     {
       f32x4 acc[kMT];
       mfma_block_t(F, bB, acc, ~0u);
-      if (p + kWaves < np) store_coef_t(lds + (p + kWaves) * kPairBytes, off, off, acc, sgn);
+      if (p + kWaves < np) store_coef_t(lds + (p + kWaves) * kPairBytes, off, acc, sgn);
     }
     load_act(rows, ld, nt, 2 * min(p + 3 * kWaves, last), lane, bB);
     issue_point();
@@ -537,7 +561,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int2* __
     // y = beta y + s P_out v
     u32x4 b[kKT];
     f32x4 acc[kMT];
-    load_tile_act(reinterpret_cast<const u16*>(tile), lane, b);
+    load_tile_act(tile, lane, b);
     wave_lds_fence();
     mfma_block(F, b, acc);
     store_act<BETA>(Y, a.ldy, nt, 2 * p, lane, acc, a.beta);
@@ -567,11 +591,9 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
   float* trash = DC ? part + a.slots : nullptr;
   // dC sums only over the tile's tokens: activation columns past its end are zeroed
   const unsigned km = (lane & 7) < nt ? ~0u : 0u;
-  // this lane's rows of the swizzled pair tile for the analysis of x (even / odd row tiles)
-  const int ln = lane & 15, lq = lane >> 4, lbs = lq >> 1;
-  const unsigned zrow_even = (lbs * kW + (ln ^ (2 * lbs))) * 16 + 8 * (lq & 1);
-  const unsigned zrow_odd = (lbs * kW + (ln ^ 4 ^ (2 * lbs))) * 16 + 8 * (lq & 1);
-  const unsigned zsgn = (ln & 1) ? 0x80008000u : 0u;
+  // this lane's place in the pair tile for the analysis of x
+  const unsigned zoff = tile_lane_off(lane);
+  const unsigned zsgn = (lane & 1) ? 0x80008000u : 0u;
   const int npi = a.nblk_in / 2, lastp = npi - 1;
 
   u32x4 fr[kFragPerThread];
@@ -605,7 +627,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
       {
         f32x4 acc[kMT];
         mfma_block_t(F, bx, acc, km);
-        store_coef_t(tile, zrow_even, zrow_odd, acc, zsgn);
+        store_tile_t(tile, zoff, acc, zsgn);
       }
       wave_lds_fence();
       load_act(X, a.ldx, nt, 2 * min(p + kWaves, lastp), lane, bx);
@@ -663,7 +685,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
       wave_lds_fence();
       u32x4 b[kKT];
       f32x4 acc[kMT];
-      load_tile_act(reinterpret_cast<const u16*>(tile), lane, b);
+      load_tile_act(tile, lane, b);
       wave_lds_fence();
       mfma_block(F, b, acc);
       store_act<BETA>(dX, a.ldy, nt, 2 * p, lane, acc, a.beta);

@@ -35,8 +35,16 @@ int token_stride(int nblk, int ldb, int esz) {
   return base + pad;
 }
 
-// Row swizzle inside a 128-row block of the 128-wide kernels' pair tiles.
-int swz128(int blk, int o) { return o ^ ((o >> 2) & 4) ^ ((blk & 1) << 1); }
+// Byte offset of coefficient `local` of block parity `par` in a 128-wide kernel's pair tile:
+// 128 rows of 32 bytes, each holding one coefficient's 8 tokens of both blocks.  Row order
+// within 32 coefficients swaps bit 2 of the coefficient with bits 3..4, so that each transposed
+// read of the synthesis operand covers 512 contiguous bytes; rows with bit 2 set hold block 1
+// first, so that the analysis writes of 16 consecutive coefficients hit distinct LDS banks.
+uint32_t tile_byte(int par, int local) {
+  const int b2 = (local >> 2) & 1;
+  const int row = (local & ~31) | (b2 << 4) | (((local >> 3) & 3) << 2) | (local & 3);
+  return (uint32_t)(row * 32 + 16 * (par ^ b2));
+}
 
 // Rows of one pair of blocks assigned whole to 64 lanes, longest first, each to the least
 // loaded lane; lanes are then renumbered by decreasing load, so in every stream row the
@@ -205,7 +213,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   if (fast) {
     // byte offset of a coefficient's row in the LDS array of a whole side, and its row in a pair tile
     auto lsrc = [&](const Loc& l) { return (uint32_t)(l.blk * 128 + l.local) * 16u; };
-    auto trow = [&](const Loc& l) { return (uint32_t)((l.blk & 1) * 128 + swz128(l.blk, l.local)); };
+    auto tbyte = [&](const Loc& l) { return tile_byte(l.blk & 1, l.local); };
     const int npo = FO.nblk / 2, npi = FI.nblk / 2;
     // entries of each destination row r = (block parity)*128 + local of a pair
     std::vector<std::vector<std::vector<int>>> frows(npo, std::vector<std::vector<int>>(256)),
@@ -230,9 +238,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
           for (size_t i = 0; i < frows[pp][r].size(); ++i, ++k) {
             const int e = frows[pp][r][i];
             const bool last = i + 1 == frows[pp][r].size();
-            const uint32_t dst = (uint32_t)((r >> 7) * 128 + swz128(r >> 7, r & 127));
+            const uint32_t dst = tile_byte(r >> 7, r & 127);
             const size_t slot = (size_t)ff::fast_slot((int64_t)row0, k, l);
-            f_st[slot] = lsrc(cloc[e]) | (dst * 16u << ff::kSlotDstShift) | ff::kSlotValid | (last ? ff::kSlotEnd : 0u);
+            f_st[slot] = lsrc(cloc[e]) | (dst << ff::kSlotDstShift) | ff::kSlotValid | (last ? ff::kSlotEnd : 0u);
             user_of_slot[slot] = e;
             slot_of_user[e] = (int)slot;
           }
@@ -258,7 +266,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
             const bool last = i + 1 == brows[pp][r].size();
             bwd_slot_of_user[e] = (int)ff::fast_slot(row0, k, l);
             b_st[(size_t)ff::fast_slot(row0, k, l)] = make_uint2(
-                lsrc(rloc[e]) | (trow(cloc[e]) * 16u << ff::kSlotDstShift) | ff::kSlotValid |
+                lsrc(rloc[e]) | (tbyte(cloc[e]) << ff::kSlotDstShift) | ff::kSlotValid |
                     (last ? ff::kSlotEnd : 0u),
                 (unsigned)slot_of_user[e]);
           }

@@ -62,14 +62,18 @@ struct PlanDev {
 };
 
 // Entry streams of the 128-wide fused kernels: per pair of adjacent 128-wide
-// blocks, `len` rows of 64 lane slots starting at stream row `off`.
+// blocks, `len` rows of 64 lane slots starting at stream row `off`.  Pair entries: (off, len,
+// mask_off, first mask word).  The forward's streams run in rounds whose last rows are marked
+// in a bit mask (bit r of word r / 32 at `mask_off`; the first word is also kept in the
+// entry); the backward's streams end rows per lane (mask fields unused).
 struct FastPlanDev {
   int enabled = 0;
-  const int2* fwd_pl = nullptr;       // v = C z, per output pair: (first stream row, rows)
+  const int4* fwd_pl = nullptr;       // v = C z, per output pair
   const uint32_t* fwd_st = nullptr;   // slot words; slot (row r, lane l) is coefficient slot 64 r + l
   const int* pad = nullptr;           // coefficient slots that hold no entry
   int npad = 0;
-  const int2* bwd_pl = nullptr;       // dC and q = C^T u, per input pair: (first stream row, rows)
+  const int4* bwd_pl = nullptr;       // dC and q = C^T u, per input pair
+  const uint32_t* fwd_em = nullptr;   // round-end masks of the forward streams
   const uint2* bwd_st = nullptr;      // (slot word, plan index)
   int bwd_slots = 0;                  // 64 * backward stream rows = dC partials per tile
   float* coef_bwd = nullptr;          // [batch][bwd_slots + 256]: c in backward slot order
@@ -150,11 +154,13 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
                          hipStream_t s);
 constexpr int kFastTileTokens = 8;
 
-// Slot words of the 128-wide kernels' entry streams: end-of-row flag (bit 0), valid flag
-// (bit 1), the byte offset of the source row in the LDS coefficient array (rows of 16 bytes;
-// bits 4..19) and the byte offset of the destination in the pair tile (rows of 32 bytes, one
-// per coefficient, holding both blocks' 8 tokens; bits 20..31).  Stream row r, lane l of a pair whose rows start at `off` (a multiple
-// of 4) is slot 64 off + 256 (r / 4) + 4 l + r % 4: each lane's four consecutive rows are
+// Slot words of the 128-wide kernels' entry streams: end flag (bit 0: the lane's row ends at
+// this slot in the backward, or with the round that ends at this slot in the forward), valid flag (bit 1: the slot holds an entry;
+// padding slots have zero coefficients), the byte offset of the source row in the LDS
+// coefficient array (rows of 16 bytes; bits 4..19) and the byte offset of the lane's current
+// row in the pair tile (rows of 32 bytes, one per coefficient, holding both blocks' 8 tokens;
+// bits 20..31).  Stream row r, lane l of a pair whose rows start at `off` (a multiple of 4)
+// is slot 64 off + 256 (r / 4) + 4 l + r % 4: each lane's four consecutive rows are
 // contiguous, so a wave loads them with one 16-byte load per lane.
 constexpr uint32_t kSlotEnd = 1u;
 constexpr uint32_t kSlotValid = 2u;

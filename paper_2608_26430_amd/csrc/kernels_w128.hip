@@ -292,25 +292,45 @@ __device__ __forceinline__ u32x4 lds_at(const unsigned char* base, unsigned byte
 __device__ __forceinline__ unsigned tile_off(unsigned e) { return e >> kSlotDstShift; }
 
 // The scaled coefficient of a slot as the two multiplier words of v_dot2_f32_bf16, (s c, 0) and
-// (0, s c).  Slots that hold no entry come after a lane's last row end in every stream, so
-// whatever they accumulate is never written and needs no mask.
+// (0, s c).  Padding slots have zero coefficients and add nothing.
 __device__ __forceinline__ void coef_words(float c, float scale, unsigned& ce, unsigned& co) {
-  ce = pack_bf2(c * scale, 0.f);
-  co = ce << 16;
+  // one conversion with a constant zero low half (the compiler builds (0, x) from two words)
+  asm("v_cvt_pk_bf16_f32 %0, 0, %1" : "=v"(co) : "v"(c * scale));
+  ce = co >> 16;
 }
 
 __device__ __forceinline__ float dot2(unsigned a, unsigned b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
 }
 
-// a[t] += c z[t] for the 8 tokens of one source row; at the end of a row of the product, write
-// it to the tile row named by the slot word and restart.
-__device__ __forceinline__ void accum_row(unsigned e, unsigned ce, unsigned co, const u32x4 zv, unsigned char* tile,
-                                          float (&a)[8]) {
+// a[t] += c z[t] for the 8 tokens of one source row.  At a round end (`end`, the same on every
+// lane) every lane writes its current row to the tile position named by its slot word, and
+// restarts it if the row ends with this round (a row that goes on is written again later).
+__device__ __forceinline__ void accum_slot(unsigned e, unsigned ce, unsigned co, const u32x4 zv, bool end,
+                                           unsigned char* tile, float (&a)[8]) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     // copy the element out first: bit-casting a vector element expression directly reads
     // element 0 with this compiler
+    const unsigned w = zv[j];
+    a[2 * j] = dot2(w, ce, a[2 * j]);
+    a[2 * j + 1] = dot2(w, co, a[2 * j + 1]);
+  }
+  if (end) {
+    *reinterpret_cast<u32x4*>(tile + tile_off(e)) =
+        u32x4{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(a[4], a[5]), pack_bf2(a[6], a[7])};
+    const bool restart = e & kSlotEnd;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) a[j] = restart ? 0.f : a[j];
+  }
+}
+
+// a[t] += c z[t] for the 8 tokens of one source row; at the end of the lane's row, write it to
+// the tile position named by the slot word and restart (the backward's streams).
+__device__ __forceinline__ void accum_row(unsigned e, unsigned ce, unsigned co, const u32x4 zv, unsigned char* tile,
+                                          float (&a)[8]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
     const unsigned w = zv[j];
     a[2 * j] = dot2(w, ce, a[2 * j]);
     a[2 * j + 1] = dot2(w, co, a[2 * j + 1]);
@@ -321,6 +341,15 @@ __device__ __forceinline__ void accum_row(unsigned e, unsigned ce, unsigned co, 
 #pragma unroll
     for (int j = 0; j < 8; ++j) a[j] = 0.f;
   }
+}
+
+// Round-end bits of stream rows k0 .. k0+31 of a pair (bit i: row k0 + i ends a round).  Row
+// mask words beyond the first come from the mask table (scalar loads: uniform address).
+__device__ __forceinline__ unsigned chunk_ends(const int4& q, const unsigned* __restrict__ em, int k0) {
+  if (k0 == 0) return (unsigned)q.w;
+  const unsigned* w = em + q.z + (k0 >> 5);
+  const unsigned long long m = (unsigned long long)w[0] | ((unsigned long long)w[1] << 32);
+  return (unsigned)(m >> (k0 & 31));
 }
 
 // ---------------------------------------------------------------- forward stream chunks
@@ -348,9 +377,10 @@ __device__ __forceinline__ void fwd_load(const unsigned* __restrict__ st, int of
   }
 }
 
-// The first n (uniform, a multiple of 4) slots of a loaded chunk; all kCh LDS rows are read first.
-__device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int n, float scale, const unsigned char* zL,
-                                            unsigned char* tile, float (&a)[8]) {
+// The first n (uniform, a multiple of 4) slots of a loaded chunk, with their round-end bits;
+// all kCh LDS rows are read first.
+__device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int n, unsigned ends, float scale,
+                                            const unsigned char* zL, unsigned char* tile, float (&a)[8]) {
   u32x4 zv[kCh];
 #pragma unroll
   for (int i = 0; i < kCh; ++i) zv[i] = lds_at(zL, ch.en[i] & kSlotSrcMask);
@@ -359,7 +389,7 @@ __device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int n, float sca
     if (i < n) {   // uniform
       unsigned ce, co;
       coef_words(ch.cc[i], scale, ce, co);
-      accum_row(ch.en[i], ce, co, zv[i], tile, a);
+      accum_slot(ch.en[i], ce, co, zv[i], (ends >> i) & 1u, tile, a);
     }
   }
 }
@@ -511,8 +541,9 @@ __device__ __forceinline__ void analysis_phase(const Frag& F, const u16* rows, l
 // The stream tables are separate restrict-qualified arguments: the kernel never writes them,
 // so their wave-uniform reads become scalar loads, which do not wait for vector stores.
 template <bool BETA>
-__global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int2* __restrict__ pl,
-                                                      const unsigned* __restrict__ fst) {
+__global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __restrict__ pl,
+                                                      const unsigned* __restrict__ fst,
+                                                      const unsigned* __restrict__ em) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* zL = smem;                                        // n rows x 8 tokens x 2 bytes
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -528,7 +559,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int2* __
   frag_fetch(a.frag, fr);
   issue_point();
   // first stream chunk of this wave's first output pair, in flight during the analysis
-  int2 q = pl[min(wave, lastp)];
+  int4 q = pl[min(wave, lastp)];
   FwdChunk ch;
   fwd_load(fst, q.x, q.y, 0, cv, lane, ch);
   issue_point();
@@ -542,18 +573,18 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int2* __
   // a whole pair ahead of its use.  The loop runs two pairs per iteration with the buffers'
   // roles swapped, so no chunk is ever copied between registers.
   auto pair = [&](int p, FwdChunk& cur, FwdChunk& nxt) {
-    const int2 qn = pl[min(p + kWaves, lastp)];
+    const int4 qn = pl[min(p + kWaves, lastp)];
     fwd_load(fst, qn.x, qn.y, 0, cv, lane, nxt);
     issue_point();
     // v = C z for this pair into the tile
     const int off = q.x, len = q.y;
     zero_tile(tile, lane);
     float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    fwd_compute(cur, min(kCh, len), a.scale, zL, tile, acc8);
+    fwd_compute(cur, min(kCh, len), (unsigned)q.w, a.scale, zL, tile, acc8);
     if (len > kCh) {   // long stream
       for (int k0 = kCh; k0 < len; k0 += kCh) {
         fwd_load(fst, off, len, k0, cv, lane, cur);
-        fwd_compute(cur, min(kCh, len - k0), a.scale, zL, tile, acc8);
+        fwd_compute(cur, min(kCh, len - k0), chunk_ends(q, em, k0), a.scale, zL, tile, acc8);
       }
       vm_wait_all();
     }
@@ -575,7 +606,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int2* __
 }
 
 template <bool DX, bool DC, bool BETA>
-__global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __restrict__ pl,
+__global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __restrict__ pl,
                                                       const uint2* __restrict__ bst) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* uL = smem;                                        // m rows x 8 tokens x 2 bytes
@@ -600,7 +631,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
   frag_fetch(a.frag, fr);
   issue_point();
   // this wave's first input pair: stream entries and x in flight during the analysis of g
-  int2 q = pl[min(wave, lastp)];
+  int4 q = pl[min(wave, lastp)];
   BwdEntries ch;
   bwd_load_entries(bst + (long)q.x * 64, q.y, 0, lane, ch);
   u32x4 bx[kKT];
@@ -619,7 +650,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
     auto pair = [&](int p, BwdEntries& ch, BwdEntries& chn) {
       const int len = q.y;
       const uint2* st = bst + (long)q.x * 64;
-      const int2 qn = pl[min(p + kWaves, lastp)];
+      const int4 qn = pl[min(p + kWaves, lastp)];
       bwd_load_entries(bst + (long)qn.x * 64, qn.y, 0, lane, chn);
       issue_point();
       // z = P_in^T x for this pair (tile columns past the tile's end zeroed), then this
@@ -664,7 +695,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int2* __
       const int len = q.y;
       const uint2* st = bst + (long)q.x * 64;
       const float* cbp = cbw + (long)q.x * 64;
-      const int2 qn = pl[min(p + kWaves, lastp)];
+      const int4 qn = pl[min(p + kWaves, lastp)];
       bwd_load_entries(bst + (long)qn.x * 64, qn.y, 0, lane, chn);
       bwd_load_coeffs(cbw + (long)qn.x * 64, qn.y, 0, lane, ccn);
       issue_point();
@@ -825,9 +856,11 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   take_timing_events(&e0, &e1);
   rec(e0, s);
   if (beta != 0.f)
-    hipLaunchKernelGGL(fwd128<true>, grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st);
+    hipLaunchKernelGGL(fwd128<true>, grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st,
+                       p->fast.fwd_em);
   else
-    hipLaunchKernelGGL(fwd128<false>, grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st);
+    hipLaunchKernelGGL(fwd128<false>, grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st,
+                       p->fast.fwd_em);
   rec(e1, s);
   return hipGetLastError();
 }
@@ -871,7 +904,7 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   if (T > 0 && (want_dx || want_dc)) {
     const dim3 grid((unsigned)ntiles, (unsigned)count);
     const size_t lds = fast128_lds_bytes(a.nblk_out);
-    const int2* pl = p->fast.bwd_pl;
+    const int4* pl = p->fast.bwd_pl;
     const uint2* st = p->fast.bwd_st;
     const bool beta = beta_dx != 0.f;
     rec(e0, s);

@@ -8,6 +8,7 @@
 // so every table stores LDS element offsets r*(W + pad) + 2i + s directly.
 #include <algorithm>
 #include <cstring>
+#include <functional>
 #include <memory>
 #include <numeric>
 
@@ -47,8 +48,8 @@ uint32_t tile_byte(int par, int local) {
 }
 
 // Rows of one pair of blocks assigned whole to 64 lanes, longest first, each to the least
-// loaded lane; lanes are then renumbered by decreasing load, so in every stream row the
-// occupied slots are a prefix of the lanes.  Returns, per lane, its rows in order.
+// loaded lane (the backward's order: every row end is tested per lane).  Returns, per lane,
+// its rows in order, and the largest lane load.
 std::vector<std::vector<int>> assign_lanes(const std::vector<int>& row_size, int& len) {
   std::vector<int> order;
   for (int r = 0; r < (int)row_size.size(); ++r)
@@ -61,6 +62,7 @@ std::vector<std::vector<int>> assign_lanes(const std::vector<int>& row_size, int
     lane_rows[l].push_back(r);
     load[l] += row_size[r];
   }
+  // lanes renumbered by decreasing load: in every stream row the occupied slots are a prefix
   std::vector<int> lanes(64);
   std::iota(lanes.begin(), lanes.end(), 0);
   std::stable_sort(lanes.begin(), lanes.end(), [&](int a, int b) { return load[a] > load[b]; });
@@ -68,6 +70,162 @@ std::vector<std::vector<int>> assign_lanes(const std::vector<int>& row_size, int
   for (int l = 0; l < 64; ++l) out[l] = lane_rows[lanes[l]];
   len = load[lanes[0]];
   return out;
+}
+
+// Round schedule of the rows of one pair of blocks for the 128-wide forward kernel.  All 64 lanes of
+// a wave run the same rounds, of L[0..R-1] slots; at the end of every round each lane writes
+// its current row to the pair tile, so row ends cost no per-slot test.  A row fills one or
+// more consecutive rounds of one lane, the rest of its last round being padding slots with
+// zero coefficients; a lane whose rows are done rewrites its last row.
+struct Span {
+  int row, first, last;   // rounds first..last of one lane
+};
+struct PairSchedule {
+  std::vector<int> L;
+  std::vector<std::vector<Span>> lanes = std::vector<std::vector<Span>>(64);
+};
+
+// Rows (longest first) each to the lane where they end in the earliest round, then with the
+// least padding, then the lowest lane; every lane's rounds fill from round 0.  Returns false
+// when some row fits on no lane.
+bool place_rows(const std::vector<int>& rows, const std::vector<int>& size, const std::vector<int>& L,
+                std::vector<std::vector<Span>>* lanes) {
+  const int R = (int)L.size();
+  std::vector<int> cum(R + 1, 0);
+  for (int j = 0; j < R; ++j) cum[j + 1] = cum[j] + L[j];
+  // free[f]: lanes whose first free round is f, highest index first
+  std::vector<std::vector<int>> free(R + 1);
+  for (int l = 63; l >= 0; --l) free[0].push_back(l);
+  for (int r : rows) {
+    int bb = -1, bw = 0, bf = -1;
+    for (int f = 0; f < R; ++f) {
+      if (free[f].empty()) continue;
+      const int idx = (int)(std::lower_bound(cum.begin(), cum.end(), cum[f] + size[r]) - cum.begin());
+      if (idx > R) continue;
+      const int b = idx - 1, w = cum[idx] - cum[f] - size[r];
+      if (bf < 0 || b < bb || (b == bb && (w < bw || (w == bw && free[f].back() < free[bf].back())))) {
+        bb = b;
+        bw = w;
+        bf = f;
+      }
+    }
+    if (bf < 0) return false;
+    const int lane = free[bf].back();
+    free[bf].pop_back();
+    auto& dst = free[bb + 1];
+    dst.insert(std::upper_bound(dst.begin(), dst.end(), lane, std::greater<int>()), lane);
+    if (lanes) (*lanes)[lane].push_back({r, bf, bb});
+  }
+  return true;
+}
+
+// Round lengths: the longest row of each group of 64 rows (always placeable), then shortened
+// or dropped by local search while the modelled cost falls: `slot_cost` per slot of the
+// stream (whole 4-slot groups), `end_cost` per round.
+PairSchedule schedule_pair(const std::vector<int>& size, int slot_cost, int end_cost) {
+  PairSchedule ps;
+  std::vector<int> rows;
+  for (int r = 0; r < (int)size.size(); ++r)
+    if (size[r] > 0) rows.push_back(r);
+  std::stable_sort(rows.begin(), rows.end(), [&](int a, int b) { return size[a] > size[b]; });
+  if (rows.empty()) return ps;
+  std::vector<int> L;
+  for (size_t j = 0; j < rows.size(); j += 64) L.push_back(size[rows[j]]);
+  struct Cost {
+    int64_t model, sum, rounds;
+    bool operator<(const Cost& o) const {
+      return model != o.model ? model < o.model : sum != o.sum ? sum < o.sum : rounds < o.rounds;
+    }
+  };
+  auto cost = [&](const std::vector<int>& v) {
+    const int64_t sum = std::accumulate(v.begin(), v.end(), (int64_t)0);
+    return Cost{slot_cost * std::max<int64_t>((sum + 3) / 4 * 4, 4) + end_cost * (int64_t)v.size(), sum,
+                (int64_t)v.size()};
+  };
+  Cost best = cost(L);
+  for (int iter = 0; iter < 4096; ++iter) {
+    std::vector<std::vector<int>> cand;
+    for (size_t j = 0; j < L.size(); ++j) {
+      if (L[j] > 1) {
+        std::vector<int> m = L;
+        --m[j];
+        cand.push_back(m);
+        for (int t = 1; t <= 3; ++t) {
+          cand.push_back(m);
+          cand.back().push_back(t);
+        }
+      }
+      if (L.size() > 1) {
+        cand.push_back(L);
+        cand.back().erase(cand.back().begin() + (long)j);
+      }
+    }
+    std::stable_sort(cand.begin(), cand.end(),
+                     [&](const std::vector<int>& a, const std::vector<int>& b) { return cost(a) < cost(b); });
+    bool moved = false;
+    for (const auto& m : cand) {
+      const Cost c = cost(m);
+      if (!(c < best)) break;
+      if (place_rows(rows, size, m, nullptr)) {
+        L = m;
+        best = c;
+        moved = true;
+        break;
+      }
+    }
+    if (!moved) break;
+  }
+  ps.L = L;
+  place_rows(rows, size, L, &ps.lanes);
+  return ps;
+}
+
+// Slot words of one pair's stream under its schedule, lane by lane: `entries[r]` are the
+// entries of row r, `word(e)` an entry's source-row bits, `dst(r)` row r's tile bits; `put`
+// receives (stream row k, lane, word, entry or -1).  Returns the stream length (whole 4-row
+// groups, at least one), or -1 if a lane holds no row and the pair has no empty row, and sets
+// the round-end mask words.
+template <class Word, class Dst, class Put>
+int emit_pair(const PairSchedule& ps, const std::vector<std::vector<int>>& entries, Word word, Dst dst, Put put,
+              std::vector<uint32_t>& mask) {
+  const int R = (int)ps.L.size();
+  std::vector<int> cum(R + 1, 0);
+  for (int j = 0; j < R; ++j) cum[j + 1] = cum[j] + ps.L[j];
+  const int len = std::max((cum[R] + 3) / 4 * 4, 4);
+  mask.assign((size_t)(len + 31) / 32 + 1, 0u);
+  for (int j = 0; j < R; ++j) mask[(size_t)(cum[j + 1] - 1) / 32] |= 1u << ((cum[j + 1] - 1) % 32);
+  auto is_end = [&](int k) { return (mask[(size_t)k / 32] >> (k % 32)) & 1u; };
+  int empty_row = -1;   // a row with no entries, for lanes that hold no row
+  for (int r = 0; r < (int)entries.size() && empty_row < 0; ++r)
+    if (entries[r].empty()) empty_row = r;
+  for (int l = 0; l < 64; ++l) {
+    const auto& sp = ps.lanes[l];
+    if (sp.empty()) {
+      if (empty_row < 0) return -1;
+      for (int k = 0; k < len; ++k) put(k, l, is_end(k) ? dst(empty_row) : 0u, -1);
+      continue;
+    }
+    int k = 0;
+    for (size_t j = 0; j < sp.size(); ++j) {
+      const Span& s = sp[j];
+      const int stop = cum[s.last + 1];
+      const auto& ent = entries[s.row];
+      // the last row is not restarted: the lane's later round ends write it again
+      const uint32_t restart = j + 1 < sp.size() ? ff::kSlotEnd : 0u;
+      for (; k < stop; ++k) {
+        const int i = k - cum[s.first];
+        const bool has = i < (int)ent.size();
+        // padding slots name the row only where a round ends (elsewhere their reads all go to
+        // offset 0, one LDS broadcast)
+        put(k, l,
+            has ? word(ent[i]) | ff::kSlotValid | dst(s.row) | (k == stop - 1 ? restart : 0u)
+                : (is_end(k) ? dst(s.row) | (k == stop - 1 ? restart : 0u) : 0u),
+            has ? ent[i] : -1);
+      }
+    }
+    for (; k < len; ++k) put(k, l, is_end(k) ? dst(sp.back().row) : 0u, -1);   // rewrites of the last row
+  }
+  return len;
 }
 
 }  // namespace
@@ -204,7 +362,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
                     f_in->transpose_is_sign_flip && f_in->half_shift_sign && f_in->B == f_out->B &&
                     n < 65536 && m < 65536 &&
                     ff::fast128_lds_bytes(std::max(FI.nblk, FO.nblk)) <= (size_t)ff::kMaxLdsBytes;
-  std::vector<int2> f_pl, b_pl;   // per pair: (first stream row, stream rows)
+  std::vector<int4> f_pl, b_pl;   // per pair: (first stream row, stream rows, mask offset, mask word 0)
+  std::vector<uint32_t> f_em;   // round-end masks of the forward streams
   std::vector<int> pad_slots;
   std::vector<uint32_t> f_st;
   std::vector<uint2> b_st;
@@ -213,7 +372,6 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   if (fast) {
     // byte offset of a coefficient's row in the LDS array of a whole side, and its row in a pair tile
     auto lsrc = [&](const Loc& l) { return (uint32_t)(l.blk * 128 + l.local) * 16u; };
-    auto tbyte = [&](const Loc& l) { return tile_byte(l.blk & 1, l.local); };
     const int npo = FO.nblk / 2, npi = FI.nblk / 2;
     // entries of each destination row r = (block parity)*128 + local of a pair
     std::vector<std::vector<std::vector<int>>> frows(npo, std::vector<std::vector<int>>(256)),
@@ -222,29 +380,36 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       frows[rloc[e].blk / 2][(rloc[e].blk & 1) * 128 + rloc[e].local].push_back((int)e);
       brows[cloc[e].blk / 2][(cloc[e].blk & 1) * 128 + cloc[e].local].push_back((int)e);
     }
+    // modelled VALU work per slot and per round end of the two kernels' sparse phases
+    constexpr int kFwdSlotCost = 11, kEndCost = 15;
+    std::vector<uint32_t> mask;
     for (int pp = 0; pp < npo; ++pp) {
       std::vector<int> sz(256);
       for (int r = 0; r < 256; ++r) sz[r] = (int)frows[pp][r].size();
-      int len = 0;
-      const auto lanes = assign_lanes(sz, len);
-      len = std::max((len + 3) / 4 * 4, 4);   // whole 4-row groups; every stream has one
+      const PairSchedule ps = schedule_pair(sz, kFwdSlotCost, kEndCost);
       const size_t row0 = f_st.size() / 64;
-      f_pl.push_back(make_int2((int)row0, len));
-      f_st.resize(f_st.size() + (size_t)len * 64, 0u);
-      user_of_slot.resize(f_st.size(), -1);
-      for (int l = 0; l < 64; ++l) {
-        int k = 0;
-        for (int r : lanes[l])
-          for (size_t i = 0; i < frows[pp][r].size(); ++i, ++k) {
-            const int e = frows[pp][r][i];
-            const bool last = i + 1 == frows[pp][r].size();
-            const uint32_t dst = tile_byte(r >> 7, r & 127);
+      // at most 64 x 256 x 2^15 slots per stream keep every offset in an int
+      const int len = emit_pair(
+          ps, frows[pp], [&](int e) { return lsrc(cloc[e]); },
+          [&](int r) { return tile_byte(r >> 7, r & 127) << ff::kSlotDstShift; },
+          [&](int k, int l, uint32_t w, int e) {
             const size_t slot = (size_t)ff::fast_slot((int64_t)row0, k, l);
-            f_st[slot] = lsrc(cloc[e]) | (dst << ff::kSlotDstShift) | ff::kSlotValid | (last ? ff::kSlotEnd : 0u);
-            user_of_slot[slot] = e;
-            slot_of_user[e] = (int)slot;
-          }
-      }
+            if (slot >= f_st.size()) {
+              f_st.resize(slot / 256 * 256 + 256, 0u);
+              user_of_slot.resize(f_st.size(), -1);
+            }
+            f_st[slot] = w;
+            if (e >= 0) {
+              user_of_slot[slot] = e;
+              slot_of_user[e] = (int)slot;
+            }
+          },
+          mask);
+      if (len < 0) return ff::fail(FF_EUNSUPPORTED, "internal: no row for a lane of output pair %d", pp);
+      f_pl.push_back(make_int4((int)row0, len, (int)f_em.size(), (int)mask[0]));
+      f_em.insert(f_em.end(), mask.begin(), mask.end());
+      f_st.resize((row0 + (size_t)len) * 64, 0u);
+      user_of_slot.resize(f_st.size(), -1);
     }
     for (size_t j = 0; j < user_of_slot.size(); ++j)
       if (user_of_slot[j] < 0) pad_slots.push_back((int)j);
@@ -254,9 +419,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       for (int r = 0; r < 256; ++r) sz[r] = (int)brows[pp][r].size();
       int len = 0;
       const auto lanes = assign_lanes(sz, len);
-      len = std::max((len + 3) / 4 * 4, 4);
+      len = std::max((len + 3) / 4 * 4, 4);   // whole 4-row groups; every stream has one
       const int64_t row0 = (int64_t)(b_st.size() / 64);
-      b_pl.push_back(make_int2((int)row0, len));
+      b_pl.push_back(make_int4((int)row0, len, 0, 0));
       b_st.resize(b_st.size() + (size_t)len * 64, make_uint2(0u, 0u));
       for (int l = 0; l < 64; ++l) {
         int k = 0;
@@ -266,7 +431,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
             const bool last = i + 1 == brows[pp][r].size();
             bwd_slot_of_user[e] = (int)ff::fast_slot(row0, k, l);
             b_st[(size_t)ff::fast_slot(row0, k, l)] = make_uint2(
-                lsrc(rloc[e]) | (tbyte(cloc[e]) << ff::kSlotDstShift) | ff::kSlotValid |
+                lsrc(rloc[e]) | (tile_byte(r >> 7, r & 127) << ff::kSlotDstShift) | ff::kSlotValid |
                     (last ? ff::kSlotEnd : 0u),
                 (unsigned)slot_of_user[e]);
           }
@@ -315,13 +480,14 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       {bwd_ptr.data(), (n + 1) * sizeof(int)},      {bwd_ent.data(), bwd_ent.size() * sizeof(int2)},
       {sdd.data(), sdd.size() * sizeof(int2)},       {mrg_ptr.data(), (nb + 1) * sizeof(int)},
       {mrg_ent.data(), mrg_ent.size() * sizeof(int4)},
-      {f_pl.data(), f_pl.size() * sizeof(int2)},      {b_pl.data(), b_pl.size() * sizeof(int2)},
+      {f_pl.data(), f_pl.size() * sizeof(int4)},      {b_pl.data(), b_pl.size() * sizeof(int4)},
       {f_st.data(), f_st.size() * sizeof(uint32_t)},  {pad_slots.data(), pad_slots.size() * sizeof(int)},
       {b_st.data(), b_st.size() * sizeof(uint2)},
       {nullptr, std::max<size_t>(partial_elems, 1) * sizeof(float)},
       // the backward's coefficients in its stream's slot order, per adapter (+ a scratch group)
       {nullptr, std::max<size_t>((size_t)max_batch * (b_st.size() + 256), 1) * sizeof(float)},
-      {bwd_pos.data(), bwd_pos.size() * sizeof(int)}};
+      {bwd_pos.data(), bwd_pos.size() * sizeof(int)},
+      {f_em.data(), f_em.size() * sizeof(uint32_t)}};
   size_t total = 0;
   for (const Blob& b : blobs) total += up(b.bytes);
   int cur = 0;
@@ -345,6 +511,12 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       where.push_back(dst);
     }
   }
+  // the backward's padding slots keep zero coefficients: the per-call copy writes only the
+  // slots that hold entries
+  if (hipMemset(where[15], 0, blobs[15].bytes) != hipSuccess) {
+    (void)hipFree(mem);
+    return ff::fail(FF_EDEVICE, "clearing the plan workspace failed");
+  }
   ff::PlanDev& pd = p->dev;
   pd.fwd_slot_off = (const int*)where[0];
   pd.fwd_ptr = (const int*)where[1];
@@ -361,8 +533,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   pd.nnz = (int)nslot;
   ff::FastPlanDev& fp = p->fast;
   fp.enabled = fast ? 1 : 0;
-  fp.fwd_pl = (const int2*)where[9];
-  fp.bwd_pl = (const int2*)where[10];
+  fp.fwd_pl = (const int4*)where[9];
+  fp.bwd_pl = (const int4*)where[10];
+  fp.fwd_em = (const uint32_t*)where[17];
   fp.fwd_st = (const uint32_t*)where[11];
   fp.pad = (const int*)where[12];
   fp.npad = (int)pad_slots.size();

@@ -125,13 +125,16 @@ def main():
     dX = torch.empty((T, n), dtype=tdt, device=dev)
     dC = torch.empty((plan.coef_slots,), dtype=torch.float32, device=dev)
 
+    # a training step: the forward also leaves the coefficients in the backward's order
+    saved = plan.new_saved(dev)
+
     def step(evs=None):
         if evs is not None:
             ff.binding.time_next_kernel(evs[0], evs[1])
-        ff.adapter_fwd(plan, X, c, data.scale, Y=Y)
+        ff.adapter_fwd(plan, X, c, data.scale, Y=Y, save=saved)
         if evs is not None:
             ff.binding.time_next_kernel(evs[2], evs[3])
-        ff.adapter_bwd(plan, X, G, c, data.scale, dX=dX, dC=dC)
+        ff.adapter_bwd(plan, X, G, c, data.scale, dX=dX, dC=dC, saved=saved)
 
     for _ in range(args.warmup):
         step()

@@ -59,6 +59,8 @@ def _load():
         "ff_plan_order": (i32, [vp, ctypes.POINTER(i64)]),
         "ff_adapter_fwd": (i32, [vp, i64, i32, vp, i64, vp, f32, f32, vp, i64, vp]),
         "ff_adapter_bwd": (i32, [vp, i64, i32, vp, i64, vp, i64, vp, f32, f32, vp, i64, i32, vp, vp]),
+        "ff_adapter_fwd_save": (i32, [vp, i64, i32, vp, i64, vp, f32, f32, vp, i64, vp, vp]),
+        "ff_adapter_bwd_saved": (i32, [vp, i64, i32, vp, i64, vp, i64, vp, vp, f32, f32, vp, i64, i32, vp, vp]),
         "ff_merge_delta": (i32, [vp, vp, f32, i32, f32, vp, i64, vp]),
         "ff_adapter_fwd_batched": (i32, [vp, i64, i64, i32, vp, i64, vp, f32, f32, vp, i64, vp]),
         "ff_adapter_bwd_batched": (i32, [vp, i64, i64, i32, vp, i64, vp, i64, vp, f32, f32, vp, i64, i32,
@@ -181,6 +183,17 @@ class Plan:
         return self.query(5)
 
     @property
+    def saved_floats(self) -> int:
+        """Length of the c_saved arrays of adapter_fwd(save=...) / adapter_bwd(saved=...) (0: none needed)."""
+        return self.query(6)
+
+    def new_saved(self, device=None):
+        """A c_saved array for one adapter of this plan (None when the plan needs none)."""
+        torch = _torch()
+        n = self.saved_floats
+        return torch.empty((n,), dtype=torch.float32, device=device or "cuda") if n else None
+
+    @property
     def order(self) -> np.ndarray:
         """User index of the support entry in each coefficient slot, -1 for padding:
         c_plan[j] = c_user[order[j]] where order[j] >= 0, dC_user[order[j]] = dC_plan[j]."""
@@ -261,8 +274,10 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def adapter_fwd(plan: Plan, X, c_vals, scale: float, Y=None, beta: float = 0.0, stream=None):
-    """Y = beta*Y + scale * P_out C P_in^T x for each token row of X; returns Y."""
+def adapter_fwd(plan: Plan, X, c_vals, scale: float, Y=None, beta: float = 0.0, stream=None, save=None):
+    """Y = beta*Y + scale * P_out C P_in^T x for each token row of X; returns Y.  With `save` (a
+    c_saved array, Plan.new_saved) the forward also stores the coefficients in the backward's
+    order, for adapter_bwd(saved=...) with the same c_vals (ff_adapter_fwd_save)."""
     torch = _torch()
     T = X.shape[0]
     if Y is None:
@@ -273,14 +288,21 @@ def adapter_fwd(plan: Plan, X, c_vals, scale: float, Y=None, beta: float = 0.0, 
     yp, ldy = _mat(Y, "Y")
     if Y.dtype != X.dtype or Y.shape[0] != T:
         raise ValueError("Y must match X in dtype and token count")
-    _check(_load().ff_adapter_fwd(plan.handle, T, _act_code(X), xp, ldx, _vec(c_vals, "c_vals", plan.coef_slots), scale,
-                                  beta, yp, ldy, _stream(stream)))
+    cp = _vec(c_vals, "c_vals", plan.coef_slots)
+    if save is not None:
+        _check(_load().ff_adapter_fwd_save(plan.handle, T, _act_code(X), xp, ldx, cp, scale, beta, yp, ldy,
+                                           _vec(save, "save", plan.saved_floats), _stream(stream)))
+    else:
+        _check(_load().ff_adapter_fwd(plan.handle, T, _act_code(X), xp, ldx, cp, scale, beta, yp, ldy,
+                                      _stream(stream)))
     return Y
 
 
 def adapter_bwd(plan: Plan, X, G, c_vals, scale: float, dX=None, dC=None, beta_dx: float = 0.0,
-                accumulate_dc: bool = False, want_dx: bool = True, want_dc: bool = True, stream=None):
-    """Backward of adapter_fwd for upstream gradient G: returns (dX, dC) (None where not wanted)."""
+                accumulate_dc: bool = False, want_dx: bool = True, want_dc: bool = True, stream=None,
+                saved=None):
+    """Backward of adapter_fwd for upstream gradient G: returns (dX, dC) (None where not wanted).
+    `saved`: the c_saved array of adapter_fwd(save=...) with the same c_vals (ff_adapter_bwd_saved)."""
     torch = _torch()
     T = G.shape[0]
     act = _act_code(G)
@@ -296,10 +318,14 @@ def adapter_bwd(plan: Plan, X, G, c_vals, scale: float, dX=None, dC=None, beta_d
     xp, ldx = _mat(X, "X") if X is not None else (None, plan.n)
     dxp, lddx = _mat(dX, "dX") if want_dx else (None, plan.n)
     dcp = _vec(dC, "dC", plan.coef_slots) if want_dc else None
-    _check(_load().ff_adapter_bwd(plan.handle, T, act, xp, ldx, gp, ldg,
-                                  _vec(c_vals, "c_vals", plan.coef_slots) if c_vals is not None else None,
-                                  scale, beta_dx,
-                                  dxp, lddx, int(accumulate_dc), dcp, _stream(stream)))
+    cp = _vec(c_vals, "c_vals", plan.coef_slots) if c_vals is not None else None
+    if saved is not None:
+        _check(_load().ff_adapter_bwd_saved(plan.handle, T, act, xp, ldx, gp, ldg, cp,
+                                            _vec(saved, "saved", plan.saved_floats), scale, beta_dx,
+                                            dxp, lddx, int(accumulate_dc), dcp, _stream(stream)))
+    else:
+        _check(_load().ff_adapter_bwd(plan.handle, T, act, xp, ldx, gp, ldg, cp, scale, beta_dx,
+                                      dxp, lddx, int(accumulate_dc), dcp, _stream(stream)))
     return (dX if want_dx else None), (dC if want_dc else None)
 
 

@@ -109,7 +109,26 @@ ff_status ff_adapter_fwd(const ff_plan* p, int64_t T, int act, const void* X, in
   if (p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
   if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
   return launched(ff::launch_fwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, c_vals, nullptr, scale,
-                                 beta, {Y, nullptr}, ldy, (hipStream_t)stream),
+                                 beta, {Y, nullptr}, ldy, nullptr, (hipStream_t)stream),
+                  "forward launch");
+}
+
+ff_status ff_adapter_fwd_save(const ff_plan* p, int64_t T, int act, const void* X, int64_t ldx,
+                              const float* c_vals, float scale, float beta, void* Y, int64_t ldy,
+                              float* c_saved, void* stream) {
+  ff::clear_error();
+  ff_status st = check_common(p, T, act, 1);
+  if (st != FF_OK) return st;
+  const bool saves = act == FF_BF16 && p->fast.enabled;
+  if (!saves) return ff_adapter_fwd(p, T, act, X, ldx, c_vals, scale, beta, Y, ldy, stream);
+  if (!c_saved || (uintptr_t)c_saved % 16) return ff::fail(FF_EINVAL, "c_saved is NULL or not 16-byte aligned");
+  if (!c_vals || (uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is NULL or not 16-byte aligned");
+  if (T > 0) {
+    if ((st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
+    if ((st = check_act("Y", Y, ldy, p->fout->d, act)) != FF_OK) return st;
+  }
+  return launched(ff::launch_fwd(p, 1, 1, (int)T, {X, nullptr}, ldx, c_vals, nullptr, scale, beta, {Y, nullptr},
+                                 ldy, c_saved, (hipStream_t)stream),
                   "forward launch");
 }
 
@@ -134,7 +153,28 @@ ff_status ff_adapter_bwd(const ff_plan* p, int64_t T, int act, const void* X, in
   }
   return launched(ff::launch_bwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, {G, nullptr}, ldg, c_vals,
                                  nullptr, scale, beta_dx, {dX, nullptr}, lddx, want_dx, accumulate_dc, dC,
-                                 nullptr, want_dc, (hipStream_t)stream),
+                                 nullptr, want_dc, nullptr, (hipStream_t)stream),
+                  "backward launch");
+}
+
+ff_status ff_adapter_bwd_saved(const ff_plan* p, int64_t T, int act, const void* X, int64_t ldx,
+                               const void* G, int64_t ldg, const float* c_vals, const float* c_saved,
+                               float scale, float beta_dx, void* dX, int64_t lddx, int accumulate_dc,
+                               float* dC, void* stream) {
+  ff::clear_error();
+  ff_status st = check_common(p, T, act, 1);
+  if (st != FF_OK) return st;
+  if (!(act == FF_BF16 && p->fast.enabled) || T == 0 || !dX)
+    return ff_adapter_bwd(p, T, act, X, ldx, G, ldg, c_vals, scale, beta_dx, dX, lddx, accumulate_dc, dC, stream);
+  if (!c_saved || (uintptr_t)c_saved % 16) return ff::fail(FF_EINVAL, "c_saved is NULL or not 16-byte aligned");
+  const bool want_dc = dC != nullptr;
+  if (dC && ((uintptr_t)dC % 4)) return ff::fail(FF_EINVAL, "dC is not 4-byte aligned");
+  if ((st = check_act("G", G, ldg, p->fout->d, act)) != FF_OK) return st;
+  if (want_dc && (st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
+  if ((st = check_act("dX", dX, lddx, p->fin->d, act)) != FF_OK) return st;
+  return launched(ff::launch_bwd(p, 1, 1, (int)T, {X, nullptr}, ldx, {G, nullptr}, ldg, c_vals, nullptr, scale,
+                                 beta_dx, {dX, nullptr}, lddx, true, accumulate_dc, dC, nullptr, want_dc, c_saved,
+                                 (hipStream_t)stream),
                   "backward launch");
 }
 
@@ -166,7 +206,7 @@ ff_status ff_adapter_fwd_batched(const ff_plan* p, int64_t count, int64_t T, int
   if (ldx % mult || ldy % mult) return ff::fail(FF_EINVAL, "leading dimension not a multiple of %lld",
                                                 (long long)mult);
   return launched(ff::launch_fwd(p, act == FF_BF16, (int)count, (int)T, {nullptr, X}, ldx, nullptr, c_vals,
-                                 scale, beta, {nullptr, (const void* const*)Y}, ldy, (hipStream_t)stream),
+                                 scale, beta, {nullptr, (const void* const*)Y}, ldy, nullptr, (hipStream_t)stream),
                   "batched forward launch");
 }
 
@@ -192,7 +232,7 @@ ff_status ff_adapter_bwd_batched(const ff_plan* p, int64_t count, int64_t T, int
   }
   return launched(ff::launch_bwd(p, act == FF_BF16, (int)count, (int)T, {nullptr, X}, ldx, {nullptr, G}, ldg,
                                  nullptr, c_vals, scale, beta_dx, {nullptr, (const void* const*)dX}, lddx,
-                                 want_dx, accumulate_dc, nullptr, dC, want_dc, (hipStream_t)stream),
+                                 want_dx, accumulate_dc, nullptr, dC, want_dc, nullptr, (hipStream_t)stream),
                   "batched backward launch");
 }
 

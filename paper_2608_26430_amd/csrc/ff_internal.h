@@ -129,13 +129,15 @@ struct ActPtrs {          // one tensor: either a single pointer or a device arr
   const void* const* many;
 };
 
+// c_saved: the backward-ordered coefficient copy of the 128-wide path (written by the
+// forward, read by the backward instead of reordering c itself); NULL elsewhere.
 hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx,
                       const float* c, const float* const* cs, float scale, float beta,
-                      ActPtrs Y, int64_t ldy, hipStream_t s);
+                      ActPtrs Y, int64_t ldy, float* c_saved, hipStream_t s);
 hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx,
                       ActPtrs G, int64_t ldg, const float* c, const float* const* cs, float scale,
                       float beta_dx, ActPtrs dX, int64_t lddx, bool want_dx, int accumulate_dc,
-                      float* dC, float* const* dCs, bool want_dc, hipStream_t s);
+                      float* dC, float* const* dCs, bool want_dc, const float* c_saved, hipStream_t s);
 hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf16, float beta,
                         void* W, int64_t ldw, hipStream_t s);
 // Set the per-kernel dynamic LDS limits once per process.
@@ -147,11 +149,12 @@ size_t fast128_lds_bytes(int nblk);
 // Floats per tile of the fused backward's dC workspace for a plan with `bwd_slots` slots.
 size_t fast128_partial_floats(size_t bwd_slots);
 hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, const float* c,
-                         const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, hipStream_t s);
+                         const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, float* c_saved,
+                         hipStream_t s);
 hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G, int64_t ldg,
                          const float* c, const float* const* cs, float scale, float beta_dx, ActPtrs dX,
                          int64_t lddx, bool want_dx, int accumulate_dc, float* dC, float* const* dCs, bool want_dc,
-                         hipStream_t s);
+                         const float* c_saved, hipStream_t s);
 constexpr int kFastTileTokens = 8;
 
 // Slot words of the 128-wide kernels' entry streams: end flag (bit 0: the lane's row ends at

@@ -413,8 +413,9 @@ hipError_t configure_kernels() {
 }
 
 hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx, const float* c,
-                      const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, hipStream_t s) {
-  if (bf16 && p->fast.enabled) return launch_fwd128(p, count, T, X, ldx, c, cs, scale, beta, Y, ldy, s);
+                      const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, float* c_saved,
+                      hipStream_t s) {
+  if (bf16 && p->fast.enabled) return launch_fwd128(p, count, T, X, ldx, c, cs, scale, beta, Y, ldy, c_saved, s);
   FwdArgs a{};
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
@@ -453,10 +454,10 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
 hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G,
                       int64_t ldg, const float* c, const float* const* cs, float scale, float beta_dx,
                       ActPtrs dX, int64_t lddx, bool want_dx, int accumulate_dc, float* dC, float* const* dCs,
-                      bool want_dc, hipStream_t s) {
+                      bool want_dc, const float* c_saved, hipStream_t s) {
   if (bf16 && p->fast.enabled)
     return launch_bwd128(p, count, T, X, ldx, G, ldg, c, cs, scale, beta_dx, dX, lddx, want_dx, accumulate_dc, dC, dCs,
-                         want_dc, s);
+                         want_dc, c_saved, s);
   BwdArgs a{};
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;

@@ -497,6 +497,9 @@ struct FastArgs {
   const float* c;
   const float* const* cs;
   const float* cb;    // backward: coefficients in backward slot order, [batch][slots + 256]
+  float* csave;       // forward: where to write that copy, [batch][slots + 256]
+  const int* pos;     // per coefficient slot: its backward slot (padding: the scratch slot)
+  int nslot;          // coefficient slots (>= 256 on this path)
   float scale, beta;
   int slots;          // dC partials per tile
   int pstride;        // floats per tile in the partial workspace: slots + a scratch row group
@@ -555,6 +558,16 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   const float* cv = a.cs ? a.cs[bi] : a.c;
   const int npo = a.nblk_out / 2, lastp = npo - 1;
 
+  // This workgroup's share of the coefficient copy in the backward's slot order (read first,
+  // written after the analysis).  Every lane loads and stores: lanes past the share repeat its
+  // last slot, an identical write.
+  const int per = (a.nslot + (int)gridDim.x - 1) / (int)gridDim.x;
+  const int j0 = (int)blockIdx.x * per, jn = min(a.nslot, j0 + per);
+  const int js = max(min(j0 + (int)threadIdx.x, jn - 1), 0);
+  const int spos = gld(a.pos)[js];
+  const float sval = gld(cv)[js];
+  float* csave = a.csave + (long)bi * (a.slots + 256);
+
   u32x4 fr[kFragPerThread];
   frag_fetch(a.frag, fr);
   issue_point();
@@ -567,6 +580,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   Frag F;
   frag_stage(fr, reinterpret_cast<u32x4*>(smem), lane, F);
   analysis_phase(F, X, a.ldx, nt, a.nblk_in / 2, wave, lane, zL);
+  gst(csave)[spos] = sval;
   __syncthreads();
 
   // One output pair: its chunk is in `cur`; the next pair's chunk is loaded into `nxt` first,
@@ -603,6 +617,9 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
     pair(p, ch, ch2);
     if (p + kWaves < npo) pair(p + kWaves, ch2, ch);
   }
+  // shares longer than one slot per thread (grids of few tiles)
+  if (per > kThreads)
+    for (int j = j0 + kThreads + (int)threadIdx.x; j < jn; j += kThreads) gst(csave)[gld(a.pos)[j]] = gld(cv)[j];
 }
 
 template <bool DX, bool DC, bool BETA>
@@ -834,8 +851,15 @@ size_t fast128_lds_bytes(int nblk) {
 size_t fast128_partial_floats(size_t bwd_slots) { return bwd_slots + 256; }
 
 hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, const float* c,
-                         const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, hipStream_t s) {
+                         const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, float* c_saved,
+                         hipStream_t s) {
   FastArgs a{};
+  // the backward-ordered coefficient copy goes to the caller's buffer, or to the plan's own
+  // copy, which every backward that is not handed a saved copy rewrites first
+  a.csave = c_saved ? c_saved : p->fast.coef_bwd;
+  a.pos = p->fast.bwd_pos;
+  a.nslot = p->fast.coef_slots;
+  a.slots = p->fast.bwd_slots;
   a.frag = p->fout->dev.fs16;
   a.T = T;
   a.nblk_in = p->fin->dev.nblk;
@@ -854,6 +878,12 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   const size_t lds = fast128_lds_bytes(a.nblk_in);
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
+  if (T == 0) {   // no tiles: the copy alone
+    if (!c_saved) return hipSuccess;
+    const dim3 g((unsigned)((a.nslot + 255) / 256), (unsigned)count);
+    hipLaunchKernelGGL(scatter_bwd_coef, g, dim3(256), 0, s, c, cs, a.pos, a.nslot, a.slots + 256, c_saved);
+    return hipGetLastError();
+  }
   rec(e0, s);
   if (beta != 0.f)
     hipLaunchKernelGGL(fwd128<true>, grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st,
@@ -868,7 +898,7 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
 hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G, int64_t ldg,
                          const float* c, const float* const* cs, float scale, float beta_dx, ActPtrs dX,
                          int64_t lddx, bool want_dx, int accumulate_dc, float* dC, float* const* dCs, bool want_dc,
-                         hipStream_t s) {
+                         const float* c_saved, hipStream_t s) {
   FastArgs a{};
   a.frag = p->fin->dev.fs16;
   a.T = T;
@@ -890,12 +920,12 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   a.slots = p->fast.bwd_slots;
   a.pstride = (int)fast128_partial_floats((size_t)a.slots);
   a.partial = p->partial;
-  a.cb = p->fast.coef_bwd;
+  a.cb = c_saved ? c_saved : p->fast.coef_bwd;
   const long ntiles = (T + kTT - 1) / kTT;
   a.ntiles = ntiles;
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
-  if (T > 0 && want_dx) {
+  if (T > 0 && want_dx && !c_saved) {
     const int nslot = p->fast.coef_slots;
     const dim3 g((unsigned)((nslot + 255) / 256), (unsigned)count);
     hipLaunchKernelGGL(scatter_bwd_coef, g, dim3(256), 0, s, c, cs, p->fast.bwd_pos, nslot, a.slots + 256,

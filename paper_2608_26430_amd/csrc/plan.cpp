@@ -578,6 +578,7 @@ extern "C" ff_status ff_plan_query(const ff_plan* p, int key, int64_t* value) {
     case FF_Q_NNZ: *value = p->nnz; return FF_OK;
     case FF_Q_FAST128: *value = p->fast.enabled; return FF_OK;
     case FF_Q_COEF_SLOTS: *value = p->coef_slots; return FF_OK;
+    case FF_Q_SAVED_FLOATS: *value = p->fast.enabled ? (int64_t)p->fast.bwd_slots + 256 : 0; return FF_OK;
     default: return ff::fail(FF_EINVAL, "unknown query key %d", key);
   }
 }

@@ -123,6 +123,42 @@ def test_small_parity(dev, shape, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[9], SHAPES[10], SHAPES[11], SHAPES[12]],
+                         ids=lambda s: "n%d_m%d_nnz%d_T%d" % (s[0], s[2], s[4], s[5]))
+def test_saved_copy_matches_plain_calls(dev, shape, dtype):
+    """adapter_fwd(save=) / adapter_bwd(saved=) give bitwise the results of the plain calls,
+    also when the copy was written by a forward with no tokens or overwritten by a later one."""
+    n, rn, m, rm, nnz, T = shape
+    rows, cols, vals, X, G = _problem(shape, dtype, seed=n + 3 * m + nnz + T)
+    f_in, f_out = ff.framegen(n, n // rn, rn), ff.framegen(m, m // rm, rm)
+    plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T)
+    assert plan.saved_floats == (plan.query(6) if plan.fast128 else 0)
+    assert (plan.saved_floats > 0) == plan.fast128
+    saved = plan.new_saved(dev)
+    if saved is None:
+        saved = torch.empty((0,), device=dev)   # accepted and ignored where no copy is needed
+    Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
+    c = plan_c(plan, vals, dev)
+    other = plan_c(plan, inputs.gaussian(inputs.rng(9), (nnz,), std=0.02), dev)
+    s = 0.31
+    Y = ff.adapter_fwd(plan, Xd, c, s)
+    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s)
+    dX0 = torch_act(inputs.gaussian(inputs.rng(4), (T, n), dtype=dtype), dtype, dev)
+    dXb, _ = ff.adapter_bwd(plan, Xd, Gd, c, s, dX=dX0.clone(), beta_dx=0.5, want_dc=False)
+    ff.adapter_fwd(plan, Xd, other, s, save=saved)               # overwritten below
+    Ys = ff.adapter_fwd(plan, Xd, c, s, save=saved)
+    dXs, dCs = ff.adapter_bwd(plan, Xd, Gd, c, s, saved=saved)
+    dXbs, _ = ff.adapter_bwd(plan, Xd, Gd, c, s, dX=dX0.clone(), beta_dx=0.5, want_dc=False, saved=saved)
+    ff.adapter_fwd(plan, Xd[:0], c, s, save=saved)               # no tokens: the copy alone
+    dXe, _ = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dc=False, saved=saved)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Ys)
+    assert torch.equal(dX, dXs) and torch.equal(dC, dCs)
+    assert torch.equal(dXb, dXbs)
+    assert torch.equal(dX, dXe)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_batched_matches_single_calls(dev, dtype):
     n, m, nnz, T, count = 4096, 4096, 4000, 21, 3
     g = inputs.rng(77)

@@ -285,6 +285,12 @@ __device__ __forceinline__ void zero_tile(unsigned char* tile, int lane) {
   wave_lds_fence();
 }
 
+// The coefficient-array row named by a slot word's source field.  The array starts the
+// kernels' dynamic LDS, which has no static LDS before it, so the field is the LDS address.
+__device__ __forceinline__ u32x4 lds_src(unsigned e) {
+  return *(const __attribute__((address_space(3))) u32x4*)(size_t)(e & kSlotSrcMask);
+}
+
 __device__ __forceinline__ u32x4 lds_at(const unsigned char* base, unsigned byte_off) {
   return *reinterpret_cast<const u32x4*>(base + byte_off);
 }
@@ -366,9 +372,10 @@ __device__ __forceinline__ void fwd_load(const unsigned* __restrict__ st, int of
                                          const float* __restrict__ cv, int lane, FwdChunk& ch) {
 #pragma unroll
   for (int g = 0; g < kCh / 4; ++g) {
-    const long base = 64L * off + 256L * min(k0 / 4 + g, len / 4 - 1) + 4 * lane;
-    const u32x4 w = gld(reinterpret_cast<const u32x4*>(st + base))[0];
-    const f32x4 c = gld(reinterpret_cast<const f32x4*>(cv + base))[0];
+    // a wave-uniform row base plus the lane's 16 bytes: scalar base, vector offset
+    const long row = 64L * off + 256L * min(k0 / 4 + g, len / 4 - 1);
+    const u32x4 w = gld(reinterpret_cast<const u32x4*>(st + row))[lane];
+    const f32x4 c = gld(reinterpret_cast<const f32x4*>(cv + row))[lane];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       ch.en[4 * g + j] = w[j];
@@ -380,10 +387,10 @@ __device__ __forceinline__ void fwd_load(const unsigned* __restrict__ st, int of
 // The first n (uniform, a multiple of 4) slots of a loaded chunk, with their round-end bits;
 // all kCh LDS rows are read first.
 __device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int n, unsigned ends, float scale,
-                                            const unsigned char* zL, unsigned char* tile, float (&a)[8]) {
+                                            unsigned char* tile, float (&a)[8]) {
   u32x4 zv[kCh];
 #pragma unroll
-  for (int i = 0; i < kCh; ++i) zv[i] = lds_at(zL, ch.en[i] & kSlotSrcMask);
+  for (int i = 0; i < kCh; ++i) zv[i] = lds_src(ch.en[i]);
 #pragma unroll
   for (int i = 0; i < kCh; ++i) {
     if (i < n) {   // uniform
@@ -406,9 +413,8 @@ __device__ __forceinline__ void bwd_load_entries(const uint2* __restrict__ st, i
                                                  BwdEntries& ch) {
 #pragma unroll
   for (int g = 0; g < kCh / 4; ++g) {
-    const long base = 256L * min(k0 / 4 + g, len / 4 - 1) + 4 * lane;
-    const FF_GLOBAL u32x4* p = gld(reinterpret_cast<const u32x4*>(st + base));
-    const u32x4 lo = p[0], hi = p[1];
+    const FF_GLOBAL u32x4* p = gld(reinterpret_cast<const u32x4*>(st + 256L * min(k0 / 4 + g, len / 4 - 1)));
+    const u32x4 lo = p[2 * lane], hi = p[2 * lane + 1];
     ch.en[4 * g + 0] = u32x2{lo[0], lo[1]};
     ch.en[4 * g + 1] = u32x2{lo[2], lo[3]};
     ch.en[4 * g + 2] = u32x2{hi[0], hi[1]};
@@ -422,7 +428,7 @@ __device__ __forceinline__ void bwd_load_coeffs(const float* __restrict__ cb, in
                                                 float (&cc)[kCh]) {
 #pragma unroll
   for (int g = 0; g < kCh / 4; ++g) {
-    const f32x4 c = gld(reinterpret_cast<const f32x4*>(cb + 256L * min(k0 / 4 + g, len / 4 - 1) + 4 * lane))[0];
+    const f32x4 c = gld(reinterpret_cast<const f32x4*>(cb + 256L * min(k0 / 4 + g, len / 4 - 1)))[lane];
 #pragma unroll
     for (int j = 0; j < 4; ++j) cc[4 * g + j] = c[j];
   }
@@ -432,7 +438,7 @@ __device__ __forceinline__ void bwd_load_coeffs(const float* __restrict__ cb, in
 // store per lane to part (the pair's slots, k0 = the chunk's first stream row); groups past the
 // stream's end (n = rows of the chunk inside it, a multiple of 4) write to the scratch row
 // `trash`.  Padding slots write values the reduction never reads.
-__device__ __forceinline__ void bwd_sddmm(const BwdEntries& ch, int n, int k0, const unsigned char* uL,
+__device__ __forceinline__ void bwd_sddmm(const BwdEntries& ch, int n, int k0,
                                           const unsigned char* tile, float* __restrict__ part,
                                           float* __restrict__ trash, int lane) {
 #pragma unroll
@@ -444,7 +450,7 @@ __device__ __forceinline__ void bwd_sddmm(const BwdEntries& ch, int n, int k0, c
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const unsigned e = ch.en[4 * g + h + i].x;
-        uv[i] = lds_at(uL, e & kSlotSrcMask);
+        uv[i] = lds_src(e);
         zv[i] = lds_at(tile, tile_off(e));
       }
 #pragma unroll
@@ -464,13 +470,13 @@ __device__ __forceinline__ void bwd_sddmm(const BwdEntries& ch, int n, int k0, c
 }
 
 __device__ __forceinline__ void bwd_spmm(const BwdEntries& ch, const float (&cc)[kCh], int n, float scale,
-                                         const unsigned char* uL, unsigned char* tile, float (&a)[8]) {
+                                         unsigned char* tile, float (&a)[8]) {
   constexpr int kH = kCh / 2;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     u32x4 uv[kH];
 #pragma unroll
-    for (int i = 0; i < kH; ++i) uv[i] = lds_at(uL, ch.en[h * kH + i].x & kSlotSrcMask);
+    for (int i = 0; i < kH; ++i) uv[i] = lds_src(ch.en[h * kH + i].x);
 #pragma unroll
     for (int i = 0; i < kH; ++i) {
       if (h * kH + i < n) {   // uniform
@@ -594,11 +600,11 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
     const int off = q.x, len = q.y;
     zero_tile(tile, lane);
     float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    fwd_compute(cur, min(kCh, len), (unsigned)q.w, a.scale, zL, tile, acc8);
+    fwd_compute(cur, min(kCh, len), (unsigned)q.w, a.scale, tile, acc8);
     if (len > kCh) {   // long stream
       for (int k0 = kCh; k0 < len; k0 += kCh) {
         fwd_load(fst, off, len, k0, cv, lane, cur);
-        fwd_compute(cur, min(kCh, len - k0), chunk_ends(q, em, k0), a.scale, zL, tile, acc8);
+        fwd_compute(cur, min(kCh, len - k0), chunk_ends(q, em, k0), a.scale, tile, acc8);
       }
       vm_wait_all();
     }
@@ -681,12 +687,12 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
       load_act(X, a.ldx, nt, 2 * min(p + kWaves, lastp), lane, bx);
       issue_point();
       float* pp = part + (long)q.x * 64;
-      bwd_sddmm(ch, min(kCh, len), 0, uL, tile, pp, trash, lane);
+      bwd_sddmm(ch, min(kCh, len), 0, tile, pp, trash, lane);
       if (len > kCh) {   // long stream
         for (int k0 = kCh; k0 < len; k0 += kCh) {
           BwdEntries ck;
           bwd_load_entries(st, len, k0, lane, ck);
-          bwd_sddmm(ck, min(kCh, len - k0), k0, uL, tile, pp, trash, lane);
+          bwd_sddmm(ck, min(kCh, len - k0), k0, tile, pp, trash, lane);
         }
         vm_wait_all();
       }
@@ -719,14 +725,14 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
       // q = C^T u for this pair, then dX = beta dX + s P_in q
       zero_tile(tile, lane);
       float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      bwd_spmm(ch, cc, min(kCh, len), a.scale, uL, tile, acc8);
+      bwd_spmm(ch, cc, min(kCh, len), a.scale, tile, acc8);
       if (len > kCh) {   // long stream
         for (int k0 = kCh; k0 < len; k0 += kCh) {
           BwdEntries ck;
           float ckc[kCh];
           bwd_load_entries(st, len, k0, lane, ck);
           bwd_load_coeffs(cbp, len, k0, lane, ckc);
-          bwd_spmm(ck, ckc, min(kCh, len - k0), a.scale, uL, tile, acc8);
+          bwd_spmm(ck, ckc, min(kCh, len - k0), a.scale, tile, acc8);
         }
         vm_wait_all();
       }

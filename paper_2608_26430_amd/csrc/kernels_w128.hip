@@ -277,6 +277,17 @@ __device__ __forceinline__ void store_act(u16* rows, long ld, int nt, int blk0, 
   }
 }
 
+// Wave priority by progress (`steps` = this wave's share of the phase, `done` = steps finished):
+// the waves with more left issue first, so the two workgroups that share a CU advance together
+// instead of the older one finishing first and leaving the other to run alone.
+__device__ __forceinline__ void prio_by_progress(int done, int steps) {
+  const int left = steps - done;   // wave-uniform
+  if (4 * left > 3 * steps) __builtin_amdgcn_s_setprio(3);
+  else if (2 * left > steps) __builtin_amdgcn_s_setprio(2);
+  else if (4 * left > steps) __builtin_amdgcn_s_setprio(1);
+  else __builtin_amdgcn_s_setprio(0);
+}
+
 __device__ __forceinline__ void zero_tile(unsigned char* tile, int lane) {
   u32x4* tz = reinterpret_cast<u32x4*>(tile);
   wave_lds_fence();
@@ -577,8 +588,11 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   u32x4 fr[kFragPerThread];
   frag_fetch(a.frag, fr);
   issue_point();
-  // first stream chunk of this wave's first output pair, in flight during the analysis
+  // first stream chunk of this wave's first output pair, in flight during the analysis; the
+  // pair entries run one pair ahead of the chunks, so their scalar loads are never waited on
+  // at a pair's start
   int4 q = pl[min(wave, lastp)];
+  int4 qn = pl[min(wave + kWaves, lastp)];
   FwdChunk ch;
   fwd_load(fst, q.x, q.y, 0, cv, lane, ch);
   issue_point();
@@ -592,9 +606,11 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   // One output pair: its chunk is in `cur`; the next pair's chunk is loaded into `nxt` first,
   // a whole pair ahead of its use.  The loop runs two pairs per iteration with the buffers'
   // roles swapped, so no chunk is ever copied between registers.
+  const int steps = (npo - wave + kWaves - 1) / kWaves;
   auto pair = [&](int p, FwdChunk& cur, FwdChunk& nxt) {
-    const int4 qn = pl[min(p + kWaves, lastp)];
+    prio_by_progress((p - wave) / kWaves, steps);
     fwd_load(fst, qn.x, qn.y, 0, cv, lane, nxt);
+    const int4 qnn = pl[min(p + 2 * kWaves, lastp)];
     issue_point();
     // v = C z for this pair into the tile
     const int off = q.x, len = q.y;
@@ -617,6 +633,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
     mfma_block(F, b, acc);
     store_act<BETA>(Y, a.ldy, nt, 2 * p, lane, acc, a.beta);
     q = qn;
+    qn = qnn;
   };
   FwdChunk ch2;
   for (int p = wave; p < npo; p += 2 * kWaves) {
@@ -667,10 +684,13 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
   __syncthreads();
 
   // Two passes over this wave's input pairs, so that each holds few registers: dC, then dX.
+  const int npw = (npi - wave + kWaves - 1) / kWaves;   // this wave's pairs per pass
+  const int steps = (DC ? npw : 0) + (DX ? npw : 0);
   if (DC) {
     // one input pair; the next pair's entries are loaded into `nxt` a whole pair ahead of
     // their use, two pairs per iteration with the buffers' roles swapped
     auto pair = [&](int p, BwdEntries& ch, BwdEntries& chn) {
+      prio_by_progress((p - wave) / kWaves, steps);
       const int len = q.y;
       const uint2* st = bst + (long)q.x * 64;
       const int4 qn = pl[min(p + kWaves, lastp)];
@@ -715,6 +735,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
     // one input pair; the next pair's entries and coefficients are loaded at its start, two
     // pairs per iteration with the buffers' roles swapped
     auto pair = [&](int p, BwdEntries& ch, float (&cc)[kCh], BwdEntries& chn, float (&ccn)[kCh]) {
+      prio_by_progress((DC ? npw : 0) + (p - wave) / kWaves, steps);
       const int len = q.y;
       const uint2* st = bst + (long)q.x * 64;
       const float* cbp = cbw + (long)q.x * 64;

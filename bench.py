@@ -79,6 +79,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="cfg2_llama7b_qproj")
+    ap.add_argument("--adapter", type=int, default=0, help="adapter of a multi-adapter workload (one layer)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run 3 device-to-device copies of this many MiB (a known-size kernel "
@@ -105,7 +106,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     wl = inputs.WORKLOADS[args.workload]
-    ad = wl.adapters[0]
+    ad = wl.adapters[args.adapter]
     data = inputs.adapter_data(wl, ad)
     T, n, m, nnz = wl.tokens, ad.d_in, ad.d_out, ad.nnz
     esz = 2 if wl.dtype == "bf16" else 4

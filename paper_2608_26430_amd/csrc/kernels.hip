@@ -149,6 +149,40 @@ __device__ __forceinline__ void frame_apply(const FrameDev& f, bool synth, int n
   }
 }
 
+// out[t][slot_off[s]] = sum over the entries e of row s of c[e.y] * in[t][e.x], for every token
+// t < nt of the tile.  A work item is one row for a group of up to 8 tokens: the row's entries
+// and coefficients are loaded once per group, and the group's products are LDS reads.
+constexpr int kRowTokens = 8;
+
+template <bool BF16>
+__device__ __forceinline__ void row_products(int nslots, const int* __restrict__ ptr, const int2* __restrict__ ent,
+                                             const int* __restrict__ slot_off, const float* cv,
+                                             const typename Act<BF16>::E* in, int ld_in,
+                                             typename Act<BF16>::E* out, int ld_out, int nt) {
+  using A = Act<BF16>;
+  const int ngrp = (nt + kRowTokens - 1) / kRowTokens;
+  for (int it = threadIdx.x; it < nslots * ngrp; it += blockDim.x) {
+    const int s = it / ngrp, t0 = (it - s * ngrp) * kRowTokens;
+    const int nt_g = min(kRowTokens, nt - t0);
+    float acc[kRowTokens];
+#pragma unroll
+    for (int t = 0; t < kRowTokens; ++t) acc[t] = 0.f;
+    const int beg = ptr[s], end = ptr[s + 1];
+    const typename Act<BF16>::E* ib = in + t0 * ld_in;
+    for (int j = beg; j < end; ++j) {
+      const int2 en = ent[j];
+      const float c = cv[en.y];
+#pragma unroll
+      for (int t = 0; t < kRowTokens; ++t)
+        if (t < nt_g) acc[t] = fmaf(c, A::ld(ib + t * ld_in + en.x), acc[t]);
+    }
+    typename Act<BF16>::E* ob = out + t0 * ld_out + slot_off[s];
+#pragma unroll
+    for (int t = 0; t < kRowTokens; ++t)
+      if (t < nt_g) A::st(ob + t * ld_out, acc[t]);
+  }
+}
+
 struct FwdArgs {
   FrameDev fin, fout;
   int T, tt, ldt_in, ldt_out, ldb_in, ldb_out;
@@ -188,18 +222,8 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
                     [&](int t, int b, int o, f32x4 v) { A::st4(zt + t * a.ldt_in + b * a.ldb_in + o, v); });
   __syncthreads();
 
-  // coefficients: v[a] = sum_{e in row a} c_e z[b_e]; lanes of one slot take consecutive tokens
-  for (int it = threadIdx.x; it < a.nslots * nt; it += blockDim.x) {
-    const int slot = it / nt, t = it - slot * nt;
-    const int beg = a.ptr[slot], end = a.ptr[slot + 1];
-    const E* zr = zt + t * a.ldt_in;
-    float acc = 0.f;
-    for (int j = beg; j < end; ++j) {
-      const int2 en = a.ent[j];
-      acc = fmaf(cv[en.y], A::ld(zr + en.x), acc);
-    }
-    A::st(vt + t * a.ldt_out + a.slot_off[slot], acc);
-  }
+  // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
+  row_products<BF16>(a.nslots, a.ptr, a.ent, a.slot_off, cv, zt, a.ldt_in, vt, a.ldt_out, nt);
   __syncthreads();
 
   // synthesis and epilogue: y = beta y + s P_out v
@@ -278,17 +302,7 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
 
   // q[b] = sum_{e in column b} c_e u[a_e], written over z
   const float* cv = a.cs ? a.cs[bi] : a.c;
-  for (int it = threadIdx.x; it < a.nslots * nt; it += blockDim.x) {
-    const int slot = it / nt, t = it - slot * nt;
-    const int beg = a.ptr[slot], end = a.ptr[slot + 1];
-    const E* ur = ut + t * a.ldt_out;
-    float acc = 0.f;
-    for (int j = beg; j < end; ++j) {
-      const int2 en = a.ent[j];
-      acc = fmaf(cv[en.y], A::ld(ur + en.x), acc);
-    }
-    A::st(zt + t * a.ldt_in + a.slot_off[slot], acc);
-  }
+  row_products<BF16>(a.nslots, a.ptr, a.ent, a.slot_off, cv, ut, a.ldt_out, zt, a.ldt_in, nt);
   __syncthreads();
 
   E* dX = reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX) + (long)t0 * a.lddx;

@@ -84,38 +84,60 @@ __device__ __forceinline__ void apply_chunk(const FrameDev& f, bool synth, int m
   const int q = lane >> 4;
 #pragma unroll
   for (int c = 0; c < kCH; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // fragments of the row tiles past the block's end repeat its last tile (their products are
+  // discarded), so every load is issued unconditionally
+  const int mlast = f.MT - 1;
   if constexpr (BF16) {
     const bf16x8* fr = reinterpret_cast<const bf16x8*>(synth ? f.fs16 : f.fa16);
-    for (int ks = 0; ks < f.KT; ++ks) {
+    // contraction step ks's fragments and activations, the next step's in flight meanwhile
+    auto load = [&](int ks, bf16x8 (&fa)[kCH], bf16x8& b) {
       const int i0 = ks * 32 + q * 8;
-      bf16x8 b = {};
+      b = bf16x8{};
       if (valid && i0 < f.W) b = *reinterpret_cast<const bf16x8*>(in + i0);
 #pragma unroll
-      for (int c = 0; c < kCH; ++c) {
-        const int mt = mt0 + c;
-        if (mt < f.MT) {
-          const bf16x8 a = fr[((size_t)mt * f.KT + ks) * 64 + lane];
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[c], 0, 0, 0);
-        }
-      }
+      for (int c = 0; c < kCH; ++c) fa[c] = fr[((size_t)min(mt0 + c, mlast) * f.KT + ks) * 64 + lane];
+    };
+    bf16x8 fa[2][kCH], b[2];
+    load(0, fa[0], b[0]);
+    for (int ks = 0; ks < f.KT; ks += 2) {
+      load(min(ks + 1, f.KT - 1), fa[1], b[1]);
+#pragma unroll
+      for (int c = 0; c < kCH; ++c)
+        if (mt0 + c < f.MT) acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[0][c], b[0], acc[c], 0, 0, 0);
+      if (ks + 1 >= f.KT) break;
+      load(min(ks + 2, f.KT - 1), fa[0], b[0]);
+#pragma unroll
+      for (int c = 0; c < kCH; ++c)
+        if (mt0 + c < f.MT) acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[1][c], b[1], acc[c], 0, 0, 0);
     }
   } else {
     const f32x4* fr = reinterpret_cast<const f32x4*>(synth ? f.fs32 : f.fa32);
-    for (int ks = 0; ks < f.KT4; ++ks) {
+    auto load = [&](int ks, f32x4 (&fa)[kCH], f32x4& b) {
       const int i0 = ks * 16 + q * 4;
-      f32x4 b = {0.f, 0.f, 0.f, 0.f};
+      b = f32x4{0.f, 0.f, 0.f, 0.f};
       if (valid && i0 < f.W) b = *reinterpret_cast<const f32x4*>(in + i0);
 #pragma unroll
+      for (int c = 0; c < kCH; ++c) fa[c] = fr[((size_t)min(mt0 + c, mlast) * f.KT4 + ks) * 64 + lane];
+    };
+    auto mma = [&](const f32x4 (&fa)[kCH], const f32x4& b) {
+#pragma unroll
       for (int c = 0; c < kCH; ++c) {
-        const int mt = mt0 + c;
-        if (mt < f.MT) {
-          const f32x4 a = fr[((size_t)mt * f.KT4 + ks) * 64 + lane];
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc[c], 0, 0, 0);
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], acc[c], 0, 0, 0);
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], acc[c], 0, 0, 0);
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], acc[c], 0, 0, 0);
+        if (mt0 + c < f.MT) {
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[c][0], b[0], acc[c], 0, 0, 0);
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[c][1], b[1], acc[c], 0, 0, 0);
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[c][2], b[2], acc[c], 0, 0, 0);
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[c][3], b[3], acc[c], 0, 0, 0);
         }
       }
+    };
+    f32x4 fa[2][kCH], b[2];
+    load(0, fa[0], b[0]);
+    for (int ks = 0; ks < f.KT4; ks += 2) {
+      load(min(ks + 1, f.KT4 - 1), fa[1], b[1]);
+      mma(fa[0], b[0]);
+      if (ks + 1 >= f.KT4) break;
+      load(min(ks + 2, f.KT4 - 1), fa[0], b[0]);
+      mma(fa[1], b[1]);
     }
   }
 }

@@ -45,12 +45,13 @@ struct PlanDev {
   // v = C z: one slot per row of C (block order), slots sorted by row length.
   const int* fwd_slot_off;   // LDS offset of the slot's row in the v tile
   const int* fwd_ptr;        // slot -> [ptr[s], ptr[s+1]) entries
-  const int2* fwd_ent;       // (LDS offset of the column in the z tile, user index e)
+  const int2* fwd_ent;       // (LDS offset of the column in the z tile, coefficient slot)
   int fwd_nslots;
+  int fwd_by_entry;          // 1: entry j of the table holds coefficient slot j
   // q = C^T u: one slot per column of C, sorted by column length.
   const int* bwd_slot_off;   // LDS offset of the slot's column in the q tile
   const int* bwd_ptr;
-  const int2* bwd_ent;       // (LDS offset of the row in the u tile, user index e)
+  const int2* bwd_ent;       // (LDS offset of the row in the u tile, coefficient slot)
   int bwd_nslots;
   // dC: per user entry e, (LDS offset of row in u tile, LDS offset of column in z tile).
   const int2* sdd;           // per coefficient slot; (-1, -1) for padding slots

@@ -171,12 +171,15 @@ __device__ __forceinline__ void frame_apply(const FrameDev& f, bool synth, int n
   }
 }
 
-// out[t][slot_off[s]] = sum over the entries e of row s of c[e.y] * in[t][e.x], for every token
-// t < nt of the tile.  A work item is one row for a group of up to 8 tokens: the row's entries
-// and coefficients are loaded once per group, and the group's products are LDS reads.
+// out[t][slot_off[s]] = sum over the entries e of row s of c * in[t][e.x], for every token
+// t < nt of the tile, where c is cv[j] for the row's j-th table entry (BY_ENTRY: the table is in
+// coefficient-slot order) or cv[e.y].  A work item is one row for a group of up to 8 tokens:
+// the row's entries and coefficients are loaded once per group, four entries at a time, and the
+// group's products are LDS reads.
 constexpr int kRowTokens = 8;
+constexpr int kRowBatch = 4;
 
-template <bool BF16>
+template <bool BF16, bool BY_ENTRY>
 __device__ __forceinline__ void row_products(int nslots, const int* __restrict__ ptr, const int2* __restrict__ ent,
                                              const int* __restrict__ slot_off, const float* cv,
                                              const typename Act<BF16>::E* in, int ld_in,
@@ -191,12 +194,27 @@ __device__ __forceinline__ void row_products(int nslots, const int* __restrict__
     for (int t = 0; t < kRowTokens; ++t) acc[t] = 0.f;
     const int beg = ptr[s], end = ptr[s + 1];
     const typename Act<BF16>::E* ib = in + t0 * ld_in;
-    for (int j = beg; j < end; ++j) {
-      const int2 en = ent[j];
-      const float c = cv[en.y];
+    for (int j0 = beg; j0 < end; j0 += kRowBatch) {
+      int2 en[kRowBatch];
+      float c[kRowBatch];
 #pragma unroll
-      for (int t = 0; t < kRowTokens; ++t)
-        if (t < nt_g) acc[t] = fmaf(c, A::ld(ib + t * ld_in + en.x), acc[t]);
+      for (int u = 0; u < kRowBatch; ++u) {   // clamped: every load is issued
+        const int j = min(j0 + u, end - 1);
+        en[u] = ent[j];
+        if (BY_ENTRY) c[u] = cv[j];
+      }
+      if (!BY_ENTRY) {
+#pragma unroll
+        for (int u = 0; u < kRowBatch; ++u) c[u] = cv[en[u].y];
+      }
+#pragma unroll
+      for (int u = 0; u < kRowBatch; ++u) {
+        if (j0 + u < end) {
+#pragma unroll
+          for (int t = 0; t < kRowTokens; ++t)
+            if (t < nt_g) acc[t] = fmaf(c[u], A::ld(ib + t * ld_in + en[u].x), acc[t]);
+        }
+      }
     }
     typename Act<BF16>::E* ob = out + t0 * ld_out + slot_off[s];
 #pragma unroll
@@ -221,6 +239,7 @@ struct FwdArgs {
   const int* ptr;
   const int2* ent;
   int nslots;
+  int by_entry;   // the table is in coefficient-slot order
 };
 
 template <bool BF16>
@@ -245,7 +264,10 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   __syncthreads();
 
   // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
-  row_products<BF16>(a.nslots, a.ptr, a.ent, a.slot_off, cv, zt, a.ldt_in, vt, a.ldt_out, nt);
+  if (a.by_entry)
+    row_products<BF16, true>(a.nslots, a.ptr, a.ent, a.slot_off, cv, zt, a.ldt_in, vt, a.ldt_out, nt);
+  else
+    row_products<BF16, false>(a.nslots, a.ptr, a.ent, a.slot_off, cv, zt, a.ldt_in, vt, a.ldt_out, nt);
   __syncthreads();
 
   // synthesis and epilogue: y = beta y + s P_out v
@@ -324,7 +346,7 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
 
   // q[b] = sum_{e in column b} c_e u[a_e], written over z
   const float* cv = a.cs ? a.cs[bi] : a.c;
-  row_products<BF16>(a.nslots, a.ptr, a.ent, a.slot_off, cv, ut, a.ldt_out, zt, a.ldt_in, nt);
+  row_products<BF16, false>(a.nslots, a.ptr, a.ent, a.slot_off, cv, ut, a.ldt_out, zt, a.ldt_in, nt);
   __syncthreads();
 
   E* dX = reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX) + (long)t0 * a.lddx;
@@ -475,6 +497,7 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.ptr = p->dev.fwd_ptr;
   a.ent = p->dev.fwd_ent;
   a.nslots = p->dev.fwd_nslots;
+  a.by_entry = p->dev.fwd_by_entry;
   const dim3 grid((unsigned)((T + a.tt - 1) / a.tt), (unsigned)count);
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);

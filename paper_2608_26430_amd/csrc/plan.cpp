@@ -438,9 +438,13 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       }
     }
   } else {
-    std::iota(slot_of_user.begin(), slot_of_user.end(), 0);
+    // the generic kernels' layout is the forward table's entry order, so the forward reads a
+    // row's coefficients by table position
     user_of_slot.resize((size_t)nnz);
-    std::iota(user_of_slot.begin(), user_of_slot.end(), 0);
+    for (int64_t j = 0; j < nnz; ++j) {
+      user_of_slot[j] = fwd_ent[j].y;
+      slot_of_user[fwd_ent[j].y] = (int)j;
+    }
   }
   const int64_t nslot = (int64_t)user_of_slot.size();   // coefficient slots (>= nnz)
   // for the 128-wide backward: the backward slot of every coefficient slot (padding slots go
@@ -522,6 +526,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   pd.fwd_ptr = (const int*)where[1];
   pd.fwd_ent = (const int2*)where[2];
   pd.fwd_nslots = (int)m;
+  pd.fwd_by_entry = fast ? 0 : 1;
   pd.bwd_slot_off = (const int*)where[3];
   pd.bwd_ptr = (const int*)where[4];
   pd.bwd_ent = (const int2*)where[5];

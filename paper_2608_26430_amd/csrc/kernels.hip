@@ -151,13 +151,25 @@ __device__ __forceinline__ void frame_apply(const FrameDev& f, bool synth, int n
                                             Epi epi) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int q = lane >> 4;
-  for (int g = wave; g * 16 < nrows; g += nw) {
+  // Work items are a 16-row group with a range of chunks of kCH output tiles.  A group is split
+  // into sf ranges only when that shortens the busiest wave (fewer groups than waves), since
+  // every range reloads the group's activations.
+  const int ngrp = (nrows + 15) / 16, nch = (f.MT + kCH - 1) / kCH;
+  int sf = 1, best = (ngrp + nw - 1) / nw * nch;
+  for (int k = 2; k <= nch; ++k) {
+    const int cost = (ngrp * k + nw - 1) / nw * ((nch + k - 1) / k);
+    if (cost < best) { best = cost; sf = k; }
+  }
+  const int cpi = (nch + sf - 1) / sf;   // chunks per item
+  for (int item = wave; item < ngrp * sf; item += nw) {
+    const int g = item / sf, c0 = (item - g * sf) * cpi, c1 = min(nch, c0 + cpi);
     const int row = g * 16 + (lane & 15);
     const bool valid = row < nrows;
     const int rr = valid ? row : 0;
     const int t = rr / f.nblk, b = rr - t * f.nblk;
     const typename Act<BF16>::E* in = src + (long)t * src_ld + (long)b * src_bs;
-    for (int mt0 = 0; mt0 < f.MT; mt0 += kCH) {
+    for (int ch = c0; ch < c1; ++ch) {
+      const int mt0 = ch * kCH;
       f32x4 acc[kCH];
       apply_chunk<BF16>(f, synth, mt0, in, valid, lane, acc);
       if (valid) {
@@ -173,11 +185,13 @@ __device__ __forceinline__ void frame_apply(const FrameDev& f, bool synth, int n
 
 // out[t][slot_off[s]] = sum over the entries e of row s of c * in[t][e.x], for every token
 // t < nt of the tile, where c is cv[j] for the row's j-th table entry (BY_ENTRY: the table is in
-// coefficient-slot order) or cv[e.y].  A work item is one row for a group of up to 8 tokens:
-// the row's entries and coefficients are loaded once per group, four entries at a time, and the
-// group's products are LDS reads.
+// coefficient-slot order) or cv[e.y].  A work item is one row for a group of up to 8 tokens: the
+// row's entries and coefficients are loaded once per group, four entries at a time, and the
+// group's products are LDS reads.  Each thread runs kRowItems items side by side, so their load
+// chains overlap.
 constexpr int kRowTokens = 8;
 constexpr int kRowBatch = 4;
+constexpr int kRowItems = 1;
 
 template <bool BF16, bool BY_ENTRY>
 __device__ __forceinline__ void row_products(int nslots, const int* __restrict__ ptr, const int2* __restrict__ ent,
@@ -185,41 +199,63 @@ __device__ __forceinline__ void row_products(int nslots, const int* __restrict__
                                              const typename Act<BF16>::E* in, int ld_in,
                                              typename Act<BF16>::E* out, int ld_out, int nt) {
   using A = Act<BF16>;
-  const int ngrp = (nt + kRowTokens - 1) / kRowTokens;
-  for (int it = threadIdx.x; it < nslots * ngrp; it += blockDim.x) {
-    const int s = it / ngrp, t0 = (it - s * ngrp) * kRowTokens;
-    const int nt_g = min(kRowTokens, nt - t0);
-    float acc[kRowTokens];
+  using E = typename A::E;
+  const int ngrp = (nt + kRowTokens - 1) / kRowTokens, items = nslots * ngrp;
+  const int last = max(ptr[nslots] - 1, 0);   // table entries: loads are clamped into the table
+  for (int base = threadIdx.x; base < items; base += kRowItems * blockDim.x) {
+    int beg[kRowItems], len[kRowItems], off[kRowItems], ntg[kRowItems];
+    const E* ib[kRowItems];
+    int maxlen = 0;
 #pragma unroll
-    for (int t = 0; t < kRowTokens; ++t) acc[t] = 0.f;
-    const int beg = ptr[s], end = ptr[s + 1];
-    const typename Act<BF16>::E* ib = in + t0 * ld_in;
-    for (int j0 = beg; j0 < end; j0 += kRowBatch) {
-      int2 en[kRowBatch];
-      float c[kRowBatch];
+    for (int r = 0; r < kRowItems; ++r) {
+      const int it = base + r * (int)blockDim.x;
+      const bool ok = it < items;
+      const int itc = ok ? it : base;
+      const int s = itc / ngrp, t0 = (itc - s * ngrp) * kRowTokens;
+      ntg[r] = ok ? min(kRowTokens, nt - t0) : 0;
+      beg[r] = ptr[s];
+      len[r] = ok ? ptr[s + 1] - beg[r] : 0;
+      off[r] = t0 * ld_out + slot_off[s];
+      ib[r] = in + t0 * ld_in;
+      maxlen = max(maxlen, len[r]);
+    }
+    float acc[kRowItems][kRowTokens];
 #pragma unroll
-      for (int u = 0; u < kRowBatch; ++u) {   // clamped: every load is issued
-        const int j = min(j0 + u, end - 1);
-        en[u] = ent[j];
-        if (BY_ENTRY) c[u] = cv[j];
-      }
+    for (int r = 0; r < kRowItems; ++r)
+#pragma unroll
+      for (int t = 0; t < kRowTokens; ++t) acc[r][t] = 0.f;
+    for (int j0 = 0; j0 < maxlen; j0 += kRowBatch) {
+      int2 en[kRowItems][kRowBatch];
+      float c[kRowItems][kRowBatch];
+#pragma unroll
+      for (int r = 0; r < kRowItems; ++r)
+#pragma unroll
+        for (int u = 0; u < kRowBatch; ++u) {
+          const int j = min(beg[r] + min(j0 + u, max(len[r] - 1, 0)), last);
+          en[r][u] = ent[j];
+          if (BY_ENTRY) c[r][u] = cv[j];
+        }
       if (!BY_ENTRY) {
 #pragma unroll
-        for (int u = 0; u < kRowBatch; ++u) c[u] = cv[en[u].y];
+        for (int r = 0; r < kRowItems; ++r)
+#pragma unroll
+          for (int u = 0; u < kRowBatch; ++u) c[r][u] = cv[en[r][u].y];
       }
 #pragma unroll
-      for (int u = 0; u < kRowBatch; ++u) {
-        if (j0 + u < end) {
+      for (int r = 0; r < kRowItems; ++r)
 #pragma unroll
-          for (int t = 0; t < kRowTokens; ++t)
-            if (t < nt_g) acc[t] = fmaf(c[u], A::ld(ib + t * ld_in + en[u].x), acc[t]);
-        }
-      }
+        for (int u = 0; u < kRowBatch; ++u)
+          if (j0 + u < len[r]) {
+#pragma unroll
+            for (int t = 0; t < kRowTokens; ++t)
+              if (t < ntg[r]) acc[r][t] = fmaf(c[r][u], A::ld(ib[r] + t * ld_in + en[r][u].x), acc[r][t]);
+          }
     }
-    typename Act<BF16>::E* ob = out + t0 * ld_out + slot_off[s];
 #pragma unroll
-    for (int t = 0; t < kRowTokens; ++t)
-      if (t < nt_g) A::st(ob + t * ld_out, acc[t]);
+    for (int r = 0; r < kRowItems; ++r)
+#pragma unroll
+      for (int t = 0; t < kRowTokens; ++t)
+        if (t < ntg[r]) A::st(out + off[r] + t * ld_out, acc[r][t]);
   }
 }
 
@@ -359,17 +395,40 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   });
 }
 
-__global__ void __launch_bounds__(256) dc_reduce(const float* __restrict__ partial, long ntiles, int nnz,
-                                                 float scale, int accumulate, float* dC, float* const* dCs) {
-  const int bi = blockIdx.y;
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= nnz) return;
-  const float* p = partial + (long)bi * ntiles * nnz + e;
+// A workgroup owns 64 coefficient slots; each of its 16 waves sums 1/16 of the tiles with all
+// loads of a pass in flight, and the 16 sums are combined in a fixed order (deterministic).
+constexpr int kDcWaves = 16;
+constexpr int kDcBatch = 8;
+
+__global__ void __launch_bounds__(64 * kDcWaves) dc_reduce(const float* __restrict__ partial, long ntiles, int nnz,
+                                                           float scale, int accumulate, float* dC,
+                                                           float* const* dCs) {
+  __shared__ float red[kDcWaves][64];
+  const int bi = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int e = blockIdx.x * 64 + lane;
+  const int ec = min(e, nnz - 1);   // lanes past the end read the last slot and write nothing
+  const float* p = partial + (long)bi * ntiles * nnz + ec;
   float sum = 0.f;
-  for (long t = 0; t < ntiles; ++t) sum += p[t * nnz];
-  float* out = dCs ? dCs[bi] : dC;
-  const float v = scale * sum;
-  out[e] = accumulate ? out[e] + v : v;
+  for (long t0 = w; t0 < ntiles; t0 += (long)kDcWaves * kDcBatch) {
+    float v[kDcBatch];
+#pragma unroll
+    for (int j = 0; j < kDcBatch; ++j) {
+      const long t = t0 + (long)j * kDcWaves;
+      v[j] = t < ntiles ? p[t * nnz] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < kDcBatch; ++j) sum += v[j];
+  }
+  red[w][lane] = sum;
+  __syncthreads();
+  if (w == 0 && e < nnz) {
+    float tot = 0.f;
+#pragma unroll
+    for (int i = 0; i < kDcWaves; ++i) tot += red[i][lane];
+    float* out = dCs ? dCs[bi] : dC;
+    const float v = scale * tot;
+    out[e] = accumulate ? out[e] + v : v;
+  }
 }
 
 struct MergeArgs {
@@ -564,9 +623,9 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
     if (e != hipSuccess) return e;
   }
   if (want_dc) {
-    const dim3 grid((unsigned)((a.nnz + 255) / 256), (unsigned)count);
-    hipLaunchKernelGGL(dc_reduce, grid, dim3(256), 0, s, p->partial, ntiles, a.nnz, scale, accumulate_dc, dC,
-                       dCs);
+    const dim3 grid((unsigned)((a.nnz + 63) / 64), (unsigned)count);
+    hipLaunchKernelGGL(dc_reduce, grid, dim3(64 * kDcWaves), 0, s, p->partial, ntiles, a.nnz, scale, accumulate_dc,
+                       dC, dCs);
   }
   return hipGetLastError();
 }

@@ -75,7 +75,8 @@ struct FastPlanDev {
   int npad = 0;
   const int4* bwd_pl = nullptr;       // dC and q = C^T u, per input pair
   const uint32_t* fwd_em = nullptr;   // round-end masks of the forward streams
-  const uint2* bwd_st = nullptr;      // (slot word, plan index)
+  const uint32_t* bwd_st = nullptr;   // slot words
+  const uint32_t* bwd_dst = nullptr;  // per backward slot: its coefficient slot, ~0 for padding
   int bwd_slots = 0;                  // 64 * backward stream rows = dC partials per tile
   float* coef_bwd = nullptr;          // [batch][bwd_slots + 256]: c in backward slot order
   const int* bwd_pos = nullptr;       // per coefficient slot: its backward slot (padding: bwd_slots)

@@ -415,21 +415,18 @@ __device__ __forceinline__ void fwd_compute(const FwdChunk& ch, int n, unsigned 
 // ---------------------------------------------------------------- backward stream chunks
 
 struct BwdEntries {
-  u32x2 en[kCh];   // (slot word, coefficient slot)
+  unsigned en[kCh];   // slot words
 };
 
 // Rows k0 .. k0+kCh-1 of a backward stream (`st` = its first row, len a multiple of 4), four
 // rows (32 bytes) per lane in two 16-byte loads; groups past the end re-read the last group.
-__device__ __forceinline__ void bwd_load_entries(const uint2* __restrict__ st, int len, int k0, int lane,
+__device__ __forceinline__ void bwd_load_entries(const unsigned* __restrict__ st, int len, int k0, int lane,
                                                  BwdEntries& ch) {
 #pragma unroll
   for (int g = 0; g < kCh / 4; ++g) {
-    const FF_GLOBAL u32x4* p = gld(reinterpret_cast<const u32x4*>(st + 256L * min(k0 / 4 + g, len / 4 - 1)));
-    const u32x4 lo = p[2 * lane], hi = p[2 * lane + 1];
-    ch.en[4 * g + 0] = u32x2{lo[0], lo[1]};
-    ch.en[4 * g + 1] = u32x2{lo[2], lo[3]};
-    ch.en[4 * g + 2] = u32x2{hi[0], hi[1]};
-    ch.en[4 * g + 3] = u32x2{hi[2], hi[3]};
+    const u32x4 w = gld(reinterpret_cast<const u32x4*>(st + 256L * min(k0 / 4 + g, len / 4 - 1)))[lane];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ch.en[4 * g + j] = w[j];
   }
 }
 
@@ -460,7 +457,7 @@ __device__ __forceinline__ void bwd_sddmm(const BwdEntries& ch, int n, int k0,
       u32x4 uv[2], zv[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const unsigned e = ch.en[4 * g + h + i].x;
+        const unsigned e = ch.en[4 * g + h + i];
         uv[i] = lds_src(e);
         zv[i] = lds_at(tile, tile_off(e));
       }
@@ -487,13 +484,13 @@ __device__ __forceinline__ void bwd_spmm(const BwdEntries& ch, const float (&cc)
   for (int h = 0; h < 2; ++h) {
     u32x4 uv[kH];
 #pragma unroll
-    for (int i = 0; i < kH; ++i) uv[i] = lds_src(ch.en[h * kH + i].x);
+    for (int i = 0; i < kH; ++i) uv[i] = lds_src(ch.en[h * kH + i]);
 #pragma unroll
     for (int i = 0; i < kH; ++i) {
       if (h * kH + i < n) {   // uniform
         unsigned ce, co;
         coef_words(cc[h * kH + i], scale, ce, co);
-        accum_row(ch.en[h * kH + i].x, ce, co, uv[i], tile, a);
+        accum_row(ch.en[h * kH + i], ce, co, uv[i], tile, a);
       }
     }
   }
@@ -647,7 +644,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
 
 template <bool DX, bool DC, bool BETA>
 __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __restrict__ pl,
-                                                      const uint2* __restrict__ bst) {
+                                                      const unsigned* __restrict__ bst) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* uL = smem;                                        // m rows x 8 tokens x 2 bytes
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -692,7 +689,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
     auto pair = [&](int p, BwdEntries& ch, BwdEntries& chn) {
       prio_by_progress((p - wave) / kWaves, steps);
       const int len = q.y;
-      const uint2* st = bst + (long)q.x * 64;
+      const unsigned* st = bst + (long)q.x * 64;
       const int4 qn = pl[min(p + kWaves, lastp)];
       bwd_load_entries(bst + (long)qn.x * 64, qn.y, 0, lane, chn);
       issue_point();
@@ -737,7 +734,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
     auto pair = [&](int p, BwdEntries& ch, float (&cc)[kCh], BwdEntries& chn, float (&ccn)[kCh]) {
       prio_by_progress((DC ? npw : 0) + (p - wave) / kWaves, steps);
       const int len = q.y;
-      const uint2* st = bst + (long)q.x * 64;
+      const unsigned* st = bst + (long)q.x * 64;
       const float* cbp = cbw + (long)q.x * 64;
       const int4 qn = pl[min(p + kWaves, lastp)];
       bwd_load_entries(bst + (long)qn.x * 64, qn.y, 0, lane, chn);
@@ -796,7 +793,7 @@ constexpr int kRedWaves = 16;
 constexpr int kRedBatch = 8;
 
 __global__ void __launch_bounds__(64 * kRedWaves) reduce128(const float* __restrict__ partial, long ntiles,
-                                                            int slots, int pstride, const uint2* __restrict__ bst,
+                                                            int slots, int pstride, const unsigned* __restrict__ dst,
                                                             float scale, int accumulate, float* dC,
                                                             float* const* dCs, const int* __restrict__ pad,
                                                             int npad, int nred) {
@@ -830,10 +827,10 @@ __global__ void __launch_bounds__(64 * kRedWaves) reduce128(const float* __restr
     float tot = 0.f;
 #pragma unroll
     for (int i = 0; i < kRedWaves; ++i) tot += red[i][lane];
-    const u32x2 en = gld(reinterpret_cast<const u32x2*>(bst))[slot];
-    if (en.x & kSlotValid) {
+    const unsigned j = gld(dst)[slot];   // the slot's coefficient slot, or ~0 for padding
+    if (j != ~0u) {
       const float v = scale * tot;
-      gst(out)[en.y] = accumulate ? gld(out)[en.y] + v : v;
+      gst(out)[j] = accumulate ? gld(out)[j] + v : v;
     }
   }
 }
@@ -962,7 +959,7 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
     const dim3 grid((unsigned)ntiles, (unsigned)count);
     const size_t lds = fast128_lds_bytes(a.nblk_out);
     const int4* pl = p->fast.bwd_pl;
-    const uint2* st = p->fast.bwd_st;
+    const unsigned* st = p->fast.bwd_st;
     const bool beta = beta_dx != 0.f;
     rec(e0, s);
     if (want_dx && want_dc && beta)
@@ -986,7 +983,7 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
     if (nred + nzero > 0) {
       const dim3 grid((unsigned)(nred + nzero), (unsigned)count);
       hipLaunchKernelGGL(reduce128, grid, dim3(64 * kRedWaves), 0, s, p->partial, ntiles, a.slots, a.pstride,
-                         p->fast.bwd_st, scale, accumulate_dc, dC, dCs, p->fast.pad, npad, nred);
+                         p->fast.bwd_dst, scale, accumulate_dc, dC, dCs, p->fast.pad, npad, nred);
     }
   }
   return hipGetLastError();

@@ -468,6 +468,12 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   p->user_order = std::move(user_of_slot);
   p->coef_slots = nslot;
   const int64_t fast_tiles = fast ? (max_tokens + ff::kFastTileTokens - 1) / ff::kFastTileTokens : 0;
+  // the backward stream as the kernel's slot words and the reduction's destinations
+  std::vector<uint32_t> b_w(b_st.size()), b_dst(b_st.size());
+  for (size_t i = 0; i < b_st.size(); ++i) {
+    b_w[i] = b_st[i].x;
+    b_dst[i] = (b_st[i].x & ff::kSlotValid) ? b_st[i].y : ~0u;
+  }
 
   // ---------------- device memory: one allocation for every table and the workspace
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -486,12 +492,12 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       {mrg_ent.data(), mrg_ent.size() * sizeof(int4)},
       {f_pl.data(), f_pl.size() * sizeof(int4)},      {b_pl.data(), b_pl.size() * sizeof(int4)},
       {f_st.data(), f_st.size() * sizeof(uint32_t)},  {pad_slots.data(), pad_slots.size() * sizeof(int)},
-      {b_st.data(), b_st.size() * sizeof(uint2)},
+      {b_w.data(), b_w.size() * sizeof(uint32_t)},
       {nullptr, std::max<size_t>(partial_elems, 1) * sizeof(float)},
       // the backward's coefficients in its stream's slot order, per adapter (+ a scratch group)
       {nullptr, std::max<size_t>((size_t)max_batch * (b_st.size() + 256), 1) * sizeof(float)},
       {bwd_pos.data(), bwd_pos.size() * sizeof(int)},
-      {f_em.data(), f_em.size() * sizeof(uint32_t)}};
+      {f_em.data(), f_em.size() * sizeof(uint32_t)},  {b_dst.data(), b_dst.size() * sizeof(uint32_t)}};
   size_t total = 0;
   for (const Blob& b : blobs) total += up(b.bytes);
   int cur = 0;
@@ -544,7 +550,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   fp.fwd_st = (const uint32_t*)where[11];
   fp.pad = (const int*)where[12];
   fp.npad = (int)pad_slots.size();
-  fp.bwd_st = (const uint2*)where[13];
+  fp.bwd_st = (const uint32_t*)where[13];
+  fp.bwd_dst = (const uint32_t*)where[18];
   fp.bwd_slots = (int)b_st.size();
   p->partial = (float*)where[14];
   fp.coef_bwd = (float*)where[15];

@@ -64,9 +64,8 @@ struct PlanDev {
 
 // Entry streams of the 128-wide fused kernels: per pair of adjacent 128-wide
 // blocks, `len` rows of 64 lane slots starting at stream row `off`.  Pair entries: (off, len,
-// mask_off, first mask word).  The forward's streams run in rounds whose last rows are marked
-// in a bit mask (bit r of word r / 32 at `mask_off`; the first word is also kept in the
-// entry); the backward's streams end rows per lane (mask fields unused).
+// mask_off, first mask word).  The streams run in rounds whose last rows are marked in a bit
+// mask (bit r of word r / 32 at `mask_off`; the first word is also kept in the entry).
 struct FastPlanDev {
   int enabled = 0;
   const int4* fwd_pl = nullptr;       // v = C z, per output pair
@@ -75,6 +74,9 @@ struct FastPlanDev {
   int npad = 0;
   const int4* bwd_pl = nullptr;       // dC and q = C^T u, per input pair
   const uint32_t* fwd_em = nullptr;   // round-end masks of the forward streams
+  const uint32_t* bwd_em = nullptr;   // round-end masks of the backward streams
+  const int* bwd_pad = nullptr;       // backward slots that hold no entry
+  int nbpad = 0;
   const uint32_t* bwd_st = nullptr;   // slot words
   const uint32_t* bwd_dst = nullptr;  // per backward slot: its coefficient slot, ~0 for padding
   int bwd_slots = 0;                  // 64 * backward stream rows = dC partials per tile
@@ -159,8 +161,8 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
                          const float* c_saved, hipStream_t s);
 constexpr int kFastTileTokens = 8;
 
-// Slot words of the 128-wide kernels' entry streams: end flag (bit 0: the lane's row ends at
-// this slot in the backward, or with the round that ends at this slot in the forward), valid flag (bit 1: the slot holds an entry;
+// Slot words of the 128-wide kernels' entry streams: restart flag (bit 0: the lane's row ends
+// with the round that ends at this slot), valid flag (bit 1: the slot holds an entry;
 // padding slots have zero coefficients), the byte offset of the source row in the LDS
 // coefficient array (rows of 16 bytes; bits 4..19) and the byte offset of the lane's current
 // row in the pair tile (rows of 32 bytes, one per coefficient, holding both blocks' 8 tokens;

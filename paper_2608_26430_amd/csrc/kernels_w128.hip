@@ -342,24 +342,6 @@ __device__ __forceinline__ void accum_slot(unsigned e, unsigned ce, unsigned co,
   }
 }
 
-// a[t] += c z[t] for the 8 tokens of one source row; at the end of the lane's row, write it to
-// the tile position named by the slot word and restart (the backward's streams).
-__device__ __forceinline__ void accum_row(unsigned e, unsigned ce, unsigned co, const u32x4 zv, unsigned char* tile,
-                                          float (&a)[8]) {
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const unsigned w = zv[j];
-    a[2 * j] = dot2(w, ce, a[2 * j]);
-    a[2 * j + 1] = dot2(w, co, a[2 * j + 1]);
-  }
-  if (e & kSlotEnd) {
-    *reinterpret_cast<u32x4*>(tile + tile_off(e)) =
-        u32x4{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(a[4], a[5]), pack_bf2(a[6], a[7])};
-#pragma unroll
-    for (int j = 0; j < 8; ++j) a[j] = 0.f;
-  }
-}
-
 // Round-end bits of stream rows k0 .. k0+31 of a pair (bit i: row k0 + i ends a round).  Row
 // mask words beyond the first come from the mask table (scalar loads: uniform address).
 __device__ __forceinline__ unsigned chunk_ends(const int4& q, const unsigned* __restrict__ em, int k0) {
@@ -477,8 +459,8 @@ __device__ __forceinline__ void bwd_sddmm(const BwdEntries& ch, int n, int k0,
   }
 }
 
-__device__ __forceinline__ void bwd_spmm(const BwdEntries& ch, const float (&cc)[kCh], int n, float scale,
-                                         unsigned char* tile, float (&a)[8]) {
+__device__ __forceinline__ void bwd_spmm(const BwdEntries& ch, const float (&cc)[kCh], int n, unsigned ends,
+                                         float scale, unsigned char* tile, float (&a)[8]) {
   constexpr int kH = kCh / 2;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -490,7 +472,7 @@ __device__ __forceinline__ void bwd_spmm(const BwdEntries& ch, const float (&cc)
       if (h * kH + i < n) {   // uniform
         unsigned ce, co;
         coef_words(cc[h * kH + i], scale, ce, co);
-        accum_row(ch.en[h * kH + i], ce, co, uv[i], tile, a);
+        accum_slot(ch.en[h * kH + i], ce, co, uv[i], (ends >> (h * kH + i)) & 1u, tile, a);
       }
     }
   }
@@ -514,6 +496,8 @@ struct FastArgs {
   float* csave;       // forward: where to write that copy, [batch][slots + 256]
   const int* pos;     // per coefficient slot: its backward slot (padding: the scratch slot)
   int nslot;          // coefficient slots (>= 256 on this path)
+  const int* bpad;    // backward slots with no entry: their copied coefficient is zero
+  int nbpad;          // >= 1 (the scratch slot stands in when there is none)
   float scale, beta;
   int slots;          // dC partials per tile
   int pstride;        // floats per tile in the partial workspace: slots + a scratch row group
@@ -572,14 +556,18 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   const float* cv = a.cs ? a.cs[bi] : a.c;
   const int npo = a.nblk_out / 2, lastp = npo - 1;
 
-  // This workgroup's share of the coefficient copy in the backward's slot order (read first,
-  // written after the analysis).  Every lane loads and stores: lanes past the share repeat its
-  // last slot, an identical write.
-  const int per = (a.nslot + (int)gridDim.x - 1) / (int)gridDim.x;
-  const int j0 = (int)blockIdx.x * per, jn = min(a.nslot, j0 + per);
+  // This workgroup's share of the coefficient copy in the backward's slot order: coefficient
+  // slots, then the backward's padding slots (zero).  Read first, written after the analysis;
+  // every lane loads and stores (lanes past the share repeat its last item, an identical write).
+  const int nitem = a.nslot + a.nbpad;
+  const int per = (nitem + (int)gridDim.x - 1) / (int)gridDim.x;
+  const int j0 = (int)blockIdx.x * per, jn = min(nitem, j0 + per);
   const int js = max(min(j0 + (int)threadIdx.x, jn - 1), 0);
-  const int spos = gld(a.pos)[js];
-  const float sval = gld(cv)[js];
+  const bool is_coef = js < a.nslot;
+  const int pc = gld(a.pos)[min(js, a.nslot - 1)], pp = gld(a.bpad)[min(max(js - a.nslot, 0), a.nbpad - 1)];
+  const float cval = gld(cv)[min(js, a.nslot - 1)];
+  const int spos = is_coef ? pc : pp;
+  const float sval = is_coef ? cval : 0.f;
   float* csave = a.csave + (long)bi * (a.slots + 256);
 
   u32x4 fr[kFragPerThread];
@@ -639,12 +627,18 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   }
   // shares longer than one slot per thread (grids of few tiles)
   if (per > kThreads)
-    for (int j = j0 + kThreads + (int)threadIdx.x; j < jn; j += kThreads) gst(csave)[gld(a.pos)[j]] = gld(cv)[j];
+    for (int j = j0 + kThreads + (int)threadIdx.x; j < jn; j += kThreads) {
+      if (j < a.nslot)
+        gst(csave)[gld(a.pos)[j]] = gld(cv)[j];
+      else
+        gst(csave)[gld(a.bpad)[j - a.nslot]] = 0.f;
+    }
 }
 
 template <bool DX, bool DC, bool BETA>
 __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __restrict__ pl,
-                                                      const unsigned* __restrict__ bst) {
+                                                      const unsigned* __restrict__ bst,
+                                                      const unsigned* __restrict__ em) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* uL = smem;                                        // m rows x 8 tokens x 2 bytes
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -743,14 +737,14 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
       // q = C^T u for this pair, then dX = beta dX + s P_in q
       zero_tile(tile, lane);
       float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      bwd_spmm(ch, cc, min(kCh, len), a.scale, tile, acc8);
+      bwd_spmm(ch, cc, min(kCh, len), (unsigned)q.w, a.scale, tile, acc8);
       if (len > kCh) {   // long stream
         for (int k0 = kCh; k0 < len; k0 += kCh) {
           BwdEntries ck;
           float ckc[kCh];
           bwd_load_entries(st, len, k0, lane, ck);
           bwd_load_coeffs(cbp, len, k0, lane, ckc);
-          bwd_spmm(ck, ckc, min(kCh, len - k0), a.scale, tile, acc8);
+          bwd_spmm(ck, ckc, min(kCh, len - k0), chunk_ends(q, em, k0), a.scale, tile, acc8);
         }
         vm_wait_all();
       }
@@ -775,13 +769,18 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
 // order (one coalesced load per coefficient, no dependent load), so that it loads them like the
 // forward does.  Padding slots go to a scratch slot past the backward slots.
 __global__ void __launch_bounds__(256) scatter_bwd_coef(const float* c, const float* const* cs,
-                                                        const int* __restrict__ pos, int nslot, int cstride,
+                                                        const int* __restrict__ pos, int nslot,
+                                                        const int* __restrict__ bpad, int nbpad, int cstride,
                                                         float* cb) {
   const int bi = blockIdx.y;
   const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= nslot) return;
-  const float* cv = cs ? cs[bi] : c;
-  gst(cb)[(long)bi * cstride + gld(pos)[j]] = gld(cv)[j];
+  if (j >= nslot + nbpad) return;
+  if (j < nslot) {
+    const float* cv = cs ? cs[bi] : c;
+    gst(cb)[(long)bi * cstride + gld(pos)[j]] = gld(cv)[j];
+  } else {
+    gst(cb)[(long)bi * cstride + gld(bpad)[j - nslot]] = 0.f;   // padding of the backward order
+  }
 }
 
 // dC[j] = [dC[j] +] s * sum_tiles partial[tile][slot] for every valid slot of the backward
@@ -883,6 +882,8 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   a.csave = c_saved ? c_saved : p->fast.coef_bwd;
   a.pos = p->fast.bwd_pos;
   a.nslot = p->fast.coef_slots;
+  a.bpad = p->fast.bwd_pad;
+  a.nbpad = p->fast.nbpad;
   a.slots = p->fast.bwd_slots;
   a.frag = p->fout->dev.fs16;
   a.T = T;
@@ -904,8 +905,9 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   take_timing_events(&e0, &e1);
   if (T == 0) {   // no tiles: the copy alone
     if (!c_saved) return hipSuccess;
-    const dim3 g((unsigned)((a.nslot + 255) / 256), (unsigned)count);
-    hipLaunchKernelGGL(scatter_bwd_coef, g, dim3(256), 0, s, c, cs, a.pos, a.nslot, a.slots + 256, c_saved);
+    const dim3 g((unsigned)((a.nslot + a.nbpad + 255) / 256), (unsigned)count);
+    hipLaunchKernelGGL(scatter_bwd_coef, g, dim3(256), 0, s, c, cs, a.pos, a.nslot, a.bpad, a.nbpad, a.slots + 256,
+                       c_saved);
     return hipGetLastError();
   }
   rec(e0, s);
@@ -951,27 +953,28 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   take_timing_events(&e0, &e1);
   if (T > 0 && want_dx && !c_saved) {
     const int nslot = p->fast.coef_slots;
-    const dim3 g((unsigned)((nslot + 255) / 256), (unsigned)count);
-    hipLaunchKernelGGL(scatter_bwd_coef, g, dim3(256), 0, s, c, cs, p->fast.bwd_pos, nslot, a.slots + 256,
-                       p->fast.coef_bwd);
+    const dim3 g((unsigned)((nslot + p->fast.nbpad + 255) / 256), (unsigned)count);
+    hipLaunchKernelGGL(scatter_bwd_coef, g, dim3(256), 0, s, c, cs, p->fast.bwd_pos, nslot, p->fast.bwd_pad,
+                       p->fast.nbpad, a.slots + 256, p->fast.coef_bwd);
   }
   if (T > 0 && (want_dx || want_dc)) {
     const dim3 grid((unsigned)ntiles, (unsigned)count);
     const size_t lds = fast128_lds_bytes(a.nblk_out);
     const int4* pl = p->fast.bwd_pl;
     const unsigned* st = p->fast.bwd_st;
+    const unsigned* em = p->fast.bwd_em;
     const bool beta = beta_dx != 0.f;
     rec(e0, s);
     if (want_dx && want_dc && beta)
-      hipLaunchKernelGGL((bwd128<true, true, true>), grid, dim3(kThreads), lds, s, a, pl, st);
+      hipLaunchKernelGGL((bwd128<true, true, true>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else if (want_dx && want_dc)
-      hipLaunchKernelGGL((bwd128<true, true, false>), grid, dim3(kThreads), lds, s, a, pl, st);
+      hipLaunchKernelGGL((bwd128<true, true, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else if (want_dx && beta)
-      hipLaunchKernelGGL((bwd128<true, false, true>), grid, dim3(kThreads), lds, s, a, pl, st);
+      hipLaunchKernelGGL((bwd128<true, false, true>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else if (want_dx)
-      hipLaunchKernelGGL((bwd128<true, false, false>), grid, dim3(kThreads), lds, s, a, pl, st);
+      hipLaunchKernelGGL((bwd128<true, false, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else
-      hipLaunchKernelGGL((bwd128<false, true, false>), grid, dim3(kThreads), lds, s, a, pl, st);
+      hipLaunchKernelGGL((bwd128<false, true, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     rec(e1, s);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

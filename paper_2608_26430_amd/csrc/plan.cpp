@@ -47,32 +47,7 @@ uint32_t tile_byte(int par, int local) {
   return (uint32_t)(row * 32 + 16 * (par ^ b2));
 }
 
-// Rows of one pair of blocks assigned whole to 64 lanes, longest first, each to the least
-// loaded lane (the backward's order: every row end is tested per lane).  Returns, per lane,
-// its rows in order, and the largest lane load.
-std::vector<std::vector<int>> assign_lanes(const std::vector<int>& row_size, int& len) {
-  std::vector<int> order;
-  for (int r = 0; r < (int)row_size.size(); ++r)
-    if (row_size[r] > 0) order.push_back(r);
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return row_size[a] > row_size[b]; });
-  std::vector<int> load(64, 0);
-  std::vector<std::vector<int>> lane_rows(64);
-  for (int r : order) {
-    const int l = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-    lane_rows[l].push_back(r);
-    load[l] += row_size[r];
-  }
-  // lanes renumbered by decreasing load: in every stream row the occupied slots are a prefix
-  std::vector<int> lanes(64);
-  std::iota(lanes.begin(), lanes.end(), 0);
-  std::stable_sort(lanes.begin(), lanes.end(), [&](int a, int b) { return load[a] > load[b]; });
-  std::vector<std::vector<int>> out(64);
-  for (int l = 0; l < 64; ++l) out[l] = lane_rows[lanes[l]];
-  len = load[lanes[0]];
-  return out;
-}
-
-// Round schedule of the rows of one pair of blocks for the 128-wide forward kernel.  All 64 lanes of
+// Round schedule of the rows of one pair of blocks for the 128-wide kernels.  All 64 lanes of
 // a wave run the same rounds, of L[0..R-1] slots; at the end of every round each lane writes
 // its current row to the pair tile, so row ends cost no per-slot test.  A row fills one or
 // more consecutive rounds of one lane, the rest of its last round being padding slots with
@@ -363,7 +338,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
                     n < 65536 && m < 65536 &&
                     ff::fast128_lds_bytes(std::max(FI.nblk, FO.nblk)) <= (size_t)ff::kMaxLdsBytes;
   std::vector<int4> f_pl, b_pl;   // per pair: (first stream row, stream rows, mask offset, mask word 0)
-  std::vector<uint32_t> f_em;   // round-end masks of the forward streams
+  std::vector<uint32_t> f_em, b_em;   // round-end masks
   std::vector<int> pad_slots;
   std::vector<uint32_t> f_st;
   std::vector<uint2> b_st;
@@ -381,7 +356,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       brows[cloc[e].blk / 2][(cloc[e].blk & 1) * 128 + cloc[e].local].push_back((int)e);
     }
     // modelled VALU work per slot and per round end of the two kernels' sparse phases
-    constexpr int kFwdSlotCost = 11, kEndCost = 15;
+    constexpr int kFwdSlotCost = 11, kBwdSlotCost = 17, kEndCost = 15;
     std::vector<uint32_t> mask;
     for (int pp = 0; pp < npo; ++pp) {
       std::vector<int> sz(256);
@@ -417,25 +392,22 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     for (int pp = 0; pp < npi; ++pp) {
       std::vector<int> sz(256);
       for (int r = 0; r < 256; ++r) sz[r] = (int)brows[pp][r].size();
-      int len = 0;
-      const auto lanes = assign_lanes(sz, len);
-      len = std::max((len + 3) / 4 * 4, 4);   // whole 4-row groups; every stream has one
+      const PairSchedule ps = schedule_pair(sz, kBwdSlotCost, kEndCost);
       const int64_t row0 = (int64_t)(b_st.size() / 64);
-      b_pl.push_back(make_int4((int)row0, len, 0, 0));
-      b_st.resize(b_st.size() + (size_t)len * 64, make_uint2(0u, 0u));
-      for (int l = 0; l < 64; ++l) {
-        int k = 0;
-        for (int r : lanes[l])
-          for (size_t i = 0; i < brows[pp][r].size(); ++i, ++k) {
-            const int e = brows[pp][r][i];
-            const bool last = i + 1 == brows[pp][r].size();
-            bwd_slot_of_user[e] = (int)ff::fast_slot(row0, k, l);
-            b_st[(size_t)ff::fast_slot(row0, k, l)] = make_uint2(
-                lsrc(rloc[e]) | (tile_byte(r >> 7, r & 127) << ff::kSlotDstShift) | ff::kSlotValid |
-                    (last ? ff::kSlotEnd : 0u),
-                (unsigned)slot_of_user[e]);
-          }
-      }
+      const int len = emit_pair(
+          ps, brows[pp], [&](int e) { return lsrc(rloc[e]); },
+          [&](int r) { return tile_byte(r >> 7, r & 127) << ff::kSlotDstShift; },
+          [&](int k, int l, uint32_t w, int e) {
+            const size_t slot = (size_t)ff::fast_slot(row0, k, l);
+            if (slot >= b_st.size()) b_st.resize(slot / 256 * 256 + 256, make_uint2(0u, 0u));
+            b_st[slot] = make_uint2(w, e >= 0 ? (unsigned)slot_of_user[e] : 0u);
+            if (e >= 0) bwd_slot_of_user[e] = (int)slot;
+          },
+          mask);
+      if (len < 0) return ff::fail(FF_EUNSUPPORTED, "internal: no row for a lane of input pair %d", pp);
+      b_pl.push_back(make_int4((int)row0, len, (int)b_em.size(), (int)mask[0]));
+      b_em.insert(b_em.end(), mask.begin(), mask.end());
+      b_st.resize((size_t)(row0 + len) * 64, make_uint2(0u, 0u));
     }
   } else {
     // the generic kernels' layout is the forward table's entry order, so the forward reads a
@@ -470,10 +442,13 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   const int64_t fast_tiles = fast ? (max_tokens + ff::kFastTileTokens - 1) / ff::kFastTileTokens : 0;
   // the backward stream as the kernel's slot words and the reduction's destinations
   std::vector<uint32_t> b_w(b_st.size()), b_dst(b_st.size());
+  std::vector<int> b_pad;   // backward slots that hold no entry (zero coefficients in any copy)
   for (size_t i = 0; i < b_st.size(); ++i) {
     b_w[i] = b_st[i].x;
     b_dst[i] = (b_st[i].x & ff::kSlotValid) ? b_st[i].y : ~0u;
+    if (!(b_st[i].x & ff::kSlotValid)) b_pad.push_back((int)i);
   }
+  if (b_pad.empty()) b_pad.push_back((int)b_st.size());   // the copy's scratch slot stands in
 
   // ---------------- device memory: one allocation for every table and the workspace
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -497,7 +472,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       // the backward's coefficients in its stream's slot order, per adapter (+ a scratch group)
       {nullptr, std::max<size_t>((size_t)max_batch * (b_st.size() + 256), 1) * sizeof(float)},
       {bwd_pos.data(), bwd_pos.size() * sizeof(int)},
-      {f_em.data(), f_em.size() * sizeof(uint32_t)},  {b_dst.data(), b_dst.size() * sizeof(uint32_t)}};
+      {f_em.data(), f_em.size() * sizeof(uint32_t)},  {b_dst.data(), b_dst.size() * sizeof(uint32_t)},
+      {b_em.data(), b_em.size() * sizeof(uint32_t)},  {b_pad.data(), b_pad.size() * sizeof(int)}};
   size_t total = 0;
   for (const Blob& b : blobs) total += up(b.bytes);
   int cur = 0;
@@ -552,6 +528,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   fp.npad = (int)pad_slots.size();
   fp.bwd_st = (const uint32_t*)where[13];
   fp.bwd_dst = (const uint32_t*)where[18];
+  fp.bwd_em = (const uint32_t*)where[19];
+  fp.bwd_pad = (const int*)where[20];
+  fp.nbpad = (int)b_pad.size();
   fp.bwd_slots = (int)b_st.size();
   p->partial = (float*)where[14];
   fp.coef_bwd = (float*)where[15];

@@ -592,11 +592,16 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   // a whole pair ahead of its use.  The loop runs two pairs per iteration with the buffers'
   // roles swapped, so no chunk is ever copied between registers.
   const int steps = (npo - wave + kWaves - 1) / kWaves;
+  // A pair's synthesis is stored at the start of the wave's next pair, after that pair's
+  // stream loads: the loads do not queue behind the stores, and the MFMA results are waited
+  // for a whole sparse phase later.
+  f32x4 acc[kMT];
   auto pair = [&](int p, FwdChunk& cur, FwdChunk& nxt) {
     prio_by_progress((p - wave) / kWaves, steps);
     fwd_load(fst, qn.x, qn.y, 0, cv, lane, nxt);
     const int4 qnn = pl[min(p + 2 * kWaves, lastp)];
     issue_point();
+    if (p != wave) store_act<BETA>(Y, a.ldy, nt, 2 * (p - kWaves), lane, acc, a.beta);
     // v = C z for this pair into the tile
     const int off = q.x, len = q.y;
     zero_tile(tile, lane);
@@ -612,19 +617,23 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
     wave_lds_fence();
     // y = beta y + s P_out v
     u32x4 b[kKT];
-    f32x4 acc[kMT];
     load_tile_act(tile, lane, b);
     wave_lds_fence();
     mfma_block(F, b, acc);
-    store_act<BETA>(Y, a.ldy, nt, 2 * p, lane, acc, a.beta);
     q = qn;
     qn = qnn;
   };
   FwdChunk ch2;
+  int plast = wave;
   for (int p = wave; p < npo; p += 2 * kWaves) {
     pair(p, ch, ch2);
-    if (p + kWaves < npo) pair(p + kWaves, ch2, ch);
+    plast = p;
+    if (p + kWaves < npo) {
+      pair(p + kWaves, ch2, ch);
+      plast = p + kWaves;
+    }
   }
+  if (wave < npo) store_act<BETA>(Y, a.ldy, nt, 2 * plast, lane, acc, a.beta);
   // shares longer than one slot per thread (grids of few tiles)
   if (per > kThreads)
     for (int j = j0 + kThreads + (int)threadIdx.x; j < jn; j += kThreads) {

@@ -53,6 +53,8 @@
 // skipped, the rare long-stream paths end with an explicit full wait, the
 // output options are template parameters rather than branches, and the loads a
 // pair needs are issued before the previous pair's stores.
+#include <type_traits>
+
 #include "ff_internal.h"
 
 namespace ff {
@@ -595,13 +597,16 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   // A pair's synthesis is stored at the start of the wave's next pair, after that pair's
   // stream loads: the loads do not queue behind the stores, and the MFMA results are waited
   // for a whole sparse phase later.
+  // The wave's first pair is a separate instance with no store, so that every other instance
+  // stores unconditionally and the compiler's memory counters stay exact (a store that may or
+  // may not have been issued makes it wait for all of them).
   f32x4 acc[kMT];
-  auto pair = [&](int p, FwdChunk& cur, FwdChunk& nxt) {
+  auto pair = [&](int p, FwdChunk& cur, FwdChunk& nxt, auto first) {
     prio_by_progress((p - wave) / kWaves, steps);
     fwd_load(fst, qn.x, qn.y, 0, cv, lane, nxt);
     const int4 qnn = pl[min(p + 2 * kWaves, lastp)];
     issue_point();
-    if (p != wave) store_act<BETA>(Y, a.ldy, nt, 2 * (p - kWaves), lane, acc, a.beta);
+    if constexpr (!decltype(first)::value) store_act<BETA>(Y, a.ldy, nt, 2 * (p - kWaves), lane, acc, a.beta);
     // v = C z for this pair into the tile
     const int off = q.x, len = q.y;
     zero_tile(tile, lane);
@@ -624,16 +629,25 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
     qn = qnn;
   };
   FwdChunk ch2;
-  int plast = wave;
-  for (int p = wave; p < npo; p += 2 * kWaves) {
-    pair(p, ch, ch2);
-    plast = p;
-    if (p + kWaves < npo) {
-      pair(p + kWaves, ch2, ch);
-      plast = p + kWaves;
+  if (wave < npo) {
+    const std::true_type first;
+    const std::false_type later;
+    int plast = wave;
+    pair(wave, ch, ch2, first);
+    if (wave + kWaves < npo) {
+      pair(wave + kWaves, ch2, ch, later);
+      plast = wave + kWaves;
     }
+    for (int p = wave + 2 * kWaves; p < npo; p += 2 * kWaves) {
+      pair(p, ch, ch2, later);
+      plast = p;
+      if (p + kWaves < npo) {
+        pair(p + kWaves, ch2, ch, later);
+        plast = p + kWaves;
+      }
+    }
+    store_act<BETA>(Y, a.ldy, nt, 2 * plast, lane, acc, a.beta);
   }
-  if (wave < npo) store_act<BETA>(Y, a.ldy, nt, 2 * plast, lane, acc, a.beta);
   // shares longer than one slot per thread (grids of few tiles)
   if (per > kThreads)
     for (int j = j0 + kThreads + (int)threadIdx.x; j < jn; j += kThreads) {

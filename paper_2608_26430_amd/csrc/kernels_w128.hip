@@ -256,26 +256,53 @@ __device__ __forceinline__ void load_tile_act(const unsigned char* tile, int lan
 
 // y[t][(blk0+bs)*128 + o] = acc (+ beta * y); the scale s is already in the coefficients.  Token
 // columns past the tile's end hold the last token's values and write them to its row again.
+// Without beta the result is first transposed through the wave's pair tile (free at this point),
+// so that each store instruction writes four whole 256-byte token rows rather than sixteen 32-byte
+// pieces: tile row n = 8 bs + t holds the row's 16-byte chunks c at position c ^ n, which keeps
+// both the 8-byte writes of one row tile and the 16-byte reads of one token row on distinct banks.
+// With beta the old values are added in fp32 before the only rounding, so that path stores
+// directly.
 template <bool BETA>
 __device__ __forceinline__ void store_act(u16* rows, long ld, int nt, int blk0, int lane, const f32x4 (&acc)[kMT],
-                                          float beta) {
-  const int n = lane & 15, t = min(n & 7, nt - 1), bs = n >> 3, q = lane >> 4;
-  FF_GLOBAL u32x2* p = gst(reinterpret_cast<u32x2*>(rows + (long)t * ld + (blk0 + bs) * kW + 4 * q));
-  u32x2 old[kMT];
-  if (BETA) {
+                                          float beta, unsigned char* tile) {
+  if constexpr (!BETA) {
+    const int n = lane & 15, q = lane >> 4;
+    wave_lds_fence();
+#pragma unroll
+    for (int mt = 0; mt < kMT; ++mt) {
+      const unsigned pos = (unsigned)((2 * mt + (q >> 1)) ^ n);
+      *reinterpret_cast<u32x2*>(tile + n * 256 + pos * 16 + 8 * (q & 1)) =
+          u32x2{pack_bf2(acc[mt][0], acc[mt][1]), pack_bf2(acc[mt][2], acc[mt][3])};
+    }
+    wave_lds_fence();
+    u32x4 v[4];
+    const int c = lane & 15;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * i + (lane >> 4);
+      v[i] = *reinterpret_cast<const u32x4*>(tile + r * 256 + (unsigned)(c ^ r) * 16);
+    }
+    wave_lds_fence();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * i + (lane >> 4), t = min(r & 7, nt - 1), bs = r >> 3;
+      *gst(reinterpret_cast<u32x4*>(rows + (long)t * ld + (blk0 + bs) * kW + 8 * c)) = v[i];
+    }
+  } else {
+    const int n = lane & 15, t = min(n & 7, nt - 1), bs = n >> 3, q = lane >> 4;
+    FF_GLOBAL u32x2* p = gst(reinterpret_cast<u32x2*>(rows + (long)t * ld + (blk0 + bs) * kW + 4 * q));
+    u32x2 old[kMT];
 #pragma unroll
     for (int mt = 0; mt < kMT; ++mt) old[mt] = p[4 * mt];
-  }
 #pragma unroll
-  for (int mt = 0; mt < kMT; ++mt) {
-    f32x4 r = acc[mt];
-    if (BETA) {
+    for (int mt = 0; mt < kMT; ++mt) {
+      f32x4 r = acc[mt];
       r[0] += beta * lo_bf(old[mt].x);
       r[1] += beta * hi_bf(old[mt].x);
       r[2] += beta * lo_bf(old[mt].y);
       r[3] += beta * hi_bf(old[mt].y);
+      p[4 * mt] = u32x2{pack_bf2(r[0], r[1]), pack_bf2(r[2], r[3])};
     }
-    p[4 * mt] = u32x2{pack_bf2(r[0], r[1]), pack_bf2(r[2], r[3])};
   }
 }
 
@@ -606,7 +633,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
     fwd_load(fst, qn.x, qn.y, 0, cv, lane, nxt);
     const int4 qnn = pl[min(p + 2 * kWaves, lastp)];
     issue_point();
-    if constexpr (!decltype(first)::value) store_act<BETA>(Y, a.ldy, nt, 2 * (p - kWaves), lane, acc, a.beta);
+    if constexpr (!decltype(first)::value) store_act<BETA>(Y, a.ldy, nt, 2 * (p - kWaves), lane, acc, a.beta, tile);
     // v = C z for this pair into the tile
     const int off = q.x, len = q.y;
     zero_tile(tile, lane);
@@ -646,7 +673,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
         plast = p + kWaves;
       }
     }
-    store_act<BETA>(Y, a.ldy, nt, 2 * plast, lane, acc, a.beta);
+    store_act<BETA>(Y, a.ldy, nt, 2 * plast, lane, acc, a.beta, tile);
   }
   // shares longer than one slot per thread (grids of few tiles)
   if (per > kThreads)
@@ -777,7 +804,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
       load_tile_act(tile, lane, b);
       wave_lds_fence();
       mfma_block(F, b, acc);
-      store_act<BETA>(dX, a.ldy, nt, 2 * p, lane, acc, a.beta);
+      store_act<BETA>(dX, a.ldy, nt, 2 * p, lane, acc, a.beta, tile);
       q = qn;
     };
     BwdEntries ch2;

@@ -534,38 +534,76 @@ struct FastArgs {
   long ntiles;
 };
 
-// Analysis of every pair of blocks of a tile into a coefficient-major LDS array, two pairs'
-// inputs in flight per wave.  Every load is issued and consumed on every path (a pair index
-// past the end is clamped to the last pair and only its LDS store is skipped), so the compiler
-// neither sinks a prefetch to its use nor falls back to full waits.
+// s_waitcnt vmcnt(n) (n < 16), other counters untouched.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
+// One 16-byte load per lane straight into LDS: lane l's bytes land at LDS address lds + 16 l
+// (lds wave-uniform).  Written as assembly because the compiler, which cannot tell which LDS
+// bytes such a load writes, would otherwise wait for every one of them before any LDS read;
+// the readers wait for exactly the loads they need with vm_wait, and the compiler, not knowing
+// these loads, can only over-count its own waits.
+__device__ __forceinline__ void dma16(const FF_GLOBAL void* src, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
+}
+
+// The input rows of one pair (16 rows of 256 bytes: row n = 8 bs + t, token columns past the
+// tile's end repeating its last token) loaded into the 4 KB at `dst` without passing through
+// registers, each load covering four whole rows; row n keeps its 16-byte chunk c at position
+// c ^ n.
+__device__ __forceinline__ void dma_rows(const u16* rows, long ld, int nt, int blk0, int lane, unsigned char* dst) {
+  const int pos = lane & 15;
+  const unsigned base = (unsigned)(size_t)(__attribute__((address_space(3))) unsigned char*)dst;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 4 * i + (lane >> 4), t = min(r & 7, nt - 1), bs = r >> 3;
+    dma16(gld(rows + (long)t * ld + (blk0 + bs) * kW + 8 * (pos ^ r)), base + 1024 * i);
+  }
+}
+
+// The analysis operand of a pair staged by dma_rows: lane (column n, k-group g) takes chunk
+// 4 ks + g of row n (inputs 32 ks + 8 g .. +7, as load_act would have loaded them).
+__device__ __forceinline__ void read_rows(const unsigned char* src, int lane, u32x4 (&b)[kKT]) {
+  const int n = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int ks = 0; ks < kKT; ++ks)
+    b[ks] = *reinterpret_cast<const u32x4*>(src + n * 256 + (unsigned)(((4 * ks + g) ^ n) * 16));
+}
+
+// Analysis of every pair of blocks of a tile into a coefficient-major LDS array.  Each pair's
+// inputs are staged in the pair's own 4 KB of the array, which its analysis overwrites only after
+// reading them (a wave's LDS operations execute in order), two pairs ahead.  Loads for pairs past
+// the end go to `spare` (the wave's free pair tile), so that every iteration issues the same
+// loads and the counted waits stay exact; they are all waited for before returning.
 __device__ __forceinline__ void analysis_phase(const Frag& F, const u16* rows, long ld, int nt, int np, int wave,
-                                               int lane, unsigned char* lds) {
+                                               int lane, unsigned char* lds, unsigned char* spare) {
   const int last = np - 1;
   const int n = lane & 15, q = lane >> 4;
   const unsigned off = ((q >> 1) * kW + n) * 16 + 8 * (q & 1);   // this lane's row of pair 0
   const unsigned sgn = (n & 1) ? 0x80008000u : 0u;               // odd coefficients negated
   constexpr unsigned kPairBytes = 2 * kW * kTT * 2;
-  u32x4 bA[kKT], bB[kKT];
-  load_act(rows, ld, nt, 2 * min(wave, last), lane, bA);
+  auto slot = [&](int p) { return p < np ? lds + p * kPairBytes : spare; };
+  wave_lds_fence();
+  dma_rows(rows, ld, nt, 2 * min(wave, last), lane, slot(wave));
+  dma_rows(rows, ld, nt, 2 * min(wave + kWaves, last), lane, slot(wave + kWaves));
   issue_point();
-  load_act(rows, ld, nt, 2 * min(wave + kWaves, last), lane, bB);
-  issue_point();
-  for (int p = wave; p < np; p += 2 * kWaves) {
-    {
-      f32x4 acc[kMT];
-      mfma_block_t(F, bA, acc, ~0u);
-      store_coef_t(lds + p * kPairBytes, off, acc, sgn);
-    }
-    load_act(rows, ld, nt, 2 * min(p + 2 * kWaves, last), lane, bA);
+  for (int p = wave; p < np; p += kWaves) {
+    vm_wait<4>();   // this pair's four loads (the next pair's four may still be in flight)
+    wave_lds_fence();
+    u32x4 b[kKT];
+    read_rows(slot(p), lane, b);
+    wave_lds_fence();
+    dma_rows(rows, ld, nt, 2 * min(p + 2 * kWaves, last), lane, slot(p + 2 * kWaves));
     issue_point();
-    {
-      f32x4 acc[kMT];
-      mfma_block_t(F, bB, acc, ~0u);
-      if (p + kWaves < np) store_coef_t(lds + (p + kWaves) * kPairBytes, off, acc, sgn);
-    }
-    load_act(rows, ld, nt, 2 * min(p + 3 * kWaves, last), lane, bB);
-    issue_point();
+    f32x4 acc[kMT];
+    mfma_block_t(F, b, acc, ~0u);
+    store_coef_t(lds + p * kPairBytes, off, acc, sgn);
   }
+  vm_wait_all();
+  wave_lds_fence();
 }
 
 // The stream tables are separate restrict-qualified arguments: the kernel never writes them,
@@ -613,7 +651,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
 
   Frag F;
   frag_stage(fr, reinterpret_cast<u32x4*>(smem), lane, F);
-  analysis_phase(F, X, a.ldx, nt, a.nblk_in / 2, wave, lane, zL);
+  analysis_phase(F, X, a.ldx, nt, a.nblk_in / 2, wave, lane, zL, tile);
   gst(csave)[spos] = sval;
   __syncthreads();
 
@@ -721,7 +759,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
 
   Frag F;
   frag_stage(fr, reinterpret_cast<u32x4*>(smem), lane, F);
-  analysis_phase(F, G, a.ldg, nt, a.nblk_out / 2, wave, lane, uL);
+  analysis_phase(F, G, a.ldg, nt, a.nblk_out / 2, wave, lane, uL, tile);
   __syncthreads();
 
   // Two passes over this wave's input pairs, so that each holds few registers: dC, then dX.

@@ -187,6 +187,11 @@ class Plan:
         """Length of the c_saved arrays of adapter_fwd(save=...) / adapter_bwd(saved=...) (0: none needed)."""
         return self.query(6)
 
+    @property
+    def bwd_tile_tokens(self) -> int:
+        """Tokens per workgroup tile of the fused 128-wide backward (16 or 8; 0 without it)."""
+        return self.query(7)
+
     def new_saved(self, device=None):
         """A c_saved array for one adapter of this plan (None when the plan needs none)."""
         torch = _torch()

@@ -83,6 +83,7 @@ struct FastPlanDev {
   float* coef_bwd = nullptr;          // [batch][bwd_slots + 256]: c in backward slot order
   const int* bwd_pos = nullptr;       // per coefficient slot: its backward slot (padding: bwd_slots)
   int coef_slots = 0;
+  int bwd16 = 0;   // the backward runs 16-token tiles (slot words address 32-byte rows)
 };
 
 }  // namespace ff
@@ -152,6 +153,8 @@ hipError_t configure_fast128();
 size_t fast128_lds_bytes(int nblk);
 // Floats per tile of the fused backward's dC workspace for a plan with `bwd_slots` slots.
 size_t fast128_partial_floats(size_t bwd_slots);
+// LDS of the 16-token backward for an output side of nblk_out 128-wide blocks.
+size_t fast16_lds_bytes(int nblk_out);
 hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, const float* c,
                          const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, float* c_saved,
                          hipStream_t s);

@@ -121,22 +121,27 @@ struct Frag {
   bf16x8 f[kHT][kKT];
 };
 
-// The 16 KB of upper-half synthesis fragments are fetched by the whole workgroup (4 x 16 B
-// per thread, issued before anything else the kernel loads), staged through LDS and read back
-// by every wave.  The fragment array is ordered [row tile][contraction step][lane], so the
-// upper half is its first half.
-constexpr int kFragPerThread = kHT * kKT * 64 / kThreads;
+// The 16 KB of upper-half synthesis fragments are fetched by the whole workgroup (NTH
+// threads, 16 KB / NTH per thread, issued before anything else the kernel loads), staged
+// through LDS and read back by every wave.  The fragment array is ordered [row tile][contraction
+// step][lane], so the upper half is its first half.
+template <int NTH>
+constexpr int frag_per_thread() { return kHT * kKT * 64 / NTH; }
+constexpr int kFragPerThread = frag_per_thread<kThreads>();
 
-__device__ __forceinline__ void frag_fetch(const void* fs16, u32x4 (&r)[kFragPerThread]) {
+template <int NTH = kThreads>
+__device__ __forceinline__ void frag_fetch(const void* fs16, u32x4 (&r)[frag_per_thread<NTH>()]) {
   const FF_GLOBAL u32x4* src = gld(reinterpret_cast<const u32x4*>(fs16));
 #pragma unroll
-  for (int j = 0; j < kFragPerThread; ++j) r[j] = src[threadIdx.x + j * kThreads];
+  for (int j = 0; j < frag_per_thread<NTH>(); ++j) r[j] = src[threadIdx.x + j * NTH];
 }
 
 // `stage` must be free LDS of 16 KB; it may be reused after return.
-__device__ __forceinline__ void frag_stage(const u32x4 (&r)[kFragPerThread], u32x4* stage, int lane, Frag& F) {
+template <int NTH = kThreads>
+__device__ __forceinline__ void frag_stage(const u32x4 (&r)[frag_per_thread<NTH>()], u32x4* stage, int lane,
+                                           Frag& F) {
 #pragma unroll
-  for (int j = 0; j < kFragPerThread; ++j) stage[threadIdx.x + j * kThreads] = r[j];
+  for (int j = 0; j < frag_per_thread<NTH>(); ++j) stage[threadIdx.x + j * NTH] = r[j];
   __syncthreads();
 #pragma unroll
   for (int mt = 0; mt < kHT; ++mt)
@@ -853,6 +858,280 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
   }
 }
 
+// ---------------------------------------------------------------- 16-token backward
+//
+// The same backward for 16 tokens per workgroup (8 waves, one workgroup per CU), used when the
+// output side's coefficient array for 16 tokens fits in LDS next to the wave tiles (m <= 4096)
+// and every backward stream has at most 16 rows.  The array has rows of 32 bytes (both token
+// halves of a coefficient), the slot words' source field addresses them, and each pair's stream
+// is loaded once and applied to the two 8-token halves in turn through the same 4 KB tile
+// layout, so that a stream's slot words, coefficients and dC partial sums serve 16 tokens: half
+// the partial sums to write and reduce, and half the stream loads per token.
+constexpr int kTT16 = 16;
+constexpr int kWaves16 = 8;
+constexpr int kThreads16 = 64 * kWaves16;
+constexpr int kCh16 = 16;   // a whole stream held in registers
+
+// Store the result of mfma_block_t for token half h into a coefficient-major array of 32-byte
+// rows, half h of row c at bytes 16 (h ^ (c & 1)) of the row, so that the 16-byte reads of one
+// half at random rows spread over all banks: `row` is this lane's byte offset in row tile 0 for
+// its half (odd coefficients negated).
+__device__ __forceinline__ void store_coef16_t(unsigned char* lds, unsigned row, const f32x4 (&acc)[kMT],
+                                               unsigned sgn) {
+#pragma unroll
+  for (int mt = 0; mt < kMT; ++mt) {
+    const unsigned w0 = pack_bf2(acc[mt][0], acc[mt][1]) ^ sgn, w1 = pack_bf2(acc[mt][2], acc[mt][3]) ^ sgn;
+    *reinterpret_cast<u32x2*>(lds + row + 512 * mt) = u32x2{w0, w1};
+  }
+}
+
+// Analysis of both token halves of every pair into the 32-byte-row array.  A pair's 8 KB stage
+// both halves' inputs (4 KB each), which are read before either half's result is written over
+// them; pairs run two ahead and every wait counts exactly the loads issued after it.  Tokens
+// 8..15 of a tile with at most 8 tokens repeat tokens 0..7 (their results are never used).
+__device__ __forceinline__ void analysis16(const Frag& F, const u16* rows, long ld, int nt, int np, int wave,
+                                           int lane, unsigned char* lds) {
+  const int n = lane & 15, q = lane >> 4;
+  // this lane's coefficient (16 mt + n of block q >> 1) has the parity of n
+  const unsigned off0 = ((q >> 1) * kW + n) * 32 + 8 * (q & 1) + 16 * (n & 1), off1 = off0 ^ 16;
+  const unsigned sgn = (n & 1) ? 0x80008000u : 0u;
+  constexpr unsigned kPair = 2 * kW * 32;
+  const u16* rows1 = nt > 8 ? rows + 8 * ld : rows;
+  const int nt0 = min(nt, 8), nt1 = nt > 8 ? nt - 8 : nt0;
+  auto issue = [&](int p) {
+    dma_rows(rows, ld, nt0, 2 * p, lane, lds + p * kPair);
+    dma_rows(rows1, ld, nt1, 2 * p, lane, lds + p * kPair + 4096);
+  };
+  wave_lds_fence();
+  if (wave < np) issue(wave);
+  if (wave + kWaves16 < np) issue(wave + kWaves16);
+  issue_point();
+  for (int p = wave; p < np; p += kWaves16) {
+    if (p + kWaves16 < np)
+      vm_wait<8>();   // this pair's eight loads (the next pair's eight may still be in flight)
+    else
+      vm_wait<0>();
+    wave_lds_fence();
+    u32x4 b0[kKT], b1[kKT];
+    read_rows(lds + p * kPair, lane, b0);
+    read_rows(lds + p * kPair + 4096, lane, b1);
+    wave_lds_fence();
+    if (p + 2 * kWaves16 < np) issue(p + 2 * kWaves16);
+    issue_point();
+    f32x4 acc[kMT];
+    mfma_block_t(F, b0, acc, ~0u);
+    store_coef16_t(lds + p * kPair, off0, acc, sgn);
+    mfma_block_t(F, b1, acc, ~0u);
+    store_coef16_t(lds + p * kPair, off1, acc, sgn);
+  }
+  wave_lds_fence();
+}
+
+// Token half h (h16 = 16 h) of the uL row of a slot word, whose source field already holds the
+// row's half 0 (at 16 (c & 1) within row c).
+__device__ __forceinline__ u32x4 lds_src16(unsigned e, unsigned h16) {
+  return *(const __attribute__((address_space(3))) u32x4*)(size_t)((e & kSlotSrcMask) ^ h16);
+}
+
+// A whole backward stream (len <= 16, a multiple of 4): slot words, four rows per 16-byte load;
+// groups past the end re-read the last group.
+__device__ __forceinline__ void bwd16_entries(const unsigned* __restrict__ st, int len, int lane,
+                                              unsigned (&en)[kCh16]) {
+#pragma unroll
+  for (int g = 0; g < kCh16 / 4; ++g) {
+    const u32x4 w = gld(reinterpret_cast<const u32x4*>(st + 256L * min(g, len / 4 - 1)))[lane];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) en[4 * g + j] = w[j];
+  }
+}
+
+__device__ __forceinline__ void bwd16_coeffs(const float* __restrict__ cb, int len, int lane, float (&cc)[kCh16]) {
+#pragma unroll
+  for (int g = 0; g < kCh16 / 4; ++g) {
+    const f32x4 c = gld(reinterpret_cast<const f32x4*>(cb + 256L * min(g, len / 4 - 1)))[lane];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cc[4 * g + j] = c[j];
+  }
+}
+
+// s[i] (+)= sum over the half's 8 tokens of u[a_i] z[b_i] for the first n slots (uniform), four
+// slots' rows in flight at a time.
+template <bool FIRST>
+__device__ __forceinline__ void sddmm16(const unsigned (&en)[kCh16], int n, const unsigned char* tile, unsigned h16,
+                                        float (&s)[kCh16]) {
+#pragma unroll
+  for (int g = 0; g < kCh16 / 4; ++g) {
+    if (4 * g < n) {   // uniform
+      u32x4 uv[4], zv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const unsigned e = en[4 * g + i];
+        uv[i] = lds_src16(e, h16);
+        zv[i] = lds_at(tile, tile_off(e));
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float d = FIRST ? 0.f : s[4 * g + i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const unsigned uw = uv[i][j], zw = zv[i][j];
+          d = dot2(uw, zw, d);
+        }
+        s[4 * g + i] = d;
+      }
+    }
+  }
+}
+
+// q = C^T u for token half h over the first n slots into the tile (round ends as in accum_slot).
+__device__ __forceinline__ void spmm16(const unsigned (&en)[kCh16], const float (&cc)[kCh16], int n, unsigned ends,
+                                       float scale, unsigned h16, unsigned char* tile, float (&a)[8]) {
+  constexpr int kH = kCh16 / 2;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (h * kH < n) {   // uniform
+      u32x4 uv[kH];
+#pragma unroll
+      for (int i = 0; i < kH; ++i) uv[i] = lds_src16(en[h * kH + i], h16);
+#pragma unroll
+      for (int i = 0; i < kH; ++i) {
+        if (h * kH + i < n) {   // uniform
+          unsigned ce, co;
+          coef_words(cc[h * kH + i], scale, ce, co);
+          accum_slot(en[h * kH + i], ce, co, uv[i], (ends >> (h * kH + i)) & 1u, tile, a);
+        }
+      }
+    }
+  }
+}
+
+template <bool DX, bool DC, bool BETA>
+__global__ void __launch_bounds__(kThreads16, 1) bwd16(FastArgs a, const int4* __restrict__ pl,
+                                                       const unsigned* __restrict__ bst) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  unsigned char* uL = smem;   // m rows x 16 tokens x 2 bytes
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  unsigned char* tile = uL + (long)a.nblk_out * kW * kTT16 * 2 + wave * (2 * kW * kTT * 2);
+  const int bi = blockIdx.y;
+  const int t0 = blockIdx.x * kTT16, nt = min(kTT16, a.T - t0);
+  const bool two = nt > 8;   // the tile has a second token half
+  const int nt0 = min(nt, 8), nt1 = two ? nt - 8 : nt0;
+  const u16* G = reinterpret_cast<const u16*>(a.Gs ? a.Gs[bi] : a.G) + (long)t0 * a.ldg;
+  const u16* X0 = DC ? reinterpret_cast<const u16*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx : nullptr;
+  const u16* X1 = DC ? (two ? X0 + 8 * a.ldx : X0) : nullptr;
+  u16* dX0 = DX ? reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy : nullptr;
+  u16* dX1 = DX ? dX0 + 8 * a.ldy : nullptr;   // stored only when the tile has a second half
+  const float* cbw = DX ? a.cb + (long)bi * (a.slots + 256) : nullptr;
+  float* part = DC ? a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.pstride : nullptr;
+  float* trash = DC ? part + a.slots : nullptr;
+  // dC sums only over the tile's tokens: activation columns past its end are zeroed
+  const unsigned km0 = (lane & 7) < nt ? ~0u : 0u, km1 = (lane & 7) + 8 < nt ? ~0u : 0u;
+  const unsigned zoff = tile_lane_off(lane);
+  const unsigned zsgn = (lane & 1) ? 0x80008000u : 0u;
+  const int npi = a.nblk_in / 2, lastp = npi - 1;
+
+  u32x4 fr[frag_per_thread<kThreads16>()];
+  frag_fetch<kThreads16>(a.frag, fr);
+  issue_point();
+  int4 q = pl[min(wave, lastp)];
+  unsigned en[kCh16];
+  bwd16_entries(bst + (long)q.x * 64, q.y, lane, en);
+  u32x4 bx0[kKT], bx1[kKT];
+  if (DC) {
+    load_act(X0, a.ldx, nt0, 2 * min(wave, lastp), lane, bx0);
+    load_act(X1, a.ldx, nt1, 2 * min(wave, lastp), lane, bx1);
+  }
+  issue_point();
+
+  Frag F;
+  frag_stage<kThreads16>(fr, reinterpret_cast<u32x4*>(smem), lane, F);
+  analysis16(F, G, a.ldg, nt, a.nblk_out / 2, wave, lane, uL);
+  __syncthreads();
+
+  const int npw = (npi - wave + kWaves16 - 1) / kWaves16;
+  const int steps = (DC ? npw : 0) + (DX ? npw : 0);
+  if (DC) {
+    auto pair = [&](int p, unsigned (&ch)[kCh16], unsigned (&chn)[kCh16]) {
+      prio_by_progress((p - wave) / kWaves16, steps);
+      const int len = q.y;
+      const int4 qn = pl[min(p + kWaves16, lastp)];
+      bwd16_entries(bst + (long)qn.x * 64, qn.y, lane, chn);
+      issue_point();
+      float sd[kCh16];
+      {
+        f32x4 acc[kMT];
+        mfma_block_t(F, bx0, acc, km0);
+        store_tile_t(tile, zoff, acc, zsgn);
+      }
+      wave_lds_fence();
+      load_act(X0, a.ldx, nt0, 2 * min(p + kWaves16, lastp), lane, bx0);
+      issue_point();
+      sddmm16<true>(ch, len, tile, 0u, sd);
+      wave_lds_fence();
+      {   // the second half (all columns masked when the tile has no second half)
+        f32x4 acc[kMT];
+        mfma_block_t(F, bx1, acc, km1);
+        store_tile_t(tile, zoff, acc, zsgn);
+        wave_lds_fence();
+        sddmm16<false>(ch, len, tile, 16u, sd);
+        wave_lds_fence();
+      }
+      load_act(X1, a.ldx, nt1, 2 * min(p + kWaves16, lastp), lane, bx1);
+      issue_point();
+      float* pp = part + (long)q.x * 64;
+#pragma unroll
+      for (int g = 0; g < kCh16 / 4; ++g) {
+        float* dst = 4 * g < len ? pp + 256L * g + 4 * lane : trash + 4 * lane;
+        *gst(reinterpret_cast<f32x4*>(dst)) = f32x4{sd[4 * g], sd[4 * g + 1], sd[4 * g + 2], sd[4 * g + 3]};
+      }
+      q = qn;
+    };
+    unsigned en2[kCh16];
+    for (int p = wave; p < npi; p += 2 * kWaves16) {
+      pair(p, en, en2);
+      if (p + kWaves16 < npi) pair(p + kWaves16, en2, en);
+    }
+    if (DX) {   // restart at this wave's first pair
+      q = pl[min(wave, lastp)];
+      bwd16_entries(bst + (long)q.x * 64, q.y, lane, en);
+    }
+  }
+  if (DX) {
+    float cc[kCh16], cc2[kCh16];
+    bwd16_coeffs(cbw + (long)q.x * 64, q.y, lane, cc);
+    auto pair = [&](int p, unsigned (&ch)[kCh16], float (&cv)[kCh16], unsigned (&chn)[kCh16],
+                    float (&cvn)[kCh16]) {
+      prio_by_progress((DC ? npw : 0) + (p - wave) / kWaves16, steps);
+      const int len = q.y;
+      const int4 qn = pl[min(p + kWaves16, lastp)];
+      bwd16_entries(bst + (long)qn.x * 64, qn.y, lane, chn);
+      bwd16_coeffs(cbw + (long)qn.x * 64, qn.y, lane, cvn);
+      issue_point();
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        zero_tile(tile, lane);
+        float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        spmm16(ch, cv, len, (unsigned)q.w, a.scale, 16u * h, tile, acc8);
+        wave_lds_fence();
+        u32x4 b[kKT];
+        f32x4 acc[kMT];
+        load_tile_act(tile, lane, b);
+        wave_lds_fence();
+        mfma_block(F, b, acc);
+        // (a tile without a second half computes one from repeated inputs and drops it; only the
+        // following pair's first wait counts the skipped stores, next to loads issued with them)
+        if (h == 0 || two) store_act<BETA>(h ? dX1 : dX0, a.ldy, h ? nt1 : nt0, 2 * p, lane, acc, a.beta, tile);
+      }
+      q = qn;
+    };
+    unsigned en2[kCh16];
+    for (int p = wave; p < npi; p += 2 * kWaves16) {
+      pair(p, en, cc, en2, cc2);
+      if (p + kWaves16 < npi) pair(p + kWaves16, en2, cc2, en, cc);
+    }
+  }
+}
+
 // cb[batch][pos[j]] = c[batch][j]: the backward's coefficients scattered into its own stream
 // order (one coalesced load per coefficient, no dependent load), so that it loads them like the
 // forward does.  Padding slots go to a scratch slot past the backward slots.
@@ -943,7 +1222,12 @@ hipError_t configure_fast128() {
                             allow_lds(&bwd128<true, true, true>),
                             allow_lds(&bwd128<true, false, false>),
                             allow_lds(&bwd128<true, false, true>),
-                            allow_lds(&bwd128<false, true, false>)};
+                            allow_lds(&bwd128<false, true, false>),
+                            allow_lds(&bwd16<true, true, false>),
+                            allow_lds(&bwd16<true, true, true>),
+                            allow_lds(&bwd16<true, false, false>),
+                            allow_lds(&bwd16<true, false, true>),
+                            allow_lds(&bwd16<false, true, false>)};
     for (hipError_t x : r)
       if (x != hipSuccess) e = x;
     return e;
@@ -960,6 +1244,13 @@ size_t fast128_lds_bytes(int nblk) {
 }
 
 size_t fast128_partial_floats(size_t bwd_slots) { return bwd_slots + 256; }
+
+// The 16-token backward: the output side's array of 32-byte rows plus eight 4 KB wave tiles.
+size_t fast16_lds_bytes(int nblk_out) {
+  const size_t b = (size_t)nblk_out * kW * kTT16 * 2 + (size_t)kWaves16 * 2 * kW * kTT * 2;
+  const size_t frag = (size_t)kHT * kKT * 64 * 16;
+  return b < frag ? frag : b;
+}
 
 hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, const float* c,
                          const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, float* c_saved,
@@ -1035,7 +1326,9 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   a.pstride = (int)fast128_partial_floats((size_t)a.slots);
   a.partial = p->partial;
   a.cb = c_saved ? c_saved : p->fast.coef_bwd;
-  const long ntiles = (T + kTT - 1) / kTT;
+  const bool b16 = p->fast.bwd16 != 0;
+  const int tt = b16 ? kTT16 : kTT;
+  const long ntiles = (T + tt - 1) / tt;
   a.ntiles = ntiles;
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
@@ -1047,12 +1340,26 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   }
   if (T > 0 && (want_dx || want_dc)) {
     const dim3 grid((unsigned)ntiles, (unsigned)count);
-    const size_t lds = fast128_lds_bytes(a.nblk_out);
     const int4* pl = p->fast.bwd_pl;
     const unsigned* st = p->fast.bwd_st;
     const unsigned* em = p->fast.bwd_em;
     const bool beta = beta_dx != 0.f;
     rec(e0, s);
+    if (b16) {
+      const size_t lds = fast16_lds_bytes(a.nblk_out);
+      const dim3 blk(kThreads16);
+      if (want_dx && want_dc && beta)
+        hipLaunchKernelGGL((bwd16<true, true, true>), grid, blk, lds, s, a, pl, st);
+      else if (want_dx && want_dc)
+        hipLaunchKernelGGL((bwd16<true, true, false>), grid, blk, lds, s, a, pl, st);
+      else if (want_dx && beta)
+        hipLaunchKernelGGL((bwd16<true, false, true>), grid, blk, lds, s, a, pl, st);
+      else if (want_dx)
+        hipLaunchKernelGGL((bwd16<true, false, false>), grid, blk, lds, s, a, pl, st);
+      else
+        hipLaunchKernelGGL((bwd16<false, true, false>), grid, blk, lds, s, a, pl, st);
+    } else {
+    const size_t lds = fast128_lds_bytes(a.nblk_out);
     if (want_dx && want_dc && beta)
       hipLaunchKernelGGL((bwd128<true, true, true>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else if (want_dx && want_dc)
@@ -1063,6 +1370,7 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
       hipLaunchKernelGGL((bwd128<true, false, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else
       hipLaunchKernelGGL((bwd128<false, true, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
+    }
     rec(e1, s);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -344,6 +344,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   std::vector<uint2> b_st;
   std::vector<int> slot_of_user((size_t)nnz), bwd_slot_of_user;
   std::vector<int64_t> user_of_slot;
+  bool bwd16 = false;
   if (fast) {
     // byte offset of a coefficient's row in the LDS array of a whole side, and its row in a pair tile
     auto lsrc = [&](const Loc& l) { return (uint32_t)(l.blk * 128 + l.local) * 16u; };
@@ -409,6 +410,17 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       b_em.insert(b_em.end(), mask.begin(), mask.end());
       b_st.resize((size_t)(row0 + len) * 64, make_uint2(0u, 0u));
     }
+    // The 16-token backward holds a whole stream in registers and the output side's array for
+    // 16 tokens in LDS; its slot words address rows of 32 bytes instead of 16, at the row's
+    // first token half, which row c keeps at bytes 16 (c & 1).
+    int max_len = 0;
+    for (const int4& e : b_pl) max_len = std::max(max_len, e.y);
+    bwd16 = max_len <= 16 && ff::fast16_lds_bytes(FO.nblk) <= (size_t)ff::kMaxLdsBytes;
+    if (bwd16)
+      for (uint2& w : b_st) {
+        const uint32_t row = (w.x & ff::kSlotSrcMask) >> 4;
+        w.x = (w.x & ~ff::kSlotSrcMask) | (row * 32 + 16 * (row & 1));
+      }
   } else {
     // the generic kernels' layout is the forward table's entry order, so the forward reads a
     // row's coefficients by table position
@@ -536,6 +548,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   fp.coef_bwd = (float*)where[15];
   fp.bwd_pos = (const int*)where[16];
   fp.coef_slots = (int)nslot;
+  fp.bwd16 = bwd16 ? 1 : 0;
   p->dev_mem = mem;
   p->workspace_bytes = total;
   p->fin->refs.fetch_add(1);
@@ -570,6 +583,7 @@ extern "C" ff_status ff_plan_query(const ff_plan* p, int key, int64_t* value) {
     case FF_Q_FAST128: *value = p->fast.enabled; return FF_OK;
     case FF_Q_COEF_SLOTS: *value = p->coef_slots; return FF_OK;
     case FF_Q_SAVED_FLOATS: *value = p->fast.enabled ? (int64_t)p->fast.bwd_slots + 256 : 0; return FF_OK;
+    case FF_Q_BWD_TILE_TOKENS: *value = !p->fast.enabled ? 0 : p->fast.bwd16 ? 16 : 8; return FF_OK;
     default: return ff::fail(FF_EINVAL, "unknown query key %d", key);
   }
 }

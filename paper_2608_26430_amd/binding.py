@@ -192,6 +192,11 @@ class Plan:
         """Tokens per workgroup tile of the fused 128-wide backward (16 or 8; 0 without it)."""
         return self.query(7)
 
+    @property
+    def radix(self):
+        """(input, output) frame application: 4 for the factored radix-4 form, 1 for dense blocks."""
+        return self.query(8), self.query(9)
+
     def new_saved(self, device=None):
         """A c_saved array for one adapter of this plan (None when the plan needs none)."""
         torch = _torch()

@@ -37,7 +37,28 @@ struct FrameDev {
   const void* fa32;  // analysis   fragments, f32x4  [MT][KT4][64]
   const void* fs32;  // synthesis  fragments, f32x4  [MT][KT4][64]
   const float* B32;  // B, W x W row-major fp32: B[u][c], u = local coordinate, c = local coefficient
+  // Factored application (radix == 4): B is the realified unitary DFT of size k = 4 k2, applied
+  // as a radix-4 stage on the vector ALUs and a dense realified DFT of size k2 (W2 = 2 k2 wide)
+  // on MFMA; the fragments above then hold that W2 x W2 matrix and MT / KT / KT4 refer to it.
+  // In LDS a block is stored as four columns of cs elements (cs = W2 rounded up to 8, the
+  // rounding zero), column a holding the coefficients of frequencies a, a + 4, a + 8, ...
+  // radix == 1: the fragments hold B itself, W2 = cs = W, and a block is stored in order.
+  int radix;
+  int k2;
+  int W2;
+  int cs;
+  const float2* tw;  // [3][k2]: (cos, sin) of 2 pi (a b mod k) / k for a = 1..3, b < k2
 };
+
+// Position of block-local coefficient c (= 2 i + s: frequency i, real or imaginary part s)
+// inside a block's LDS storage.
+inline int lds_position(const FrameDev& f, int c) {
+  if (f.radix == 1) return c;
+  const int i = c >> 1;
+  return (i & 3) * f.cs + 2 * (i >> 2) + (c & 1);
+}
+// Elements a block occupies in LDS (before padding).
+inline int lds_block_span(const FrameDev& f) { return f.radix == 1 ? f.W : 4 * f.cs; }
 
 // Device tables of a plan.  "LDS offset" means an element offset inside one
 // token row of an LDS tile laid out block by block (block stride W + kBlockPad).

@@ -19,6 +19,7 @@
 // with rho/2 identical square blocks B (2k x 2k): B[2 tau + t][2 i + s] is the
 // entry of column (i, r, s) at real row 2(r k + tau) + t.  The device works on
 // B alone.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <map>
@@ -133,6 +134,108 @@ ff_status build_host(int64_t d, int64_t k, int64_t rho,
   return FF_OK;
 }
 
+// Radix-4 factorization of the block (Sec. 3.2 modulation: with k*rho = d the block B is the
+// realified unitary DFT of size k, analysis z = B^T x being the forward transform with 1/sqrt(k)).
+// For k = 4 k2 and input index tau = a k2 + b, frequency i = a' + 4 l:
+//   analysis   Y_a'[b] = w^(-a' b) sum_a X[a k2 + b] (-i)^(a a'),   w = e^(2 pi i / k)
+//              Z[a' + 4 l] = (1/sqrt(k)) sum_b e^(-2 pi i b l / k2) Y_a'[b]
+//   synthesis  Y'_a'[b] = (1/sqrt(k)) sum_l e^(+2 pi i b l / k2) Z[a' + 4 l]
+//              X[a k2 + b] = sum_a' i^(a a') w^(a' b) Y'_a'[b]
+// M2 is the realified k2-point matrix of the analysis (W2 x W2, rows 2 l + s, columns 2 b + t);
+// synthesis uses its transpose.  tw holds (cos, sin) of 2 pi (a' b mod k) / k.  The factored
+// operator is checked against B on every unit vector, in both directions, before it is used.
+bool factor_radix4(const std::vector<double>& B, int64_t k, std::vector<double>& M2, std::vector<double>& tw) {
+  if (k % 4 != 0 || k < 8) return false;
+  const int64_t k2 = k / 4, W = 2 * k, W2 = 2 * k2;
+  const double isk = 1.0 / std::sqrt((double)k);
+  M2.assign((size_t)(W2 * W2), 0.0);
+  for (int64_t l = 0; l < k2; ++l)
+    for (int64_t b = 0; b < k2; ++b) {
+      const double th = 2.0 * M_PI * (double)((b * l) % k2) / (double)k2;
+      const double re = std::cos(th) * isk, im = -std::sin(th) * isk;   // e^(-i th) / sqrt(k)
+      M2[(2 * l) * W2 + 2 * b] = re;
+      M2[(2 * l) * W2 + 2 * b + 1] = -im;
+      M2[(2 * l + 1) * W2 + 2 * b] = im;
+      M2[(2 * l + 1) * W2 + 2 * b + 1] = re;
+    }
+  tw.assign((size_t)(3 * k2 * 2), 0.0);
+  for (int64_t a = 1; a < 4; ++a)
+    for (int64_t b = 0; b < k2; ++b) {
+      const double ph = 2.0 * M_PI * (double)((a * b) % k) / (double)k;
+      tw[((a - 1) * k2 + b) * 2] = std::cos(ph);
+      tw[((a - 1) * k2 + b) * 2 + 1] = std::sin(ph);
+    }
+  typedef std::pair<double, double> cx;
+  auto mul = [](cx p, cx q) { return cx(p.first * q.first - p.second * q.second, p.first * q.second + p.second * q.first); };
+  auto twid = [&](int64_t a, int64_t b, bool conj) {
+    if (a == 0) return cx(1.0, 0.0);
+    const double c = tw[((a - 1) * k2 + b) * 2], sn = tw[((a - 1) * k2 + b) * 2 + 1];
+    return cx(c, conj ? -sn : sn);
+  };
+  // (-i)^e and i^e
+  auto ipow = [](int64_t e, bool neg) {
+    static const cx t[4] = {cx(1, 0), cx(0, 1), cx(-1, 0), cx(0, -1)};
+    const int64_t r = ((neg ? -e : e) % 4 + 4) % 4;
+    return t[r];
+  };
+  std::vector<double> x((size_t)W), y((size_t)W), z((size_t)W);
+  for (int64_t u = 0; u < W; ++u) {
+    // analysis of the unit vector e_u against column u of B^T (row u of B)
+    std::fill(x.begin(), x.end(), 0.0);
+    x[u] = 1.0;
+    for (int64_t a2 = 0; a2 < 4; ++a2)
+      for (int64_t b = 0; b < k2; ++b) {
+        cx acc(0.0, 0.0);
+        for (int64_t a = 0; a < 4; ++a) {
+          const cx X(x[2 * (a * k2 + b)], x[2 * (a * k2 + b) + 1]);
+          const cx t = mul(X, ipow(a * a2, true));
+          acc.first += t.first;
+          acc.second += t.second;
+        }
+        acc = mul(acc, twid(a2, b, true));
+        y[a2 * W2 + 2 * b] = acc.first;
+        y[a2 * W2 + 2 * b + 1] = acc.second;
+      }
+    double err = 0.0;
+    for (int64_t a2 = 0; a2 < 4; ++a2)
+      for (int64_t o = 0; o < W2; ++o) {
+        double v = 0.0;
+        for (int64_t i = 0; i < W2; ++i) v += M2[o * W2 + i] * y[a2 * W2 + i];
+        const int64_t freq = a2 + 4 * (o >> 1), c = 2 * freq + (o & 1);
+        err = std::max(err, std::fabs(v - B[u * W + c]));
+      }
+    if (err > 1e-12) return false;
+  }
+  for (int64_t c = 0; c < W; ++c) {
+    // synthesis of the unit coefficient e_c against column c of B
+    std::fill(z.begin(), z.end(), 0.0);
+    const int64_t freq = c >> 1, a2 = freq & 3, l = freq >> 2;
+    z[a2 * W2 + 2 * l + (c & 1)] = 1.0;   // coefficient c at its factored position
+    for (int64_t q = 0; q < 4; ++q)
+      for (int64_t o = 0; o < W2; ++o) {
+        double v = 0.0;
+        for (int64_t i = 0; i < W2; ++i) v += M2[i * W2 + o] * z[q * W2 + i];
+        y[q * W2 + o] = v;
+      }
+    double err = 0.0;
+    for (int64_t a = 0; a < 4; ++a)
+      for (int64_t b = 0; b < k2; ++b) {
+        cx acc(0.0, 0.0);
+        for (int64_t q = 0; q < 4; ++q) {
+          const cx Y = mul(cx(y[q * W2 + 2 * b], y[q * W2 + 2 * b + 1]), twid(q, b, false));
+          const cx t = mul(Y, ipow(a * q, false));
+          acc.first += t.first;
+          acc.second += t.second;
+        }
+        const int64_t u = 2 * (a * k2 + b);
+        err = std::max(err, std::fabs(acc.first - B[u * W + c]));
+        err = std::max(err, std::fabs(acc.second - B[(u + 1) * W + c]));
+      }
+    if (err > 1e-12) return false;
+  }
+  return true;
+}
+
 uint16_t bf16_rne(float f) {
   uint32_t u;
   std::memcpy(&u, &f, 4);
@@ -225,21 +328,37 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return ff::fail(FF_EDEVICE, "no HIP device");
 
+  // Blocks wider than 128 are applied in factored form when the radix-4 split reproduces them.
+  std::vector<double> M2, tw;
+  const bool factored = W > 128 && W / 4 <= 128 && factor_radix4(B, k, M2, tw);
+
   ff::FrameDev fd{};
   fd.d = (int)d;
   fd.W = (int)W;
   fd.nblk = (int)(rho / 2);
-  fd.MT = (int)((W + 15) / 16);
-  fd.KT = (int)((W + 31) / 32);
-  fd.KT4 = (int)((W + 15) / 16);
+  fd.radix = factored ? 4 : 1;
+  fd.k2 = factored ? (int)(k / 4) : (int)k;
+  fd.W2 = factored ? (int)(W / 4) : (int)W;
+  fd.cs = (fd.W2 + 7) / 8 * 8;
+  const int64_t W2 = fd.W2;
+  fd.MT = (int)((W2 + 15) / 16);
+  fd.KT = (int)((W2 + 31) / 32);
+  fd.KT4 = (int)((W2 + 15) / 16);
   const size_t n16 = (size_t)fd.MT * fd.KT * 64 * 8;     // bf16 elements per fragment set
   const size_t n32 = (size_t)fd.MT * fd.KT4 * 64 * 4;    // fp32 elements per fragment set
   std::vector<uint16_t> fa16(n16, 0), fs16(n16, 0);
   std::vector<float> fa32(n32, 0.f), fs32(n32, 0.f), B32((size_t)(W * W));
   // analysis computes out[c] = sum_u B[u][c] in[u]  (matrix M_a[o][i] = B[i][o]);
   // synthesis computes out[u] = sum_c B[u][c] in[c] (matrix M_s[o][i] = B[o][i]).
-  auto Ma = [&](int64_t o, int64_t i) { return (o < W && i < W) ? B[i * W + o] : 0.0; };
-  auto Ms = [&](int64_t o, int64_t i) { return (o < W && i < W) ? B[o * W + i] : 0.0; };
+  // Factored: M_a = M2 and M_s = M2^T.
+  auto Ma = [&](int64_t o, int64_t i) {
+    if (o >= W2 || i >= W2) return 0.0;
+    return factored ? M2[o * W2 + i] : B[i * W + o];
+  };
+  auto Ms = [&](int64_t o, int64_t i) {
+    if (o >= W2 || i >= W2) return 0.0;
+    return factored ? M2[i * W2 + o] : B[o * W + i];
+  };
   for (int mt = 0; mt < fd.MT; ++mt)
     for (int lane = 0; lane < 64; ++lane) {
       const int64_t o = 16 * mt + (lane & 15), q = lane >> 4;
@@ -260,9 +379,12 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
     }
   for (size_t e = 0; e < B32.size(); ++e) B32[e] = (float)B[e];
 
-  const size_t b16 = n16 * 2, b32 = n32 * 4, bB = B32.size() * 4;
+  std::vector<float> tw32(std::max<size_t>(tw.size(), 2));
+  for (size_t e = 0; e < tw.size(); ++e) tw32[e] = (float)tw[e];
+
+  const size_t b16 = n16 * 2, b32 = n32 * 4, bB = B32.size() * 4, bT = tw32.size() * 4;
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t total = 2 * up(b16) + 2 * up(b32) + up(bB);
+  const size_t total = 2 * up(b16) + 2 * up(b32) + up(bB) + up(bT);
   void* mem = nullptr;
   if (hipMalloc(&mem, total) != hipSuccess) {
     (void)hipGetLastError();
@@ -280,7 +402,8 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   fd.fa32 = put(fa32.data(), b32);
   fd.fs32 = put(fs32.data(), b32);
   fd.B32 = (const float*)put(B32.data(), bB);
-  if (!fd.fa16 || !fd.fs16 || !fd.fa32 || !fd.fs32 || !fd.B32) {
+  fd.tw = (const float2*)put(tw32.data(), bT);
+  if (!fd.fa16 || !fd.fs16 || !fd.fa32 || !fd.fs32 || !fd.B32 || !fd.tw) {
     (void)hipFree(mem);
     return ff::fail(FF_EDEVICE, "copying frame to the device failed");
   }

@@ -71,116 +71,350 @@ struct Act<false> {
   static __device__ __forceinline__ void st4(E* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
 };
 
-// Output tiles (16 outputs each) computed per pass over the contraction.
-constexpr int kCH = 8;
+// ---------------------------------------------------------------------------------------------
+// Frame application.  A "column" is one vector the frame's MFMA matrix M (W2 x W2: the block
+// B or B^T, or for factored frames the size-k/4 DFT of the radix-4 split) is applied to: the
+// inputs of one (token, block) for dense frames, of one (token, block, residue) for factored
+// ones.  Sixteen columns form the B operand of v_mfma_f32_16x16x32_bf16 (16x16x4 for fp32);
+// lane l holds column l % 16 and contraction elements 8 (l / 16) .. +7 of each step (4 for fp32).
+// Inputs at or past `lim` (the column's storage length) are taken as zero; M is zero there too.
 
-// acc[c] (lane's 4 outputs 16*(mt0+c) + 4*(lane>>4) + j of the lane's row) =
-// sum_i M[o][i] * in[i], where M is the frame block in analysis or synthesis
-// orientation and `in` points at the lane's activation row (2k values).
 template <bool BF16>
-__device__ __forceinline__ void apply_chunk(const FrameDev& f, bool synth, int mt0,
-                                            const typename Act<BF16>::E* in, bool valid, int lane,
-                                            f32x4 (&acc)[kCH]) {
-  const int q = lane >> 4;
+struct Mfma;
+
+template <>
+struct Mfma<true> {
+  using V = bf16x8;
+  static constexpr int KS = 32, VL = 8;   // contraction per step, elements per lane and step
+  static __device__ __forceinline__ f32x4 step(const V& a, const V& b, f32x4 acc) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+  }
+};
+
+template <>
+struct Mfma<false> {
+  using V = f32x4;
+  static constexpr int KS = 16, VL = 4;
+  static __device__ __forceinline__ f32x4 step(const V& a, const V& b, f32x4 acc) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], acc, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], acc, 0, 0, 0);
+  }
+};
+
+// This lane's contraction inputs of step ks for a column whose storage starts at `in`.
+template <bool BF16>
+__device__ __forceinline__ typename Mfma<BF16>::V load_operand(const typename Act<BF16>::E* in, bool ok, int lim,
+                                                               int ks, int q) {
+  using M = Mfma<BF16>;
+  typename M::V b{};
+  const int i0 = ks * M::KS + q * M::VL;
+  if (ok && i0 < lim) b = *reinterpret_cast<const typename M::V*>(in + i0);
+  return b;
+}
+
+// Every column c < ncols: epi(c, o, acc) receives outputs o..o+3 (o = 16 mt + 4 (lane / 16)) of
+// M applied to the column starting at col(c).  The MT x KT fragments of M stay in registers for
+// the whole call; each wave takes every nw-th group of 16 columns and loads the next group's
+// inputs while it multiplies the current one.
+template <bool BF16, int MT, int KT, class Col, class Epi>
+__device__ __forceinline__ void column_apply_reg(const void* frag, int ncols, int lim, Col col, Epi epi) {
+  using M = Mfma<BF16>;
+  using V = typename M::V;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6, q = lane >> 4;
+  const int ngrp = (ncols + 15) / 16;
+  if (wave >= ngrp) return;
+  const V* fr = reinterpret_cast<const V*>(frag);
+  V fa[MT][KT];
 #pragma unroll
-  for (int c = 0; c < kCH; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // fragments of the row tiles past the block's end repeat its last tile (their products are
-  // discarded), so every load is issued unconditionally
-  const int mlast = f.MT - 1;
-  if constexpr (BF16) {
-    const bf16x8* fr = reinterpret_cast<const bf16x8*>(synth ? f.fs16 : f.fa16);
-    // contraction step ks's fragments and activations, the next step's in flight meanwhile
-    auto load = [&](int ks, bf16x8 (&fa)[kCH], bf16x8& b) {
-      const int i0 = ks * 32 + q * 8;
-      b = bf16x8{};
-      if (valid && i0 < f.W) b = *reinterpret_cast<const bf16x8*>(in + i0);
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int c = 0; c < kCH; ++c) fa[c] = fr[((size_t)min(mt0 + c, mlast) * f.KT + ks) * 64 + lane];
-    };
-    bf16x8 fa[2][kCH], b[2];
-    load(0, fa[0], b[0]);
-    for (int ks = 0; ks < f.KT; ks += 2) {
-      load(min(ks + 1, f.KT - 1), fa[1], b[1]);
+    for (int ks = 0; ks < KT; ++ks) fa[mt][ks] = fr[(mt * KT + ks) * 64 + lane];
+  V cur[KT], nxt[KT];
+  auto load = [&](int g, V (&b)[KT]) {
+    const int c = g * 16 + (lane & 15);
+    const bool ok = c < ncols;
+    const auto* in = col(ok ? c : 0);
 #pragma unroll
-      for (int c = 0; c < kCH; ++c)
-        if (mt0 + c < f.MT) acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[0][c], b[0], acc[c], 0, 0, 0);
-      if (ks + 1 >= f.KT) break;
-      load(min(ks + 2, f.KT - 1), fa[0], b[0]);
+    for (int ks = 0; ks < KT; ++ks) b[ks] = load_operand<BF16>(in, ok, lim, ks, q);
+  };
+  load(wave, cur);
+  for (int g = wave; g < ngrp; g += nw) {
+    if (g + nw < ngrp) load(g + nw, nxt);
+    f32x4 acc[MT];
 #pragma unroll
-      for (int c = 0; c < kCH; ++c)
-        if (mt0 + c < f.MT) acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[1][c], b[1], acc[c], 0, 0, 0);
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KT; ++ks)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = M::step(fa[mt][ks], cur[ks], acc[mt]);
+    const int c = g * 16 + (lane & 15);
+    if (c < ncols) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) epi(c, 16 * mt + 4 * q, acc[mt]);
     }
-  } else {
-    const f32x4* fr = reinterpret_cast<const f32x4*>(synth ? f.fs32 : f.fa32);
-    auto load = [&](int ks, f32x4 (&fa)[kCH], f32x4& b) {
-      const int i0 = ks * 16 + q * 4;
-      b = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (valid && i0 < f.W) b = *reinterpret_cast<const f32x4*>(in + i0);
 #pragma unroll
-      for (int c = 0; c < kCH; ++c) fa[c] = fr[((size_t)min(mt0 + c, mlast) * f.KT4 + ks) * 64 + lane];
-    };
-    auto mma = [&](const f32x4 (&fa)[kCH], const f32x4& b) {
+    for (int ks = 0; ks < KT; ++ks) cur[ks] = nxt[ks];
+  }
+}
+
+// The same for matrices too large to keep in registers: fragments are read from memory (L1 / L2)
+// for every group, four output tiles at a time.  With at most kPre contraction steps a column's
+// inputs are all loaded before its first output is stored, so the column may be transformed in
+// place (factored frames always qualify: W2 <= 128); longer contractions reload them per output
+// chunk and need a separate destination.
+template <bool BF16, class Col, class Epi>
+__device__ __forceinline__ void column_apply_mem(const void* frag, int MT, int KT, int ncols, int lim, Col col,
+                                                 Epi epi) {
+  using M = Mfma<BF16>;
+  using V = typename M::V;
+  constexpr int kC = 4, kPre = 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6, q = lane >> 4;
+  const int ngrp = (ncols + 15) / 16;
+  const V* fr = reinterpret_cast<const V*>(frag);
+  const bool pre = KT <= kPre;
+  for (int g = wave; g < ngrp; g += nw) {
+    const int c = g * 16 + (lane & 15);
+    const bool ok = c < ncols;
+    const auto* in = col(ok ? c : 0);
+    V bp[kPre];
+    if (pre) {
 #pragma unroll
-      for (int c = 0; c < kCH; ++c) {
-        if (mt0 + c < f.MT) {
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[c][0], b[0], acc[c], 0, 0, 0);
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[c][1], b[1], acc[c], 0, 0, 0);
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[c][2], b[2], acc[c], 0, 0, 0);
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[c][3], b[3], acc[c], 0, 0, 0);
+      for (int ks = 0; ks < kPre; ++ks) bp[ks] = ks < KT ? load_operand<BF16>(in, ok, lim, ks, q) : V{};
+    }
+    for (int mt0 = 0; mt0 < MT; mt0 += kC) {
+      f32x4 acc[kC];
+#pragma unroll
+      for (int j = 0; j < kC; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int ks = 0; ks < KT; ++ks) {
+        V b;
+        if (pre) {
+          b = bp[0];
+#pragma unroll
+          for (int j = 1; j < kPre; ++j)
+            if (ks == j) b = bp[j];
+        } else {
+          b = load_operand<BF16>(in, ok, lim, ks, q);
+        }
+#pragma unroll
+        for (int j = 0; j < kC; ++j) {
+          const V a = fr[((size_t)min(mt0 + j, MT - 1) * KT + ks) * 64 + lane];
+          if (mt0 + j < MT) acc[j] = M::step(a, b, acc[j]);
         }
       }
-    };
-    f32x4 fa[2][kCH], b[2];
-    load(0, fa[0], b[0]);
-    for (int ks = 0; ks < f.KT4; ks += 2) {
-      load(min(ks + 1, f.KT4 - 1), fa[1], b[1]);
-      mma(fa[0], b[0]);
-      if (ks + 1 >= f.KT4) break;
-      load(min(ks + 2, f.KT4 - 1), fa[0], b[0]);
-      mma(fa[1], b[1]);
+      if (ok) {
+#pragma unroll
+        for (int j = 0; j < kC; ++j)
+          if (mt0 + j < MT) epi(c, 16 * (mt0 + j) + 4 * q, acc[j]);
+      }
     }
   }
 }
 
-// Apply the frame block to every (token, block) row of a tile.  Row r is
-// token t = r / nblk, block b = r % nblk; its input starts at
-// src + t*src_ld + b*src_bs.  epi(t, b, o, acc) consumes outputs o..o+3.
-template <bool BF16, class Epi>
-__device__ __forceinline__ void frame_apply(const FrameDev& f, bool synth, int nrows,
-                                            const typename Act<BF16>::E* src, long src_ld, int src_bs,
-                                            Epi epi) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const int q = lane >> 4;
-  // Work items are a 16-row group with a range of chunks of kCH output tiles.  A group is split
-  // into sf ranges only when that shortens the busiest wave (fewer groups than waves), since
-  // every range reloads the group's activations.
-  const int ngrp = (nrows + 15) / 16, nch = (f.MT + kCH - 1) / kCH;
-  int sf = 1, best = (ngrp + nw - 1) / nw * nch;
-  for (int k = 2; k <= nch; ++k) {
-    const int cost = (ngrp * k + nw - 1) / nw * ((nch + k - 1) / k);
-    if (cost < best) { best = cost; sf = k; }
-  }
-  const int cpi = (nch + sf - 1) / sf;   // chunks per item
-  for (int item = wave; item < ngrp * sf; item += nw) {
-    const int g = item / sf, c0 = (item - g * sf) * cpi, c1 = min(nch, c0 + cpi);
-    const int row = g * 16 + (lane & 15);
-    const bool valid = row < nrows;
-    const int rr = valid ? row : 0;
-    const int t = rr / f.nblk, b = rr - t * f.nblk;
-    const typename Act<BF16>::E* in = src + (long)t * src_ld + (long)b * src_bs;
-    for (int ch = c0; ch < c1; ++ch) {
-      const int mt0 = ch * kCH;
-      f32x4 acc[kCH];
-      apply_chunk<BF16>(f, synth, mt0, in, valid, lane, acc);
-      if (valid) {
-#pragma unroll
-        for (int c = 0; c < kCH; ++c) {
-          const int o = 16 * (mt0 + c) + 4 * q;
-          if (o < f.W) epi(t, b, o, acc[c]);
-        }
-      }
+// Dispatch on the matrix shape: register-resident for the shapes the frames here produce.
+template <bool BF16, class Col, class Epi>
+__device__ __forceinline__ void column_apply(const FrameDev& f, bool synth, int ncols, int lim, Col col, Epi epi) {
+  const void* frag = BF16 ? (synth ? f.fs16 : f.fa16) : (synth ? f.fs32 : f.fa32);
+  const int KT = BF16 ? f.KT : f.KT4;
+#define FF_SHAPE(mt, kt)                                                       \
+  case (mt) * 64 + (kt):                                                       \
+    column_apply_reg<BF16, mt, kt>(frag, ncols, lim, col, epi);                \
+    return;
+  if constexpr (BF16) {
+    switch (f.MT * 64 + KT) {
+      FF_SHAPE(1, 1) FF_SHAPE(2, 1) FF_SHAPE(3, 2) FF_SHAPE(4, 2) FF_SHAPE(5, 3) FF_SHAPE(6, 3)
+      FF_SHAPE(7, 4) FF_SHAPE(8, 4)
+      default: break;
+    }
+  } else {
+    switch (f.MT * 64 + KT) {
+      FF_SHAPE(1, 1) FF_SHAPE(2, 2) FF_SHAPE(3, 3) FF_SHAPE(4, 4) FF_SHAPE(5, 5) FF_SHAPE(6, 6)
+      default: break;
     }
   }
+#undef FF_SHAPE
+  column_apply_mem<BF16>(frag, f.MT, KT, ncols, lim, col, epi);
+}
+
+// Two consecutive activations (one complex coordinate) as fp32, and back.
+template <bool BF16>
+__device__ __forceinline__ float2 ld2(const typename Act<BF16>::E* p) {
+  if constexpr (BF16) {
+    const unsigned w = *reinterpret_cast<const unsigned*>(p);
+    return make_float2(bf2f((u16)(w & 0xffff)), bf2f((u16)(w >> 16)));
+  } else {
+    return *reinterpret_cast<const float2*>(p);
+  }
+}
+template <bool BF16>
+__device__ __forceinline__ void st2(typename Act<BF16>::E* p, float2 v) {
+  if constexpr (BF16)
+    *reinterpret_cast<unsigned*>(p) = (unsigned)f2bf(v.x) | ((unsigned)f2bf(v.y) << 16);
+  else
+    *reinterpret_cast<float2*>(p) = v;
+}
+__device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ float2 csub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
+// a * (c + i s) and a * (c - i s)
+__device__ __forceinline__ float2 cmul(float2 a, float2 w) {
+  return make_float2(fmaf(a.x, w.x, -a.y * w.y), fmaf(a.y, w.x, a.x * w.y));
+}
+__device__ __forceinline__ float2 cmulc(float2 a, float2 w) {
+  return make_float2(fmaf(a.x, w.x, a.y * w.y), fmaf(a.y, w.x, -a.x * w.y));
+}
+
+// Radix-4 stage of the factored analysis for every (token, block, b < k2) of a tile:
+// Y_a'[b] = w^(-a' b) sum_a X[a k2 + b] (-i)^(a a'), read from the token rows at src and written
+// to column a' of the block in the LDS tile (which also gets its padding zeroed).
+template <bool BF16>
+__device__ __forceinline__ void radix4_analysis(const FrameDev& f, int nt, const typename Act<BF16>::E* src,
+                                                long ld, typename Act<BF16>::E* dst, int ldt, int ldb) {
+  const int k2 = f.k2, W = f.W, cs = f.cs, W2 = f.W2;
+  const int per_tok = f.nblk * k2, items = nt * per_tok;
+  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+    const int t = it / per_tok, r = it - t * per_tok, blk = r / k2, b = r - blk * k2;
+    const typename Act<BF16>::E* x = src + (long)t * ld + blk * W + 2 * b;
+    const float2 x0 = ld2<BF16>(x), x1 = ld2<BF16>(x + 2 * k2), x2 = ld2<BF16>(x + 4 * k2),
+                 x3 = ld2<BF16>(x + 6 * k2);
+    const float2 s02 = cadd(x0, x2), d02 = csub(x0, x2), s13 = cadd(x1, x3), d13 = csub(x1, x3);
+    const float2 y0 = cadd(s02, s13), y2 = csub(s02, s13);
+    const float2 y1 = make_float2(d02.x + d13.y, d02.y - d13.x);   // d02 - i d13
+    const float2 y3 = make_float2(d02.x - d13.y, d02.y + d13.x);   // d02 + i d13
+    typename Act<BF16>::E* y = dst + t * ldt + blk * ldb + 2 * b;
+    st2<BF16>(y, y0);
+    st2<BF16>(y + cs, cmulc(y1, f.tw[b]));
+    st2<BF16>(y + 2 * cs, cmulc(y2, f.tw[k2 + b]));
+    st2<BF16>(y + 3 * cs, cmulc(y3, f.tw[2 * k2 + b]));
+    if (b == 0)
+      for (int a = 0; a < 4; ++a)
+        for (int e = W2; e < cs; ++e) Act<BF16>::st(y + a * cs + e, 0.f);
+  }
+}
+
+// Radix-4 stage of the factored synthesis: X[a k2 + b] = sum_a' i^(a a') w^(a' b) Y'_a'[b] from
+// the LDS tile, then out = s X (+ beta out) into the token rows at dst.
+template <bool BF16>
+__device__ __forceinline__ void radix4_synthesis(const FrameDev& f, int nt, const typename Act<BF16>::E* src,
+                                                 int ldt, int ldb, typename Act<BF16>::E* dst, long ld, float s,
+                                                 float beta) {
+  const int k2 = f.k2, W = f.W, cs = f.cs;
+  const int per_tok = f.nblk * k2, items = nt * per_tok;
+  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+    const int t = it / per_tok, r = it - t * per_tok, blk = r / k2, b = r - blk * k2;
+    const typename Act<BF16>::E* y = src + t * ldt + blk * ldb + 2 * b;
+    const float2 y0 = ld2<BF16>(y), y1 = cmul(ld2<BF16>(y + cs), f.tw[b]),
+                 y2 = cmul(ld2<BF16>(y + 2 * cs), f.tw[k2 + b]), y3 = cmul(ld2<BF16>(y + 3 * cs), f.tw[2 * k2 + b]);
+    const float2 s02 = cadd(y0, y2), d02 = csub(y0, y2), s13 = cadd(y1, y3), d13 = csub(y1, y3);
+    float2 xo[4];
+    xo[0] = cadd(s02, s13);
+    xo[2] = csub(s02, s13);
+    xo[1] = make_float2(d02.x - d13.y, d02.y + d13.x);   // d02 + i d13
+    xo[3] = make_float2(d02.x + d13.y, d02.y - d13.x);   // d02 - i d13
+    typename Act<BF16>::E* out = dst + (long)t * ld + blk * W + 2 * b;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      float2 v = make_float2(s * xo[a].x, s * xo[a].y);
+      if (beta != 0.f) {
+        const float2 old = ld2<BF16>(out + 2 * a * k2);
+        v.x = fmaf(beta, old.x, v.x);
+        v.y = fmaf(beta, old.y, v.y);
+      }
+      st2<BF16>(out + 2 * a * k2, v);
+    }
+  }
+}
+
+// Zero the padding of every column of a factored tile whose coefficients another phase writes
+// (the MFMA reads whole columns of cs elements).
+template <bool BF16>
+__device__ __forceinline__ void zero_column_pads(const FrameDev& f, int nt, typename Act<BF16>::E* tile, int ldt,
+                                                 int ldb) {
+  if (f.radix == 1 || f.cs == f.W2) return;
+  const int padw = f.cs - f.W2, per_tok = f.nblk * 4 * padw, items = nt * per_tok;
+  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+    const int t = it / per_tok, r = it - t * per_tok, col = r / padw, e = r - col * padw;
+    const int blk = col >> 2, a = col & 3;
+    Act<BF16>::st(tile + t * ldt + blk * ldb + a * f.cs + f.W2 + e, 0.f);
+  }
+}
+
+// z = P^T x for a tile: token rows at src (global) -> coefficients in the LDS tile.
+template <bool BF16>
+__device__ __forceinline__ void analysis_to_lds(const FrameDev& f, int nt, const typename Act<BF16>::E* src, long ld,
+                                                typename Act<BF16>::E* dst, int ldt, int ldb) {
+  using A = Act<BF16>;
+  using E = typename A::E;
+  const int nblk = f.nblk;
+  if (f.radix == 1) {
+    const int W = f.W;
+    column_apply<BF16>(
+        f, false, nt * nblk, W,
+        [&](int c) {
+          const int t = c / nblk;
+          return src + (long)t * ld + (c - t * nblk) * W;
+        },
+        [&](int c, int o, f32x4 v) {
+          if (o < W) {
+            const int t = c / nblk;
+            A::st4(dst + t * ldt + (c - t * nblk) * ldb + o, v);
+          }
+        });
+    return;
+  }
+  radix4_analysis<BF16>(f, nt, src, ld, dst, ldt, ldb);
+  __syncthreads();
+  const int cs = f.cs;
+  auto at = [&](int c) -> E* {
+    const int tb = c >> 2, t = tb / nblk;
+    return dst + t * ldt + (tb - t * nblk) * ldb + (c & 3) * cs;
+  };
+  column_apply<BF16>(
+      f, false, nt * nblk * 4, cs, [&](int c) -> const E* { return at(c); },
+      [&](int c, int o, f32x4 v) {
+        if (o < cs) A::st4(at(c) + o, v);
+      });
+}
+
+// out = s P q (+ beta out) for a tile: coefficients in the LDS tile at src -> token rows at dst.
+// Factored frames transform the tile in place first, so src is overwritten.
+template <bool BF16>
+__device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, int nt, typename Act<BF16>::E* src, int ldt,
+                                                   int ldb, typename Act<BF16>::E* dst, long ld, float s, float beta) {
+  using A = Act<BF16>;
+  using E = typename A::E;
+  const int nblk = f.nblk;
+  if (f.radix == 1) {
+    const int W = f.W;
+    column_apply<BF16>(
+        f, true, nt * nblk, W,
+        [&](int c) -> const E* {
+          const int t = c / nblk;
+          return src + t * ldt + (c - t * nblk) * ldb;
+        },
+        [&](int c, int o, f32x4 v) {
+          if (o < W) {
+            const int t = c / nblk;
+            E* p = dst + (long)t * ld + (c - t * nblk) * W + o;
+            f32x4 r = v * s;
+            if (beta != 0.f) r += beta * A::ld4(p);
+            A::st4(p, r);
+          }
+        });
+    return;
+  }
+  const int cs = f.cs;
+  auto at = [&](int c) -> E* {
+    const int tb = c >> 2, t = tb / nblk;
+    return src + t * ldt + (tb - t * nblk) * ldb + (c & 3) * cs;
+  };
+  column_apply<BF16>(
+      f, true, nt * nblk * 4, cs, [&](int c) -> const E* { return at(c); },
+      [&](int c, int o, f32x4 v) {
+        if (o < cs) A::st4(at(c) + o, v);
+      });
+  __syncthreads();
+  radix4_synthesis<BF16>(f, nt, src, ldt, ldb, dst, ld, s, beta);
 }
 
 // out[t][slot_off[s]] = sum over the entries e of row s of c * in[t][e.x], for every token
@@ -295,8 +529,8 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   Y += (long)t0 * a.ldy;
 
   // analysis: z = P_in^T x for every (token, input block)
-  frame_apply<BF16>(a.fin, false, nt * a.fin.nblk, X, a.ldx, a.fin.W,
-                    [&](int t, int b, int o, f32x4 v) { A::st4(zt + t * a.ldt_in + b * a.ldb_in + o, v); });
+  zero_column_pads<BF16>(a.fout, nt, vt, a.ldt_out, a.ldb_out);
+  analysis_to_lds<BF16>(a.fin, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
   __syncthreads();
 
   // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
@@ -308,13 +542,7 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
 
   // synthesis and epilogue: y = beta y + s P_out v
   const float s = a.scale, beta = a.beta;
-  frame_apply<BF16>(a.fout, true, nt * a.fout.nblk, vt, a.ldt_out, a.ldb_out,
-                    [&](int t, int b, int o, f32x4 v) {
-                      E* yp = Y + (long)t * a.ldy + b * a.fout.W + o;
-                      f32x4 r = v * s;
-                      if (beta != 0.f) r += beta * A::ld4(yp);
-                      A::st4(yp, r);
-                    });
+  synthesis_from_lds<BF16>(a.fout, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, s, beta);
 }
 
 struct BwdArgs {
@@ -357,12 +585,12 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   const int nt = min(a.tt, a.T - t0);
   const E* G = reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G) + (long)t0 * a.ldg;
 
-  frame_apply<BF16>(a.fout, false, nt * a.fout.nblk, G, a.ldg, a.fout.W,
-                    [&](int t, int b, int o, f32x4 v) { A::st4(ut + t * a.ldt_out + b * a.ldb_out + o, v); });
+  // q is written over z and then synthesized from whole columns: their padding must be zero
+  zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
+  analysis_to_lds<BF16>(a.fout, nt, G, a.ldg, ut, a.ldt_out, a.ldb_out);
   if (a.want_dc) {
     const E* X = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx;
-    frame_apply<BF16>(a.fin, false, nt * a.fin.nblk, X, a.ldx, a.fin.W,
-                      [&](int t, int b, int o, f32x4 v) { A::st4(zt + t * a.ldt_in + b * a.ldb_in + o, v); });
+    analysis_to_lds<BF16>(a.fin, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
   }
   __syncthreads();
 
@@ -387,12 +615,7 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
 
   E* dX = reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX) + (long)t0 * a.lddx;
   const float s = a.scale, beta = a.beta;
-  frame_apply<BF16>(a.fin, true, nt * a.fin.nblk, zt, a.ldt_in, a.ldb_in, [&](int t, int b, int o, f32x4 v) {
-    E* p = dX + (long)t * a.lddx + b * a.fin.W + o;
-    f32x4 r = v * s;
-    if (beta != 0.f) r += beta * A::ld4(p);
-    A::st4(p, r);
-  });
+  synthesis_from_lds<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in, dX, a.lddx, s, beta);
 }
 
 // A workgroup owns 64 coefficient slots; each of its 16 waves sums 1/16 of the tiles with all

@@ -244,8 +244,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   p->max_tokens = max_tokens;
   p->max_batch = max_batch;
   p->device = f_in->device;
-  p->ldb_in = FI.W + ff::kBlockPad;
-  p->ldb_out = FO.W + ff::kBlockPad;
+  p->ldb_in = ff::lds_block_span(FI) + ff::kBlockPad;
+  p->ldb_out = ff::lds_block_span(FO) + ff::kBlockPad;
   for (int dt = 0; dt < 2; ++dt) {
     const int esz = dt == FF_BF16 ? 2 : 4;
     p->ldt_in[dt] = token_stride(FI.nblk, p->ldb_in, esz);
@@ -267,8 +267,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     rloc[e] = locate(rows[e], f_out->rho);
     cloc[e] = locate(cols[e], f_in->rho);
   }
-  auto off_out = [&](const Loc& l) { return l.blk * p->ldb_out + l.local; };
-  auto off_in = [&](const Loc& l) { return l.blk * p->ldb_in + l.local; };
+  auto off_out = [&](const Loc& l) { return l.blk * p->ldb_out + ff::lds_position(FO, l.local); };
+  auto off_in = [&](const Loc& l) { return l.blk * p->ldb_in + ff::lds_position(FI, l.local); };
 
   // forward CSR over all m rows, slots sorted by row length (longest first)
   std::vector<int> rcount((size_t)m, 0), ccount((size_t)n, 0);
@@ -584,6 +584,8 @@ extern "C" ff_status ff_plan_query(const ff_plan* p, int key, int64_t* value) {
     case FF_Q_COEF_SLOTS: *value = p->coef_slots; return FF_OK;
     case FF_Q_SAVED_FLOATS: *value = p->fast.enabled ? (int64_t)p->fast.bwd_slots + 256 : 0; return FF_OK;
     case FF_Q_BWD_TILE_TOKENS: *value = !p->fast.enabled ? 0 : p->fast.bwd16 ? 16 : 8; return FF_OK;
+    case FF_Q_RADIX_IN: *value = p->fin->dev.radix; return FF_OK;
+    case FF_Q_RADIX_OUT: *value = p->fout->dev.radix; return FF_OK;
     default: return ff::fail(FF_EINVAL, "unknown query key %d", key);
   }
 }

@@ -83,6 +83,8 @@ def test_small_parity(dev, shape, dtype):
     assert plan.fast128 == (n // rn == 64 and m // rm == 64 and (n // 128) % 2 == 0 and (m // 128) % 2 == 0)
     if plan.fast128:
         assert plan.bwd_tile_tokens == (8 if m > 4096 or nnz > 20000 else 16)
+    # blocks wider than 128 (k = 172, 224) are applied as a radix-4 stage plus a DFT of size k/4
+    assert plan.radix == (4 if 2 * n // rn > 128 else 1, 4 if 2 * m // rm > 128 else 1)
     tol = TOL[dtype]
     Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
     c = plan_c(plan, vals, dev)

@@ -18,6 +18,9 @@ namespace ff {
 constexpr int kBlockPad = 8;
 // Largest LDS allocation of one workgroup on gfx950.
 constexpr int kMaxLdsBytes = 160 * 1024;
+// LDS the generic kernels keep after their tiles for the twiddle factors of factored frames:
+// [0, 1536) bytes input frame, [1536, 3072) output frame (3 k2 float2 each, k2 <= 64).
+constexpr int kTwLdsBytes = 3072;
 // Upper bound on tokens per workgroup tile.
 constexpr int kMaxTileTokens = 64;
 // Threads per workgroup of the fused forward / backward kernels.
@@ -60,27 +63,36 @@ inline int lds_position(const FrameDev& f, int c) {
 // Elements a block occupies in LDS (before padding).
 inline int lds_block_span(const FrameDev& f) { return f.radix == 1 ? f.W : 4 * f.cs; }
 
-// Device tables of a plan.  "LDS offset" means an element offset inside one
-// token row of an LDS tile laid out block by block (block stride W + kBlockPad).
+// Streamed sparse tables of the generic kernels.  Slots (rows of C for v = C z, columns for
+// q = C^T u) are sorted by entry count and grouped into slabs of 64; slab s is len_s >= 1 stream
+// rows of 64 entries, lane l holding the entries of slot 64 s + l (padding where the slot has
+// fewer, or past the last slot).  Entry (row r, lane l) is element 64 r + l.  Each of the
+// kGenWaves waves of a workgroup walks a contiguous run of whole slabs.
+constexpr int kGenWaves = kFusedThreads / 64;
+constexpr int kRowLast = (int)0x80000000u;   // flag in ent.x: the last stream row of its slab
+struct GenStream {
+  const int2* ent;        // (LDS element offset of the source coefficient within a token row
+                          //  | kRowLast, LDS element offset of the lane's destination or -1)
+  const int* coef;        // coefficient slot of the entry, -1 for padding
+  const int* wave_row;    // [kGenWaves + 1]: first stream row of each wave
+  int rows;               // stream rows; entries = 64 * rows
+};
+
+// Device tables of a plan.  "LDS offset" means an element offset inside one token row of an LDS
+// tile laid out block by block (block stride ldb = block span + kBlockPad).
 struct PlanDev {
-  // v = C z: one slot per row of C (block order), slots sorted by row length.
-  const int* fwd_slot_off;   // LDS offset of the slot's row in the v tile
-  const int* fwd_ptr;        // slot -> [ptr[s], ptr[s+1]) entries
-  const int2* fwd_ent;       // (LDS offset of the column in the z tile, coefficient slot)
-  int fwd_nslots;
-  int fwd_by_entry;          // 1: entry j of the table holds coefficient slot j
-  // q = C^T u: one slot per column of C, sorted by column length.
-  const int* bwd_slot_off;   // LDS offset of the slot's column in the q tile
-  const int* bwd_ptr;
-  const int2* bwd_ent;       // (LDS offset of the row in the u tile, coefficient slot)
-  int bwd_nslots;
-  // dC: per user entry e, (LDS offset of row in u tile, LDS offset of column in z tile).
-  const int2* sdd;           // per coefficient slot; (-1, -1) for padding slots
+  GenStream fwd;             // v = C z: source z, destination v
+  GenStream bwd;             // q = C^T u and dC: source u, destination q (over z)
+  int fwd_by_pos;            // 1: the coefficient layout is the forward stream's entry order
+  const int* coef_pad;       // coefficient slots that hold no entry (dC writes zero there)
+  int ncoef_pad;
   // merge: entries bucketed by (output block R, input block S), bucket = R*nblk_in + S.
   const int* mrg_ptr;
-  const int4* mrg_ent;       // (local row a', local column b', user index e, 0)
+  const int4* mrg_ent;       // (local row a', local column b', coefficient slot, 0)
   int mrg_max_bucket;
   int nnz;                   // coefficient slots (nnz plus padding)
+  float* c_fwd;              // [batch][64 fwd.rows]: coefficients in forward order (fwd_by_pos == 0)
+  float* c_bwd;              // [batch][64 bwd.rows]: coefficients in backward stream order
 };
 
 // Entry streams of the 128-wide fused kernels: per pair of adjacent 128-wide

@@ -131,7 +131,8 @@ __device__ __forceinline__ void column_apply_reg(const void* frag, int ncols, in
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int ks = 0; ks < KT; ++ks) fa[mt][ks] = fr[(mt * KT + ks) * 64 + lane];
-  V cur[KT], nxt[KT];
+  // two operand buffers used in turn (no copies, which would wait for the loads in flight)
+  V ba[KT], bb[KT];
   auto load = [&](int g, V (&b)[KT]) {
     const int c = g * 16 + (lane & 15);
     const bool ok = c < ncols;
@@ -139,23 +140,27 @@ __device__ __forceinline__ void column_apply_reg(const void* frag, int ncols, in
 #pragma unroll
     for (int ks = 0; ks < KT; ++ks) b[ks] = load_operand<BF16>(in, ok, lim, ks, q);
   };
-  load(wave, cur);
-  for (int g = wave; g < ngrp; g += nw) {
-    if (g + nw < ngrp) load(g + nw, nxt);
+  auto mul = [&](int g, const V (&b)[KT]) {
     f32x4 acc[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KT; ++ks)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[mt] = M::step(fa[mt][ks], cur[ks], acc[mt]);
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = M::step(fa[mt][ks], b[ks], acc[mt]);
     const int c = g * 16 + (lane & 15);
     if (c < ncols) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) epi(c, 16 * mt + 4 * q, acc[mt]);
     }
-#pragma unroll
-    for (int ks = 0; ks < KT; ++ks) cur[ks] = nxt[ks];
+  };
+  load(wave, ba);
+  for (int g = wave; g < ngrp; g += 2 * nw) {
+    if (g + nw < ngrp) load(g + nw, bb);
+    mul(g, ba);
+    if (g + nw >= ngrp) break;
+    if (g + 2 * nw < ngrp) load(g + 2 * nw, ba);
+    mul(g + nw, bb);
   }
 }
 
@@ -264,63 +269,115 @@ __device__ __forceinline__ float2 cmulc(float2 a, float2 w) {
   return make_float2(fmaf(a.x, w.x, a.y * w.y), fmaf(a.y, w.x, -a.x * w.y));
 }
 
+// x / d for 0 <= x < 2^24 and 0 < d, with inv = 1 / d in fp32: the product is within one of the
+// quotient, which the two corrections make exact.
+__device__ __forceinline__ int div_small(int x, int d, float inv) {
+  int q = (int)((float)x * inv);
+  q -= q * d > x;
+  q += (q + 1) * d <= x;
+  return q;
+}
+
+// The twiddle factors of a factored frame, copied to LDS (the caller synchronizes).
+__device__ __forceinline__ void stage_twiddles(const FrameDev& f, float2* lds) {
+  if (f.radix == 1) return;
+  for (int i = threadIdx.x; i < 3 * f.k2; i += blockDim.x) lds[i] = f.tw[i];
+}
+
 // Radix-4 stage of the factored analysis for every (token, block, b < k2) of a tile:
 // Y_a'[b] = w^(-a' b) sum_a X[a k2 + b] (-i)^(a a'), read from the token rows at src and written
-// to column a' of the block in the LDS tile (which also gets its padding zeroed).
+// to column a' of the block in the LDS tile (which also gets its padding zeroed).  A thread takes
+// kRB items at a time with all their loads issued first.
+constexpr int kRB = 8;
+
 template <bool BF16>
-__device__ __forceinline__ void radix4_analysis(const FrameDev& f, int nt, const typename Act<BF16>::E* src,
-                                                long ld, typename Act<BF16>::E* dst, int ldt, int ldb) {
+__device__ __forceinline__ void radix4_analysis(const FrameDev& f, const float2* tw, int nt,
+                                                const typename Act<BF16>::E* src, long ld,
+                                                typename Act<BF16>::E* dst, int ldt, int ldb) {
+  using E = typename Act<BF16>::E;
   const int k2 = f.k2, W = f.W, cs = f.cs, W2 = f.W2;
   const int per_tok = f.nblk * k2, items = nt * per_tok;
-  for (int it = threadIdx.x; it < items; it += blockDim.x) {
-    const int t = it / per_tok, r = it - t * per_tok, blk = r / k2, b = r - blk * k2;
-    const typename Act<BF16>::E* x = src + (long)t * ld + blk * W + 2 * b;
-    const float2 x0 = ld2<BF16>(x), x1 = ld2<BF16>(x + 2 * k2), x2 = ld2<BF16>(x + 4 * k2),
-                 x3 = ld2<BF16>(x + 6 * k2);
-    const float2 s02 = cadd(x0, x2), d02 = csub(x0, x2), s13 = cadd(x1, x3), d13 = csub(x1, x3);
-    const float2 y0 = cadd(s02, s13), y2 = csub(s02, s13);
-    const float2 y1 = make_float2(d02.x + d13.y, d02.y - d13.x);   // d02 - i d13
-    const float2 y3 = make_float2(d02.x - d13.y, d02.y + d13.x);   // d02 + i d13
-    typename Act<BF16>::E* y = dst + t * ldt + blk * ldb + 2 * b;
-    st2<BF16>(y, y0);
-    st2<BF16>(y + cs, cmulc(y1, f.tw[b]));
-    st2<BF16>(y + 2 * cs, cmulc(y2, f.tw[k2 + b]));
-    st2<BF16>(y + 3 * cs, cmulc(y3, f.tw[2 * k2 + b]));
-    if (b == 0)
-      for (int a = 0; a < 4; ++a)
-        for (int e = W2; e < cs; ++e) Act<BF16>::st(y + a * cs + e, 0.f);
+  const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
+  for (int it0 = threadIdx.x; it0 < items; it0 += kRB * blockDim.x) {
+    float2 x[kRB][4], w[kRB][3];
+    int b[kRB];
+    E* y[kRB];
+#pragma unroll
+    for (int u = 0; u < kRB; ++u) {
+      const int it = min(it0 + u * (int)blockDim.x, items - 1);   // past the end: a repeat, not stored
+      const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
+      b[u] = r - blk * k2;
+      const E* xp = src + (long)t * ld + blk * W + 2 * b[u];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) x[u][a] = ld2<BF16>(xp + 2 * a * k2);
+#pragma unroll
+      for (int a = 0; a < 3; ++a) w[u][a] = tw[a * k2 + b[u]];
+      y[u] = dst + t * ldt + blk * ldb + 2 * b[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kRB; ++u) {
+      if (it0 + u * (int)blockDim.x >= items) break;
+      const float2 s02 = cadd(x[u][0], x[u][2]), d02 = csub(x[u][0], x[u][2]);
+      const float2 s13 = cadd(x[u][1], x[u][3]), d13 = csub(x[u][1], x[u][3]);
+      const float2 y1 = make_float2(d02.x + d13.y, d02.y - d13.x);   // d02 - i d13
+      const float2 y3 = make_float2(d02.x - d13.y, d02.y + d13.x);   // d02 + i d13
+      st2<BF16>(y[u], cadd(s02, s13));
+      st2<BF16>(y[u] + cs, cmulc(y1, w[u][0]));
+      st2<BF16>(y[u] + 2 * cs, cmulc(csub(s02, s13), w[u][1]));
+      st2<BF16>(y[u] + 3 * cs, cmulc(y3, w[u][2]));
+      if (b[u] == 0)
+        for (int a = 0; a < 4; ++a)
+          for (int e = W2; e < cs; ++e) Act<BF16>::st(y[u] + a * cs + e, 0.f);
+    }
   }
 }
 
 // Radix-4 stage of the factored synthesis: X[a k2 + b] = sum_a' i^(a a') w^(a' b) Y'_a'[b] from
 // the LDS tile, then out = s X (+ beta out) into the token rows at dst.
 template <bool BF16>
-__device__ __forceinline__ void radix4_synthesis(const FrameDev& f, int nt, const typename Act<BF16>::E* src,
-                                                 int ldt, int ldb, typename Act<BF16>::E* dst, long ld, float s,
-                                                 float beta) {
+__device__ __forceinline__ void radix4_synthesis(const FrameDev& f, const float2* tw, int nt,
+                                                 const typename Act<BF16>::E* src, int ldt, int ldb,
+                                                 typename Act<BF16>::E* dst, long ld, float s, float beta) {
+  using E = typename Act<BF16>::E;
   const int k2 = f.k2, W = f.W, cs = f.cs;
   const int per_tok = f.nblk * k2, items = nt * per_tok;
-  for (int it = threadIdx.x; it < items; it += blockDim.x) {
-    const int t = it / per_tok, r = it - t * per_tok, blk = r / k2, b = r - blk * k2;
-    const typename Act<BF16>::E* y = src + t * ldt + blk * ldb + 2 * b;
-    const float2 y0 = ld2<BF16>(y), y1 = cmul(ld2<BF16>(y + cs), f.tw[b]),
-                 y2 = cmul(ld2<BF16>(y + 2 * cs), f.tw[k2 + b]), y3 = cmul(ld2<BF16>(y + 3 * cs), f.tw[2 * k2 + b]);
-    const float2 s02 = cadd(y0, y2), d02 = csub(y0, y2), s13 = cadd(y1, y3), d13 = csub(y1, y3);
-    float2 xo[4];
-    xo[0] = cadd(s02, s13);
-    xo[2] = csub(s02, s13);
-    xo[1] = make_float2(d02.x - d13.y, d02.y + d13.x);   // d02 + i d13
-    xo[3] = make_float2(d02.x + d13.y, d02.y - d13.x);   // d02 - i d13
-    typename Act<BF16>::E* out = dst + (long)t * ld + blk * W + 2 * b;
+  const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
+  for (int it0 = threadIdx.x; it0 < items; it0 += kRB * blockDim.x) {
+    float2 yv[kRB][4], w[kRB][3];
+    E* out[kRB];
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      float2 v = make_float2(s * xo[a].x, s * xo[a].y);
-      if (beta != 0.f) {
-        const float2 old = ld2<BF16>(out + 2 * a * k2);
-        v.x = fmaf(beta, old.x, v.x);
-        v.y = fmaf(beta, old.y, v.y);
+    for (int u = 0; u < kRB; ++u) {
+      const int it = min(it0 + u * (int)blockDim.x, items - 1);
+      const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
+      const int b = r - blk * k2;
+      const E* yp = src + t * ldt + blk * ldb + 2 * b;
+#pragma unroll
+      for (int a = 0; a < 4; ++a) yv[u][a] = ld2<BF16>(yp + a * cs);
+#pragma unroll
+      for (int a = 0; a < 3; ++a) w[u][a] = tw[a * k2 + b];
+      out[u] = dst + (long)t * ld + blk * W + 2 * b;
+    }
+#pragma unroll
+    for (int u = 0; u < kRB; ++u) {
+      if (it0 + u * (int)blockDim.x >= items) break;
+      const float2 y0 = yv[u][0], y1 = cmul(yv[u][1], w[u][0]), y2 = cmul(yv[u][2], w[u][1]),
+                   y3 = cmul(yv[u][3], w[u][2]);
+      const float2 s02 = cadd(y0, y2), d02 = csub(y0, y2), s13 = cadd(y1, y3), d13 = csub(y1, y3);
+      float2 xo[4];
+      xo[0] = cadd(s02, s13);
+      xo[2] = csub(s02, s13);
+      xo[1] = make_float2(d02.x - d13.y, d02.y + d13.x);   // d02 + i d13
+      xo[3] = make_float2(d02.x + d13.y, d02.y - d13.x);   // d02 - i d13
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        float2 v = make_float2(s * xo[a].x, s * xo[a].y);
+        if (beta != 0.f) {
+          const float2 old = ld2<BF16>(out[u] + 2 * a * k2);
+          v.x = fmaf(beta, old.x, v.x);
+          v.y = fmaf(beta, old.y, v.y);
+        }
+        st2<BF16>(out[u] + 2 * a * k2, v);
       }
-      st2<BF16>(out + 2 * a * k2, v);
     }
   }
 }
@@ -341,8 +398,9 @@ __device__ __forceinline__ void zero_column_pads(const FrameDev& f, int nt, type
 
 // z = P^T x for a tile: token rows at src (global) -> coefficients in the LDS tile.
 template <bool BF16>
-__device__ __forceinline__ void analysis_to_lds(const FrameDev& f, int nt, const typename Act<BF16>::E* src, long ld,
-                                                typename Act<BF16>::E* dst, int ldt, int ldb) {
+__device__ __forceinline__ void analysis_to_lds(const FrameDev& f, const float2* tw, int nt,
+                                                const typename Act<BF16>::E* src, long ld, typename Act<BF16>::E* dst,
+                                                int ldt, int ldb) {
   using A = Act<BF16>;
   using E = typename A::E;
   const int nblk = f.nblk;
@@ -362,7 +420,7 @@ __device__ __forceinline__ void analysis_to_lds(const FrameDev& f, int nt, const
         });
     return;
   }
-  radix4_analysis<BF16>(f, nt, src, ld, dst, ldt, ldb);
+  radix4_analysis<BF16>(f, tw, nt, src, ld, dst, ldt, ldb);
   __syncthreads();
   const int cs = f.cs;
   auto at = [&](int c) -> E* {
@@ -379,8 +437,9 @@ __device__ __forceinline__ void analysis_to_lds(const FrameDev& f, int nt, const
 // out = s P q (+ beta out) for a tile: coefficients in the LDS tile at src -> token rows at dst.
 // Factored frames transform the tile in place first, so src is overwritten.
 template <bool BF16>
-__device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, int nt, typename Act<BF16>::E* src, int ldt,
-                                                   int ldb, typename Act<BF16>::E* dst, long ld, float s, float beta) {
+__device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const float2* tw, int nt,
+                                                   typename Act<BF16>::E* src, int ldt, int ldb,
+                                                   typename Act<BF16>::E* dst, long ld, float s, float beta) {
   using A = Act<BF16>;
   using E = typename A::E;
   const int nblk = f.nblk;
@@ -414,82 +473,126 @@ __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, int nt, ty
         if (o < cs) A::st4(at(c) + o, v);
       });
   __syncthreads();
-  radix4_synthesis<BF16>(f, nt, src, ldt, ldb, dst, ld, s, beta);
+  radix4_synthesis<BF16>(f, tw, nt, src, ldt, ldb, dst, ld, s, beta);
 }
 
-// out[t][slot_off[s]] = sum over the entries e of row s of c * in[t][e.x], for every token
-// t < nt of the tile, where c is cv[j] for the row's j-th table entry (BY_ENTRY: the table is in
-// coefficient-slot order) or cv[e.y].  A work item is one row for a group of up to 8 tokens: the
-// row's entries and coefficients are loaded once per group, four entries at a time, and the
-// group's products are LDS reads.  Each thread runs kRowItems items side by side, so their load
-// chains overlap.
-constexpr int kRowTokens = 8;
-constexpr int kRowBatch = 4;
-constexpr int kRowItems = 1;
+// Sparse products over a generic stream (GenStream).  Each wave walks its run of stream rows
+// with the next kSD rows' entries and coefficients in flight.  Lane l accumulates, for tokens
+// tg0 .. tg0 + ntg - 1 of the tile, its slot's entries times the source coefficients (src tile)
+// and, at the last row of each slab, stores the sums at its destination in the dst tile.
+// BWD (q = C^T u over the columns of C): the walk also yields, per entry, this pass's share of
+// dC / s = sum_t u_t[row] z_t[column], z being read from the lane's destination before q is
+// written over it; part receives one float per stream element (added to when part_add).
+constexpr int kSD = 8;   // stream rows per buffer (two buffers: up to 16 rows in flight)
+constexpr int kTG = 8;   // most tokens per pass over the stream
 
-template <bool BF16, bool BY_ENTRY>
-__device__ __forceinline__ void row_products(int nslots, const int* __restrict__ ptr, const int2* __restrict__ ent,
-                                             const int* __restrict__ slot_off, const float* cv,
-                                             const typename Act<BF16>::E* in, int ld_in,
-                                             typename Act<BF16>::E* out, int ld_out, int nt) {
+template <bool BF16, bool BWD, bool PART_ADD, int kTG>
+__device__ __forceinline__ void stream_products(const GenStream& S, const float* __restrict__ cv,
+                                                const typename Act<BF16>::E* src, int ld_src,
+                                                typename Act<BF16>::E* dst, int ld_dst, int tg0, int ntg,
+                                                bool write_dst, float* part) {
   using A = Act<BF16>;
-  using E = typename A::E;
-  const int ngrp = (nt + kRowTokens - 1) / kRowTokens, items = nslots * ngrp;
-  const int last = max(ptr[nslots] - 1, 0);   // table entries: loads are clamped into the table
-  for (int base = threadIdx.x; base < items; base += kRowItems * blockDim.x) {
-    int beg[kRowItems], len[kRowItems], off[kRowItems], ntg[kRowItems];
-    const E* ib[kRowItems];
-    int maxlen = 0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r0 = S.wave_row[wave], r1 = S.wave_row[wave + 1];
+  if (r0 >= r1) return;
+  src += tg0 * ld_src;
+  dst += tg0 * ld_dst;
+  // Two buffers of kSD rows, each refilled right after it is consumed, so that the other one's
+  // loads stay in flight meanwhile (a copy between buffers would wait for them).
+  int2 ea[kSD], eb[kSD];
+  float ca[kSD], cb[kSD];
+  auto load = [&](int r, int2 (&e)[kSD], float (&c)[kSD]) {
 #pragma unroll
-    for (int r = 0; r < kRowItems; ++r) {
-      const int it = base + r * (int)blockDim.x;
-      const bool ok = it < items;
-      const int itc = ok ? it : base;
-      const int s = itc / ngrp, t0 = (itc - s * ngrp) * kRowTokens;
-      ntg[r] = ok ? min(kRowTokens, nt - t0) : 0;
-      beg[r] = ptr[s];
-      len[r] = ok ? ptr[s + 1] - beg[r] : 0;
-      off[r] = t0 * ld_out + slot_off[s];
-      ib[r] = in + t0 * ld_in;
-      maxlen = max(maxlen, len[r]);
+    for (int i = 0; i < kSD; ++i) {
+      const int j = min(r + i, r1 - 1) * 64 + lane;   // rows past the run repeat its last one, unused
+      e[i] = S.ent[j];
+      c[i] = cv[j];
     }
-    float acc[kRowItems][kRowTokens];
+  };
+  // Every row reads kTG token rows without branches (tokens past ntg repeat the last one; their
+  // sums are never stored and their dC weights zb are zero), so the reads overlap.
+  int tso[kTG], tdo[kTG];
 #pragma unroll
-    for (int r = 0; r < kRowItems; ++r)
+  for (int t = 0; t < kTG; ++t) {
+    tso[t] = min(t, ntg - 1) * ld_src;
+    tdo[t] = min(t, ntg - 1) * ld_dst;
+  }
+  float acc[kTG], zb[kTG];
 #pragma unroll
-      for (int t = 0; t < kRowTokens; ++t) acc[r][t] = 0.f;
-    for (int j0 = 0; j0 < maxlen; j0 += kRowBatch) {
-      int2 en[kRowItems][kRowBatch];
-      float c[kRowItems][kRowBatch];
+  for (int t = 0; t < kTG; ++t) acc[t] = zb[t] = 0.f;
+  bool start = true;   // the next row begins a slab
+  auto consume = [&](int r, const int2 (&e)[kSD], const float (&c)[kSD]) {
 #pragma unroll
-      for (int r = 0; r < kRowItems; ++r)
+    for (int i = 0; i < kSD; ++i) {
+      if (r + i >= r1) break;
+      const int so = e[i].x & 0x7fffffff, d = e[i].y;
+      if (BWD && part && start) {
+        const int dc0 = max(d, 0);
+        float zv[kTG];
 #pragma unroll
-        for (int u = 0; u < kRowBatch; ++u) {
-          const int j = min(beg[r] + min(j0 + u, max(len[r] - 1, 0)), last);
-          en[r][u] = ent[j];
-          if (BY_ENTRY) c[r][u] = cv[j];
-        }
-      if (!BY_ENTRY) {
+        for (int t = 0; t < kTG; ++t) zv[t] = A::ld(dst + tdo[t] + dc0);
 #pragma unroll
-        for (int r = 0; r < kRowItems; ++r)
-#pragma unroll
-          for (int u = 0; u < kRowBatch; ++u) c[r][u] = cv[en[r][u].y];
+        for (int t = 0; t < kTG; ++t) zb[t] = (t < ntg && d >= 0) ? zv[t] : 0.f;
       }
+      start = false;
+      float x[kTG];
 #pragma unroll
-      for (int r = 0; r < kRowItems; ++r)
+      for (int t = 0; t < kTG; ++t) x[t] = A::ld(src + tso[t] + so);
+      float dc = 0.f;
 #pragma unroll
-        for (int u = 0; u < kRowBatch; ++u)
-          if (j0 + u < len[r]) {
+      for (int t = 0; t < kTG; ++t) {
+        acc[t] = fmaf(c[i], x[t], acc[t]);
+        if (BWD) dc = fmaf(x[t], zb[t], dc);
+      }
+      if (BWD && part) {
+        // a plain store unless a previous token pass wrote this element (the compiler would
+        // otherwise load it on every pass)
+        float* pp = part + (long)(r + i) * 64 + lane;
+        if constexpr (PART_ADD)
+          *pp += dc;
+        else
+          *pp = dc;
+      }
+      if (__builtin_amdgcn_readfirstlane(e[i].x) < 0) {   // the slab's last row (same in every lane)
+        if (write_dst && d >= 0) {
 #pragma unroll
-            for (int t = 0; t < kRowTokens; ++t)
-              if (t < ntg[r]) acc[r][t] = fmaf(c[r][u], A::ld(ib[r] + t * ld_in + en[r][u].x), acc[r][t]);
-          }
+          for (int t = 0; t < kTG; ++t)
+            if (t < ntg) A::st(dst + t * ld_dst + d, acc[t]);
+        }
+#pragma unroll
+        for (int t = 0; t < kTG; ++t) acc[t] = 0.f;
+        start = true;
+      }
     }
-#pragma unroll
-    for (int r = 0; r < kRowItems; ++r)
-#pragma unroll
-      for (int t = 0; t < kRowTokens; ++t)
-        if (t < ntg[r]) A::st(out + off[r] + t * ld_out, acc[r][t]);
+  };
+  load(r0, ea, ca);
+  load(r0 + kSD, eb, cb);
+  for (int r = r0; r < r1; r += 2 * kSD) {
+    consume(r, ea, ca);
+    if (r + kSD >= r1) break;
+    load(r + 2 * kSD, ea, ca);
+    consume(r + kSD, eb, cb);
+    load(r + 3 * kSD, eb, cb);
+  }
+}
+
+// All tokens of a tile, kTG at a time, each pass reading only as many token rows as it needs.
+template <bool BF16, bool BWD>
+__device__ __forceinline__ void stream_all(const GenStream& S, const float* __restrict__ cv,
+                                           const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
+                                           int ld_dst, int nt, bool write_dst, float* part) {
+  for (int tg = 0; tg < nt; tg += kTG) {
+    const int ntg = min(kTG, nt - tg);
+    if (tg == 0) {
+      if (ntg <= 2)
+        stream_products<BF16, BWD, false, 2>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+      else if (ntg <= 4)
+        stream_products<BF16, BWD, false, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+      else
+        stream_products<BF16, BWD, false, kTG>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    } else {
+      stream_products<BF16, BWD, true, kTG>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    }
   }
 }
 
@@ -502,14 +605,12 @@ struct FwdArgs {
   void* Y;
   void* const* Ys;
   long ldy;
-  const float* c;
-  const float* const* cs;
+  const float* c;             // coefficients in forward stream order: c (batch: cs[bi]) or
+  const float* const* cs;     // ccopy + bi * cstride when the layout differs
+  const float* ccopy;
+  long cstride;
   float scale, beta;
-  const int* slot_off;
-  const int* ptr;
-  const int2* ent;
-  int nslots;
-  int by_entry;   // the table is in coefficient-slot order
+  GenStream st;
 };
 
 template <bool BF16>
@@ -522,27 +623,30 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   const int bi = blockIdx.y;
   const E* X = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X);
   E* Y = reinterpret_cast<E*>(a.Ys ? a.Ys[bi] : a.Y);
-  const float* cv = a.cs ? a.cs[bi] : a.c;
+  const float* cv = a.ccopy ? a.ccopy + bi * a.cstride : a.cs ? a.cs[bi] : a.c;
   const int t0 = blockIdx.x * a.tt;
   const int nt = min(a.tt, a.T - t0);
   X += (long)t0 * a.ldx;
   Y += (long)t0 * a.ldy;
 
+  // twiddle factors of factored frames after the tiles
+  float2* tw_in = reinterpret_cast<float2*>(vt + (size_t)a.tt * a.ldt_out);
+  float2* tw_out = tw_in + kTwLdsBytes / 16;
+  stage_twiddles(a.fin, tw_in);
+  stage_twiddles(a.fout, tw_out);
+  if (a.fin.radix != 1 || a.fout.radix != 1) __syncthreads();
+
   // analysis: z = P_in^T x for every (token, input block)
   zero_column_pads<BF16>(a.fout, nt, vt, a.ldt_out, a.ldb_out);
-  analysis_to_lds<BF16>(a.fin, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
+  analysis_to_lds<BF16>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
   __syncthreads();
 
   // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
-  if (a.by_entry)
-    row_products<BF16, true>(a.nslots, a.ptr, a.ent, a.slot_off, cv, zt, a.ldt_in, vt, a.ldt_out, nt);
-  else
-    row_products<BF16, false>(a.nslots, a.ptr, a.ent, a.slot_off, cv, zt, a.ldt_in, vt, a.ldt_out, nt);
+  stream_all<BF16, false>(a.st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
   __syncthreads();
 
   // synthesis and epilogue: y = beta y + s P_out v
-  const float s = a.scale, beta = a.beta;
-  synthesis_from_lds<BF16>(a.fout, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, s, beta);
+  synthesis_from_lds<BF16>(a.fout, tw_out, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, a.scale, a.beta);
 }
 
 struct BwdArgs {
@@ -557,19 +661,12 @@ struct BwdArgs {
   void* dX;
   void* const* dXs;
   long lddx;
-  const float* c;
-  const float* const* cs;
+  const float* ccopy;   // coefficients in backward stream order, [batch][cstride]
+  long cstride;
   float scale, beta;
   int want_dx, want_dc;
-  // q = C^T u tables
-  const int* slot_off;
-  const int* ptr;
-  const int2* ent;
-  int nslots;
-  // dC tables and partial sums [batch][tile][coefficient slot]
-  const int2* sdd;
-  int nnz;
-  float* partial;
+  GenStream st;
+  float* partial;       // dC partial sums [batch][tile][cstride]
   long ntiles;
 };
 
@@ -585,72 +682,87 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   const int nt = min(a.tt, a.T - t0);
   const E* G = reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G) + (long)t0 * a.ldg;
 
+  // twiddle factors of factored frames after the tiles
+  float2* tw_in = reinterpret_cast<float2*>(zt + (size_t)a.tt * a.ldt_in);
+  float2* tw_out = tw_in + kTwLdsBytes / 16;
+  stage_twiddles(a.fin, tw_in);
+  stage_twiddles(a.fout, tw_out);
+  if (a.fin.radix != 1 || a.fout.radix != 1) __syncthreads();
+
   // q is written over z and then synthesized from whole columns: their padding must be zero
   zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
-  analysis_to_lds<BF16>(a.fout, nt, G, a.ldg, ut, a.ldt_out, a.ldb_out);
+  analysis_to_lds<BF16>(a.fout, tw_out, nt, G, a.ldg, ut, a.ldt_out, a.ldb_out);
   if (a.want_dc) {
     const E* X = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx;
-    analysis_to_lds<BF16>(a.fin, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
+    analysis_to_lds<BF16>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
   }
   __syncthreads();
 
-  if (a.want_dc) {
-    // this tile's share of dC_e / s = sum_t u_t[row_e] z_t[col_e]
-    float* part = a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.nnz;
-    for (int e = threadIdx.x; e < a.nnz; e += blockDim.x) {
-      const int2 o = a.sdd[e];
-      float acc = 0.f;
-      if (o.x >= 0)   // padding slots hold no entry
-        for (int t = 0; t < nt; ++t) acc = fmaf(A::ld(ut + t * a.ldt_out + o.x), A::ld(zt + t * a.ldt_in + o.y), acc);
-      part[e] = acc;
-    }
-    if (!a.want_dx) return;
-    __syncthreads();
-  }
-
-  // q[b] = sum_{e in column b} c_e u[a_e], written over z
-  const float* cv = a.cs ? a.cs[bi] : a.c;
-  row_products<BF16, false>(a.nslots, a.ptr, a.ent, a.slot_off, cv, ut, a.ldt_out, zt, a.ldt_in, nt);
+  // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
+  const float* cv = a.ccopy + bi * a.cstride;
+  float* part = a.want_dc ? a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.cstride : nullptr;
+  stream_all<BF16, true>(a.st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part);
+  if (!a.want_dx) return;
   __syncthreads();
 
   E* dX = reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX) + (long)t0 * a.lddx;
-  const float s = a.scale, beta = a.beta;
-  synthesis_from_lds<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in, dX, a.lddx, s, beta);
+  synthesis_from_lds<BF16>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX, a.lddx, a.scale, a.beta);
 }
 
-// A workgroup owns 64 coefficient slots; each of its 16 waves sums 1/16 of the tiles with all
-// loads of a pass in flight, and the 16 sums are combined in a fixed order (deterministic).
+// out[bi][j] = c_bi[idx[j]] (0 where idx[j] < 0): coefficients in a stream's order.
+__global__ void __launch_bounds__(256) gather_coef(const float* c, const float* const* cs, const int* __restrict__ idx,
+                                                   int len, float* out) {
+  const int bi = blockIdx.y, j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= len) return;
+  const float* cv = cs ? cs[bi] : c;
+  const int k = idx[j];
+  out[(long)bi * len + j] = k >= 0 ? cv[k] : 0.f;
+}
+
+// A workgroup owns 64 backward stream elements; each of its 16 waves sums 1/16 of the tiles
+// with all loads of a pass in flight, and the 16 sums are combined in a fixed order
+// (deterministic) and stored at the element's coefficient slot.  Workgroups past the stream
+// zero the coefficient slots that hold no entry (when not accumulating).
 constexpr int kDcWaves = 16;
 constexpr int kDcBatch = 8;
 
-__global__ void __launch_bounds__(64 * kDcWaves) dc_reduce(const float* __restrict__ partial, long ntiles, int nnz,
-                                                           float scale, int accumulate, float* dC,
+__global__ void __launch_bounds__(64 * kDcWaves) dc_reduce(const float* __restrict__ partial, long ntiles, int len,
+                                                           const int* __restrict__ dst, const int* __restrict__ pad,
+                                                           int npad, float scale, int accumulate, float* dC,
                                                            float* const* dCs) {
   __shared__ float red[kDcWaves][64];
   const int bi = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  float* out = dCs ? dCs[bi] : dC;
+  const int nmain = (len + 63) / 64;
+  if ((int)blockIdx.x >= nmain) {
+    const int j = ((int)blockIdx.x - nmain) * (int)blockDim.x + threadIdx.x;
+    if (!accumulate && j < npad) out[pad[j]] = 0.f;
+    return;
+  }
   const int e = blockIdx.x * 64 + lane;
-  const int ec = min(e, nnz - 1);   // lanes past the end read the last slot and write nothing
-  const float* p = partial + (long)bi * ntiles * nnz + ec;
+  const int ec = min(e, len - 1);   // lanes past the end read the last element and write nothing
+  const float* p = partial + (long)bi * ntiles * len + ec;
   float sum = 0.f;
   for (long t0 = w; t0 < ntiles; t0 += (long)kDcWaves * kDcBatch) {
     float v[kDcBatch];
 #pragma unroll
     for (int j = 0; j < kDcBatch; ++j) {
       const long t = t0 + (long)j * kDcWaves;
-      v[j] = t < ntiles ? p[t * nnz] : 0.f;
+      v[j] = t < ntiles ? p[t * len] : 0.f;
     }
 #pragma unroll
     for (int j = 0; j < kDcBatch; ++j) sum += v[j];
   }
   red[w][lane] = sum;
   __syncthreads();
-  if (w == 0 && e < nnz) {
+  if (w == 0 && e < len) {
+    const int slot = dst[e];
+    if (slot < 0) return;
     float tot = 0.f;
 #pragma unroll
     for (int i = 0; i < kDcWaves; ++i) tot += red[i][lane];
-    float* out = dCs ? dCs[bi] : dC;
     const float v = scale * tot;
-    out[e] = accumulate ? out[e] + v : v;
+    out[slot] = accumulate ? out[slot] + v : v;
   }
 }
 
@@ -752,6 +864,14 @@ hipError_t configure_kernels() {
   return once;
 }
 
+// Coefficients of every adapter in a stream's order: out[bi][j] = c_bi[idx[j]].
+hipError_t launch_gather(const float* c, const float* const* cs, const int* idx, int len, int count, float* out,
+                         hipStream_t s) {
+  const dim3 grid((unsigned)((len + 255) / 256), (unsigned)count);
+  hipLaunchKernelGGL(gather_coef, grid, dim3(256), 0, s, c, cs, idx, len, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx, const float* c,
                       const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, float* c_saved,
                       hipStream_t s) {
@@ -775,11 +895,13 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.cs = cs;
   a.scale = scale;
   a.beta = beta;
-  a.slot_off = p->dev.fwd_slot_off;
-  a.ptr = p->dev.fwd_ptr;
-  a.ent = p->dev.fwd_ent;
-  a.nslots = p->dev.fwd_nslots;
-  a.by_entry = p->dev.fwd_by_entry;
+  a.st = p->dev.fwd;
+  if (!p->dev.fwd_by_pos) {   // the coefficient layout is another path's: reorder for this stream
+    a.cstride = 64L * a.st.rows;
+    a.ccopy = p->dev.c_fwd;
+    const hipError_t e = launch_gather(c, cs, a.st.coef, (int)a.cstride, count, p->dev.c_fwd, s);
+    if (e != hipSuccess) return e;
+  }
   const dim3 grid((unsigned)((T + a.tt - 1) / a.tt), (unsigned)count);
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
@@ -817,24 +939,21 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.dX = const_cast<void*>(dX.one);
   a.dXs = const_cast<void* const*>(dX.many);
   a.lddx = (long)lddx;
-  a.c = c;
-  a.cs = cs;
   a.scale = scale;
   a.beta = beta_dx;
   a.want_dx = want_dx;
   a.want_dc = want_dc;
-  a.slot_off = p->dev.bwd_slot_off;
-  a.ptr = p->dev.bwd_ptr;
-  a.ent = p->dev.bwd_ent;
-  a.nslots = p->dev.bwd_nslots;
-  a.sdd = p->dev.sdd;
-  a.nnz = p->dev.nnz;
+  a.st = p->dev.bwd;
+  a.cstride = 64L * a.st.rows;
+  a.ccopy = p->dev.c_bwd;
   a.partial = p->partial;
   const long ntiles = (T + a.tt - 1) / a.tt;
   a.ntiles = ntiles;
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
   if (T > 0 && (want_dx || want_dc)) {
+    hipError_t e = launch_gather(c, cs, a.st.coef, (int)a.cstride, count, p->dev.c_bwd, s);
+    if (e != hipSuccess) return e;
     const dim3 grid((unsigned)ntiles, (unsigned)count);
     record(e0, s);
     if (bf16)
@@ -842,13 +961,15 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
     else
       hipLaunchKernelGGL(bwd_kernel<false>, grid, dim3(kFusedThreads), p->lds_bytes[0], s, a);
     record(e1, s);
-    hipError_t e = hipGetLastError();
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   if (want_dc) {
-    const dim3 grid((unsigned)((a.nnz + 63) / 64), (unsigned)count);
-    hipLaunchKernelGGL(dc_reduce, grid, dim3(64 * kDcWaves), 0, s, p->partial, ntiles, a.nnz, scale, accumulate_dc,
-                       dC, dCs);
+    const int len = (int)a.cstride, nmain = (len + 63) / 64;
+    const int npadb = (p->dev.ncoef_pad + 64 * kDcWaves - 1) / (64 * kDcWaves);
+    const dim3 grid((unsigned)(nmain + npadb), (unsigned)count);
+    hipLaunchKernelGGL(dc_reduce, grid, dim3(64 * kDcWaves), 0, s, p->partial, ntiles, len, a.st.coef,
+                       p->dev.coef_pad, p->dev.ncoef_pad, scale, accumulate_dc, dC, dCs);
   }
   return hipGetLastError();
 }

@@ -205,6 +205,60 @@ int emit_pair(const PairSchedule& ps, const std::vector<std::vector<int>>& entri
 
 }  // namespace
 
+// A generic stream (GenStream) on the host: entry words, the user entry of every stream element
+// (-1: padding) and the first row of each wave.
+struct StreamHost {
+  std::vector<int2> ent;
+  std::vector<int> id;
+  std::vector<int> wave_row;
+  int64_t rows = 0;
+};
+
+// Slots are the indices of `lists` (entries of each slot, in stream order), sorted by entry count
+// with the longest first; src(e) is the LDS offset an entry reads, dst(slot) where its slot's
+// result goes.
+template <class Src, class Dst>
+StreamHost build_stream(const std::vector<std::vector<int>>& lists, Src src, Dst dst) {
+  const int64_t nslots = (int64_t)lists.size(), nslab = (nslots + 63) / 64;
+  std::vector<int> order((size_t)nslots);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return lists[a].size() > lists[b].size(); });
+  std::vector<int64_t> slab_row((size_t)nslab + 1, 0);
+  for (int64_t s = 0; s < nslab; ++s) {
+    size_t len = 1;   // every slab has a row, so every slot's result is written
+    for (int64_t l = 0; l < 64 && 64 * s + l < nslots; ++l) len = std::max(len, lists[order[64 * s + l]].size());
+    slab_row[s + 1] = slab_row[s] + (int64_t)len;
+  }
+  StreamHost h;
+  h.rows = slab_row[nslab];
+  h.ent.assign((size_t)(h.rows * 64), make_int2(0, -1));
+  h.id.assign((size_t)(h.rows * 64), -1);
+  for (int64_t s = 0; s < nslab; ++s) {
+    const int64_t len = slab_row[s + 1] - slab_row[s];
+    for (int64_t l = 0; l < 64; ++l) {
+      const int64_t slot = 64 * s + l;
+      const bool real = slot < nslots;
+      const int d = real ? dst(order[slot]) : -1;
+      for (int64_t k = 0; k < len; ++k) {
+        const size_t j = (size_t)((slab_row[s] + k) * 64 + l);
+        const int e = real && k < (int64_t)lists[order[slot]].size() ? lists[order[slot]][k] : -1;
+        h.ent[j] = make_int2((e >= 0 ? src(e) : 0) | (k == len - 1 ? ff::kRowLast : 0), d);
+        h.id[j] = e;
+      }
+    }
+  }
+  // waves take contiguous runs of slabs with about equal numbers of rows
+  h.wave_row.assign(ff::kGenWaves + 1, (int)h.rows);
+  h.wave_row[0] = 0;
+  int64_t s = 0;
+  for (int w = 1; w < ff::kGenWaves; ++w) {
+    const int64_t target = h.rows * w / ff::kGenWaves;
+    while (s < nslab && slab_row[s] < target) ++s;
+    h.wave_row[w] = (int)std::max<int64_t>(slab_row[s], h.wave_row[w - 1]);
+  }
+  return h;
+}
+
 extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out, int64_t nnz,
                                     const int32_t* rows, const int32_t* cols, int64_t max_tokens,
                                     int64_t max_batch, ff_plan** out) {
@@ -251,13 +305,13 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     p->ldt_in[dt] = token_stride(FI.nblk, p->ldb_in, esz);
     p->ldt_out[dt] = token_stride(FO.nblk, p->ldb_out, esz);
     const int64_t per_token = (int64_t)(p->ldt_in[dt] + p->ldt_out[dt]) * esz;
-    int64_t tt = ff::kMaxLdsBytes / per_token;
+    int64_t tt = (ff::kMaxLdsBytes - ff::kTwLdsBytes) / per_token;
     if (tt < 1)
       return ff::fail(FF_EUNSUPPORTED, "one token of %lld + %lld coefficients exceeds LDS", (long long)n,
                       (long long)m);
     tt = std::min<int64_t>(tt, ff::kMaxTileTokens);
     p->tile_tokens[dt] = (int)tt;
-    p->lds_bytes[dt] = (size_t)(tt * per_token);
+    p->lds_bytes[dt] = (size_t)(tt * per_token) + ff::kTwLdsBytes;
     p->max_tiles = std::max<int64_t>(p->max_tiles, (max_tokens + tt - 1) / tt);
   }
 
@@ -270,44 +324,22 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   auto off_out = [&](const Loc& l) { return l.blk * p->ldb_out + ff::lds_position(FO, l.local); };
   auto off_in = [&](const Loc& l) { return l.blk * p->ldb_in + ff::lds_position(FI, l.local); };
 
-  // forward CSR over all m rows, slots sorted by row length (longest first)
-  std::vector<int> rcount((size_t)m, 0), ccount((size_t)n, 0);
-  for (int64_t e = 0; e < nnz; ++e) {
-    rcount[rows[e]]++;
-    ccount[cols[e]]++;
-  }
-  auto build_slots = [](const std::vector<int>& count, std::vector<int>& order) {
-    order.resize(count.size());
-    std::iota(order.begin(), order.end(), 0);
-    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return count[a] > count[b]; });
-  };
-  std::vector<int> rorder, corder;
-  build_slots(rcount, rorder);
-  build_slots(ccount, corder);
-  std::vector<int> rslot_of((size_t)m), cslot_of((size_t)n);
-  for (int64_t s = 0; s < m; ++s) rslot_of[rorder[s]] = (int)s;
-  for (int64_t s = 0; s < n; ++s) cslot_of[corder[s]] = (int)s;
-
-  std::vector<int> fwd_ptr((size_t)m + 1, 0), bwd_ptr((size_t)n + 1, 0);
-  for (int64_t s = 0; s < m; ++s) fwd_ptr[s + 1] = fwd_ptr[s] + rcount[rorder[s]];
-  for (int64_t s = 0; s < n; ++s) bwd_ptr[s + 1] = bwd_ptr[s] + ccount[corder[s]];
-  std::vector<int> fwd_slot_off((size_t)m), bwd_slot_off((size_t)n);
-  for (int64_t s = 0; s < m; ++s) fwd_slot_off[s] = off_out(locate(rorder[s], f_out->rho));
-  for (int64_t s = 0; s < n; ++s) bwd_slot_off[s] = off_in(locate(corder[s], f_in->rho));
-  std::vector<int2> fwd_ent((size_t)std::max<int64_t>(nnz, 1)), bwd_ent((size_t)std::max<int64_t>(nnz, 1)),
-      sdd((size_t)std::max<int64_t>(nnz, 1));
+  // generic streams: v = C z over the rows of C and q = C^T u over its columns, slots sorted
+  // by entry count (longest first), entries within a slot in order of their other index
+  std::vector<std::vector<int>> by_row((size_t)m), by_col((size_t)n);
   {
-    std::vector<int> fpos(fwd_ptr.begin(), fwd_ptr.end() - 1), bpos(bwd_ptr.begin(), bwd_ptr.end() - 1);
-    // entries in order of their column (forward) / row (backward) for locality
     std::vector<int64_t> byc((size_t)nnz), byr((size_t)nnz);
     std::iota(byc.begin(), byc.end(), 0);
     std::iota(byr.begin(), byr.end(), 0);
     std::stable_sort(byc.begin(), byc.end(), [&](int64_t a, int64_t b) { return cols[a] < cols[b]; });
     std::stable_sort(byr.begin(), byr.end(), [&](int64_t a, int64_t b) { return rows[a] < rows[b]; });
-    for (int64_t e : byc) fwd_ent[fpos[rslot_of[rows[e]]]++] = make_int2(off_in(cloc[e]), (int)e);
-    for (int64_t e : byr) bwd_ent[bpos[cslot_of[cols[e]]]++] = make_int2(off_out(rloc[e]), (int)e);
-    for (int64_t e = 0; e < nnz; ++e) sdd[e] = make_int2(off_out(rloc[e]), off_in(cloc[e]));
+    for (int64_t e : byc) by_row[rows[e]].push_back((int)e);
+    for (int64_t e : byr) by_col[cols[e]].push_back((int)e);
   }
+  const StreamHost gfwd = build_stream(
+      by_row, [&](int e) { return off_in(cloc[e]); }, [&](int64_t r) { return off_out(locate(r, f_out->rho)); });
+  const StreamHost gbwd = build_stream(
+      by_col, [&](int e) { return off_out(rloc[e]); }, [&](int64_t c) { return off_in(locate(c, f_in->rho)); });
   // merge buckets (R, S)
   const int64_t nb = (int64_t)FO.nblk * FI.nblk;
   std::vector<int> mrg_ptr((size_t)nb + 1, 0);
@@ -422,13 +454,11 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
         w.x = (w.x & ~ff::kSlotSrcMask) | (row * 32 + 16 * (row & 1));
       }
   } else {
-    // the generic kernels' layout is the forward table's entry order, so the forward reads a
-    // row's coefficients by table position
-    user_of_slot.resize((size_t)nnz);
-    for (int64_t j = 0; j < nnz; ++j) {
-      user_of_slot[j] = fwd_ent[j].y;
-      slot_of_user[fwd_ent[j].y] = (int)j;
-    }
+    // the generic kernels' layout is the forward stream's entry order, padding included, so
+    // the forward reads coefficients by stream position
+    user_of_slot.assign(gfwd.id.begin(), gfwd.id.end());
+    for (size_t j = 0; j < gfwd.id.size(); ++j)
+      if (gfwd.id[j] >= 0) slot_of_user[gfwd.id[j]] = (int)j;
   }
   const int64_t nslot = (int64_t)user_of_slot.size();   // coefficient slots (>= nnz)
   // for the 128-wide backward: the backward slot of every coefficient slot (padding slots go
@@ -439,16 +469,14 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     for (int64_t j = 0; j < nslot; ++j)
       bwd_pos[j] = user_of_slot[j] >= 0 ? bwd_slot_of_user[user_of_slot[j]] : (int)b_st.size();
   }
-  // the generic kernels index coefficients by slot too; padding slots of the dC table are
-  // marked (-1, -1) and produce zeros
-  for (auto& en : fwd_ent) en.y = nnz ? slot_of_user[en.y] : 0;
-  for (auto& en : bwd_ent) en.y = nnz ? slot_of_user[en.y] : 0;
   for (auto& en : mrg_ent) en.z = nnz ? slot_of_user[en.z] : 0;
-  {
-    std::vector<int2> sdd_slot((size_t)std::max<int64_t>(nslot, 1), make_int2(-1, -1));
-    for (int64_t e = 0; e < nnz; ++e) sdd_slot[slot_of_user[e]] = sdd[e];
-    sdd = std::move(sdd_slot);
-  }
+  // coefficient slot of every generic stream element (-1: padding), and the slots with no entry
+  std::vector<int> fcoef(gfwd.id.size()), bcoef(gbwd.id.size()), coef_pad;
+  for (size_t j = 0; j < fcoef.size(); ++j) fcoef[j] = gfwd.id[j] >= 0 ? slot_of_user[gfwd.id[j]] : -1;
+  for (size_t j = 0; j < bcoef.size(); ++j) bcoef[j] = gbwd.id[j] >= 0 ? slot_of_user[gbwd.id[j]] : -1;
+  for (int64_t j = 0; j < nslot; ++j)
+    if (user_of_slot[j] < 0) coef_pad.push_back((int)j);
+  const size_t gf_elems = gfwd.ent.size(), gb_elems = gbwd.ent.size();
   p->user_order = std::move(user_of_slot);
   p->coef_slots = nslot;
   const int64_t fast_tiles = fast ? (max_tokens + ff::kFastTileTokens - 1) / ff::kFastTileTokens : 0;
@@ -464,28 +492,44 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
 
   // ---------------- device memory: one allocation for every table and the workspace
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t partial_elems = std::max((size_t)max_batch * (size_t)p->max_tiles * (size_t)nslot,
+  const size_t partial_elems = std::max((size_t)max_batch * (size_t)p->max_tiles * gb_elems,
                                         (size_t)max_batch * (size_t)fast_tiles *
                                             (fast ? ff::fast128_partial_floats(b_st.size()) : 0));
   struct Blob {
     const void* src;
     size_t bytes;
   };
-  const std::vector<Blob> blobs = {
-      {fwd_slot_off.data(), m * sizeof(int)},      {fwd_ptr.data(), (m + 1) * sizeof(int)},
-      {fwd_ent.data(), fwd_ent.size() * sizeof(int2)}, {bwd_slot_off.data(), n * sizeof(int)},
-      {bwd_ptr.data(), (n + 1) * sizeof(int)},      {bwd_ent.data(), bwd_ent.size() * sizeof(int2)},
-      {sdd.data(), sdd.size() * sizeof(int2)},       {mrg_ptr.data(), (nb + 1) * sizeof(int)},
-      {mrg_ent.data(), mrg_ent.size() * sizeof(int4)},
-      {f_pl.data(), f_pl.size() * sizeof(int4)},      {b_pl.data(), b_pl.size() * sizeof(int4)},
-      {f_st.data(), f_st.size() * sizeof(uint32_t)},  {pad_slots.data(), pad_slots.size() * sizeof(int)},
-      {b_w.data(), b_w.size() * sizeof(uint32_t)},
-      {nullptr, std::max<size_t>(partial_elems, 1) * sizeof(float)},
-      // the backward's coefficients in its stream's slot order, per adapter (+ a scratch group)
-      {nullptr, std::max<size_t>((size_t)max_batch * (b_st.size() + 256), 1) * sizeof(float)},
-      {bwd_pos.data(), bwd_pos.size() * sizeof(int)},
-      {f_em.data(), f_em.size() * sizeof(uint32_t)},  {b_dst.data(), b_dst.size() * sizeof(uint32_t)},
-      {b_em.data(), b_em.size() * sizeof(uint32_t)},  {b_pad.data(), b_pad.size() * sizeof(int)}};
+  enum {
+    kGfEnt, kGfCoef, kGfWave, kGbEnt, kGbCoef, kGbWave, kCoefPad, kCfwd, kCbwd, kMrgPtr, kMrgEnt,
+    kFPl, kBPl, kFSt, kPadSlots, kBW, kPartial, kCoefBwd, kBwdPos, kFEm, kBDst, kBEm, kBPad, kNumBlobs
+  };
+  std::vector<Blob> blobs(kNumBlobs);
+  blobs[kGfEnt] = {gfwd.ent.data(), gf_elems * sizeof(int2)};
+  blobs[kGfCoef] = {fcoef.data(), gf_elems * sizeof(int)};
+  blobs[kGfWave] = {gfwd.wave_row.data(), gfwd.wave_row.size() * sizeof(int)};
+  blobs[kGbEnt] = {gbwd.ent.data(), gb_elems * sizeof(int2)};
+  blobs[kGbCoef] = {bcoef.data(), gb_elems * sizeof(int)};
+  blobs[kGbWave] = {gbwd.wave_row.data(), gbwd.wave_row.size() * sizeof(int)};
+  blobs[kCoefPad] = {coef_pad.data(), coef_pad.size() * sizeof(int)};
+  // per-call coefficient copies in the generic streams' orders (the forward's only when the
+  // coefficient layout is not already its order)
+  blobs[kCfwd] = {nullptr, (fast ? (size_t)max_batch * gf_elems : 1) * sizeof(float)};
+  blobs[kCbwd] = {nullptr, (size_t)max_batch * gb_elems * sizeof(float)};
+  blobs[kMrgPtr] = {mrg_ptr.data(), (nb + 1) * sizeof(int)};
+  blobs[kMrgEnt] = {mrg_ent.data(), mrg_ent.size() * sizeof(int4)};
+  blobs[kFPl] = {f_pl.data(), f_pl.size() * sizeof(int4)};
+  blobs[kBPl] = {b_pl.data(), b_pl.size() * sizeof(int4)};
+  blobs[kFSt] = {f_st.data(), f_st.size() * sizeof(uint32_t)};
+  blobs[kPadSlots] = {pad_slots.data(), pad_slots.size() * sizeof(int)};
+  blobs[kBW] = {b_w.data(), b_w.size() * sizeof(uint32_t)};
+  blobs[kPartial] = {nullptr, std::max<size_t>(partial_elems, 1) * sizeof(float)};
+  // the backward's coefficients in its stream's slot order, per adapter (+ a scratch group)
+  blobs[kCoefBwd] = {nullptr, std::max<size_t>((size_t)max_batch * (b_st.size() + 256), 1) * sizeof(float)};
+  blobs[kBwdPos] = {bwd_pos.data(), bwd_pos.size() * sizeof(int)};
+  blobs[kFEm] = {f_em.data(), f_em.size() * sizeof(uint32_t)};
+  blobs[kBDst] = {b_dst.data(), b_dst.size() * sizeof(uint32_t)};
+  blobs[kBEm] = {b_em.data(), b_em.size() * sizeof(uint32_t)};
+  blobs[kBPad] = {b_pad.data(), b_pad.size() * sizeof(int)};
   size_t total = 0;
   for (const Blob& b : blobs) total += up(b.bytes);
   int cur = 0;
@@ -511,42 +555,39 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   }
   // the backward's padding slots keep zero coefficients: the per-call copy writes only the
   // slots that hold entries
-  if (hipMemset(where[15], 0, blobs[15].bytes) != hipSuccess) {
+  if (hipMemset(where[kCoefBwd], 0, blobs[kCoefBwd].bytes) != hipSuccess) {
     (void)hipFree(mem);
     return ff::fail(FF_EDEVICE, "clearing the plan workspace failed");
   }
   ff::PlanDev& pd = p->dev;
-  pd.fwd_slot_off = (const int*)where[0];
-  pd.fwd_ptr = (const int*)where[1];
-  pd.fwd_ent = (const int2*)where[2];
-  pd.fwd_nslots = (int)m;
-  pd.fwd_by_entry = fast ? 0 : 1;
-  pd.bwd_slot_off = (const int*)where[3];
-  pd.bwd_ptr = (const int*)where[4];
-  pd.bwd_ent = (const int2*)where[5];
-  pd.bwd_nslots = (int)n;
-  pd.sdd = (const int2*)where[6];
-  pd.mrg_ptr = (const int*)where[7];
-  pd.mrg_ent = (const int4*)where[8];
+  pd.fwd = {(const int2*)where[kGfEnt], (const int*)where[kGfCoef], (const int*)where[kGfWave], (int)gfwd.rows};
+  pd.bwd = {(const int2*)where[kGbEnt], (const int*)where[kGbCoef], (const int*)where[kGbWave], (int)gbwd.rows};
+  pd.fwd_by_pos = fast ? 0 : 1;
+  pd.coef_pad = (const int*)where[kCoefPad];
+  pd.ncoef_pad = (int)coef_pad.size();
+  pd.c_fwd = (float*)where[kCfwd];
+  pd.c_bwd = (float*)where[kCbwd];
+  pd.mrg_ptr = (const int*)where[kMrgPtr];
+  pd.mrg_ent = (const int4*)where[kMrgEnt];
   pd.mrg_max_bucket = max_bucket;
   pd.nnz = (int)nslot;
   ff::FastPlanDev& fp = p->fast;
   fp.enabled = fast ? 1 : 0;
-  fp.fwd_pl = (const int4*)where[9];
-  fp.bwd_pl = (const int4*)where[10];
-  fp.fwd_em = (const uint32_t*)where[17];
-  fp.fwd_st = (const uint32_t*)where[11];
-  fp.pad = (const int*)where[12];
+  fp.fwd_pl = (const int4*)where[kFPl];
+  fp.bwd_pl = (const int4*)where[kBPl];
+  fp.fwd_em = (const uint32_t*)where[kFEm];
+  fp.fwd_st = (const uint32_t*)where[kFSt];
+  fp.pad = (const int*)where[kPadSlots];
   fp.npad = (int)pad_slots.size();
-  fp.bwd_st = (const uint32_t*)where[13];
-  fp.bwd_dst = (const uint32_t*)where[18];
-  fp.bwd_em = (const uint32_t*)where[19];
-  fp.bwd_pad = (const int*)where[20];
+  fp.bwd_st = (const uint32_t*)where[kBW];
+  fp.bwd_dst = (const uint32_t*)where[kBDst];
+  fp.bwd_em = (const uint32_t*)where[kBEm];
+  fp.bwd_pad = (const int*)where[kBPad];
   fp.nbpad = (int)b_pad.size();
   fp.bwd_slots = (int)b_st.size();
-  p->partial = (float*)where[14];
-  fp.coef_bwd = (float*)where[15];
-  fp.bwd_pos = (const int*)where[16];
+  p->partial = (float*)where[kPartial];
+  fp.coef_bwd = (float*)where[kCoefBwd];
+  fp.bwd_pos = (const int*)where[kBwdPos];
   fp.coef_slots = (int)nslot;
   fp.bwd16 = bwd16 ? 1 : 0;
   p->dev_mem = mem;

@@ -31,6 +31,29 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16;
 
+// Accesses to global memory go through global-address-space pointers, so that they compile to
+// global rather than flat instructions: a flat access also counts against the LDS counter, and a
+// wait for an LDS read would then wait for every global load in flight.
+#define FF_GLOBAL __attribute__((address_space(1)))
+// (HIP's vector types cannot be accessed through such pointers; they move as raw words.)
+typedef unsigned raw2 __attribute__((ext_vector_type(2)));
+typedef unsigned raw4 __attribute__((ext_vector_type(4)));
+template <int N> struct Raw;
+template <> struct Raw<2> { using T = unsigned short; };
+template <> struct Raw<4> { using T = unsigned; };
+template <> struct Raw<8> { using T = raw2; };
+template <> struct Raw<16> { using T = raw4; };
+template <class T>
+__device__ __forceinline__ T gload(const T* p) {
+  using R = typename Raw<sizeof(T)>::T;
+  return __builtin_bit_cast(T, *(const FF_GLOBAL R*)p);
+}
+template <class T>
+__device__ __forceinline__ void gstore(T* p, const T& v) {
+  using R = typename Raw<sizeof(T)>::T;
+  *(FF_GLOBAL R*)p = __builtin_bit_cast(R, v);
+}
+
 __device__ __forceinline__ float bf2f(u16 h) { return __uint_as_float((unsigned)h << 16); }
 
 // fp32 -> bf16, round to nearest even (NaN kept quiet).
@@ -49,16 +72,19 @@ struct Act<true> {
   using E = u16;
   static __device__ __forceinline__ float ld(const E* p) { return bf2f(*p); }
   static __device__ __forceinline__ void st(E* p, float v) { *p = f2bf(v); }
-  static __device__ __forceinline__ f32x4 ld4(const E* p) {
-    const uint2 w = *reinterpret_cast<const uint2*>(p);
-    return f32x4{bf2f((u16)(w.x & 0xffff)), bf2f((u16)(w.x >> 16)), bf2f((u16)(w.y & 0xffff)),
-                 bf2f((u16)(w.y >> 16))};
-  }
-  static __device__ __forceinline__ void st4(E* p, f32x4 v) {
+  static __device__ __forceinline__ f32x4 ld4(const E* p) { return unpack4(*reinterpret_cast<const uint2*>(p)); }
+  static __device__ __forceinline__ void st4(E* p, f32x4 v) { *reinterpret_cast<uint2*>(p) = pack4(v); }
+  static __device__ __forceinline__ f32x4 gld4(const E* p) { return unpack4(gload(reinterpret_cast<const uint2*>(p))); }
+  static __device__ __forceinline__ void gst4(E* p, f32x4 v) { gstore(reinterpret_cast<uint2*>(p), pack4(v)); }
+  static __device__ __forceinline__ uint2 pack4(f32x4 v) {
     uint2 w;
     w.x = (unsigned)f2bf(v[0]) | ((unsigned)f2bf(v[1]) << 16);
     w.y = (unsigned)f2bf(v[2]) | ((unsigned)f2bf(v[3]) << 16);
-    *reinterpret_cast<uint2*>(p) = w;
+    return w;
+  }
+  static __device__ __forceinline__ f32x4 unpack4(uint2 w) {
+    return f32x4{bf2f((u16)(w.x & 0xffff)), bf2f((u16)(w.x >> 16)), bf2f((u16)(w.y & 0xffff)),
+                 bf2f((u16)(w.y >> 16))};
   }
 };
 
@@ -69,6 +95,8 @@ struct Act<false> {
   static __device__ __forceinline__ void st(E* p, float v) { *p = v; }
   static __device__ __forceinline__ f32x4 ld4(const E* p) { return *reinterpret_cast<const f32x4*>(p); }
   static __device__ __forceinline__ void st4(E* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+  static __device__ __forceinline__ f32x4 gld4(const E* p) { return gload(reinterpret_cast<const f32x4*>(p)); }
+  static __device__ __forceinline__ void gst4(E* p, f32x4 v) { gstore(reinterpret_cast<f32x4*>(p), v); }
 };
 
 // ---------------------------------------------------------------------------------------------
@@ -104,13 +132,14 @@ struct Mfma<false> {
 };
 
 // This lane's contraction inputs of step ks for a column whose storage starts at `in`.
-template <bool BF16>
+template <bool BF16, bool GSRC>
 __device__ __forceinline__ typename Mfma<BF16>::V load_operand(const typename Act<BF16>::E* in, bool ok, int lim,
                                                                int ks, int q) {
   using M = Mfma<BF16>;
-  typename M::V b{};
+  using V = typename M::V;
+  V b{};
   const int i0 = ks * M::KS + q * M::VL;
-  if (ok && i0 < lim) b = *reinterpret_cast<const typename M::V*>(in + i0);
+  if (ok && i0 < lim) b = GSRC ? gload(reinterpret_cast<const V*>(in + i0)) : *reinterpret_cast<const V*>(in + i0);
   return b;
 }
 
@@ -118,19 +147,20 @@ __device__ __forceinline__ typename Mfma<BF16>::V load_operand(const typename Ac
 // M applied to the column starting at col(c).  The MT x KT fragments of M stay in registers for
 // the whole call; each wave takes every nw-th group of 16 columns and loads the next group's
 // inputs while it multiplies the current one.
-template <bool BF16, int MT, int KT, class Col, class Epi>
+template <bool BF16, bool GSRC, int MT, int KT, class Col, class Epi>
 __device__ __forceinline__ void column_apply_reg(const void* frag, int ncols, int lim, Col col, Epi epi) {
   using M = Mfma<BF16>;
   using V = typename M::V;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6, q = lane >> 4;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
+            q = lane >> 4;
   const int ngrp = (ncols + 15) / 16;
   if (wave >= ngrp) return;
-  const V* fr = reinterpret_cast<const V*>(frag);
+  const V* fr = (reinterpret_cast<const V*>(frag));
   V fa[MT][KT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int ks = 0; ks < KT; ++ks) fa[mt][ks] = fr[(mt * KT + ks) * 64 + lane];
+    for (int ks = 0; ks < KT; ++ks) fa[mt][ks] = gload(&fr[(mt * KT + ks) * 64 + lane]);
   // two operand buffers used in turn (no copies, which would wait for the loads in flight)
   V ba[KT], bb[KT];
   auto load = [&](int g, V (&b)[KT]) {
@@ -138,7 +168,7 @@ __device__ __forceinline__ void column_apply_reg(const void* frag, int ncols, in
     const bool ok = c < ncols;
     const auto* in = col(ok ? c : 0);
 #pragma unroll
-    for (int ks = 0; ks < KT; ++ks) b[ks] = load_operand<BF16>(in, ok, lim, ks, q);
+    for (int ks = 0; ks < KT; ++ks) b[ks] = load_operand<BF16, GSRC>(in, ok, lim, ks, q);
   };
   auto mul = [&](int g, const V (&b)[KT]) {
     f32x4 acc[MT];
@@ -169,15 +199,16 @@ __device__ __forceinline__ void column_apply_reg(const void* frag, int ncols, in
 // inputs are all loaded before its first output is stored, so the column may be transformed in
 // place (factored frames always qualify: W2 <= 128); longer contractions reload them per output
 // chunk and need a separate destination.
-template <bool BF16, class Col, class Epi>
+template <bool BF16, bool GSRC, class Col, class Epi>
 __device__ __forceinline__ void column_apply_mem(const void* frag, int MT, int KT, int ncols, int lim, Col col,
                                                  Epi epi) {
   using M = Mfma<BF16>;
   using V = typename M::V;
   constexpr int kC = 4, kPre = 8;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6, q = lane >> 4;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
+            q = lane >> 4;
   const int ngrp = (ncols + 15) / 16;
-  const V* fr = reinterpret_cast<const V*>(frag);
+  const V* fr = (reinterpret_cast<const V*>(frag));
   const bool pre = KT <= kPre;
   for (int g = wave; g < ngrp; g += nw) {
     const int c = g * 16 + (lane & 15);
@@ -186,7 +217,7 @@ __device__ __forceinline__ void column_apply_mem(const void* frag, int MT, int K
     V bp[kPre];
     if (pre) {
 #pragma unroll
-      for (int ks = 0; ks < kPre; ++ks) bp[ks] = ks < KT ? load_operand<BF16>(in, ok, lim, ks, q) : V{};
+      for (int ks = 0; ks < kPre; ++ks) bp[ks] = ks < KT ? load_operand<BF16, GSRC>(in, ok, lim, ks, q) : V{};
     }
     for (int mt0 = 0; mt0 < MT; mt0 += kC) {
       f32x4 acc[kC];
@@ -200,11 +231,11 @@ __device__ __forceinline__ void column_apply_mem(const void* frag, int MT, int K
           for (int j = 1; j < kPre; ++j)
             if (ks == j) b = bp[j];
         } else {
-          b = load_operand<BF16>(in, ok, lim, ks, q);
+          b = load_operand<BF16, GSRC>(in, ok, lim, ks, q);
         }
 #pragma unroll
         for (int j = 0; j < kC; ++j) {
-          const V a = fr[((size_t)min(mt0 + j, MT - 1) * KT + ks) * 64 + lane];
+          const V a = gload(&fr[((size_t)min(mt0 + j, MT - 1) * KT + ks) * 64 + lane]);
           if (mt0 + j < MT) acc[j] = M::step(a, b, acc[j]);
         }
       }
@@ -218,13 +249,13 @@ __device__ __forceinline__ void column_apply_mem(const void* frag, int MT, int K
 }
 
 // Dispatch on the matrix shape: register-resident for the shapes the frames here produce.
-template <bool BF16, class Col, class Epi>
+template <bool BF16, bool GSRC, class Col, class Epi>
 __device__ __forceinline__ void column_apply(const FrameDev& f, bool synth, int ncols, int lim, Col col, Epi epi) {
   const void* frag = BF16 ? (synth ? f.fs16 : f.fa16) : (synth ? f.fs32 : f.fa32);
   const int KT = BF16 ? f.KT : f.KT4;
 #define FF_SHAPE(mt, kt)                                                       \
   case (mt) * 64 + (kt):                                                       \
-    column_apply_reg<BF16, mt, kt>(frag, ncols, lim, col, epi);                \
+    column_apply_reg<BF16, GSRC, mt, kt>(frag, ncols, lim, col, epi);          \
     return;
   if constexpr (BF16) {
     switch (f.MT * 64 + KT) {
@@ -239,7 +270,7 @@ __device__ __forceinline__ void column_apply(const FrameDev& f, bool synth, int 
     }
   }
 #undef FF_SHAPE
-  column_apply_mem<BF16>(frag, f.MT, KT, ncols, lim, col, epi);
+  column_apply_mem<BF16, GSRC>(frag, f.MT, KT, ncols, lim, col, epi);
 }
 
 // Two consecutive activations (one complex coordinate) as fp32, and back.
@@ -258,6 +289,22 @@ __device__ __forceinline__ void st2(typename Act<BF16>::E* p, float2 v) {
     *reinterpret_cast<unsigned*>(p) = (unsigned)f2bf(v.x) | ((unsigned)f2bf(v.y) << 16);
   else
     *reinterpret_cast<float2*>(p) = v;
+}
+template <bool BF16>
+__device__ __forceinline__ float2 gld2(const typename Act<BF16>::E* p) {
+  if constexpr (BF16) {
+    const unsigned w = gload(reinterpret_cast<const unsigned*>(p));
+    return make_float2(bf2f((u16)(w & 0xffff)), bf2f((u16)(w >> 16)));
+  } else {
+    return gload(reinterpret_cast<const float2*>(p));
+  }
+}
+template <bool BF16>
+__device__ __forceinline__ void gst2(typename Act<BF16>::E* p, float2 v) {
+  if constexpr (BF16)
+    gstore(reinterpret_cast<unsigned*>(p), (unsigned)f2bf(v.x) | ((unsigned)f2bf(v.y) << 16));
+  else
+    gstore(reinterpret_cast<float2*>(p), v);
 }
 __device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
 __device__ __forceinline__ float2 csub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
@@ -281,7 +328,8 @@ __device__ __forceinline__ int div_small(int x, int d, float inv) {
 // The twiddle factors of a factored frame, copied to LDS (the caller synchronizes).
 __device__ __forceinline__ void stage_twiddles(const FrameDev& f, float2* lds) {
   if (f.radix == 1) return;
-  for (int i = threadIdx.x; i < 3 * f.k2; i += blockDim.x) lds[i] = f.tw[i];
+  const float2* tw = (f.tw);
+  for (int i = threadIdx.x; i < 3 * f.k2; i += blockDim.x) lds[i] = gload(&tw[i]);
 }
 
 // Radix-4 stage of the factored analysis for every (token, block, b < k2) of a tile:
@@ -309,7 +357,7 @@ __device__ __forceinline__ void radix4_analysis(const FrameDev& f, const float2*
       b[u] = r - blk * k2;
       const E* xp = src + (long)t * ld + blk * W + 2 * b[u];
 #pragma unroll
-      for (int a = 0; a < 4; ++a) x[u][a] = ld2<BF16>(xp + 2 * a * k2);
+      for (int a = 0; a < 4; ++a) x[u][a] = gld2<BF16>(xp + 2 * a * k2);
 #pragma unroll
       for (int a = 0; a < 3; ++a) w[u][a] = tw[a * k2 + b[u]];
       y[u] = dst + t * ldt + blk * ldb + 2 * b[u];
@@ -372,11 +420,11 @@ __device__ __forceinline__ void radix4_synthesis(const FrameDev& f, const float2
       for (int a = 0; a < 4; ++a) {
         float2 v = make_float2(s * xo[a].x, s * xo[a].y);
         if (beta != 0.f) {
-          const float2 old = ld2<BF16>(out[u] + 2 * a * k2);
+          const float2 old = gld2<BF16>(out[u] + 2 * a * k2);
           v.x = fmaf(beta, old.x, v.x);
           v.y = fmaf(beta, old.y, v.y);
         }
-        st2<BF16>(out[u] + 2 * a * k2, v);
+        gst2<BF16>(out[u] + 2 * a * k2, v);
       }
     }
   }
@@ -406,7 +454,7 @@ __device__ __forceinline__ void analysis_to_lds(const FrameDev& f, const float2*
   const int nblk = f.nblk;
   if (f.radix == 1) {
     const int W = f.W;
-    column_apply<BF16>(
+    column_apply<BF16, true>(
         f, false, nt * nblk, W,
         [&](int c) {
           const int t = c / nblk;
@@ -427,7 +475,7 @@ __device__ __forceinline__ void analysis_to_lds(const FrameDev& f, const float2*
     const int tb = c >> 2, t = tb / nblk;
     return dst + t * ldt + (tb - t * nblk) * ldb + (c & 3) * cs;
   };
-  column_apply<BF16>(
+  column_apply<BF16, false>(
       f, false, nt * nblk * 4, cs, [&](int c) -> const E* { return at(c); },
       [&](int c, int o, f32x4 v) {
         if (o < cs) A::st4(at(c) + o, v);
@@ -445,7 +493,7 @@ __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const floa
   const int nblk = f.nblk;
   if (f.radix == 1) {
     const int W = f.W;
-    column_apply<BF16>(
+    column_apply<BF16, false>(
         f, true, nt * nblk, W,
         [&](int c) -> const E* {
           const int t = c / nblk;
@@ -456,8 +504,8 @@ __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const floa
             const int t = c / nblk;
             E* p = dst + (long)t * ld + (c - t * nblk) * W + o;
             f32x4 r = v * s;
-            if (beta != 0.f) r += beta * A::ld4(p);
-            A::st4(p, r);
+            if (beta != 0.f) r += beta * A::gld4(p);
+            A::gst4(p, r);
           }
         });
     return;
@@ -467,7 +515,7 @@ __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const floa
     const int tb = c >> 2, t = tb / nblk;
     return src + t * ldt + (tb - t * nblk) * ldb + (c & 3) * cs;
   };
-  column_apply<BF16>(
+  column_apply<BF16, false>(
       f, true, nt * nblk * 4, cs, [&](int c) -> const E* { return at(c); },
       [&](int c, int o, f32x4 v) {
         if (o < cs) A::st4(at(c) + o, v);
@@ -492,21 +540,22 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
                                                 typename Act<BF16>::E* dst, int ld_dst, int tg0, int ntg,
                                                 bool write_dst, float* part) {
   using A = Act<BF16>;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r0 = S.wave_row[wave], r1 = S.wave_row[wave + 1];
   if (r0 >= r1) return;
+  const int2* ent = (S.ent);
   src += tg0 * ld_src;
   dst += tg0 * ld_dst;
   // Two buffers of kSD rows, each refilled right after it is consumed, so that the other one's
-  // loads stay in flight meanwhile (a copy between buffers would wait for them).
+  // loads stay in flight meanwhile.
   int2 ea[kSD], eb[kSD];
   float ca[kSD], cb[kSD];
   auto load = [&](int r, int2 (&e)[kSD], float (&c)[kSD]) {
 #pragma unroll
     for (int i = 0; i < kSD; ++i) {
       const int j = min(r + i, r1 - 1) * 64 + lane;   // rows past the run repeat its last one, unused
-      e[i] = S.ent[j];
-      c[i] = cv[j];
+      e[i] = gload(&ent[j]);
+      c[i] = gload(&cv[j]);
     }
   };
   // Every row reads kTG token rows without branches (tokens past ntg repeat the last one; their
@@ -521,11 +570,23 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
 #pragma unroll
   for (int t = 0; t < kTG; ++t) acc[t] = zb[t] = 0.f;
   bool start = true;   // the next row begins a slab
-  auto consume = [&](int r, const int2 (&e)[kSD], const float (&c)[kSD]) {
+  // The source values of row i + 1 are read before row i is processed (the source tile is not
+  // written during the walk), alternating between two register sets.
+  auto read = [&](const int2& e, float (&x)[kTG]) {
+    const int so = e.x & 0x7fffffff;
+#pragma unroll
+    for (int t = 0; t < kTG; ++t) x[t] = A::ld(src + tso[t] + so);
+  };
+  // Rows r .. r + n - 1 of a buffer (n = kSD in the main loop, so that its body has no exits).
+  auto consume = [&](int r, const int2 (&e)[kSD], const float (&c)[kSD], int n) {
+    float xa[kTG], xb[kTG];
+    read(e[0], xa);
 #pragma unroll
     for (int i = 0; i < kSD; ++i) {
-      if (r + i >= r1) break;
-      const int so = e[i].x & 0x7fffffff, d = e[i].y;
+      if (i >= n) break;
+      float (&x)[kTG] = (i & 1) ? xb : xa;
+      if (i + 1 < kSD && i + 1 < n) read(e[i + 1], (i & 1) ? xa : xb);
+      const int d = e[i].y;
       if (BWD && part && start) {
         const int dc0 = max(d, 0);
         float zv[kTG];
@@ -535,9 +596,6 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
         for (int t = 0; t < kTG; ++t) zb[t] = (t < ntg && d >= 0) ? zv[t] : 0.f;
       }
       start = false;
-      float x[kTG];
-#pragma unroll
-      for (int t = 0; t < kTG; ++t) x[t] = A::ld(src + tso[t] + so);
       float dc = 0.f;
 #pragma unroll
       for (int t = 0; t < kTG; ++t) {
@@ -545,13 +603,11 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
         if (BWD) dc = fmaf(x[t], zb[t], dc);
       }
       if (BWD && part) {
-        // a plain store unless a previous token pass wrote this element (the compiler would
-        // otherwise load it on every pass)
         float* pp = part + (long)(r + i) * 64 + lane;
         if constexpr (PART_ADD)
-          *pp += dc;
+          gstore(pp, gload(pp) + dc);
         else
-          *pp = dc;
+          gstore(pp, dc);
       }
       if (__builtin_amdgcn_readfirstlane(e[i].x) < 0) {   // the slab's last row (same in every lane)
         if (write_dst && d >= 0) {
@@ -565,14 +621,19 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
       }
     }
   };
+  // whole pairs of buffers first, then the remaining rows
+  const int rend = r0 + (r1 - r0) / (2 * kSD) * (2 * kSD);
   load(r0, ea, ca);
   load(r0 + kSD, eb, cb);
-  for (int r = r0; r < r1; r += 2 * kSD) {
-    consume(r, ea, ca);
-    if (r + kSD >= r1) break;
+  for (int r = r0; r < rend; r += 2 * kSD) {
+    consume(r, ea, ca, kSD);
     load(r + 2 * kSD, ea, ca);
-    consume(r + kSD, eb, cb);
+    consume(r + kSD, eb, cb, kSD);
     load(r + 3 * kSD, eb, cb);
+  }
+  if (rend < r1) {
+    consume(rend, ea, ca, min(kSD, r1 - rend));
+    if (rend + kSD < r1) consume(rend + kSD, eb, cb, r1 - rend - kSD);
   }
 }
 
@@ -621,9 +682,9 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   E* zt = reinterpret_cast<E*>(smem);           // tt x ldt_in   z = P_in^T x
   E* vt = zt + (size_t)a.tt * a.ldt_in;         // tt x ldt_out  v = C z
   const int bi = blockIdx.y;
-  const E* X = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X);
-  E* Y = reinterpret_cast<E*>(a.Ys ? a.Ys[bi] : a.Y);
-  const float* cv = a.ccopy ? a.ccopy + bi * a.cstride : a.cs ? a.cs[bi] : a.c;
+  const E* X = (reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X));
+  E* Y = (reinterpret_cast<E*>(a.Ys ? a.Ys[bi] : a.Y));
+  const float* cv = (a.ccopy ? a.ccopy + bi * a.cstride : a.cs ? a.cs[bi] : a.c);
   const int t0 = blockIdx.x * a.tt;
   const int nt = min(a.tt, a.T - t0);
   X += (long)t0 * a.ldx;
@@ -680,7 +741,7 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   const int bi = blockIdx.y;
   const int t0 = blockIdx.x * a.tt;
   const int nt = min(a.tt, a.T - t0);
-  const E* G = reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G) + (long)t0 * a.ldg;
+  const E* G = (reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G)) + (long)t0 * a.ldg;
 
   // twiddle factors of factored frames after the tiles
   float2* tw_in = reinterpret_cast<float2*>(zt + (size_t)a.tt * a.ldt_in);
@@ -693,19 +754,19 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
   analysis_to_lds<BF16>(a.fout, tw_out, nt, G, a.ldg, ut, a.ldt_out, a.ldb_out);
   if (a.want_dc) {
-    const E* X = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx;
+    const E* X = (reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X)) + (long)t0 * a.ldx;
     analysis_to_lds<BF16>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
   }
   __syncthreads();
 
   // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
-  const float* cv = a.ccopy + bi * a.cstride;
-  float* part = a.want_dc ? a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.cstride : nullptr;
+  const float* cv = (a.ccopy + bi * a.cstride);
+  float* part = a.want_dc ? (a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.cstride) : nullptr;
   stream_all<BF16, true>(a.st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part);
   if (!a.want_dx) return;
   __syncthreads();
 
-  E* dX = reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX) + (long)t0 * a.lddx;
+  E* dX = (reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX)) + (long)t0 * a.lddx;
   synthesis_from_lds<BF16>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX, a.lddx, a.scale, a.beta);
 }
 

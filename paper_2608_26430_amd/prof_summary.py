@@ -30,7 +30,7 @@ def table(stats_csv: str) -> str:
     return "\n".join(out)
 
 
-KERNELS = {"fwd128": "fwd_kernel", "bwd128": "bwd_kernel", "reduce128": "reduce_kernel",
+KERNELS = {"fwd128": "fwd_kernel", "bwd128": "bwd_kernel", "bwd16": "bwd_kernel", "reduce128": "reduce_kernel",
            "fwd_kernel": "fwd_kernel", "bwd_kernel": "bwd_kernel", "dc_reduce": "reduce_kernel"}
 
 

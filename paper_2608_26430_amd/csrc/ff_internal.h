@@ -144,6 +144,7 @@ struct ff_plan {
   int tile_tokens[2] = {0, 0};     // tokens per fused-kernel tile
   size_t lds_bytes[2] = {0, 0};
   int64_t max_tiles = 0;           // tiles of the largest call, per adapter
+  int gen_wgs = 1;                 // workgroups per adapter of the generic backward (one per CU)
   float* partial = nullptr;        // dC partial sums per tile (layout depends on the kernels)
   size_t workspace_bytes = 0;
   void* dev_mem = nullptr;

@@ -155,7 +155,10 @@ __device__ __forceinline__ void column_apply_reg(const void* frag, int ncols, in
             q = lane >> 4;
   const int ngrp = (ncols + 15) / 16;
   if (wave >= ngrp) return;
-  const V* fr = (reinterpret_cast<const V*>(frag));
+  const V* fr = reinterpret_cast<const V*>(frag);
+  // opaque at every call, so that a caller's loop does not keep the fragments of all its frame
+  // applies live across iterations (they would not fit in registers)
+  asm volatile("" : "+s"(fr));
   V fa[MT][KT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
@@ -208,7 +211,7 @@ __device__ __forceinline__ void column_apply_mem(const void* frag, int MT, int K
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
             q = lane >> 4;
   const int ngrp = (ncols + 15) / 16;
-  const V* fr = (reinterpret_cast<const V*>(frag));
+  const V* fr = reinterpret_cast<const V*>(frag);
   const bool pre = KT <= kPre;
   for (int g = wave; g < ngrp; g += nw) {
     const int c = g * 16 + (lane & 15);
@@ -550,12 +553,14 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
   // loads stay in flight meanwhile.
   int2 ea[kSD], eb[kSD];
   float ca[kSD], cb[kSD];
-  auto load = [&](int r, int2 (&e)[kSD], float (&c)[kSD]) {
+  float pa[kSD], pb[kSD];   // PART_ADD: the partial sums to add to, loaded with the entries
+  auto load = [&](int r, int2 (&e)[kSD], float (&c)[kSD], float (&pv)[kSD]) {
 #pragma unroll
     for (int i = 0; i < kSD; ++i) {
       const int j = min(r + i, r1 - 1) * 64 + lane;   // rows past the run repeat its last one, unused
       e[i] = gload(&ent[j]);
       c[i] = gload(&cv[j]);
+      if (BWD && PART_ADD && part) pv[i] = gload(&part[j]);
     }
   };
   // Every row reads kTG token rows without branches (tokens past ntg repeat the last one; their
@@ -578,7 +583,7 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
     for (int t = 0; t < kTG; ++t) x[t] = A::ld(src + tso[t] + so);
   };
   // Rows r .. r + n - 1 of a buffer (n = kSD in the main loop, so that its body has no exits).
-  auto consume = [&](int r, const int2 (&e)[kSD], const float (&c)[kSD], int n) {
+  auto consume = [&](int r, const int2 (&e)[kSD], const float (&c)[kSD], const float (&pv)[kSD], int n) {
     float xa[kTG], xb[kTG];
     read(e[0], xa);
 #pragma unroll
@@ -603,11 +608,7 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
         if (BWD) dc = fmaf(x[t], zb[t], dc);
       }
       if (BWD && part) {
-        float* pp = part + (long)(r + i) * 64 + lane;
-        if constexpr (PART_ADD)
-          gstore(pp, gload(pp) + dc);
-        else
-          gstore(pp, dc);
+        gstore(part + (long)(r + i) * 64 + lane, PART_ADD ? pv[i] + dc : dc);
       }
       if (__builtin_amdgcn_readfirstlane(e[i].x) < 0) {   // the slab's last row (same in every lane)
         if (write_dst && d >= 0) {
@@ -623,17 +624,17 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
   };
   // whole pairs of buffers first, then the remaining rows
   const int rend = r0 + (r1 - r0) / (2 * kSD) * (2 * kSD);
-  load(r0, ea, ca);
-  load(r0 + kSD, eb, cb);
+  load(r0, ea, ca, pa);
+  load(r0 + kSD, eb, cb, pb);
   for (int r = r0; r < rend; r += 2 * kSD) {
-    consume(r, ea, ca, kSD);
-    load(r + 2 * kSD, ea, ca);
-    consume(r + kSD, eb, cb, kSD);
-    load(r + 3 * kSD, eb, cb);
+    consume(r, ea, ca, pa, kSD);
+    load(r + 2 * kSD, ea, ca, pa);
+    consume(r + kSD, eb, cb, pb, kSD);
+    load(r + 3 * kSD, eb, cb, pb);
   }
   if (rend < r1) {
-    consume(rend, ea, ca, min(kSD, r1 - rend));
-    if (rend + kSD < r1) consume(rend + kSD, eb, cb, r1 - rend - kSD);
+    consume(rend, ea, ca, pa, min(kSD, r1 - rend));
+    if (rend + kSD < r1) consume(rend + kSD, eb, cb, pb, r1 - rend - kSD);
   }
 }
 
@@ -641,10 +642,10 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
 template <bool BF16, bool BWD>
 __device__ __forceinline__ void stream_all(const GenStream& S, const float* __restrict__ cv,
                                            const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
-                                           int ld_dst, int nt, bool write_dst, float* part) {
+                                           int ld_dst, int nt, bool write_dst, float* part, bool part_add = false) {
   for (int tg = 0; tg < nt; tg += kTG) {
     const int ntg = min(kTG, nt - tg);
-    if (tg == 0) {
+    if (tg == 0 && !part_add) {
       if (ntg <= 2)
         stream_products<BF16, BWD, false, 2>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
       else if (ntg <= 4)
@@ -739,9 +740,12 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   E* ut = reinterpret_cast<E*>(smem);           // tt x ldt_out  u = P_out^T g
   E* zt = ut + (size_t)a.tt * a.ldt_out;        // tt x ldt_in   z = P_in^T x, later q = C^T u
   const int bi = blockIdx.y;
-  const int t0 = blockIdx.x * a.tt;
-  const int nt = min(a.tt, a.T - t0);
-  const E* G = (reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G)) + (long)t0 * a.ldg;
+  const E* G0 = reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G);
+  const E* X0 = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X);
+  E* dX0 = reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX);
+  const float* cv = a.ccopy + bi * a.cstride;
+  // one partial row per workgroup, accumulated over the workgroup's tiles
+  float* part = a.want_dc ? a.partial + ((long)bi * gridDim.x + blockIdx.x) * a.cstride : nullptr;
 
   // twiddle factors of factored frames after the tiles
   float2* tw_in = reinterpret_cast<float2*>(zt + (size_t)a.tt * a.ldt_in);
@@ -750,24 +754,24 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   stage_twiddles(a.fout, tw_out);
   if (a.fin.radix != 1 || a.fout.radix != 1) __syncthreads();
 
-  // q is written over z and then synthesized from whole columns: their padding must be zero
-  zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
-  analysis_to_lds<BF16>(a.fout, tw_out, nt, G, a.ldg, ut, a.ldt_out, a.ldb_out);
-  if (a.want_dc) {
-    const E* X = (reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X)) + (long)t0 * a.ldx;
-    analysis_to_lds<BF16>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
+  for (long tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+    const long t0 = tile * a.tt;
+    const int nt = (int)min((long)a.tt, (long)a.T - t0);
+    if (tile != blockIdx.x) __syncthreads();   // the previous tile's LDS reads are done
+
+    // q is written over z and then synthesized from whole columns: their padding must be zero
+    zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
+    analysis_to_lds<BF16>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
+    if (a.want_dc) analysis_to_lds<BF16>(a.fin, tw_in, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
+    __syncthreads();
+
+    // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
+    stream_all<BF16, true>(a.st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
+    if (!a.want_dx) continue;
+    __syncthreads();
+
+    synthesis_from_lds<BF16>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale, a.beta);
   }
-  __syncthreads();
-
-  // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
-  const float* cv = (a.ccopy + bi * a.cstride);
-  float* part = a.want_dc ? (a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.cstride) : nullptr;
-  stream_all<BF16, true>(a.st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part);
-  if (!a.want_dx) return;
-  __syncthreads();
-
-  E* dX = (reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX)) + (long)t0 * a.lddx;
-  synthesis_from_lds<BF16>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX, a.lddx, a.scale, a.beta);
 }
 
 // out[bi][j] = c_bi[idx[j]] (0 where idx[j] < 0): coefficients in a stream's order.
@@ -1012,10 +1016,11 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.ntiles = ntiles;
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
+  const long nwg = std::min<long>(ntiles, p->gen_wgs);   // partial rows
   if (T > 0 && (want_dx || want_dc)) {
     hipError_t e = launch_gather(c, cs, a.st.coef, (int)a.cstride, count, p->dev.c_bwd, s);
     if (e != hipSuccess) return e;
-    const dim3 grid((unsigned)ntiles, (unsigned)count);
+    const dim3 grid((unsigned)nwg, (unsigned)count);
     record(e0, s);
     if (bf16)
       hipLaunchKernelGGL(bwd_kernel<true>, grid, dim3(kFusedThreads), p->lds_bytes[1], s, a);
@@ -1029,7 +1034,7 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
     const int len = (int)a.cstride, nmain = (len + 63) / 64;
     const int npadb = (p->dev.ncoef_pad + 64 * kDcWaves - 1) / (64 * kDcWaves);
     const dim3 grid((unsigned)(nmain + npadb), (unsigned)count);
-    hipLaunchKernelGGL(dc_reduce, grid, dim3(64 * kDcWaves), 0, s, p->partial, ntiles, len, a.st.coef,
+    hipLaunchKernelGGL(dc_reduce, grid, dim3(64 * kDcWaves), 0, s, p->partial, nwg, len, a.st.coef,
                        p->dev.coef_pad, p->dev.ncoef_pad, scale, accumulate_dc, dC, dCs);
   }
   return hipGetLastError();

@@ -492,7 +492,16 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
 
   // ---------------- device memory: one allocation for every table and the workspace
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t partial_elems = std::max((size_t)max_batch * (size_t)p->max_tiles * gb_elems,
+  // the generic backward runs at most one workgroup per CU and adapter, each accumulating the
+  // dC partial sums of all its tiles in one row
+  {
+    int ncu = 0;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess || ncu < 1)
+      return ff::fail(FF_EDEVICE, "querying the device's compute units failed");
+    p->gen_wgs = ncu;
+  }
+  const size_t gen_rows = (size_t)std::max<int64_t>(1, std::min<int64_t>(p->max_tiles, p->gen_wgs));
+  const size_t partial_elems = std::max((size_t)max_batch * gen_rows * gb_elems,
                                         (size_t)max_batch * (size_t)fast_tiles *
                                             (fast ? ff::fast128_partial_floats(b_st.size()) : 0));
   struct Blob {

@@ -196,6 +196,42 @@ def test_batched_matches_single_calls(dev, dtype):
         assert rel(user_dc(plan, dCd[i]), dc_ref) <= tol
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_generic_backward_many_tiles_per_workgroup(dev, dtype):
+    """The generic backward runs at most one workgroup per CU, looping over tiles: with several
+    tiles per workgroup, a dX-only call (no dC rows to accumulate into), a dC-only call and a
+    call with both match the oracle, and dC is deterministic."""
+    n, rn, m, rm, nnz = 2752, 16, 1024, 16, 3000
+    f_in, f_out = ff.framegen(n, n // rn, rn), ff.framegen(m, m // rm, rm)
+    g = inputs.rng(4242)
+    rows, cols = inputs.support(g, m, n, nnz)
+    probe = ff.plan_create(f_in, f_out, rows, cols, max_tokens=1)
+    tt = probe.tile_tokens(dtype)
+    ncu = torch.cuda.get_device_properties(dev).multi_processor_count
+    T = tt * (2 * ncu + 3) + 1   # two to three tiles per workgroup, a ragged last tile
+    vals = inputs.gaussian(g, (nnz,), std=0.02)
+    X = inputs.gaussian(g, (T, n), dtype=dtype)
+    G = inputs.gaussian(g, (T, m), dtype=dtype)
+    plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T)
+    assert plan.radix == (4, 1) and not plan.fast128
+    Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
+    c = plan_c(plan, vals, dev)
+    s = -0.7
+    dXo, _ = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dc=False)
+    _, dCo = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dx=False)
+    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s)
+    torch.cuda.synchronize()
+    P_in, P_out = oracle_frame(n // rn, rn, n), oracle_frame(m // rm, rm, m)
+    tok = _sample_tokens(T, 64, 11)
+    dx_ref, _ = O.adapter_bwd(P_in, P_out, rows, cols, vals, s, X[tok], G[tok])
+    dc_ref = O.coeff_grad_entries(P_in, P_out, rows, cols, s, X, G)
+    tol = TOL[dtype]
+    assert rel(to_np(dXo[tok]), dx_ref) <= tol
+    assert rel(to_np(dX[tok]), dx_ref) <= tol
+    assert rel(user_dc(plan, dCo), dc_ref) <= tol
+    assert torch.equal(dC, dCo), "dC is not deterministic"
+
+
 def test_empty_batch_is_noop_and_zeroes_dc(dev):
     n = m = 256
     rows, cols, vals, X, G = _problem((n, 16, m, 16, 100, 4), "f32", 1)

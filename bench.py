@@ -73,6 +73,107 @@ def cpu_baseline(wl, ad, data, budget_s=12.0):
             "seconds": round(elapsed, 3)}
 
 
+def bench_stack(args, torch, ff, inputs, dev):
+    """The whole adapter step of a multi-layer workload (the 32-layer x 7-projection Llama-2-7B
+    stack): adapters of one shape share a plan (the support is shared across layers) and run as
+    one batched forward and one batched backward launch per shape.  Activations, upstream
+    gradients and coefficients are seeded device draws (a timing workload; the stack's parity is
+    tested on its first and last layers)."""
+    wl = inputs.WORKLOADS[args.workload]
+    T, L = wl.tokens, wl.layers
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    esz = 2 if wl.dtype == "bf16" else 4
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(wl.seed)
+    shapes = {}
+    for ad in wl.adapters:
+        shapes.setdefault((ad.d_in, ad.d_out, ad.rho_in, ad.rho_out, ad.nnz), []).append(ad)
+    frames, groups = {}, []
+    t0 = time.perf_counter()
+    for gi, ((n, m, rn, rm, nnz), ads) in enumerate(shapes.items()):
+        for d, r in ((n, rn), (m, rm)):
+            if (d, r) not in frames:
+                frames[(d, r)] = ff.framegen(d, d // r, r)
+        rows, cols = inputs.support(inputs.rng(wl.seed + 10 * gi), m, n, nnz)
+        count = L * len(ads)
+        plan = ff.plan_create(frames[(n, rn)], frames[(m, rm)], rows, cols, max_tokens=T, max_batch=count)
+        Xs = [torch.randn((T, n), generator=gen, device=dev).to(tdt) for _ in range(count)]
+        Gs = [torch.randn((T, m), generator=gen, device=dev).to(tdt) for _ in range(count)]
+        order = torch.from_numpy(plan.order).to(dev)
+        cs = []
+        for _ in range(count):
+            v = torch.randn((nnz,), generator=gen, device=dev) * 0.02
+            c = torch.zeros((plan.coef_slots,), device=dev)
+            c[order >= 0] = v[order[order >= 0]]
+            cs.append(c)
+        Ys = [torch.empty((T, m), dtype=tdt, device=dev) for _ in range(count)]
+        dXs = [torch.empty((T, n), dtype=tdt, device=dev) for _ in range(count)]
+        dCs = [torch.empty((plan.coef_slots,), device=dev) for _ in range(count)]
+        pa = ff.binding.pointer_array
+        groups.append(dict(name="+".join(a.name for a in ads), n=n, m=m, nnz=nnz, count=count, plan=plan,
+                           scale=inputs.scale_for(wl, ads[0]), X=Xs, G=Gs, Y=Ys, dX=dXs, dC=dCs, c=cs,
+                           fptr=(pa(Xs, dev), pa(cs, dev), pa(Ys, dev)),
+                           bptr=(pa(Xs, dev), pa(Gs, dev), pa(cs, dev), pa(dXs, dev), pa(dCs, dev))))
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t0
+
+    def step(evs=None):
+        for i, g in enumerate(groups):
+            if evs is not None:
+                ff.binding.time_next_kernel(evs[i][0], evs[i][1])
+            ff.adapter_fwd_batched(g["plan"], g["X"], g["c"], g["scale"], g["Y"], ptrs=g["fptr"])
+            if evs is not None:
+                ff.binding.time_next_kernel(evs[i][2], evs[i][3])
+            ff.adapter_bwd_batched(g["plan"], g["X"], g["G"], g["c"], g["scale"], g["dX"], g["dC"],
+                                   ptrs=g["bptr"])
+
+    for _ in range(args.warmup):
+        step()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3
+    ms_per_step = start.elapsed_time(stop) / args.steps
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in groups] for _ in range(args.steps)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    kernels, step_bytes, dom = {}, 0, None
+    for i, g in enumerate(groups):
+        b_fwd, b_bwd, b_red = algorithmic_bytes(T, g["n"], g["m"], g["nnz"], esz)
+        step_bytes += g["count"] * (b_fwd + b_bwd + b_red)
+        for j, (lab, b) in enumerate((("fwd", b_fwd), ("bwd", b_bwd))):
+            us = 1e3 * float(np.mean([e[i][2 * j].elapsed_time(e[i][2 * j + 1]) for e in evs]))
+            key = f"{lab}_kernel[{g['name']} x{g['count']}]"
+            kernels[key] = round(us, 2)
+            if dom is None or us > dom[1]:
+                dom = (key, us, g["count"] * b)
+    achieved = dom[2] / (dom[1] * 1e-6) / 1e9
+    out = {
+        "metric": METRIC, "value": round(T / (ms_per_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {L} layers x {len(wl.adapters)} projections "
+                               f"({', '.join(a.name for a in wl.adapters)}), {T} tokens, batched fwd+bwd(dX,dC) "
+                               f"per projection shape",
+                   "tokens": T, "adapters": L * len(wl.adapters)},
+        "roofline": {"bound": "hbm", "kernel": dom[0], "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": dom[2], "avg_us": round(dom[1], 3)},
+        "step_roofline": {"bytes_per_step": step_bytes,
+                          "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "kernel_us": kernels},
+        "context": {"setup_s": round(setup_s, 3), "wall_ms_timed": round(wall_ms, 3), "kernel_hash": kernel_hash()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -80,6 +181,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="cfg2_llama7b_qproj")
     ap.add_argument("--adapter", type=int, default=0, help="adapter of a multi-adapter workload (one layer)")
+    ap.add_argument("--stack", action="store_true",
+                    help="time every adapter of every layer of the workload (the 7B stack) as batched calls")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run 3 device-to-device copies of this many MiB (a known-size kernel "
@@ -105,6 +208,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.stack:
+        bench_stack(args, torch, ff, inputs, dev)
+        return
     wl = inputs.WORKLOADS[args.workload]
     ad = wl.adapters[args.adapter]
     data = inputs.adapter_data(wl, ad)

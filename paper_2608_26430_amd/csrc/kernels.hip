@@ -652,6 +652,10 @@ __device__ __forceinline__ void stream_all(const GenStream& S, const float* __re
         stream_products<BF16, BWD, false, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
       else
         stream_products<BF16, BWD, false, kTG>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    } else if (BWD && ntg <= 2) {
+      stream_products<BF16, BWD, true, 2>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    } else if (BWD && ntg <= 4) {
+      stream_products<BF16, BWD, true, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
     } else {
       stream_products<BF16, BWD, true, kTG>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
     }

@@ -310,6 +310,13 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       return ff::fail(FF_EUNSUPPORTED, "one token of %lld + %lld coefficients exceeds LDS", (long long)n,
                       (long long)m);
     tt = std::min<int64_t>(tt, ff::kMaxTileTokens);
+    // The sparse phase walks a tile's tokens 8 at a time (a last pass of 2 or 4 when fewer
+    // remain), reading 8, 4 or 2 token rows per table row; a tile of whole passes wastes none of
+    // those reads: a multiple of 8 tokens, or a power of two below 8.
+    if (tt >= 8)
+      tt -= tt % 8;
+    else
+      while (tt & (tt - 1)) --tt;
     p->tile_tokens[dt] = (int)tt;
     p->lds_bytes[dt] = (size_t)(tt * per_token) + ff::kTwLdsBytes;
     p->max_tiles = std::max<int64_t>(p->max_tiles, (max_tokens + tt - 1) / tt);

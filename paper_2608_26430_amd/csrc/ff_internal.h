@@ -143,8 +143,8 @@ struct ff_plan {
   int ldt_out[2] = {0, 0};
   int tile_tokens[2] = {0, 0};     // tokens per fused-kernel tile
   size_t lds_bytes[2] = {0, 0};
-  int64_t max_tiles = 0;           // tiles of the largest call, per adapter
-  int gen_wgs = 1;                 // workgroups per adapter of the generic backward (one per CU)
+  int gen_wgs = 1;                 // compute units: resident workgroups of the generic kernels
+  int gen_rows = 1;                // dC partial rows per adapter = most workgroups of the generic backward
   float* partial = nullptr;        // dC partial sums per tile (layout depends on the kernels)
   size_t workspace_bytes = 0;
   void* dev_mem = nullptr;

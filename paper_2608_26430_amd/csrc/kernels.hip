@@ -638,27 +638,36 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
   }
 }
 
+// One pass over ntg <= kTG tokens with the walk for exactly that many (a single token takes the
+// 2-token walk): every token row read per table row is used.
+template <bool BF16, bool BWD, bool PART_ADD>
+__device__ __forceinline__ void stream_pass(const GenStream& S, const float* __restrict__ cv,
+                                            const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
+                                            int ld_dst, int tg, int ntg, bool write_dst, float* part) {
+  switch (ntg) {
+    case 1:
+    case 2: stream_products<BF16, BWD, PART_ADD, 2>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    case 3: stream_products<BF16, BWD, PART_ADD, 3>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    case 4: stream_products<BF16, BWD, PART_ADD, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    case 5: stream_products<BF16, BWD, PART_ADD, 5>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    case 6: stream_products<BF16, BWD, PART_ADD, 6>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    case 7: stream_products<BF16, BWD, PART_ADD, 7>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    default: stream_products<BF16, BWD, PART_ADD, kTG>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+  }
+}
+
 // All tokens of a tile, kTG at a time, each pass reading only as many token rows as it needs.
+// Backward passes after the first of a workgroup add to its dC partial row (PART_ADD).
 template <bool BF16, bool BWD>
 __device__ __forceinline__ void stream_all(const GenStream& S, const float* __restrict__ cv,
                                            const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
                                            int ld_dst, int nt, bool write_dst, float* part, bool part_add = false) {
   for (int tg = 0; tg < nt; tg += kTG) {
     const int ntg = min(kTG, nt - tg);
-    if (tg == 0 && !part_add) {
-      if (ntg <= 2)
-        stream_products<BF16, BWD, false, 2>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-      else if (ntg <= 4)
-        stream_products<BF16, BWD, false, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-      else
-        stream_products<BF16, BWD, false, kTG>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    } else if (BWD && ntg <= 2) {
-      stream_products<BF16, BWD, true, 2>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    } else if (BWD && ntg <= 4) {
-      stream_products<BF16, BWD, true, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    } else {
-      stream_products<BF16, BWD, true, kTG>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    }
+    if (!BWD || (tg == 0 && !part_add))
+      stream_pass<BF16, BWD, false>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    else
+      stream_pass<BF16, BWD, true>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
   }
 }
 
@@ -941,6 +950,27 @@ hipError_t launch_gather(const float* c, const float* const* cs, const int* idx,
   return hipGetLastError();
 }
 
+// Tokens per tile for a call of T tokens on `count` adapters.  The generic kernels run one
+// workgroup per CU, so tiles go in rounds of `slots` and a call costs about rounds x (token rows
+// its sparse walks read per table row + a fixed part worth kTileOverhead of them).  Of the tile
+// sizes up to tt (the plan's LDS limit) the cheapest is taken, the larger one on ties (fewer
+// passes over the tables).
+constexpr int kTileOverhead = 2;
+
+int call_tile_tokens(int tt, long T, int count, int slots) {
+  if (T <= 0 || slots < 1) return tt;
+  int best = tt;
+  long best_cost = -1;
+  for (int t = tt; t >= 1; --t) {
+    const long tiles = (T + t - 1) / t * count;
+    const long rounds = (tiles + slots - 1) / slots;
+    const int rem = t % kTG, walk = t - rem + (rem ? std::max(rem, 2) : 0);
+    const long cost = rounds * (walk + kTileOverhead);
+    if (best_cost < 0 || cost < best_cost) best = t, best_cost = cost;
+  }
+  return best;
+}
+
 hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx, const float* c,
                       const float* const* cs, float scale, float beta, ActPtrs Y, int64_t ldy, float* c_saved,
                       hipStream_t s) {
@@ -949,7 +979,7 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
   a.T = T;
-  a.tt = p->tile_tokens[bf16];
+  a.tt = call_tile_tokens(p->tile_tokens[bf16], T, count, p->gen_wgs);
   a.ldt_in = p->ldt_in[bf16];
   a.ldt_out = p->ldt_out[bf16];
   a.ldb_in = p->ldb_in;
@@ -994,7 +1024,7 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
   a.T = T;
-  a.tt = p->tile_tokens[bf16];
+  a.tt = call_tile_tokens(p->tile_tokens[bf16], T, count, p->gen_wgs);
   a.ldt_in = p->ldt_in[bf16];
   a.ldt_out = p->ldt_out[bf16];
   a.ldb_in = p->ldb_in;
@@ -1020,7 +1050,7 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.ntiles = ntiles;
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
-  const long nwg = std::min<long>(ntiles, p->gen_wgs);   // partial rows
+  const long nwg = std::min<long>(ntiles, p->gen_rows);   // partial rows
   if (T > 0 && (want_dx || want_dc)) {
     hipError_t e = launch_gather(c, cs, a.st.coef, (int)a.cstride, count, p->dev.c_bwd, s);
     if (e != hipSuccess) return e;

@@ -310,16 +310,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       return ff::fail(FF_EUNSUPPORTED, "one token of %lld + %lld coefficients exceeds LDS", (long long)n,
                       (long long)m);
     tt = std::min<int64_t>(tt, ff::kMaxTileTokens);
-    // The sparse phase walks a tile's tokens 8 at a time (a last pass of 2 or 4 when fewer
-    // remain), reading 8, 4 or 2 token rows per table row; a tile of whole passes wastes none of
-    // those reads: a multiple of 8 tokens, or a power of two below 8.
-    if (tt >= 8)
-      tt -= tt % 8;
-    else
-      while (tt & (tt - 1)) --tt;
     p->tile_tokens[dt] = (int)tt;
     p->lds_bytes[dt] = (size_t)(tt * per_token) + ff::kTwLdsBytes;
-    p->max_tiles = std::max<int64_t>(p->max_tiles, (max_tokens + tt - 1) / tt);
   }
 
   // ---------------- host tables
@@ -507,8 +499,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       return ff::fail(FF_EDEVICE, "querying the device's compute units failed");
     p->gen_wgs = ncu;
   }
-  const size_t gen_rows = (size_t)std::max<int64_t>(1, std::min<int64_t>(p->max_tiles, p->gen_wgs));
-  const size_t partial_elems = std::max((size_t)max_batch * gen_rows * gb_elems,
+  // (a call may use tiles of fewer tokens than the LDS allows, so up to one tile per token)
+  p->gen_rows = (int)std::max<int64_t>(1, std::min<int64_t>(max_tokens, p->gen_wgs));
+  const size_t partial_elems = std::max((size_t)max_batch * (size_t)p->gen_rows * gb_elems,
                                         (size_t)max_batch * (size_t)fast_tiles *
                                             (fast ? ff::fast128_partial_floats(b_st.size()) : 0));
   struct Blob {

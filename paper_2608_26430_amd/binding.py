@@ -197,6 +197,15 @@ class Plan:
         """(input, output) frame application: 4 for the factored radix-4 form, 1 for dense blocks."""
         return self.query(8), self.query(9)
 
+    @property
+    def gen_bwd_chunks(self) -> int:
+        """Input-side chunks of a generic backward tile (1: the whole input side at once)."""
+        return self.query(10)
+
+    def gen_bwd_tile_tokens(self, dtype: str) -> int:
+        """Most tokens per generic backward tile."""
+        return self.query(12 if dtype == "bf16" else 11)
+
     def new_saved(self, device=None):
         """A c_saved array for one adapter of this plan (None when the plan needs none)."""
         torch = _torch()

@@ -741,17 +741,21 @@ struct BwdArgs {
   float scale, beta;
   int want_dx, want_dc;
   GenStream st;
-  float* partial;       // dC partial sums [batch][tile][cstride]
+  float* partial;       // dC partial sums [batch][workgroup][cstride]
   long ntiles;
+  int nch;              // input-side chunks: blocks chunk_blk[i] .. chunk_blk[i + 1] - 1
+  int chunk_blk[kMaxBwdChunks + 1];
 };
 
-template <bool BF16>
+// CHUNKED: the input side in a.nch chunks of blocks; otherwise whole (a.nch == 1), in code of
+// its own (the chunk loop costs registers that the whole-side kernel then spills).
+template <bool BF16, bool CHUNKED>
 __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   using A = Act<BF16>;
   using E = typename A::E;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   E* ut = reinterpret_cast<E*>(smem);           // tt x ldt_out  u = P_out^T g
-  E* zt = ut + (size_t)a.tt * a.ldt_out;        // tt x ldt_in   z = P_in^T x, later q = C^T u
+  E* zt = ut + (size_t)a.tt * a.ldt_out;        // tt x ldt_in   z = P_in^T x of one chunk, later q = C^T u
   const int bi = blockIdx.y;
   const E* G0 = reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G);
   const E* X0 = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X);
@@ -772,18 +776,45 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
     const int nt = (int)min((long)a.tt, (long)a.T - t0);
     if (tile != blockIdx.x) __syncthreads();   // the previous tile's LDS reads are done
 
-    // q is written over z and then synthesized from whole columns: their padding must be zero
-    zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
+    if constexpr (!CHUNKED) {
+      // q is written over z and then synthesized from whole columns: their padding must be zero
+      zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
+      analysis_to_lds<BF16>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
+      if (a.want_dc) analysis_to_lds<BF16>(a.fin, tw_in, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
+      __syncthreads();
+
+      // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
+      stream_all<BF16, true>(a.st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
+      if (!a.want_dx) continue;
+      __syncthreads();
+
+      synthesis_from_lds<BF16>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale,
+                               a.beta);
+      continue;
+    }
     analysis_to_lds<BF16>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
-    if (a.want_dc) analysis_to_lds<BF16>(a.fin, tw_in, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
-    __syncthreads();
+    for (int ch = 0; ch < a.nch; ++ch) {
+      // the chunk's blocks as a frame of their own, at column b0 W of the token rows
+      const int b0 = a.chunk_blk[ch];
+      FrameDev fc = a.fin;
+      fc.nblk = a.chunk_blk[ch + 1] - b0;
+      const long col0 = (long)b0 * a.fin.W;
+      if (ch > 0) __syncthreads();   // the previous chunk is done with the z / q tile
+      // q is written over z and then synthesized from whole columns: their padding must be zero
+      zero_column_pads<BF16>(fc, nt, zt, a.ldt_in, a.ldb_in);
+      if (a.want_dc) analysis_to_lds<BF16>(fc, tw_in, nt, X0 + t0 * a.ldx + col0, a.ldx, zt, a.ldt_in, a.ldb_in);
+      __syncthreads();
 
-    // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
-    stream_all<BF16, true>(a.st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
-    if (!a.want_dx) continue;
-    __syncthreads();
+      // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
+      GenStream sc = a.st;
+      sc.wave_row += ch * (kGenWaves + 1);
+      stream_all<BF16, true>(sc, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
+      if (!a.want_dx) continue;
+      __syncthreads();
 
-    synthesis_from_lds<BF16>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale, a.beta);
+      synthesis_from_lds<BF16>(fc, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx + col0, a.lddx, a.scale,
+                               a.beta);
+    }
   }
 }
 
@@ -933,8 +964,10 @@ hipError_t configure_kernels() {
     };
     set(reinterpret_cast<const void*>(&fwd_kernel<true>));
     set(reinterpret_cast<const void*>(&fwd_kernel<false>));
-    set(reinterpret_cast<const void*>(&bwd_kernel<true>));
-    set(reinterpret_cast<const void*>(&bwd_kernel<false>));
+    set(reinterpret_cast<const void*>(&bwd_kernel<true, false>));
+    set(reinterpret_cast<const void*>(&bwd_kernel<false, false>));
+    set(reinterpret_cast<const void*>(&bwd_kernel<true, true>));
+    set(reinterpret_cast<const void*>(&bwd_kernel<false, true>));
     set(reinterpret_cast<const void*>(&merge_kernel<true>));
     set(reinterpret_cast<const void*>(&merge_kernel<false>));
     return e;
@@ -1024,11 +1057,13 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
   a.T = T;
-  a.tt = call_tile_tokens(p->tile_tokens[bf16], T, count, p->gen_wgs);
-  a.ldt_in = p->ldt_in[bf16];
+  a.tt = call_tile_tokens(p->bwd_tile_tokens[bf16], T, count, p->gen_wgs);
+  a.ldt_in = p->bwd_ldt_in[bf16];
   a.ldt_out = p->ldt_out[bf16];
   a.ldb_in = p->ldb_in;
   a.ldb_out = p->ldb_out;
+  a.nch = p->bwd_nch;
+  for (int i = 0; i <= p->bwd_nch; ++i) a.chunk_blk[i] = p->bwd_chunk_blk[i];
   a.X = X.one;
   a.Xs = X.many;
   a.ldx = (long)ldx;
@@ -1056,10 +1091,18 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)nwg, (unsigned)count);
     record(e0, s);
-    if (bf16)
-      hipLaunchKernelGGL(bwd_kernel<true>, grid, dim3(kFusedThreads), p->lds_bytes[1], s, a);
-    else
-      hipLaunchKernelGGL(bwd_kernel<false>, grid, dim3(kFusedThreads), p->lds_bytes[0], s, a);
+    const size_t lds = p->bwd_lds_bytes[bf16];
+    if (a.nch > 1) {
+      if (bf16)
+        hipLaunchKernelGGL((bwd_kernel<true, true>), grid, dim3(kFusedThreads), lds, s, a);
+      else
+        hipLaunchKernelGGL((bwd_kernel<false, true>), grid, dim3(kFusedThreads), lds, s, a);
+    } else {
+      if (bf16)
+        hipLaunchKernelGGL((bwd_kernel<true, false>), grid, dim3(kFusedThreads), lds, s, a);
+      else
+        hipLaunchKernelGGL((bwd_kernel<false, false>), grid, dim3(kFusedThreads), lds, s, a);
+    }
     record(e1, s);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -232,6 +232,47 @@ def test_generic_backward_many_tiles_per_workgroup(dev, dtype):
     assert torch.equal(dC, dCo), "dC is not deterministic"
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_generic_backward_input_chunks(dev, dtype):
+    """An input side too wide to sit whole next to u for 8 tokens (factored 256-wide blocks) and
+    a dense enough support (nnz >= 4 (n + m)): the generic backward takes the input side a chunk
+    of blocks at a time.  With several tiles per workgroup, a dX-only call, a dC-only call and a
+    call with both match the oracle, dC is deterministic, and beta accumulates into dX."""
+    n, rn, m, rm, nnz = 8192, 64, 2048, 64, 42000
+    f_in, f_out = ff.framegen(n, n // rn, rn), ff.framegen(m, m // rm, rm)
+    g = inputs.rng(5151)
+    rows, cols = inputs.support(g, m, n, nnz)
+    probe = ff.plan_create(f_in, f_out, rows, cols, max_tokens=1)
+    assert probe.gen_bwd_chunks > 1 and probe.radix == (4, 1) and not probe.fast128
+    tt = probe.gen_bwd_tile_tokens(dtype)
+    assert tt > probe.tile_tokens(dtype)
+    ncu = torch.cuda.get_device_properties(dev).multi_processor_count
+    T = tt * (ncu + 2) + 1   # more tiles than workgroups, a ragged last tile
+    vals = inputs.gaussian(g, (nnz,), std=0.02)
+    X = inputs.gaussian(g, (T, n), dtype=dtype)
+    G = inputs.gaussian(g, (T, m), dtype=dtype)
+    plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T)
+    Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
+    c = plan_c(plan, vals, dev)
+    s = 0.9
+    dXo, _ = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dc=False)
+    _, dCo = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dx=False)
+    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s)
+    dX2 = dX.clone()
+    ff.adapter_bwd(plan, Xd, Gd, c, s, dX=dX2, beta_dx=1.0, want_dc=False)
+    torch.cuda.synchronize()
+    P_in, P_out = oracle_frame(n // rn, rn, n), oracle_frame(m // rm, rm, m)
+    tok = _sample_tokens(T, 48, 12)
+    dx_ref, _ = O.adapter_bwd(P_in, P_out, rows, cols, vals, s, X[tok], G[tok])
+    dc_ref = O.coeff_grad_entries(P_in, P_out, rows, cols, s, X, G)
+    tol = TOL[dtype]
+    assert rel(to_np(dXo[tok]), dx_ref) <= tol
+    assert rel(to_np(dX[tok]), dx_ref) <= tol
+    assert rel(to_np(dX2[tok]), 2.0 * dx_ref) <= tol
+    assert rel(user_dc(plan, dCo), dc_ref) <= tol
+    assert torch.equal(dC, dCo), "dC is not deterministic"
+
+
 def test_empty_batch_is_noop_and_zeroes_dc(dev):
     n = m = 256
     rows, cols, vals, X, G = _problem((n, 16, m, 16, 100, 4), "f32", 1)
@@ -278,7 +319,7 @@ def _sample_tokens(T, k, seed):
     return np.unique(np.concatenate([[0, 1, T // 2, T - 1], extra]))
 
 
-def _full_size_check(dev, wl_name, adapter_index=0, n_tok=48, n_nnz=384, n_rows=6):
+def _full_size_check(dev, wl_name, adapter_index=0, n_tok=48, n_nnz=384, n_rows=6, bwd_chunked=None):
     wl = inputs.WORKLOADS[wl_name]
     ad = wl.adapters[adapter_index]
     data = inputs.adapter_data(wl, ad, seed=wl.seed + adapter_index)
@@ -288,6 +329,8 @@ def _full_size_check(dev, wl_name, adapter_index=0, n_tok=48, n_nnz=384, n_rows=
     f_in = ff.framegen(ad.d_in, ad.k_in, ad.rho_in)
     f_out = ff.framegen(ad.d_out, ad.k_out, ad.rho_out)
     plan = ff.plan_create(f_in, f_out, data.rows, data.cols, max_tokens=T)
+    if bwd_chunked is not None:
+        assert (plan.gen_bwd_chunks > 1) == bwd_chunked
     Xd, Gd = torch_act(data.X, dtype, dev), torch_act(data.G, dtype, dev)
     c = plan_c(plan, data.vals, dev)
     Y = ff.adapter_fwd(plan, Xd, c, data.scale)
@@ -330,11 +373,11 @@ def test_cfg3_llama7b_mlp_up_full(dev):
 
 
 def test_cfg3_llama7b_mlp_down_full(dev):
-    _full_size_check(dev, "cfg3_llama7b_mlp", adapter_index=1, n_tok=24, n_nnz=256, n_rows=4)
+    _full_size_check(dev, "cfg3_llama7b_mlp", adapter_index=1, n_tok=24, n_nnz=256, n_rows=4, bwd_chunked=False)
 
 
 def test_cfg5_llama70b_down_full(dev):
-    _full_size_check(dev, "cfg5_llama70b_down", n_tok=12, n_nnz=192, n_rows=3)
+    _full_size_check(dev, "cfg5_llama70b_down", n_tok=12, n_nnz=192, n_rows=3, bwd_chunked=True)
 
 
 def test_cfg5_vitb16_qkv_full(dev):

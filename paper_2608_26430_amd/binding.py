@@ -198,12 +198,12 @@ class Plan:
         return self.query(8), self.query(9)
 
     @property
-    def gen_bwd_chunks(self) -> int:
-        """Input-side chunks of a generic backward tile (1: the whole input side at once)."""
+    def gen_chunks(self) -> int:
+        """Input-side chunks of a generic-kernel tile (1: the whole input side at once)."""
         return self.query(10)
 
-    def gen_bwd_tile_tokens(self, dtype: str) -> int:
-        """Most tokens per generic backward tile."""
+    def gen_tile_tokens(self, dtype: str) -> int:
+        """Most tokens per generic-kernel tile with those chunks."""
         return self.query(12 if dtype == "bf16" else 11)
 
     def new_saved(self, device=None):

@@ -23,8 +23,8 @@ constexpr int kMaxLdsBytes = 160 * 1024;
 constexpr int kTwLdsBytes = 3072;
 // Upper bound on tokens per workgroup tile.
 constexpr int kMaxTileTokens = 64;
-// Most input-side chunks of a generic backward tile.
-constexpr int kMaxBwdChunks = 64;
+// Most input-side chunks of a generic-kernel tile.
+constexpr int kMaxGenChunks = 64;
 // Threads per workgroup of the fused forward / backward kernels.
 constexpr int kFusedThreads = 512;
 
@@ -76,8 +76,8 @@ struct GenStream {
   const int2* ent;        // (LDS element offset of the source coefficient within a token row
                           //  | kRowLast, LDS element offset of the lane's destination or -1)
   const int* coef;        // coefficient slot of the entry, -1 for padding
-  const int* wave_row;    // [kGenWaves + 1]: first stream row of each wave (the backward stream:
-                          // [chunks][kGenWaves + 1], one stream per input-side chunk)
+  const int* wave_row;    // [chunks][kGenWaves + 1]: first stream row of each wave, one stream per
+                          // input-side chunk
   int rows;               // stream rows; entries = 64 * rows
 };
 
@@ -146,13 +146,14 @@ struct ff_plan {
   int ldt_out[2] = {0, 0};
   int tile_tokens[2] = {0, 0};     // tokens per fused-kernel tile
   size_t lds_bytes[2] = {0, 0};
-  // Generic backward tiles: u (output side) whole and z / q (input side) one chunk of input
-  // blocks at a time, chunk i = blocks bwd_chunk_blk[i] .. bwd_chunk_blk[i + 1] - 1.
-  int bwd_nch = 1;
-  int bwd_chunk_blk[ff::kMaxBwdChunks + 1] = {};
-  int bwd_ldt_in[2] = {0, 0};      // LDS token stride of the input-side chunk tile
-  int bwd_tile_tokens[2] = {0, 0};
-  size_t bwd_lds_bytes[2] = {0, 0};
+  // Generic-kernel tiles with the input side in chunks: the output side (v, u) whole and z / q
+  // one chunk of input blocks at a time, chunk i = blocks gen_chunk_blk[i] .. gen_chunk_blk[i + 1] - 1
+  // (one chunk: the whole-side geometry above).
+  int gen_nch = 1;
+  int gen_chunk_blk[ff::kMaxGenChunks + 1] = {};
+  int gen_ldt_in[2] = {0, 0};      // LDS token stride of the input-side chunk tile
+  int gen_tile_tokens[2] = {0, 0};
+  size_t gen_lds_bytes[2] = {0, 0};
   int gen_wgs = 1;                 // compute units: resident workgroups of the generic kernels
   int gen_rows = 1;                // dC partial rows per adapter = most workgroups of the generic backward
   float* partial = nullptr;        // dC partial sums per tile (layout depends on the kernels)

@@ -614,7 +614,11 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
         if (write_dst && d >= 0) {
 #pragma unroll
           for (int t = 0; t < kTG; ++t)
-            if (t < ntg) A::st(dst + t * ld_dst + d, acc[t]);
+            if (t < ntg) {
+              float v = acc[t];
+              if constexpr (!BWD && PART_ADD) v += A::ld(dst + t * ld_dst + d);   // a later input chunk
+              A::st(dst + t * ld_dst + d, v);
+            }
         }
 #pragma unroll
         for (int t = 0; t < kTG; ++t) acc[t] = 0.f;
@@ -657,17 +661,18 @@ __device__ __forceinline__ void stream_pass(const GenStream& S, const float* __r
 }
 
 // All tokens of a tile, kTG at a time, each pass reading only as many token rows as it needs.
-// Backward passes after the first of a workgroup add to its dC partial row (PART_ADD).
-template <bool BF16, bool BWD>
+// `add` (MAY_ADD only): backward, add to the dC partial row (as do the tile's later passes);
+// forward, add the sums to the destination (the input side's later chunks).
+template <bool BF16, bool BWD, bool MAY_ADD = BWD>
 __device__ __forceinline__ void stream_all(const GenStream& S, const float* __restrict__ cv,
                                            const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
-                                           int ld_dst, int nt, bool write_dst, float* part, bool part_add = false) {
+                                           int ld_dst, int nt, bool write_dst, float* part, bool add = false) {
   for (int tg = 0; tg < nt; tg += kTG) {
     const int ntg = min(kTG, nt - tg);
-    if (!BWD || (tg == 0 && !part_add))
-      stream_pass<BF16, BWD, false>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    if (MAY_ADD && (add || (BWD && tg > 0)))
+      stream_pass<BF16, BWD, MAY_ADD>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
     else
-      stream_pass<BF16, BWD, true>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+      stream_pass<BF16, BWD, false>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
   }
 }
 
@@ -686,14 +691,18 @@ struct FwdArgs {
   long cstride;
   float scale, beta;
   GenStream st;
+  int nch;              // input-side chunks: blocks chunk_blk[i] .. chunk_blk[i + 1] - 1
+  int chunk_blk[kMaxGenChunks + 1];
 };
 
-template <bool BF16>
+// CHUNKED: the input side in a.nch chunks of blocks, v accumulated over them; otherwise whole
+// (a.nch == 1), in code of its own.
+template <bool BF16, bool CHUNKED>
 __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   using A = Act<BF16>;
   using E = typename A::E;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  E* zt = reinterpret_cast<E*>(smem);           // tt x ldt_in   z = P_in^T x
+  E* zt = reinterpret_cast<E*>(smem);           // tt x ldt_in   z = P_in^T x (of one chunk)
   E* vt = zt + (size_t)a.tt * a.ldt_in;         // tt x ldt_out  v = C z
   const int bi = blockIdx.y;
   const E* X = (reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X));
@@ -711,13 +720,30 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   stage_twiddles(a.fout, tw_out);
   if (a.fin.radix != 1 || a.fout.radix != 1) __syncthreads();
 
-  // analysis: z = P_in^T x for every (token, input block)
   zero_column_pads<BF16>(a.fout, nt, vt, a.ldt_out, a.ldb_out);
-  analysis_to_lds<BF16>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
-  __syncthreads();
+  if constexpr (!CHUNKED) {
+    // analysis: z = P_in^T x for every (token, input block)
+    analysis_to_lds<BF16>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
+    __syncthreads();
 
-  // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
-  stream_all<BF16, false>(a.st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
+    // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
+    stream_all<BF16, false>(a.st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
+  } else {
+    for (int ch = 0; ch < a.nch; ++ch) {
+      // the chunk's blocks as a frame of their own, at column b0 W of the token rows
+      const int b0 = a.chunk_blk[ch];
+      FrameDev fc = a.fin;
+      fc.nblk = a.chunk_blk[ch + 1] - b0;
+      if (ch > 0) __syncthreads();   // the previous chunk's products are done reading z
+      analysis_to_lds<BF16>(fc, tw_in, nt, X + (long)b0 * a.fin.W, a.ldx, zt, a.ldt_in, a.ldb_in);
+      __syncthreads();
+
+      // v[a] (+)= sum over the chunk's entries of row a of c_e z[b_e]
+      GenStream sc = a.st;
+      sc.wave_row += ch * (kGenWaves + 1);
+      stream_all<BF16, false, true>(sc, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr, ch > 0);
+    }
+  }
   __syncthreads();
 
   // synthesis and epilogue: y = beta y + s P_out v
@@ -744,7 +770,7 @@ struct BwdArgs {
   float* partial;       // dC partial sums [batch][workgroup][cstride]
   long ntiles;
   int nch;              // input-side chunks: blocks chunk_blk[i] .. chunk_blk[i + 1] - 1
-  int chunk_blk[kMaxBwdChunks + 1];
+  int chunk_blk[kMaxGenChunks + 1];
 };
 
 // CHUNKED: the input side in a.nch chunks of blocks; otherwise whole (a.nch == 1), in code of
@@ -962,8 +988,10 @@ hipError_t configure_kernels() {
       hipError_t r = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
       if (r != hipSuccess) e = r;
     };
-    set(reinterpret_cast<const void*>(&fwd_kernel<true>));
-    set(reinterpret_cast<const void*>(&fwd_kernel<false>));
+    set(reinterpret_cast<const void*>(&fwd_kernel<true, false>));
+    set(reinterpret_cast<const void*>(&fwd_kernel<false, false>));
+    set(reinterpret_cast<const void*>(&fwd_kernel<true, true>));
+    set(reinterpret_cast<const void*>(&fwd_kernel<false, true>));
     set(reinterpret_cast<const void*>(&bwd_kernel<true, false>));
     set(reinterpret_cast<const void*>(&bwd_kernel<false, false>));
     set(reinterpret_cast<const void*>(&bwd_kernel<true, true>));
@@ -1012,9 +1040,11 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
   a.T = T;
-  a.tt = call_tile_tokens(p->tile_tokens[bf16], T, count, p->gen_wgs);
-  a.ldt_in = p->ldt_in[bf16];
+  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, count, p->gen_wgs);
+  a.ldt_in = p->gen_ldt_in[bf16];
   a.ldt_out = p->ldt_out[bf16];
+  a.nch = p->gen_nch;
+  for (int i = 0; i <= p->gen_nch; ++i) a.chunk_blk[i] = p->gen_chunk_blk[i];
   a.ldb_in = p->ldb_in;
   a.ldb_out = p->ldb_out;
   a.X = X.one;
@@ -1038,10 +1068,18 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
   record(e0, s);
-  if (bf16)
-    hipLaunchKernelGGL(fwd_kernel<true>, grid, dim3(kFusedThreads), p->lds_bytes[1], s, a);
-  else
-    hipLaunchKernelGGL(fwd_kernel<false>, grid, dim3(kFusedThreads), p->lds_bytes[0], s, a);
+  const size_t lds = p->gen_lds_bytes[bf16];
+  if (a.nch > 1) {
+    if (bf16)
+      hipLaunchKernelGGL((fwd_kernel<true, true>), grid, dim3(kFusedThreads), lds, s, a);
+    else
+      hipLaunchKernelGGL((fwd_kernel<false, true>), grid, dim3(kFusedThreads), lds, s, a);
+  } else {
+    if (bf16)
+      hipLaunchKernelGGL((fwd_kernel<true, false>), grid, dim3(kFusedThreads), lds, s, a);
+    else
+      hipLaunchKernelGGL((fwd_kernel<false, false>), grid, dim3(kFusedThreads), lds, s, a);
+  }
   record(e1, s);
   return hipGetLastError();
 }
@@ -1057,13 +1095,13 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
   a.T = T;
-  a.tt = call_tile_tokens(p->bwd_tile_tokens[bf16], T, count, p->gen_wgs);
-  a.ldt_in = p->bwd_ldt_in[bf16];
+  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, count, p->gen_wgs);
+  a.ldt_in = p->gen_ldt_in[bf16];
   a.ldt_out = p->ldt_out[bf16];
   a.ldb_in = p->ldb_in;
   a.ldb_out = p->ldb_out;
-  a.nch = p->bwd_nch;
-  for (int i = 0; i <= p->bwd_nch; ++i) a.chunk_blk[i] = p->bwd_chunk_blk[i];
+  a.nch = p->gen_nch;
+  for (int i = 0; i <= p->gen_nch; ++i) a.chunk_blk[i] = p->gen_chunk_blk[i];
   a.X = X.one;
   a.Xs = X.many;
   a.ldx = (long)ldx;
@@ -1091,7 +1129,7 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)nwg, (unsigned)count);
     record(e0, s);
-    const size_t lds = p->bwd_lds_bytes[bf16];
+    const size_t lds = p->gen_lds_bytes[bf16];
     if (a.nch > 1) {
       if (bf16)
         hipLaunchKernelGGL((bwd_kernel<true, true>), grid, dim3(kFusedThreads), lds, s, a);

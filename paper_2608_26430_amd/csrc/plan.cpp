@@ -259,6 +259,14 @@ StreamHost build_stream(const std::vector<std::vector<int>>& lists, Src src, Dst
   return h;
 }
 
+// Chunk streams are concatenated; each keeps its own wave runs (rows offset by those before).
+void append_stream(StreamHost& all, const StreamHost& h) {
+  for (int w = 0; w <= ff::kGenWaves; ++w) all.wave_row.push_back((int)(all.rows + h.wave_row[w]));
+  all.ent.insert(all.ent.end(), h.ent.begin(), h.ent.end());
+  all.id.insert(all.id.end(), h.id.begin(), h.id.end());
+  all.rows += h.rows;
+}
+
 extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out, int64_t nnz,
                                     const int32_t* rows, const int32_t* cols, int64_t max_tokens,
                                     int64_t max_batch, ff_plan** out) {
@@ -313,35 +321,36 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     p->tile_tokens[dt] = (int)tt;
     p->lds_bytes[dt] = (size_t)(tt * per_token) + ff::kTwLdsBytes;
   }
-  // Generic backward: u is needed whole, but z / q only one input-side chunk at a time, so
-  // chunking lets a tile hold more tokens (fewer passes over the stream tables and fewer dC
-  // partial-row updates per token, at the price of a barrier-separated phase sequence per
-  // chunk).  It pays where the stream dominates, nnz >= 4 (n + m) (measured: the 70B down
-  // projection's backward 25% faster; the 7B MLP down projection's about even at 50k
-  // coefficients and 9% slower at 10k).  The chunk count is the smallest one that reaches min(8, twice the
-  // whole-tile count) tokens in bf16 (the same chunks serve fp32), else 1.
-  auto bwd_tokens = [&](int nch, int dt) -> int64_t {
+  // Generic kernels: the output side (v in the forward, u in the backward) is needed whole, but
+  // the input side (z, q) only one chunk of input blocks at a time, so chunking lets a tile hold
+  // more tokens (fewer passes over the stream tables and, backward, fewer dC partial-row updates
+  // per token, at the price of a barrier-separated phase sequence per chunk).  It pays where the
+  // stream dominates, nnz >= 4 (n + m) (measured on the backward: the 70B down projection 25%
+  // faster; the 7B MLP down projection about even at 50k coefficients and 9% slower at 10k).
+  // The chunk count is the smallest one that reaches min(8, twice the whole-tile count) tokens
+  // in bf16 (the same chunks serve fp32), else 1.
+  auto chunk_tokens = [&](int nch, int dt) -> int64_t {
     const int esz = dt == FF_BF16 ? 2 : 4;
     const int ldc = token_stride((FI.nblk + nch - 1) / nch, p->ldb_in, esz);
     const int64_t tt = (ff::kMaxLdsBytes - ff::kTwLdsBytes) / ((int64_t)(p->ldt_out[dt] + ldc) * esz);
     return std::min<int64_t>(tt, ff::kMaxTileTokens);
   };
   {
-    const int64_t whole = bwd_tokens(1, FF_BF16), want = std::min<int64_t>(8, 2 * whole);
+    const int64_t whole = chunk_tokens(1, FF_BF16), want = std::min<int64_t>(8, 2 * whole);
     int nch = 1;
     const bool dense_stream = nnz >= 4 * (n + m);
-    for (int c = 2; dense_stream && whole < want && c <= std::min(FI.nblk, ff::kMaxBwdChunks); ++c)
-      if (bwd_tokens(c, FF_BF16) >= want) {
+    for (int c = 2; dense_stream && whole < want && c <= std::min(FI.nblk, ff::kMaxGenChunks); ++c)
+      if (chunk_tokens(c, FF_BF16) >= want) {
         nch = c;
         break;
       }
-    p->bwd_nch = nch;
-    for (int c = 0; c <= nch; ++c) p->bwd_chunk_blk[c] = (int)((int64_t)c * FI.nblk / nch);
+    p->gen_nch = nch;
+    for (int c = 0; c <= nch; ++c) p->gen_chunk_blk[c] = (int)((int64_t)c * FI.nblk / nch);
     for (int dt = 0; dt < 2; ++dt) {
       const int esz = dt == FF_BF16 ? 2 : 4;
-      p->bwd_ldt_in[dt] = token_stride((FI.nblk + nch - 1) / nch, p->ldb_in, esz);
-      p->bwd_tile_tokens[dt] = (int)bwd_tokens(nch, dt);
-      p->bwd_lds_bytes[dt] = (size_t)p->bwd_tile_tokens[dt] * (size_t)(p->ldt_out[dt] + p->bwd_ldt_in[dt]) * esz +
+      p->gen_ldt_in[dt] = token_stride((FI.nblk + nch - 1) / nch, p->ldb_in, esz);
+      p->gen_tile_tokens[dt] = (int)chunk_tokens(nch, dt);
+      p->gen_lds_bytes[dt] = (size_t)p->gen_tile_tokens[dt] * (size_t)(p->ldt_out[dt] + p->gen_ldt_in[dt]) * esz +
                              ff::kTwLdsBytes;
     }
   }
@@ -367,13 +376,25 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     for (int64_t e : byc) by_row[rows[e]].push_back((int)e);
     for (int64_t e : byr) by_col[cols[e]].push_back((int)e);
   }
-  const StreamHost gfwd = build_stream(
-      by_row, [&](int e) { return off_in(cloc[e]); }, [&](int64_t r) { return off_out(locate(r, f_out->rho)); });
+  // the forward stream: one stream per input-side chunk over every row of C (the row's entries
+  // in that chunk; sources relative to the chunk's first block), concatenated
+  StreamHost gfwd;
+  for (int ch = 0; ch < p->gen_nch; ++ch) {
+    const int b0 = p->gen_chunk_blk[ch], b1 = p->gen_chunk_blk[ch + 1];
+    std::vector<std::vector<int>> lists((size_t)m);
+    for (int64_t r = 0; r < m; ++r)
+      for (int e : by_row[r])
+        if (cloc[e].blk >= b0 && cloc[e].blk < b1) lists[r].push_back(e);
+    const StreamHost h = build_stream(
+        lists, [&](int e) { return off_in(Loc{cloc[e].blk - b0, cloc[e].local}); },
+        [&](int64_t r) { return off_out(locate(r, f_out->rho)); });
+    append_stream(gfwd, h);
+  }
   // the backward stream: one stream per input-side chunk (its columns, destinations relative to
   // the chunk's first block), concatenated, with per-chunk wave runs
   StreamHost gbwd;
-  for (int ch = 0; ch < p->bwd_nch; ++ch) {
-    const int b0 = p->bwd_chunk_blk[ch], b1 = p->bwd_chunk_blk[ch + 1];
+  for (int ch = 0; ch < p->gen_nch; ++ch) {
+    const int b0 = p->gen_chunk_blk[ch], b1 = p->gen_chunk_blk[ch + 1];
     std::vector<int64_t> col_of;
     std::vector<std::vector<int>> lists;
     for (int64_t c = 0; c < n; ++c) {
@@ -389,18 +410,20 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
           const Loc l = locate(col_of[slot], f_in->rho);
           return off_in(Loc{l.blk - b0, l.local});
         });
-    for (int w = 0; w <= ff::kGenWaves; ++w) gbwd.wave_row.push_back((int)(gbwd.rows + h.wave_row[w]));
-    gbwd.ent.insert(gbwd.ent.end(), h.ent.begin(), h.ent.end());
-    gbwd.id.insert(gbwd.id.end(), h.id.begin(), h.id.end());
-    gbwd.rows += h.rows;
+    append_stream(gbwd, h);
   }
   {
-    // every backward offset stays inside its tile row (u whole, z / q one chunk)
-    const int cmax = (FI.nblk + p->bwd_nch - 1) / p->bwd_nch;
+    // every stream offset stays inside its tile row (output side whole, input side one chunk)
+    const int cmax = (FI.nblk + p->gen_nch - 1) / p->gen_nch;
     for (const int2& e : gbwd.ent) {
       const int so = e.x & ~ff::kRowLast;
       if (so < 0 || so >= FO.nblk * p->ldb_out || e.y < -1 || e.y >= cmax * p->ldb_in)
         return ff::fail(FF_EINVAL, "internal: backward stream offset outside its tile");
+    }
+    for (const int2& e : gfwd.ent) {
+      const int so = e.x & ~ff::kRowLast;
+      if (so < 0 || so >= cmax * p->ldb_in || e.y < -1 || e.y >= FO.nblk * p->ldb_out)
+        return ff::fail(FF_EINVAL, "internal: forward stream offset outside its tile");
     }
   }
   // merge buckets (R, S)
@@ -700,9 +723,9 @@ extern "C" ff_status ff_plan_query(const ff_plan* p, int key, int64_t* value) {
     case FF_Q_BWD_TILE_TOKENS: *value = !p->fast.enabled ? 0 : p->fast.bwd16 ? 16 : 8; return FF_OK;
     case FF_Q_RADIX_IN: *value = p->fin->dev.radix; return FF_OK;
     case FF_Q_RADIX_OUT: *value = p->fout->dev.radix; return FF_OK;
-    case FF_Q_GEN_BWD_CHUNKS: *value = p->bwd_nch; return FF_OK;
-    case FF_Q_GEN_BWD_TOKENS_F32: *value = p->bwd_tile_tokens[FF_F32]; return FF_OK;
-    case FF_Q_GEN_BWD_TOKENS_BF16: *value = p->bwd_tile_tokens[FF_BF16]; return FF_OK;
+    case FF_Q_GEN_CHUNKS: *value = p->gen_nch; return FF_OK;
+    case FF_Q_GEN_TILE_TOKENS_F32: *value = p->gen_tile_tokens[FF_F32]; return FF_OK;
+    case FF_Q_GEN_TILE_TOKENS_BF16: *value = p->gen_tile_tokens[FF_BF16]; return FF_OK;
     default: return ff::fail(FF_EINVAL, "unknown query key %d", key);
   }
 }

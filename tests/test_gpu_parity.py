@@ -233,18 +233,19 @@ def test_generic_backward_many_tiles_per_workgroup(dev, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_generic_backward_input_chunks(dev, dtype):
-    """An input side too wide to sit whole next to u for 8 tokens (factored 256-wide blocks) and
-    a dense enough support (nnz >= 4 (n + m)): the generic backward takes the input side a chunk
-    of blocks at a time.  With several tiles per workgroup, a dX-only call, a dC-only call and a
+def test_generic_input_chunks(dev, dtype):
+    """An input side too wide to sit whole next to the output side for 8 tokens (factored
+    256-wide blocks) and a dense enough support (nnz >= 4 (n + m)): the generic kernels take the
+    input side a chunk of blocks at a time.  The forward (v summed over chunks; also with beta)
+    matches the oracle; with several tiles per workgroup, a dX-only call, a dC-only call and a
     call with both match the oracle, dC is deterministic, and beta accumulates into dX."""
     n, rn, m, rm, nnz = 8192, 64, 2048, 64, 42000
     f_in, f_out = ff.framegen(n, n // rn, rn), ff.framegen(m, m // rm, rm)
     g = inputs.rng(5151)
     rows, cols = inputs.support(g, m, n, nnz)
     probe = ff.plan_create(f_in, f_out, rows, cols, max_tokens=1)
-    assert probe.gen_bwd_chunks > 1 and probe.radix == (4, 1) and not probe.fast128
-    tt = probe.gen_bwd_tile_tokens(dtype)
+    assert probe.gen_chunks > 1 and probe.radix == (4, 1) and not probe.fast128
+    tt = probe.gen_tile_tokens(dtype)
     assert tt > probe.tile_tokens(dtype)
     ncu = torch.cuda.get_device_properties(dev).multi_processor_count
     T = tt * (ncu + 2) + 1   # more tiles than workgroups, a ragged last tile
@@ -255,6 +256,9 @@ def test_generic_backward_input_chunks(dev, dtype):
     Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
     c = plan_c(plan, vals, dev)
     s = 0.9
+    Y = ff.adapter_fwd(plan, Xd, c, s)
+    Y2 = Y.clone()
+    ff.adapter_fwd(plan, Xd, c, s, Y=Y2, beta=1.0)
     dXo, _ = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dc=False)
     _, dCo = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dx=False)
     dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s)
@@ -263,9 +267,12 @@ def test_generic_backward_input_chunks(dev, dtype):
     torch.cuda.synchronize()
     P_in, P_out = oracle_frame(n // rn, rn, n), oracle_frame(m // rm, rm, m)
     tok = _sample_tokens(T, 48, 12)
+    y_ref = O.adapter_fwd(P_in, P_out, rows, cols, vals, s, X[tok])
     dx_ref, _ = O.adapter_bwd(P_in, P_out, rows, cols, vals, s, X[tok], G[tok])
     dc_ref = O.coeff_grad_entries(P_in, P_out, rows, cols, s, X, G)
     tol = TOL[dtype]
+    assert rel(to_np(Y[tok]), y_ref) <= tol
+    assert rel(to_np(Y2[tok]), 2.0 * y_ref) <= tol
     assert rel(to_np(dXo[tok]), dx_ref) <= tol
     assert rel(to_np(dX[tok]), dx_ref) <= tol
     assert rel(to_np(dX2[tok]), 2.0 * dx_ref) <= tol
@@ -330,7 +337,7 @@ def _full_size_check(dev, wl_name, adapter_index=0, n_tok=48, n_nnz=384, n_rows=
     f_out = ff.framegen(ad.d_out, ad.k_out, ad.rho_out)
     plan = ff.plan_create(f_in, f_out, data.rows, data.cols, max_tokens=T)
     if bwd_chunked is not None:
-        assert (plan.gen_bwd_chunks > 1) == bwd_chunked
+        assert (plan.gen_chunks > 1) == bwd_chunked
     Xd, Gd = torch_act(data.X, dtype, dev), torch_act(data.G, dtype, dev)
     c = plan_c(plan, data.vals, dev)
     Y = ff.adapter_fwd(plan, Xd, c, data.scale)

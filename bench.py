@@ -311,7 +311,8 @@ def main():
                           "fwd_kernel_us": round(fwd_us, 3), "bwd_kernel_us": round(bwd_us, 3)},
         "context": {"w0_gemm_us": round(gemm_us, 2), "setup_s": round(setup_s, 3),
                     "wall_ms_timed": round(wall_ms, 3),
-                    "tile_tokens": plan.tile_tokens(wl.dtype), "kernel_hash": kernel_hash()},
+                    "tile_tokens": plan.tile_tokens(wl.dtype), "input_chunks": plan.gen_chunks,
+                    "chunk_tile_tokens": plan.gen_tile_tokens(wl.dtype), "kernel_hash": kernel_hash()},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, ad, data)

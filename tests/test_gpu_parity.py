@@ -58,6 +58,10 @@ SHAPES = [
     # streams too long for its registers
     (1024, 16, 8192, 128, 6000, 21),
     (1024, 16, 1024, 16, 40000, 11),
+    # input side in chunks of blocks (dense support, 256-wide factored input blocks): fewer
+    # tokens than a tile, and a single token
+    (8192, 64, 2048, 64, 42000, 5),
+    (8192, 64, 2048, 64, 42000, 1),
 ]
 
 
@@ -85,6 +89,8 @@ def test_small_parity(dev, shape, dtype):
         assert plan.bwd_tile_tokens == (8 if m > 4096 or nnz > 20000 else 16)
     # blocks wider than 128 (k = 172, 224) are applied as a radix-4 stage plus a DFT of size k/4
     assert plan.radix == (4 if 2 * n // rn > 128 else 1, 4 if 2 * m // rm > 128 else 1)
+    # the generic kernels chunk the input side only for the wide, dense-support shapes
+    assert (plan.gen_chunks > 1) == (n == 8192)
     tol = TOL[dtype]
     Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
     c = plan_c(plan, vals, dev)

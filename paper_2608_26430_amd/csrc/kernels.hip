@@ -535,7 +535,9 @@ __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const floa
 // dC / s = sum_t u_t[row] z_t[column], z being read from the lane's destination before q is
 // written over it; part receives one float per stream element (added to when part_add).
 constexpr int kSD = 8;   // stream rows per buffer (two buffers: up to 16 rows in flight)
-constexpr int kTG = 8;   // most tokens per pass over the stream
+constexpr int kTG = 8;        // tokens per pass over the stream (a last pass may take 2 to 7)
+constexpr int kTGWide = 16;   // tokens per pass while at least that many remain: each pass
+                              // starts with a latency-bound load of its first entries
 
 template <bool BF16, bool BWD, bool PART_ADD, int kTG>
 __device__ __forceinline__ void stream_products(const GenStream& S, const float* __restrict__ cv,
@@ -660,19 +662,28 @@ __device__ __forceinline__ void stream_pass(const GenStream& S, const float* __r
   }
 }
 
-// All tokens of a tile, kTG at a time, each pass reading only as many token rows as it needs.
+// All tokens of a tile, kTGWide at a time while that many remain, then kTG, each pass reading
+// only as many token rows as it needs.
 // `add` (MAY_ADD only): backward, add to the dC partial row (as do the tile's later passes);
 // forward, add the sums to the destination (the input side's later chunks).
 template <bool BF16, bool BWD, bool MAY_ADD = BWD>
 __device__ __forceinline__ void stream_all(const GenStream& S, const float* __restrict__ cv,
                                            const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
                                            int ld_dst, int nt, bool write_dst, float* part, bool add = false) {
-  for (int tg = 0; tg < nt; tg += kTG) {
-    const int ntg = min(kTG, nt - tg);
-    if (MAY_ADD && (add || (BWD && tg > 0)))
+  for (int tg = 0; tg < nt;) {
+    const int ntg = nt - tg >= kTGWide ? kTGWide : min(kTG, nt - tg);
+    const bool add_now = MAY_ADD && (add || (BWD && tg > 0));
+    if (ntg == kTGWide) {
+      if (add_now)
+        stream_products<BF16, BWD, MAY_ADD, kTGWide>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+      else
+        stream_products<BF16, BWD, false, kTGWide>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    } else if (add_now) {
       stream_pass<BF16, BWD, MAY_ADD>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    else
+    } else {
       stream_pass<BF16, BWD, false>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    }
+    tg += ntg;
   }
 }
 

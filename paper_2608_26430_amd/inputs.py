@@ -135,6 +135,25 @@ def support(g: np.random.Generator, m: int, n: int, nnz: int):
     return (flat // n).astype(np.int32), (flat % n).astype(np.int32)
 
 
+def support_block_diagonal(g: np.random.Generator, k: int, rho_out: int, rho_in: int, nnz: int):
+    """nnz distinct positions drawn uniformly from the diagonal blocks of C = diag(C_1..C_k).
+
+    Sec. 3.1 writes C as block diagonal, block i (rho_out x rho_in) coupling output subspace i
+    with input subspace i; Sec. 3.3 spreads the nonzeros uniformly across those blocks.  In the
+    subspace-major coefficient order (P = [P_1 ... P_k]) block i covers rows
+    [i rho_out, (i + 1) rho_out) and columns [i rho_in, (i + 1) rho_in).  Both frames must have
+    the same number k of subspaces.
+    """
+    per = rho_out * rho_in
+    if nnz > k * per:
+        raise ValueError("nnz exceeds the diagonal blocks")
+    flat = g.choice(k * per, size=nnz, replace=False)
+    blk, within = flat // per, flat % per
+    rows = blk * rho_out + within // rho_in
+    cols = blk * rho_in + within % rho_in
+    return rows.astype(np.int32), cols.astype(np.int32)
+
+
 @dataclass
 class AdapterData:
     """Host arrays for one adapter call: all fp32 (bf16-valued when dtype is bf16)."""

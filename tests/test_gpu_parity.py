@@ -438,3 +438,57 @@ def test_cfg4_stack_batched_full(dev, group):
         ent = np.random.default_rng(wl.seed + i).choice(len(rows), size=128, replace=False)
         dc_ref = O.coeff_grad_entries(P_in, P_out, rows[ent], cols[ent], s, d.X, d.G)
         assert rel(user_dc(plan, dCd[i])[ent], dc_ref) <= tol
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(256, 16, 256, 16, 512, 64), (4096, 64, 4096, 64, 10_000, 40),
+                                   (768, 64, 768, 64, 3_000, 37)],
+                         ids=lambda s: "n%d_m%d_nnz%d_T%d" % (s[0], s[2], s[4], s[5]))
+def test_block_diagonal_support(dev, shape, dtype):
+    """C = diag(C_1..C_k) with the nonzeros spread uniformly over the diagonal blocks (Sec. 3.1,
+    Sec. 3.3): forward, backward and merge against the oracle."""
+    n, rn, m, rm, nnz, T = shape
+    k = n // rn
+    g = inputs.rng(n + nnz + T)
+    rows, cols = inputs.support_block_diagonal(g, k, rm, rn, nnz)
+    vals = inputs.gaussian(g, (nnz,), std=0.02)
+    X = inputs.gaussian(g, (T, n), dtype=dtype)
+    G = inputs.gaussian(g, (T, m), dtype=dtype)
+    s = 0.31
+    P_in, P_out = oracle_frame(k, rn, n), oracle_frame(m // rm, rm, m)
+    f_in = ff.framegen(n, k, rn)
+    f_out = f_in if (m, rm) == (n, rn) else ff.framegen(m, m // rm, rm)
+    plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T)
+    c = plan_c(plan, vals, dev)
+    Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
+    Y = ff.adapter_fwd(plan, Xd, c, s)
+    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s)
+    Wd = ff.merge_delta(plan, c, s, torch.zeros((m, n), device=dev), beta=0.0)
+    torch.cuda.synchronize()
+    tol = TOL[dtype]
+    dx_ref, dc_ref = O.adapter_bwd(P_in, P_out, rows, cols, vals, s, X, G)
+    assert rel(to_np(Y), O.adapter_fwd(P_in, P_out, rows, cols, vals, s, X)) <= tol
+    assert rel(to_np(dX), dx_ref) <= tol
+    assert rel(user_dc(plan, dC), dc_ref) <= tol
+    assert rel(to_np(Wd), O.merge_delta(P_in, P_out, rows, cols, vals, s)) <= 1e-5
+
+
+def test_hot_swap_merge_then_unmerge(dev):
+    """Merging s P_out C P_in^T into W and then merging with -s (the hot swap of Sec. 3.3) gives
+    back W up to fp32 rounding, and the merged weight reproduces W0 x + adapter forward."""
+    n = m = 4096
+    rows, cols, vals, X, _ = _problem((n, 64, m, 64, 10_000, 16), "f32", 77)
+    f = ff.framegen(n, 64, 64)
+    plan = ff.plan_create(f, f, rows, cols, max_tokens=16)
+    c = plan_c(plan, vals, dev)
+    s = 200.0 / 4096.0
+    W0 = torch.from_numpy(inputs.weight(inputs.rng(8), m, n, "f32")).to(dev)
+    W = W0.clone()
+    ff.merge_delta(plan, c, s, W, beta=1.0)
+    Xd = torch.from_numpy(X).to(dev)
+    y_merged = Xd @ W.T
+    y_split = Xd @ W0.T + ff.adapter_fwd(plan, Xd, c, s)
+    ff.merge_delta(plan, c, -s, W, beta=1.0)
+    torch.cuda.synchronize()
+    assert rel(to_np(y_merged), to_np(y_split)) <= 1e-5
+    assert torch.max(torch.abs(W - W0)).item() <= 2.0 ** -20

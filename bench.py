@@ -174,6 +174,41 @@ def bench_stack(args, torch, ff, inputs, dev):
     print(json.dumps(out), flush=True)
 
 
+# Query and value projections (d_in -> d_out) of the models whose frame construction time the
+# paper reports on an A100 (Appendix, basis generation time: Spectral Tetris rows, seconds).
+FRAMEGEN_MODELS = {
+    "Llama-2-7B": ([(4096, 4096), (4096, 4096)], 0.09),
+    "Gemma-2-9B": ([(3584, 4096), (3584, 2048)], 0.21),
+    "Llama-3.1-8B": ([(4096, 4096), (4096, 1024)], 0.11),
+}
+
+
+def bench_framegen(torch, ff, rho=64, reps=5):
+    """Wall time of building every distinct frame one model's adapted projections need.
+
+    Frames depend only on (d, k, rho) and are shared across layers (Sec. 3.3), so a model needs one
+    frame per distinct dimension.  The paper's instruction-tuning runs use rho = 2 (a single dense
+    block of width d per frame), which the GPU path does not take; rho = 64 is timed instead.
+    """
+    out = {}
+    for name, (projs, paper_s) in FRAMEGEN_MODELS.items():
+        dims = sorted({d for p in projs for d in p})
+        times = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            frames = [ff.framegen(d, d // rho, rho) for d in dims]
+            torch.cuda.synchronize()
+            times.append(time.perf_counter() - t0)
+            del frames
+        out[name] = {"dims": dims, "rho": rho, "median_s": round(float(np.median(times)), 5),
+                     "paper_s_a100_spectral_tetris": paper_s}
+    print(json.dumps({"metric": "frame construction time (ff_framegen: host construction, "
+                                "exact tightness checks, upload)", "unit": "s",
+                      "higher_is_better": False, "models": out,
+                      "note": "paper's times are an A100 PyTorch run at rho = 2; context, not a target"}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -184,6 +219,9 @@ def main():
     ap.add_argument("--stack", action="store_true",
                     help="time every adapter of every layer of the workload (the 7B stack) as batched calls")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--framegen", action="store_true",
+                    help="time frame construction (ff_framegen, host build and upload) for the adapted "
+                         "projections of the models in the paper's basis-generation-time table")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run 3 device-to-device copies of this many MiB (a known-size kernel "
                          "that calibrates the HBM byte counters of a --pmc profile)")
@@ -210,6 +248,9 @@ def main():
         del src, dst
     if args.stack:
         bench_stack(args, torch, ff, inputs, dev)
+        return
+    if args.framegen:
+        bench_framegen(torch, ff)
         return
     wl = inputs.WORKLOADS[args.workload]
     ad = wl.adapters[args.adapter]

@@ -174,6 +174,57 @@ def bench_stack(args, torch, ff, inputs, dev):
     print(json.dumps(out), flush=True)
 
 
+def bench_merge(args, torch, ff, inputs, dev):
+    """Merge into the frozen weight (Algorithm 1 steps 5-6): W = W + s P_out C P_in^T in place on
+    a bf16 m x n weight, alternating +s and -s (merge, then unmerge: the hot swap of Sec. 3.3).
+
+    Algorithmic bytes per merge: read and write W (4 m n B for bf16) plus the coefficients
+    (4 B each); the rank-1 work is nnz (2 k_out) (2 k_in) fused multiply-adds.  W0 is drawn on
+    the device (seeded); this mode times the kernel and checks nothing.
+    """
+    wl = inputs.WORKLOADS[args.workload]
+    ad = wl.adapters[args.adapter]
+    data = inputs.adapter_data(wl, ad, tokens=1)
+    n, m, nnz = ad.d_in, ad.d_out, ad.nnz
+    f_in = ff.framegen(n, ad.k_in, ad.rho_in)
+    f_out = f_in if (m, ad.k_out, ad.rho_out) == (n, ad.k_in, ad.rho_in) else ff.framegen(m, ad.k_out, ad.rho_out)
+    plan = ff.plan_create(f_in, f_out, data.rows, data.cols, max_tokens=1)
+    c = torch.from_numpy(plan.to_plan(data.vals)).to(dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(wl.seed)
+    W = (torch.randn((m, n), generator=gen, device=dev) * (1.0 / np.sqrt(n))).to(torch.bfloat16)
+    for i in range(args.warmup):
+        ff.merge_delta(plan, c, data.scale if i % 2 == 0 else -data.scale, W, beta=1.0)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(args.steps):
+        ff.merge_delta(plan, c, data.scale if i % 2 == 0 else -data.scale, W, beta=1.0)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for i, (e0, e1) in enumerate(evs):
+        ff.binding.time_next_kernel(e0, e1)
+        ff.merge_delta(plan, c, data.scale if i % 2 == 0 else -data.scale, W, beta=1.0)
+    torch.cuda.synchronize()
+    avg_us = float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs])) * 1e3
+    nbytes = 4 * m * n + 4 * nnz
+    fma = nnz * (2 * ad.k_out) * (2 * ad.k_in)
+    ach = nbytes / (avg_us * 1e-6) / 1e9
+    print(json.dumps({
+        "metric": "FrameFT merge W += s P_out C P_in^T into a bf16 weight (HBM GB/s)", "value": round(ach, 1),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "dtype": "f32 arithmetic, bf16 weight", "data": "synthetic",
+        "config": {"workload": f"{args.workload}: merge of {ad.name} {n}->{m}, nnz={nnz}, frames "
+                               f"(k={ad.k_in}, rho={ad.rho_in}) -> (k={ad.k_out}, rho={ad.rho_out})"},
+        "roofline": {"bound": "hbm", "kernel": "merge_kernel", "achieved": round(ach, 1), "peak": 8000.0,
+                     "unit": "GB/s", "frac": round(ach / 8000.0, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": nbytes, "avg_us": round(avg_us, 3)},
+        "context": {"rank1_fma": fma, "rank1_tflops": round(2 * fma / (avg_us * 1e-6) / 1e12, 2),
+                    "fp32_vector_peak_tflops": 157.3, "kernel_hash": kernel_hash()}}))
+
+
 # Query and value projections (d_in -> d_out) of the models whose frame construction time the
 # paper reports on an A100 (Appendix, basis generation time: Spectral Tetris rows, seconds).
 FRAMEGEN_MODELS = {
@@ -219,6 +270,9 @@ def main():
     ap.add_argument("--stack", action="store_true",
                     help="time every adapter of every layer of the workload (the 7B stack) as batched calls")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--merge", action="store_true",
+                    help="time the merge W += s P_out C P_in^T into the workload adapter's bf16 weight "
+                         "(alternating +s and -s, the hot swap) instead of the training step")
     ap.add_argument("--framegen", action="store_true",
                     help="time frame construction (ff_framegen, host build and upload) for the adapted "
                          "projections of the models in the paper's basis-generation-time table")
@@ -251,6 +305,9 @@ def main():
         return
     if args.framegen:
         bench_framegen(torch, ff)
+        return
+    if args.merge:
+        bench_merge(args, torch, ff, inputs, dev)
         return
     wl = inputs.WORKLOADS[args.workload]
     ad = wl.adapters[args.adapter]

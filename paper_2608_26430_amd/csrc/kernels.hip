@@ -915,7 +915,7 @@ __global__ void __launch_bounds__(64 * kDcWaves) dc_reduce(const float* __restri
 struct MergeArgs {
   const float* Bm;   // output-frame block, W_m x W_m
   const float* Bn;   // input-frame block,  W_n x W_n
-  int Wm, Wn, nblk_in, rows_per_wg, nsub, chunk;
+  int Wm, Wn, nblk_in, nsub_r, nsub_c, vec;
   const int* ptr;
   const int4* ent;
   const float* c;
@@ -925,63 +925,138 @@ struct MergeArgs {
 };
 
 constexpr int kMergeThreads = 256;
-constexpr int kMergeEPT = 8;   // output elements per thread
+constexpr int kMergeRows = 128;                // output rows of a workgroup: 32 groups of 4
+constexpr int kMergeCols = 64;                 // output columns of a workgroup: 8 groups of 8
+constexpr int kMergeChunk = 64;                // entries staged per pass
+constexpr int kMergeUS = kMergeRows + 4;       // LDS row strides in floats: rows stay 16-byte
+constexpr int kMergeVS = kMergeCols + 4;       // aligned, staging writes spread over the banks
 
+// W[block R rows, block S columns] = beta W + sum_e U_e V_e^T over the entries e of the block pair,
+// U_e = s c_e B_m[:, a'_e] and V_e = B_n[:, b'_e] (the rank-1 terms of P_out C P_in^T).  A
+// workgroup owns 128 rows x 64 columns of one block pair and each thread a 4 x 8 patch held in
+// registers; U and V columns of up to 64 entries at a time are staged in LDS (each entry's
+// frame values gathered once per workgroup), and every output sums its terms in bucket order.
 template <bool BF16W>
 __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int OR = a.rows_per_wg;
-  float* cb = reinterpret_cast<float*>(smem);    // chunk x OR : s * c_e * B_m[u][a'_e]
-  float* bn = cb + a.chunk * OR;                 // chunk x W_n: B_n[p][b'_e]
-  const int sub = blockIdx.x % a.nsub;
-  const int tile = blockIdx.x / a.nsub;          // R * nblk_in + S
+  __shared__ __attribute__((aligned(16))) float us[kMergeChunk * kMergeUS];
+  __shared__ __attribute__((aligned(16))) float vs[kMergeChunk * kMergeVS];
+  const int nsub = a.nsub_r * a.nsub_c;
+  const int sub = blockIdx.x % nsub, tile = blockIdx.x / nsub;
   const int R = tile / a.nblk_in, S = tile - R * a.nblk_in;
-  const int u0 = sub * OR;
-  const int rows = min(OR, a.Wm - u0);
-  const int nel = rows * a.Wn;
-  int eo[kMergeEPT], ep[kMergeEPT];
-  float acc[kMergeEPT];
+  const int u0 = (sub / a.nsub_c) * kMergeRows, p0 = (sub % a.nsub_c) * kMergeCols;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int r = ((lane >> 3) + 8 * wv) * 4;    // the thread's first row within the workgroup's rows
+  const int q = (lane & 7) * 8;                // its first column within the workgroup's columns
+  // W_m and W_n are multiples of 8, so a patch lies wholly inside or wholly outside the block
+  const bool live = u0 + r < a.Wm && p0 + q < a.Wn;
+  const long row0 = (long)R * a.Wm + u0 + r;
+  const long col0 = (long)S * a.Wn + p0 + q;
+  const bool rmw = a.beta != 0.f;
+
+  float old[4][8];
 #pragma unroll
-  for (int k = 0; k < kMergeEPT; ++k) {
-    const int idx = threadIdx.x + k * kMergeThreads;
-    eo[k] = idx < nel ? idx / a.Wn : -1;
-    ep[k] = idx < nel ? idx - eo[k] * a.Wn : 0;
-    acc[k] = 0.f;
-  }
-  const int beg = a.ptr[tile], end = a.ptr[tile + 1];
-  for (int c0 = beg; c0 < end; c0 += a.chunk) {
-    const int nch = min(a.chunk, end - c0);
-    for (int x = threadIdx.x; x < nch * OR; x += kMergeThreads) {
-      const int e = x / OR, u = x - e * OR;
-      const int4 en = a.ent[c0 + e];
-      cb[e * OR + u] = (u < rows) ? a.scale * a.c[en.z] * a.Bm[(u0 + u) * a.Wm + en.x] : 0.f;
-    }
-    for (int x = threadIdx.x; x < nch * a.Wn; x += kMergeThreads) {
-      const int e = x / a.Wn, p = x - e * a.Wn;
-      bn[e * a.Wn + p] = a.Bn[p * a.Wn + a.ent[c0 + e].y];
-    }
-    __syncthreads();
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int k = 0; k < kMergeEPT; ++k) {
-      if (eo[k] >= 0) {
-        float s = acc[k];
-        for (int e = 0; e < nch; ++e) s = fmaf(cb[e * OR + eo[k]], bn[e * a.Wn + ep[k]], s);
-        acc[k] = s;
+    for (int j = 0; j < 8; ++j) old[i][j] = 0.f;
+  if (live && rmw) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const long off = (row0 + i) * a.ldw + col0;
+      if constexpr (BF16W) {
+        const u16* w = reinterpret_cast<const u16*>(a.W) + off;
+        if (a.vec) {
+          const uint4 v = *reinterpret_cast<const uint4*>(w);
+          const unsigned x[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            old[i][2 * j] = bf2f((u16)(x[j] & 0xffffu));
+            old[i][2 * j + 1] = bf2f((u16)(x[j] >> 16));
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) old[i][j] = bf2f(w[j]);
+        }
+      } else {
+        const float* w = reinterpret_cast<const float*>(a.W) + off;
+        if (a.vec) {
+          const float4 v0 = *reinterpret_cast<const float4*>(w);
+          const float4 v1 = *reinterpret_cast<const float4*>(w + 4);
+          old[i][0] = v0.x; old[i][1] = v0.y; old[i][2] = v0.z; old[i][3] = v0.w;
+          old[i][4] = v1.x; old[i][5] = v1.y; old[i][6] = v1.z; old[i][7] = v1.w;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) old[i][j] = w[j];
+        }
       }
     }
-    __syncthreads();
   }
+
+  float acc[4][8];
 #pragma unroll
-  for (int k = 0; k < kMergeEPT; ++k) {
-    if (eo[k] < 0) continue;
-    const long off = (long)(R * a.Wm + u0 + eo[k]) * a.ldw + (long)S * a.Wn + ep[k];
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = 0.f;
+  const int beg = a.ptr[tile], end = a.ptr[tile + 1];
+  for (int c0 = beg; c0 < end; c0 += kMergeChunk) {
+    const int nch = min(kMergeChunk, end - c0);
+    __syncthreads();   // the previous pass has finished reading us / vs
+    // staging index x: entry e = 8 * (x / (8 rows)) + x % 8, so a wave gathers 8 entries of 8 rows
+    const int ngrp = (nch + 7) >> 3;
+    for (int x = threadIdx.x; x < ngrp * 8 * kMergeRows; x += kMergeThreads) {
+      const int e = ((x / (8 * kMergeRows)) << 3) | (x & 7), u = (x >> 3) & (kMergeRows - 1);
+      if (e < nch && u0 + u < a.Wm) {
+        const int4 en = a.ent[c0 + e];
+        us[e * kMergeUS + u] = a.scale * a.c[en.z] * a.Bm[(long)(u0 + u) * a.Wm + en.x];
+      }
+    }
+    for (int x = threadIdx.x; x < ngrp * 8 * kMergeCols; x += kMergeThreads) {
+      const int e = ((x / (8 * kMergeCols)) << 3) | (x & 7), p = (x >> 3) & (kMergeCols - 1);
+      if (e < nch && p0 + p < a.Wn) vs[e * kMergeVS + p] = a.Bn[(long)(p0 + p) * a.Wn + a.ent[c0 + e].y];
+    }
+    __syncthreads();
+    if (live) {
+      for (int e = 0; e < nch; ++e) {
+        const float4 uu = *reinterpret_cast<const float4*>(&us[e * kMergeUS + r]);
+        const float4 va = *reinterpret_cast<const float4*>(&vs[e * kMergeVS + q]);
+        const float4 vb = *reinterpret_cast<const float4*>(&vs[e * kMergeVS + q + 4]);
+        const float uv[4] = {uu.x, uu.y, uu.z, uu.w};
+        const float vv[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) acc[i][j] = fmaf(uv[i], vv[j], acc[i][j]);
+      }
+    }
+  }
+  if (!live) return;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const long off = (row0 + i) * a.ldw + col0;
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = rmw ? a.beta * old[i][j] + acc[i][j] : acc[i][j];
     if constexpr (BF16W) {
       u16* w = reinterpret_cast<u16*>(a.W) + off;
-      const float v = a.beta != 0.f ? a.beta * bf2f(*w) + acc[k] : acc[k];
-      *w = f2bf(v);
+      if (a.vec) {
+        uint4 o;
+        o.x = (unsigned)f2bf(v[0]) | ((unsigned)f2bf(v[1]) << 16);
+        o.y = (unsigned)f2bf(v[2]) | ((unsigned)f2bf(v[3]) << 16);
+        o.z = (unsigned)f2bf(v[4]) | ((unsigned)f2bf(v[5]) << 16);
+        o.w = (unsigned)f2bf(v[6]) | ((unsigned)f2bf(v[7]) << 16);
+        *reinterpret_cast<uint4*>(w) = o;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) w[j] = f2bf(v[j]);
+      }
     } else {
       float* w = reinterpret_cast<float*>(a.W) + off;
-      *w = a.beta != 0.f ? a.beta * *w + acc[k] : acc[k];
+      if (a.vec) {
+        *reinterpret_cast<float4*>(w) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(w + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) w[j] = v[j];
+      }
     }
   }
 }
@@ -1007,8 +1082,6 @@ hipError_t configure_kernels() {
     set(reinterpret_cast<const void*>(&bwd_kernel<false, false>));
     set(reinterpret_cast<const void*>(&bwd_kernel<true, true>));
     set(reinterpret_cast<const void*>(&bwd_kernel<false, true>));
-    set(reinterpret_cast<const void*>(&merge_kernel<true>));
-    set(reinterpret_cast<const void*>(&merge_kernel<false>));
     return e;
   }();
   return once;
@@ -1173,10 +1246,13 @@ hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf1
   a.Bn = p->fin->dev.B32;
   a.Wm = p->fout->dev.W;
   a.Wn = p->fin->dev.W;
+  if (a.Wm % 8 != 0 || a.Wn % 8 != 0) return hipErrorInvalidValue;   // patches of 4 rows x 8 columns
   a.nblk_in = p->fin->dev.nblk;
-  a.rows_per_wg = std::max(1, std::min(a.Wm, kMergeThreads * kMergeEPT / a.Wn));
-  a.nsub = (a.Wm + a.rows_per_wg - 1) / a.rows_per_wg;
-  a.chunk = std::max(1, std::min(32, (int)(65536 / ((a.rows_per_wg + a.Wn) * sizeof(float)))));
+  a.nsub_r = (a.Wm + kMergeRows - 1) / kMergeRows;
+  a.nsub_c = (a.Wn + kMergeCols - 1) / kMergeCols;
+  const size_t esz = w_bf16 ? 2 : 4;
+  // 16-byte accesses when the base and the row stride keep every 8-column patch aligned
+  a.vec = (reinterpret_cast<uintptr_t>(W) % 16 == 0) && ((size_t)ldw * esz) % 16 == 0;
   a.ptr = p->dev.mrg_ptr;
   a.ent = p->dev.mrg_ent;
   a.c = c;
@@ -1184,15 +1260,14 @@ hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf1
   a.beta = beta;
   a.W = W;
   a.ldw = (long)ldw;
-  const size_t lds = (size_t)a.chunk * (a.rows_per_wg + a.Wn) * sizeof(float);
-  const long nwg = (long)p->fout->dev.nblk * p->fin->dev.nblk * a.nsub;
+  const long nwg = (long)p->fout->dev.nblk * p->fin->dev.nblk * a.nsub_r * a.nsub_c;
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
   record(e0, s);
   if (w_bf16)
-    hipLaunchKernelGGL(merge_kernel<true>, dim3((unsigned)nwg), dim3(kMergeThreads), lds, s, a);
+    hipLaunchKernelGGL(merge_kernel<true>, dim3((unsigned)nwg), dim3(kMergeThreads), 0, s, a);
   else
-    hipLaunchKernelGGL(merge_kernel<false>, dim3((unsigned)nwg), dim3(kMergeThreads), lds, s, a);
+    hipLaunchKernelGGL(merge_kernel<false>, dim3((unsigned)nwg), dim3(kMergeThreads), 0, s, a);
   record(e1, s);
   return hipGetLastError();
 }

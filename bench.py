@@ -222,7 +222,7 @@ def bench_merge(args, torch, ff, inputs, dev):
                      "unit": "GB/s", "frac": round(ach / 8000.0, 4), "traffic": None,
                      "algorithmic_bytes_per_launch": nbytes, "avg_us": round(avg_us, 3)},
         "context": {"rank1_fma": fma, "rank1_tflops": round(2 * fma / (avg_us * 1e-6) / 1e12, 2),
-                    "fp32_vector_peak_tflops": 157.3, "kernel_hash": kernel_hash()}}))
+                    "fp32_vector_tflops_unpacked": 78.6, "kernel_hash": kernel_hash()}}))
 
 
 # Query and value projections (d_in -> d_out) of the models whose frame construction time the

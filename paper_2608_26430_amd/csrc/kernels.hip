@@ -927,14 +927,14 @@ struct MergeArgs {
 constexpr int kMergeThreads = 256;
 constexpr int kMergeRows = 128;                // output rows of a workgroup: 32 groups of 4
 constexpr int kMergeCols = 64;                 // output columns of a workgroup: 8 groups of 8
-constexpr int kMergeChunk = 64;                // entries staged per pass
+constexpr int kMergeChunk = 32;                // entries staged per pass (25.6 KB of LDS)
 constexpr int kMergeUS = kMergeRows + 4;       // LDS row strides in floats: rows stay 16-byte
 constexpr int kMergeVS = kMergeCols + 4;       // aligned, staging writes spread over the banks
 
 // W[block R rows, block S columns] = beta W + sum_e U_e V_e^T over the entries e of the block pair,
 // U_e = s c_e B_m[:, a'_e] and V_e = B_n[:, b'_e] (the rank-1 terms of P_out C P_in^T).  A
 // workgroup owns 128 rows x 64 columns of one block pair and each thread a 4 x 8 patch held in
-// registers; U and V columns of up to 64 entries at a time are staged in LDS (each entry's
+// registers; U and V columns of up to 32 entries at a time are staged in LDS (each entry's
 // frame values gathered once per workgroup), and every output sums its terms in bucket order.
 template <bool BF16W>
 __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {

@@ -940,6 +940,8 @@ template <bool BF16W>
 __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
   __shared__ __attribute__((aligned(16))) float us[kMergeChunk * kMergeUS];
   __shared__ __attribute__((aligned(16))) float vs[kMergeChunk * kMergeVS];
+  __shared__ float es[kMergeChunk];   // s c_e of the pass's entries
+  __shared__ int ea[kMergeChunk], eb[kMergeChunk];   // their columns a'_e of B_m and b'_e of B_n
   const int nsub = a.nsub_r * a.nsub_c;
   const int sub = blockIdx.x % nsub, tile = blockIdx.x / nsub;
   const int R = tile / a.nblk_in, S = tile - R * a.nblk_in;
@@ -999,19 +1001,26 @@ __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
   const int beg = a.ptr[tile], end = a.ptr[tile + 1];
   for (int c0 = beg; c0 < end; c0 += kMergeChunk) {
     const int nch = min(kMergeChunk, end - c0);
-    __syncthreads();   // the previous pass has finished reading us / vs
-    // staging index x: entry e = 8 * (x / (8 rows)) + x % 8, so a wave gathers 8 entries of 8 rows
+    __syncthreads();   // the previous pass has finished reading us / vs / es / ea / eb
+    if ((int)threadIdx.x < nch) {
+      const int4 en = a.ent[c0 + threadIdx.x];
+      ea[threadIdx.x] = en.x;
+      eb[threadIdx.x] = en.y;
+      es[threadIdx.x] = a.scale * a.c[en.z];
+    }
+    __syncthreads();
+    // staging index x: entry e = 8 * (x / (8 rows)) + x % 8, so a wave gathers 8 entries of 8 rows;
+    // the loops are unrolled so that several independent frame loads are in flight per thread
     const int ngrp = (nch + 7) >> 3;
+#pragma unroll 8
     for (int x = threadIdx.x; x < ngrp * 8 * kMergeRows; x += kMergeThreads) {
       const int e = ((x / (8 * kMergeRows)) << 3) | (x & 7), u = (x >> 3) & (kMergeRows - 1);
-      if (e < nch && u0 + u < a.Wm) {
-        const int4 en = a.ent[c0 + e];
-        us[e * kMergeUS + u] = a.scale * a.c[en.z] * a.Bm[(long)(u0 + u) * a.Wm + en.x];
-      }
+      if (e < nch && u0 + u < a.Wm) us[e * kMergeUS + u] = es[e] * a.Bm[(long)(u0 + u) * a.Wm + ea[e]];
     }
+#pragma unroll 8
     for (int x = threadIdx.x; x < ngrp * 8 * kMergeCols; x += kMergeThreads) {
       const int e = ((x / (8 * kMergeCols)) << 3) | (x & 7), p = (x >> 3) & (kMergeCols - 1);
-      if (e < nch && p0 + p < a.Wn) vs[e * kMergeVS + p] = a.Bn[(long)(p0 + p) * a.Wn + a.ent[c0 + e].y];
+      if (e < nch && p0 + p < a.Wn) vs[e * kMergeVS + p] = a.Bn[(long)(p0 + p) * a.Wn + eb[e]];
     }
     __syncthreads();
     if (live) {

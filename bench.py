@@ -47,30 +47,72 @@ def algorithmic_bytes(T, n, m, nnz, esz):
     return fwd, bwd, red
 
 
-def cpu_baseline(wl, ad, data, budget_s=12.0):
-    """fp64 oracle fwd+bwd on the first S tokens of the same workload, single-threaded."""
+_CPU = {}   # oracle inputs shared with the forked CPU-baseline workers
+
+
+def _oracle_tokens(span):
+    """Oracle forward + backward (dX, dC) on tokens [lo, hi) of the benchmark workload, one thread."""
     from threadpoolctl import threadpool_limits
+    from oracle import frameft_oracle as O
+    lo, hi = span
+    c = _CPU
+    d = c["data"]
+    with threadpool_limits(limits=1):
+        O.adapter_fwd(c["P_in"], c["P_out"], d.rows, d.cols, d.vals, d.scale, d.X[lo:hi])
+        _, dc = O.adapter_bwd(c["P_in"], c["P_out"], d.rows, d.cols, d.vals, d.scale, d.X[lo:hi], d.G[lo:hi])
+    return dc
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, ad, data, budget_s=12.0):
+    """The fp64 oracle's forward + backward on the benchmark workload, on the host cores.
+
+    Runs before anything touches the GPU, so that worker processes can be forked.  The tokens are
+    split over one single-threaded worker process per core (at most 16, the host share of one
+    GPU); each runs the oracle unchanged on its share, and the dC parts are summed.  The sample is
+    the whole token batch, repeated while the budget allows; a single-thread figure on a prefix
+    is reported next to it."""
+    import multiprocessing as mp
     from oracle import frameft_oracle as O
     t0 = time.perf_counter()
     P_in = O.tight_fusion_frame(ad.k_in, ad.rho_in, ad.d_in)
     P_out = P_in if (ad.k_out, ad.rho_out, ad.d_out) == (ad.k_in, ad.rho_in, ad.d_in) else \
         O.tight_fusion_frame(ad.k_out, ad.rho_out, ad.d_out)
     setup = time.perf_counter() - t0
-    S, elapsed = 16, 0.0
-    with threadpool_limits(limits=1):
+    _CPU.update(P_in=P_in, P_out=P_out, data=data)
+    T = wl.tokens
+    # one thread on a prefix
+    S = min(T, 256)
+    t0 = time.perf_counter()
+    _oracle_tokens((0, S))
+    one = S / (time.perf_counter() - t0)
+    cores = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()))
+    spans = [(T * i // cores, T * (i + 1) // cores) for i in range(cores)]
+    with mp.get_context("fork").Pool(cores) as pool:
+        pool.map(_oracle_tokens, [(0, 1)] * cores)        # workers started before the clock
+        reps, t0 = 0, time.perf_counter()
         while True:
-            S = min(S, wl.tokens)
-            t0 = time.perf_counter()
-            O.adapter_fwd(P_in, P_out, data.rows, data.cols, data.vals, data.scale, data.X[:S])
-            O.adapter_bwd(P_in, P_out, data.rows, data.cols, data.vals, data.scale, data.X[:S], data.G[:S])
+            parts = pool.map(_oracle_tokens, spans)
+            reps += 1
             elapsed = time.perf_counter() - t0
-            if elapsed >= budget_s / 3 or S == wl.tokens:
+            if elapsed >= budget_s / 2 or reps >= 8:
                 break
-            S = int(S * max(2.0, min(8.0, (budget_s / 3) / max(elapsed, 1e-3))))
-    return {"value": round(S / elapsed, 2), "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {S} of {wl.tokens} tokens, fp64 scipy-sparse oracle fwd+bwd (dX, dC), "
-                      f"1 thread, frame construction ({setup:.1f} s) excluded",
-            "seconds": round(elapsed, 3)}
+    dc = np.sum(parts, axis=0)
+    assert dc.shape == (ad.nnz,) and np.all(np.isfinite(dc))
+    return {"value": round(reps * T / elapsed, 2), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"all {T} tokens x {reps}, fp64 scipy-sparse oracle fwd+bwd (dX, dC) split over {cores} "
+                      f"single-threaded processes; frame construction ({setup:.1f} s) excluded",
+            "seconds": round(elapsed, 3), "cpu_model": _cpu_model(),
+            "single_thread": {"value": round(one, 2), "sample": f"first {S} tokens, 1 thread"}}
 
 
 def bench_stack(args, torch, ff, inputs, dev):
@@ -176,7 +218,7 @@ def bench_stack(args, torch, ff, inputs, dev):
 
 def bench_merge(args, torch, ff, inputs, dev):
     """Merge into the frozen weight (Algorithm 1 steps 5-6): W = W + s P_out C P_in^T in place on
-    a bf16 m x n weight, alternating +s and -s (merge, then unmerge: the hot swap of Sec. 3.3).
+    a bf16 m x n weight, alternating +s and -s (merge, then unmerge: the hot swap of Sec. 3.4, "Storage efficiency").
 
     Algorithmic bytes per merge: read and write W (4 m n B for bf16) plus the coefficients
     (4 B each); the rank-1 work is nnz (2 k_out) (2 k_in) fused multiply-adds.  W0 is drawn on
@@ -237,7 +279,7 @@ FRAMEGEN_MODELS = {
 def bench_framegen(torch, ff, rho=64, reps=5):
     """Wall time of building every distinct frame one model's adapted projections need.
 
-    Frames depend only on (d, k, rho) and are shared across layers (Sec. 3.3), so a model needs one
+    Frames depend only on (d, k, rho) and are shared across layers (Sec. 3.4, "Memory Overhead"), so a model needs one
     frame per distinct dimension.  The paper's instruction-tuning runs use rho = 2 (a single dense
     block of width d per frame), which the GPU path does not take; rho = 64 is timed instead.
     """
@@ -270,6 +312,9 @@ def main():
     ap.add_argument("--stack", action="store_true",
                     help="time every adapter of every layer of the workload (the 7B stack) as batched calls")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sets", type=int, default=0,
+                    help="buffer sets rotated over the steps (0: enough to exceed 512 MiB; 1: one set, "
+                         "which may stay in the last-level cache)")
     ap.add_argument("--merge", action="store_true",
                     help="time the merge W += s P_out C P_in^T into the workload adapter's bf16 weight "
                          "(alternating +s and -s, the hot swap) instead of the training step")
@@ -286,9 +331,14 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    from paper_2608_26430_amd import inputs
+    cpu = None
+    if not (args.stack or args.framegen or args.merge or args.no_cpu_baseline):
+        wl = inputs.WORKLOADS[args.workload]
+        cpu = cpu_baseline(wl, wl.adapters[args.adapter], inputs.adapter_data(wl, wl.adapters[args.adapter]))
+
     import torch
     import paper_2608_26430_amd as ff
-    from paper_2608_26430_amd import inputs
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
@@ -323,44 +373,53 @@ def main():
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
 
-    X = torch.from_numpy(data.X).to(dev, tdt)
-    G = torch.from_numpy(data.G).to(dev, tdt)
-    c = torch.from_numpy(plan.to_plan(data.vals)).to(dev)      # plan layout (padded)
-    Y = torch.empty((T, m), dtype=tdt, device=dev)
-    dX = torch.empty((T, n), dtype=tdt, device=dev)
-    dC = torch.empty((plan.coef_slots,), dtype=torch.float32, device=dev)
+    # Buffer sets (X, G, Y, dX, c, dC and the saved copy) rotated from step to step, enough of them
+    # that the working set is well beyond the 256 MB last-level cache (Infinity Cache): each
+    # timed step then streams its activations from HBM, as a step over fresh data would.
+    set_bytes = esz * T * (2 * n + 2 * m)
+    nsets = 1 if args.sets == 1 else max(2, min(8, -(-(512 << 20) // set_bytes))) if args.sets == 0 else args.sets
+    X0 = torch.from_numpy(data.X).to(dev, tdt)
+    G0 = torch.from_numpy(data.G).to(dev, tdt)
+    c0 = torch.from_numpy(plan.to_plan(data.vals)).to(dev)      # plan layout (padded)
+    sets = [dict(X=X0.clone(), G=G0.clone(), c=c0.clone(), Y=torch.empty((T, m), dtype=tdt, device=dev),
+                 dX=torch.empty((T, n), dtype=tdt, device=dev),
+                 dC=torch.empty((plan.coef_slots,), dtype=torch.float32, device=dev),
+                 # a training step: the forward also leaves the coefficients in the backward's order
+                 saved=plan.new_saved(dev)) for _ in range(nsets)]
+    del X0, G0
 
-    # a training step: the forward also leaves the coefficients in the backward's order
-    saved = plan.new_saved(dev)
-
-    def step(evs=None):
+    def step(i, evs=None):
+        b = sets[i % nsets]
         if evs is not None:
             ff.binding.time_next_kernel(evs[0], evs[1])
-        ff.adapter_fwd(plan, X, c, data.scale, Y=Y, save=saved)
+        ff.adapter_fwd(plan, b["X"], b["c"], data.scale, Y=b["Y"], save=b["saved"])
         if evs is not None:
             ff.binding.time_next_kernel(evs[2], evs[3])
-        ff.adapter_bwd(plan, X, G, c, data.scale, dX=dX, dC=dC, saved=saved)
+        ff.adapter_bwd(plan, b["X"], b["G"], b["c"], data.scale, dX=b["dX"], dC=b["dC"], saved=b["saved"])
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    def timed(steps, first):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        start.record()
+        for i in range(steps):
+            step(first(i))
+        stop.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / steps, (time.perf_counter() - w0) * 1e3
 
-    # timed region: K whole steps, no per-kernel events (step time)
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for i in range(args.warmup):
+        step(i)
     torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    start.record()
-    for _ in range(args.steps):
-        step()
-    stop.record()
-    torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - w0) * 1e3
-    ms_per_step = start.elapsed_time(stop) / args.steps
+    # timed region: K whole steps over the rotated sets, no per-kernel events (step time)
+    ms_per_step, wall_ms = timed(args.steps, lambda i: i)
+    # context: the same steps on one set, whose 128 MB may stay partly in the last-level cache
+    ms_warm, _ = timed(args.steps, lambda i: 0)
 
-    # per-kernel durations: the same steps with events around the fused kernels
+    # per-kernel durations: the same rotated steps with events around the fused kernels
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    for e in evs:
-        step(e)
+    for i, e in enumerate(evs):
+        step(i, e)
     torch.cuda.synchronize()
     fwd_us = 1e3 * float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     bwd_us = 1e3 * float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
@@ -382,13 +441,14 @@ def main():
 
     # context: the frozen W0 GEMM of this layer through the vendor BLAS (not part of the step)
     W0 = torch.randn((m, n), device=dev, dtype=tdt)
+    Xg = sets[0]["X"]
     for _ in range(3):
-        torch.matmul(X, W0.t())
+        torch.matmul(Xg, W0.t())
     torch.cuda.synchronize()
     g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     g0.record()
     for _ in range(10):
-        torch.matmul(X, W0.t())
+        torch.matmul(Xg, W0.t())
     g1.record()
     torch.cuda.synchronize()
     gemm_us = 1e3 * g0.elapsed_time(g1) / 10
@@ -408,12 +468,15 @@ def main():
                                                                        / HBM_PEAK_GBS, 4),
                           "fwd_kernel_us": round(fwd_us, 3), "bwd_kernel_us": round(bwd_us, 3)},
         "context": {"w0_gemm_us": round(gemm_us, 2), "setup_s": round(setup_s, 3),
-                    "wall_ms_timed": round(wall_ms, 3),
+                    "wall_ms_timed": round(wall_ms, 3), "buffer_sets": nsets,
+                    "buffer_set_mb": round(set_bytes / 1e6, 1),
+                    "one_set_ms_per_step": round(ms_warm, 5),
+                    "one_set_tokens_per_s": round(T / (ms_warm * 1e-3), 1),
                     "tile_tokens": plan.tile_tokens(wl.dtype), "input_chunks": plan.gen_chunks,
                     "chunk_tile_tokens": plan.gen_tile_tokens(wl.dtype), "kernel_hash": kernel_hash()},
     }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, ad, data)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
 
 

@@ -6,5 +6,6 @@ load the library; the first call does, and fails loudly if it is missing.
 """
 from .binding import (  # noqa: F401
     Frame, Plan, FrameFTError, framegen, tff_host, plan_create, adapter_fwd,
-    adapter_bwd, merge_delta, adapter_fwd_batched, adapter_bwd_batched, library_path,
+    adapter_bwd, merge_delta, adapter_fwd_batched, adapter_bwd_batched, coef_to_plan,
+    coef_to_user, library_path,
 )

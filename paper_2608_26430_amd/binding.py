@@ -66,6 +66,8 @@ def _load():
         "ff_adapter_bwd_batched": (i32, [vp, i64, i64, i32, vp, i64, vp, i64, vp, f32, f32, vp, i64, i32,
                                          vp, vp]),
         "ff_time_next_kernel": (i32, [vp, vp]),
+        "ff_coef_to_plan": (i32, [vp, vp, vp, vp]),
+        "ff_coef_to_user": (i32, [vp, vp, vp, i32, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -348,6 +350,30 @@ def adapter_bwd(plan: Plan, X, G, c_vals, scale: float, dX=None, dC=None, beta_d
     return (dX if want_dx else None), (dC if want_dc else None)
 
 
+def coef_to_plan(plan: Plan, c_user, c_plan=None, stream=None):
+    """Device user-order coefficients (nnz fp32) -> plan layout (Plan.coef_slots, zero padding),
+    on the device (ff_coef_to_plan); returns c_plan."""
+    torch = _torch()
+    if c_plan is None:
+        c_plan = torch.empty((plan.coef_slots,), dtype=torch.float32, device=c_user.device)
+    _check(_load().ff_coef_to_plan(plan.handle, _vec(c_user, "c_user", plan.nnz),
+                                   _vec(c_plan, "c_plan", plan.coef_slots), _stream(stream)))
+    return c_plan
+
+
+def coef_to_user(plan: Plan, c_plan, c_user=None, accumulate: bool = False, stream=None):
+    """Device plan-layout array (Plan.coef_slots) -> user order (nnz), added to c_user when
+    accumulate (ff_coef_to_user); returns c_user."""
+    torch = _torch()
+    if c_user is None:
+        if accumulate:
+            raise ValueError("accumulate needs an existing c_user")
+        c_user = torch.empty((plan.nnz,), dtype=torch.float32, device=c_plan.device)
+    _check(_load().ff_coef_to_user(plan.handle, _vec(c_plan, "c_plan", plan.coef_slots),
+                                   _vec(c_user, "c_user", plan.nnz), int(accumulate), _stream(stream)))
+    return c_user
+
+
 def merge_delta(plan: Plan, c_vals, scale: float, W, beta: float = 1.0, stream=None):
     """W = beta*W + scale * P_out C P_in^T in place; returns W."""
     torch = _torch()
@@ -393,11 +419,13 @@ def adapter_bwd_batched(plan: Plan, Xs: Sequence, Gs: Sequence, cs: Sequence, sc
     if ptrs is not None:
         px, pg, pc, pdx, pdc = ptrs
     else:
-        px, pg, pc = pointer_array(Xs, dev), pointer_array(Gs, dev), pointer_array(cs, dev)
+        px, pg = pointer_array(Xs, dev), pointer_array(Gs, dev)
+        pc = pointer_array(cs, dev) if cs is not None else None     # not needed without dX
         pdx = pointer_array(dXs, dev) if dXs is not None else None
         pdc = pointer_array(dCs, dev) if dCs is not None else None
     _check(_load().ff_adapter_bwd_batched(plan.handle, count, T, _act_code(Gs[0]), px.data_ptr(), ldx,
-                                          pg.data_ptr(), ldg, pc.data_ptr(), scale, beta_dx,
+                                          pg.data_ptr(), ldg, pc.data_ptr() if pc is not None else None,
+                                          scale, beta_dx,
                                           pdx.data_ptr() if pdx is not None else None, lddx,
                                           int(accumulate_dc), pdc.data_ptr() if pdc is not None else None,
                                           _stream(stream)))

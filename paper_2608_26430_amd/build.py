@@ -15,7 +15,12 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libframeft.so")
-SOURCES = ["capi.cpp", "framegen.cpp", "plan.cpp", "kernels.hip", "kernels_w128.hip"]
+# (source, object name, extra flags): the generic kernels are instantiated by one source compiled
+# once per direction and activation type, so that their long compiles run in parallel
+SOURCES = [("capi.cpp", "capi.cpp.o", []), ("framegen.cpp", "framegen.cpp.o", []), ("plan.cpp", "plan.cpp.o", []),
+           ("kernels.hip", "kernels.hip.o", []), ("kernels_w128.hip", "kernels_w128.hip.o", [])] + [
+    ("gen_inst.hip", f"gen_{d}_{t}.o", [f"-DGEN_BWD={int(d == 'bwd')}", f"-DGEN_BF16={int(t == 'bf16')}"])
+    for d in ("bwd", "fwd") for t in ("bf16", "f32")]
 
 ARCH = "gfx950"
 COMMON = [
@@ -34,9 +39,10 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [hipcc(), *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(entry) -> str:
+    src, name, flags = entry
+    obj = os.path.join(BUILD_DIR, name)
+    cmd = [hipcc(), *COMMON, *flags, "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -52,7 +58,7 @@ def _compile(src: str) -> str:
 def build(verbose: bool = True) -> str:
     """Compile every source and link libframeft.so; always rebuilds."""
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
+    with cf.ThreadPoolExecutor(max_workers=min(max(2, (os.cpu_count() or 4) - 1), len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,--no-undefined", *objs, "-o", tmp]

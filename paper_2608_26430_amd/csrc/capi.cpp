@@ -68,6 +68,32 @@ ff_status launched(hipError_t e, const char* what) {
   return FF_OK;
 }
 
+// Argument checks of a single-adapter backward.  Sets *done when the call has nothing to launch.
+ff_status check_bwd(const ff_plan* p, int64_t T, int act, const void* X, int64_t ldx, const void* G, int64_t ldg,
+                    const float* c_vals, void* dX, int64_t lddx, int accumulate_dc, float* dC, bool* want_dx,
+                    bool* want_dc, bool* done) {
+  ff_status st = check_common(p, T, act, 1);
+  if (st != FF_OK) return st;
+  *want_dx = dX != nullptr;
+  *want_dc = dC != nullptr && p->coef_slots > 0;
+  *done = false;
+  if (dC && ((uintptr_t)dC % 4)) return ff::fail(FF_EINVAL, "dC is not 4-byte aligned");
+  if (T == 0) {
+    *done = !*want_dc || accumulate_dc;               // empty sum: dC = 0 unless accumulating
+    return FF_OK;
+  }
+  if (!*want_dx && !*want_dc) {
+    *done = true;
+    return FF_OK;
+  }
+  if ((st = check_act("G", G, ldg, p->fout->d, act)) != FF_OK) return st;
+  if (*want_dc && (st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
+  if (*want_dx && (st = check_act("dX", dX, lddx, p->fin->d, act)) != FF_OK) return st;
+  if (*want_dx && p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
+  if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
+  return FF_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -137,20 +163,10 @@ ff_status ff_adapter_bwd(const ff_plan* p, int64_t T, int act, const void* X, in
                          float beta_dx, void* dX, int64_t lddx, int accumulate_dc, float* dC,
                          void* stream) {
   ff::clear_error();
-  ff_status st = check_common(p, T, act, 1);
-  if (st != FF_OK) return st;
-  const bool want_dx = dX != nullptr, want_dc = dC != nullptr && p->coef_slots > 0;
-  if (dC && ((uintptr_t)dC % 4)) return ff::fail(FF_EINVAL, "dC is not 4-byte aligned");
-  if (T == 0) {
-    if (!want_dc || accumulate_dc) return FF_OK;       // empty sum: dC = 0 unless accumulating
-  } else {
-    if (!want_dx && !want_dc) return FF_OK;
-    if ((st = check_act("G", G, ldg, p->fout->d, act)) != FF_OK) return st;
-    if (want_dc && (st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
-    if (want_dx && (st = check_act("dX", dX, lddx, p->fin->d, act)) != FF_OK) return st;
-    if (want_dx && p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
-    if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
-  }
+  bool want_dx, want_dc, done;
+  const ff_status st = check_bwd(p, T, act, X, ldx, G, ldg, c_vals, dX, lddx, accumulate_dc, dC, &want_dx, &want_dc,
+                                 &done);
+  if (st != FF_OK || done) return st;
   return launched(ff::launch_bwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, {G, nullptr}, ldg, c_vals,
                                  nullptr, scale, beta_dx, {dX, nullptr}, lddx, want_dx, accumulate_dc, dC,
                                  nullptr, want_dc, nullptr, (hipStream_t)stream),
@@ -191,6 +207,32 @@ ff_status ff_merge_delta(const ff_plan* p, const float* c_vals, float scale, int
   if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
   return launched(ff::launch_merge(p, c_vals, scale, w_dtype == FF_BF16, beta, W, ldw, (hipStream_t)stream),
                   "merge launch");
+}
+
+ff_status ff_coef_to_plan(const ff_plan* p, const float* c_user, float* c_plan, void* stream) {
+  ff::clear_error();
+  ff_status st = check_common(p, 0, FF_F32, 1);
+  if (st != FF_OK) return st;
+  if (p->coef_slots == 0) return FF_OK;
+  if (!c_plan || (uintptr_t)c_plan % 16) return ff::fail(FF_EINVAL, "c_plan is NULL or not 16-byte aligned");
+  if (p->nnz > 0 && (!c_user || (uintptr_t)c_user % 4)) return ff::fail(FF_EINVAL, "c_user is NULL or misaligned");
+  if (p->nnz > 0 && (const void*)c_user < (const void*)(c_plan + p->coef_slots) &&
+      (const void*)c_plan < (const void*)(c_user + p->nnz))
+    return ff::fail(FF_EINVAL, "c_user and c_plan overlap");
+  return launched(ff::launch_coef_to_plan(p, c_user, c_plan, (hipStream_t)stream), "coefficient layout launch");
+}
+
+ff_status ff_coef_to_user(const ff_plan* p, const float* c_plan, float* c_user, int accumulate, void* stream) {
+  ff::clear_error();
+  ff_status st = check_common(p, 0, FF_F32, 1);
+  if (st != FF_OK) return st;
+  if (p->nnz == 0) return FF_OK;
+  if (!c_plan || (uintptr_t)c_plan % 16) return ff::fail(FF_EINVAL, "c_plan is NULL or not 16-byte aligned");
+  if (!c_user || (uintptr_t)c_user % 4) return ff::fail(FF_EINVAL, "c_user is NULL or misaligned");
+  if ((const void*)c_user < (const void*)(c_plan + p->coef_slots) && (const void*)c_plan < (const void*)(c_user + p->nnz))
+    return ff::fail(FF_EINVAL, "c_user and c_plan overlap");
+  return launched(ff::launch_coef_to_user(p, c_plan, c_user, accumulate, (hipStream_t)stream),
+                  "coefficient layout launch");
 }
 
 ff_status ff_adapter_fwd_batched(const ff_plan* p, int64_t count, int64_t T, int act,

@@ -94,6 +94,9 @@ struct PlanDev {
   const int4* mrg_ent;       // (local row a', local column b', coefficient slot, 0)
   int mrg_max_bucket;
   int nnz;                   // coefficient slots (nnz plus padding)
+  const int* user_of_slot;   // [coefficient slots]: user index of the slot's entry, -1 for padding
+  const int* slot_of_user;   // [support entries]: coefficient slot of user entry e
+  int nnz_user;              // support entries
   float* c_fwd;              // [batch][64 fwd.rows]: coefficients in forward order (fwd_by_pos == 0)
   float* c_bwd;              // [batch][64 bwd.rows]: coefficients in backward stream order
 };
@@ -190,6 +193,12 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
                       float* dC, float* const* dCs, bool want_dc, const float* c_saved, hipStream_t s);
 hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf16, float beta,
                         void* W, int64_t ldw, hipStream_t s);
+// Coefficient vectors between the caller's support order and the plan layout (Algorithm 1,
+// step 4): to_plan writes every slot (zero in padding slots), to_user every user entry (added to
+// the old value when accumulate).
+hipError_t launch_coef_to_plan(const ff_plan* p, const float* c_user, float* c_plan, hipStream_t s);
+hipError_t launch_coef_to_user(const ff_plan* p, const float* c_plan, float* c_user, int accumulate,
+                               hipStream_t s);
 // Set the per-kernel dynamic LDS limits once per process.
 hipError_t configure_kernels();
 

@@ -20,840 +20,12 @@
 //   dc_reduce     dC[j] = [dC[j] +] s * sum_tiles partial[tile][j]   (fixed order, per coefficient slot)
 //   merge_kernel  W = beta W + s P_out C P_in^T, per (output block, input block)
 //                 tile as a sum of rank-1 products of block columns.
-#include <algorithm>
-
-#include "ff_internal.h"
+#include "gen_kernels.h"
 
 namespace ff {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned short u16;
-
-// Accesses to global memory go through global-address-space pointers, so that they compile to
-// global rather than flat instructions: a flat access also counts against the LDS counter, and a
-// wait for an LDS read would then wait for every global load in flight.
-#define FF_GLOBAL __attribute__((address_space(1)))
-// (HIP's vector types cannot be accessed through such pointers; they move as raw words.)
-typedef unsigned raw2 __attribute__((ext_vector_type(2)));
-typedef unsigned raw4 __attribute__((ext_vector_type(4)));
-template <int N> struct Raw;
-template <> struct Raw<2> { using T = unsigned short; };
-template <> struct Raw<4> { using T = unsigned; };
-template <> struct Raw<8> { using T = raw2; };
-template <> struct Raw<16> { using T = raw4; };
-template <class T>
-__device__ __forceinline__ T gload(const T* p) {
-  using R = typename Raw<sizeof(T)>::T;
-  return __builtin_bit_cast(T, *(const FF_GLOBAL R*)p);
-}
-template <class T>
-__device__ __forceinline__ void gstore(T* p, const T& v) {
-  using R = typename Raw<sizeof(T)>::T;
-  *(FF_GLOBAL R*)p = __builtin_bit_cast(R, v);
-}
-
-__device__ __forceinline__ float bf2f(u16 h) { return __uint_as_float((unsigned)h << 16); }
-
-// fp32 -> bf16, round to nearest even (NaN kept quiet).
-__device__ __forceinline__ u16 f2bf(float f) {
-  unsigned u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (u16)(u >> 16);
-}
-
-template <bool BF16>
-struct Act;
-
-template <>
-struct Act<true> {
-  using E = u16;
-  static __device__ __forceinline__ float ld(const E* p) { return bf2f(*p); }
-  static __device__ __forceinline__ void st(E* p, float v) { *p = f2bf(v); }
-  static __device__ __forceinline__ f32x4 ld4(const E* p) { return unpack4(*reinterpret_cast<const uint2*>(p)); }
-  static __device__ __forceinline__ void st4(E* p, f32x4 v) { *reinterpret_cast<uint2*>(p) = pack4(v); }
-  static __device__ __forceinline__ f32x4 gld4(const E* p) { return unpack4(gload(reinterpret_cast<const uint2*>(p))); }
-  static __device__ __forceinline__ void gst4(E* p, f32x4 v) { gstore(reinterpret_cast<uint2*>(p), pack4(v)); }
-  static __device__ __forceinline__ uint2 pack4(f32x4 v) {
-    uint2 w;
-    w.x = (unsigned)f2bf(v[0]) | ((unsigned)f2bf(v[1]) << 16);
-    w.y = (unsigned)f2bf(v[2]) | ((unsigned)f2bf(v[3]) << 16);
-    return w;
-  }
-  static __device__ __forceinline__ f32x4 unpack4(uint2 w) {
-    return f32x4{bf2f((u16)(w.x & 0xffff)), bf2f((u16)(w.x >> 16)), bf2f((u16)(w.y & 0xffff)),
-                 bf2f((u16)(w.y >> 16))};
-  }
-};
-
-template <>
-struct Act<false> {
-  using E = float;
-  static __device__ __forceinline__ float ld(const E* p) { return *p; }
-  static __device__ __forceinline__ void st(E* p, float v) { *p = v; }
-  static __device__ __forceinline__ f32x4 ld4(const E* p) { return *reinterpret_cast<const f32x4*>(p); }
-  static __device__ __forceinline__ void st4(E* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
-  static __device__ __forceinline__ f32x4 gld4(const E* p) { return gload(reinterpret_cast<const f32x4*>(p)); }
-  static __device__ __forceinline__ void gst4(E* p, f32x4 v) { gstore(reinterpret_cast<f32x4*>(p), v); }
-};
-
-// ---------------------------------------------------------------------------------------------
-// Frame application.  A "column" is one vector the frame's MFMA matrix M (W2 x W2: the block
-// B or B^T, or for factored frames the size-k/4 DFT of the radix-4 split) is applied to: the
-// inputs of one (token, block) for dense frames, of one (token, block, residue) for factored
-// ones.  Sixteen columns form the B operand of v_mfma_f32_16x16x32_bf16 (16x16x4 for fp32);
-// lane l holds column l % 16 and contraction elements 8 (l / 16) .. +7 of each step (4 for fp32).
-// Inputs at or past `lim` (the column's storage length) are taken as zero; M is zero there too.
-
-template <bool BF16>
-struct Mfma;
-
-template <>
-struct Mfma<true> {
-  using V = bf16x8;
-  static constexpr int KS = 32, VL = 8;   // contraction per step, elements per lane and step
-  static __device__ __forceinline__ f32x4 step(const V& a, const V& b, f32x4 acc) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
-  }
-};
-
-template <>
-struct Mfma<false> {
-  using V = f32x4;
-  static constexpr int KS = 16, VL = 4;
-  static __device__ __forceinline__ f32x4 step(const V& a, const V& b, f32x4 acc) {
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], acc, 0, 0, 0);
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], acc, 0, 0, 0);
-  }
-};
-
-// This lane's contraction inputs of step ks for a column whose storage starts at `in`.
-template <bool BF16, bool GSRC>
-__device__ __forceinline__ typename Mfma<BF16>::V load_operand(const typename Act<BF16>::E* in, bool ok, int lim,
-                                                               int ks, int q) {
-  using M = Mfma<BF16>;
-  using V = typename M::V;
-  V b{};
-  const int i0 = ks * M::KS + q * M::VL;
-  if (ok && i0 < lim) b = GSRC ? gload(reinterpret_cast<const V*>(in + i0)) : *reinterpret_cast<const V*>(in + i0);
-  return b;
-}
-
-// Every column c < ncols: epi(c, o, acc) receives outputs o..o+3 (o = 16 mt + 4 (lane / 16)) of
-// M applied to the column starting at col(c).  The MT x KT fragments of M stay in registers for
-// the whole call; each wave takes every nw-th group of 16 columns and loads the next group's
-// inputs while it multiplies the current one.
-template <bool BF16, bool GSRC, int MT, int KT, class Col, class Epi>
-__device__ __forceinline__ void column_apply_reg(const void* frag, int ncols, int lim, Col col, Epi epi) {
-  using M = Mfma<BF16>;
-  using V = typename M::V;
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
-            q = lane >> 4;
-  const int ngrp = (ncols + 15) / 16;
-  if (wave >= ngrp) return;
-  const V* fr = reinterpret_cast<const V*>(frag);
-  // opaque at every call, so that a caller's loop does not keep the fragments of all its frame
-  // applies live across iterations (they would not fit in registers)
-  asm volatile("" : "+s"(fr));
-  V fa[MT][KT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int ks = 0; ks < KT; ++ks) fa[mt][ks] = gload(&fr[(mt * KT + ks) * 64 + lane]);
-  // two operand buffers used in turn (no copies, which would wait for the loads in flight)
-  V ba[KT], bb[KT];
-  auto load = [&](int g, V (&b)[KT]) {
-    const int c = g * 16 + (lane & 15);
-    const bool ok = c < ncols;
-    const auto* in = col(ok ? c : 0);
-#pragma unroll
-    for (int ks = 0; ks < KT; ++ks) b[ks] = load_operand<BF16, GSRC>(in, ok, lim, ks, q);
-  };
-  auto mul = [&](int g, const V (&b)[KT]) {
-    f32x4 acc[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KT; ++ks)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[mt] = M::step(fa[mt][ks], b[ks], acc[mt]);
-    const int c = g * 16 + (lane & 15);
-    if (c < ncols) {
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) epi(c, 16 * mt + 4 * q, acc[mt]);
-    }
-  };
-  load(wave, ba);
-  for (int g = wave; g < ngrp; g += 2 * nw) {
-    if (g + nw < ngrp) load(g + nw, bb);
-    mul(g, ba);
-    if (g + nw >= ngrp) break;
-    if (g + 2 * nw < ngrp) load(g + 2 * nw, ba);
-    mul(g + nw, bb);
-  }
-}
-
-// The same for matrices too large to keep in registers: fragments are read from memory (L1 / L2)
-// for every group, four output tiles at a time.  With at most kPre contraction steps a column's
-// inputs are all loaded before its first output is stored, so the column may be transformed in
-// place (factored frames always qualify: W2 <= 128); longer contractions reload them per output
-// chunk and need a separate destination.
-template <bool BF16, bool GSRC, class Col, class Epi>
-__device__ __forceinline__ void column_apply_mem(const void* frag, int MT, int KT, int ncols, int lim, Col col,
-                                                 Epi epi) {
-  using M = Mfma<BF16>;
-  using V = typename M::V;
-  constexpr int kC = 4, kPre = 8;
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
-            q = lane >> 4;
-  const int ngrp = (ncols + 15) / 16;
-  const V* fr = reinterpret_cast<const V*>(frag);
-  const bool pre = KT <= kPre;
-  for (int g = wave; g < ngrp; g += nw) {
-    const int c = g * 16 + (lane & 15);
-    const bool ok = c < ncols;
-    const auto* in = col(ok ? c : 0);
-    V bp[kPre];
-    if (pre) {
-#pragma unroll
-      for (int ks = 0; ks < kPre; ++ks) bp[ks] = ks < KT ? load_operand<BF16, GSRC>(in, ok, lim, ks, q) : V{};
-    }
-    for (int mt0 = 0; mt0 < MT; mt0 += kC) {
-      f32x4 acc[kC];
-#pragma unroll
-      for (int j = 0; j < kC; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int ks = 0; ks < KT; ++ks) {
-        V b;
-        if (pre) {
-          b = bp[0];
-#pragma unroll
-          for (int j = 1; j < kPre; ++j)
-            if (ks == j) b = bp[j];
-        } else {
-          b = load_operand<BF16, GSRC>(in, ok, lim, ks, q);
-        }
-#pragma unroll
-        for (int j = 0; j < kC; ++j) {
-          const V a = gload(&fr[((size_t)min(mt0 + j, MT - 1) * KT + ks) * 64 + lane]);
-          if (mt0 + j < MT) acc[j] = M::step(a, b, acc[j]);
-        }
-      }
-      if (ok) {
-#pragma unroll
-        for (int j = 0; j < kC; ++j)
-          if (mt0 + j < MT) epi(c, 16 * (mt0 + j) + 4 * q, acc[j]);
-      }
-    }
-  }
-}
-
-// Dispatch on the matrix shape: register-resident for the shapes the frames here produce.
-template <bool BF16, bool GSRC, class Col, class Epi>
-__device__ __forceinline__ void column_apply(const FrameDev& f, bool synth, int ncols, int lim, Col col, Epi epi) {
-  const void* frag = BF16 ? (synth ? f.fs16 : f.fa16) : (synth ? f.fs32 : f.fa32);
-  const int KT = BF16 ? f.KT : f.KT4;
-#define FF_SHAPE(mt, kt)                                                       \
-  case (mt) * 64 + (kt):                                                       \
-    column_apply_reg<BF16, GSRC, mt, kt>(frag, ncols, lim, col, epi);          \
-    return;
-  if constexpr (BF16) {
-    switch (f.MT * 64 + KT) {
-      FF_SHAPE(1, 1) FF_SHAPE(2, 1) FF_SHAPE(3, 2) FF_SHAPE(4, 2) FF_SHAPE(5, 3) FF_SHAPE(6, 3)
-      FF_SHAPE(7, 4) FF_SHAPE(8, 4)
-      default: break;
-    }
-  } else {
-    switch (f.MT * 64 + KT) {
-      FF_SHAPE(1, 1) FF_SHAPE(2, 2) FF_SHAPE(3, 3) FF_SHAPE(4, 4) FF_SHAPE(5, 5) FF_SHAPE(6, 6)
-      default: break;
-    }
-  }
-#undef FF_SHAPE
-  column_apply_mem<BF16, GSRC>(frag, f.MT, KT, ncols, lim, col, epi);
-}
-
-// Two consecutive activations (one complex coordinate) as fp32, and back.
-template <bool BF16>
-__device__ __forceinline__ float2 ld2(const typename Act<BF16>::E* p) {
-  if constexpr (BF16) {
-    const unsigned w = *reinterpret_cast<const unsigned*>(p);
-    return make_float2(bf2f((u16)(w & 0xffff)), bf2f((u16)(w >> 16)));
-  } else {
-    return *reinterpret_cast<const float2*>(p);
-  }
-}
-template <bool BF16>
-__device__ __forceinline__ void st2(typename Act<BF16>::E* p, float2 v) {
-  if constexpr (BF16)
-    *reinterpret_cast<unsigned*>(p) = (unsigned)f2bf(v.x) | ((unsigned)f2bf(v.y) << 16);
-  else
-    *reinterpret_cast<float2*>(p) = v;
-}
-template <bool BF16>
-__device__ __forceinline__ float2 gld2(const typename Act<BF16>::E* p) {
-  if constexpr (BF16) {
-    const unsigned w = gload(reinterpret_cast<const unsigned*>(p));
-    return make_float2(bf2f((u16)(w & 0xffff)), bf2f((u16)(w >> 16)));
-  } else {
-    return gload(reinterpret_cast<const float2*>(p));
-  }
-}
-template <bool BF16>
-__device__ __forceinline__ void gst2(typename Act<BF16>::E* p, float2 v) {
-  if constexpr (BF16)
-    gstore(reinterpret_cast<unsigned*>(p), (unsigned)f2bf(v.x) | ((unsigned)f2bf(v.y) << 16));
-  else
-    gstore(reinterpret_cast<float2*>(p), v);
-}
-__device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
-__device__ __forceinline__ float2 csub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
-// a * (c + i s) and a * (c - i s)
-__device__ __forceinline__ float2 cmul(float2 a, float2 w) {
-  return make_float2(fmaf(a.x, w.x, -a.y * w.y), fmaf(a.y, w.x, a.x * w.y));
-}
-__device__ __forceinline__ float2 cmulc(float2 a, float2 w) {
-  return make_float2(fmaf(a.x, w.x, a.y * w.y), fmaf(a.y, w.x, -a.x * w.y));
-}
-
-// x / d for 0 <= x < 2^24 and 0 < d, with inv = 1 / d in fp32: the product is within one of the
-// quotient, which the two corrections make exact.
-__device__ __forceinline__ int div_small(int x, int d, float inv) {
-  int q = (int)((float)x * inv);
-  q -= q * d > x;
-  q += (q + 1) * d <= x;
-  return q;
-}
-
-// The twiddle factors of a factored frame, copied to LDS (the caller synchronizes).
-__device__ __forceinline__ void stage_twiddles(const FrameDev& f, float2* lds) {
-  if (f.radix == 1) return;
-  const float2* tw = (f.tw);
-  for (int i = threadIdx.x; i < 3 * f.k2; i += blockDim.x) lds[i] = gload(&tw[i]);
-}
-
-// Radix-4 stage of the factored analysis for every (token, block, b < k2) of a tile:
-// Y_a'[b] = w^(-a' b) sum_a X[a k2 + b] (-i)^(a a'), read from the token rows at src and written
-// to column a' of the block in the LDS tile (which also gets its padding zeroed).  A thread takes
-// kRB items at a time with all their loads issued first.
-constexpr int kRB = 8;
-
-template <bool BF16>
-__device__ __forceinline__ void radix4_analysis(const FrameDev& f, const float2* tw, int nt,
-                                                const typename Act<BF16>::E* src, long ld,
-                                                typename Act<BF16>::E* dst, int ldt, int ldb) {
-  using E = typename Act<BF16>::E;
-  const int k2 = f.k2, W = f.W, cs = f.cs, W2 = f.W2;
-  const int per_tok = f.nblk * k2, items = nt * per_tok;
-  const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
-  for (int it0 = threadIdx.x; it0 < items; it0 += kRB * blockDim.x) {
-    float2 x[kRB][4], w[kRB][3];
-    int b[kRB];
-    E* y[kRB];
-#pragma unroll
-    for (int u = 0; u < kRB; ++u) {
-      const int it = min(it0 + u * (int)blockDim.x, items - 1);   // past the end: a repeat, not stored
-      const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
-      b[u] = r - blk * k2;
-      const E* xp = src + (long)t * ld + blk * W + 2 * b[u];
-#pragma unroll
-      for (int a = 0; a < 4; ++a) x[u][a] = gld2<BF16>(xp + 2 * a * k2);
-#pragma unroll
-      for (int a = 0; a < 3; ++a) w[u][a] = tw[a * k2 + b[u]];
-      y[u] = dst + t * ldt + blk * ldb + 2 * b[u];
-    }
-#pragma unroll
-    for (int u = 0; u < kRB; ++u) {
-      if (it0 + u * (int)blockDim.x >= items) break;
-      const float2 s02 = cadd(x[u][0], x[u][2]), d02 = csub(x[u][0], x[u][2]);
-      const float2 s13 = cadd(x[u][1], x[u][3]), d13 = csub(x[u][1], x[u][3]);
-      const float2 y1 = make_float2(d02.x + d13.y, d02.y - d13.x);   // d02 - i d13
-      const float2 y3 = make_float2(d02.x - d13.y, d02.y + d13.x);   // d02 + i d13
-      st2<BF16>(y[u], cadd(s02, s13));
-      st2<BF16>(y[u] + cs, cmulc(y1, w[u][0]));
-      st2<BF16>(y[u] + 2 * cs, cmulc(csub(s02, s13), w[u][1]));
-      st2<BF16>(y[u] + 3 * cs, cmulc(y3, w[u][2]));
-      if (b[u] == 0)
-        for (int a = 0; a < 4; ++a)
-          for (int e = W2; e < cs; ++e) Act<BF16>::st(y[u] + a * cs + e, 0.f);
-    }
-  }
-}
-
-// Radix-4 stage of the factored synthesis: X[a k2 + b] = sum_a' i^(a a') w^(a' b) Y'_a'[b] from
-// the LDS tile, then out = s X (+ beta out) into the token rows at dst.
-template <bool BF16>
-__device__ __forceinline__ void radix4_synthesis(const FrameDev& f, const float2* tw, int nt,
-                                                 const typename Act<BF16>::E* src, int ldt, int ldb,
-                                                 typename Act<BF16>::E* dst, long ld, float s, float beta) {
-  using E = typename Act<BF16>::E;
-  const int k2 = f.k2, W = f.W, cs = f.cs;
-  const int per_tok = f.nblk * k2, items = nt * per_tok;
-  const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
-  for (int it0 = threadIdx.x; it0 < items; it0 += kRB * blockDim.x) {
-    float2 yv[kRB][4], w[kRB][3];
-    E* out[kRB];
-#pragma unroll
-    for (int u = 0; u < kRB; ++u) {
-      const int it = min(it0 + u * (int)blockDim.x, items - 1);
-      const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
-      const int b = r - blk * k2;
-      const E* yp = src + t * ldt + blk * ldb + 2 * b;
-#pragma unroll
-      for (int a = 0; a < 4; ++a) yv[u][a] = ld2<BF16>(yp + a * cs);
-#pragma unroll
-      for (int a = 0; a < 3; ++a) w[u][a] = tw[a * k2 + b];
-      out[u] = dst + (long)t * ld + blk * W + 2 * b;
-    }
-#pragma unroll
-    for (int u = 0; u < kRB; ++u) {
-      if (it0 + u * (int)blockDim.x >= items) break;
-      const float2 y0 = yv[u][0], y1 = cmul(yv[u][1], w[u][0]), y2 = cmul(yv[u][2], w[u][1]),
-                   y3 = cmul(yv[u][3], w[u][2]);
-      const float2 s02 = cadd(y0, y2), d02 = csub(y0, y2), s13 = cadd(y1, y3), d13 = csub(y1, y3);
-      float2 xo[4];
-      xo[0] = cadd(s02, s13);
-      xo[2] = csub(s02, s13);
-      xo[1] = make_float2(d02.x - d13.y, d02.y + d13.x);   // d02 + i d13
-      xo[3] = make_float2(d02.x + d13.y, d02.y - d13.x);   // d02 - i d13
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        float2 v = make_float2(s * xo[a].x, s * xo[a].y);
-        if (beta != 0.f) {
-          const float2 old = gld2<BF16>(out[u] + 2 * a * k2);
-          v.x = fmaf(beta, old.x, v.x);
-          v.y = fmaf(beta, old.y, v.y);
-        }
-        gst2<BF16>(out[u] + 2 * a * k2, v);
-      }
-    }
-  }
-}
-
-// Zero the padding of every column of a factored tile whose coefficients another phase writes
-// (the MFMA reads whole columns of cs elements).
-template <bool BF16>
-__device__ __forceinline__ void zero_column_pads(const FrameDev& f, int nt, typename Act<BF16>::E* tile, int ldt,
-                                                 int ldb) {
-  if (f.radix == 1 || f.cs == f.W2) return;
-  const int padw = f.cs - f.W2, per_tok = f.nblk * 4 * padw, items = nt * per_tok;
-  for (int it = threadIdx.x; it < items; it += blockDim.x) {
-    const int t = it / per_tok, r = it - t * per_tok, col = r / padw, e = r - col * padw;
-    const int blk = col >> 2, a = col & 3;
-    Act<BF16>::st(tile + t * ldt + blk * ldb + a * f.cs + f.W2 + e, 0.f);
-  }
-}
-
-// z = P^T x for a tile: token rows at src (global) -> coefficients in the LDS tile.
-template <bool BF16>
-__device__ __forceinline__ void analysis_to_lds(const FrameDev& f, const float2* tw, int nt,
-                                                const typename Act<BF16>::E* src, long ld, typename Act<BF16>::E* dst,
-                                                int ldt, int ldb) {
-  using A = Act<BF16>;
-  using E = typename A::E;
-  const int nblk = f.nblk;
-  if (f.radix == 1) {
-    const int W = f.W;
-    column_apply<BF16, true>(
-        f, false, nt * nblk, W,
-        [&](int c) {
-          const int t = c / nblk;
-          return src + (long)t * ld + (c - t * nblk) * W;
-        },
-        [&](int c, int o, f32x4 v) {
-          if (o < W) {
-            const int t = c / nblk;
-            A::st4(dst + t * ldt + (c - t * nblk) * ldb + o, v);
-          }
-        });
-    return;
-  }
-  radix4_analysis<BF16>(f, tw, nt, src, ld, dst, ldt, ldb);
-  __syncthreads();
-  const int cs = f.cs;
-  auto at = [&](int c) -> E* {
-    const int tb = c >> 2, t = tb / nblk;
-    return dst + t * ldt + (tb - t * nblk) * ldb + (c & 3) * cs;
-  };
-  column_apply<BF16, false>(
-      f, false, nt * nblk * 4, cs, [&](int c) -> const E* { return at(c); },
-      [&](int c, int o, f32x4 v) {
-        if (o < cs) A::st4(at(c) + o, v);
-      });
-}
-
-// out = s P q (+ beta out) for a tile: coefficients in the LDS tile at src -> token rows at dst.
-// Factored frames transform the tile in place first, so src is overwritten.
-template <bool BF16>
-__device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const float2* tw, int nt,
-                                                   typename Act<BF16>::E* src, int ldt, int ldb,
-                                                   typename Act<BF16>::E* dst, long ld, float s, float beta) {
-  using A = Act<BF16>;
-  using E = typename A::E;
-  const int nblk = f.nblk;
-  if (f.radix == 1) {
-    const int W = f.W;
-    column_apply<BF16, false>(
-        f, true, nt * nblk, W,
-        [&](int c) -> const E* {
-          const int t = c / nblk;
-          return src + t * ldt + (c - t * nblk) * ldb;
-        },
-        [&](int c, int o, f32x4 v) {
-          if (o < W) {
-            const int t = c / nblk;
-            E* p = dst + (long)t * ld + (c - t * nblk) * W + o;
-            f32x4 r = v * s;
-            if (beta != 0.f) r += beta * A::gld4(p);
-            A::gst4(p, r);
-          }
-        });
-    return;
-  }
-  const int cs = f.cs;
-  auto at = [&](int c) -> E* {
-    const int tb = c >> 2, t = tb / nblk;
-    return src + t * ldt + (tb - t * nblk) * ldb + (c & 3) * cs;
-  };
-  column_apply<BF16, false>(
-      f, true, nt * nblk * 4, cs, [&](int c) -> const E* { return at(c); },
-      [&](int c, int o, f32x4 v) {
-        if (o < cs) A::st4(at(c) + o, v);
-      });
-  __syncthreads();
-  radix4_synthesis<BF16>(f, tw, nt, src, ldt, ldb, dst, ld, s, beta);
-}
-
-// Sparse products over a generic stream (GenStream).  Each wave walks its run of stream rows
-// with the next kSD rows' entries and coefficients in flight.  Lane l accumulates, for tokens
-// tg0 .. tg0 + ntg - 1 of the tile, its slot's entries times the source coefficients (src tile)
-// and, at the last row of each slab, stores the sums at its destination in the dst tile.
-// BWD (q = C^T u over the columns of C): the walk also yields, per entry, this pass's share of
-// dC / s = sum_t u_t[row] z_t[column], z being read from the lane's destination before q is
-// written over it; part receives one float per stream element (added to when part_add).
-constexpr int kSD = 8;   // stream rows per buffer (two buffers: up to 16 rows in flight)
-constexpr int kTG = 8;        // tokens per pass over the stream (a last pass may take 2 to 7)
-constexpr int kTGWide = 16;   // tokens per pass while at least that many remain: each pass
-                              // starts with a latency-bound load of its first entries
-
-template <bool BF16, bool BWD, bool PART_ADD, int kTG>
-__device__ __forceinline__ void stream_products(const GenStream& S, const float* __restrict__ cv,
-                                                const typename Act<BF16>::E* src, int ld_src,
-                                                typename Act<BF16>::E* dst, int ld_dst, int tg0, int ntg,
-                                                bool write_dst, float* part) {
-  using A = Act<BF16>;
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int r0 = S.wave_row[wave], r1 = S.wave_row[wave + 1];
-  if (r0 >= r1) return;
-  const int2* ent = (S.ent);
-  src += tg0 * ld_src;
-  dst += tg0 * ld_dst;
-  // Two buffers of kSD rows, each refilled right after it is consumed, so that the other one's
-  // loads stay in flight meanwhile.
-  int2 ea[kSD], eb[kSD];
-  float ca[kSD], cb[kSD];
-  float pa[kSD], pb[kSD];   // PART_ADD: the partial sums to add to, loaded with the entries
-  auto load = [&](int r, int2 (&e)[kSD], float (&c)[kSD], float (&pv)[kSD]) {
-#pragma unroll
-    for (int i = 0; i < kSD; ++i) {
-      const int j = min(r + i, r1 - 1) * 64 + lane;   // rows past the run repeat its last one, unused
-      e[i] = gload(&ent[j]);
-      c[i] = gload(&cv[j]);
-      if (BWD && PART_ADD && part) pv[i] = gload(&part[j]);
-    }
-  };
-  // Every row reads kTG token rows without branches (tokens past ntg repeat the last one; their
-  // sums are never stored and their dC weights zb are zero), so the reads overlap.
-  int tso[kTG], tdo[kTG];
-#pragma unroll
-  for (int t = 0; t < kTG; ++t) {
-    tso[t] = min(t, ntg - 1) * ld_src;
-    tdo[t] = min(t, ntg - 1) * ld_dst;
-  }
-  float acc[kTG], zb[kTG];
-#pragma unroll
-  for (int t = 0; t < kTG; ++t) acc[t] = zb[t] = 0.f;
-  bool start = true;   // the next row begins a slab
-  // The source values of row i + 1 are read before row i is processed (the source tile is not
-  // written during the walk), alternating between two register sets.
-  auto read = [&](const int2& e, float (&x)[kTG]) {
-    const int so = e.x & 0x7fffffff;
-#pragma unroll
-    for (int t = 0; t < kTG; ++t) x[t] = A::ld(src + tso[t] + so);
-  };
-  // Rows r .. r + n - 1 of a buffer (n = kSD in the main loop, so that its body has no exits).
-  auto consume = [&](int r, const int2 (&e)[kSD], const float (&c)[kSD], const float (&pv)[kSD], int n) {
-    float xa[kTG], xb[kTG];
-    read(e[0], xa);
-#pragma unroll
-    for (int i = 0; i < kSD; ++i) {
-      if (i >= n) break;
-      float (&x)[kTG] = (i & 1) ? xb : xa;
-      if (i + 1 < kSD && i + 1 < n) read(e[i + 1], (i & 1) ? xa : xb);
-      const int d = e[i].y;
-      if (BWD && part && start) {
-        const int dc0 = max(d, 0);
-        float zv[kTG];
-#pragma unroll
-        for (int t = 0; t < kTG; ++t) zv[t] = A::ld(dst + tdo[t] + dc0);
-#pragma unroll
-        for (int t = 0; t < kTG; ++t) zb[t] = (t < ntg && d >= 0) ? zv[t] : 0.f;
-      }
-      start = false;
-      float dc = 0.f;
-#pragma unroll
-      for (int t = 0; t < kTG; ++t) {
-        acc[t] = fmaf(c[i], x[t], acc[t]);
-        if (BWD) dc = fmaf(x[t], zb[t], dc);
-      }
-      if (BWD && part) {
-        gstore(part + (long)(r + i) * 64 + lane, PART_ADD ? pv[i] + dc : dc);
-      }
-      if (__builtin_amdgcn_readfirstlane(e[i].x) < 0) {   // the slab's last row (same in every lane)
-        if (write_dst && d >= 0) {
-#pragma unroll
-          for (int t = 0; t < kTG; ++t)
-            if (t < ntg) {
-              float v = acc[t];
-              if constexpr (!BWD && PART_ADD) v += A::ld(dst + t * ld_dst + d);   // a later input chunk
-              A::st(dst + t * ld_dst + d, v);
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < kTG; ++t) acc[t] = 0.f;
-        start = true;
-      }
-    }
-  };
-  // whole pairs of buffers first, then the remaining rows
-  const int rend = r0 + (r1 - r0) / (2 * kSD) * (2 * kSD);
-  load(r0, ea, ca, pa);
-  load(r0 + kSD, eb, cb, pb);
-  for (int r = r0; r < rend; r += 2 * kSD) {
-    consume(r, ea, ca, pa, kSD);
-    load(r + 2 * kSD, ea, ca, pa);
-    consume(r + kSD, eb, cb, pb, kSD);
-    load(r + 3 * kSD, eb, cb, pb);
-  }
-  if (rend < r1) {
-    consume(rend, ea, ca, pa, min(kSD, r1 - rend));
-    if (rend + kSD < r1) consume(rend + kSD, eb, cb, pb, r1 - rend - kSD);
-  }
-}
-
-// One pass over ntg <= kTG tokens with the walk for exactly that many (a single token takes the
-// 2-token walk): every token row read per table row is used.
-template <bool BF16, bool BWD, bool PART_ADD>
-__device__ __forceinline__ void stream_pass(const GenStream& S, const float* __restrict__ cv,
-                                            const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
-                                            int ld_dst, int tg, int ntg, bool write_dst, float* part) {
-  switch (ntg) {
-    case 1:
-    case 2: stream_products<BF16, BWD, PART_ADD, 2>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
-    case 3: stream_products<BF16, BWD, PART_ADD, 3>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
-    case 4: stream_products<BF16, BWD, PART_ADD, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
-    case 5: stream_products<BF16, BWD, PART_ADD, 5>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
-    case 6: stream_products<BF16, BWD, PART_ADD, 6>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
-    case 7: stream_products<BF16, BWD, PART_ADD, 7>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
-    default: stream_products<BF16, BWD, PART_ADD, kTG>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-  }
-}
-
-// All tokens of a tile, kTGWide at a time while that many remain, then kTG, each pass reading
-// only as many token rows as it needs.
-// `add` (MAY_ADD only): backward, add to the dC partial row (as do the tile's later passes);
-// forward, add the sums to the destination (the input side's later chunks).
-template <bool BF16, bool BWD, bool MAY_ADD = BWD>
-__device__ __forceinline__ void stream_all(const GenStream& S, const float* __restrict__ cv,
-                                           const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
-                                           int ld_dst, int nt, bool write_dst, float* part, bool add = false) {
-  for (int tg = 0; tg < nt;) {
-    const int ntg = nt - tg >= kTGWide ? kTGWide : min(kTG, nt - tg);
-    const bool add_now = MAY_ADD && (add || (BWD && tg > 0));
-    if (ntg == kTGWide) {
-      if (add_now)
-        stream_products<BF16, BWD, MAY_ADD, kTGWide>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-      else
-        stream_products<BF16, BWD, false, kTGWide>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    } else if (add_now) {
-      stream_pass<BF16, BWD, MAY_ADD>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    } else {
-      stream_pass<BF16, BWD, false>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    }
-    tg += ntg;
-  }
-}
-
-struct FwdArgs {
-  FrameDev fin, fout;
-  int T, tt, ldt_in, ldt_out, ldb_in, ldb_out;
-  const void* X;
-  const void* const* Xs;
-  long ldx;
-  void* Y;
-  void* const* Ys;
-  long ldy;
-  const float* c;             // coefficients in forward stream order: c (batch: cs[bi]) or
-  const float* const* cs;     // ccopy + bi * cstride when the layout differs
-  const float* ccopy;
-  long cstride;
-  float scale, beta;
-  GenStream st;
-  int nch;              // input-side chunks: blocks chunk_blk[i] .. chunk_blk[i + 1] - 1
-  int chunk_blk[kMaxGenChunks + 1];
-};
-
-// CHUNKED: the input side in a.nch chunks of blocks, v accumulated over them; otherwise whole
-// (a.nch == 1), in code of its own.
-template <bool BF16, bool CHUNKED>
-__global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
-  using A = Act<BF16>;
-  using E = typename A::E;
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  E* zt = reinterpret_cast<E*>(smem);           // tt x ldt_in   z = P_in^T x (of one chunk)
-  E* vt = zt + (size_t)a.tt * a.ldt_in;         // tt x ldt_out  v = C z
-  const int bi = blockIdx.y;
-  const E* X = (reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X));
-  E* Y = (reinterpret_cast<E*>(a.Ys ? a.Ys[bi] : a.Y));
-  const float* cv = (a.ccopy ? a.ccopy + bi * a.cstride : a.cs ? a.cs[bi] : a.c);
-  const int t0 = blockIdx.x * a.tt;
-  const int nt = min(a.tt, a.T - t0);
-  X += (long)t0 * a.ldx;
-  Y += (long)t0 * a.ldy;
-
-  // twiddle factors of factored frames after the tiles
-  float2* tw_in = reinterpret_cast<float2*>(vt + (size_t)a.tt * a.ldt_out);
-  float2* tw_out = tw_in + kTwLdsBytes / 16;
-  stage_twiddles(a.fin, tw_in);
-  stage_twiddles(a.fout, tw_out);
-  if (a.fin.radix != 1 || a.fout.radix != 1) __syncthreads();
-
-  zero_column_pads<BF16>(a.fout, nt, vt, a.ldt_out, a.ldb_out);
-  if constexpr (!CHUNKED) {
-    // analysis: z = P_in^T x for every (token, input block)
-    analysis_to_lds<BF16>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
-    __syncthreads();
-
-    // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
-    stream_all<BF16, false>(a.st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
-  } else {
-    for (int ch = 0; ch < a.nch; ++ch) {
-      // the chunk's blocks as a frame of their own, at column b0 W of the token rows
-      const int b0 = a.chunk_blk[ch];
-      FrameDev fc = a.fin;
-      fc.nblk = a.chunk_blk[ch + 1] - b0;
-      if (ch > 0) __syncthreads();   // the previous chunk's products are done reading z
-      analysis_to_lds<BF16>(fc, tw_in, nt, X + (long)b0 * a.fin.W, a.ldx, zt, a.ldt_in, a.ldb_in);
-      __syncthreads();
-
-      // v[a] (+)= sum over the chunk's entries of row a of c_e z[b_e]
-      GenStream sc = a.st;
-      sc.wave_row += ch * (kGenWaves + 1);
-      stream_all<BF16, false, true>(sc, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr, ch > 0);
-    }
-  }
-  __syncthreads();
-
-  // synthesis and epilogue: y = beta y + s P_out v
-  synthesis_from_lds<BF16>(a.fout, tw_out, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, a.scale, a.beta);
-}
-
-struct BwdArgs {
-  FrameDev fin, fout;
-  int T, tt, ldt_in, ldt_out, ldb_in, ldb_out;
-  const void* X;
-  const void* const* Xs;
-  long ldx;
-  const void* G;
-  const void* const* Gs;
-  long ldg;
-  void* dX;
-  void* const* dXs;
-  long lddx;
-  const float* ccopy;   // coefficients in backward stream order, [batch][cstride]
-  long cstride;
-  float scale, beta;
-  int want_dx, want_dc;
-  GenStream st;
-  float* partial;       // dC partial sums [batch][workgroup][cstride]
-  long ntiles;
-  int nch;              // input-side chunks: blocks chunk_blk[i] .. chunk_blk[i + 1] - 1
-  int chunk_blk[kMaxGenChunks + 1];
-};
-
-// CHUNKED: the input side in a.nch chunks of blocks; otherwise whole (a.nch == 1), in code of
-// its own (the chunk loop costs registers that the whole-side kernel then spills).
-template <bool BF16, bool CHUNKED>
-__global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
-  using A = Act<BF16>;
-  using E = typename A::E;
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  E* ut = reinterpret_cast<E*>(smem);           // tt x ldt_out  u = P_out^T g
-  E* zt = ut + (size_t)a.tt * a.ldt_out;        // tt x ldt_in   z = P_in^T x of one chunk, later q = C^T u
-  const int bi = blockIdx.y;
-  const E* G0 = reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G);
-  const E* X0 = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X);
-  E* dX0 = reinterpret_cast<E*>(a.dXs ? a.dXs[bi] : a.dX);
-  const float* cv = a.ccopy + bi * a.cstride;
-  // one partial row per workgroup, accumulated over the workgroup's tiles
-  float* part = a.want_dc ? a.partial + ((long)bi * gridDim.x + blockIdx.x) * a.cstride : nullptr;
-
-  // twiddle factors of factored frames after the tiles
-  float2* tw_in = reinterpret_cast<float2*>(zt + (size_t)a.tt * a.ldt_in);
-  float2* tw_out = tw_in + kTwLdsBytes / 16;
-  stage_twiddles(a.fin, tw_in);
-  stage_twiddles(a.fout, tw_out);
-  if (a.fin.radix != 1 || a.fout.radix != 1) __syncthreads();
-
-  for (long tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
-    const long t0 = tile * a.tt;
-    const int nt = (int)min((long)a.tt, (long)a.T - t0);
-    if (tile != blockIdx.x) __syncthreads();   // the previous tile's LDS reads are done
-
-    if constexpr (!CHUNKED) {
-      // q is written over z and then synthesized from whole columns: their padding must be zero
-      zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
-      analysis_to_lds<BF16>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
-      if (a.want_dc) analysis_to_lds<BF16>(a.fin, tw_in, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
-      __syncthreads();
-
-      // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
-      stream_all<BF16, true>(a.st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
-      if (!a.want_dx) continue;
-      __syncthreads();
-
-      synthesis_from_lds<BF16>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale,
-                               a.beta);
-      continue;
-    }
-    analysis_to_lds<BF16>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
-    for (int ch = 0; ch < a.nch; ++ch) {
-      // the chunk's blocks as a frame of their own, at column b0 W of the token rows
-      const int b0 = a.chunk_blk[ch];
-      FrameDev fc = a.fin;
-      fc.nblk = a.chunk_blk[ch + 1] - b0;
-      const long col0 = (long)b0 * a.fin.W;
-      if (ch > 0) __syncthreads();   // the previous chunk is done with the z / q tile
-      // q is written over z and then synthesized from whole columns: their padding must be zero
-      zero_column_pads<BF16>(fc, nt, zt, a.ldt_in, a.ldb_in);
-      if (a.want_dc) analysis_to_lds<BF16>(fc, tw_in, nt, X0 + t0 * a.ldx + col0, a.ldx, zt, a.ldt_in, a.ldb_in);
-      __syncthreads();
-
-      // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
-      GenStream sc = a.st;
-      sc.wave_row += ch * (kGenWaves + 1);
-      stream_all<BF16, true>(sc, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
-      if (!a.want_dx) continue;
-      __syncthreads();
-
-      synthesis_from_lds<BF16>(fc, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx + col0, a.lddx, a.scale,
-                               a.beta);
-    }
-  }
-}
+using namespace gen;
 
 // out[bi][j] = c_bi[idx[j]] (0 where idx[j] < 0): coefficients in a stream's order.
 __global__ void __launch_bounds__(256) gather_coef(const float* c, const float* const* cs, const int* __restrict__ idx,
@@ -1070,6 +242,24 @@ __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
   }
 }
 
+// c_plan[j] = c_user[user_of_slot[j]], zero in padding slots.
+__global__ void __launch_bounds__(256) coef_to_plan(const float* __restrict__ cu, const int* __restrict__ user_of_slot,
+                                                    int nslot, float* __restrict__ cp) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= nslot) return;
+  const int e = user_of_slot[j];
+  cp[j] = e >= 0 ? cu[e] : 0.f;
+}
+
+// c_user[e] (+)= c_plan[slot_of_user[e]].
+__global__ void __launch_bounds__(256) coef_to_user(const float* __restrict__ cp, const int* __restrict__ slot_of_user,
+                                                    int nnz, int accumulate, float* __restrict__ cu) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= nnz) return;
+  const float v = cp[slot_of_user[e]];
+  cu[e] = accumulate ? cu[e] + v : v;
+}
+
 void record(hipEvent_t ev, hipStream_t s) {
   if (ev) (void)hipEventRecord(ev, s);
 }
@@ -1079,18 +269,9 @@ void record(hipEvent_t ev, hipStream_t s) {
 hipError_t configure_kernels() {
   static hipError_t once = [] {
     hipError_t e = hipSuccess;
-    auto set = [&](const void* fn) {
-      hipError_t r = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
+    for (const hipError_t r : {gen::configure_fwd_bf16(), gen::configure_fwd_f32(), gen::configure_bwd_bf16(),
+                               gen::configure_bwd_f32()})
       if (r != hipSuccess) e = r;
-    };
-    set(reinterpret_cast<const void*>(&fwd_kernel<true, false>));
-    set(reinterpret_cast<const void*>(&fwd_kernel<false, false>));
-    set(reinterpret_cast<const void*>(&fwd_kernel<true, true>));
-    set(reinterpret_cast<const void*>(&fwd_kernel<false, true>));
-    set(reinterpret_cast<const void*>(&bwd_kernel<true, false>));
-    set(reinterpret_cast<const void*>(&bwd_kernel<false, false>));
-    set(reinterpret_cast<const void*>(&bwd_kernel<true, true>));
-    set(reinterpret_cast<const void*>(&bwd_kernel<false, true>));
     return e;
   }();
   return once;
@@ -1162,19 +343,9 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   take_timing_events(&e0, &e1);
   record(e0, s);
   const size_t lds = p->gen_lds_bytes[bf16];
-  if (a.nch > 1) {
-    if (bf16)
-      hipLaunchKernelGGL((fwd_kernel<true, true>), grid, dim3(kFusedThreads), lds, s, a);
-    else
-      hipLaunchKernelGGL((fwd_kernel<false, true>), grid, dim3(kFusedThreads), lds, s, a);
-  } else {
-    if (bf16)
-      hipLaunchKernelGGL((fwd_kernel<true, false>), grid, dim3(kFusedThreads), lds, s, a);
-    else
-      hipLaunchKernelGGL((fwd_kernel<false, false>), grid, dim3(kFusedThreads), lds, s, a);
-  }
+  const hipError_t e = bf16 ? gen::launch_fwd_bf16(a, grid, lds, s) : gen::launch_fwd_f32(a, grid, lds, s);
   record(e1, s);
-  return hipGetLastError();
+  return e != hipSuccess ? e : hipGetLastError();
 }
 
 hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G,
@@ -1218,24 +389,19 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   take_timing_events(&e0, &e1);
   const long nwg = std::min<long>(ntiles, p->gen_rows);   // partial rows
   if (T > 0 && (want_dx || want_dc)) {
-    hipError_t e = launch_gather(c, cs, a.st.coef, (int)a.cstride, count, p->dev.c_bwd, s);
-    if (e != hipSuccess) return e;
+    // the coefficients feed only q = C^T u: a dC-only call neither reads c_vals (which may then be
+    // NULL) nor uses the copy, whose stale values reach no output
+    if (want_dx) {
+      const hipError_t e = launch_gather(c, cs, a.st.coef, (int)a.cstride, count, p->dev.c_bwd, s);
+      if (e != hipSuccess) return e;
+    }
     const dim3 grid((unsigned)nwg, (unsigned)count);
     record(e0, s);
     const size_t lds = p->gen_lds_bytes[bf16];
-    if (a.nch > 1) {
-      if (bf16)
-        hipLaunchKernelGGL((bwd_kernel<true, true>), grid, dim3(kFusedThreads), lds, s, a);
-      else
-        hipLaunchKernelGGL((bwd_kernel<false, true>), grid, dim3(kFusedThreads), lds, s, a);
-    } else {
-      if (bf16)
-        hipLaunchKernelGGL((bwd_kernel<true, false>), grid, dim3(kFusedThreads), lds, s, a);
-      else
-        hipLaunchKernelGGL((bwd_kernel<false, false>), grid, dim3(kFusedThreads), lds, s, a);
-    }
+    const hipError_t eb = bf16 ? gen::launch_bwd_bf16(a, grid, lds, s) : gen::launch_bwd_f32(a, grid, lds, s);
     record(e1, s);
-    e = hipGetLastError();
+    if (eb != hipSuccess) return eb;
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   if (want_dc) {
@@ -1245,6 +411,22 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
     hipLaunchKernelGGL(dc_reduce, grid, dim3(64 * kDcWaves), 0, s, p->partial, nwg, len, a.st.coef,
                        p->dev.coef_pad, p->dev.ncoef_pad, scale, accumulate_dc, dC, dCs);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_coef_to_plan(const ff_plan* p, const float* c_user, float* c_plan, hipStream_t s) {
+  const int n = p->dev.nnz;
+  if (n > 0)
+    hipLaunchKernelGGL(coef_to_plan, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, c_user, p->dev.user_of_slot,
+                       n, c_plan);
+  return hipGetLastError();
+}
+
+hipError_t launch_coef_to_user(const ff_plan* p, const float* c_plan, float* c_user, int accumulate, hipStream_t s) {
+  const int n = p->dev.nnz_user;
+  if (n > 0)
+    hipLaunchKernelGGL(coef_to_user, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, c_plan, p->dev.slot_of_user,
+                       n, accumulate, c_user);
   return hipGetLastError();
 }
 

@@ -597,8 +597,11 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   };
   enum {
     kGfEnt, kGfCoef, kGfWave, kGbEnt, kGbCoef, kGbWave, kCoefPad, kCfwd, kCbwd, kMrgPtr, kMrgEnt,
-    kFPl, kBPl, kFSt, kPadSlots, kBW, kPartial, kCoefBwd, kBwdPos, kFEm, kBDst, kBEm, kBPad, kNumBlobs
+    kFPl, kBPl, kFSt, kPadSlots, kBW, kPartial, kCoefBwd, kBwdPos, kFEm, kBDst, kBEm, kBPad, kUserOfSlot,
+    kSlotOfUser, kNumBlobs
   };
+  // both directions of the coefficient layout, for the device-side conversions
+  std::vector<int> user_of_slot32(p->user_order.begin(), p->user_order.end());
   std::vector<Blob> blobs(kNumBlobs);
   blobs[kGfEnt] = {gfwd.ent.data(), gf_elems * sizeof(int2)};
   blobs[kGfCoef] = {fcoef.data(), gf_elems * sizeof(int)};
@@ -626,6 +629,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   blobs[kBDst] = {b_dst.data(), b_dst.size() * sizeof(uint32_t)};
   blobs[kBEm] = {b_em.data(), b_em.size() * sizeof(uint32_t)};
   blobs[kBPad] = {b_pad.data(), b_pad.size() * sizeof(int)};
+  blobs[kUserOfSlot] = {user_of_slot32.data(), user_of_slot32.size() * sizeof(int)};
+  blobs[kSlotOfUser] = {slot_of_user.data(), (size_t)nnz * sizeof(int)};
   size_t total = 0;
   for (const Blob& b : blobs) total += up(b.bytes);
   int cur = 0;
@@ -667,6 +672,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   pd.mrg_ent = (const int4*)where[kMrgEnt];
   pd.mrg_max_bucket = max_bucket;
   pd.nnz = (int)nslot;
+  pd.user_of_slot = (const int*)where[kUserOfSlot];
+  pd.slot_of_user = (const int*)where[kSlotOfUser];
+  pd.nnz_user = (int)nnz;
   ff::FastPlanDev& fp = p->fast;
   fp.enabled = fast ? 1 : 0;
   fp.fwd_pl = (const int4*)where[kFPl];

@@ -11,7 +11,7 @@ methods"); no dataset or pretrained weight is involved:
 
 * activations x and upstream gradients g are i.i.d. N(0, 1);
 * coefficient values are N(0, 0.02) in fp32 (the adapter is kept in fp32,
-  Sec. 3.3 "Storage efficiency");
+  Sec. 3.4, "Storage efficiency");
 * the support of C is uniform over the m x n coefficient grid, drawn without
   replacement (Sec. 3.3: random support, shared across layers);
 * W0 ~ N(0, 1/n);

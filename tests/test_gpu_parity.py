@@ -11,7 +11,8 @@ import pytest
 
 from oracle import frameft_oracle as O
 from paper_2608_26430_amd import inputs
-from tests.parity_util import TOL, merge_abs_terms, merged_bf16_ok, oracle_frame, plan_c, rel, to_np, torch_act, user_dc
+from tests.parity_util import (TOL, U32, BwdBounds, FwdBounds, guarded, guards_intact, max_rel, merge_abs_terms, merge_bound,
+                               merged_bf16_ok, oracle_frame, plan_c, rel, to_np, torch_act, user_dc, within)
 
 torch = pytest.importorskip("torch")
 import paper_2608_26430_amd as ff  # noqa: E402
@@ -75,65 +76,109 @@ def _problem(shape, dtype, seed):
     return rows, cols, vals, X, G
 
 
+def _adapter_rms_like(g, shape, ref, dtype):
+    """Random N(0, rms(ref)^2) values (bf16-rounded for bf16): an existing Y or dX of the adapter
+    term's own magnitude, so that a beta epilogue which dropped the adapter term would fail."""
+    r = float(np.sqrt(np.mean(np.square(ref)))) if np.size(ref) else 1.0
+    return inputs.gaussian(g, shape, std=max(r, 1e-6), dtype=dtype)
+
+
+def _check(name, got, ref, bound, report):
+    ok, worst = within(got, ref, bound)
+    report[name] = (round(worst, 4), round(max_rel(got, ref), 6))
+    assert ok, f"{name}: element-wise bound exceeded (max err/bound {worst:.3g}); {report}"
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "n%d_m%d_nnz%d_T%d" % (s[0], s[2], s[4], s[5]))
 def test_small_parity(dev, shape, dtype):
+    """Every output against the oracle element by element (token space, and for y / dX also
+    coefficient space, where a single lost support entry stands out), with inputs and outputs in
+    views whose leading dimension exceeds their width: the padding columns of X and G hold NaN
+    patterns that must not leak into any result, and the padding and guard regions around Y, dX,
+    dC and W must come back untouched."""
     n, rn, m, rm, nnz, T = shape
     rows, cols, vals, X, G = _problem(shape, dtype, seed=n * 7 + m + nnz + T)
     s = 0.173
-    P_in, P_out = oracle_frame(n // rn, rn, n), oracle_frame(m // rm, rm, m)
-    f_in, f_out = ff.framegen(n, n // rn, rn), ff.framegen(m, m // rm, rm)
+    k_in, k_out = n // rn, m // rm
+    P_in, P_out = oracle_frame(k_in, rn, n), oracle_frame(k_out, rm, m)
+    f_in, f_out = ff.framegen(n, k_in, rn), ff.framegen(m, k_out, rm)
     plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T)
-    assert plan.fast128 == (n // rn == 64 and m // rm == 64 and (n // 128) % 2 == 0 and (m // 128) % 2 == 0)
+    assert plan.fast128 == (k_in == 64 and k_out == 64 and (n // 128) % 2 == 0 and (m // 128) % 2 == 0)
     if plan.fast128:
         assert plan.bwd_tile_tokens == (8 if m > 4096 or nnz > 20000 else 16)
     # blocks wider than 128 (k = 172, 224) are applied as a radix-4 stage plus a DFT of size k/4
-    assert plan.radix == (4 if 2 * n // rn > 128 else 1, 4 if 2 * m // rm > 128 else 1)
+    assert plan.radix == (4 if 2 * k_in > 128 else 1, 4 if 2 * k_out > 128 else 1)
     # the generic kernels chunk the input side only for the wide, dense-support shapes
     assert (plan.gen_chunks > 1) == (n == 8192)
-    tol = TOL[dtype]
-    Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
+    pad = 8 if dtype == "bf16" else 4
+    xbuf, Xd = guarded(T, n, n + pad, dtype, dev, X)
+    gbuf, Gd = guarded(T, m, m + 2 * pad, dtype, dev, G)
     c = plan_c(plan, vals, dev)
     order = plan.order
     assert np.array_equal(np.sort(order[order >= 0]), np.arange(nnz))
     assert plan.coef_slots == order.size >= nnz
+    L = plan.coef_slots
 
-    # forward, overwrite and accumulate into an existing Y
-    y_ref = O.adapter_fwd(P_in, P_out, rows, cols, vals, s, X)
+    fb = FwdBounds(P_in, P_out, rows, cols, vals, s, X, dtype, k_in, k_out)
+    bb = BwdBounds(P_in, P_out, rows, cols, vals, s, X, G, dtype, k_in, k_out)
+    Y0 = _adapter_rms_like(inputs.rng(3), (T, m), fb.y, dtype)
+    dX0 = _adapter_rms_like(inputs.rng(4), (T, n), bb.dx, dtype)
+    fbb = FwdBounds(P_in, P_out, rows, cols, vals, s, X, dtype, k_in, k_out, beta_y0=0.75 * Y0)
+    bbb = BwdBounds(P_in, P_out, rows, cols, vals, s, X, G, dtype, k_in, k_out, beta_dx0=-1.5 * dX0)
+
+    # forward: overwrite a contiguous Y, and beta-accumulate into a padded, guarded one
     Y = ff.adapter_fwd(plan, Xd, c, s)
-    Y0 = inputs.gaussian(inputs.rng(3), (T, m), dtype=dtype)
-    Yb = ff.adapter_fwd(plan, Xd, c, s, Y=torch_act(Y0, dtype, dev), beta=0.75)
-    # backward: overwrite, then accumulate
-    dx_ref, dc_ref = O.adapter_bwd(P_in, P_out, rows, cols, vals, s, X, G)
-    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s, dC=torch.full((plan.coef_slots,), float("nan"), device=dev))
-    dX0 = inputs.gaussian(inputs.rng(4), (T, n), dtype=dtype)
+    ybuf, Yb = guarded(T, m, m + pad, dtype, dev, Y0)
+    ff.adapter_fwd(plan, Xd, c, s, Y=Yb, beta=0.75)
+    # backward: overwrite, then beta / accumulate into padded, guarded outputs
+    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s, dC=torch.full((L,), float("nan"), device=dev))
+    dxbuf, dXb = guarded(T, n, n + 3 * pad, dtype, dev, dX0)
     dC0 = inputs.gaussian(inputs.rng(5), (nnz,)).astype(np.float32)
     dC_init = plan.to_plan(dC0)
     dC_init[order < 0] = 5.0            # accumulating calls leave padding slots alone
-    dXb, dCb = ff.adapter_bwd(plan, Xd, Gd, c, s, dX=torch_act(dX0, dtype, dev), beta_dx=-1.5,
-                              dC=torch.from_numpy(dC_init).to(dev), accumulate_dc=True)
+    dcbuf, dCb2 = guarded(1, L, L, "f32", dev, dC_init[None, :])
+    dCb = dCb2[0]
+    ff.adapter_bwd(plan, Xd, Gd, c, s, dX=dXb, beta_dx=-1.5, dC=dCb, accumulate_dc=True)
     _, dC2 = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dx=False)
-    # merge: dense delta into fp32, and in place into a bf16 weight
+    # merge: dense delta into a padded fp32 array, and in place into a bf16 weight
     dw_ref = O.merge_delta(P_in, P_out, rows, cols, vals, s)
-    Wd = ff.merge_delta(plan, c, s, torch.full((m, n), float("nan"), device=dev), beta=0.0)
+    wbuf, Wd = guarded(m, n, n + 4, "f32", dev)
+    ff.merge_delta(plan, c, s, Wd, beta=0.0)
     W0 = inputs.weight(inputs.rng(6), m, n, "bf16")
     Wb = ff.merge_delta(plan, c, s, torch_act(W0, "bf16", dev), beta=1.0)
     torch.cuda.synchronize()
 
+    for name, buf, rr, ww, ld, dt in (("Y", ybuf, T, m, m + pad, dtype), ("dX", dxbuf, T, n, n + 3 * pad, dtype),
+                                      ("dC", dcbuf, 1, L, L, "f32"), ("W", wbuf, m, n, n + 4, "f32"),
+                                      ("X", xbuf, T, n, n + pad, dtype), ("G", gbuf, T, m, m + 2 * pad, dtype)):
+        assert guards_intact(buf, rr, ww, ld, dt), f"{name}: padding or guard region overwritten"
+    rep = {}
     if nnz == 0:
         assert np.all(to_np(Y) == 0) and np.all(to_np(dX) == 0) and np.all(to_np(Wd) == 0)
-        assert dC.numel() == plan.coef_slots and np.all(to_np(dC) == 0)   # padding only
+        assert dC.numel() == L and np.all(to_np(dC) == 0)   # padding only
+        _check("y beta", to_np(Yb), fbb.y, fbb.by, rep)
+        _check("dX beta", to_np(dXb), bbb.dx, bbb.bdx, rep)
         return
-    assert rel(to_np(Y), y_ref) <= tol
-    assert rel(to_np(Yb), 0.75 * Y0 + y_ref) <= tol
-    assert rel(to_np(dX), dx_ref) <= tol
-    assert rel(user_dc(plan, dC), dc_ref) <= tol
-    assert rel(to_np(dXb), -1.5 * dX0 + dx_ref) <= tol
+    _check("y", to_np(Y), fb.y, fb.by, rep)
+    _check("y coef", fb.coef(to_np(Y)), fb.v, fb.bv, rep)
+    _check("y beta", to_np(Yb), fbb.y, fbb.by, rep)
+    _check("y beta coef", fbb.coef(to_np(Yb)), fbb.v, fbb.bv, rep)
+    _check("dX", to_np(dX), bb.dx, bb.bdx, rep)
+    _check("dX coef", bb.coef(to_np(dX)), bb.q, bb.bq, rep)
+    _check("dX beta", to_np(dXb), bbb.dx, bbb.bdx, rep)
+    _check("dX beta coef", bbb.coef(to_np(dXb)), bbb.q, bbb.bq, rep)
+    _check("dC", user_dc(plan, dC), bb.dc, bb.bdc, rep)
     assert np.all(to_np(dCb)[order < 0] == 5.0)
-    assert rel(plan.to_user(to_np(dCb)), dC0 + dc_ref) <= tol
+    _check("dC acc", plan.to_user(to_np(dCb)), dC0 + bb.dc,
+           bb.bdc + 2 * U32 * (np.abs(dC0) + np.abs(bb.dc)), rep)
     assert torch.equal(dC, dC2), "dC is not deterministic"
-    assert rel(to_np(Wd), dw_ref) <= 1e-5
-    assert merged_bf16_ok(to_np(Wb), W0, dw_ref, *merge_abs_terms(P_in, P_out, rows, cols, vals, s, rn, rm))
+    dW_abs, depth = merge_abs_terms(P_in, P_out, rows, cols, vals, s, rn, rm)
+    _check("dW", to_np(Wd), dw_ref, merge_bound(dW_abs, depth), rep)
+    assert merged_bf16_ok(to_np(Wb), W0, dw_ref, dW_abs, depth)
+    # the normwise figures of the tolerance statement, for the record
+    assert rel(to_np(Y), fb.y) <= TOL[dtype] and rel(user_dc(plan, dC), bb.dc) <= TOL[dtype]
+    print(f"\n{shape} {dtype}: (max err/bound, max-abs/max|ref|) {rep}")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -284,6 +329,73 @@ def test_generic_input_chunks(dev, dtype):
     assert rel(to_np(dX2[tok]), 2.0 * dx_ref) <= tol
     assert rel(user_dc(plan, dCo), dc_ref) <= tol
     assert torch.equal(dC, dCo), "dC is not deterministic"
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(256, 16, 512, 32, 700, 37), (4096, 64, 4096, 64, 10000, 13)],
+                         ids=lambda s: "n%d_m%d" % (s[0], s[2]))
+def test_dc_only_without_coefficients(dev, shape, dtype):
+    """A backward that asks only for dC needs no coefficients: with c_vals NULL (single call) and a
+    NULL pointer array (batched call) dC still matches the oracle element by element, on the
+    generic kernels (every fp32 call, and bf16 on the 256 -> 512 layer) and the fused ones."""
+    n, rn, m, rm, nnz, T = shape
+    rows, cols, vals, X, G = _problem(shape, dtype, seed=n + m + T + 17)
+    k_in, k_out = n // rn, m // rm
+    f_in, f_out = ff.framegen(n, k_in, rn), ff.framegen(m, k_out, rm)
+    plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T, max_batch=2)
+    s = -0.37
+    Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
+    _, dC = ff.adapter_bwd(plan, Xd, Gd, None, s, want_dx=False)
+    dCs = [torch.full((plan.coef_slots,), float("nan"), device=dev) for _ in range(2)]
+    ff.adapter_bwd_batched(plan, [Xd, Xd], [Gd, Gd], None, s, None, dCs)
+    torch.cuda.synchronize()
+    P_in, P_out = oracle_frame(k_in, rn, n), oracle_frame(k_out, rm, m)
+    bb = BwdBounds(P_in, P_out, rows, cols, vals, s, X, G, dtype, k_in, k_out)
+    rep = {}
+    _check("dC", user_dc(plan, dC), bb.dc, bb.bdc, rep)
+    for i in range(2):
+        assert torch.equal(dCs[i], dC)
+
+
+@pytest.mark.parametrize("shape", [(256, 16, 512, 32, 700, 37), (4096, 64, 4096, 64, 10000, 13)],
+                         ids=lambda s: "n%d_m%d" % (s[0], s[2]))
+def test_coef_layout_conversion(dev, shape):
+    """ff_coef_to_plan / ff_coef_to_user (Algorithm 1 step 4 on the device): a training step kept
+    entirely in the caller's support order -- C converted to the plan layout, forward and
+    backward, dC converted back (overwrite and accumulate) -- matches the oracle in user order;
+    the conversions equal the host permutation exactly and write nothing outside their arrays."""
+    n, rn, m, rm, nnz, T = shape
+    dtype = "bf16"
+    rows, cols, vals, X, G = _problem(shape, dtype, seed=n + 2 * m + T)
+    k_in, k_out = n // rn, m // rm
+    f_in, f_out = ff.framegen(n, k_in, rn), ff.framegen(m, k_out, rm)
+    plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T)
+    L = plan.coef_slots
+    s = 0.21
+    cubuf, cu2 = guarded(1, nnz, nnz, "f32", dev, vals[None, :])
+    cpbuf, cp2 = guarded(1, L, L, "f32", dev)
+    ff.coef_to_plan(plan, cu2[0], cp2[0])
+    Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
+    Y = ff.adapter_fwd(plan, Xd, cp2[0], s)
+    _, dCp = ff.adapter_bwd(plan, Xd, Gd, cp2[0], s, want_dx=False)
+    dubuf, du2 = guarded(1, nnz, nnz, "f32", dev)
+    ff.coef_to_user(plan, dCp, du2[0])
+    acc = torch.from_numpy(np.arange(nnz, dtype=np.float32)).to(dev)
+    ff.coef_to_user(plan, dCp, acc, accumulate=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(cp2[0]), plan.to_plan(vals).astype(np.float64))
+    assert np.array_equal(to_np(du2[0]), plan.to_user(to_np(dCp)))
+    assert np.array_equal(to_np(acc), (np.arange(nnz, dtype=np.float32) + plan.to_user(to_np(dCp)).astype(np.float32)))
+    for buf, w in ((cubuf, nnz), (cpbuf, L), (dubuf, nnz)):
+        assert guards_intact(buf, 1, w, w, "f32")
+    P_in, P_out = oracle_frame(k_in, rn, n), oracle_frame(k_out, rm, m)
+    fb = FwdBounds(P_in, P_out, rows, cols, vals, s, X, dtype, k_in, k_out)
+    bb = BwdBounds(P_in, P_out, rows, cols, vals, s, X, G, dtype, k_in, k_out)
+    rep = {}
+    _check("y coef", fb.coef(to_np(Y)), fb.v, fb.bv, rep)
+    _check("dC user order", to_np(du2[0]), bb.dc, bb.bdc, rep)
+    with pytest.raises(ff.FrameFTError):            # overlapping arrays are refused
+        ff.coef_to_user(plan, dCp, dCp[:nnz])
 
 
 def test_empty_batch_is_noop_and_zeroes_dc(dev):
@@ -474,7 +586,7 @@ def test_block_diagonal_support(dev, shape, dtype):
 
 
 def test_hot_swap_merge_then_unmerge(dev):
-    """Merging s P_out C P_in^T into W and then merging with -s (the hot swap of Sec. 3.3) gives
+    """Merging s P_out C P_in^T into W and then merging with -s (the hot swap of Sec. 3.4, "Storage efficiency") gives
     back W up to fp32 rounding, and the merged weight reproduces W0 x + adapter forward."""
     n = m = 4096
     rows, cols, vals, X, _ = _problem((n, 64, m, 64, 10_000, 16), "f32", 77)

@@ -66,6 +66,7 @@ def _load():
         "ff_adapter_bwd_batched": (i32, [vp, i64, i64, i32, vp, i64, vp, i64, vp, f32, f32, vp, i64, i32,
                                          vp, vp]),
         "ff_time_next_kernel": (i32, [vp, vp]),
+        "ff_adapter_bwd_noalloc": (i32, [vp, i64, i32, vp, i64, vp, i64, vp, f32, f32, vp, i64, i32, vp, vp]),
         "ff_coef_to_plan": (i32, [vp, vp, vp, vp]),
         "ff_coef_to_user": (i32, [vp, vp, vp, i32, vp]),
     }
@@ -348,6 +349,21 @@ def adapter_bwd(plan: Plan, X, G, c_vals, scale: float, dX=None, dC=None, beta_d
         _check(_load().ff_adapter_bwd(plan.handle, T, act, xp, ldx, gp, ldg, cp, scale, beta_dx,
                                       dxp, lddx, int(accumulate_dc), dcp, _stream(stream)))
     return (dX if want_dx else None), (dC if want_dc else None)
+
+
+def adapter_bwd_noalloc(plan: Plan, X, G, c_vals, scale: float, dX, dC, beta_dx: float = 0.0,
+                        accumulate_dc: bool = False, stream=None):
+    """adapter_bwd through ff_adapter_bwd_noalloc: the library allocates nothing and uses its static
+    scratch.  The outputs dX and dC (either may be None to skip it) are the caller's."""
+    T = G.shape[0]
+    gp, ldg = _mat(G, "G")
+    xp, ldx = _mat(X, "X") if X is not None else (None, plan.n)
+    dxp, lddx = _mat(dX, "dX") if dX is not None else (None, plan.n)
+    dcp = _vec(dC, "dC", plan.coef_slots) if dC is not None else None
+    cp = _vec(c_vals, "c_vals", plan.coef_slots) if c_vals is not None else None
+    _check(_load().ff_adapter_bwd_noalloc(plan.handle, T, _act_code(G), xp, ldx, gp, ldg, cp, scale, beta_dx,
+                                          dxp, lddx, int(accumulate_dc), dcp, _stream(stream)))
+    return dX, dC
 
 
 def coef_to_plan(plan: Plan, c_user, c_plan=None, stream=None):

@@ -3,6 +3,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "ff_internal.h"
 
@@ -94,6 +95,31 @@ ff_status check_bwd(const ff_plan* p, int64_t T, int act, const void* X, int64_t
   return FF_OK;
 }
 
+// Scratch of ff_adapter_bwd_noalloc: the backward's dC partial sums and reordered coefficients,
+// in device memory that the code object itself holds (no allocation at run time).  Each device
+// has its own copy of the array at its own address, taken once per device with
+// hipGetSymbolAddress; host code uses that address only, never the array's name.  Calls on one
+// device share the array, so overlapping calls on one device race.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+ff_status scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return ff::fail(FF_EDEVICE, "device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return ff::fail(FF_EDEVICE, "address of the static scratch on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return FF_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -170,6 +196,28 @@ ff_status ff_adapter_bwd(const ff_plan* p, int64_t T, int act, const void* X, in
   return launched(ff::launch_bwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, {G, nullptr}, ldg, c_vals,
                                  nullptr, scale, beta_dx, {dX, nullptr}, lddx, want_dx, accumulate_dc, dC,
                                  nullptr, want_dc, nullptr, (hipStream_t)stream),
+                  "backward launch");
+}
+
+ff_status ff_adapter_bwd_noalloc(const ff_plan* p, int64_t T, int act, const void* X, int64_t ldx,
+                                 const void* G, int64_t ldg, const float* c_vals, float scale,
+                                 float beta_dx, void* dX, int64_t lddx, int accumulate_dc, float* dC,
+                                 void* stream) {
+  ff::clear_error();
+  bool want_dx, want_dc, done;
+  ff_status st = check_bwd(p, T, act, X, ldx, G, ldg, c_vals, dX, lddx, accumulate_dc, dC, &want_dx, &want_dc,
+                           &done);
+  if (st != FF_OK || done) return st;
+  const size_t need = ff::bwd_scratch_floats(p, act == FF_BF16, (int)T) * sizeof(float);
+  if (need > kScratchBytes)
+    return ff::fail(FF_EINVAL, "this backward needs %zu bytes of scratch, more than the %zu bytes of the static "
+                    "scratch (use fewer tokens per call)", need, kScratchBytes);
+  void* base = nullptr;
+  if ((st = scratch_address(p->device, &base)) != FF_OK) return st;
+  const ff::BwdScratch ws{static_cast<float*>(base), kScratchBytes / sizeof(float)};
+  return launched(ff::launch_bwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, {G, nullptr}, ldg, c_vals,
+                                 nullptr, scale, beta_dx, {dX, nullptr}, lddx, want_dx, accumulate_dc, dC,
+                                 nullptr, want_dc, nullptr, (hipStream_t)stream, &ws),
                   "backward launch");
 }
 

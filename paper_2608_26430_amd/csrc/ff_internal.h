@@ -187,10 +187,21 @@ struct ActPtrs {          // one tensor: either a single pointer or a device arr
 hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx,
                       const float* c, const float* const* cs, float scale, float beta,
                       ActPtrs Y, int64_t ldy, float* c_saved, hipStream_t s);
+// Scratch for a single-adapter backward supplied by the caller (ff_adapter_bwd_noalloc) in place of
+// the plan's workspace: `floats` floats at `base`, 256-byte aligned, holding the coefficients in
+// the backward's order and then the dC partial sums.  Its contents on entry do not matter.
+struct BwdScratch {
+  float* base;
+  size_t floats;
+};
+// Floats of BwdScratch a single-adapter backward of T tokens needs (0 for T = 0).
+size_t bwd_scratch_floats(const ff_plan* p, int bf16, int T);
+size_t fast128_bwd_scratch_floats(const ff_plan* p, int T, size_t* partial_off);
 hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx,
                       ActPtrs G, int64_t ldg, const float* c, const float* const* cs, float scale,
                       float beta_dx, ActPtrs dX, int64_t lddx, bool want_dx, int accumulate_dc,
-                      float* dC, float* const* dCs, bool want_dc, const float* c_saved, hipStream_t s);
+                      float* dC, float* const* dCs, bool want_dc, const float* c_saved, hipStream_t s,
+                      const BwdScratch* ws = nullptr);
 hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf16, float beta,
                         void* W, int64_t ldw, hipStream_t s);
 // Coefficient vectors between the caller's support order and the plan layout (Algorithm 1,
@@ -215,7 +226,7 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
 hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G, int64_t ldg,
                          const float* c, const float* const* cs, float scale, float beta_dx, ActPtrs dX,
                          int64_t lddx, bool want_dx, int accumulate_dc, float* dC, float* const* dCs, bool want_dc,
-                         const float* c_saved, hipStream_t s);
+                         const float* c_saved, hipStream_t s, const BwdScratch* ws);
 constexpr int kFastTileTokens = 8;
 
 // Slot words of the 128-wide kernels' entry streams: restart flag (bit 0: the lane's row ends

@@ -348,13 +348,31 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   return e != hipSuccess ? e : hipGetLastError();
 }
 
+// Floats of backward scratch (coefficient copy, then dC partial rows) that a single-adapter
+// call of T tokens uses on the generic kernels; the partial rows start 256-byte aligned.
+size_t gen_bwd_scratch_floats(const ff_plan* p, int bf16, int T, size_t* partial_off) {
+  const long cstride = 64L * p->dev.bwd.rows;
+  const int tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, 1, p->gen_wgs);
+  const long nwg = std::min<long>((T + tt - 1) / tt, p->gen_rows);
+  const size_t off = ((size_t)cstride + 63) / 64 * 64;
+  if (partial_off) *partial_off = off;
+  return off + (size_t)nwg * (size_t)cstride;
+}
+
+size_t bwd_scratch_floats(const ff_plan* p, int bf16, int T) {
+  if (T <= 0) return 0;
+  if (bf16 && p->fast.enabled) return fast128_bwd_scratch_floats(p, T, nullptr);
+  return gen_bwd_scratch_floats(p, bf16, T, nullptr);
+}
+
 hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G,
                       int64_t ldg, const float* c, const float* const* cs, float scale, float beta_dx,
                       ActPtrs dX, int64_t lddx, bool want_dx, int accumulate_dc, float* dC, float* const* dCs,
-                      bool want_dc, const float* c_saved, hipStream_t s) {
+                      bool want_dc, const float* c_saved, hipStream_t s, const BwdScratch* ws) {
   if (bf16 && p->fast.enabled)
     return launch_bwd128(p, count, T, X, ldx, G, ldg, c, cs, scale, beta_dx, dX, lddx, want_dx, accumulate_dc, dC, dCs,
-                         want_dc, c_saved, s);
+                         want_dc, c_saved, s, ws);
+  if (ws && count != 1) return hipErrorInvalidValue;   // a caller's scratch serves one adapter
   BwdArgs a{};
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
@@ -383,6 +401,12 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.cstride = 64L * a.st.rows;
   a.ccopy = p->dev.c_bwd;
   a.partial = p->partial;
+  if (ws) {   // the caller's scratch instead of the plan's workspace
+    size_t off = 0;
+    if (gen_bwd_scratch_floats(p, bf16, T, &off) > ws->floats) return hipErrorInvalidValue;
+    a.ccopy = ws->base;
+    a.partial = ws->base + off;
+  }
   const long ntiles = (T + a.tt - 1) / a.tt;
   a.ntiles = ntiles;
   hipEvent_t e0, e1;
@@ -392,7 +416,7 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
     // the coefficients feed only q = C^T u: a dC-only call neither reads c_vals (which may then be
     // NULL) nor uses the copy, whose stale values reach no output
     if (want_dx) {
-      const hipError_t e = launch_gather(c, cs, a.st.coef, (int)a.cstride, count, p->dev.c_bwd, s);
+      const hipError_t e = launch_gather(c, cs, a.st.coef, (int)a.cstride, count, const_cast<float*>(a.ccopy), s);
       if (e != hipSuccess) return e;
     }
     const dim3 grid((unsigned)nwg, (unsigned)count);
@@ -408,7 +432,7 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
     const int len = (int)a.cstride, nmain = (len + 63) / 64;
     const int npadb = (p->dev.ncoef_pad + 64 * kDcWaves - 1) / (64 * kDcWaves);
     const dim3 grid((unsigned)(nmain + npadb), (unsigned)count);
-    hipLaunchKernelGGL(dc_reduce, grid, dim3(64 * kDcWaves), 0, s, p->partial, nwg, len, a.st.coef,
+    hipLaunchKernelGGL(dc_reduce, grid, dim3(64 * kDcWaves), 0, s, a.partial, nwg, len, a.st.coef,
                        p->dev.coef_pad, p->dev.ncoef_pad, scale, accumulate_dc, dC, dCs);
   }
   return hipGetLastError();

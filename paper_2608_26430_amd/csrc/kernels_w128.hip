@@ -1150,6 +1150,12 @@ __global__ void __launch_bounds__(256) scatter_bwd_coef(const float* c, const fl
   }
 }
 
+// p[0 .. n) = 0 (a fill kernel rather than a memset node, so that captured graphs replay it).
+__global__ void __launch_bounds__(256) fill_zero(float* p, int n) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j < n) gst(p)[j] = 0.f;
+}
+
 // dC[j] = [dC[j] +] s * sum_tiles partial[tile][slot] for every valid slot of the backward
 // streams (j = the slot's coefficient slot).  A workgroup owns 64 backward slots; each of its
 // 16 waves sums 1/16 of the tiles with all loads of a pass in flight, and the 16 sums are
@@ -1300,10 +1306,21 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   return hipGetLastError();
 }
 
+// Floats of backward scratch (the backward-ordered coefficient copy, then the dC partial rows of
+// every tile) that a single-adapter call of T tokens uses; the partial rows start 256-byte aligned.
+size_t fast128_bwd_scratch_floats(const ff_plan* p, int T, size_t* partial_off) {
+  const int tt = p->fast.bwd16 ? kTT16 : kTT;
+  const size_t pstride = fast128_partial_floats((size_t)p->fast.bwd_slots);
+  const size_t off = (pstride + 63) / 64 * 64;
+  if (partial_off) *partial_off = off;
+  return off + (size_t)((T + tt - 1) / tt) * pstride;
+}
+
 hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t ldx, ActPtrs G, int64_t ldg,
                          const float* c, const float* const* cs, float scale, float beta_dx, ActPtrs dX,
                          int64_t lddx, bool want_dx, int accumulate_dc, float* dC, float* const* dCs, bool want_dc,
-                         const float* c_saved, hipStream_t s) {
+                         const float* c_saved, hipStream_t s, const BwdScratch* ws) {
+  if (ws && count != 1) return hipErrorInvalidValue;   // a caller's scratch serves one adapter
   FastArgs a{};
   a.frag = p->fin->dev.fs16;
   a.T = T;
@@ -1325,7 +1342,14 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   a.slots = p->fast.bwd_slots;
   a.pstride = (int)fast128_partial_floats((size_t)a.slots);
   a.partial = p->partial;
-  a.cb = c_saved ? c_saved : p->fast.coef_bwd;
+  float* copy = p->fast.coef_bwd;   // where the coefficients are put in backward slot order
+  if (ws) {   // the caller's scratch instead of the plan's workspace
+    size_t off = 0;
+    if (fast128_bwd_scratch_floats(p, T, &off) > ws->floats) return hipErrorInvalidValue;
+    copy = ws->base;
+    a.partial = ws->base + off;
+  }
+  a.cb = c_saved ? c_saved : copy;
   const bool b16 = p->fast.bwd16 != 0;
   const int tt = b16 ? kTT16 : kTT;
   const long ntiles = (T + tt - 1) / tt;
@@ -1334,9 +1358,13 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   take_timing_events(&e0, &e1);
   if (T > 0 && want_dx && !c_saved) {
     const int nslot = p->fast.coef_slots;
+    if (ws) {   // the plan's copy was cleared once at creation; a shared scratch holds anything
+      const int n = a.slots + 256;
+      hipLaunchKernelGGL(fill_zero, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, copy, n);
+    }
     const dim3 g((unsigned)((nslot + p->fast.nbpad + 255) / 256), (unsigned)count);
     hipLaunchKernelGGL(scatter_bwd_coef, g, dim3(256), 0, s, c, cs, p->fast.bwd_pos, nslot, p->fast.bwd_pad,
-                       p->fast.nbpad, a.slots + 256, p->fast.coef_bwd);
+                       p->fast.nbpad, a.slots + 256, copy);
   }
   if (T > 0 && (want_dx || want_dc)) {
     const dim3 grid((unsigned)ntiles, (unsigned)count);
@@ -1381,7 +1409,7 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
     const int nzero = (npad + 64 * kRedWaves - 1) / (64 * kRedWaves);
     if (nred + nzero > 0) {
       const dim3 grid((unsigned)(nred + nzero), (unsigned)count);
-      hipLaunchKernelGGL(reduce128, grid, dim3(64 * kRedWaves), 0, s, p->partial, ntiles, a.slots, a.pstride,
+      hipLaunchKernelGGL(reduce128, grid, dim3(64 * kRedWaves), 0, s, a.partial, ntiles, a.slots, a.pstride,
                          p->fast.bwd_dst, scale, accumulate_dc, dC, dCs, p->fast.pad, npad, nred);
     }
   }

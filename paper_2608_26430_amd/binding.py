@@ -67,6 +67,9 @@ def _load():
                                          vp, vp]),
         "ff_time_next_kernel": (i32, [vp, vp]),
         "ff_adapter_bwd_noalloc": (i32, [vp, i64, i32, vp, i64, vp, i64, vp, f32, f32, vp, i64, i32, vp, vp]),
+        "ff_adamw_step": (i32, [i64, vp, vp, vp, vp, f32, f32, f32, f32, f32, i64, vp]),
+        "ff_adamw_step_batched": (i32, [i64, i64, vp, vp, vp, vp, f32, f32, f32, f32, f32, i64, vp]),
+        "ff_lr_linear_warmup": (ctypes.c_double, [i64, i64, i64, ctypes.c_double]),
         "ff_coef_to_plan": (i32, [vp, vp, vp, vp]),
         "ff_coef_to_user": (i32, [vp, vp, vp, i32, vp]),
     }
@@ -364,6 +367,43 @@ def adapter_bwd_noalloc(plan: Plan, X, G, c_vals, scale: float, dX, dC, beta_dx:
     _check(_load().ff_adapter_bwd_noalloc(plan.handle, T, _act_code(G), xp, ldx, gp, ldg, cp, scale, beta_dx,
                                           dxp, lddx, int(accumulate_dc), dcp, _stream(stream)))
     return dX, dC
+
+
+def _fvec(t, name, n=None):
+    torch = _torch()
+    if t.dtype != torch.float32 or not t.is_contiguous() or not t.is_cuda or (n is not None and t.numel() != n):
+        raise ValueError(f"{name} must be a contiguous fp32 device tensor of {n} elements")
+    return t.data_ptr()
+
+
+def adamw_step(c, g, m, v, lr: float, step: int, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+               weight_decay: float = 0.0, stream=None):
+    """One AdamW step on device fp32 vectors c, m, v (in place) with gradient g (ff_adamw_step)."""
+    n = c.numel()
+    _check(_load().ff_adamw_step(n, _fvec(c, "c", n), _fvec(g, "g", n), _fvec(m, "m", n), _fvec(v, "v", n),
+                                 lr, beta1, beta2, eps, weight_decay, step, _stream(stream)))
+    return c
+
+
+def adamw_step_batched(cs: Sequence, gs: Sequence, ms: Sequence, vs: Sequence, lr: float, step: int,
+                       beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8, weight_decay: float = 0.0,
+                       stream=None):
+    """adamw_step over equally long vectors of many adapters in one launch (ff_adamw_step_batched)."""
+    n, dev = cs[0].numel(), cs[0].device
+    for group, name in ((cs, "c"), (gs, "g"), (ms, "m"), (vs, "v")):
+        for t in group:
+            _fvec(t, name, n)
+            if t.data_ptr() % 16:
+                raise ValueError(f"{name} arrays must be 16-byte aligned")
+    ptrs = [pointer_array(x, dev) for x in (cs, gs, ms, vs)]
+    _check(_load().ff_adamw_step_batched(len(cs), n, *[p.data_ptr() for p in ptrs], lr, beta1, beta2, eps,
+                                         weight_decay, step, _stream(stream)))
+    return cs
+
+
+def lr_linear_warmup(step: int, warmup: int, total: int, base_lr: float) -> float:
+    """Learning rate of optimizer step `step` (0-based) under the linear schedule with warmup."""
+    return float(_load().ff_lr_linear_warmup(step, warmup, total, base_lr))
 
 
 def coef_to_plan(plan: Plan, c_user, c_plan=None, stream=None):

@@ -99,3 +99,12 @@ def test_framegen_without_device_reports_device_error():
     with pytest.raises(ff.FrameFTError) as ei:
         ff.framegen(256, 16, 16)
     assert ei.value.name == "FF_EDEVICE"
+
+
+def test_lr_schedule_host_function_matches_oracle():
+    from oracle import optim_oracle as OO
+    for total, ratio in ((1000, 0.06), (217, 0.03), (5, 0.5)):
+        warm = OO.warmup_steps(total, ratio)
+        for step in list(range(0, total + 2, max(1, total // 37))) + [warm - 1, warm, warm + 1, total - 1]:
+            want = OO.linear_warmup_lr(step, warm, total, 0.33)
+            assert ff.lr_linear_warmup(step, warm, total, 0.33) == pytest.approx(want, rel=1e-14, abs=1e-300)

@@ -67,6 +67,10 @@ def _load():
                                          vp, vp]),
         "ff_time_next_kernel": (i32, [vp, vp]),
         "ff_adapter_bwd_noalloc": (i32, [vp, i64, i32, vp, i64, vp, i64, vp, f32, f32, vp, i64, i32, vp, vp]),
+        "ff_plan_group_create": (i32, [i64, vp, ctypes.POINTER(vp)]),
+        "ff_plan_group_destroy": (None, [vp]),
+        "ff_adapter_fwd_group": (i32, [vp, i64, vp, i32, vp, i64, vp, f32, f32, vp, i64, vp]),
+        "ff_adapter_bwd_group": (i32, [vp, i64, vp, i32, vp, i64, vp, i64, vp, f32, f32, vp, i64, i32, vp, vp]),
         "ff_adamw_step": (i32, [i64, vp, vp, vp, vp, f32, f32, f32, f32, f32, i64, vp]),
         "ff_adamw_step_batched": (i32, [i64, i64, vp, vp, vp, vp, f32, f32, f32, f32, f32, i64, vp]),
         "ff_lr_linear_warmup": (ctypes.c_double, [i64, i64, i64, ctypes.c_double]),
@@ -486,6 +490,84 @@ def adapter_bwd_batched(plan: Plan, Xs: Sequence, Gs: Sequence, cs: Sequence, sc
                                           int(accumulate_dc), pdc.data_ptr() if pdc is not None else None,
                                           _stream(stream)))
     return dXs, dCs
+
+
+class PlanGroup:
+    """Adapters over one frame pair with a support each (ff_plan_group_create): plans[i] serves
+    adapter i.  Keeps the plans alive."""
+
+    def __init__(self, plans: Sequence[Plan]):
+        h = ctypes.c_void_p()
+        arr = (ctypes.c_void_p * len(plans))(*[p.handle.value for p in plans])
+        _check(_load().ff_plan_group_create(len(plans), ctypes.cast(arr, ctypes.c_void_p), ctypes.byref(h)))
+        self._h = h
+        self.plans = list(plans)
+        self.count = len(plans)
+        self.n, self.m = plans[0].n, plans[0].m
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if self._h:
+            _load().ff_plan_group_destroy(self._h)
+            self._h = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def plan_group(plans: Sequence[Plan]) -> PlanGroup:
+    return PlanGroup(plans)
+
+
+def adapter_fwd_group(group: PlanGroup, Xs: Sequence, cs: Sequence, scale: float, Ys: Sequence, beta: float = 0.0,
+                      tokens=None, T: Optional[int] = None, stream=None):
+    """Forward of adapter i on plans[i] (one launch).  `tokens`: optional device int32 tensor of
+    per-adapter token counts (each clamped to T, the launch size, default Xs[0].shape[0])."""
+    T = Xs[0].shape[0] if T is None else T
+    _, ldx = _mat(Xs[0], "X")
+    _, ldy = _mat(Ys[0], "Y")
+    dev = Xs[0].device
+    px, pc, py = pointer_array(Xs, dev), pointer_array(cs, dev), pointer_array(Ys, dev)
+    tp = _tokens_ptr(tokens, group.count)
+    _check(_load().ff_adapter_fwd_group(group.handle, T, tp, _act_code(Xs[0]), px.data_ptr(), ldx, pc.data_ptr(),
+                                        scale, beta, py.data_ptr(), ldy, _stream(stream)))
+    return Ys
+
+
+def adapter_bwd_group(group: PlanGroup, Xs: Sequence, Gs: Sequence, cs: Optional[Sequence], scale: float,
+                      dXs: Optional[Sequence], dCs: Optional[Sequence], beta_dx: float = 0.0,
+                      accumulate_dc: bool = False, tokens=None, T: Optional[int] = None, stream=None):
+    """Backward of adapter i on plans[i] (dX and/or dC; one launch plus the dC reduction)."""
+    T = Gs[0].shape[0] if T is None else T
+    dev = Gs[0].device
+    _, ldg = _mat(Gs[0], "G")
+    _, ldx = _mat(Xs[0], "X")
+    lddx = _mat(dXs[0], "dX")[1] if dXs is not None else group.n
+    px, pg = pointer_array(Xs, dev), pointer_array(Gs, dev)
+    pc = pointer_array(cs, dev) if cs is not None else None
+    pdx = pointer_array(dXs, dev) if dXs is not None else None
+    pdc = pointer_array(dCs, dev) if dCs is not None else None
+    tp = _tokens_ptr(tokens, group.count)
+    _check(_load().ff_adapter_bwd_group(group.handle, T, tp, _act_code(Gs[0]), px.data_ptr(), ldx, pg.data_ptr(),
+                                        ldg, pc.data_ptr() if pc is not None else None, scale, beta_dx,
+                                        pdx.data_ptr() if pdx is not None else None, lddx, int(accumulate_dc),
+                                        pdc.data_ptr() if pdc is not None else None, _stream(stream)))
+    return dXs, dCs
+
+
+def _tokens_ptr(tokens, count):
+    if tokens is None:
+        return None
+    torch = _torch()
+    if tokens.dtype != torch.int32 or not tokens.is_cuda or not tokens.is_contiguous() or tokens.numel() != count:
+        raise ValueError("tokens must be a contiguous int32 device tensor with one count per adapter")
+    return tokens.data_ptr()
 
 
 def time_next_kernel(ev_start, ev_stop):

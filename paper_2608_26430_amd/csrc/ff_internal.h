@@ -125,6 +125,32 @@ struct FastPlanDev {
   int bwd16 = 0;   // the backward runs 16-token tiles (slot words address 32-byte rows)
 };
 
+// One adapter's view of its plan inside a plan group (ff_plan_group): the tables and the
+// workspace (batch slot 0 of the plan's own) that the group kernels read per adapter.
+struct FastDesc {   // fused 128-wide kernels
+  const int4* fwd_pl;
+  const uint32_t* fwd_st;
+  const uint32_t* fwd_em;
+  const int4* bwd_pl;
+  const uint32_t* bwd_st;
+  const uint32_t* bwd_em;
+  const uint32_t* bwd_dst;
+  const int* pad;
+  const int* bwd_pad;
+  const int* bwd_pos;
+  float* coef;      // coefficients in backward slot order, bwd_slots + 256
+  float* partial;   // dC partials, [tile][bwd_slots + 256]
+  int npad, nbpad, slots, coef_slots;
+};
+struct GenDesc {    // generic kernels
+  GenStream fwd, bwd;
+  const int* coef_pad;
+  float* c_fwd;     // coefficients in forward stream order (when the layout is not that order)
+  float* c_bwd;     // coefficients in backward stream order
+  float* partial;   // dC partial rows, [workgroup][64 bwd.rows]
+  int fwd_by_pos, ncoef_pad;
+};
+
 }  // namespace ff
 
 struct ff_frame {
@@ -167,6 +193,27 @@ struct ff_plan {
   std::vector<int64_t> user_order;  // user index of each coefficient slot, -1 for padding
 };
 
+// Adapters with their own supports over one frame pair (per-layer masks, tenants), run together:
+// plans[i] serves adapter i.  The plans must outlive the group and agree on everything but the
+// support (frames, kernel path, tile geometry).
+struct ff_plan_group {
+  int64_t count = 0;
+  std::vector<const ff_plan*> plans;
+  const ff_plan* ref = nullptr;   // plans[0]: the shared geometry
+  int64_t max_tokens = 0;         // smallest max_tokens of the plans
+  int max_fast_items = 0;         // largest coef_slots + nbpad (fused coefficient scatter)
+  int max_fast_slots = 0;         // largest bwd_slots
+  int max_fast_npad = 0;
+  int max_gen_fwd = 0;            // largest 64 fwd.rows / 64 bwd.rows (generic streams)
+  int max_gen_bwd = 0;
+  int max_gen_npad = 0;
+  int any_fwd_gather = 0;         // some plan's layout is not its forward stream's order
+  int min_gen_rows = 0;           // fewest dC partial rows (generic backward) of any plan
+  void* dev_mem = nullptr;
+  const ff::FastDesc* fast = nullptr;   // [count], device
+  const ff::GenDesc* gen = nullptr;     // [count], device
+};
+
 namespace ff {
 
 // Error reporting (capi.cpp): remember a message for ff_last_error and return s.
@@ -204,6 +251,25 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
                       const BwdScratch* ws = nullptr);
 hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf16, float beta,
                         void* W, int64_t ldw, hipStream_t s);
+// Group calls: adapter i runs plans[i] on tokens[i] (device int32, clamped to [0, T]; NULL: all T)
+// of its own X / Y / G / dX / c / dC (device pointer arrays).
+hipError_t launch_fwd_group(const ff_plan_group* g, int bf16, int T, const int* tokens, const void* const* X,
+                            int64_t ldx, const float* const* cs, float scale, float beta, void* const* Y, int64_t ldy,
+                            hipStream_t s);
+hipError_t launch_bwd_group(const ff_plan_group* g, int bf16, int T, const int* tokens, const void* const* X,
+                            int64_t ldx, const void* const* G, int64_t ldg, const float* const* cs, float scale,
+                            float beta_dx, void* const* dX, int64_t lddx, bool want_dx, int accumulate_dc,
+                            float* const* dCs, bool want_dc, hipStream_t s);
+hipError_t launch_fwd128_group(const ff_plan_group* g, int T, const int* tokens, const void* const* X, int64_t ldx,
+                               const float* const* cs, float scale, float beta, void* const* Y, int64_t ldy,
+                               hipStream_t s);
+hipError_t launch_bwd128_group(const ff_plan_group* g, int T, const int* tokens, const void* const* X, int64_t ldx,
+                               const void* const* G, int64_t ldg, const float* const* cs, float scale, float beta_dx,
+                               void* const* dX, int64_t lddx, bool want_dx, int accumulate_dc, float* const* dCs,
+                               bool want_dc, hipStream_t s);
+// Generic-kernel tile size of a call (kernels.hip), shared by single, batched and group calls.
+int call_tile_tokens(int tt, long T, int count, int slots);
+
 // Coefficient vectors between the caller's support order and the plan layout (Algorithm 1,
 // step 4): to_plan writes every slot (zero in padding slots), to_user every user entry (added to
 // the old value when accumulate).

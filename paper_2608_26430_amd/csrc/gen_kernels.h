@@ -688,7 +688,15 @@ struct FwdArgs {
   GenStream st;
   int nch;              // input-side chunks: blocks chunk_blk[i] .. chunk_blk[i + 1] - 1
   int chunk_blk[kMaxGenChunks + 1];
+  // group calls: adapter blockIdx.y's own plan (stream, coefficient copy) and token count
+  // (device, clamped to [0, T]; NULL: T)
+  const GenDesc* group;
+  const int* tokens;
 };
+
+__device__ __forceinline__ int group_tokens(const int* tokens, int T, int bi) {
+  return tokens ? max(0, min(gload(tokens + bi), T)) : T;
+}
 
 // CHUNKED: the input side in a.nch chunks of blocks, v accumulated over them; otherwise whole
 // (a.nch == 1), in code of its own.
@@ -703,8 +711,17 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   const E* X = (reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X));
   E* Y = (reinterpret_cast<E*>(a.Ys ? a.Ys[bi] : a.Y));
   const float* cv = (a.ccopy ? a.ccopy + bi * a.cstride : a.cs ? a.cs[bi] : a.c);
+  GenStream st = a.st;
+  int T = a.T;
+  if (a.group) {   // the adapter's own plan and tokens
+    const GenDesc* d = a.group + bi;
+    st = d->fwd;
+    cv = d->fwd_by_pos ? a.cs[bi] : d->c_fwd;
+    T = group_tokens(a.tokens, a.T, bi);
+  }
   const int t0 = blockIdx.x * a.tt;
-  const int nt = min(a.tt, a.T - t0);
+  const int nt = min(a.tt, T - t0);
+  if (nt <= 0) return;   // past this adapter's tokens (group calls; uniform)
   X += (long)t0 * a.ldx;
   Y += (long)t0 * a.ldy;
 
@@ -722,7 +739,7 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
     __syncthreads();
 
     // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
-    stream_all<BF16, false>(a.st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
+    stream_all<BF16, false>(st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
   } else {
     for (int ch = 0; ch < a.nch; ++ch) {
       // the chunk's blocks as a frame of their own, at column b0 W of the token rows
@@ -734,7 +751,7 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
       __syncthreads();
 
       // v[a] (+)= sum over the chunk's entries of row a of c_e z[b_e]
-      GenStream sc = a.st;
+      GenStream sc = st;
       sc.wave_row += ch * (kGenWaves + 1);
       stream_all<BF16, false, true>(sc, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr, ch > 0);
     }
@@ -766,6 +783,10 @@ struct BwdArgs {
   long ntiles;
   int nch;              // input-side chunks: blocks chunk_blk[i] .. chunk_blk[i + 1] - 1
   int chunk_blk[kMaxGenChunks + 1];
+  // group calls: adapter blockIdx.y's own plan (stream, coefficient copy, partial rows) and
+  // token count (device, clamped to [0, T]; NULL: T)
+  const GenDesc* group;
+  const int* tokens;
 };
 
 // CHUNKED: the input side in a.nch chunks of blocks; otherwise whole (a.nch == 1), in code of
@@ -784,6 +805,17 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   const float* cv = a.ccopy + bi * a.cstride;
   // one partial row per workgroup, accumulated over the workgroup's tiles
   float* part = a.want_dc ? a.partial + ((long)bi * gridDim.x + blockIdx.x) * a.cstride : nullptr;
+  GenStream st = a.st;
+  long ntiles = a.ntiles;
+  int Tb = a.T;
+  if (a.group) {   // the adapter's own plan, workspace and tokens
+    const GenDesc* d = a.group + bi;
+    st = d->bwd;
+    cv = d->c_bwd;
+    part = a.want_dc ? d->partial + (long)blockIdx.x * 64 * st.rows : nullptr;
+    Tb = group_tokens(a.tokens, a.T, bi);
+    ntiles = (Tb + a.tt - 1) / a.tt;
+  }
 
   // twiddle factors of factored frames after the tiles
   float2* tw_in = reinterpret_cast<float2*>(zt + (size_t)a.tt * a.ldt_in);
@@ -792,9 +824,9 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   stage_twiddles(a.fout, tw_out);
   if (a.fin.radix != 1 || a.fout.radix != 1) __syncthreads();
 
-  for (long tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+  for (long tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const long t0 = tile * a.tt;
-    const int nt = (int)min((long)a.tt, (long)a.T - t0);
+    const int nt = (int)min((long)a.tt, (long)Tb - t0);
     if (tile != blockIdx.x) __syncthreads();   // the previous tile's LDS reads are done
 
     if constexpr (!CHUNKED) {
@@ -805,7 +837,7 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
       __syncthreads();
 
       // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
-      stream_all<BF16, true>(a.st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
+      stream_all<BF16, true>(st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
       if (!a.want_dx) continue;
       __syncthreads();
 
@@ -827,7 +859,7 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
       __syncthreads();
 
       // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
-      GenStream sc = a.st;
+      GenStream sc = st;
       sc.wave_row += ch * (kGenWaves + 1);
       stream_all<BF16, true>(sc, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
       if (!a.want_dx) continue;

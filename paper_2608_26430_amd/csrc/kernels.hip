@@ -242,6 +242,62 @@ __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
   }
 }
 
+// Group calls: gather_coef with each adapter's own stream (bwd: backward stream into c_bwd,
+// else forward stream into c_fwd).
+__global__ void __launch_bounds__(256) gather_coef_group(const float* const* cs, const GenDesc* group, int bwd) {
+  const int bi = blockIdx.y;
+  const GenDesc* d = group + bi;
+  const GenStream st = bwd ? d->bwd : d->fwd;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= 64 * st.rows) return;
+  const int k = gload(st.coef + j);
+  gstore((bwd ? d->c_bwd : d->c_fwd) + j, k >= 0 ? gload(cs[bi] + k) : 0.f);
+}
+
+// Group calls: dc_reduce over each adapter's own partial rows (one per workgroup that had a tile
+// of its tokens), stream and padding slots.
+__global__ void __launch_bounds__(64 * kDcWaves) dc_reduce_group(const GenDesc* group, const int* tokens, int T,
+                                                                 int tt, int nwg_grid, float scale, int accumulate,
+                                                                 float* const* dCs) {
+  __shared__ float red[kDcWaves][64];
+  const int bi = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const GenDesc* d = group + bi;
+  float* out = dCs[bi];
+  const int len = 64 * d->bwd.rows, nmain = (len + 63) / 64;
+  if ((int)blockIdx.x >= nmain) {
+    const int j = ((int)blockIdx.x - nmain) * (int)blockDim.x + threadIdx.x;
+    if (!accumulate && j < d->ncoef_pad) gstore(out + gload(d->coef_pad + j), 0.f);
+    return;
+  }
+  const int Tb = group_tokens(tokens, T, bi);
+  const long nwg = min((long)(Tb + tt - 1) / tt, (long)nwg_grid);
+  const int e = blockIdx.x * 64 + lane;
+  const int ec = min(e, len - 1);
+  const float* p = d->partial + ec;
+  float sum = 0.f;
+  for (long t0 = w; t0 < nwg; t0 += (long)kDcWaves * kDcBatch) {
+    float v[kDcBatch];
+#pragma unroll
+    for (int j = 0; j < kDcBatch; ++j) {
+      const long t = t0 + (long)j * kDcWaves;
+      v[j] = t < nwg ? gload(p + t * len) : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < kDcBatch; ++j) sum += v[j];
+  }
+  red[w][lane] = sum;
+  __syncthreads();
+  if (w == 0 && e < len) {
+    const int slot = gload(d->bwd.coef + e);
+    if (slot < 0) return;
+    float tot = 0.f;
+#pragma unroll
+    for (int i = 0; i < kDcWaves; ++i) tot += red[i][lane];
+    const float v = scale * tot;
+    gstore(out + slot, accumulate ? gload(out + slot) + v : v);
+  }
+}
+
 // c_plan[j] = c_user[user_of_slot[j]], zero in padding slots.
 __global__ void __launch_bounds__(256) coef_to_plan(const float* __restrict__ cu, const int* __restrict__ user_of_slot,
                                                     int nslot, float* __restrict__ cp) {
@@ -434,6 +490,104 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
     const dim3 grid((unsigned)(nmain + npadb), (unsigned)count);
     hipLaunchKernelGGL(dc_reduce, grid, dim3(64 * kDcWaves), 0, s, a.partial, nwg, len, a.st.coef,
                        p->dev.coef_pad, p->dev.ncoef_pad, scale, accumulate_dc, dC, dCs);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fwd_group(const ff_plan_group* g, int bf16, int T, const int* tokens, const void* const* X,
+                            int64_t ldx, const float* const* cs, float scale, float beta, void* const* Y, int64_t ldy,
+                            hipStream_t s) {
+  const ff_plan* p = g->ref;
+  if (bf16 && p->fast.enabled) return launch_fwd128_group(g, T, tokens, X, ldx, cs, scale, beta, Y, ldy, s);
+  const unsigned count = (unsigned)g->count;
+  FwdArgs a{};
+  a.fin = p->fin->dev;
+  a.fout = p->fout->dev;
+  a.T = T;
+  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, (int)count, p->gen_wgs);
+  a.ldt_in = p->gen_ldt_in[bf16];
+  a.ldt_out = p->ldt_out[bf16];
+  a.nch = p->gen_nch;
+  for (int i = 0; i <= p->gen_nch; ++i) a.chunk_blk[i] = p->gen_chunk_blk[i];
+  a.ldb_in = p->ldb_in;
+  a.ldb_out = p->ldb_out;
+  a.Xs = X;
+  a.ldx = (long)ldx;
+  a.Ys = Y;
+  a.ldy = (long)ldy;
+  a.cs = cs;
+  a.scale = scale;
+  a.beta = beta;
+  a.st = p->dev.fwd;
+  a.group = g->gen;
+  a.tokens = tokens;
+  if (g->any_fwd_gather)   // the layouts are other paths' orders: each adapter's coefficients reordered
+    hipLaunchKernelGGL(gather_coef_group, dim3((unsigned)((g->max_gen_fwd + 255) / 256), count), dim3(256), 0, s, cs,
+                       g->gen, 0);
+  const dim3 grid((unsigned)((T + a.tt - 1) / a.tt), count);
+  hipEvent_t e0, e1;
+  take_timing_events(&e0, &e1);
+  record(e0, s);
+  const size_t lds = p->gen_lds_bytes[bf16];
+  const hipError_t e = bf16 ? gen::launch_fwd_bf16(a, grid, lds, s) : gen::launch_fwd_f32(a, grid, lds, s);
+  record(e1, s);
+  return e != hipSuccess ? e : hipGetLastError();
+}
+
+hipError_t launch_bwd_group(const ff_plan_group* g, int bf16, int T, const int* tokens, const void* const* X,
+                            int64_t ldx, const void* const* G, int64_t ldg, const float* const* cs, float scale,
+                            float beta_dx, void* const* dX, int64_t lddx, bool want_dx, int accumulate_dc,
+                            float* const* dCs, bool want_dc, hipStream_t s) {
+  const ff_plan* p = g->ref;
+  if (bf16 && p->fast.enabled)
+    return launch_bwd128_group(g, T, tokens, X, ldx, G, ldg, cs, scale, beta_dx, dX, lddx, want_dx, accumulate_dc,
+                               dCs, want_dc, s);
+  const unsigned count = (unsigned)g->count;
+  BwdArgs a{};
+  a.fin = p->fin->dev;
+  a.fout = p->fout->dev;
+  a.T = T;
+  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, (int)count, p->gen_wgs);
+  a.ldt_in = p->gen_ldt_in[bf16];
+  a.ldt_out = p->ldt_out[bf16];
+  a.ldb_in = p->ldb_in;
+  a.ldb_out = p->ldb_out;
+  a.nch = p->gen_nch;
+  for (int i = 0; i <= p->gen_nch; ++i) a.chunk_blk[i] = p->gen_chunk_blk[i];
+  a.Xs = X;
+  a.ldx = (long)ldx;
+  a.Gs = G;
+  a.ldg = (long)ldg;
+  a.dXs = dX;
+  a.lddx = (long)lddx;
+  a.scale = scale;
+  a.beta = beta_dx;
+  a.want_dx = want_dx;
+  a.want_dc = want_dc;
+  a.st = p->dev.bwd;
+  a.group = g->gen;
+  a.tokens = tokens;
+  a.ntiles = (T + a.tt - 1) / a.tt;
+  // at most one workgroup per CU and adapter, and no more than every plan has partial rows for
+  const long nwg = std::min<long>(a.ntiles, g->min_gen_rows);
+  hipEvent_t e0, e1;
+  take_timing_events(&e0, &e1);
+  if (want_dx && nwg > 0)
+    hipLaunchKernelGGL(gather_coef_group, dim3((unsigned)((g->max_gen_bwd + 255) / 256), count), dim3(256), 0, s, cs,
+                       g->gen, 1);
+  record(e0, s);
+  if (nwg > 0) {   // (no tokens: the reduction below writes zeros)
+    const size_t lds = p->gen_lds_bytes[bf16];
+    const hipError_t eb = bf16 ? gen::launch_bwd_bf16(a, dim3((unsigned)nwg, count), lds, s)
+                               : gen::launch_bwd_f32(a, dim3((unsigned)nwg, count), lds, s);
+    if (eb != hipSuccess) return eb;
+  }
+  record(e1, s);
+  if (want_dc) {
+    const int nmain = (g->max_gen_bwd + 63) / 64;
+    const int npadb = (g->max_gen_npad + 64 * kDcWaves - 1) / (64 * kDcWaves);
+    hipLaunchKernelGGL(dc_reduce_group, dim3((unsigned)(nmain + npadb), count), dim3(64 * kDcWaves), 0, s, g->gen,
+                       tokens, T, a.tt, (int)nwg, scale, accumulate_dc, dCs);
   }
   return hipGetLastError();
 }

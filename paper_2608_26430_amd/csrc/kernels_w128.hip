@@ -537,7 +537,17 @@ struct FastArgs {
   int pstride;        // floats per tile in the partial workspace: slots + a scratch row group
   float* partial;     // [batch][tile][pstride]
   long ntiles;
+  // group calls: adapter blockIdx.y's own plan tables and workspace, and its token count
+  // (device, clamped to [0, T]; NULL: T)
+  const FastDesc* group;
+  const int* tokens;
 };
+
+// Tokens of adapter bi in a group call (uniform in the workgroup).
+__device__ __forceinline__ int group_tokens(const FastArgs& a, int bi) {
+  const int t = a.tokens ? gld(a.tokens)[bi] : a.T;
+  return max(0, min(t, a.T));
+}
 
 // s_waitcnt vmcnt(n) (n < 16), other counters untouched.
 template <int N>
@@ -613,7 +623,9 @@ __device__ __forceinline__ void analysis_phase(const Frag& F, const u16* rows, l
 
 // The stream tables are separate restrict-qualified arguments: the kernel never writes them,
 // so their wave-uniform reads become scalar loads, which do not wait for vector stores.
-template <bool BETA>
+// GROUP: adapter blockIdx.y runs its own plan (a.group) on its own token count; such calls keep
+// no backward-ordered copy (the group backward writes its own).
+template <bool BETA, bool GROUP>
 __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __restrict__ pl,
                                                       const unsigned* __restrict__ fst,
                                                       const unsigned* __restrict__ em) {
@@ -622,7 +634,15 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   unsigned char* tile = zL + (long)a.nblk_in * kW * kTT * 2 + wave * (2 * kW * kTT * 2);
   const int bi = blockIdx.y;
+  if constexpr (GROUP) {
+    const FastDesc* d = a.group + bi;
+    pl = d->fwd_pl;
+    fst = d->fwd_st;
+    em = d->fwd_em;
+    a.T = group_tokens(a, bi);
+  }
   const int t0 = blockIdx.x * kTT, nt = min(kTT, a.T - t0);
+  if (GROUP && nt <= 0) return;   // past this adapter's tokens (uniform)
   const u16* X = reinterpret_cast<const u16*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx;
   u16* Y = reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy;
   const float* cv = a.cs ? a.cs[bi] : a.c;
@@ -631,16 +651,21 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   // This workgroup's share of the coefficient copy in the backward's slot order: coefficient
   // slots, then the backward's padding slots (zero).  Read first, written after the analysis;
   // every lane loads and stores (lanes past the share repeat its last item, an identical write).
-  const int nitem = a.nslot + a.nbpad;
+  const int nitem = GROUP ? 0 : a.nslot + a.nbpad;
   const int per = (nitem + (int)gridDim.x - 1) / (int)gridDim.x;
   const int j0 = (int)blockIdx.x * per, jn = min(nitem, j0 + per);
-  const int js = max(min(j0 + (int)threadIdx.x, jn - 1), 0);
-  const bool is_coef = js < a.nslot;
-  const int pc = gld(a.pos)[min(js, a.nslot - 1)], pp = gld(a.bpad)[min(max(js - a.nslot, 0), a.nbpad - 1)];
-  const float cval = gld(cv)[min(js, a.nslot - 1)];
-  const int spos = is_coef ? pc : pp;
-  const float sval = is_coef ? cval : 0.f;
-  float* csave = a.csave + (long)bi * (a.slots + 256);
+  int spos = 0;
+  float sval = 0.f;
+  float* csave = nullptr;
+  if constexpr (!GROUP) {
+    const int js = max(min(j0 + (int)threadIdx.x, jn - 1), 0);
+    const bool is_coef = js < a.nslot;
+    const int pc = gld(a.pos)[min(js, a.nslot - 1)], pp = gld(a.bpad)[min(max(js - a.nslot, 0), a.nbpad - 1)];
+    const float cval = gld(cv)[min(js, a.nslot - 1)];
+    spos = is_coef ? pc : pp;
+    sval = is_coef ? cval : 0.f;
+    csave = a.csave + (long)bi * (a.slots + 256);
+  }
 
   u32x4 fr[kFragPerThread];
   frag_fetch(a.frag, fr);
@@ -657,7 +682,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
   Frag F;
   frag_stage(fr, reinterpret_cast<u32x4*>(smem), lane, F);
   analysis_phase(F, X, a.ldx, nt, a.nblk_in / 2, wave, lane, zL, tile);
-  gst(csave)[spos] = sval;
+  if constexpr (!GROUP) gst(csave)[spos] = sval;
   __syncthreads();
 
   // One output pair: its chunk is in `cur`; the next pair's chunk is loaded into `nxt` first,
@@ -719,7 +744,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
     store_act<BETA>(Y, a.ldy, nt, 2 * plast, lane, acc, a.beta, tile);
   }
   // shares longer than one slot per thread (grids of few tiles)
-  if (per > kThreads)
+  if (!GROUP && per > kThreads)
     for (int j = j0 + kThreads + (int)threadIdx.x; j < jn; j += kThreads) {
       if (j < a.nslot)
         gst(csave)[gld(a.pos)[j]] = gld(cv)[j];
@@ -728,7 +753,7 @@ __global__ void __launch_bounds__(kThreads, 2) fwd128(FastArgs a, const int4* __
     }
 }
 
-template <bool DX, bool DC, bool BETA>
+template <bool DX, bool DC, bool BETA, bool GROUP>
 __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __restrict__ pl,
                                                       const unsigned* __restrict__ bst,
                                                       const unsigned* __restrict__ em) {
@@ -737,12 +762,26 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   unsigned char* tile = uL + (long)a.nblk_out * kW * kTT * 2 + wave * (2 * kW * kTT * 2);
   const int bi = blockIdx.y;
+  long tile_row = (long)bi * a.ntiles + blockIdx.x;   // this tile's dC partial row
+  if constexpr (GROUP) {   // the adapter's own plan, workspace (batch slot 0) and tokens
+    const FastDesc* d = a.group + bi;
+    pl = d->bwd_pl;
+    bst = d->bwd_st;
+    em = d->bwd_em;
+    a.slots = d->slots;
+    a.pstride = d->slots + 256;
+    a.cb = d->coef;
+    a.partial = d->partial;
+    a.T = group_tokens(a, bi);
+    tile_row = blockIdx.x;
+  }
   const int t0 = blockIdx.x * kTT, nt = min(kTT, a.T - t0);
+  if (GROUP && nt <= 0) return;   // past this adapter's tokens (uniform)
   const u16* G = reinterpret_cast<const u16*>(a.Gs ? a.Gs[bi] : a.G) + (long)t0 * a.ldg;
   const u16* X = DC ? reinterpret_cast<const u16*>(a.Xs ? a.Xs[bi] : a.X) + (long)t0 * a.ldx : nullptr;
   u16* dX = DX ? reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy : nullptr;
-  const float* cbw = DX ? a.cb + (long)bi * (a.slots + 256) : nullptr;
-  float* part = DC ? a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.pstride : nullptr;
+  const float* cbw = DX ? a.cb + (GROUP ? 0L : (long)bi * (a.slots + 256)) : nullptr;
+  float* part = DC ? a.partial + tile_row * a.pstride : nullptr;
   float* trash = DC ? part + a.slots : nullptr;
   // dC sums only over the tile's tokens: activation columns past its end are zeroed
   const unsigned km = (lane & 7) < nt ? ~0u : 0u;
@@ -1005,7 +1044,7 @@ __device__ __forceinline__ void spmm16(const unsigned (&en)[kCh16], const float 
   }
 }
 
-template <bool DX, bool DC, bool BETA>
+template <bool DX, bool DC, bool BETA, bool GROUP>
 __global__ void __launch_bounds__(kThreads16, 1) bwd16(FastArgs a, const int4* __restrict__ pl,
                                                        const unsigned* __restrict__ bst) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -1013,7 +1052,20 @@ __global__ void __launch_bounds__(kThreads16, 1) bwd16(FastArgs a, const int4* _
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   unsigned char* tile = uL + (long)a.nblk_out * kW * kTT16 * 2 + wave * (2 * kW * kTT * 2);
   const int bi = blockIdx.y;
+  long tile_row = (long)bi * a.ntiles + blockIdx.x;   // this tile's dC partial row
+  if constexpr (GROUP) {   // the adapter's own plan, workspace (batch slot 0) and tokens
+    const FastDesc* d = a.group + bi;
+    pl = d->bwd_pl;
+    bst = d->bwd_st;
+    a.slots = d->slots;
+    a.pstride = d->slots + 256;
+    a.cb = d->coef;
+    a.partial = d->partial;
+    a.T = group_tokens(a, bi);
+    tile_row = blockIdx.x;
+  }
   const int t0 = blockIdx.x * kTT16, nt = min(kTT16, a.T - t0);
+  if (GROUP && nt <= 0) return;   // past this adapter's tokens (uniform)
   const bool two = nt > 8;   // the tile has a second token half
   const int nt0 = min(nt, 8), nt1 = two ? nt - 8 : nt0;
   const u16* G = reinterpret_cast<const u16*>(a.Gs ? a.Gs[bi] : a.G) + (long)t0 * a.ldg;
@@ -1021,8 +1073,8 @@ __global__ void __launch_bounds__(kThreads16, 1) bwd16(FastArgs a, const int4* _
   const u16* X1 = DC ? (two ? X0 + 8 * a.ldx : X0) : nullptr;
   u16* dX0 = DX ? reinterpret_cast<u16*>(a.Ys ? a.Ys[bi] : a.Y) + (long)t0 * a.ldy : nullptr;
   u16* dX1 = DX ? dX0 + 8 * a.ldy : nullptr;   // stored only when the tile has a second half
-  const float* cbw = DX ? a.cb + (long)bi * (a.slots + 256) : nullptr;
-  float* part = DC ? a.partial + ((long)bi * a.ntiles + blockIdx.x) * a.pstride : nullptr;
+  const float* cbw = DX ? a.cb + (GROUP ? 0L : (long)bi * (a.slots + 256)) : nullptr;
+  float* part = DC ? a.partial + tile_row * a.pstride : nullptr;
   float* trash = DC ? part + a.slots : nullptr;
   // dC sums only over the tile's tokens: activation columns past its end are zeroed
   const unsigned km0 = (lane & 7) < nt ? ~0u : 0u, km1 = (lane & 7) + 8 < nt ? ~0u : 0u;
@@ -1207,6 +1259,75 @@ __global__ void __launch_bounds__(64 * kRedWaves) reduce128(const float* __restr
   }
 }
 
+// Group calls: scatter_bwd_coef with every adapter's own plan (its copy cleared first, since
+// its over-read margin may hold another plan's values).
+__global__ void __launch_bounds__(256) scatter_bwd_coef_group(const float* const* cs, const FastDesc* group) {
+  const int bi = blockIdx.y;
+  const FastDesc* d = group + bi;
+  const int nslot = d->coef_slots, nbpad = d->nbpad;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= nslot + nbpad) return;
+  if (j < nslot)
+    gst(d->coef)[gld(d->bwd_pos)[j]] = gld(cs[bi])[j];
+  else
+    gst(d->coef)[gld(d->bwd_pad)[j - nslot]] = 0.f;
+}
+
+__global__ void __launch_bounds__(256) clear_copy_group(const FastDesc* group) {
+  const FastDesc* d = group + blockIdx.y;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j < d->slots + 256) gst(d->coef)[j] = 0.f;
+}
+
+// Group calls: reduce128 over each adapter's own tiles (its token count / tt of them), slots and
+// destinations; blocks past an adapter's share return.
+__global__ void __launch_bounds__(64 * kRedWaves) reduce128_group(const FastDesc* group, const int* tokens, int T,
+                                                                  int tt, float scale, int accumulate,
+                                                                  float* const* dCs) {
+  __shared__ float red[kRedWaves][64];
+  const int bi = blockIdx.y;
+  const FastDesc* d = group + bi;
+  float* out = dCs[bi];
+  const int slots = d->slots, pstride = d->slots + 256;
+  const int nred = (slots + 63) / 64;
+  const int npad = accumulate ? 0 : d->npad;
+  const int Tb = tokens ? max(0, min(gld(tokens)[bi], T)) : T;
+  const long ntiles = (Tb + tt - 1) / tt;
+  if ((int)blockIdx.x >= nred) {
+    const int i = ((int)blockIdx.x - nred) * 64 * kRedWaves + (int)threadIdx.x;
+    if (i < npad) gst(out)[gld(d->pad)[i]] = 0.f;
+    return;
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int slot = blockIdx.x * 64 + lane;
+  float s = 0.f;
+  if (slot < slots) {
+    const float* p = d->partial + slot;
+    for (long t0 = w; t0 < ntiles; t0 += (long)kRedWaves * kRedBatch) {
+      float v[kRedBatch];
+#pragma unroll
+      for (int j = 0; j < kRedBatch; ++j) {
+        const long t = t0 + (long)j * kRedWaves;
+        v[j] = t < ntiles ? gld(p)[t * pstride] : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < kRedBatch; ++j) s += v[j];
+    }
+  }
+  red[w][lane] = s;
+  __syncthreads();
+  if (w == 0 && slot < slots) {
+    float tot = 0.f;
+#pragma unroll
+    for (int i = 0; i < kRedWaves; ++i) tot += red[i][lane];
+    const unsigned j = gld(d->bwd_dst)[slot];
+    if (j != ~0u) {
+      const float v = scale * tot;
+      gst(out)[j] = accumulate ? gld(out)[j] + v : v;
+    }
+  }
+}
+
 void rec(hipEvent_t ev, hipStream_t s) {
   if (ev) (void)hipEventRecord(ev, s);
 }
@@ -1222,18 +1343,18 @@ hipError_t allow_lds(K* kernel) {
 hipError_t configure_fast128() {
   static hipError_t once = [] {
     hipError_t e = hipSuccess;
-    const hipError_t r[] = {allow_lds(&fwd128<false>),
-                            allow_lds(&fwd128<true>),
-                            allow_lds(&bwd128<true, true, false>),
-                            allow_lds(&bwd128<true, true, true>),
-                            allow_lds(&bwd128<true, false, false>),
-                            allow_lds(&bwd128<true, false, true>),
-                            allow_lds(&bwd128<false, true, false>),
-                            allow_lds(&bwd16<true, true, false>),
-                            allow_lds(&bwd16<true, true, true>),
-                            allow_lds(&bwd16<true, false, false>),
-                            allow_lds(&bwd16<true, false, true>),
-                            allow_lds(&bwd16<false, true, false>)};
+    const hipError_t r[] = {allow_lds(&fwd128<false, false>),       allow_lds(&fwd128<true, false>),
+                            allow_lds(&bwd128<true, true, false, false>), allow_lds(&bwd128<true, true, true, false>),
+                            allow_lds(&bwd128<true, false, false, false>), allow_lds(&bwd128<true, false, true, false>),
+                            allow_lds(&bwd128<false, true, false, false>), allow_lds(&bwd16<true, true, false, false>),
+                            allow_lds(&bwd16<true, true, true, false>),   allow_lds(&bwd16<true, false, false, false>),
+                            allow_lds(&bwd16<true, false, true, false>),  allow_lds(&bwd16<false, true, false, false>),
+                            allow_lds(&fwd128<false, true>),        allow_lds(&fwd128<true, true>),
+                            allow_lds(&bwd128<true, true, false, true>), allow_lds(&bwd128<true, true, true, true>),
+                            allow_lds(&bwd128<true, false, false, true>), allow_lds(&bwd128<true, false, true, true>),
+                            allow_lds(&bwd128<false, true, false, true>), allow_lds(&bwd16<true, true, false, true>),
+                            allow_lds(&bwd16<true, true, true, true>),   allow_lds(&bwd16<true, false, false, true>),
+                            allow_lds(&bwd16<true, false, true, true>),  allow_lds(&bwd16<false, true, false, true>)};
     for (hipError_t x : r)
       if (x != hipSuccess) e = x;
     return e;
@@ -1297,10 +1418,10 @@ hipError_t launch_fwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
   }
   rec(e0, s);
   if (beta != 0.f)
-    hipLaunchKernelGGL(fwd128<true>, grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st,
+    hipLaunchKernelGGL((fwd128<true, false>), grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st,
                        p->fast.fwd_em);
   else
-    hipLaunchKernelGGL(fwd128<false>, grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st,
+    hipLaunchKernelGGL((fwd128<false, false>), grid, dim3(kThreads), lds, s, a, p->fast.fwd_pl, p->fast.fwd_st,
                        p->fast.fwd_em);
   rec(e1, s);
   return hipGetLastError();
@@ -1377,27 +1498,27 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
       const size_t lds = fast16_lds_bytes(a.nblk_out);
       const dim3 blk(kThreads16);
       if (want_dx && want_dc && beta)
-        hipLaunchKernelGGL((bwd16<true, true, true>), grid, blk, lds, s, a, pl, st);
+        hipLaunchKernelGGL((bwd16<true, true, true, false>), grid, blk, lds, s, a, pl, st);
       else if (want_dx && want_dc)
-        hipLaunchKernelGGL((bwd16<true, true, false>), grid, blk, lds, s, a, pl, st);
+        hipLaunchKernelGGL((bwd16<true, true, false, false>), grid, blk, lds, s, a, pl, st);
       else if (want_dx && beta)
-        hipLaunchKernelGGL((bwd16<true, false, true>), grid, blk, lds, s, a, pl, st);
+        hipLaunchKernelGGL((bwd16<true, false, true, false>), grid, blk, lds, s, a, pl, st);
       else if (want_dx)
-        hipLaunchKernelGGL((bwd16<true, false, false>), grid, blk, lds, s, a, pl, st);
+        hipLaunchKernelGGL((bwd16<true, false, false, false>), grid, blk, lds, s, a, pl, st);
       else
-        hipLaunchKernelGGL((bwd16<false, true, false>), grid, blk, lds, s, a, pl, st);
+        hipLaunchKernelGGL((bwd16<false, true, false, false>), grid, blk, lds, s, a, pl, st);
     } else {
     const size_t lds = fast128_lds_bytes(a.nblk_out);
     if (want_dx && want_dc && beta)
-      hipLaunchKernelGGL((bwd128<true, true, true>), grid, dim3(kThreads), lds, s, a, pl, st, em);
+      hipLaunchKernelGGL((bwd128<true, true, true, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else if (want_dx && want_dc)
-      hipLaunchKernelGGL((bwd128<true, true, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
+      hipLaunchKernelGGL((bwd128<true, true, false, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else if (want_dx && beta)
-      hipLaunchKernelGGL((bwd128<true, false, true>), grid, dim3(kThreads), lds, s, a, pl, st, em);
+      hipLaunchKernelGGL((bwd128<true, false, true, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else if (want_dx)
-      hipLaunchKernelGGL((bwd128<true, false, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
+      hipLaunchKernelGGL((bwd128<true, false, false, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     else
-      hipLaunchKernelGGL((bwd128<false, true, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
+      hipLaunchKernelGGL((bwd128<false, true, false, false>), grid, dim3(kThreads), lds, s, a, pl, st, em);
     }
     rec(e1, s);
     const hipError_t e = hipGetLastError();
@@ -1412,6 +1533,114 @@ hipError_t launch_bwd128(const ff_plan* p, int count, int T, ActPtrs X, int64_t 
       hipLaunchKernelGGL(reduce128, grid, dim3(64 * kRedWaves), 0, s, a.partial, ntiles, a.slots, a.pstride,
                          p->fast.bwd_dst, scale, accumulate_dc, dC, dCs, p->fast.pad, npad, nred);
     }
+  }
+  return hipGetLastError();
+}
+
+
+hipError_t launch_fwd128_group(const ff_plan_group* g, int T, const int* tokens, const void* const* X, int64_t ldx,
+                               const float* const* cs, float scale, float beta, void* const* Y, int64_t ldy,
+                               hipStream_t s) {
+  const ff_plan* p = g->ref;
+  FastArgs a{};
+  a.frag = p->fout->dev.fs16;
+  a.T = T;
+  a.nblk_in = p->fin->dev.nblk;
+  a.nblk_out = p->fout->dev.nblk;
+  a.Xs = X;
+  a.ldx = (long)ldx;
+  a.Ys = Y;
+  a.ldy = (long)ldy;
+  a.cs = cs;
+  a.scale = scale;
+  a.beta = beta;
+  a.group = g->fast;
+  a.tokens = tokens;
+  const dim3 grid((unsigned)((T + kTT - 1) / kTT), (unsigned)g->count);
+  const size_t lds = fast128_lds_bytes(a.nblk_in);
+  hipEvent_t e0, e1;
+  take_timing_events(&e0, &e1);
+  rec(e0, s);
+  if (beta != 0.f)
+    hipLaunchKernelGGL((fwd128<true, true>), grid, dim3(kThreads), lds, s, a, nullptr, nullptr, nullptr);
+  else
+    hipLaunchKernelGGL((fwd128<false, true>), grid, dim3(kThreads), lds, s, a, nullptr, nullptr, nullptr);
+  rec(e1, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd128_group(const ff_plan_group* g, int T, const int* tokens, const void* const* X, int64_t ldx,
+                               const void* const* G, int64_t ldg, const float* const* cs, float scale, float beta_dx,
+                               void* const* dX, int64_t lddx, bool want_dx, int accumulate_dc, float* const* dCs,
+                               bool want_dc, hipStream_t s) {
+  const ff_plan* p = g->ref;
+  const unsigned count = (unsigned)g->count;
+  FastArgs a{};
+  a.frag = p->fin->dev.fs16;
+  a.T = T;
+  a.nblk_in = p->fin->dev.nblk;
+  a.nblk_out = p->fout->dev.nblk;
+  a.Xs = X;
+  a.ldx = (long)ldx;
+  a.Gs = G;
+  a.ldg = (long)ldg;
+  a.Ys = dX;
+  a.ldy = (long)lddx;
+  a.cs = cs;
+  a.scale = scale;
+  a.beta = beta_dx;
+  a.group = g->fast;
+  a.tokens = tokens;
+  const bool b16 = p->fast.bwd16 != 0;
+  const int tt = b16 ? kTT16 : kTT;
+  hipEvent_t e0, e1;
+  take_timing_events(&e0, &e1);
+  if (want_dx && T > 0) {   // every adapter's coefficients in its backward's slot order
+    const int nc = g->max_fast_slots + 256;
+    hipLaunchKernelGGL(clear_copy_group, dim3((unsigned)((nc + 255) / 256), count), dim3(256), 0, s, g->fast);
+    hipLaunchKernelGGL(scatter_bwd_coef_group, dim3((unsigned)((g->max_fast_items + 255) / 256), count), dim3(256),
+                       0, s, cs, g->fast);
+  }
+  const dim3 grid((unsigned)((T + tt - 1) / tt), count);
+  const bool beta = beta_dx != 0.f;
+  rec(e0, s);
+  if (T == 0) {
+    // no tiles: the reduction below writes zeros
+  } else if (b16) {
+    const size_t lds = fast16_lds_bytes(a.nblk_out);
+    const dim3 blk(kThreads16);
+    if (want_dx && want_dc && beta)
+      hipLaunchKernelGGL((bwd16<true, true, true, true>), grid, blk, lds, s, a, nullptr, nullptr);
+    else if (want_dx && want_dc)
+      hipLaunchKernelGGL((bwd16<true, true, false, true>), grid, blk, lds, s, a, nullptr, nullptr);
+    else if (want_dx && beta)
+      hipLaunchKernelGGL((bwd16<true, false, true, true>), grid, blk, lds, s, a, nullptr, nullptr);
+    else if (want_dx)
+      hipLaunchKernelGGL((bwd16<true, false, false, true>), grid, blk, lds, s, a, nullptr, nullptr);
+    else
+      hipLaunchKernelGGL((bwd16<false, true, false, true>), grid, blk, lds, s, a, nullptr, nullptr);
+  } else {
+    const size_t lds = fast128_lds_bytes(a.nblk_out);
+    const dim3 blk(kThreads);
+    if (want_dx && want_dc && beta)
+      hipLaunchKernelGGL((bwd128<true, true, true, true>), grid, blk, lds, s, a, nullptr, nullptr, nullptr);
+    else if (want_dx && want_dc)
+      hipLaunchKernelGGL((bwd128<true, true, false, true>), grid, blk, lds, s, a, nullptr, nullptr, nullptr);
+    else if (want_dx && beta)
+      hipLaunchKernelGGL((bwd128<true, false, true, true>), grid, blk, lds, s, a, nullptr, nullptr, nullptr);
+    else if (want_dx)
+      hipLaunchKernelGGL((bwd128<true, false, false, true>), grid, blk, lds, s, a, nullptr, nullptr, nullptr);
+    else
+      hipLaunchKernelGGL((bwd128<false, true, false, true>), grid, blk, lds, s, a, nullptr, nullptr, nullptr);
+  }
+  rec(e1, s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (want_dc) {
+    const int nred = (g->max_fast_slots + 63) / 64;
+    const int nzero = accumulate_dc ? 0 : (g->max_fast_npad + 64 * kRedWaves - 1) / (64 * kRedWaves);
+    hipLaunchKernelGGL(reduce128_group, dim3((unsigned)(nred + nzero), count), dim3(64 * kRedWaves), 0, s, g->fast,
+                       tokens, T, tt, scale, accumulate_dc, dCs);
   }
   return hipGetLastError();
 }

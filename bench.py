@@ -136,23 +136,31 @@ def bench_stack(args, torch, ff, inputs, dev):
         for d, r in ((n, rn), (m, rm)):
             if (d, r) not in frames:
                 frames[(d, r)] = ff.framegen(d, d // r, r)
-        rows, cols = inputs.support(inputs.rng(wl.seed + 10 * gi), m, n, nnz)
         count = L * len(ads)
-        plan = ff.plan_create(frames[(n, rn)], frames[(m, rm)], rows, cols, max_tokens=T, max_batch=count)
+        if args.per_layer_masks:   # every adapter its own random support: a plan group per shape
+            plans = [ff.plan_create(frames[(n, rn)], frames[(m, rm)],
+                                    *inputs.support(inputs.rng(wl.seed + 10 * gi + 1000 * (i + 1)), m, n, nnz),
+                                    max_tokens=T) for i in range(count)]
+            plan = ff.plan_group(plans)
+        else:                      # one support shared by the layers (Sec. 3.3)
+            rows, cols = inputs.support(inputs.rng(wl.seed + 10 * gi), m, n, nnz)
+            plans = [ff.plan_create(frames[(n, rn)], frames[(m, rm)], rows, cols, max_tokens=T, max_batch=count)]
+            plan = plans[0]
         Xs = [torch.randn((T, n), generator=gen, device=dev).to(tdt) for _ in range(count)]
         Gs = [torch.randn((T, m), generator=gen, device=dev).to(tdt) for _ in range(count)]
-        order = torch.from_numpy(plan.order).to(dev)
         cs = []
-        for _ in range(count):
+        for i in range(count):
+            pl = plans[i % len(plans)]
+            order = torch.from_numpy(pl.order).to(dev)
             v = torch.randn((nnz,), generator=gen, device=dev) * 0.02
-            c = torch.zeros((plan.coef_slots,), device=dev)
+            c = torch.zeros((pl.coef_slots,), device=dev)
             c[order >= 0] = v[order[order >= 0]]
             cs.append(c)
         Ys = [torch.empty((T, m), dtype=tdt, device=dev) for _ in range(count)]
         dXs = [torch.empty((T, n), dtype=tdt, device=dev) for _ in range(count)]
-        dCs = [torch.empty((plan.coef_slots,), device=dev) for _ in range(count)]
+        dCs = [torch.empty((plans[i % len(plans)].coef_slots,), device=dev) for i in range(count)]
         pa = ff.binding.pointer_array
-        groups.append(dict(name="+".join(a.name for a in ads), n=n, m=m, nnz=nnz, count=count, plan=plan,
+        groups.append(dict(name="+".join(a.name for a in ads), n=n, m=m, nnz=nnz, count=count, plan=plan, plans=plans,
                            scale=inputs.scale_for(wl, ads[0]), X=Xs, G=Gs, Y=Ys, dX=dXs, dC=dCs, c=cs,
                            fptr=(pa(Xs, dev), pa(cs, dev), pa(Ys, dev)),
                            bptr=(pa(Xs, dev), pa(Gs, dev), pa(cs, dev), pa(dXs, dev), pa(dCs, dev))))
@@ -161,13 +169,14 @@ def bench_stack(args, torch, ff, inputs, dev):
 
     def step(evs=None):
         for i, g in enumerate(groups):
+            fwd, bwd = ((ff.adapter_fwd_group, ff.adapter_bwd_group) if args.per_layer_masks else
+                        (ff.adapter_fwd_batched, ff.adapter_bwd_batched))
             if evs is not None:
                 ff.binding.time_next_kernel(evs[i][0], evs[i][1])
-            ff.adapter_fwd_batched(g["plan"], g["X"], g["c"], g["scale"], g["Y"], ptrs=g["fptr"])
+            fwd(g["plan"], g["X"], g["c"], g["scale"], g["Y"], ptrs=g["fptr"])
             if evs is not None:
                 ff.binding.time_next_kernel(evs[i][2], evs[i][3])
-            ff.adapter_bwd_batched(g["plan"], g["X"], g["G"], g["c"], g["scale"], g["dX"], g["dC"],
-                                   ptrs=g["bptr"])
+            bwd(g["plan"], g["X"], g["G"], g["c"], g["scale"], g["dX"], g["dC"], ptrs=g["bptr"])
 
     for _ in range(args.warmup):
         step()
@@ -203,8 +212,10 @@ def bench_stack(args, torch, ff, inputs, dev):
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: {L} layers x {len(wl.adapters)} projections "
                                f"({', '.join(a.name for a in wl.adapters)}), {T} tokens, batched fwd+bwd(dX,dC) "
-                               f"per projection shape",
-                   "tokens": T, "adapters": L * len(wl.adapters)},
+                               f"per projection shape"
+                               + (", a random support per adapter (plan groups)" if args.per_layer_masks else
+                                  ", one support per projection shape shared by the layers"),
+                   "tokens": T, "adapters": L * len(wl.adapters), "per_layer_masks": bool(args.per_layer_masks)},
         "roofline": {"bound": "hbm", "kernel": dom[0], "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                      "algorithmic_bytes_per_launch": dom[2], "avg_us": round(dom[1], 3)},
@@ -311,6 +322,8 @@ def main():
     ap.add_argument("--adapter", type=int, default=0, help="adapter of a multi-adapter workload (one layer)")
     ap.add_argument("--stack", action="store_true",
                     help="time every adapter of every layer of the workload (the 7B stack) as batched calls")
+    ap.add_argument("--per-layer-masks", action="store_true",
+                    help="with --stack: a random support per adapter (plan groups) instead of one per shape")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sets", type=int, default=0,
                     help="buffer sets rotated over the steps (0: enough to exceed 512 MiB; 1: one set, "

@@ -526,14 +526,16 @@ def plan_group(plans: Sequence[Plan]) -> PlanGroup:
 
 
 def adapter_fwd_group(group: PlanGroup, Xs: Sequence, cs: Sequence, scale: float, Ys: Sequence, beta: float = 0.0,
-                      tokens=None, T: Optional[int] = None, stream=None):
+                      tokens=None, T: Optional[int] = None, stream=None, ptrs=None):
     """Forward of adapter i on plans[i] (one launch).  `tokens`: optional device int32 tensor of
-    per-adapter token counts (each clamped to T, the launch size, default Xs[0].shape[0])."""
+    per-adapter token counts (each clamped to T, the launch size, default Xs[0].shape[0]).  `ptrs`
+    may hold precomputed pointer arrays (X, c, Y) from pointer_array()."""
     T = Xs[0].shape[0] if T is None else T
     _, ldx = _mat(Xs[0], "X")
     _, ldy = _mat(Ys[0], "Y")
     dev = Xs[0].device
-    px, pc, py = pointer_array(Xs, dev), pointer_array(cs, dev), pointer_array(Ys, dev)
+    px, pc, py = ptrs if ptrs is not None else (pointer_array(Xs, dev), pointer_array(cs, dev),
+                                                 pointer_array(Ys, dev))
     tp = _tokens_ptr(tokens, group.count)
     _check(_load().ff_adapter_fwd_group(group.handle, T, tp, _act_code(Xs[0]), px.data_ptr(), ldx, pc.data_ptr(),
                                         scale, beta, py.data_ptr(), ldy, _stream(stream)))
@@ -542,17 +544,21 @@ def adapter_fwd_group(group: PlanGroup, Xs: Sequence, cs: Sequence, scale: float
 
 def adapter_bwd_group(group: PlanGroup, Xs: Sequence, Gs: Sequence, cs: Optional[Sequence], scale: float,
                       dXs: Optional[Sequence], dCs: Optional[Sequence], beta_dx: float = 0.0,
-                      accumulate_dc: bool = False, tokens=None, T: Optional[int] = None, stream=None):
-    """Backward of adapter i on plans[i] (dX and/or dC; one launch plus the dC reduction)."""
+                      accumulate_dc: bool = False, tokens=None, T: Optional[int] = None, stream=None, ptrs=None):
+    """Backward of adapter i on plans[i] (dX and/or dC; one launch plus the dC reduction).  `ptrs`
+    may hold precomputed pointer arrays (X, G, c, dX, dC)."""
     T = Gs[0].shape[0] if T is None else T
     dev = Gs[0].device
     _, ldg = _mat(Gs[0], "G")
     _, ldx = _mat(Xs[0], "X")
     lddx = _mat(dXs[0], "dX")[1] if dXs is not None else group.n
-    px, pg = pointer_array(Xs, dev), pointer_array(Gs, dev)
-    pc = pointer_array(cs, dev) if cs is not None else None
-    pdx = pointer_array(dXs, dev) if dXs is not None else None
-    pdc = pointer_array(dCs, dev) if dCs is not None else None
+    if ptrs is not None:
+        px, pg, pc, pdx, pdc = ptrs
+    else:
+        px, pg = pointer_array(Xs, dev), pointer_array(Gs, dev)
+        pc = pointer_array(cs, dev) if cs is not None else None
+        pdx = pointer_array(dXs, dev) if dXs is not None else None
+        pdc = pointer_array(dCs, dev) if dCs is not None else None
     tp = _tokens_ptr(tokens, group.count)
     _check(_load().ff_adapter_bwd_group(group.handle, T, tp, _act_code(Gs[0]), px.data_ptr(), ldx, pg.data_ptr(),
                                         ldg, pc.data_ptr() if pc is not None else None, scale, beta_dx,

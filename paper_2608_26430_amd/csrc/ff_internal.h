@@ -141,6 +141,7 @@ struct FastDesc {   // fused 128-wide kernels
   float* coef;      // coefficients in backward slot order, bwd_slots + 256
   float* partial;   // dC partials, [tile][bwd_slots + 256]
   int npad, nbpad, slots, coef_slots;
+  int bwd16;        // this plan's backward runs 16-token tiles (else 8)
 };
 struct GenDesc {    // generic kernels
   GenStream fwd, bwd;
@@ -204,6 +205,7 @@ struct ff_plan_group {
   int max_fast_items = 0;         // largest coef_slots + nbpad (fused coefficient scatter)
   int max_fast_slots = 0;         // largest bwd_slots
   int max_fast_npad = 0;
+  int fast16 = 0, fast8 = 0;      // some plan's fused backward runs 16-token / 8-token tiles
   int max_gen_fwd = 0;            // largest 64 fwd.rows / 64 bwd.rows (generic streams)
   int max_gen_bwd = 0;
   int max_gen_npad = 0;

@@ -58,9 +58,8 @@ ff_status ff_plan_group_create(int64_t count, const ff_plan* const* plans, ff_pl
     if (p->fin != ref->fin || p->fout != ref->fout)
       return ff::fail(FF_EINVAL, "plan %lld uses other frames than plan 0", (long long)i);
     if (p->device != ref->device) return ff::fail(FF_EINVAL, "plan %lld is on another device", (long long)i);
-    if (p->fast.enabled != ref->fast.enabled || p->fast.bwd16 != ref->fast.bwd16)
-      return ff::fail(FF_EUNSUPPORTED, "plan %lld takes another fused-kernel path than plan 0 (%d/%d vs %d/%d)",
-                      (long long)i, p->fast.enabled, p->fast.bwd16, ref->fast.enabled, ref->fast.bwd16);
+    if (p->fast.enabled != ref->fast.enabled)
+      return ff::fail(FF_EUNSUPPORTED, "plan %lld takes another kernel path than plan 0", (long long)i);
     bool same = p->gen_nch == ref->gen_nch && p->dev.fwd_by_pos == ref->dev.fwd_by_pos;
     for (int k = 0; k < 2; ++k)
       same = same && p->gen_tile_tokens[k] == ref->gen_tile_tokens[k] && p->gen_ldt_in[k] == ref->gen_ldt_in[k] &&
@@ -84,7 +83,10 @@ ff_status ff_plan_group_create(int64_t count, const ff_plan* const* plans, ff_pl
     g->min_gen_rows = std::min(g->min_gen_rows, p->gen_rows);
     const ff::FastPlanDev& f = p->fast;
     fast[i] = ff::FastDesc{f.fwd_pl, f.fwd_st, f.fwd_em, f.bwd_pl, f.bwd_st, f.bwd_em, f.bwd_dst, f.pad, f.bwd_pad,
-                           f.bwd_pos, f.coef_bwd, p->partial, f.npad, f.nbpad, f.bwd_slots, f.coef_slots};
+                           f.bwd_pos, f.coef_bwd, p->partial, f.npad, f.nbpad, f.bwd_slots, f.coef_slots,
+                           f.bwd16};
+    g->fast16 |= f.bwd16 ? 1 : 0;
+    g->fast8 |= f.bwd16 ? 0 : 1;
     const ff::PlanDev& d = p->dev;
     gen[i] = ff::GenDesc{d.fwd, d.bwd, d.coef_pad, d.c_fwd, d.c_bwd, p->partial, d.fwd_by_pos, d.ncoef_pad};
     g->max_fast_items = std::max(g->max_fast_items, f.coef_slots + f.nbpad);

@@ -765,6 +765,7 @@ __global__ void __launch_bounds__(kThreads, 2) bwd128(FastArgs a, const int4* __
   long tile_row = (long)bi * a.ntiles + blockIdx.x;   // this tile's dC partial row
   if constexpr (GROUP) {   // the adapter's own plan, workspace (batch slot 0) and tokens
     const FastDesc* d = a.group + bi;
+    if (d->bwd16) return;   // served by the 16-token kernel of the same call
     pl = d->bwd_pl;
     bst = d->bwd_st;
     em = d->bwd_em;
@@ -1055,6 +1056,7 @@ __global__ void __launch_bounds__(kThreads16, 1) bwd16(FastArgs a, const int4* _
   long tile_row = (long)bi * a.ntiles + blockIdx.x;   // this tile's dC partial row
   if constexpr (GROUP) {   // the adapter's own plan, workspace (batch slot 0) and tokens
     const FastDesc* d = a.group + bi;
+    if (!d->bwd16) return;   // served by the 8-token kernel of the same call
     pl = d->bwd_pl;
     bst = d->bwd_st;
     a.slots = d->slots;
@@ -1282,8 +1284,7 @@ __global__ void __launch_bounds__(256) clear_copy_group(const FastDesc* group) {
 // Group calls: reduce128 over each adapter's own tiles (its token count / tt of them), slots and
 // destinations; blocks past an adapter's share return.
 __global__ void __launch_bounds__(64 * kRedWaves) reduce128_group(const FastDesc* group, const int* tokens, int T,
-                                                                  int tt, float scale, int accumulate,
-                                                                  float* const* dCs) {
+                                                                  float scale, int accumulate, float* const* dCs) {
   __shared__ float red[kRedWaves][64];
   const int bi = blockIdx.y;
   const FastDesc* d = group + bi;
@@ -1292,6 +1293,7 @@ __global__ void __launch_bounds__(64 * kRedWaves) reduce128_group(const FastDesc
   const int nred = (slots + 63) / 64;
   const int npad = accumulate ? 0 : d->npad;
   const int Tb = tokens ? max(0, min(gld(tokens)[bi], T)) : T;
+  const int tt = d->bwd16 ? kTT16 : kTT;
   const long ntiles = (Tb + tt - 1) / tt;
   if ((int)blockIdx.x >= nred) {
     const int i = ((int)blockIdx.x - nred) * 64 * kRedWaves + (int)threadIdx.x;
@@ -1591,8 +1593,6 @@ hipError_t launch_bwd128_group(const ff_plan_group* g, int T, const int* tokens,
   a.beta = beta_dx;
   a.group = g->fast;
   a.tokens = tokens;
-  const bool b16 = p->fast.bwd16 != 0;
-  const int tt = b16 ? kTT16 : kTT;
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
   if (want_dx && T > 0) {   // every adapter's coefficients in its backward's slot order
@@ -1601,12 +1601,12 @@ hipError_t launch_bwd128_group(const ff_plan_group* g, int T, const int* tokens,
     hipLaunchKernelGGL(scatter_bwd_coef_group, dim3((unsigned)((g->max_fast_items + 255) / 256), count), dim3(256),
                        0, s, cs, g->fast);
   }
-  const dim3 grid((unsigned)((T + tt - 1) / tt), count);
   const bool beta = beta_dx != 0.f;
   rec(e0, s);
-  if (T == 0) {
-    // no tiles: the reduction below writes zeros
-  } else if (b16) {
+  // adapters whose plans run 16-token tiles, then those that run 8-token tiles: each kernel skips
+  // the other kind (no tiles at all for T = 0: the reduction below writes zeros)
+  if (T > 0 && g->fast16) {
+    const dim3 grid((unsigned)((T + kTT16 - 1) / kTT16), count);
     const size_t lds = fast16_lds_bytes(a.nblk_out);
     const dim3 blk(kThreads16);
     if (want_dx && want_dc && beta)
@@ -1619,7 +1619,9 @@ hipError_t launch_bwd128_group(const ff_plan_group* g, int T, const int* tokens,
       hipLaunchKernelGGL((bwd16<true, false, false, true>), grid, blk, lds, s, a, nullptr, nullptr);
     else
       hipLaunchKernelGGL((bwd16<false, true, false, true>), grid, blk, lds, s, a, nullptr, nullptr);
-  } else {
+  }
+  if (T > 0 && g->fast8) {
+    const dim3 grid((unsigned)((T + kTT - 1) / kTT), count);
     const size_t lds = fast128_lds_bytes(a.nblk_out);
     const dim3 blk(kThreads);
     if (want_dx && want_dc && beta)
@@ -1640,7 +1642,7 @@ hipError_t launch_bwd128_group(const ff_plan_group* g, int T, const int* tokens,
     const int nred = (g->max_fast_slots + 63) / 64;
     const int nzero = accumulate_dc ? 0 : (g->max_fast_npad + 64 * kRedWaves - 1) / (64 * kRedWaves);
     hipLaunchKernelGGL(reduce128_group, dim3((unsigned)(nred + nzero), count), dim3(64 * kRedWaves), 0, s, g->fast,
-                       tokens, T, tt, scale, accumulate_dc, dCs);
+                       tokens, T, scale, accumulate_dc, dCs);
   }
   return hipGetLastError();
 }

@@ -91,6 +91,35 @@ def test_group_of_supports(dev, case, ragged):
             assert torch.equal(single[i][2], dCd[i])
 
 
+def test_group_mixes_fused_backward_tile_sizes(dev):
+    """A sparse support runs the 16-token fused backward, a dense one (streams too long for its
+    registers) the 8-token one; a group of both runs each adapter on its own kind, bitwise as the
+    single calls, with per-adapter token counts."""
+    n = m = 1024
+    f = ff.framegen(n, 64, 16)
+    g = inputs.rng(99)
+    sups = [inputs.support(g, m, n, nnz) for nnz in (3000, 40000, 3000)]
+    T = 40
+    plans = [ff.plan_create(f, f, r, c, max_tokens=T) for r, c in sups]
+    assert [p.bwd_tile_tokens for p in plans] == [16, 8, 16]
+    group = ff.plan_group(plans)
+    toks = [T, 19, 7]
+    tokens = torch.tensor(toks, dtype=torch.int32, device=dev)
+    X = [torch_act(inputs.gaussian(g, (T, n), dtype="bf16"), "bf16", dev) for _ in plans]
+    G = [torch_act(inputs.gaussian(g, (T, m), dtype="bf16"), "bf16", dev) for _ in plans]
+    c = [torch.from_numpy(p.to_plan(inputs.gaussian(g, (len(r),), std=0.02))).to(dev) for p, (r, _) in zip(plans, sups)]
+    dX = [torch.zeros((T, n), dtype=torch.bfloat16, device=dev) for _ in plans]
+    dC = [torch.empty((p.coef_slots,), device=dev) for p in plans]
+    ff.adapter_bwd_group(group, X, G, c, 0.3, dX, dC, tokens=tokens)
+    torch.cuda.synchronize()
+    for i, p in enumerate(plans):
+        t = toks[i]
+        rx, rc = ff.adapter_bwd(p, X[i][:t], G[i][:t], c[i], 0.3)
+        torch.cuda.synchronize()
+        assert torch.equal(rx, dX[i][:t]) and torch.all(dX[i][t:] == 0)
+        assert torch.equal(rc, dC[i])
+
+
 def test_group_rejects_mismatched_plans(dev):
     f16, f32_ = ff.framegen(256, 16, 16), ff.framegen(512, 16, 32)
     r, c = inputs.support(inputs.rng(1), 256, 256, 300)

@@ -20,8 +20,9 @@ LIB = os.path.join(HERE, "libframeft.so")
 SOURCES = [("capi.cpp", "capi.cpp.o", []), ("framegen.cpp", "framegen.cpp.o", []), ("plan.cpp", "plan.cpp.o", []),
            ("kernels.hip", "kernels.hip.o", []), ("kernels_w128.hip", "kernels_w128.hip.o", []),
            ("optim.hip", "optim.hip.o", []), ("group.cpp", "group.cpp.o", [])] + [
-    ("gen_inst.hip", f"gen_{d}_{t}.o", [f"-DGEN_BWD={int(d == 'bwd')}", f"-DGEN_BF16={int(t == 'bf16')}"])
-    for d in ("bwd", "fwd") for t in ("bf16", "f32")]
+    ("gen_inst.hip", f"gen_{d}_{t}{'_ms' if ms else ''}.o",
+     [f"-DGEN_BWD={int(d == 'bwd')}", f"-DGEN_BF16={int(t == 'bf16')}", f"-DGEN_MS={ms}"])
+    for d in ("bwd", "fwd") for t in ("bf16", "f32") for ms in (0, 1)]
 
 ARCH = "gfx950"
 COMMON = [

@@ -53,17 +53,30 @@ struct FrameDev {
   int W2;
   int cs;
   const float2* tw;  // [3][k2]: (cos, sin) of 2 pi (a b mod k) / k for a = 1..3, b < k2
+  // Several radix-4 stages (nst = S >= 2, k = 4^S k2): the S decimation-in-frequency stages run in
+  // registers, one thread per residue b < k2 holding x[b + k2 j] for j < 4^S, and the block is
+  // stored in LDS as ncol = 4^S columns of cs elements; column j holds the sequence whose
+  // frequency digits (a_1', ..., a_S') read j = a_1' 4^(S-1) + ... + a_S' (base-4 digit reversal
+  // of the frequency).  twk[j] = (cos, sin) of 2 pi j / k for j < k.  nst = 1 is the single stage
+  // above (twiddles staged in LDS), nst = 0 the dense block.
+  int nst;
+  int ncol;
+  const float2* twk;
 };
 
 // Position of block-local coefficient c (= 2 i + s: frequency i, real or imaginary part s)
 // inside a block's LDS storage.
 inline int lds_position(const FrameDev& f, int c) {
   if (f.radix == 1) return c;
-  const int i = c >> 1;
-  return (i & 3) * f.cs + 2 * (i >> 2) + (c & 1);
+  int r = c >> 1, col = 0;
+  for (int t = 0; t < f.nst; ++t) {   // frequency digits a_1', a_2', ..., least significant first
+    col = 4 * col + (r & 3);
+    r >>= 2;
+  }
+  return col * f.cs + 2 * r + (c & 1);
 }
 // Elements a block occupies in LDS (before padding).
-inline int lds_block_span(const FrameDev& f) { return f.radix == 1 ? f.W : 4 * f.cs; }
+inline int lds_block_span(const FrameDev& f) { return f.radix == 1 ? f.W : f.ncol * f.cs; }
 
 // Streamed sparse tables of the generic kernels.  Slots (rows of C for v = C z, columns for
 // q = C^T u) are sorted by entry count and grouped into slabs of 64; slab s is len_s >= 1 stream

@@ -21,6 +21,7 @@
 // B alone.
 #include <algorithm>
 #include <cmath>
+#include <complex>
 #include <cstring>
 #include <map>
 #include <utility>
@@ -132,6 +133,115 @@ ff_status build_host(int64_t d, int64_t k, int64_t rho,
   Frows.assign(rho / 2, {});
   for (const auto& e : F) Frows[e.r].push_back({e.j, e.v});
   return FF_OK;
+}
+
+// S-stage radix-4 factorization (S >= 2) of the realified DFT block of size k = 4^S k2, as the
+// generic kernels apply it: the input index is b + sum_t a_t K_t (K_t = k / 4^t, b < k2), the
+// stages are decimation in frequency (stage t: y_a' = w_k^(-a' n 4^(t-1)) sum_a v_a (-i)^(a a'),
+// n the index left in the parent sequence), and the 4^S sequences of length k2 then get the dense
+// k2-point DFT (M2, with the 1/sqrt(k) of the unitary transform).  Frequency
+// i = a_1' + 4 a_2' + ... + 4^(S-1) a_S' + 4^S l.  twk holds (cos, sin) of 2 pi j / k, j < k.
+// Checked against B on every unit vector, both directions (a unit input reaches one residue b).
+bool factor_multistage(const std::vector<double>& B, int64_t k, int S, std::vector<double>& M2,
+                       std::vector<double>& twk) {
+  int64_t n4 = 1;
+  for (int t = 0; t < S; ++t) n4 *= 4;
+  if (k % n4 != 0) return false;
+  const int64_t k2 = k / n4, W = 2 * k, W2 = 2 * k2;
+  const double isk = 1.0 / std::sqrt((double)k);
+  M2.assign((size_t)(W2 * W2), 0.0);
+  for (int64_t l = 0; l < k2; ++l)
+    for (int64_t b = 0; b < k2; ++b) {
+      const double th = 2.0 * M_PI * (double)((b * l) % k2) / (double)k2;
+      const double re = std::cos(th) * isk, im = -std::sin(th) * isk;
+      M2[(2 * l) * W2 + 2 * b] = re;
+      M2[(2 * l) * W2 + 2 * b + 1] = -im;
+      M2[(2 * l + 1) * W2 + 2 * b] = im;
+      M2[(2 * l + 1) * W2 + 2 * b + 1] = re;
+    }
+  twk.assign((size_t)(2 * k), 0.0);
+  for (int64_t j = 0; j < k; ++j) {
+    const double ph = 2.0 * M_PI * (double)j / (double)k;
+    twk[2 * j] = std::cos(ph);
+    twk[2 * j + 1] = std::sin(ph);
+  }
+  typedef std::complex<double> cx;
+  const cx mpow[4] = {cx(1, 0), cx(0, -1), cx(-1, 0), cx(0, 1)};   // (-i)^e
+  const cx ppow[4] = {cx(1, 0), cx(0, 1), cx(-1, 0), cx(0, -1)};    // i^e
+  // the stages on one residue's 4^S values, forward (analysis) or adjoint (synthesis)
+  auto stages = [&](std::vector<cx>& v, int64_t b, bool adjoint) {
+    for (int tt = 0; tt < S; ++tt) {
+      const int t = adjoint ? S - tt : tt + 1;
+      int64_t st = 1;
+      for (int q = t; q < S; ++q) st *= 4;
+      int64_t tws = 1;
+      for (int q = 1; q < t; ++q) tws *= 4;
+      for (int64_t hi = 0; hi < n4 / (4 * st); ++hi)
+        for (int64_t lo = 0; lo < st; ++lo) {
+          const int64_t base = hi * 4 * st + lo, n = b + k2 * lo;
+          cx in[4], out[4];
+          for (int a = 0; a < 4; ++a) in[a] = v[base + a * st];
+          auto w = [&](int64_t a) {   // w_k^(a n 4^(t-1))
+            const int64_t j = (a * n * tws) % k;
+            return cx(twk[2 * j], twk[2 * j + 1]);
+          };
+          for (int o = 0; o < 4; ++o) {
+            cx acc(0.0, 0.0);
+            if (!adjoint) {   // out_a' = conj(w^a') sum_a (-i)^(a a') in_a
+              for (int a = 0; a < 4; ++a) acc += in[a] * mpow[(a * o) % 4];
+              acc *= std::conj(w(o));
+            } else {          // out_a = sum_a' i^(a a') w^a' in_a'
+              for (int a = 0; a < 4; ++a) acc += in[a] * w(a) * ppow[(a * o) % 4];
+            }
+            out[o] = acc;
+          }
+          for (int a = 0; a < 4; ++a) v[base + a * st] = out[a];
+        }
+    }
+  };
+  auto col_of = [&](int64_t i) {   // base-4 digit reversal of i mod 4^S
+    int64_t r = i, col = 0;
+    for (int t = 0; t < S; ++t) {
+      col = 4 * col + (r & 3);
+      r >>= 2;
+    }
+    return std::make_pair(col, r);
+  };
+  std::vector<cx> v((size_t)n4);
+  // analysis of every unit vector e_u against row u of B
+  for (int64_t u = 0; u < W; ++u) {
+    const int64_t tau = u / 2, b = tau % k2, j0 = tau / k2;
+    std::fill(v.begin(), v.end(), cx(0.0, 0.0));
+    v[(size_t)j0] = (u & 1) ? cx(0.0, 1.0) : cx(1.0, 0.0);
+    stages(v, b, false);
+    double err = 0.0;
+    for (int64_t c = 0; c < W; ++c) {
+      const auto cl = col_of(c >> 1);
+      const int64_t o = 2 * cl.second + (c & 1);
+      const cx y = v[(size_t)cl.first];
+      const double z = M2[o * W2 + 2 * b] * y.real() + M2[o * W2 + 2 * b + 1] * y.imag();
+      err = std::max(err, std::fabs(z - B[u * W + c]));
+    }
+    if (err > 1e-12) return false;
+  }
+  // synthesis of every unit coefficient e_c against column c of B
+  for (int64_t c = 0; c < W; ++c) {
+    const auto cl = col_of(c >> 1);
+    const int64_t o = 2 * cl.second + (c & 1);
+    double err = 0.0;
+    for (int64_t b = 0; b < k2; ++b) {
+      std::fill(v.begin(), v.end(), cx(0.0, 0.0));
+      v[(size_t)cl.first] = cx(M2[o * W2 + 2 * b], M2[o * W2 + 2 * b + 1]);   // row o of M2 = column of M2^T
+      stages(v, b, true);
+      for (int64_t j = 0; j < n4; ++j) {
+        const int64_t u = 2 * (b + k2 * j);
+        err = std::max(err, std::fabs(v[(size_t)j].real() - B[u * W + c]));
+        err = std::max(err, std::fabs(v[(size_t)j].imag() - B[(u + 1) * W + c]));
+      }
+    }
+    if (err > 1e-12) return false;
+  }
+  return true;
 }
 
 // Radix-4 factorization of the block (Sec. 3.2 modulation: with k*rho = d the block B is the
@@ -278,7 +388,7 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   const int64_t W = 2 * k;
   if (W % 8 != 0)
     return ff::fail(FF_EUNSUPPORTED, "GPU path needs 2k to be a multiple of 8 (k=%lld)", (long long)k);
-  if (W > 2048) return ff::fail(FF_EUNSUPPORTED, "frame block 2k=%lld too wide", (long long)W);
+  if (W > 4096) return ff::fail(FF_EUNSUPPORTED, "frame block 2k=%lld too wide (at most 4096)", (long long)W);
 
   // Extract the diagonal block and confirm that P is block diagonal with identical blocks.
   std::vector<double> B((size_t)(W * W), 0.0);
@@ -328,17 +438,33 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) return ff::fail(FF_EDEVICE, "no HIP device");
 
-  // Blocks wider than 128 are applied in factored form when the radix-4 split reproduces them.
-  std::vector<double> M2, tw;
-  const bool factored = W > 128 && W / 4 <= 128 && factor_radix4(B, k, M2, tw);
+  // Blocks wider than 128 are applied in factored form when the radix-4 split reproduces them:
+  // one stage up to 512 wide, beyond that 2 or 3 stages leaving a DFT of at most 64 points.
+  std::vector<double> M2, tw, twk;
+  int nst = 0;
+  if (W > 128 && W / 4 <= 128 && factor_radix4(B, k, M2, tw)) {
+    nst = 1;
+  } else if (W > 512) {
+    for (int S = 2; S <= 3 && nst == 0; ++S) {
+      const int64_t n4 = (int64_t)1 << (2 * S);
+      if (k % n4 == 0 && k / n4 <= 64 && factor_multistage(B, k, S, M2, twk)) nst = S;
+    }
+    if (nst == 0)
+      return ff::fail(FF_EUNSUPPORTED, "frame block 2k=%lld: k is not 4^S k2 with S <= 3 and k2 <= 64",
+                      (long long)W);
+  }
+  const bool factored = nst > 0;
+  const int64_t n4 = factored ? (int64_t)1 << (2 * nst) : 1;
 
   ff::FrameDev fd{};
   fd.d = (int)d;
   fd.W = (int)W;
   fd.nblk = (int)(rho / 2);
   fd.radix = factored ? 4 : 1;
-  fd.k2 = factored ? (int)(k / 4) : (int)k;
-  fd.W2 = factored ? (int)(W / 4) : (int)W;
+  fd.nst = nst;
+  fd.ncol = (int)n4;
+  fd.k2 = factored ? (int)(k / n4) : (int)k;
+  fd.W2 = factored ? (int)(W / n4) : (int)W;
   fd.cs = (fd.W2 + 7) / 8 * 8;
   const int64_t W2 = fd.W2;
   fd.MT = (int)((W2 + 15) / 16);
@@ -379,12 +505,13 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
     }
   for (size_t e = 0; e < B32.size(); ++e) B32[e] = (float)B[e];
 
-  std::vector<float> tw32(std::max<size_t>(tw.size(), 2));
+  std::vector<float> tw32(std::max<size_t>(tw.size(), 2)), twk32(std::max<size_t>(twk.size(), 2));
   for (size_t e = 0; e < tw.size(); ++e) tw32[e] = (float)tw[e];
+  for (size_t e = 0; e < twk.size(); ++e) twk32[e] = (float)twk[e];
 
-  const size_t b16 = n16 * 2, b32 = n32 * 4, bB = B32.size() * 4, bT = tw32.size() * 4;
+  const size_t b16 = n16 * 2, b32 = n32 * 4, bB = B32.size() * 4, bT = tw32.size() * 4, bK = twk32.size() * 4;
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t total = 2 * up(b16) + 2 * up(b32) + up(bB) + up(bT);
+  const size_t total = 2 * up(b16) + 2 * up(b32) + up(bB) + up(bT) + up(bK);
   void* mem = nullptr;
   if (hipMalloc(&mem, total) != hipSuccess) {
     (void)hipGetLastError();
@@ -403,7 +530,8 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   fd.fs32 = put(fs32.data(), b32);
   fd.B32 = (const float*)put(B32.data(), bB);
   fd.tw = (const float2*)put(tw32.data(), bT);
-  if (!fd.fa16 || !fd.fs16 || !fd.fa32 || !fd.fs32 || !fd.B32 || !fd.tw) {
+  fd.twk = (const float2*)put(twk32.data(), bK);
+  if (!fd.fa16 || !fd.fs16 || !fd.fa32 || !fd.fs32 || !fd.B32 || !fd.tw || !fd.twk) {
     (void)hipFree(mem);
     return ff::fail(FF_EDEVICE, "copying frame to the device failed");
   }

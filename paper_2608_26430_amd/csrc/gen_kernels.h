@@ -312,9 +312,9 @@ __device__ __forceinline__ int div_small(int x, int d, float inv) {
   return q;
 }
 
-// The twiddle factors of a factored frame, copied to LDS (the caller synchronizes).
+// The twiddle factors of a single-stage factored frame, copied to LDS (the caller synchronizes).
 __device__ __forceinline__ void stage_twiddles(const FrameDev& f, float2* lds) {
-  if (f.radix == 1) return;
+  if (f.radix == 1 || f.nst != 1) return;
   const float2* tw = (f.tw);
   for (int i = threadIdx.x; i < 3 * f.k2; i += blockDim.x) lds[i] = gload(&tw[i]);
 }
@@ -417,22 +417,160 @@ __device__ __forceinline__ void radix4_synthesis(const FrameDev& f, const float2
   }
 }
 
+// Multi-stage factored analysis, k = 4^S k2 (S = 2 or 3), for every (token, block, b < k2) of a
+// tile: the item holds v[j] = x[b + k2 j] for j < 4^S (the digits of j, most significant first,
+// are the stage digits a_1 .. a_S of the input index b + sum_t a_t K_t, K_t = k / 4^t) and runs
+// the S decimation-in-frequency stages in registers.  Stage t combines over digit a_t with the
+// other digits fixed, y_a' = sum_a v_a (-i)^(a a'), then scales y_a' by w_k^(-a' n 4^(t-1)), where
+// n = b + k2 lo is the index left in the parent sequence (lo: the digits below a_t).  The output
+// digit a_t' takes a_t's place, so v[j] ends as sequence j = (a_1' .. a_S') at b, stored in LDS
+// column j (base-4 digit reversal of the frequency, lds_position), where the MFMA applies the dense
+// DFT of size k2.  fp32 throughout; LDS receives the activation type.
+// Stage T of S on the 4^S values (T a template parameter, so that every index into v is a
+// constant and v stays in registers).
+template <int S, int T, bool INV>
+__device__ __forceinline__ void msr_stage(float2 (&v)[1 << (2 * S)], int b, int k2, const float2* __restrict__ twk) {
+  constexpr int N = 1 << (2 * S);
+  constexpr int st = 1 << (2 * (S - T));     // stride of digit a_T in j
+  constexpr int tws = 1 << (2 * (T - 1));    // w_{K_{T-1}} = w_k^(4^(T-1))
+  constexpr bool inverse = INV;
+  // w_k^(a (b + k2 lo) tws) = w_k^(a b tws) w_k^(a k2 lo tws): a per-lane base loaded once per
+  // stage times a factor that is the same in every lane (k = 4^S k2 makes it a 4^S-th root of
+  // unity), so that few twiddles are in registers at a time
+  float2 wb[3];
+#pragma unroll
+  for (int a = 1; a < 4; ++a) wb[a - 1] = gload(twk + a * b * tws);
+  {
+#pragma unroll
+    for (int hi = 0; hi < N / (4 * st); ++hi)
+#pragma unroll
+      for (int lo = 0; lo < st; ++lo) {
+        const int base = hi * 4 * st + lo;
+        float2 w[3];
+#pragma unroll
+        for (int a = 1; a < 4; ++a) {
+          // the same address in every lane: read through the constant address space, as a scalar
+          // load into SGPRs
+          using R = Raw<sizeof(float2)>::T;
+          const float2 wu =
+              __builtin_bit_cast(float2, *((const __attribute__((address_space(4))) R*)(twk + a * k2 * lo * tws)));
+          w[a - 1] = lo == 0 ? wb[a - 1] : cmul(wb[a - 1], wu);
+        }
+        if constexpr (!inverse) {
+          const float2 x0 = v[base], x1 = v[base + st], x2 = v[base + 2 * st], x3 = v[base + 3 * st];
+          const float2 s02 = cadd(x0, x2), d02 = csub(x0, x2), s13 = cadd(x1, x3), d13 = csub(x1, x3);
+          v[base] = cadd(s02, s13);
+          v[base + st] = cmulc(make_float2(d02.x + d13.y, d02.y - d13.x), w[0]);      // d02 - i d13
+          v[base + 2 * st] = cmulc(csub(s02, s13), w[1]);
+          v[base + 3 * st] = cmulc(make_float2(d02.x - d13.y, d02.y + d13.x), w[2]);  // d02 + i d13
+        } else {   // the adjoint of the stage: twiddles w instead of conj(w), then i^(a a')
+          const float2 y0 = v[base], y1 = cmul(v[base + st], w[0]), y2 = cmul(v[base + 2 * st], w[1]),
+                       y3 = cmul(v[base + 3 * st], w[2]);
+          const float2 s02 = cadd(y0, y2), d02 = csub(y0, y2), s13 = cadd(y1, y3), d13 = csub(y1, y3);
+          v[base] = cadd(s02, s13);
+          v[base + st] = make_float2(d02.x - d13.y, d02.y + d13.x);        // d02 + i d13
+          v[base + 2 * st] = csub(s02, s13);
+          v[base + 3 * st] = make_float2(d02.x + d13.y, d02.y - d13.x);    // d02 - i d13
+        }
+      }
+  }
+}
+
+// All S stages: 1 .. S for the analysis, the adjoints S .. 1 for the synthesis.
+template <int S>
+__device__ __forceinline__ void msr_stages(float2 (&v)[1 << (2 * S)], int b, int k2, const float2* __restrict__ twk,
+                                           bool inverse) {
+  if (!inverse) {
+    msr_stage<S, 1, false>(v, b, k2, twk);
+    if constexpr (S >= 2) msr_stage<S, 2, false>(v, b, k2, twk);
+    if constexpr (S >= 3) msr_stage<S, 3, false>(v, b, k2, twk);
+  } else {
+    if constexpr (S >= 3) msr_stage<S, 3, true>(v, b, k2, twk);
+    if constexpr (S >= 2) msr_stage<S, 2, true>(v, b, k2, twk);
+    msr_stage<S, 1, true>(v, b, k2, twk);
+  }
+}
+
+template <bool BF16, int S>
+__device__ __forceinline__ void msr_analysis(const FrameDev& f, int nt, const typename Act<BF16>::E* src, long ld,
+                                             typename Act<BF16>::E* dst, int ldt, int ldb) {
+  using E = typename Act<BF16>::E;
+  constexpr int N = 1 << (2 * S);
+  const int k2 = f.k2, W = f.W, cs = f.cs, W2 = f.W2;
+  const int per_tok = f.nblk * k2, items = nt * per_tok;
+  const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
+  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+    const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
+    const int b = r - blk * k2;
+    const E* xp = src + (long)t * ld + blk * W + 2 * b;
+    float2 v[N];
+#pragma unroll
+    for (int j = 0; j < N; ++j) v[j] = gld2<BF16>(xp + 2 * k2 * j);
+    msr_stages<S>(v, b, k2, f.twk, false);
+    E* y = dst + t * ldt + blk * ldb + 2 * b;
+#pragma unroll
+    for (int j = 0; j < N; ++j) st2<BF16>(y + j * cs, v[j]);
+    if (b == 0)
+      for (int j = 0; j < N; ++j)
+        for (int e = W2; e < cs; ++e) Act<BF16>::st(y + j * cs + e, 0.f);
+  }
+}
+
+// Multi-stage factored synthesis: the inverse stages on each (token, block, b) item read from the
+// LDS columns (after the dense DFT^H), then out = s x (+ beta out) into the token rows at dst.
+template <bool BF16, int S>
+__device__ __forceinline__ void msr_synthesis(const FrameDev& f, int nt, const typename Act<BF16>::E* src, int ldt,
+                                              int ldb, typename Act<BF16>::E* dst, long ld, float s, float beta) {
+  using E = typename Act<BF16>::E;
+  constexpr int N = 1 << (2 * S);
+  const int k2 = f.k2, W = f.W, cs = f.cs;
+  const int per_tok = f.nblk * k2, items = nt * per_tok;
+  const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
+  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+    const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
+    const int b = r - blk * k2;
+    const E* yp = src + t * ldt + blk * ldb + 2 * b;
+    float2 v[N];
+#pragma unroll
+    for (int j = 0; j < N; ++j) v[j] = ld2<BF16>(yp + j * cs);
+    msr_stages<S>(v, b, k2, f.twk, true);
+    E* out = dst + (long)t * ld + blk * W + 2 * b;
+    // in groups of 16, so that the old values of a beta epilogue are not all loaded at once
+#pragma unroll
+    for (int j0 = 0; j0 < N; j0 += 16) {
+#pragma unroll
+      for (int j = j0; j < j0 + 16 && j < N; ++j) {
+        float2 o = make_float2(s * v[j].x, s * v[j].y);
+        if (beta != 0.f) {
+          const float2 old = gld2<BF16>(out + 2 * k2 * j);
+          o.x = fmaf(beta, old.x, o.x);
+          o.y = fmaf(beta, old.y, o.y);
+        }
+        gst2<BF16>(out + 2 * k2 * j, o);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
 // Zero the padding of every column of a factored tile whose coefficients another phase writes
 // (the MFMA reads whole columns of cs elements).
 template <bool BF16>
 __device__ __forceinline__ void zero_column_pads(const FrameDev& f, int nt, typename Act<BF16>::E* tile, int ldt,
                                                  int ldb) {
   if (f.radix == 1 || f.cs == f.W2) return;
-  const int padw = f.cs - f.W2, per_tok = f.nblk * 4 * padw, items = nt * per_tok;
+  const int padw = f.cs - f.W2, per_tok = f.nblk * f.ncol * padw, items = nt * per_tok;
   for (int it = threadIdx.x; it < items; it += blockDim.x) {
     const int t = it / per_tok, r = it - t * per_tok, col = r / padw, e = r - col * padw;
-    const int blk = col >> 2, a = col & 3;
+    const int blk = col / f.ncol, a = col - blk * f.ncol;
     Act<BF16>::st(tile + t * ldt + blk * ldb + a * f.cs + f.W2 + e, 0.f);
   }
 }
 
 // z = P^T x for a tile: token rows at src (global) -> coefficients in the LDS tile.
-template <bool BF16>
+// MS: the frame may be applied in several radix-4 stages (nst >= 2); only the kernels built for
+// such frames carry that code, so the others keep their register allocation.
+template <bool BF16, bool MS = false>
 __device__ __forceinline__ void analysis_to_lds(const FrameDev& f, const float2* tw, int nt,
                                                 const typename Act<BF16>::E* src, long ld, typename Act<BF16>::E* dst,
                                                 int ldt, int ldb) {
@@ -455,15 +593,22 @@ __device__ __forceinline__ void analysis_to_lds(const FrameDev& f, const float2*
         });
     return;
   }
-  radix4_analysis<BF16>(f, tw, nt, src, ld, dst, ldt, ldb);
+  if (!MS || f.nst == 1)
+    radix4_analysis<BF16>(f, tw, nt, src, ld, dst, ldt, ldb);
+  else if constexpr (MS) {
+    if (f.nst == 2)
+      msr_analysis<BF16, 2>(f, nt, src, ld, dst, ldt, ldb);
+    else
+      msr_analysis<BF16, 3>(f, nt, src, ld, dst, ldt, ldb);
+  }
   __syncthreads();
-  const int cs = f.cs;
+  const int cs = f.cs, ncol = f.ncol;
   auto at = [&](int c) -> E* {
-    const int tb = c >> 2, t = tb / nblk;
-    return dst + t * ldt + (tb - t * nblk) * ldb + (c & 3) * cs;
+    const int tb = c / ncol, t = tb / nblk;
+    return dst + t * ldt + (tb - t * nblk) * ldb + (c - tb * ncol) * cs;
   };
   column_apply<BF16, false>(
-      f, false, nt * nblk * 4, cs, [&](int c) -> const E* { return at(c); },
+      f, false, nt * nblk * ncol, cs, [&](int c) -> const E* { return at(c); },
       [&](int c, int o, f32x4 v) {
         if (o < cs) A::st4(at(c) + o, v);
       });
@@ -471,7 +616,7 @@ __device__ __forceinline__ void analysis_to_lds(const FrameDev& f, const float2*
 
 // out = s P q (+ beta out) for a tile: coefficients in the LDS tile at src -> token rows at dst.
 // Factored frames transform the tile in place first, so src is overwritten.
-template <bool BF16>
+template <bool BF16, bool MS = false>
 __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const float2* tw, int nt,
                                                    typename Act<BF16>::E* src, int ldt, int ldb,
                                                    typename Act<BF16>::E* dst, long ld, float s, float beta) {
@@ -497,18 +642,25 @@ __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const floa
         });
     return;
   }
-  const int cs = f.cs;
+  const int cs = f.cs, ncol = f.ncol;
   auto at = [&](int c) -> E* {
-    const int tb = c >> 2, t = tb / nblk;
-    return src + t * ldt + (tb - t * nblk) * ldb + (c & 3) * cs;
+    const int tb = c / ncol, t = tb / nblk;
+    return src + t * ldt + (tb - t * nblk) * ldb + (c - tb * ncol) * cs;
   };
   column_apply<BF16, false>(
-      f, true, nt * nblk * 4, cs, [&](int c) -> const E* { return at(c); },
+      f, true, nt * nblk * ncol, cs, [&](int c) -> const E* { return at(c); },
       [&](int c, int o, f32x4 v) {
         if (o < cs) A::st4(at(c) + o, v);
       });
   __syncthreads();
-  radix4_synthesis<BF16>(f, tw, nt, src, ldt, ldb, dst, ld, s, beta);
+  if (!MS || f.nst == 1)
+    radix4_synthesis<BF16>(f, tw, nt, src, ldt, ldb, dst, ld, s, beta);
+  else if constexpr (MS) {
+    if (f.nst == 2)
+      msr_synthesis<BF16, 2>(f, nt, src, ldt, ldb, dst, ld, s, beta);
+    else
+      msr_synthesis<BF16, 3>(f, nt, src, ldt, ldb, dst, ld, s, beta);
+  }
 }
 
 // Sparse products over a generic stream (GenStream).  Each wave walks its run of stream rows
@@ -700,7 +852,7 @@ __device__ __forceinline__ int group_tokens(const int* tokens, int T, int bi) {
 
 // CHUNKED: the input side in a.nch chunks of blocks, v accumulated over them; otherwise whole
 // (a.nch == 1), in code of its own.
-template <bool BF16, bool CHUNKED>
+template <bool BF16, bool CHUNKED, bool MS = false>
 __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   using A = Act<BF16>;
   using E = typename A::E;
@@ -735,7 +887,7 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   zero_column_pads<BF16>(a.fout, nt, vt, a.ldt_out, a.ldb_out);
   if constexpr (!CHUNKED) {
     // analysis: z = P_in^T x for every (token, input block)
-    analysis_to_lds<BF16>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
+    analysis_to_lds<BF16, MS>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
     __syncthreads();
 
     // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
@@ -747,7 +899,7 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
       FrameDev fc = a.fin;
       fc.nblk = a.chunk_blk[ch + 1] - b0;
       if (ch > 0) __syncthreads();   // the previous chunk's products are done reading z
-      analysis_to_lds<BF16>(fc, tw_in, nt, X + (long)b0 * a.fin.W, a.ldx, zt, a.ldt_in, a.ldb_in);
+      analysis_to_lds<BF16, MS>(fc, tw_in, nt, X + (long)b0 * a.fin.W, a.ldx, zt, a.ldt_in, a.ldb_in);
       __syncthreads();
 
       // v[a] (+)= sum over the chunk's entries of row a of c_e z[b_e]
@@ -759,7 +911,7 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   __syncthreads();
 
   // synthesis and epilogue: y = beta y + s P_out v
-  synthesis_from_lds<BF16>(a.fout, tw_out, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, a.scale, a.beta);
+  synthesis_from_lds<BF16, MS>(a.fout, tw_out, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, a.scale, a.beta);
 }
 
 struct BwdArgs {
@@ -791,7 +943,7 @@ struct BwdArgs {
 
 // CHUNKED: the input side in a.nch chunks of blocks; otherwise whole (a.nch == 1), in code of
 // its own (the chunk loop costs registers that the whole-side kernel then spills).
-template <bool BF16, bool CHUNKED>
+template <bool BF16, bool CHUNKED, bool MS = false>
 __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   using A = Act<BF16>;
   using E = typename A::E;
@@ -832,8 +984,8 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
     if constexpr (!CHUNKED) {
       // q is written over z and then synthesized from whole columns: their padding must be zero
       zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
-      analysis_to_lds<BF16>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
-      if (a.want_dc) analysis_to_lds<BF16>(a.fin, tw_in, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
+      analysis_to_lds<BF16, MS>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
+      if (a.want_dc) analysis_to_lds<BF16, MS>(a.fin, tw_in, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
       __syncthreads();
 
       // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
@@ -841,11 +993,11 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
       if (!a.want_dx) continue;
       __syncthreads();
 
-      synthesis_from_lds<BF16>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale,
+      synthesis_from_lds<BF16, MS>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale,
                                a.beta);
       continue;
     }
-    analysis_to_lds<BF16>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
+    analysis_to_lds<BF16, MS>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
     for (int ch = 0; ch < a.nch; ++ch) {
       // the chunk's blocks as a frame of their own, at column b0 W of the token rows
       const int b0 = a.chunk_blk[ch];
@@ -855,7 +1007,7 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
       if (ch > 0) __syncthreads();   // the previous chunk is done with the z / q tile
       // q is written over z and then synthesized from whole columns: their padding must be zero
       zero_column_pads<BF16>(fc, nt, zt, a.ldt_in, a.ldb_in);
-      if (a.want_dc) analysis_to_lds<BF16>(fc, tw_in, nt, X0 + t0 * a.ldx + col0, a.ldx, zt, a.ldt_in, a.ldb_in);
+      if (a.want_dc) analysis_to_lds<BF16, MS>(fc, tw_in, nt, X0 + t0 * a.ldx + col0, a.ldx, zt, a.ldt_in, a.ldb_in);
       __syncthreads();
 
       // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
@@ -865,7 +1017,7 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
       if (!a.want_dx) continue;
       __syncthreads();
 
-      synthesis_from_lds<BF16>(fc, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx + col0, a.lddx, a.scale,
+      synthesis_from_lds<BF16, MS>(fc, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx + col0, a.lddx, a.scale,
                                a.beta);
     }
   }

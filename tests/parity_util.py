@@ -127,8 +127,10 @@ def _depth(P):
 
 
 def _kappa(k):
-    """Frame application: direct for blocks up to 128 wide, factored beyond (see above)."""
-    return 1.0 if 2 * k <= 128 else 4.0
+    """Frame application: direct for blocks up to 128 wide, one radix-4 stage up to 512 wide, two
+    or three stages beyond (the stages' butterflies sum up to 4^S unit-modulus terms per value, so
+    the absolute products of the factors reach a few times |P|; see above)."""
+    return 1.0 if 2 * k <= 128 else 4.0 if 2 * k <= 512 else 8.0
 
 
 def coef_matrix(rows, cols, vals, scale, m_coef, n_coef):

@@ -200,6 +200,12 @@ struct ff_plan {
   int gen_wgs = 1;                 // compute units: resident workgroups of the generic kernels
   int gen_rows = 1;                // dC partial rows per adapter = most workgroups of the generic backward
   float* partial = nullptr;        // dC partial sums per tile (layout depends on the kernels)
+  // Merge through the backward (frames applied in several radix-4 stages): mrg_rows output rows at
+  // a time, their unit vectors as fp32 "upstream gradients" (mrg_rows x m) and, for bf16 or
+  // unaligned weights, the fp32 rows before they are added in (mrg_rows x n).
+  int mrg_rows = 0;
+  float* mrg_g = nullptr;
+  float* mrg_out = nullptr;
   size_t workspace_bytes = 0;
   void* dev_mem = nullptr;
   ff::PlanDev dev{};

@@ -598,8 +598,11 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   enum {
     kGfEnt, kGfCoef, kGfWave, kGbEnt, kGbCoef, kGbWave, kCoefPad, kCfwd, kCbwd, kMrgPtr, kMrgEnt,
     kFPl, kBPl, kFSt, kPadSlots, kBW, kPartial, kCoefBwd, kBwdPos, kFEm, kBDst, kBEm, kBPad, kUserOfSlot,
-    kSlotOfUser, kNumBlobs
+    kSlotOfUser, kMrgG, kMrgOut, kNumBlobs
   };
+  // frames applied in several radix-4 stages merge through the backward, a chunk of rows at a time
+  const bool mrg_transform = FI.nst >= 2 || FO.nst >= 2;
+  const int64_t mrg_rows = mrg_transform ? std::min<int64_t>(m, 1024) : 0;
   // both directions of the coefficient layout, for the device-side conversions
   std::vector<int> user_of_slot32(p->user_order.begin(), p->user_order.end());
   std::vector<Blob> blobs(kNumBlobs);
@@ -631,6 +634,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   blobs[kBPad] = {b_pad.data(), b_pad.size() * sizeof(int)};
   blobs[kUserOfSlot] = {user_of_slot32.data(), user_of_slot32.size() * sizeof(int)};
   blobs[kSlotOfUser] = {slot_of_user.data(), (size_t)nnz * sizeof(int)};
+  blobs[kMrgG] = {nullptr, (size_t)mrg_rows * (size_t)m * sizeof(float)};
+  blobs[kMrgOut] = {nullptr, (size_t)mrg_rows * (size_t)n * sizeof(float)};
   size_t total = 0;
   for (const Blob& b : blobs) total += up(b.bytes);
   int cur = 0;
@@ -675,6 +680,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   pd.user_of_slot = (const int*)where[kUserOfSlot];
   pd.slot_of_user = (const int*)where[kSlotOfUser];
   pd.nnz_user = (int)nnz;
+  p->mrg_rows = (int)mrg_rows;
+  p->mrg_g = (float*)where[kMrgG];
+  p->mrg_out = (float*)where[kMrgOut];
   ff::FastPlanDev& fp = p->fast;
   fp.enabled = fast ? 1 : 0;
   fp.fwd_pl = (const int4*)where[kFPl];

@@ -95,6 +95,13 @@ WORKLOADS = {
     "cfg5_vitb16_qkv": Workload("cfg5_vitb16_qkv", 64 * 197, "bf16", 250.0,
                                 (Adapter("qkv", 768, 2304, 64, 64, 3_000),),
                                 seed=SEED_BASE + 5 + 50),
+    # The paper's own frames (Sec. 4.1, 4.2): subspace dimension 2, k rho = d, so each frame is
+    # one realified DFT of size d/2.  Llama-2-7B q_proj with the instruction-tuning support of
+    # 5000 coefficients, and a RoBERTa-large-sized 1024-wide query with 1000 coefficients.
+    "rho2_llama7b_qproj": Workload("rho2_llama7b_qproj", 4096, "bf16", 200.0,
+                                   (Adapter("q_proj", 4096, 4096, 2, 2, 5_000),), seed=SEED_BASE + 6),
+    "rho2_roberta_large_query": Workload("rho2_roberta_large_query", 4096, "bf16", 20.0,
+                                         (Adapter("query", 1024, 1024, 2, 2, 1_000),), seed=SEED_BASE + 7),
 }
 
 

@@ -76,6 +76,39 @@ def test_rho2_fwd_bwd_parity(dev, case, dtype):
     _ok("dC", user_dc(plan, dC), bb.dc, bb.bdc)
 
 
+def test_rho2_merge_through_backward(dev):
+    """d = 4096: the merge runs as the backward of unit vectors, 1024 rows at a time: into an
+    aligned fp32 array (directly), a misaligned fp32 view (through the staging rows) and in place
+    into a bf16 weight; sampled rows against the oracle."""
+    from tests.parity_util import merged_bf16_ok
+    d, nnz = 4096, 5000
+    k = d // 2
+    g = inputs.rng(11)
+    rows, cols = inputs.support(g, d, d, nnz)
+    vals = inputs.gaussian(g, (nnz,), std=0.02)
+    s = 200.0 / d
+    f = ff.framegen(d, k, 2)
+    plan = ff.plan_create(f, f, rows, cols, max_tokens=1)
+    c = torch.from_numpy(plan.to_plan(vals)).to(dev)
+    Wd = ff.merge_delta(plan, c, s, torch.full((d, d), float("nan"), device=dev), beta=0.0)
+    buf = torch.zeros(d * (d + 1) + 1, device=dev)
+    Wu = buf[1:].view(d, d + 1)[:, :d]                 # 4 bytes off 16-byte alignment, odd ldw
+    Wu.copy_(Wd)
+    ff.merge_delta(plan, c, -s, Wu, beta=1.0)          # unmerge: back to zero
+    W0 = inputs.weight(inputs.rng(12), d, d, "bf16")
+    Wb = ff.merge_delta(plan, c, s, torch_act(W0, "bf16", dev), beta=1.0)
+    torch.cuda.synchronize()
+    P = oracle_frame(k, 2, d)
+    r = np.unique(np.concatenate([[0, 1, 2047, 2048, d - 1], np.random.default_rng(3).integers(0, d, 11)]))
+    dw = O.merge_delta_rows(P, P, rows, cols, vals, s, r)
+    dW_abs, depth = merge_abs_terms(P, P, rows, cols, vals, s, 2, 2, r)
+    _ok("dW", to_np(Wd[r]), dw, merge_bound(dW_abs, depth))
+    _ok("unmerged", to_np(Wu[r]), np.zeros_like(dw), 2 * merge_bound(dW_abs, depth))
+    assert merged_bf16_ok(to_np(Wb[r]), W0[r], dw, dW_abs, depth)
+    nrm = float(torch.linalg.vector_norm(Wd.double()))   # orthogonal frames: ||dW||_F = |s| ||C||_F
+    assert abs(nrm - abs(s) * np.linalg.norm(vals.astype(np.float64))) <= 1e-5 * nrm
+
+
 def test_rho2_merge_parity(dev):
     d, nnz = 1024, 1000
     k = d // 2

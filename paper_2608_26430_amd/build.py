@@ -19,7 +19,8 @@ LIB = os.path.join(HERE, "libframeft.so")
 # once per direction and activation type, so that their long compiles run in parallel
 SOURCES = [("capi.cpp", "capi.cpp.o", []), ("framegen.cpp", "framegen.cpp.o", []), ("plan.cpp", "plan.cpp.o", []),
            ("kernels.hip", "kernels.hip.o", []), ("kernels_w128.hip", "kernels_w128.hip.o", []),
-           ("optim.hip", "optim.hip.o", []), ("group.cpp", "group.cpp.o", [])] + [
+           ("optim.hip", "optim.hip.o", []), ("group.cpp", "group.cpp.o", []),
+           ("lift.hip", "lift.hip.o", [])] + [
     ("gen_inst.hip", f"gen_{d}_{t}{'_ms' if ms else ''}.o",
      [f"-DGEN_BWD={int(d == 'bwd')}", f"-DGEN_BF16={int(t == 'bf16')}", f"-DGEN_MS={ms}"])
     for d in ("bwd", "fwd") for t in ("bf16", "f32") for ms in (0, 1)]

@@ -39,10 +39,16 @@ bool aligned(const void* ptr, int act) {
   return ((uintptr_t)ptr % 16) == 0;
 }
 
-ff_status check_act(const char* name, const void* ptr, int64_t ld, int64_t width, int act) {
+// Activation arrays.  Plans with a lift read and write the caller's rows one element at a time
+// (lift.hip), so they need only element alignment; the other kernels use 16-byte accesses.
+ff_status check_act(const char* name, const void* ptr, int64_t ld, int64_t width, int act, bool lifted = false) {
   if (!ptr) return ff::fail(FF_EINVAL, "%s is NULL", name);
   if (ld < width) return ff::fail(FF_EINVAL, "leading dimension of %s (%lld) < %lld", name, (long long)ld,
                                   (long long)width);
+  if (lifted) {
+    if ((uintptr_t)ptr % (act == FF_BF16 ? 2 : 4)) return ff::fail(FF_EINVAL, "%s is misaligned", name);
+    return FF_OK;
+  }
   const int64_t mult = act == FF_BF16 ? 8 : 4;
   if (ld % mult) return ff::fail(FF_EINVAL, "leading dimension of %s must be a multiple of %lld", name,
                                  (long long)mult);
@@ -87,9 +93,9 @@ ff_status check_bwd(const ff_plan* p, int64_t T, int act, const void* X, int64_t
     *done = true;
     return FF_OK;
   }
-  if ((st = check_act("G", G, ldg, p->fout->d, act)) != FF_OK) return st;
-  if (*want_dc && (st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
-  if (*want_dx && (st = check_act("dX", dX, lddx, p->fin->d, act)) != FF_OK) return st;
+  if ((st = check_act("G", G, ldg, p->fout->d, act, p->lifted)) != FF_OK) return st;
+  if (*want_dc && (st = check_act("X", X, ldx, p->fin->d, act, p->lifted)) != FF_OK) return st;
+  if (*want_dx && (st = check_act("dX", dX, lddx, p->fin->d, act, p->lifted)) != FF_OK) return st;
   if (*want_dx && p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
   if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
   return FF_OK;
@@ -156,10 +162,14 @@ ff_status ff_adapter_fwd(const ff_plan* p, int64_t T, int act, const void* X, in
   ff_status st = check_common(p, T, act, 1);
   if (st != FF_OK) return st;
   if (T == 0) return FF_OK;
-  if ((st = check_act("X", X, ldx, p->fin->d, act)) != FF_OK) return st;
-  if ((st = check_act("Y", Y, ldy, p->fout->d, act)) != FF_OK) return st;
+  if ((st = check_act("X", X, ldx, p->fin->d, act, p->lifted)) != FF_OK) return st;
+  if ((st = check_act("Y", Y, ldy, p->fout->d, act, p->lifted)) != FF_OK) return st;
   if (p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
   if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
+  if (p->lifted)
+    return launched(ff::launch_fwd_lifted(p, act == FF_BF16, (int)T, X, ldx, c_vals, scale, beta, Y, ldy,
+                                          (hipStream_t)stream),
+                    "forward launch");
   return launched(ff::launch_fwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, c_vals, nullptr, scale,
                                  beta, {Y, nullptr}, ldy, nullptr, (hipStream_t)stream),
                   "forward launch");
@@ -193,6 +203,10 @@ ff_status ff_adapter_bwd(const ff_plan* p, int64_t T, int act, const void* X, in
   const ff_status st = check_bwd(p, T, act, X, ldx, G, ldg, c_vals, dX, lddx, accumulate_dc, dC, &want_dx, &want_dc,
                                  &done);
   if (st != FF_OK || done) return st;
+  if (p->lifted)
+    return launched(ff::launch_bwd_lifted(p, act == FF_BF16, (int)T, X, ldx, G, ldg, c_vals, scale, beta_dx, dX, lddx,
+                                          want_dx, accumulate_dc, dC, want_dc, (hipStream_t)stream),
+                    "backward launch");
   return launched(ff::launch_bwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, {G, nullptr}, ldg, c_vals,
                                  nullptr, scale, beta_dx, {dX, nullptr}, lddx, want_dx, accumulate_dc, dC,
                                  nullptr, want_dc, nullptr, (hipStream_t)stream),
@@ -208,13 +222,19 @@ ff_status ff_adapter_bwd_noalloc(const ff_plan* p, int64_t T, int act, const voi
   ff_status st = check_bwd(p, T, act, X, ldx, G, ldg, c_vals, dX, lddx, accumulate_dc, dC, &want_dx, &want_dc,
                            &done);
   if (st != FF_OK || done) return st;
-  const size_t need = ff::bwd_scratch_floats(p, act == FF_BF16, (int)T) * sizeof(float);
+  // plans with a lift run the kernels in fp32 whatever the activation type
+  const int kbf16 = act == FF_BF16 && !p->lifted;
+  const size_t need = ff::bwd_scratch_floats(p, kbf16, (int)T) * sizeof(float);
   if (need > kScratchBytes)
     return ff::fail(FF_EINVAL, "this backward needs %zu bytes of scratch, more than the %zu bytes of the static "
                     "scratch (use fewer tokens per call)", need, kScratchBytes);
   void* base = nullptr;
   if ((st = scratch_address(p->device, &base)) != FF_OK) return st;
   const ff::BwdScratch ws{static_cast<float*>(base), kScratchBytes / sizeof(float)};
+  if (p->lifted)
+    return launched(ff::launch_bwd_lifted(p, act == FF_BF16, (int)T, X, ldx, G, ldg, c_vals, scale, beta_dx, dX, lddx,
+                                          want_dx, accumulate_dc, dC, want_dc, (hipStream_t)stream, &ws),
+                    "backward launch");
   return launched(ff::launch_bwd(p, act == FF_BF16, 1, (int)T, {X, nullptr}, ldx, {G, nullptr}, ldg, c_vals,
                                  nullptr, scale, beta_dx, {dX, nullptr}, lddx, want_dx, accumulate_dc, dC,
                                  nullptr, want_dc, nullptr, (hipStream_t)stream, &ws),
@@ -253,6 +273,9 @@ ff_status ff_merge_delta(const ff_plan* p, const float* c_vals, float scale, int
   if ((uintptr_t)W % (w_dtype == FF_BF16 ? 2 : 4)) return ff::fail(FF_EINVAL, "W is misaligned");
   if (p->coef_slots > 0 && !c_vals) return ff::fail(FF_EINVAL, "c_vals is NULL");
   if ((uintptr_t)c_vals % 16) return ff::fail(FF_EINVAL, "c_vals is not 16-byte aligned");
+  if (p->lifted)
+    return launched(ff::launch_merge_lifted(p, c_vals, scale, w_dtype == FF_BF16, beta, W, ldw, (hipStream_t)stream),
+                    "merge launch");
   return launched(ff::launch_merge(p, c_vals, scale, w_dtype == FF_BF16, beta, W, ldw, (hipStream_t)stream),
                   "merge launch");
 }
@@ -289,6 +312,7 @@ ff_status ff_adapter_fwd_batched(const ff_plan* p, int64_t count, int64_t T, int
   ff::clear_error();
   ff_status st = check_common(p, T, act, count);
   if (st != FF_OK) return st;
+  if (p->lifted) return ff::fail(FF_EUNSUPPORTED, "batched calls need frames with k rho == d");
   if (T == 0) return FF_OK;
   if (!X || !Y || !c_vals) return ff::fail(FF_EINVAL, "pointer array is NULL");
   if (ldx < p->fin->d || ldy < p->fout->d) return ff::fail(FF_EINVAL, "leading dimension too small");
@@ -308,6 +332,7 @@ ff_status ff_adapter_bwd_batched(const ff_plan* p, int64_t count, int64_t T, int
   ff::clear_error();
   ff_status st = check_common(p, T, act, count);
   if (st != FF_OK) return st;
+  if (p->lifted) return ff::fail(FF_EUNSUPPORTED, "batched calls need frames with k rho == d");
   const bool want_dx = dX != nullptr, want_dc = dC != nullptr && p->coef_slots > 0;
   if (T == 0 && (!want_dc || accumulate_dc)) return FF_OK;
   if (T > 0) {

@@ -64,6 +64,22 @@ struct FrameDev {
   const float2* twk;
 };
 
+// The lift L of a frame P = L^T Pv (every frame the library builds has one).  Pv is the block-
+// diagonal frame of the coefficient-space dimension dv = k rho (complex k rho / 2), whose block r is
+// the unitary k-point DFT; L (dv x d) places row r of the Spectral Tetris frame F: user complex
+// coordinate j of the row's window goes to virtual coordinate r k + (j mod k), weighted by F[r][j].
+// The modulation by the k-th roots of unity sees j only through j mod k, so z = Pv^T (L x) is the
+// analysis of the requested frame, and y = L^T (Pv v) its synthesis.  With k rho = d, L is the
+// identity.  Every user coordinate lies in one or two windows (two inside a T(x) block).
+struct LiftDev {
+  int dc;                // user complex coordinates, d / 2
+  int dvc;               // virtual complex coordinates, k rho / 2
+  const int* up_src;     // [dvc] user coordinate feeding virtual coordinate v, -1 for none
+  const float* up_w;     // [dvc] its weight F[r][j]
+  const int2* dn_v;      // [dc]  the virtual coordinates holding user coordinate j (-1: none)
+  const float2* dn_w;    // [dc]  their weights
+};
+
 // Position of block-local coefficient c (= 2 i + s: frequency i, real or imaginary part s)
 // inside a block's LDS storage.
 inline int lds_position(const FrameDev& f, int c) {
@@ -170,6 +186,9 @@ struct GenDesc {    // generic kernels
 struct ff_frame {
   std::atomic<int> refs{1};
   int64_t d = 0, k = 0, rho = 0;
+  int64_t dv = 0;          // coefficient-space dimension k rho (the kernels' frame works in it)
+  bool lifted = false;     // k rho != d: P = L^T Pv with a lift L that is not the identity
+  ff::LiftDev lift{};
   int device = 0;
   std::vector<double> B;   // W x W fp64 block on the host
   bool transpose_is_sign_flip = false;   // B^T == D B D exactly, D = diag((-1)^i)
@@ -206,6 +225,14 @@ struct ff_plan {
   int mrg_rows = 0;
   float* mrg_g = nullptr;
   float* mrg_out = nullptr;
+  // Frames with a lift (k rho != d on either side): every call lifts its inputs into fp32 staging
+  // rows of the coefficient-space width, runs the kernels there in fp32 and lifts the results
+  // back.  lift_x: max_tokens x dv_in (X), lift_g: max_tokens x dv_out (G, or the forward's output
+  // before the lift), lift_dx: max_tokens x dv_in (dX before the lift).
+  bool lifted = false;
+  float* lift_x = nullptr;
+  float* lift_g = nullptr;
+  float* lift_dx = nullptr;
   size_t workspace_bytes = 0;
   void* dev_mem = nullptr;
   ff::PlanDev dev{};
@@ -288,6 +315,16 @@ hipError_t launch_bwd128_group(const ff_plan_group* g, int T, const int* tokens,
                                const void* const* G, int64_t ldg, const float* const* cs, float scale, float beta_dx,
                                void* const* dX, int64_t lddx, bool want_dx, int accumulate_dc, float* const* dCs,
                                bool want_dc, hipStream_t s);
+// Calls on plans with a lift (lift.hip): the same contracts as launch_fwd / launch_bwd /
+// launch_merge for one adapter, in the user's dimensions.
+hipError_t launch_fwd_lifted(const ff_plan* p, int bf16, int T, const void* X, int64_t ldx, const float* c,
+                             float scale, float beta, void* Y, int64_t ldy, hipStream_t s);
+hipError_t launch_bwd_lifted(const ff_plan* p, int bf16, int T, const void* X, int64_t ldx, const void* G,
+                             int64_t ldg, const float* c, float scale, float beta_dx, void* dX, int64_t lddx,
+                             bool want_dx, int accumulate_dc, float* dC, bool want_dc, hipStream_t s,
+                             const BwdScratch* ws = nullptr);
+hipError_t launch_merge_lifted(const ff_plan* p, const float* c, float scale, int w_bf16, float beta, void* W,
+                               int64_t ldw, hipStream_t s);
 // Generic-kernel tile size of a call (kernels.hip), shared by single, batched and group calls.
 int call_tile_tokens(int tt, long T, int count, int slots);
 

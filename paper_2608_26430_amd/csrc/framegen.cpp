@@ -18,7 +18,11 @@
 // When k*rho = d every row of F is k consecutive ones, so P is block diagonal
 // with rho/2 identical square blocks B (2k x 2k): B[2 tau + t][2 i + s] is the
 // entry of column (i, r, s) at real row 2(r k + tau) + t.  The device works on
-// B alone.
+// B alone.  Any other tight (k, rho, d) -- redundant frames, k rho > d, and
+// those with a non-integer d / rho -- factors as P = L^T Pv: Pv is the block
+// frame of dimension k rho, and the sparse lift L places each row of F at the
+// positions j mod k of its block with the row's weights (modulation depends on
+// j only mod k, and tightness keeps a row's columns distinct mod k).
 #include <algorithm>
 #include <cmath>
 #include <complex>
@@ -346,6 +350,36 @@ bool factor_radix4(const std::vector<double>& B, int64_t k, std::vector<double>&
   return true;
 }
 
+// The lift of the frame with rows Frows (see LiftDev): row r's entry (j, F[r][j]) goes to virtual
+// complex coordinate r k + (j mod k).  Two entries of one row that agree mod k would share a virtual
+// coordinate; tightness (check_tight) already excludes that, and it is checked again here.
+ff_status build_lift(const std::vector<std::vector<std::pair<int64_t, double>>>& Frows, int64_t k, int64_t d_c,
+                     std::vector<int>& up_src, std::vector<float>& up_w, std::vector<int>& dn_v,
+                     std::vector<float>& dn_w) {
+  const int64_t rho_c = (int64_t)Frows.size(), dvc = rho_c * k;
+  up_src.assign((size_t)dvc, -1);
+  up_w.assign((size_t)dvc, 0.f);
+  dn_v.assign((size_t)(2 * d_c), -1);
+  dn_w.assign((size_t)(2 * d_c), 0.f);
+  for (int64_t r = 0; r < rho_c; ++r)
+    for (const auto& jv : Frows[r]) {
+      const int64_t j = jv.first, v = r * k + j % k;
+      if (up_src[v] >= 0)
+        return ff::fail(FF_ENOTFF, "row %lld of F holds columns %d and %lld, equal mod k=%lld: not a tight frame",
+                        (long long)r, up_src[v], (long long)j, (long long)k);
+      up_src[v] = (int)j;
+      up_w[v] = (float)jv.second;
+      const int slot = dn_v[2 * j] < 0 ? 0 : 1;
+      if (slot == 1 && dn_v[2 * j + 1] >= 0)
+        return ff::fail(FF_ENOTFF, "column %lld of F lies in more than two rows", (long long)j);
+      dn_v[2 * j + slot] = (int)v;
+      dn_w[2 * j + slot] = (float)jv.second;
+    }
+  for (int64_t j = 0; j < d_c; ++j)
+    if (dn_v[2 * j] < 0) return ff::fail(FF_ENOTFF, "column %lld of F is empty", (long long)j);
+  return FF_OK;
+}
+
 uint16_t bf16_rne(float f) {
   uint32_t u;
   std::memcpy(&u, &f, 4);
@@ -382,12 +416,37 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   std::vector<std::vector<std::pair<int64_t, double>>> Frows;
   ff_status st = build_host(d, k, rho, Frows);
   if (st != FF_OK) return st;
-  if (k * rho != d)
-    return ff::fail(FF_EUNSUPPORTED, "GPU path needs k*rho == d (k=%lld, rho=%lld, d=%lld)",
-                    (long long)k, (long long)rho, (long long)d);
+  // The kernels apply the block-diagonal frame Pv of dimension dv = k rho; a frame with k rho != d
+  // (a redundant one, or a non-integer d / rho) is P = L^T Pv with the lift L of its own rows.
+  const int64_t dv = k * rho;
+  const bool lifted = dv != d;
+  std::vector<int> up_src, dn_v;
+  std::vector<float> up_w, dn_w;
+  std::vector<std::vector<std::pair<int64_t, double>>> Fvrows;
+  if (lifted) {
+    if (dv > (int64_t)1 << 24) return ff::fail(FF_EUNSUPPORTED, "k rho = %lld too large", (long long)dv);
+    if ((st = build_lift(Frows, k, d / 2, up_src, up_w, dn_v, dn_w)) != FF_OK) return st;
+    if ((st = build_host(dv, k, rho, Fvrows)) != FF_OK) return st;
+  } else {   // the identity lift
+    up_src.resize((size_t)(d / 2));
+    up_w.assign((size_t)(d / 2), 1.f);
+    dn_v.resize((size_t)d);
+    dn_w.assign((size_t)d, 0.f);
+    for (int64_t j = 0; j < d / 2; ++j) {
+      up_src[j] = (int)j;
+      dn_v[2 * j] = (int)j;
+      dn_v[2 * j + 1] = -1;
+      dn_w[2 * j] = 1.f;
+    }
+  }
+  const auto& Fb = lifted ? Fvrows : Frows;
   const int64_t W = 2 * k;
-  if (W % 8 != 0)
-    return ff::fail(FF_EUNSUPPORTED, "GPU path needs 2k to be a multiple of 8 (k=%lld)", (long long)k);
+  // Lifted frames run the kernels in fp32, whose 4-element accesses need 2k to be a multiple of 4
+  // only (bf16 accesses are of 8); the dense path serves those up to 128 wide.
+  const bool narrow_ok = lifted && W % 4 == 0 && W <= 128;
+  if (W % 8 != 0 && !narrow_ok)
+    return ff::fail(FF_EUNSUPPORTED, "GPU path needs 2k to be a multiple of 8 (or of 4 for k rho != d, 2k <= 128; k=%lld)",
+                    (long long)k);
   if (W > 4096) return ff::fail(FF_EUNSUPPORTED, "frame block 2k=%lld too wide (at most 4096)", (long long)W);
 
   // Extract the diagonal block and confirm that P is block diagonal with identical blocks.
@@ -396,7 +455,7 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   for (int64_t c = 0; c < k * rho; ++c) {
     const int64_t i = c / rho, rem = c % rho, r = rem / 2, s = rem % 2;
     const int64_t lc = 2 * i + s;
-    real_column(Frows, k, rho, c, colv);
+    real_column(Fb, k, rho, c, colv);
     for (const auto& rv : colv) {
       const int64_t u = rv.first - r * W;
       if (u < 0 || u >= W)
@@ -457,7 +516,7 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   const int64_t n4 = factored ? (int64_t)1 << (2 * nst) : 1;
 
   ff::FrameDev fd{};
-  fd.d = (int)d;
+  fd.d = (int)dv;
   fd.W = (int)W;
   fd.nblk = (int)(rho / 2);
   fd.radix = factored ? 4 : 1;
@@ -510,8 +569,9 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   for (size_t e = 0; e < twk.size(); ++e) twk32[e] = (float)twk[e];
 
   const size_t b16 = n16 * 2, b32 = n32 * 4, bB = B32.size() * 4, bT = tw32.size() * 4, bK = twk32.size() * 4;
+  const size_t bU = up_src.size() * 4, bD = dn_v.size() * 4;
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t total = 2 * up(b16) + 2 * up(b32) + up(bB) + up(bT) + up(bK);
+  const size_t total = 2 * up(b16) + 2 * up(b32) + up(bB) + up(bT) + up(bK) + 2 * up(bU) + 2 * up(bD);
   void* mem = nullptr;
   if (hipMalloc(&mem, total) != hipSuccess) {
     (void)hipGetLastError();
@@ -531,7 +591,15 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   fd.B32 = (const float*)put(B32.data(), bB);
   fd.tw = (const float2*)put(tw32.data(), bT);
   fd.twk = (const float2*)put(twk32.data(), bK);
-  if (!fd.fa16 || !fd.fs16 || !fd.fa32 || !fd.fs32 || !fd.B32 || !fd.tw || !fd.twk) {
+  ff::LiftDev lift{};
+  lift.dc = (int)(d / 2);
+  lift.dvc = (int)(dv / 2);
+  lift.up_src = (const int*)put(up_src.data(), bU);
+  lift.up_w = (const float*)put(up_w.data(), bU);
+  lift.dn_v = (const int2*)put(dn_v.data(), bD);
+  lift.dn_w = (const float2*)put(dn_w.data(), bD);
+  if (!fd.fa16 || !fd.fs16 || !fd.fa32 || !fd.fs32 || !fd.B32 || !fd.tw || !fd.twk || !lift.up_src || !lift.up_w ||
+      !lift.dn_v || !lift.dn_w) {
     (void)hipFree(mem);
     return ff::fail(FF_EDEVICE, "copying frame to the device failed");
   }
@@ -543,6 +611,9 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   f->d = d;
   f->k = k;
   f->rho = rho;
+  f->dv = dv;
+  f->lifted = lifted;
+  f->lift = lift;
   f->device = dev;
   f->B = std::move(B);
   f->transpose_is_sign_flip = sign_flip;
@@ -559,14 +630,24 @@ extern "C" ff_status ff_frame_export(const ff_frame* f, int64_t col0, int64_t nc
   const int64_t d = f->d, k = f->k, rho = f->rho, W = 2 * k;
   if (col0 < 0 || ncols < 0 || col0 + ncols > k * rho)
     return ff::fail(FF_EINVAL, "column range outside [0, %lld)", (long long)(k * rho));
-  std::vector<float> B32((size_t)(W * W));
-  if (hipMemcpy(B32.data(), f->dev.B32, B32.size() * 4, hipMemcpyDeviceToHost) != hipSuccess)
+  std::vector<float> B32((size_t)(W * W)), up_w((size_t)f->lift.dvc);
+  std::vector<int> up_src((size_t)f->lift.dvc);
+  if (hipMemcpy(B32.data(), f->dev.B32, B32.size() * 4, hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemcpy(up_src.data(), f->lift.up_src, up_src.size() * 4, hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemcpy(up_w.data(), f->lift.up_w, up_w.size() * 4, hipMemcpyDeviceToHost) != hipSuccess)
     return ff::fail(FF_EDEVICE, "reading the frame back failed");
   std::memset(out, 0, sizeof(double) * (size_t)d * (size_t)ncols);
+  // column c of P = L^T Pv: its block entries B[u][2 i + s] at virtual coordinate r k + u / 2,
+  // carried to the user coordinate that feeds it, with that coordinate's weight
   for (int64_t cc = 0; cc < ncols; ++cc) {
     const int64_t c = col0 + cc;
     const int64_t i = c / rho, rem = c % rho, r = rem / 2, s = rem % 2;
-    for (int64_t u = 0; u < W; ++u) out[(r * W + u) * ncols + cc] = (double)B32[u * W + 2 * i + s];
+    for (int64_t u = 0; u < W; ++u) {
+      const int64_t v = r * k + u / 2;
+      const int j = up_src[v];
+      if (j < 0) continue;
+      out[(2 * (int64_t)j + u % 2) * ncols + cc] += (double)up_w[v] * (double)B32[u * W + 2 * i + s];
+    }
   }
   return FF_OK;
 }

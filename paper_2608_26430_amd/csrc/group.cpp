@@ -48,6 +48,7 @@ ff_status ff_plan_group_create(int64_t count, const ff_plan* const* plans, ff_pl
   if (count < 1 || count > 65535 || !plans) return ff::fail(FF_EINVAL, "need 1 <= count <= 65535 plans");
   const ff_plan* ref = plans[0];
   if (!ref) return ff::fail(FF_EINVAL, "plan 0 is NULL");
+  if (ref->lifted) return ff::fail(FF_EUNSUPPORTED, "plan groups need frames with k rho == d");
   std::set<const ff_plan*> seen;
   for (int64_t i = 0; i < count; ++i) {
     const ff_plan* p = plans[i];

@@ -275,7 +275,7 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   *out = nullptr;
   if (!f_in || !f_out) return ff::fail(FF_EINVAL, "frame is NULL");
   if (f_in->device != f_out->device) return ff::fail(FF_EINVAL, "frames live on different devices");
-  const int64_t n = f_in->d, m = f_out->d;          // k*rho == d on the GPU path
+  const int64_t n = f_in->dv, m = f_out->dv;        // the coefficient grid, (k rho_m) x (k rho_n)
   if (nnz < 0 || nnz > m * n || nnz > ((int64_t)1 << 30))
     return ff::fail(FF_EINVAL, "nnz=%lld out of range", (long long)nnz);
   if (nnz > 0 && (!rows || !cols)) return ff::fail(FF_EINVAL, "rows/cols is NULL");
@@ -451,7 +451,8 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   // Backward stream (dC and q = C^T u), one per pair of input blocks, grouped by column
   // of C: (byte offset of the source row of u | tile row of the column | end-of-column | valid,
   // coefficient slot).
-  const bool fast = FI.W == 128 && FO.W == 128 && FI.nblk % 2 == 0 && FO.nblk % 2 == 0 &&
+  const bool fast = !f_in->lifted && !f_out->lifted && FI.W == 128 && FO.W == 128 && FI.nblk % 2 == 0 &&
+                    FO.nblk % 2 == 0 &&
                     f_in->transpose_is_sign_flip && f_in->half_shift_sign && f_in->B == f_out->B &&
                     n < 65536 && m < 65536 &&
                     ff::fast128_lds_bytes(std::max(FI.nblk, FO.nblk)) <= (size_t)ff::kMaxLdsBytes;
@@ -598,11 +599,14 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   enum {
     kGfEnt, kGfCoef, kGfWave, kGbEnt, kGbCoef, kGbWave, kCoefPad, kCfwd, kCbwd, kMrgPtr, kMrgEnt,
     kFPl, kBPl, kFSt, kPadSlots, kBW, kPartial, kCoefBwd, kBwdPos, kFEm, kBDst, kBEm, kBPad, kUserOfSlot,
-    kSlotOfUser, kMrgG, kMrgOut, kNumBlobs
+    kSlotOfUser, kMrgG, kMrgOut, kLiftX, kLiftG, kLiftDX, kNumBlobs
   };
-  // frames applied in several radix-4 stages merge through the backward, a chunk of rows at a time
-  const bool mrg_transform = FI.nst >= 2 || FO.nst >= 2;
-  const int64_t mrg_rows = mrg_transform ? std::min<int64_t>(m, 1024) : 0;
+  // frames applied in several radix-4 stages, and frames with a lift, merge through the backward,
+  // a chunk of (user) rows at a time
+  const bool lifted = f_in->lifted || f_out->lifted;
+  const bool mrg_transform = FI.nst >= 2 || FO.nst >= 2 || lifted;
+  const int64_t mrg_rows = mrg_transform ? std::min<int64_t>(f_out->d, 1024) : 0;
+  const size_t lift_rows = lifted ? (size_t)max_tokens : 0;
   // both directions of the coefficient layout, for the device-side conversions
   std::vector<int> user_of_slot32(p->user_order.begin(), p->user_order.end());
   std::vector<Blob> blobs(kNumBlobs);
@@ -636,6 +640,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   blobs[kSlotOfUser] = {slot_of_user.data(), (size_t)nnz * sizeof(int)};
   blobs[kMrgG] = {nullptr, (size_t)mrg_rows * (size_t)m * sizeof(float)};
   blobs[kMrgOut] = {nullptr, (size_t)mrg_rows * (size_t)n * sizeof(float)};
+  blobs[kLiftX] = {nullptr, lift_rows * (size_t)n * sizeof(float)};
+  blobs[kLiftG] = {nullptr, lift_rows * (size_t)m * sizeof(float)};
+  blobs[kLiftDX] = {nullptr, lift_rows * (size_t)n * sizeof(float)};
   size_t total = 0;
   for (const Blob& b : blobs) total += up(b.bytes);
   int cur = 0;
@@ -683,6 +690,10 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
   p->mrg_rows = (int)mrg_rows;
   p->mrg_g = (float*)where[kMrgG];
   p->mrg_out = (float*)where[kMrgOut];
+  p->lifted = lifted;
+  p->lift_x = (float*)where[kLiftX];
+  p->lift_g = (float*)where[kLiftG];
+  p->lift_dx = (float*)where[kLiftDX];
   ff::FastPlanDev& fp = p->fast;
   fp.enabled = fast ? 1 : 0;
   fp.fwd_pl = (const int4*)where[kFPl];

@@ -71,9 +71,10 @@ def test_host_frame_rejects_bad_column_range():
 
 
 def test_framegen_shape_checks_precede_device_use():
-    # redundant frame (k*rho > d) and 2k not a multiple of 8 are rejected on the host
-    for (d, k, rho), status in [((22, 6, 6), "FF_EUNSUPPORTED"), ((16, 2, 8), "FF_EUNSUPPORTED"),
-                                ((10, 2, 4), "FF_ENOTFF")]:
+    # block widths the kernels do not take (2k not a multiple of 8 with k rho = d, not a multiple of
+    # 4 for a redundant frame) and frames that are not tight are rejected on the host
+    for (d, k, rho), status in [((22, 7, 6), "FF_EUNSUPPORTED"), ((16, 2, 8), "FF_EUNSUPPORTED"),
+                                ((10, 2, 4), "FF_ENOTFF"), ((22, 4, 6), "FF_ENOTFF")]:
         with pytest.raises(ff.FrameFTError) as ei:
             ff.framegen(d, k, rho)
         assert ei.value.name == status

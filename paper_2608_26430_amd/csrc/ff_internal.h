@@ -42,6 +42,8 @@ struct FrameDev {
   const void* fa32;  // analysis   fragments, f32x4  [MT][KT4][64]
   const void* fs32;  // synthesis  fragments, f32x4  [MT][KT4][64]
   const float* B32;  // B, W x W row-major fp32: B[u][c], u = local coordinate, c = local coefficient
+  const float* Bt32; // B transposed (B[u][c] at Bt32[c W + u]) for the merge; NULL for frames applied in
+                     // several radix-4 stages (they merge through the backward)
   // Factored application (radix == 4): B is the realified unitary DFT of size k = 4 k2, applied
   // as a radix-4 stage on the vector ALUs and a dense realified DFT of size k2 (W2 = 2 k2 wide)
   // on MFMA; the fragments above then hold that W2 x W2 matrix and MT / KT / KT4 refer to it.

@@ -563,15 +563,19 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
         }
     }
   for (size_t e = 0; e < B32.size(); ++e) B32[e] = (float)B[e];
+  std::vector<float> Bt32(nst >= 2 ? 1 : (size_t)(W * W));
+  if (nst < 2)
+    for (int64_t u = 0; u < W; ++u)
+      for (int64_t c = 0; c < W; ++c) Bt32[c * W + u] = (float)B[u * W + c];
 
   std::vector<float> tw32(std::max<size_t>(tw.size(), 2)), twk32(std::max<size_t>(twk.size(), 2));
   for (size_t e = 0; e < tw.size(); ++e) tw32[e] = (float)tw[e];
   for (size_t e = 0; e < twk.size(); ++e) twk32[e] = (float)twk[e];
 
   const size_t b16 = n16 * 2, b32 = n32 * 4, bB = B32.size() * 4, bT = tw32.size() * 4, bK = twk32.size() * 4;
-  const size_t bU = up_src.size() * 4, bD = dn_v.size() * 4;
+  const size_t bU = up_src.size() * 4, bD = dn_v.size() * 4, bBt = Bt32.size() * 4;
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t total = 2 * up(b16) + 2 * up(b32) + up(bB) + up(bT) + up(bK) + 2 * up(bU) + 2 * up(bD);
+  const size_t total = 2 * up(b16) + 2 * up(b32) + up(bB) + up(bBt) + up(bT) + up(bK) + 2 * up(bU) + 2 * up(bD);
   void* mem = nullptr;
   if (hipMalloc(&mem, total) != hipSuccess) {
     (void)hipGetLastError();
@@ -589,6 +593,7 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   fd.fa32 = put(fa32.data(), b32);
   fd.fs32 = put(fs32.data(), b32);
   fd.B32 = (const float*)put(B32.data(), bB);
+  fd.Bt32 = (const float*)put(Bt32.data(), bBt);
   fd.tw = (const float2*)put(tw32.data(), bT);
   fd.twk = (const float2*)put(twk32.data(), bK);
   ff::LiftDev lift{};
@@ -598,11 +603,12 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
   lift.up_w = (const float*)put(up_w.data(), bU);
   lift.dn_v = (const int2*)put(dn_v.data(), bD);
   lift.dn_w = (const float2*)put(dn_w.data(), bD);
-  if (!fd.fa16 || !fd.fs16 || !fd.fa32 || !fd.fs32 || !fd.B32 || !fd.tw || !fd.twk || !lift.up_src || !lift.up_w ||
-      !lift.dn_v || !lift.dn_w) {
+  if (!fd.fa16 || !fd.fs16 || !fd.fa32 || !fd.fs32 || !fd.B32 || !fd.Bt32 || !fd.tw || !fd.twk || !lift.up_src ||
+      !lift.up_w || !lift.dn_v || !lift.dn_w) {
     (void)hipFree(mem);
     return ff::fail(FF_EDEVICE, "copying frame to the device failed");
   }
+  if (nst >= 2) fd.Bt32 = nullptr;
   if (ff::configure_kernels() != hipSuccess || ff::configure_fast128() != hipSuccess) {
     (void)hipFree(mem);
     return ff::fail(FF_EDEVICE, "configuring kernels failed");

@@ -85,8 +85,8 @@ __global__ void __launch_bounds__(64 * kDcWaves) dc_reduce(const float* __restri
 }
 
 struct MergeArgs {
-  const float* Bm;   // output-frame block, W_m x W_m
-  const float* Bn;   // input-frame block,  W_n x W_n
+  const float* Btm;  // output-frame block transposed, W_m x W_m: column a of B_m at Btm + a W_m
+  const float* Btn;  // input-frame block transposed,  W_n x W_n
   int Wm, Wn, nblk_in, nsub_r, nsub_c, vec;
   const int* ptr;
   const int4* ent;
@@ -97,149 +97,238 @@ struct MergeArgs {
 };
 
 constexpr int kMergeThreads = 256;
-constexpr int kMergeRows = 128;                // output rows of a workgroup: 32 groups of 4
-constexpr int kMergeCols = 64;                 // output columns of a workgroup: 8 groups of 8
-constexpr int kMergeChunk = 32;                // entries staged per pass (25.6 KB of LDS)
-constexpr int kMergeUS = kMergeRows + 4;       // LDS row strides in floats: rows stay 16-byte
-constexpr int kMergeVS = kMergeCols + 4;       // aligned, staging writes spread over the banks
+constexpr int kMergeTile = 128;                // output rows and columns of a workgroup
+constexpr int kMergeChunk = 32;                // entries staged per pass
+constexpr int kMergeLd = kMergeTile + 16;      // fp32 staging: LDS row stride (floats) per entry; the 4
+                                               // entry rows one MFMA operand read touches fall on disjoint banks
+constexpr int kMergeBLd = kMergeTile + 16;     // bf16 staging: row stride (bf16) per entry; the 4 rows
+                                               // one transposed read touches fall on disjoint banks
+typedef short mrg_i16x4 __attribute__((ext_vector_type(4)));
 
-// W[block R rows, block S columns] = beta W + sum_e U_e V_e^T over the entries e of the block pair,
-// U_e = s c_e B_m[:, a'_e] and V_e = B_n[:, b'_e] (the rank-1 terms of P_out C P_in^T).  A
-// workgroup owns 128 rows x 64 columns of one block pair and each thread a 4 x 8 patch held in
-// registers; U and V columns of up to 32 entries at a time are staged in LDS (each entry's
-// frame values gathered once per workgroup), and every output sums its terms in bucket order.
+typedef __bf16 mrg_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float mrg_f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded to nearest even bf16, packed low then high (one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ unsigned pk_bf16(float a, float b) {
+  return __builtin_bit_cast(unsigned, __builtin_convertvector(mrg_f32x2{a, b}, mrg_bf16x2));
+}
+
+// The bf16 split x = hi + lo + d of four values (hi = RNE_bf16(x), lo = RNE_bf16(x - hi), x - hi
+// exact in fp32, |d| <= 2^-16 |x|), packed into the hi and lo operand words.
+__device__ __forceinline__ void split4_bf16(float4 x, uint2& hi, uint2& lo) {
+  hi.x = pk_bf16(x.x, x.y);
+  hi.y = pk_bf16(x.z, x.w);
+  lo.x = pk_bf16(x.x - __uint_as_float(hi.x << 16), x.y - __uint_as_float(hi.x & 0xffff0000u));
+  lo.y = pk_bf16(x.z - __uint_as_float(hi.y << 16), x.w - __uint_as_float(hi.y & 0xffff0000u));
+}
+
+// W[block R rows, block S columns] = beta W + U V^T over the entries e of the block pair (R, S):
+// column e of U is s c_e B_m[:, a'_e], column e of V is B_n[:, b'_e] (the rank-1 terms of
+// P_out C P_in^T).  A workgroup owns a 128 x 128 tile of the block pair and each of its waves a
+// 64 x 64 quadrant; U and V columns of up to 32 entries at a time are gathered from the transposed
+// blocks (coalesced across rows) into LDS and contracted on MFMA.  The MFMA computes the transposed
+// tile, so that each lane ends with 4 consecutive columns of one row of W.  The old values of W are
+// loaded at the start, so that their reads overlap the contraction.
+//  * fp32 W: fp32 operands on v_mfma_f32_16x16x4_f32 (4 entries per instruction), fp32 products and
+//    accumulation throughout.
+//  * bf16 W: each operand split into bf16 hi and lo parts and the three products hi hi + hi lo +
+//    lo hi accumulated on v_mfma_f32_16x16x32_bf16 (32 entries per instruction); each is exact in
+//    fp32, so a term u v carries at most 3.01 2^-16 |u v| of error besides the fp32 accumulation,
+//    far below the bf16 resolution of the merged weight, at a fifth of the MFMA time.
+// Entries past a chunk's end are zero columns.
 template <bool BF16W>
 __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
-  __shared__ __attribute__((aligned(16))) float us[kMergeChunk * kMergeUS];
-  __shared__ __attribute__((aligned(16))) float vs[kMergeChunk * kMergeVS];
-  __shared__ float es[kMergeChunk];   // s c_e of the pass's entries
-  __shared__ int ea[kMergeChunk], eb[kMergeChunk];   // their columns a'_e of B_m and b'_e of B_n
+  constexpr int kF32Bytes = 2 * kMergeChunk * kMergeLd * 4;
+  constexpr int kBfBytes = 4 * kMergeChunk * kMergeBLd * 2;
+  __shared__ __attribute__((aligned(16))) unsigned char stage[BF16W ? kBfBytes : kF32Bytes];
+  __shared__ float es[kMergeChunk];
+  __shared__ int ea[kMergeChunk], eb[kMergeChunk];
   const int nsub = a.nsub_r * a.nsub_c;
   const int sub = blockIdx.x % nsub, tile = blockIdx.x / nsub;
   const int R = tile / a.nblk_in, S = tile - R * a.nblk_in;
-  const int u0 = (sub / a.nsub_c) * kMergeRows, p0 = (sub % a.nsub_c) * kMergeCols;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int r = ((lane >> 3) + 8 * wv) * 4;    // the thread's first row within the workgroup's rows
-  const int q = (lane & 7) * 8;                // its first column within the workgroup's columns
-  // W_m and W_n are multiples of 8, so a patch lies wholly inside or wholly outside the block
-  const bool live = u0 + r < a.Wm && p0 + q < a.Wn;
-  const long row0 = (long)R * a.Wm + u0 + r;
-  const long col0 = (long)S * a.Wn + p0 + q;
+  const int u0 = (sub / a.nsub_c) * kMergeTile, p0 = (sub % a.nsub_c) * kMergeTile;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, n = lane & 15, q = lane >> 4;
+  const int wr = (wv >> 1) * 64, wc = (wv & 1) * 64;   // the wave's quadrant: rows u, columns p
   const bool rmw = a.beta != 0.f;
-
-  float old[4][8];
+  using Old = typename std::conditional<BF16W, uint2, float4>::type;
+  // lane's outputs: W[u = u0 + wr + 16 i + n][p = p0 + wc + 16 j + 4 q + r], r = 0..3
+  auto out_off = [&](int i, int j) -> long {
+    return ((long)R * a.Wm + u0 + wr + 16 * i + n) * a.ldw + (long)S * a.Wn + p0 + wc + 16 * j + 4 * q;
+  };
+  auto live = [&](int i, int j) { return u0 + wr + 16 * i + n < a.Wm && p0 + wc + 16 * j + 4 * q < a.Wn; };
+  Old old[4][4];
+  if (rmw && a.vec) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) old[i][j] = 0.f;
-  if (live && rmw) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const long off = (row0 + i) * a.ldw + col0;
-      if constexpr (BF16W) {
-        const u16* w = reinterpret_cast<const u16*>(a.W) + off;
-        if (a.vec) {
-          const uint4 v = *reinterpret_cast<const uint4*>(w);
-          const unsigned x[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            old[i][2 * j] = bf2f((u16)(x[j] & 0xffffu));
-            old[i][2 * j + 1] = bf2f((u16)(x[j] >> 16));
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) old[i][j] = bf2f(w[j]);
-        }
-      } else {
-        const float* w = reinterpret_cast<const float*>(a.W) + off;
-        if (a.vec) {
-          const float4 v0 = *reinterpret_cast<const float4*>(w);
-          const float4 v1 = *reinterpret_cast<const float4*>(w + 4);
-          old[i][0] = v0.x; old[i][1] = v0.y; old[i][2] = v0.z; old[i][3] = v0.w;
-          old[i][4] = v1.x; old[i][5] = v1.y; old[i][6] = v1.z; old[i][7] = v1.w;
-        } else {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) old[i][j] = w[j];
+      for (int j = 0; j < 4; ++j) {
+        old[i][j] = Old{};
+        if (live(i, j)) {
+          if constexpr (BF16W)
+            old[i][j] = gload(reinterpret_cast<const uint2*>(reinterpret_cast<const u16*>(a.W) + out_off(i, j)));
+          else
+            old[i][j] = gload(reinterpret_cast<const float4*>(reinterpret_cast<const float*>(a.W) + out_off(i, j)));
         }
       }
-    }
   }
 
-  float acc[4][8];
+  f32x4 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = 0.f;
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int beg = a.ptr[tile], end = a.ptr[tile + 1];
   for (int c0 = beg; c0 < end; c0 += kMergeChunk) {
     const int nch = min(kMergeChunk, end - c0);
-    __syncthreads();   // the previous pass has finished reading us / vs / es / ea / eb
-    if ((int)threadIdx.x < nch) {
-      const int4 en = a.ent[c0 + threadIdx.x];
+    __syncthreads();   // the previous pass has finished reading the staging and es / ea / eb
+    if ((int)threadIdx.x < kMergeChunk) {
+      const bool in = (int)threadIdx.x < nch;
+      const int4 en = in ? a.ent[c0 + threadIdx.x] : make_int4(0, 0, 0, 0);
       ea[threadIdx.x] = en.x;
       eb[threadIdx.x] = en.y;
-      es[threadIdx.x] = a.scale * a.c[en.z];
+      es[threadIdx.x] = in ? a.scale * a.c[en.z] : 0.f;
     }
     __syncthreads();
-    // staging index x: entry e = 8 * (x / (8 rows)) + x % 8, so a wave gathers 8 entries of 8 rows;
-    // the loops are unrolled so that several independent frame loads are in flight per thread
-    const int ngrp = (nch + 7) >> 3;
-#pragma unroll 8
-    for (int x = threadIdx.x; x < ngrp * 8 * kMergeRows; x += kMergeThreads) {
-      const int e = ((x / (8 * kMergeRows)) << 3) | (x & 7), u = (x >> 3) & (kMergeRows - 1);
-      if (e < nch && u0 + u < a.Wm) us[e * kMergeUS + u] = es[e] * a.Bm[(long)(u0 + u) * a.Wm + ea[e]];
-    }
-#pragma unroll 8
-    for (int x = threadIdx.x; x < ngrp * 8 * kMergeCols; x += kMergeThreads) {
-      const int e = ((x / (8 * kMergeCols)) << 3) | (x & 7), p = (x >> 3) & (kMergeCols - 1);
-      if (e < nch && p0 + p < a.Wn) vs[e * kMergeVS + p] = a.Bn[(long)(p0 + p) * a.Wn + eb[e]];
-    }
-    __syncthreads();
-    if (live) {
-      for (int e = 0; e < nch; ++e) {
-        const float4 uu = *reinterpret_cast<const float4*>(&us[e * kMergeUS + r]);
-        const float4 va = *reinterpret_cast<const float4*>(&vs[e * kMergeVS + q]);
-        const float4 vb = *reinterpret_cast<const float4*>(&vs[e * kMergeVS + q + 4]);
-        const float uv[4] = {uu.x, uu.y, uu.z, uu.w};
-        const float vv[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
+    if constexpr (BF16W) {
+      // entry-major hi / lo rows of U and V (as the fp32 staging, 4 rows or columns per piece)
+      u16* uh = reinterpret_cast<u16*>(stage);
+      u16* ul = uh + kMergeChunk * kMergeBLd;
+      u16* vh = ul + kMergeChunk * kMergeBLd;
+      u16* vl = vh + kMergeChunk * kMergeBLd;
+#pragma unroll
+      for (int it = 0; it < kMergeChunk * 32 / kMergeThreads; ++it) {
+        const int x = it * kMergeThreads + threadIdx.x, e = x >> 5, f = (x & 31) * 4;
+        float4 uu = make_float4(0.f, 0.f, 0.f, 0.f), vv = uu;
+        if (e < nch && u0 + f < a.Wm) {
+          const float4 b = *reinterpret_cast<const float4*>(a.Btm + (long)ea[e] * a.Wm + u0 + f);
+          const float sc = es[e];
+          uu = make_float4(sc * b.x, sc * b.y, sc * b.z, sc * b.w);
+        }
+        if (e < nch && p0 + f < a.Wn) vv = *reinterpret_cast<const float4*>(a.Btn + (long)eb[e] * a.Wn + p0 + f);
+        const int o = e * kMergeBLd + f;
+        uint2 h, l;
+        split4_bf16(uu, h, l);
+        *reinterpret_cast<uint2*>(uh + o) = h;
+        *reinterpret_cast<uint2*>(ul + o) = l;
+        split4_bf16(vv, h, l);
+        *reinterpret_cast<uint2*>(vh + o) = h;
+        *reinterpret_cast<uint2*>(vl + o) = l;
+      }
+      __syncthreads();
+      // Operand of lane (n, q): row base + n of U or V at entries 8 q .. 8 q + 7, by two transposed
+      // reads (ds_read_b64_tr_b16: within 16 lanes the 8-byte chunks form 4 rows of 16 values and
+      // lane i receives value i of each row).  Lane L of the group loads entry 8 q + 4 h + L / 4 at
+      // rows base + 4 (L % 4) .. + 3, so lane i receives entries 8 q + 4 h .. + 3 of row base + i.
+      const int L = lane & 15;
+      auto opnd = [&](const u16* arr, int base) -> bf16x8 {
+        unsigned w[4];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const u16* pp = arr + (8 * q + 4 * h + (L >> 2)) * kMergeBLd + base + 4 * (L & 3);
+          auto* lp = (__attribute__((address_space(3))) mrg_i16x4*)(const_cast<u16*>(pp));
+          const raw2 r = __builtin_bit_cast(raw2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(lp));
+          w[2 * h] = r.x;
+          w[2 * h + 1] = r.y;
+        }
+        return __builtin_bit_cast(bf16x8, raw4{w[0], w[1], w[2], w[3]});
+      };
+      bf16x8 ah[4], al[4], bh[4], bl[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        ah[j] = opnd(vh, wc + 16 * j);
+        al[j] = opnd(vl, wc + 16 * j);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        bh[i] = opnd(uh, wr + 16 * i);
+        bl[i] = opnd(ul, wr + 16 * i);
+      }
+      // the small products first; each pass over the 16 accumulators keeps dependent MFMAs apart
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[j], bh[i], acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[j], bl[i], acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[j], bh[i], acc[i][j], 0, 0, 0);
+    } else {
+      float* us = reinterpret_cast<float*>(stage);
+      float* vs = us + kMergeChunk * kMergeLd;
+      // entry e's 128 rows of U (and columns of V) as 32 float4 pieces; a thread stages 4 of each
+#pragma unroll
+      for (int it = 0; it < kMergeChunk * 32 / kMergeThreads; ++it) {
+        const int x = it * kMergeThreads + threadIdx.x, e = x >> 5, f = (x & 31) * 4;
+        float4 uu = make_float4(0.f, 0.f, 0.f, 0.f), vv = uu;
+        if (e < nch && u0 + f < a.Wm) {   // W_m and W_n are multiples of 4: a piece is wholly in or out
+          const float4 b = *reinterpret_cast<const float4*>(a.Btm + (long)ea[e] * a.Wm + u0 + f);
+          const float sc = es[e];
+          uu = make_float4(sc * b.x, sc * b.y, sc * b.z, sc * b.w);
+        }
+        if (p0 + f < a.Wn && e < nch) vv = *reinterpret_cast<const float4*>(a.Btn + (long)eb[e] * a.Wn + p0 + f);
+        *reinterpret_cast<float4*>(&us[e * kMergeLd + f]) = uu;
+        *reinterpret_cast<float4*>(&vs[e * kMergeLd + f]) = vv;
+      }
+      __syncthreads();
+      // lane (n, q) supplies V[p = wc + 16 j + n][e0 + q] as the A operand and
+      // U[u = wr + 16 i + n][e0 + q] as the B operand
+      for (int e0 = 0; e0 < nch; e0 += 4) {
+        float av[4], bu[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) av[j] = vs[(e0 + q) * kMergeLd + wc + 16 * j + n];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) bu[i] = us[(e0 + q) * kMergeLd + wr + 16 * i + n];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int j = 0; j < 8; ++j) acc[i][j] = fmaf(uv[i], vv[j], acc[i][j]);
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j], bu[i], acc[i][j], 0, 0, 0);
       }
     }
   }
-  if (!live) return;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const long off = (row0 + i) * a.ldw + col0;
-    float v[8];
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = rmw ? a.beta * old[i][j] + acc[i][j] : acc[i][j];
-    if constexpr (BF16W) {
-      u16* w = reinterpret_cast<u16*>(a.W) + off;
-      if (a.vec) {
-        uint4 o;
-        o.x = (unsigned)f2bf(v[0]) | ((unsigned)f2bf(v[1]) << 16);
-        o.y = (unsigned)f2bf(v[2]) | ((unsigned)f2bf(v[3]) << 16);
-        o.z = (unsigned)f2bf(v[4]) | ((unsigned)f2bf(v[5]) << 16);
-        o.w = (unsigned)f2bf(v[6]) | ((unsigned)f2bf(v[7]) << 16);
-        *reinterpret_cast<uint4*>(w) = o;
+    for (int j = 0; j < 4; ++j) {
+      if (!live(i, j)) continue;
+      const long off = out_off(i, j);
+      f32x4 v = acc[i][j];
+      if constexpr (BF16W) {
+        u16* w = reinterpret_cast<u16*>(a.W) + off;
+        if (a.vec) {
+          if (rmw) {
+            const uint2 o = old[i][j];
+            v[0] = fmaf(a.beta, bf2f((u16)(o.x & 0xffffu)), v[0]);
+            v[1] = fmaf(a.beta, bf2f((u16)(o.x >> 16)), v[1]);
+            v[2] = fmaf(a.beta, bf2f((u16)(o.y & 0xffffu)), v[2]);
+            v[3] = fmaf(a.beta, bf2f((u16)(o.y >> 16)), v[3]);
+          }
+          gstore(reinterpret_cast<uint2*>(w), make_uint2(pk_bf16(v[0], v[1]), pk_bf16(v[2], v[3])));
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) w[r] = f2bf(rmw ? fmaf(a.beta, bf2f(w[r]), v[r]) : v[r]);
+        }
       } else {
+        float* w = reinterpret_cast<float*>(a.W) + off;
+        if (a.vec) {
+          if (rmw) {
+            const float4 o = old[i][j];
+            v[0] = fmaf(a.beta, o.x, v[0]);
+            v[1] = fmaf(a.beta, o.y, v[1]);
+            v[2] = fmaf(a.beta, o.z, v[2]);
+            v[3] = fmaf(a.beta, o.w, v[3]);
+          }
+          gstore(reinterpret_cast<float4*>(w), make_float4(v[0], v[1], v[2], v[3]));
+        } else {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) w[j] = f2bf(v[j]);
-      }
-    } else {
-      float* w = reinterpret_cast<float*>(a.W) + off;
-      if (a.vec) {
-        *reinterpret_cast<float4*>(w) = make_float4(v[0], v[1], v[2], v[3]);
-        *reinterpret_cast<float4*>(w + 4) = make_float4(v[4], v[5], v[6], v[7]);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) w[j] = v[j];
+          for (int r = 0; r < 4; ++r) w[r] = rmw ? fmaf(a.beta, w[r], v[r]) : v[r];
+        }
       }
     }
-  }
 }
 
 // Group calls: gather_coef with each adapter's own stream (bwd: backward stream into c_bwd,
@@ -677,17 +766,18 @@ hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf1
     return e;
   }
   MergeArgs a{};
-  a.Bm = p->fout->dev.B32;
-  a.Bn = p->fin->dev.B32;
+  a.Btm = p->fout->dev.Bt32;
+  a.Btn = p->fin->dev.Bt32;
   a.Wm = p->fout->dev.W;
   a.Wn = p->fin->dev.W;
-  if (a.Wm % 8 != 0 || a.Wn % 8 != 0) return hipErrorInvalidValue;   // patches of 4 rows x 8 columns
+  // 4-row / 4-column pieces of the staged columns and of the stores
+  if (a.Wm % 4 != 0 || a.Wn % 4 != 0 || !a.Btm || !a.Btn) return hipErrorInvalidValue;
   a.nblk_in = p->fin->dev.nblk;
-  a.nsub_r = (a.Wm + kMergeRows - 1) / kMergeRows;
-  a.nsub_c = (a.Wn + kMergeCols - 1) / kMergeCols;
+  a.nsub_r = (a.Wm + kMergeTile - 1) / kMergeTile;
+  a.nsub_c = (a.Wn + kMergeTile - 1) / kMergeTile;
   const size_t esz = w_bf16 ? 2 : 4;
-  // 16-byte accesses when the base and the row stride keep every 8-column patch aligned
-  a.vec = (reinterpret_cast<uintptr_t>(W) % 16 == 0) && ((size_t)ldw * esz) % 16 == 0;
+  // whole 4-column groups in one access when the base and the row stride keep them aligned
+  a.vec = (reinterpret_cast<uintptr_t>(W) % (4 * esz) == 0) && ((size_t)ldw * esz) % (4 * esz) == 0;
   a.ptr = p->dev.mrg_ptr;
   a.ent = p->dev.mrg_ent;
   a.c = c;

@@ -39,7 +39,7 @@ def bf16_ulp(x):
     return np.exp2(e - 7)
 
 
-def merged_bf16_ok(got, W0, dW, dW_abs=None, depth=0):
+def merged_bf16_ok(got, W0, dW, dW_abs=None, depth=0, split=False):
     """bf16 merge check: within one bf16 ulp of RNE(W0 + dW), widened by the fp32 rounding of
     W0 + dW (2^-22 (|W0| + |dW|)), which matters only where the two nearly cancel.
 
@@ -48,13 +48,22 @@ def merged_bf16_ok(got, W0, dW, dW_abs=None, depth=0):
     one element), also by the recursive-summation bound of the kernel's fp32 arithmetic,
     (depth + 4) 2^-24 dW_abs: each term is a product of four fp32-rounded factors and each fused
     multiply-add rounds the running sum once.  Near W0 + dW = 0 that error is not small next to
-    the bf16 spacing of the result."""
+    the bf16 spacing of the result.
+
+    split: the merge into a bf16 weight forms each term u v from bf16 hi / lo splits of its fp32
+    factors (hi hi + hi lo + lo hi, each exact in fp32), which leaves at most 3.01 2^-16 |u v|
+    per term, and sums three products per term: 3.01 2^-16 dW_abs + (3 depth + 5) 2^-24 dW_abs
+    instead of the fp32 term."""
     from paper_2608_26430_amd import inputs
     exact = W0.astype(np.float64) + dW
     want = inputs.bf16_round(exact.astype(np.float32)).astype(np.float64)
     bound = bf16_ulp(want) + 2.0 ** -22 * (np.abs(W0) + np.abs(dW)) + 1e-30
     if dW_abs is not None:
-        bound = bound + (depth + 4) * 2.0 ** -24 * 1.01 * np.asarray(dW_abs, dtype=np.float64)
+        dW_abs = np.asarray(dW_abs, dtype=np.float64)
+        if split:
+            bound = bound + (3.01 * 2.0 ** -16 + (3 * depth + 5) * 2.0 ** -24) * 1.01 * dW_abs
+        else:
+            bound = bound + (depth + 4) * 2.0 ** -24 * 1.01 * dW_abs
     return bool(np.all(np.abs(np.asarray(got, dtype=np.float64) - want) <= bound))
 
 

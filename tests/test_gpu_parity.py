@@ -175,7 +175,7 @@ def test_small_parity(dev, shape, dtype):
     assert torch.equal(dC, dC2), "dC is not deterministic"
     dW_abs, depth = merge_abs_terms(P_in, P_out, rows, cols, vals, s, rn, rm)
     _check("dW", to_np(Wd), dw_ref, merge_bound(dW_abs, depth), rep)
-    assert merged_bf16_ok(to_np(Wb), W0, dw_ref, dW_abs, depth)
+    assert merged_bf16_ok(to_np(Wb), W0, dw_ref, dW_abs, depth, split=True)
     # the normwise figures of the tolerance statement, for the record
     assert rel(to_np(Y), fb.y) <= TOL[dtype] and rel(user_dc(plan, dC), bb.dc) <= TOL[dtype]
     print(f"\n{shape} {dtype}: (max err/bound, max-abs/max|ref|) {rep}")
@@ -479,7 +479,7 @@ def _full_size_check(dev, wl_name, adapter_index=0, n_tok=48, n_nnz=384, n_rows=
     assert rel(to_np(Wd[r]), dw_ref) <= 1e-5
     assert merged_bf16_ok(to_np(Wb[r]), W0[r], dw_ref,
                           *merge_abs_terms(P_in, P_out, data.rows, data.cols, data.vals, data.scale,
-                                          ad.rho_in, ad.rho_out, r))
+                                          ad.rho_in, ad.rho_out, r), split=True)
     # the frames are orthogonal, so ||dW||_F = |s| ||C||_F for the whole matrix
     nrm = float(torch.linalg.vector_norm(Wd.double()))
     assert abs(nrm - abs(data.scale) * np.linalg.norm(data.vals.astype(np.float64))) <= 1e-5 * nrm

@@ -116,3 +116,27 @@ def test_single_entry_detection_rate(problem):
     want = {1: (0.3, 0.9), 13: (0.7, 0.8), 100: (0.9, 0.7)}[T]
     assert min(hit_v.mean(), hit_q.mean()) >= want[0]
     assert hit_dc.mean() >= want[1]
+
+
+def test_split_bf16_product_error():
+    """The bf16 merge forms u v as hi(u) hi(v) + hi(u) lo(v) + lo(u) hi(v) with hi = RNE_bf16(x) and
+    lo = RNE_bf16(x - hi) (x - hi computed in fp32, exactly); each product is exact in fp32.  The
+    per-term error bound that merged_bf16_ok(split=True) uses is 3.01 2^-16 |u v|: checked here on
+    random fp32 factors over many binades, and found tight to within a factor of a few."""
+    from paper_2608_26430_amd import inputs
+    g = np.random.default_rng(7)
+    u = (g.standard_normal(200000) * np.exp2(g.integers(-20, 20, 200000))).astype(np.float32)
+    v = (g.standard_normal(200000) * np.exp2(g.integers(-20, 20, 200000))).astype(np.float32)
+
+    def split(x):
+        hi = inputs.bf16_round(x)
+        lo = inputs.bf16_round((x - hi).astype(np.float32))
+        return hi.astype(np.float64), lo.astype(np.float64)
+
+    hu, lu = split(u)
+    hv, lv = split(v)
+    got = hu * hv + hu * lv + lu * hv
+    exact = u.astype(np.float64) * v.astype(np.float64)
+    rel = np.abs(got - exact) / np.abs(exact)
+    assert rel.max() <= 3.01 * 2.0 ** -16
+    assert rel.max() >= 0.5 * 2.0 ** -16      # the bound is not loose by orders of magnitude

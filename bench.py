@@ -443,6 +443,27 @@ def main():
     torch.cuda.synchronize()
     fwd_us = 1e3 * float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     bwd_us = 1e3 * float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    # spread of single steps: events between consecutive rotated steps, median and CoV
+    sev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    sev[0].record()
+    for i in range(args.steps):
+        step(i)
+        sev[i + 1].record()
+    torch.cuda.synchronize()
+    per_step = np.array([1e3 * sev[i].elapsed_time(sev[i + 1]) for i in range(args.steps)])
+
+    # a plain device copy of 256 MiB (read + write), the achievable HBM rate beside the 8 TB/s peak
+    csrc = torch.empty(64 << 20, dtype=torch.float32, device=dev)
+    cdst = torch.empty_like(csrc)
+    cdst.copy_(csrc)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(5):
+        cdst.copy_(csrc)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2 * csrc.numel() * 4 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del csrc, cdst
 
     b_fwd, b_bwd, b_red = algorithmic_bytes(T, n, m, nnz, esz)
     if bwd_us >= fwd_us:
@@ -487,7 +508,10 @@ def main():
         "step_roofline": {"bytes_per_step": step_bytes, "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9
                                                                        / HBM_PEAK_GBS, 4),
                           "fwd_kernel_us": round(fwd_us, 3), "bwd_kernel_us": round(bwd_us, 3)},
-        "context": {"w0_gemm_us": round(gemm_us, 2), "setup_s": round(setup_s, 3),
+        "context": {"step_us_median": round(float(np.median(per_step)), 3),
+                    "step_us_cov": round(float(np.std(per_step) / np.mean(per_step)), 4),
+                    "copy_256mib_gbs": round(copy_gbs, 1),
+                    "w0_gemm_us": round(gemm_us, 2), "setup_s": round(setup_s, 3),
                     "wall_ms_timed": round(wall_ms, 3), "buffer_sets": nsets,
                     "buffer_set_mb": round(set_bytes / 1e6, 1),
                     "one_set_ms_per_step": round(ms_warm, 5),

@@ -99,6 +99,7 @@ struct MergeArgs {
 constexpr int kMergeThreads = 256;
 constexpr int kMergeTile = 128;                // output rows and columns of a workgroup
 constexpr int kMergeChunk = 32;                // entries staged per pass
+constexpr int kMergeBatch = 256;               // entries whose columns and s c_e sit in LDS at once
 constexpr int kMergeLd = kMergeTile + 16;      // fp32 staging: LDS row stride (floats) per entry; the 4
                                                // entry rows one MFMA operand read touches fall on disjoint banks
 constexpr int kMergeBLd = kMergeTile + 16;     // bf16 staging: row stride (bf16) per entry; the 4 rows
@@ -141,8 +142,8 @@ __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
   constexpr int kF32Bytes = 2 * kMergeChunk * kMergeLd * 4;
   constexpr int kBfBytes = 4 * kMergeChunk * kMergeBLd * 2;
   __shared__ __attribute__((aligned(16))) unsigned char stage[BF16W ? kBfBytes : kF32Bytes];
-  __shared__ float es[kMergeChunk];
-  __shared__ int ea[kMergeChunk], eb[kMergeChunk];
+  __shared__ float es[kMergeBatch];
+  __shared__ int ea[kMergeBatch], eb[kMergeBatch];
   const int nsub = a.nsub_r * a.nsub_c;
   const int sub = blockIdx.x % nsub, tile = blockIdx.x / nsub;
   const int R = tile / a.nblk_in, S = tile - R * a.nblk_in;
@@ -178,17 +179,23 @@ __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int beg = a.ptr[tile], end = a.ptr[tile + 1];
+  // The tile's entries in batches of up to 256 (usually one): their frame columns and s c_e are put
+  // in LDS once per batch (one dependent load chain), then consumed 32 at a time.
   for (int c0 = beg; c0 < end; c0 += kMergeChunk) {
+    const int k0 = (c0 - beg) % kMergeBatch;   // position of the chunk in its batch
     const int nch = min(kMergeChunk, end - c0);
-    __syncthreads();   // the previous pass has finished reading the staging and es / ea / eb
-    if ((int)threadIdx.x < kMergeChunk) {
-      const bool in = (int)threadIdx.x < nch;
-      const int4 en = in ? a.ent[c0 + threadIdx.x] : make_int4(0, 0, 0, 0);
-      ea[threadIdx.x] = en.x;
-      eb[threadIdx.x] = en.y;
-      es[threadIdx.x] = in ? a.scale * a.c[en.z] : 0.f;
+    __syncthreads();   // the previous pass has finished reading the staging (and, at a batch start, es / ea / eb)
+    if (k0 == 0) {
+      const int nb = min(kMergeBatch, end - c0);
+      if ((int)threadIdx.x < kMergeBatch) {
+        const bool in = (int)threadIdx.x < nb;
+        const int4 en = in ? a.ent[c0 + threadIdx.x] : make_int4(0, 0, 0, 0);
+        ea[threadIdx.x] = en.x;
+        eb[threadIdx.x] = en.y;
+        es[threadIdx.x] = in ? a.scale * a.c[en.z] : 0.f;
+      }
+      __syncthreads();
     }
-    __syncthreads();
     if constexpr (BF16W) {
       // entry-major hi / lo rows of U and V (as the fp32 staging, 4 rows or columns per piece)
       u16* uh = reinterpret_cast<u16*>(stage);
@@ -200,11 +207,11 @@ __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
         const int x = it * kMergeThreads + threadIdx.x, e = x >> 5, f = (x & 31) * 4;
         float4 uu = make_float4(0.f, 0.f, 0.f, 0.f), vv = uu;
         if (e < nch && u0 + f < a.Wm) {
-          const float4 b = *reinterpret_cast<const float4*>(a.Btm + (long)ea[e] * a.Wm + u0 + f);
-          const float sc = es[e];
+          const float4 b = *reinterpret_cast<const float4*>(a.Btm + (long)ea[k0 + e] * a.Wm + u0 + f);
+          const float sc = es[k0 + e];
           uu = make_float4(sc * b.x, sc * b.y, sc * b.z, sc * b.w);
         }
-        if (e < nch && p0 + f < a.Wn) vv = *reinterpret_cast<const float4*>(a.Btn + (long)eb[e] * a.Wn + p0 + f);
+        if (e < nch && p0 + f < a.Wn) vv = *reinterpret_cast<const float4*>(a.Btn + (long)eb[k0 + e] * a.Wn + p0 + f);
         const int o = e * kMergeBLd + f;
         uint2 h, l;
         split4_bf16(uu, h, l);
@@ -265,11 +272,11 @@ __global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
         const int x = it * kMergeThreads + threadIdx.x, e = x >> 5, f = (x & 31) * 4;
         float4 uu = make_float4(0.f, 0.f, 0.f, 0.f), vv = uu;
         if (e < nch && u0 + f < a.Wm) {   // W_m and W_n are multiples of 4: a piece is wholly in or out
-          const float4 b = *reinterpret_cast<const float4*>(a.Btm + (long)ea[e] * a.Wm + u0 + f);
-          const float sc = es[e];
+          const float4 b = *reinterpret_cast<const float4*>(a.Btm + (long)ea[k0 + e] * a.Wm + u0 + f);
+          const float sc = es[k0 + e];
           uu = make_float4(sc * b.x, sc * b.y, sc * b.z, sc * b.w);
         }
-        if (p0 + f < a.Wn && e < nch) vv = *reinterpret_cast<const float4*>(a.Btn + (long)eb[e] * a.Wn + p0 + f);
+        if (p0 + f < a.Wn && e < nch) vv = *reinterpret_cast<const float4*>(a.Btn + (long)eb[k0 + e] * a.Wn + p0 + f);
         *reinterpret_cast<float4*>(&us[e * kMergeLd + f]) = uu;
         *reinterpret_cast<float4*>(&vs[e * kMergeLd + f]) = vv;
       }

@@ -42,8 +42,7 @@ struct FrameDev {
   const void* fa32;  // analysis   fragments, f32x4  [MT][KT4][64]
   const void* fs32;  // synthesis  fragments, f32x4  [MT][KT4][64]
   const float* B32;  // B, W x W row-major fp32: B[u][c], u = local coordinate, c = local coefficient
-  const float* Bt32; // B transposed (B[u][c] at Bt32[c W + u]) for the merge; NULL for frames applied in
-                     // several radix-4 stages (they merge through the backward)
+  const float* Bt32; // B transposed (B[u][c] at Bt32[c W + u]) for the merge
   // Factored application (radix == 4): B is the realified unitary DFT of size k = 4 k2, applied
   // as a radix-4 stage on the vector ALUs and a dense realified DFT of size k2 (W2 = 2 k2 wide)
   // on MFMA; the fragments above then hold that W2 x W2 matrix and MT / KT / KT4 refer to it.
@@ -221,9 +220,9 @@ struct ff_plan {
   int gen_wgs = 1;                 // compute units: resident workgroups of the generic kernels
   int gen_rows = 1;                // dC partial rows per adapter = most workgroups of the generic backward
   float* partial = nullptr;        // dC partial sums per tile (layout depends on the kernels)
-  // Merge through the backward (frames applied in several radix-4 stages): mrg_rows output rows at
-  // a time, their unit vectors as fp32 "upstream gradients" (mrg_rows x m) and, for bf16 or
-  // unaligned weights, the fp32 rows before they are added in (mrg_rows x n).
+  // Merge through the backward (frames with a lift): mrg_rows output rows at a time, their lifted
+  // unit vectors as fp32 "upstream gradients" (mrg_rows x m) and the fp32 rows before they are
+  // lifted back into the weight (mrg_rows x n).
   int mrg_rows = 0;
   float* mrg_g = nullptr;
   float* mrg_out = nullptr;

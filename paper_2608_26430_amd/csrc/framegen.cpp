@@ -563,10 +563,10 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
         }
     }
   for (size_t e = 0; e < B32.size(); ++e) B32[e] = (float)B[e];
-  std::vector<float> Bt32(nst >= 2 ? 1 : (size_t)(W * W));
-  if (nst < 2)
-    for (int64_t u = 0; u < W; ++u)
-      for (int64_t c = 0; c < W; ++c) Bt32[c * W + u] = (float)B[u * W + c];
+  // the transposed block for the merge (a column of B is then a contiguous row)
+  std::vector<float> Bt32((size_t)(W * W));
+  for (int64_t u = 0; u < W; ++u)
+    for (int64_t c = 0; c < W; ++c) Bt32[c * W + u] = (float)B[u * W + c];
 
   std::vector<float> tw32(std::max<size_t>(tw.size(), 2)), twk32(std::max<size_t>(twk.size(), 2));
   for (size_t e = 0; e < tw.size(); ++e) tw32[e] = (float)tw[e];
@@ -608,7 +608,6 @@ extern "C" ff_status ff_framegen(int64_t d, int64_t k, int64_t rho, ff_frame** o
     (void)hipFree(mem);
     return ff::fail(FF_EDEVICE, "copying frame to the device failed");
   }
-  if (nst >= 2) fd.Bt32 = nullptr;
   if (ff::configure_kernels() != hipSuccess || ff::configure_fast128() != hipSuccess) {
     (void)hipFree(mem);
     return ff::fail(FF_EDEVICE, "configuring kernels failed");

@@ -394,31 +394,6 @@ __global__ void __launch_bounds__(64 * kDcWaves) dc_reduce_group(const GenDesc* 
   }
 }
 
-// g[r][i] = (i == row0 + r): the unit vectors of output rows row0 .. row0 + rows - 1.
-__global__ void __launch_bounds__(256) unit_rows(float* g, int rows, int m, int row0) {
-  const long j = (long)blockIdx.x * 256 + threadIdx.x;
-  if (j >= (long)rows * m) return;
-  const int r = (int)(j / m), i = (int)(j - (long)r * m);
-  gstore(g + j, i == row0 + r ? 1.f : 0.f);
-}
-
-// W[row0 + r][j] = beta W[row0 + r][j] + add[r][j] (rounded to nearest even for a bf16 W).
-__global__ void __launch_bounds__(256) merge_add(const float* add, int rows, int n, float beta, void* W, long ldw,
-                                                 int row0, int bf16) {
-  const long e = (long)blockIdx.x * 256 + threadIdx.x;
-  if (e >= (long)rows * n) return;
-  const int r = (int)(e / n), j = (int)(e - (long)r * n);
-  const long off = (long)(row0 + r) * ldw + j;
-  const float v = gload(add + e);
-  if (bf16) {
-    u16* w = static_cast<u16*>(W) + off;
-    *w = f2bf(beta != 0.f ? fmaf(beta, bf2f(*w), v) : v);
-  } else {
-    float* w = static_cast<float*>(W) + off;
-    *w = beta != 0.f ? fmaf(beta, *w, v) : v;
-  }
-}
-
 // c_plan[j] = c_user[user_of_slot[j]], zero in padding slots.
 __global__ void __launch_bounds__(256) coef_to_plan(const float* __restrict__ cu, const int* __restrict__ user_of_slot,
                                                     int nslot, float* __restrict__ cp) {
@@ -729,49 +704,8 @@ hipError_t launch_coef_to_user(const ff_plan* p, const float* c_plan, float* c_u
   return hipGetLastError();
 }
 
-// Merge through the backward: row i of dW = s P_out C P_in^T is (s P_in C^T P_out^T e_i)^T, the dX
-// of a backward whose upstream gradient is the unit vector e_i (Appendix A's chain rule read the
-// other way).  Frames applied in several radix-4 stages merge so, a chunk of rows at a time: the
-// chunk's unit vectors are written as fp32 rows, the fp32 backward computes their dX (straight
-// into an aligned fp32 W with beta, otherwise into a staging chunk that merge_add folds in).
-hipError_t launch_merge_transform(const ff_plan* p, const float* c, float scale, int w_bf16, float beta, void* W,
-                                  int64_t ldw, hipStream_t s) {
-  const int m = p->fout->d, n = p->fin->d, R = p->mrg_rows;
-  const bool direct = !w_bf16 && reinterpret_cast<uintptr_t>(W) % 16 == 0 && ldw % 4 == 0;
-  for (int row0 = 0; row0 < m; row0 += R) {
-    const int rows = std::min(R, m - row0);
-    const long cells = (long)rows * m;
-    hipLaunchKernelGGL(unit_rows, dim3((unsigned)((cells + 255) / 256)), dim3(256), 0, s, p->mrg_g, rows, m, row0);
-    hipError_t e;
-    if (direct) {
-      float* Wr = static_cast<float*>(W) + (long)row0 * ldw;
-      e = launch_bwd(p, 0, 1, rows, {nullptr, nullptr}, n, {p->mrg_g, nullptr}, m, c, nullptr, scale, beta,
-                     {Wr, nullptr}, ldw, true, 0, nullptr, nullptr, false, nullptr, s);
-    } else {
-      e = launch_bwd(p, 0, 1, rows, {nullptr, nullptr}, n, {p->mrg_g, nullptr}, m, c, nullptr, scale, 0.f,
-                     {p->mrg_out, nullptr}, n, true, 0, nullptr, nullptr, false, nullptr, s);
-      if (e == hipSuccess) {
-        const long outs = (long)rows * n;
-        hipLaunchKernelGGL(merge_add, dim3((unsigned)((outs + 255) / 256)), dim3(256), 0, s, p->mrg_out, rows, n,
-                           beta, W, ldw, row0, w_bf16);
-        e = hipGetLastError();
-      }
-    }
-    if (e != hipSuccess) return e;
-  }
-  return hipGetLastError();
-}
-
 hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf16, float beta, void* W,
                         int64_t ldw, hipStream_t s) {
-  if (p->mrg_rows > 0) {
-    hipEvent_t e0, e1;
-    take_timing_events(&e0, &e1);
-    record(e0, s);
-    const hipError_t e = launch_merge_transform(p, c, scale, w_bf16, beta, W, ldw, s);
-    record(e1, s);
-    return e;
-  }
   MergeArgs a{};
   a.Btm = p->fout->dev.Bt32;
   a.Btn = p->fin->dev.Bt32;

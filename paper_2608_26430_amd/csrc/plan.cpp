@@ -601,10 +601,9 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     kFPl, kBPl, kFSt, kPadSlots, kBW, kPartial, kCoefBwd, kBwdPos, kFEm, kBDst, kBEm, kBPad, kUserOfSlot,
     kSlotOfUser, kMrgG, kMrgOut, kLiftX, kLiftG, kLiftDX, kNumBlobs
   };
-  // frames applied in several radix-4 stages, and frames with a lift, merge through the backward,
-  // a chunk of (user) rows at a time
+  // frames with a lift merge through the backward, a chunk of (user) rows at a time
   const bool lifted = f_in->lifted || f_out->lifted;
-  const bool mrg_transform = FI.nst >= 2 || FO.nst >= 2 || lifted;
+  const bool mrg_transform = lifted;
   const int64_t mrg_rows = mrg_transform ? std::min<int64_t>(f_out->d, 1024) : 0;
   const size_t lift_rows = lifted ? (size_t)max_tokens : 0;
   // both directions of the coefficient layout, for the device-side conversions

@@ -417,77 +417,119 @@ __device__ __forceinline__ void radix4_synthesis(const FrameDev& f, const float2
   }
 }
 
-// Multi-stage factored analysis, k = 4^S k2 (S = 2 or 3), for every (token, block, b < k2) of a
-// tile: the item holds v[j] = x[b + k2 j] for j < 4^S (the digits of j, most significant first,
-// are the stage digits a_1 .. a_S of the input index b + sum_t a_t K_t, K_t = k / 4^t) and runs
-// the S decimation-in-frequency stages in registers.  Stage t combines over digit a_t with the
-// other digits fixed, y_a' = sum_a v_a (-i)^(a a'), then scales y_a' by w_k^(-a' n 4^(t-1)), where
-// n = b + k2 lo is the index left in the parent sequence (lo: the digits below a_t).  The output
-// digit a_t' takes a_t's place, so v[j] ends as sequence j = (a_1' .. a_S') at b, stored in LDS
-// column j (base-4 digit reversal of the frequency, lds_position), where the MFMA applies the dense
-// DFT of size k2.  fp32 throughout; LDS receives the activation type.
-// Stage T of S on the 4^S values (T a template parameter, so that every index into v is a
-// constant and v stays in registers).
+// Multi-stage factored apply (nst = S >= 2, k = 4^S k2), four lanes per (token, block, residue b):
+// the 4^S values x[b + k2 j] of a residue are split over the lanes of a quad by the lowest radix-4
+// digit of j, lane q holding v[m] = x[b + k2 (4 m + q)] (4^(S-1) values).  Stages 1 .. S-1 (digits
+// a_1 .. a_(S-1), of stride 4^(S-T) in j and 4^(S-T-1) in m) are then local to the lane; a 4 x 4
+// transpose within the quad regroups every block of four m into the four values of one group
+// {4 m' + a} (lane q then holds m' = 4 g + q, a = 0..3 in v[4 g + a]), and stage S runs locally
+// too.  Stage T is decimation in frequency over digit a_T: y_a' = w_k^(-a' n 4^(T-1)) sum_a v_a
+// (-i)^(a a'), n = b + k2 (digits of j below a_T); the twiddle is a per-lane base w_k^(a (b +
+// k2 q) 4^(T-1)) times w_k^(a 4 k2 lo 4^(T-1)) (lo the digits of m below a_T), which is the same in
+// every lane and read through the constant address space.  The output digit a_T' takes a_T's
+// place, so position j = (a_1' .. a_S') ends in LDS column j (the base-4 digit reversal of the
+// frequency, lds_position), where the MFMA applies the dense DFT of size k2.  fp32 throughout; LDS
+// receives the activation type.  The synthesis runs the adjoints in reverse order.  A lane holds 32
+// of the 128 values of a three-stage residue, and four times the lanes are at work.
 template <int S, int T, bool INV>
-__device__ __forceinline__ void msr_stage(float2 (&v)[1 << (2 * S)], int b, int k2, const float2* __restrict__ twk) {
-  constexpr int N = 1 << (2 * S);
-  constexpr int st = 1 << (2 * (S - T));     // stride of digit a_T in j
-  constexpr int tws = 1 << (2 * (T - 1));    // w_{K_{T-1}} = w_k^(4^(T-1))
-  constexpr bool inverse = INV;
-  // w_k^(a (b + k2 lo) tws) = w_k^(a b tws) w_k^(a k2 lo tws): a per-lane base loaded once per
-  // stage times a factor that is the same in every lane (k = 4^S k2 makes it a 4^S-th root of
-  // unity), so that few twiddles are in registers at a time
+__device__ __forceinline__ void msr_stage(float2 (&v)[1 << (2 * S - 2)], int bq, int k2,
+                                          const float2* __restrict__ twk) {
+  constexpr int NL = 1 << (2 * S - 2);
+  constexpr int st = 1 << (2 * (S - T) - 2);   // stride of digit a_T in m (T < S)
+  constexpr int tws = 1 << (2 * (T - 1));      // w_{K_{T-1}} = w_k^(4^(T-1))
   float2 wb[3];
 #pragma unroll
-  for (int a = 1; a < 4; ++a) wb[a - 1] = gload(twk + a * b * tws);
-  {
+  for (int a = 1; a < 4; ++a) wb[a - 1] = gload(twk + a * bq * tws);
 #pragma unroll
-    for (int hi = 0; hi < N / (4 * st); ++hi)
+  for (int hi = 0; hi < NL / (4 * st); ++hi)
 #pragma unroll
-      for (int lo = 0; lo < st; ++lo) {
-        const int base = hi * 4 * st + lo;
-        float2 w[3];
+    for (int lo = 0; lo < st; ++lo) {
+      const int base = hi * 4 * st + lo;
+      float2 w[3];
 #pragma unroll
-        for (int a = 1; a < 4; ++a) {
-          // the same address in every lane: read through the constant address space, as a scalar
-          // load into SGPRs
-          using R = Raw<sizeof(float2)>::T;
-          const float2 wu =
-              __builtin_bit_cast(float2, *((const __attribute__((address_space(4))) R*)(twk + a * k2 * lo * tws)));
-          w[a - 1] = lo == 0 ? wb[a - 1] : cmul(wb[a - 1], wu);
-        }
-        if constexpr (!inverse) {
-          const float2 x0 = v[base], x1 = v[base + st], x2 = v[base + 2 * st], x3 = v[base + 3 * st];
-          const float2 s02 = cadd(x0, x2), d02 = csub(x0, x2), s13 = cadd(x1, x3), d13 = csub(x1, x3);
-          v[base] = cadd(s02, s13);
-          v[base + st] = cmulc(make_float2(d02.x + d13.y, d02.y - d13.x), w[0]);      // d02 - i d13
-          v[base + 2 * st] = cmulc(csub(s02, s13), w[1]);
-          v[base + 3 * st] = cmulc(make_float2(d02.x - d13.y, d02.y + d13.x), w[2]);  // d02 + i d13
-        } else {   // the adjoint of the stage: twiddles w instead of conj(w), then i^(a a')
-          const float2 y0 = v[base], y1 = cmul(v[base + st], w[0]), y2 = cmul(v[base + 2 * st], w[1]),
-                       y3 = cmul(v[base + 3 * st], w[2]);
-          const float2 s02 = cadd(y0, y2), d02 = csub(y0, y2), s13 = cadd(y1, y3), d13 = csub(y1, y3);
-          v[base] = cadd(s02, s13);
-          v[base + st] = make_float2(d02.x - d13.y, d02.y + d13.x);        // d02 + i d13
-          v[base + 2 * st] = csub(s02, s13);
-          v[base + 3 * st] = make_float2(d02.x + d13.y, d02.y - d13.x);    // d02 - i d13
-        }
+      for (int a = 1; a < 4; ++a) {
+        using R = Raw<sizeof(float2)>::T;
+        const float2 wu =
+            __builtin_bit_cast(float2, *((const __attribute__((address_space(4))) R*)(twk + a * 4 * k2 * lo * tws)));
+        w[a - 1] = lo == 0 ? wb[a - 1] : cmul(wb[a - 1], wu);
       }
+      float2* x = v + base;
+      if constexpr (!INV) {
+        const float2 x0 = x[0], x1 = x[st], x2 = x[2 * st], x3 = x[3 * st];
+        const float2 s02 = cadd(x0, x2), d02 = csub(x0, x2), s13 = cadd(x1, x3), d13 = csub(x1, x3);
+        x[0] = cadd(s02, s13);
+        x[st] = cmulc(make_float2(d02.x + d13.y, d02.y - d13.x), w[0]);       // d02 - i d13
+        x[2 * st] = cmulc(csub(s02, s13), w[1]);
+        x[3 * st] = cmulc(make_float2(d02.x - d13.y, d02.y + d13.x), w[2]);   // d02 + i d13
+      } else {   // the adjoint of the stage: twiddles w instead of conj(w), then i^(a a')
+        const float2 y0 = x[0], y1 = cmul(x[st], w[0]), y2 = cmul(x[2 * st], w[1]), y3 = cmul(x[3 * st], w[2]);
+        const float2 s02 = cadd(y0, y2), d02 = csub(y0, y2), s13 = cadd(y1, y3), d13 = csub(y1, y3);
+        x[0] = cadd(s02, s13);
+        x[st] = make_float2(d02.x - d13.y, d02.y + d13.x);       // d02 + i d13
+        x[2 * st] = csub(s02, s13);
+        x[3 * st] = make_float2(d02.x + d13.y, d02.y - d13.x);   // d02 - i d13
+      }
+    }
+}
+
+// Stage S, local after the quad transpose: groups v[4 g .. 4 g + 3] over the lowest digit (n = b).
+template <int S, bool INV>
+__device__ __forceinline__ void msr_last_stage(float2 (&v)[1 << (2 * S - 2)], int b, const float2* __restrict__ twk) {
+  constexpr int NL = 1 << (2 * S - 2);
+  constexpr int tws = 1 << (2 * (S - 1));
+  float2 w[3];
+#pragma unroll
+  for (int a = 1; a < 4; ++a) w[a - 1] = gload(twk + a * b * tws);
+#pragma unroll
+  for (int g = 0; g < NL / 4; ++g) {
+    float2* x = v + 4 * g;
+    if constexpr (!INV) {
+      const float2 s02 = cadd(x[0], x[2]), d02 = csub(x[0], x[2]), s13 = cadd(x[1], x[3]), d13 = csub(x[1], x[3]);
+      x[0] = cadd(s02, s13);
+      x[1] = cmulc(make_float2(d02.x + d13.y, d02.y - d13.x), w[0]);
+      x[2] = cmulc(csub(s02, s13), w[1]);
+      x[3] = cmulc(make_float2(d02.x - d13.y, d02.y + d13.x), w[2]);
+    } else {
+      const float2 y0 = x[0], y1 = cmul(x[1], w[0]), y2 = cmul(x[2], w[1]), y3 = cmul(x[3], w[2]);
+      const float2 s02 = cadd(y0, y2), d02 = csub(y0, y2), s13 = cadd(y1, y3), d13 = csub(y1, y3);
+      x[0] = cadd(s02, s13);
+      x[1] = make_float2(d02.x - d13.y, d02.y + d13.x);
+      x[2] = csub(s02, s13);
+      x[3] = make_float2(d02.x + d13.y, d02.y - d13.x);
+    }
   }
 }
 
-// All S stages: 1 .. S for the analysis, the adjoints S .. 1 for the synthesis.
-template <int S>
-__device__ __forceinline__ void msr_stages(float2 (&v)[1 << (2 * S)], int b, int k2, const float2* __restrict__ twk,
-                                           bool inverse) {
-  if (!inverse) {
-    msr_stage<S, 1, false>(v, b, k2, twk);
-    if constexpr (S >= 2) msr_stage<S, 2, false>(v, b, k2, twk);
-    if constexpr (S >= 3) msr_stage<S, 3, false>(v, b, k2, twk);
-  } else {
-    if constexpr (S >= 3) msr_stage<S, 3, true>(v, b, k2, twk);
-    if constexpr (S >= 2) msr_stage<S, 2, true>(v, b, k2, twk);
-    msr_stage<S, 1, true>(v, b, k2, twk);
+// One component of a register exchanged with lane q ^ D of the quad (DPP quad permutation).
+template <int D>
+__device__ __forceinline__ float quad_swap(float x) {
+  constexpr int ctrl = D == 1 ? 0xB1 : 0x4E;   // quad_perm [1,0,3,2] / [2,3,0,1]
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), ctrl, 0xF, 0xF, false));
+}
+
+// Lane q's registers v[4 g + i] become lane i's v[4 g + q] (a 4 x 4 transpose per group g): two
+// rounds, each swapping one bit of the lane index with the same bit of the register index.
+template <int NL>
+__device__ __forceinline__ void quad_transpose(float2 (&v)[NL], int q) {
+#pragma unroll
+  for (int g = 0; g < NL / 4; ++g) {
+    float2* x = v + 4 * g;
+    const bool o1 = q & 1, o2 = q & 2;
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {   // bit 0: register pairs (2p, 2p + 1)
+      const float2 send = o1 ? x[2 * p] : x[2 * p + 1];
+      const float2 got = make_float2(quad_swap<1>(send.x), quad_swap<1>(send.y));
+      // selects with constant indices (a store to a selected element would put v in scratch)
+      x[2 * p] = o1 ? got : x[2 * p];
+      x[2 * p + 1] = o1 ? x[2 * p + 1] : got;
+    }
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {   // bit 1: register pairs (p, p + 2)
+      const float2 send = o2 ? x[p] : x[p + 2];
+      const float2 got = make_float2(quad_swap<2>(send.x), quad_swap<2>(send.y));
+      x[p] = o2 ? got : x[p];
+      x[p + 2] = o2 ? x[p + 2] : got;
+    }
   }
 }
 
@@ -495,60 +537,72 @@ template <bool BF16, int S>
 __device__ __forceinline__ void msr_analysis(const FrameDev& f, int nt, const typename Act<BF16>::E* src, long ld,
                                              typename Act<BF16>::E* dst, int ldt, int ldb) {
   using E = typename Act<BF16>::E;
-  constexpr int N = 1 << (2 * S);
+  constexpr int NL = 1 << (2 * S - 2);
   const int k2 = f.k2, W = f.W, cs = f.cs, W2 = f.W2;
   const int per_tok = f.nblk * k2, items = nt * per_tok;
   const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
-  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+  // whole quads: 4 items is a multiple of 4 and so is blockDim
+  for (int it4 = threadIdx.x; it4 < 4 * items; it4 += blockDim.x) {
+    const int q = it4 & 3, it = it4 >> 2;
     const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
     const int b = r - blk * k2;
-    const E* xp = src + (long)t * ld + blk * W + 2 * b;
-    float2 v[N];
+    const E* xp = src + (long)t * ld + blk * W + 2 * (b + k2 * q);
+    float2 v[NL];
 #pragma unroll
-    for (int j = 0; j < N; ++j) v[j] = gld2<BF16>(xp + 2 * k2 * j);
-    msr_stages<S>(v, b, k2, f.twk, false);
+    for (int m = 0; m < NL; ++m) v[m] = gld2<BF16>(xp + 8 * k2 * m);
+    const int bq = b + k2 * q;
+    msr_stage<S, 1, false>(v, bq, k2, f.twk);
+    if constexpr (S >= 3) msr_stage<S, 2, false>(v, bq, k2, f.twk);
+    quad_transpose(v, q);
+    msr_last_stage<S, false>(v, b, f.twk);
+    // v[4 g + a] is position j = 4 (4 g + q) + a: LDS column j
     E* y = dst + t * ldt + blk * ldb + 2 * b;
 #pragma unroll
-    for (int j = 0; j < N; ++j) st2<BF16>(y + j * cs, v[j]);
+    for (int g = 0; g < NL / 4; ++g)
+#pragma unroll
+      for (int a = 0; a < 4; ++a) st2<BF16>(y + (16 * g + 4 * q + a) * cs, v[4 * g + a]);
     if (b == 0)
-      for (int j = 0; j < N; ++j)
-        for (int e = W2; e < cs; ++e) Act<BF16>::st(y + j * cs + e, 0.f);
+      for (int g = 0; g < NL / 4; ++g)
+        for (int a = 0; a < 4; ++a)
+          for (int e = W2; e < cs; ++e) Act<BF16>::st(y + (16 * g + 4 * q + a) * cs + e, 0.f);
   }
 }
 
-// Multi-stage factored synthesis: the inverse stages on each (token, block, b) item read from the
+// Multi-stage factored synthesis: the inverse stages on each (token, block, b) quad read from the
 // LDS columns (after the dense DFT^H), then out = s x (+ beta out) into the token rows at dst.
 template <bool BF16, int S>
 __device__ __forceinline__ void msr_synthesis(const FrameDev& f, int nt, const typename Act<BF16>::E* src, int ldt,
                                               int ldb, typename Act<BF16>::E* dst, long ld, float s, float beta) {
   using E = typename Act<BF16>::E;
-  constexpr int N = 1 << (2 * S);
+  constexpr int NL = 1 << (2 * S - 2);
   const int k2 = f.k2, W = f.W, cs = f.cs;
   const int per_tok = f.nblk * k2, items = nt * per_tok;
   const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
-  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+  for (int it4 = threadIdx.x; it4 < 4 * items; it4 += blockDim.x) {
+    const int q = it4 & 3, it = it4 >> 2;
     const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
     const int b = r - blk * k2;
     const E* yp = src + t * ldt + blk * ldb + 2 * b;
-    float2 v[N];
+    float2 v[NL];
 #pragma unroll
-    for (int j = 0; j < N; ++j) v[j] = ld2<BF16>(yp + j * cs);
-    msr_stages<S>(v, b, k2, f.twk, true);
-    E* out = dst + (long)t * ld + blk * W + 2 * b;
-    // in groups of 16, so that the old values of a beta epilogue are not all loaded at once
+    for (int g = 0; g < NL / 4; ++g)
 #pragma unroll
-    for (int j0 = 0; j0 < N; j0 += 16) {
+      for (int a = 0; a < 4; ++a) v[4 * g + a] = ld2<BF16>(yp + (16 * g + 4 * q + a) * cs);
+    msr_last_stage<S, true>(v, b, f.twk);
+    quad_transpose(v, q);
+    const int bq = b + k2 * q;
+    if constexpr (S >= 3) msr_stage<S, 2, true>(v, bq, k2, f.twk);
+    msr_stage<S, 1, true>(v, bq, k2, f.twk);
+    E* out = dst + (long)t * ld + blk * W + 2 * (b + k2 * q);
 #pragma unroll
-      for (int j = j0; j < j0 + 16 && j < N; ++j) {
-        float2 o = make_float2(s * v[j].x, s * v[j].y);
-        if (beta != 0.f) {
-          const float2 old = gld2<BF16>(out + 2 * k2 * j);
-          o.x = fmaf(beta, old.x, o.x);
-          o.y = fmaf(beta, old.y, o.y);
-        }
-        gst2<BF16>(out + 2 * k2 * j, o);
+    for (int m = 0; m < NL; ++m) {
+      float2 o = make_float2(s * v[m].x, s * v[m].y);
+      if (beta != 0.f) {
+        const float2 old = gld2<BF16>(out + 8 * k2 * m);
+        o.x = fmaf(beta, old.x, o.x);
+        o.y = fmaf(beta, old.y, o.y);
       }
-      __builtin_amdgcn_sched_barrier(0);
+      gst2<BF16>(out + 8 * k2 * m, o);
     }
   }
 }

@@ -216,6 +216,11 @@ class Plan:
         """Most tokens per generic-kernel tile with those chunks."""
         return self.query(12 if dtype == "bf16" else 11)
 
+    @property
+    def gen_token_groups(self) -> bool:
+        """True when bf16 generic-kernel tiles keep four tokens of a coefficient together."""
+        return bool(self.query(13))
+
     def new_saved(self, device=None):
         """A c_saved array for one adapter of this plan (None when the plan needs none)."""
         torch = _torch()

@@ -217,6 +217,9 @@ struct ff_plan {
   int gen_ldt_in[2] = {0, 0};      // LDS token stride of the input-side chunk tile
   int gen_tile_tokens[2] = {0, 0};
   size_t gen_lds_bytes[2] = {0, 0};
+  // bf16 generic kernels on token-grouped tiles (four tokens per coefficient; tiles a multiple of
+  // four tokens): frames applied directly with blocks up to 128 wide, one chunk, no lift.
+  int gen_g4 = 0;
   int gen_wgs = 1;                 // compute units: resident workgroups of the generic kernels
   int gen_rows = 1;                // dC partial rows per adapter = most workgroups of the generic backward
   float* partial = nullptr;        // dC partial sums per tile (layout depends on the kernels)
@@ -327,7 +330,7 @@ hipError_t launch_bwd_lifted(const ff_plan* p, int bf16, int T, const void* X, i
 hipError_t launch_merge_lifted(const ff_plan* p, const float* c, float scale, int w_bf16, float beta, void* W,
                                int64_t ldw, hipStream_t s);
 // Generic-kernel tile size of a call (kernels.hip), shared by single, batched and group calls.
-int call_tile_tokens(int tt, long T, int count, int slots);
+int call_tile_tokens(int tt, long T, int count, int slots, bool g4);
 
 // Coefficient vectors between the caller's support order and the plan layout (Algorithm 1,
 // step 4): to_plan writes every slot (zero in padding slots), to_user every user entry (added to

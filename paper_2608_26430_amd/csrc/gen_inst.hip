@@ -54,6 +54,12 @@ hipError_t GEN_CONFIGURE_MS() {
 #else
 hipError_t GEN_LAUNCH(const GEN_ARGS& a, dim3 grid, size_t lds, hipStream_t s) {
   if (a.fin.nst >= 2 || a.fout.nst >= 2) return GEN_LAUNCH_MS(a, grid, lds, s);
+#if GEN_BF16
+  if (a.g4) {   // token-grouped tiles (the plan sets g4 only with one chunk and direct frames)
+    hipLaunchKernelGGL((GEN_KERNEL<true, false, false, true>), grid, dim3(kFusedThreads), lds, s, a);
+    return hipGetLastError();
+  }
+#endif
   if (a.nch > 1)
     hipLaunchKernelGGL((GEN_KERNEL<GEN_BF16 != 0, true>), grid, dim3(kFusedThreads), lds, s, a);
   else
@@ -64,7 +70,13 @@ hipError_t GEN_LAUNCH(const GEN_ARGS& a, dim3 grid, size_t lds, hipStream_t s) {
 hipError_t GEN_CONFIGURE() {
   hipError_t e = GEN_CONFIGURE_MS();
   for (const void* fn : {reinterpret_cast<const void*>(&GEN_KERNEL<GEN_BF16 != 0, true>),
-                         reinterpret_cast<const void*>(&GEN_KERNEL<GEN_BF16 != 0, false>)}) {
+                         reinterpret_cast<const void*>(&GEN_KERNEL<GEN_BF16 != 0, false>),
+#if GEN_BF16
+                         reinterpret_cast<const void*>(&GEN_KERNEL<true, false, false, true>)
+#else
+                         reinterpret_cast<const void*>(&GEN_KERNEL<false, false>)
+#endif
+       }) {
     const hipError_t r = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
     if (r != hipSuccess) e = r;
   }

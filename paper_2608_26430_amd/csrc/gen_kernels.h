@@ -260,6 +260,118 @@ __device__ __forceinline__ void column_apply(const FrameDev& f, bool synth, int 
   column_apply_mem<BF16, GSRC>(frag, f.MT, KT, ncols, lim, col, epi);
 }
 
+// ---------------------------------------------------------------------------------------------
+// Token-grouped tiles (bf16 activations, frame blocks applied directly, up to 128 wide).  The
+// element of token t at token-row offset p (the layout of one token row is unchanged) lives at
+// ((t / 4) ldt + p) 4 + t % 4: every coefficient holds four consecutive tokens in 8 bytes, so a
+// table row of the sparse phases reads or writes four tokens with one LDS access instead of four.
+// The frame applies keep full-width LDS accesses.  A group of 16 MFMA columns is four tokens
+// (4 tg .. 4 tg + 3) of four consecutive blocks (4 sq .. 4 sq + 3), column j being token j % 4
+// of block j / 4.  Analysis runs the MFMA with its operands swapped (D = X^T M^T: rows are the
+// group's columns), so that lane (q, L) ends with the four tokens of block 4 sq + q at output
+// coefficient 16 mt + L, one 8-byte LDS write; synthesis reads its operand with
+// ds_read_b64_tr_b16.  Token slots past the tile's tokens receive zeros from the analysis (their
+// operands are zero), so the sparse phases may read and write whole groups.
+
+typedef short g4_i16x4 __attribute__((ext_vector_type(4)));
+
+// Contraction elements 32 ks + 8 q .. + 7 of column L of a group from a token-grouped LDS tile,
+// by two transposed reads: within each 16 lanes the 8-byte chunks form 4 rows of 16 values and
+// lane L receives value L of each row.  For read h, lane L supplies element k0 + L / 4 (k0 =
+// 32 ks + 8 q + 4 h) of block 4 sq + L % 4, i.e. that block's four tokens, so lane L receives
+// elements k0 .. k0 + 3 of its own column.  at(c4, k) is the 8-byte chunk of block 4 sq + c4 at
+// element k (k < lim); elements at or past lim are returned as zero.
+template <int KT, class At>
+__device__ __forceinline__ void g4_tile_operand(At at, int lim, int q, int L, bf16x8 (&b)[KT]) {
+#pragma unroll
+  for (int ks = 0; ks < KT; ++ks) {
+    unsigned w[4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int k0 = 32 * ks + 8 * q + 4 * h;
+      const u16* p = at(L & 3, min(k0 + (L >> 2), lim - 1));
+      const raw2 r = __builtin_bit_cast(
+          raw2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) g4_i16x4*)(const_cast<u16*>(p))));
+      const int nv = lim - k0;   // valid elements of this read (the same in the 16 lanes)
+      w[2 * h] = nv >= 2 ? r.x : nv == 1 ? (r.x & 0xffffu) : 0u;
+      w[2 * h + 1] = nv >= 4 ? r.y : nv == 3 ? (r.y & 0xffffu) : 0u;
+    }
+    b[ks] = __builtin_bit_cast(bf16x8, raw4{w[0], w[1], w[2], w[3]});
+  }
+}
+
+// Every group g < ngrp (token group g / nsq, block quad g % nsq): SWAP (analysis, operands from
+// token rows in global memory: colg(tg, sq, L) is column L's row start, NULL outside the tile)
+// gives epi(tg, sq, mt, acc) tokens 0..3 of block 4 sq + q at coefficient 16 mt + L; otherwise
+// (synthesis, operands from the LDS tile through at(tg, sq, c4, k)) outputs 16 mt + 4 q .. + 3 of
+// column L.  The fragments stay in registers; each wave takes every nw-th group with the next
+// group's operands in flight.
+template <bool SWAP, int MT, int KT, class ColG, class At, class Epi>
+__device__ __forceinline__ void column_apply_g4(const void* frag, int ngrp, int nsq, int lim, ColG colg, At at,
+                                                Epi epi) {
+  using M = Mfma<true>;
+  using V = typename M::V;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
+            q = lane >> 4, L = lane & 15;
+  if (wave >= ngrp) return;
+  const V* fr = reinterpret_cast<const V*>(frag);
+  asm volatile("" : "+s"(fr));
+  V fa[MT][KT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int ks = 0; ks < KT; ++ks) fa[mt][ks] = gload(&fr[(mt * KT + ks) * 64 + lane]);
+  V ba[KT], bb[KT];
+  auto load = [&](int g, V (&b)[KT]) {
+    const int tg = g / nsq, sq = g - tg * nsq;
+    if constexpr (SWAP) {
+      const u16* in = colg(tg, sq, L);
+      const bool ok = in != nullptr;
+#pragma unroll
+      for (int ks = 0; ks < KT; ++ks) b[ks] = load_operand<true, true>(ok ? in : colg(0, 0, 0), ok, lim, ks, q);
+    } else {
+      g4_tile_operand<KT>([&](int c4, int k) { return at(tg, sq, c4, k); }, lim, q, L, b);
+    }
+  };
+  auto mul = [&](int g, const V (&b)[KT]) {
+    f32x4 acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KT; ++ks)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        acc[mt] = SWAP ? M::step(b[ks], fa[mt][ks], acc[mt]) : M::step(fa[mt][ks], b[ks], acc[mt]);
+    const int tg = g / nsq, sq = g - tg * nsq;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) epi(tg, sq, mt, acc[mt]);
+  };
+  load(wave, ba);
+  for (int g = wave; g < ngrp; g += 2 * nw) {
+    if (g + nw < ngrp) load(g + nw, bb);
+    mul(g, ba);
+    if (g + nw >= ngrp) break;
+    if (g + 2 * nw < ngrp) load(g + 2 * nw, ba);
+    mul(g + nw, bb);
+  }
+}
+
+template <bool SWAP, class ColG, class At, class Epi>
+__device__ __forceinline__ void column_apply_g4(const FrameDev& f, bool synth, int ngrp, int nsq, ColG colg, At at,
+                                                Epi epi) {
+  const void* frag = synth ? f.fs16 : f.fa16;
+#define FF_SHAPE(mt, kt)                                                           \
+  case (mt) * 64 + (kt):                                                           \
+    column_apply_g4<SWAP, mt, kt>(frag, ngrp, nsq, f.W, colg, at, epi);            \
+    return;
+  switch (f.MT * 64 + f.KT) {
+    FF_SHAPE(1, 1) FF_SHAPE(2, 1) FF_SHAPE(3, 2) FF_SHAPE(4, 2) FF_SHAPE(5, 3) FF_SHAPE(6, 3)
+    FF_SHAPE(7, 4) FF_SHAPE(8, 4)
+    default: break;   // not taken: the plan uses these tiles only for blocks up to 128 wide
+  }
+#undef FF_SHAPE
+}
+
 // Two consecutive activations (one complex coordinate) as fp32, and back.
 template <bool BF16>
 __device__ __forceinline__ float2 ld2(const typename Act<BF16>::E* p) {
@@ -717,6 +829,47 @@ __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const floa
   }
 }
 
+// z = P^T x for a tile into a token-grouped LDS tile (frames applied directly): every token slot
+// of the tile's groups is written, those past nt with zeros.
+__device__ __forceinline__ void analysis_g4(const FrameDev& f, int nt, const u16* src, long ld, u16* dst, int ldt,
+                                            int ldb) {
+  const int nblk = f.nblk, W = f.W, nsq = (nblk + 3) / 4, ngrp = (nt + 3) / 4 * nsq;
+  const int lane = threadIdx.x & 63, q = lane >> 4, L = lane & 15;
+  column_apply_g4<true>(
+      f, false, ngrp, nsq,
+      [&](int tg, int sq, int c) -> const u16* {
+        const int t = 4 * tg + (c & 3), b = 4 * sq + (c >> 2);
+        return t < nt && b < nblk ? src + (long)t * ld + b * W : nullptr;
+      },
+      [&](int, int, int, int) -> const u16* { return dst; },
+      [&](int tg, int sq, int mt, f32x4 v) {
+        const int b = 4 * sq + q, o = 16 * mt + L;
+        if (b < nblk && o < W) Act<true>::st4(dst + 4 * (tg * ldt + b * ldb + o), v);
+      });
+}
+
+// out = s P v (+ beta out) for a tile from a token-grouped LDS tile (frames applied directly).
+__device__ __forceinline__ void synthesis_g4(const FrameDev& f, int nt, const u16* src, int ldt, int ldb, u16* dst,
+                                             long ld, float s, float beta) {
+  const int nblk = f.nblk, W = f.W, nsq = (nblk + 3) / 4, ngrp = (nt + 3) / 4 * nsq;
+  const int lane = threadIdx.x & 63, q = lane >> 4, L = lane & 15;
+  column_apply_g4<false>(
+      f, true, ngrp, nsq, [&](int, int, int) -> const u16* { return src; },
+      [&](int tg, int sq, int c4, int k) -> const u16* {
+        const int b = min(4 * sq + c4, nblk - 1);
+        return src + 4 * (tg * ldt + b * ldb + k);
+      },
+      [&](int tg, int sq, int mt, f32x4 v) {
+        const int t = 4 * tg + (L & 3), b = 4 * sq + (L >> 2), o = 16 * mt + 4 * q;
+        if (t < nt && b < nblk && o < W) {
+          u16* p = dst + (long)t * ld + b * W + o;
+          f32x4 r = v * s;
+          if (beta != 0.f) r += beta * Act<true>::gld4(p);
+          Act<true>::gst4(p, r);
+        }
+      });
+}
+
 // Sparse products over a generic stream (GenStream).  Each wave walks its run of stream rows
 // with the next kSD rows' entries and coefficients in flight.  Lane l accumulates, for tokens
 // tg0 .. tg0 + ntg - 1 of the tile, its slot's entries times the source coefficients (src tile)
@@ -877,6 +1030,130 @@ __device__ __forceinline__ void stream_all(const GenStream& S, const float* __re
   }
 }
 
+// The sparse products on token-grouped tiles: the same walk, each table row reading NG groups of
+// four tokens (one 8-byte LDS read each) for the pass's tokens tg0 .. tg0 + 4 NG - 1 (tg0 a
+// multiple of 4) and writing whole groups at a slab's end.  Token slots past ntg hold zeros in the
+// source tile, so their sums are zero; their dC weights zb are zero as well.
+template <bool BWD, bool PART_ADD, int NG>
+__device__ __forceinline__ void stream_products_g4(const GenStream& S, const float* __restrict__ cv, const u16* src,
+                                                   int ld_src, u16* dst, int ld_dst, int tg0, int ntg,
+                                                   bool write_dst, float* part) {
+  using A = Act<true>;
+  constexpr int NT = 4 * NG;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r0 = S.wave_row[wave], r1 = S.wave_row[wave + 1];
+  if (r0 >= r1) return;
+  const int2* ent = (S.ent);
+  src += tg0 * ld_src;   // group tg0 / 4 starts at element 4 (tg0 / 4) ld
+  dst += tg0 * ld_dst;
+  const int gs = 4 * ld_src, gd = 4 * ld_dst;
+  int2 ea[kSD], eb[kSD];
+  float ca[kSD], cb[kSD];
+  float pa[kSD], pb[kSD];
+  auto load = [&](int r, int2 (&e)[kSD], float (&c)[kSD], float (&pv)[kSD]) {
+#pragma unroll
+    for (int i = 0; i < kSD; ++i) {
+      const int j = min(r + i, r1 - 1) * 64 + lane;
+      e[i] = gload(&ent[j]);
+      c[i] = gload(&cv[j]);
+      if (BWD && PART_ADD && part) pv[i] = gload(&part[j]);
+    }
+  };
+  float acc[NT], zb[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = zb[t] = 0.f;
+  bool start = true;
+  auto read = [&](const int2& e, float (&x)[NT]) {
+    const int so = 4 * (e.x & 0x7fffffff);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const f32x4 v = A::ld4(src + g * gs + so);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[4 * g + i] = v[i];
+    }
+  };
+  auto consume = [&](int r, const int2 (&e)[kSD], const float (&c)[kSD], const float (&pv)[kSD], int n) {
+    float xa[NT], xb[NT];
+    read(e[0], xa);
+#pragma unroll
+    for (int i = 0; i < kSD; ++i) {
+      if (i >= n) break;
+      float (&x)[NT] = (i & 1) ? xb : xa;
+      if (i + 1 < kSD && i + 1 < n) read(e[i + 1], (i & 1) ? xa : xb);
+      const int d = e[i].y;
+      if (BWD && part && start) {
+        const int dc0 = 4 * max(d, 0);
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          const f32x4 zv = A::ld4(dst + g * gd + dc0);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) zb[4 * g + k] = (4 * g + k < ntg && d >= 0) ? zv[k] : 0.f;
+        }
+      }
+      start = false;
+      float dc = 0.f;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        acc[t] = fmaf(c[i], x[t], acc[t]);
+        if (BWD) dc = fmaf(x[t], zb[t], dc);
+      }
+      if (BWD && part) gstore(part + (long)(r + i) * 64 + lane, PART_ADD ? pv[i] + dc : dc);
+      if (__builtin_amdgcn_readfirstlane(e[i].x) < 0) {   // the slab's last row (same in every lane)
+        if (write_dst && d >= 0) {
+#pragma unroll
+          for (int g = 0; g < NG; ++g) {
+            f32x4 v = f32x4{acc[4 * g], acc[4 * g + 1], acc[4 * g + 2], acc[4 * g + 3]};
+            if constexpr (!BWD && PART_ADD) v += A::ld4(dst + g * gd + 4 * d);   // a later input chunk
+            A::st4(dst + g * gd + 4 * d, v);
+          }
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[t] = 0.f;
+        start = true;
+      }
+    }
+  };
+  const int rend = r0 + (r1 - r0) / (2 * kSD) * (2 * kSD);
+  load(r0, ea, ca, pa);
+  load(r0 + kSD, eb, cb, pb);
+  for (int r = r0; r < rend; r += 2 * kSD) {
+    consume(r, ea, ca, pa, kSD);
+    load(r + 2 * kSD, ea, ca, pa);
+    consume(r + kSD, eb, cb, pb, kSD);
+    load(r + 3 * kSD, eb, cb, pb);
+  }
+  if (rend < r1) {
+    consume(rend, ea, ca, pa, min(kSD, r1 - rend));
+    if (rend + kSD < r1) consume(rend + kSD, eb, cb, pb, r1 - rend - kSD);
+  }
+}
+
+template <bool BWD, bool PART_ADD>
+__device__ __forceinline__ void stream_pass_g4(const GenStream& S, const float* __restrict__ cv, const u16* src,
+                                               int ld_src, u16* dst, int ld_dst, int tg, int ntg, bool write_dst,
+                                               float* part) {
+  switch ((ntg + 3) / 4) {
+    case 1: stream_products_g4<BWD, PART_ADD, 1>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    case 2: stream_products_g4<BWD, PART_ADD, 2>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    case 3: stream_products_g4<BWD, PART_ADD, 3>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    default: stream_products_g4<BWD, PART_ADD, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+  }
+}
+
+// All tokens of a token-grouped tile, 16 at a time, the last pass reading only the groups it needs.
+template <bool BWD>
+__device__ __forceinline__ void stream_all_g4(const GenStream& S, const float* __restrict__ cv, const u16* src,
+                                              int ld_src, u16* dst, int ld_dst, int nt, bool write_dst, float* part,
+                                              bool add = false) {
+  for (int tg = 0; tg < nt; tg += 16) {
+    const int ntg = min(16, nt - tg);
+    if (BWD && (add || tg > 0))
+      stream_pass_g4<BWD, BWD>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    else
+      stream_pass_g4<BWD, false>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+  }
+}
+
 struct FwdArgs {
   FrameDev fin, fout;
   int T, tt, ldt_in, ldt_out, ldb_in, ldb_out;
@@ -898,6 +1175,7 @@ struct FwdArgs {
   // (device, clamped to [0, T]; NULL: T)
   const GenDesc* group;
   const int* tokens;
+  int g4;               // token-grouped tiles (bf16, frames applied directly, whole input side)
 };
 
 __device__ __forceinline__ int group_tokens(const int* tokens, int T, int bi) {
@@ -905,14 +1183,16 @@ __device__ __forceinline__ int group_tokens(const int* tokens, int T, int bi) {
 }
 
 // CHUNKED: the input side in a.nch chunks of blocks, v accumulated over them; otherwise whole
-// (a.nch == 1), in code of its own.
-template <bool BF16, bool CHUNKED, bool MS = false>
+// (a.nch == 1), in code of its own.  G4: token-grouped tiles (bf16, whole input side, frames
+// applied directly), whose token slots are rounded up to whole groups of four.
+template <bool BF16, bool CHUNKED, bool MS = false, bool G4 = false>
 __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   using A = Act<BF16>;
   using E = typename A::E;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  E* zt = reinterpret_cast<E*>(smem);           // tt x ldt_in   z = P_in^T x (of one chunk)
-  E* vt = zt + (size_t)a.tt * a.ldt_in;         // tt x ldt_out  v = C z
+  const int cap = G4 ? (a.tt + 3) & ~3 : a.tt;   // token slots of a tile
+  E* zt = reinterpret_cast<E*>(smem);           // cap x ldt_in   z = P_in^T x (of one chunk)
+  E* vt = zt + (size_t)cap * a.ldt_in;          // cap x ldt_out  v = C z
   const int bi = blockIdx.y;
   const E* X = (reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X));
   E* Y = (reinterpret_cast<E*>(a.Ys ? a.Ys[bi] : a.Y));
@@ -931,8 +1211,18 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   X += (long)t0 * a.ldx;
   Y += (long)t0 * a.ldy;
 
+  if constexpr (G4) {
+    static_assert(BF16 && !CHUNKED && !MS, "token-grouped tiles: bf16, whole input side, direct frames");
+    analysis_g4(a.fin, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
+    __syncthreads();
+    stream_all_g4<false>(st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
+    __syncthreads();
+    synthesis_g4(a.fout, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, a.scale, a.beta);
+    return;
+  }
+
   // twiddle factors of factored frames after the tiles
-  float2* tw_in = reinterpret_cast<float2*>(vt + (size_t)a.tt * a.ldt_out);
+  float2* tw_in = reinterpret_cast<float2*>(vt + (size_t)cap * a.ldt_out);
   float2* tw_out = tw_in + kTwLdsBytes / 16;
   stage_twiddles(a.fin, tw_in);
   stage_twiddles(a.fout, tw_out);
@@ -993,17 +1283,20 @@ struct BwdArgs {
   // token count (device, clamped to [0, T]; NULL: T)
   const GenDesc* group;
   const int* tokens;
+  int g4;               // token-grouped tiles (bf16, frames applied directly, whole input side)
 };
 
 // CHUNKED: the input side in a.nch chunks of blocks; otherwise whole (a.nch == 1), in code of
-// its own (the chunk loop costs registers that the whole-side kernel then spills).
-template <bool BF16, bool CHUNKED, bool MS = false>
+// its own (the chunk loop costs registers that the whole-side kernel then spills).  G4 as for the
+// forward.
+template <bool BF16, bool CHUNKED, bool MS = false, bool G4 = false>
 __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   using A = Act<BF16>;
   using E = typename A::E;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  E* ut = reinterpret_cast<E*>(smem);           // tt x ldt_out  u = P_out^T g
-  E* zt = ut + (size_t)a.tt * a.ldt_out;        // tt x ldt_in   z = P_in^T x of one chunk, later q = C^T u
+  const int cap = G4 ? (a.tt + 3) & ~3 : a.tt;   // token slots of a tile
+  E* ut = reinterpret_cast<E*>(smem);           // cap x ldt_out  u = P_out^T g
+  E* zt = ut + (size_t)cap * a.ldt_out;         // cap x ldt_in   z = P_in^T x of one chunk, later q = C^T u
   const int bi = blockIdx.y;
   const E* G0 = reinterpret_cast<const E*>(a.Gs ? a.Gs[bi] : a.G);
   const E* X0 = reinterpret_cast<const E*>(a.Xs ? a.Xs[bi] : a.X);
@@ -1024,7 +1317,7 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
   }
 
   // twiddle factors of factored frames after the tiles
-  float2* tw_in = reinterpret_cast<float2*>(zt + (size_t)a.tt * a.ldt_in);
+  float2* tw_in = reinterpret_cast<float2*>(zt + (size_t)cap * a.ldt_in);
   float2* tw_out = tw_in + kTwLdsBytes / 16;
   stage_twiddles(a.fin, tw_in);
   stage_twiddles(a.fout, tw_out);
@@ -1035,6 +1328,17 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
     const int nt = (int)min((long)a.tt, (long)Tb - t0);
     if (tile != blockIdx.x) __syncthreads();   // the previous tile's LDS reads are done
 
+    if constexpr (G4) {
+      static_assert(BF16 && !CHUNKED && !MS, "token-grouped tiles: bf16, whole input side, direct frames");
+      analysis_g4(a.fout, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
+      if (a.want_dc) analysis_g4(a.fin, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
+      __syncthreads();
+      stream_all_g4<true>(st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
+      if (!a.want_dx) continue;
+      __syncthreads();
+      synthesis_g4(a.fin, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale, a.beta);
+      continue;
+    }
     if constexpr (!CHUNKED) {
       // q is written over z and then synthesized from whole columns: their padding must be zero
       zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);

@@ -61,7 +61,7 @@ ff_status ff_plan_group_create(int64_t count, const ff_plan* const* plans, ff_pl
     if (p->device != ref->device) return ff::fail(FF_EINVAL, "plan %lld is on another device", (long long)i);
     if (p->fast.enabled != ref->fast.enabled)
       return ff::fail(FF_EUNSUPPORTED, "plan %lld takes another kernel path than plan 0", (long long)i);
-    bool same = p->gen_nch == ref->gen_nch && p->dev.fwd_by_pos == ref->dev.fwd_by_pos;
+    bool same = p->gen_nch == ref->gen_nch && p->gen_g4 == ref->gen_g4 && p->dev.fwd_by_pos == ref->dev.fwd_by_pos;
     for (int k = 0; k < 2; ++k)
       same = same && p->gen_tile_tokens[k] == ref->gen_tile_tokens[k] && p->gen_ldt_in[k] == ref->gen_ldt_in[k] &&
              p->ldt_out[k] == ref->ldt_out[k] && p->gen_lds_bytes[k] == ref->gen_lds_bytes[k];

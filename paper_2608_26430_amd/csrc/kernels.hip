@@ -441,17 +441,17 @@ hipError_t launch_gather(const float* c, const float* const* cs, const int* idx,
 // workgroup per CU, so tiles go in rounds of `slots` and a call costs about rounds x (token rows
 // its sparse walks read per table row + a fixed part worth kTileOverhead of them).  Of the tile
 // sizes up to tt (the plan's LDS limit) the cheapest is taken, the larger one on ties (fewer
-// passes over the tables).
+// passes over the tables).  Token-grouped tiles (g4) read whole groups of four tokens.
 constexpr int kTileOverhead = 2;
 
-int call_tile_tokens(int tt, long T, int count, int slots) {
+int call_tile_tokens(int tt, long T, int count, int slots, bool g4) {
   if (T <= 0 || slots < 1) return tt;
   int best = tt;
   long best_cost = -1;
   for (int t = tt; t >= 1; --t) {
     const long tiles = (T + t - 1) / t * count;
     const long rounds = (tiles + slots - 1) / slots;
-    const int rem = t % kTG, walk = t - rem + (rem ? std::max(rem, 2) : 0);
+    const int rem = t % kTG, walk = g4 ? (t + 3) & ~3 : t - rem + (rem ? std::max(rem, 2) : 0);
     const long cost = rounds * (walk + kTileOverhead);
     if (best_cost < 0 || cost < best_cost) best = t, best_cost = cost;
   }
@@ -466,10 +466,11 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
   a.T = T;
-  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, count, p->gen_wgs);
+  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, count, p->gen_wgs, bf16 && p->gen_g4);
   a.ldt_in = p->gen_ldt_in[bf16];
   a.ldt_out = p->ldt_out[bf16];
   a.nch = p->gen_nch;
+  a.g4 = bf16 ? p->gen_g4 : 0;
   for (int i = 0; i <= p->gen_nch; ++i) a.chunk_blk[i] = p->gen_chunk_blk[i];
   a.ldb_in = p->ldb_in;
   a.ldb_out = p->ldb_out;
@@ -504,7 +505,7 @@ hipError_t launch_fwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
 // call of T tokens uses on the generic kernels; the partial rows start 256-byte aligned.
 size_t gen_bwd_scratch_floats(const ff_plan* p, int bf16, int T, size_t* partial_off) {
   const long cstride = 64L * p->dev.bwd.rows;
-  const int tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, 1, p->gen_wgs);
+  const int tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, 1, p->gen_wgs, bf16 && p->gen_g4);
   const long nwg = std::min<long>((T + tt - 1) / tt, p->gen_rows);
   const size_t off = ((size_t)cstride + 63) / 64 * 64;
   if (partial_off) *partial_off = off;
@@ -529,12 +530,13 @@ hipError_t launch_bwd(const ff_plan* p, int bf16, int count, int T, ActPtrs X, i
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
   a.T = T;
-  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, count, p->gen_wgs);
+  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, count, p->gen_wgs, bf16 && p->gen_g4);
   a.ldt_in = p->gen_ldt_in[bf16];
   a.ldt_out = p->ldt_out[bf16];
   a.ldb_in = p->ldb_in;
   a.ldb_out = p->ldb_out;
   a.nch = p->gen_nch;
+  a.g4 = bf16 ? p->gen_g4 : 0;
   for (int i = 0; i <= p->gen_nch; ++i) a.chunk_blk[i] = p->gen_chunk_blk[i];
   a.X = X.one;
   a.Xs = X.many;
@@ -600,10 +602,11 @@ hipError_t launch_fwd_group(const ff_plan_group* g, int bf16, int T, const int* 
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
   a.T = T;
-  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, (int)count, p->gen_wgs);
+  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, (int)count, p->gen_wgs, bf16 && p->gen_g4);
   a.ldt_in = p->gen_ldt_in[bf16];
   a.ldt_out = p->ldt_out[bf16];
   a.nch = p->gen_nch;
+  a.g4 = bf16 ? p->gen_g4 : 0;
   for (int i = 0; i <= p->gen_nch; ++i) a.chunk_blk[i] = p->gen_chunk_blk[i];
   a.ldb_in = p->ldb_in;
   a.ldb_out = p->ldb_out;
@@ -643,12 +646,13 @@ hipError_t launch_bwd_group(const ff_plan_group* g, int bf16, int T, const int* 
   a.fin = p->fin->dev;
   a.fout = p->fout->dev;
   a.T = T;
-  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, (int)count, p->gen_wgs);
+  a.tt = call_tile_tokens(p->gen_tile_tokens[bf16], T, (int)count, p->gen_wgs, bf16 && p->gen_g4);
   a.ldt_in = p->gen_ldt_in[bf16];
   a.ldt_out = p->ldt_out[bf16];
   a.ldb_in = p->ldb_in;
   a.ldb_out = p->ldb_out;
   a.nch = p->gen_nch;
+  a.g4 = bf16 ? p->gen_g4 : 0;
   for (int i = 0; i <= p->gen_nch; ++i) a.chunk_blk[i] = p->gen_chunk_blk[i];
   a.Xs = X;
   a.ldx = (long)ldx;

@@ -346,10 +346,16 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
       }
     p->gen_nch = nch;
     for (int c = 0; c <= nch; ++c) p->gen_chunk_blk[c] = (int)((int64_t)c * FI.nblk / nch);
+    // bf16 token-grouped tiles (gen_kernels.h): every table row of the sparse phases reads four
+    // tokens per LDS access; they need whole groups of four tokens and the dense block apply
+    const bool direct = FI.radix == 1 && FO.radix == 1 && FI.nst == 0 && FO.nst == 0 && FI.W <= 128 &&
+                        FO.W <= 128;
+    p->gen_g4 = direct && nch == 1 && !f_in->lifted && !f_out->lifted && chunk_tokens(nch, FF_BF16) >= 4;
     for (int dt = 0; dt < 2; ++dt) {
       const int esz = dt == FF_BF16 ? 2 : 4;
       p->gen_ldt_in[dt] = token_stride((FI.nblk + nch - 1) / nch, p->ldb_in, esz);
       p->gen_tile_tokens[dt] = (int)chunk_tokens(nch, dt);
+      if (dt == FF_BF16 && p->gen_g4) p->gen_tile_tokens[dt] &= ~3;
       p->gen_lds_bytes[dt] = (size_t)p->gen_tile_tokens[dt] * (size_t)(p->ldt_out[dt] + p->gen_ldt_in[dt]) * esz +
                              ff::kTwLdsBytes;
     }
@@ -752,6 +758,7 @@ extern "C" ff_status ff_plan_query(const ff_plan* p, int key, int64_t* value) {
     case FF_Q_GEN_CHUNKS: *value = p->gen_nch; return FF_OK;
     case FF_Q_GEN_TILE_TOKENS_F32: *value = p->gen_tile_tokens[FF_F32]; return FF_OK;
     case FF_Q_GEN_TILE_TOKENS_BF16: *value = p->gen_tile_tokens[FF_BF16]; return FF_OK;
+    case FF_Q_GEN_TOKEN_GROUPS: *value = p->gen_g4; return FF_OK;
     default: return ff::fail(FF_EINVAL, "unknown query key %d", key);
   }
 }

@@ -111,6 +111,11 @@ def test_small_parity(dev, shape, dtype):
     assert plan.radix == (4 if 2 * k_in > 128 else 1, 4 if 2 * k_out > 128 else 1)
     # the generic kernels chunk the input side only for the wide, dense-support shapes
     assert (plan.gen_chunks > 1) == (n == 8192)
+    # bf16 tiles keep four tokens per coefficient together where both blocks are applied directly
+    # (whole multiples of four tokens per tile)
+    assert plan.gen_token_groups == (plan.radix == (1, 1) and plan.gen_chunks == 1)
+    if plan.gen_token_groups:
+        assert plan.gen_tile_tokens("bf16") % 4 == 0 and plan.gen_tile_tokens("bf16") >= 4
     pad = 8 if dtype == "bf16" else 4
     xbuf, Xd = guarded(T, n, n + pad, dtype, dev, X)
     gbuf, Gd = guarded(T, m, m + 2 * pad, dtype, dev, G)
@@ -248,11 +253,14 @@ def test_batched_matches_single_calls(dev, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_generic_backward_many_tiles_per_workgroup(dev, dtype):
+@pytest.mark.parametrize("shape", [(2752, 16, 1024, 16, 3000), (768, 64, 2304, 64, 3000)],
+                         ids=["factored_in", "direct_vit"])
+def test_generic_backward_many_tiles_per_workgroup(dev, dtype, shape):
     """The generic backward runs at most one workgroup per CU, looping over tiles: with several
     tiles per workgroup, a dX-only call (no dC rows to accumulate into), a dC-only call and a
-    call with both match the oracle, and dC is deterministic."""
-    n, rn, m, rm, nnz = 2752, 16, 1024, 16, 3000
+    call with both match the oracle, and dC is deterministic.  Shapes: a factored input frame,
+    and directly applied frames (token-grouped tiles in bf16)."""
+    n, rn, m, rm, nnz = shape
     f_in, f_out = ff.framegen(n, n // rn, rn), ff.framegen(m, m // rm, rm)
     g = inputs.rng(4242)
     rows, cols = inputs.support(g, m, n, nnz)
@@ -264,7 +272,8 @@ def test_generic_backward_many_tiles_per_workgroup(dev, dtype):
     X = inputs.gaussian(g, (T, n), dtype=dtype)
     G = inputs.gaussian(g, (T, m), dtype=dtype)
     plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T)
-    assert plan.radix == (4, 1) and not plan.fast128
+    assert plan.radix == ((4, 1) if n == 2752 else (1, 1)) and not plan.fast128
+    assert plan.gen_token_groups == (n == 768)
     Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
     c = plan_c(plan, vals, dev)
     s = -0.7

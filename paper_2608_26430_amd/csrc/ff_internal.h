@@ -218,7 +218,7 @@ struct ff_plan {
   int gen_tile_tokens[2] = {0, 0};
   size_t gen_lds_bytes[2] = {0, 0};
   // bf16 generic kernels on token-grouped tiles (four tokens per coefficient; tiles a multiple of
-  // four tokens): frames applied directly with blocks up to 128 wide, one chunk, no lift.
+  // four tokens): frames applied directly (blocks up to 128 wide) or in one radix-4 stage, no lift.
   int gen_g4 = 0;
   int gen_wgs = 1;                 // compute units: resident workgroups of the generic kernels
   int gen_rows = 1;                // dC partial rows per adapter = most workgroups of the generic backward

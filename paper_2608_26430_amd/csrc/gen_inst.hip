@@ -55,8 +55,11 @@ hipError_t GEN_CONFIGURE_MS() {
 hipError_t GEN_LAUNCH(const GEN_ARGS& a, dim3 grid, size_t lds, hipStream_t s) {
   if (a.fin.nst >= 2 || a.fout.nst >= 2) return GEN_LAUNCH_MS(a, grid, lds, s);
 #if GEN_BF16
-  if (a.g4) {   // token-grouped tiles (the plan sets g4 only with one chunk and direct frames)
-    hipLaunchKernelGGL((GEN_KERNEL<true, false, false, true>), grid, dim3(kFusedThreads), lds, s, a);
+  if (a.g4) {   // token-grouped tiles (the plan sets g4 only for frames in at most one radix-4 stage)
+    if (a.nch > 1)
+      hipLaunchKernelGGL((GEN_KERNEL<true, true, false, true>), grid, dim3(kFusedThreads), lds, s, a);
+    else
+      hipLaunchKernelGGL((GEN_KERNEL<true, false, false, true>), grid, dim3(kFusedThreads), lds, s, a);
     return hipGetLastError();
   }
 #endif
@@ -72,7 +75,8 @@ hipError_t GEN_CONFIGURE() {
   for (const void* fn : {reinterpret_cast<const void*>(&GEN_KERNEL<GEN_BF16 != 0, true>),
                          reinterpret_cast<const void*>(&GEN_KERNEL<GEN_BF16 != 0, false>),
 #if GEN_BF16
-                         reinterpret_cast<const void*>(&GEN_KERNEL<true, false, false, true>)
+                         reinterpret_cast<const void*>(&GEN_KERNEL<true, false, false, true>),
+                         reinterpret_cast<const void*>(&GEN_KERNEL<true, true, false, true>)
 #else
                          reinterpret_cast<const void*>(&GEN_KERNEL<false, false>)
 #endif

@@ -275,6 +275,15 @@ __device__ __forceinline__ void column_apply(const FrameDev& f, bool synth, int 
 
 typedef short g4_i16x4 __attribute__((ext_vector_type(4)));
 
+// threadIdx.x, opaque to the optimizer: what a phase derives from it is computed in that phase
+// instead of being hoisted out of the backward's tile loop, where it would stay live (and, with
+// every phase's share together, spill) through all the other phases.
+__device__ __forceinline__ int phase_tid() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
 // Contraction elements 32 ks + 8 q .. + 7 of column L of a group from a token-grouped LDS tile,
 // by two transposed reads: within each 16 lanes the 8-byte chunks form 4 rows of 16 values and
 // lane L receives value L of each row.  For read h, lane L supplies element k0 + L / 4 (k0 =
@@ -300,18 +309,20 @@ __device__ __forceinline__ void g4_tile_operand(At at, int lim, int q, int L, bf
   }
 }
 
-// Every group g < ngrp (token group g / nsq, block quad g % nsq): SWAP (analysis, operands from
-// token rows in global memory: colg(tg, sq, L) is column L's row start, NULL outside the tile)
-// gives epi(tg, sq, mt, acc) tokens 0..3 of block 4 sq + q at coefficient 16 mt + L; otherwise
-// (synthesis, operands from the LDS tile through at(tg, sq, c4, k)) outputs 16 mt + 4 q .. + 3 of
-// column L.  The fragments stay in registers; each wave takes every nw-th group with the next
-// group's operands in flight.
-template <bool SWAP, int MT, int KT, class ColG, class At, class Epi>
+// Every group g < ngrp (token group g / nsq, quad of sub-columns g % nsq; a sub-column is a
+// block, or a (block, radix-4 column) of a factored frame): operands from token rows in global
+// memory (GSRC: colg(tg, sq, L) is column L's row start, NULL outside the tile) or from the LDS
+// tile through at(tg, sq, c4, k).  SWAP gives epi(tg, sq, mt, acc) tokens 0..3 of sub-column
+// 4 sq + q at output 16 mt + L (analysis, also in place: a group's operands are all read before
+// its outputs are written, and groups are disjoint); otherwise outputs 16 mt + 4 q .. + 3 of
+// column L (synthesis).  The fragments stay in registers; each wave takes every nw-th group with
+// the next group's operands in flight.
+template <bool GSRC, bool SWAP, int MT, int KT, class ColG, class At, class Epi>
 __device__ __forceinline__ void column_apply_g4(const void* frag, int ngrp, int nsq, int lim, ColG colg, At at,
                                                 Epi epi) {
   using M = Mfma<true>;
   using V = typename M::V;
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
+  const int lane = phase_tid() & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
             q = lane >> 4, L = lane & 15;
   if (wave >= ngrp) return;
   const V* fr = reinterpret_cast<const V*>(frag);
@@ -324,7 +335,7 @@ __device__ __forceinline__ void column_apply_g4(const void* frag, int ngrp, int 
   V ba[KT], bb[KT];
   auto load = [&](int g, V (&b)[KT]) {
     const int tg = g / nsq, sq = g - tg * nsq;
-    if constexpr (SWAP) {
+    if constexpr (GSRC) {
       const u16* in = colg(tg, sq, L);
       const bool ok = in != nullptr;
 #pragma unroll
@@ -356,18 +367,20 @@ __device__ __forceinline__ void column_apply_g4(const void* frag, int ngrp, int 
   }
 }
 
-template <bool SWAP, class ColG, class At, class Epi>
-__device__ __forceinline__ void column_apply_g4(const FrameDev& f, bool synth, int ngrp, int nsq, ColG colg, At at,
-                                                Epi epi) {
+// Dispatch on the matrix shape (MT x KT tiles of M, whose columns have lim elements: W for a
+// directly applied block, cs for the DFT of size k/4 of a factored one).
+template <bool GSRC, bool SWAP, class ColG, class At, class Epi>
+__device__ __forceinline__ void column_apply_g4(const FrameDev& f, bool synth, int ngrp, int nsq, int lim, ColG colg,
+                                                At at, Epi epi) {
   const void* frag = synth ? f.fs16 : f.fa16;
 #define FF_SHAPE(mt, kt)                                                           \
   case (mt) * 64 + (kt):                                                           \
-    column_apply_g4<SWAP, mt, kt>(frag, ngrp, nsq, f.W, colg, at, epi);            \
+    column_apply_g4<GSRC, SWAP, mt, kt>(frag, ngrp, nsq, lim, colg, at, epi);      \
     return;
   switch (f.MT * 64 + f.KT) {
     FF_SHAPE(1, 1) FF_SHAPE(2, 1) FF_SHAPE(3, 2) FF_SHAPE(4, 2) FF_SHAPE(5, 3) FF_SHAPE(6, 3)
     FF_SHAPE(7, 4) FF_SHAPE(8, 4)
-    default: break;   // not taken: the plan uses these tiles only for blocks up to 128 wide
+    default: break;   // not taken: the plan uses these tiles only for matrices up to 128 wide
   }
 #undef FF_SHAPE
 }
@@ -719,12 +732,216 @@ __device__ __forceinline__ void msr_synthesis(const FrameDev& f, int nt, const t
   }
 }
 
+// z = P^T x for a tile into a token-grouped LDS tile (frames applied directly): every token slot
+// of the tile's groups is written, those past nt with zeros.
+__device__ __forceinline__ void analysis_g4(const FrameDev& f, int nt, const u16* src, long ld, u16* dst, int ldt,
+                                            int ldb) {
+  const int nblk = f.nblk, W = f.W, nsq = (nblk + 3) / 4, ngrp = (nt + 3) / 4 * nsq;
+  const int lane = phase_tid() & 63, q = lane >> 4, L = lane & 15;
+  column_apply_g4<true, true>(
+      f, false, ngrp, nsq, W,
+      [&](int tg, int sq, int c) -> const u16* {
+        const int t = 4 * tg + (c & 3), b = 4 * sq + (c >> 2);
+        return t < nt && b < nblk ? src + (long)t * ld + b * W : nullptr;
+      },
+      [&](int, int, int, int) -> const u16* { return dst; },
+      [&](int tg, int sq, int mt, f32x4 v) {
+        const int b = 4 * sq + q, o = 16 * mt + L;
+        if (b < nblk && o < W) Act<true>::st4(dst + 4 * (tg * ldt + b * ldb + o), v);
+      });
+}
+
+// out = s P v (+ beta out) for a tile from a token-grouped LDS tile (frames applied directly).
+__device__ __forceinline__ void synthesis_g4(const FrameDev& f, int nt, const u16* src, int ldt, int ldb, u16* dst,
+                                             long ld, float s, float beta) {
+  const int nblk = f.nblk, W = f.W, nsq = (nblk + 3) / 4, ngrp = (nt + 3) / 4 * nsq;
+  const int lane = phase_tid() & 63, q = lane >> 4, L = lane & 15;
+  column_apply_g4<false, false>(
+      f, true, ngrp, nsq, W, [&](int, int, int) -> const u16* { return src; },
+      [&](int tg, int sq, int c4, int k) -> const u16* {
+        const int b = min(4 * sq + c4, nblk - 1);
+        return src + 4 * (tg * ldt + b * ldb + k);
+      },
+      [&](int tg, int sq, int mt, f32x4 v) {
+        const int t = 4 * tg + (L & 3), b = 4 * sq + (L >> 2), o = 16 * mt + 4 * q;
+        if (t < nt && b < nblk && o < W) {
+          u16* p = dst + (long)t * ld + b * W + o;
+          f32x4 r = v * s;
+          if (beta != 0.f) r += beta * Act<true>::gld4(p);
+          Act<true>::gst4(p, r);
+        }
+      });
+}
+
+// Radix-4 stage of the factored analysis on a token-grouped tile (single-stage frames): an item is
+// (token group, block, residue b < k2); it reads x[a k2 + b] (a = 0..3) of its four tokens from
+// the token rows (tokens past nt as zero) and writes the real and the imaginary parts of column
+// a' row b, four tokens per 8-byte write.  The columns' padding rows W2 .. cs - 1 are never
+// written: the DFT of size k/4 reads its operands only below W2.
+constexpr int kRB4 = 2;   // items per thread in flight (16 complex loads each)
+
+__device__ __forceinline__ void radix4_analysis_g4(const FrameDev& f, const float2* tw, int nt, const u16* src,
+                                                   long ld, u16* dst, int ldt, int ldb) {
+  const int k2 = f.k2, W = f.W, cs = f.cs;
+  const int per_tg = f.nblk * k2, items = (nt + 3) / 4 * per_tg;
+  const float inv_pt = 1.f / (float)per_tg, inv_k2 = 1.f / (float)k2;
+  for (int it0 = phase_tid(); it0 < items; it0 += kRB4 * blockDim.x) {
+    float2 x[kRB4][4][4], w[kRB4][3];   // [item][token][a]
+    u16* y[kRB4];
+#pragma unroll
+    for (int u = 0; u < kRB4; ++u) {
+      const int it = min(it0 + u * (int)blockDim.x, items - 1);   // past the end: a repeat, not stored
+      const int tg = div_small(it, per_tg, inv_pt), r = it - tg * per_tg, blk = div_small(r, k2, inv_k2);
+      const int b = r - blk * k2;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {   // rows past nt: the last token's, read unconditionally and dropped
+        const int t = 4 * tg + i;
+        const u16* xp = src + (long)min(t, nt - 1) * ld + blk * W + 2 * b;
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const float2 v = gld2<true>(xp + 2 * a * k2);
+          x[u][i][a] = t < nt ? v : make_float2(0.f, 0.f);
+        }
+      }
+#pragma unroll
+      for (int a = 0; a < 3; ++a) w[u][a] = tw[a * k2 + b];
+      y[u] = dst + 4 * (tg * ldt + blk * ldb + 2 * b);
+    }
+#pragma unroll
+    for (int u = 0; u < kRB4; ++u) {
+      if (it0 + u * (int)blockDim.x >= items) break;
+      f32x4 yr[4], yi[4];   // [a'] over the four tokens
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float2* xi = x[u][i];
+        const float2 s02 = cadd(xi[0], xi[2]), d02 = csub(xi[0], xi[2]);
+        const float2 s13 = cadd(xi[1], xi[3]), d13 = csub(xi[1], xi[3]);
+        const float2 o[4] = {cadd(s02, s13), cmulc(make_float2(d02.x + d13.y, d02.y - d13.x), w[u][0]),
+                             cmulc(csub(s02, s13), w[u][1]), cmulc(make_float2(d02.x - d13.y, d02.y + d13.x), w[u][2])};
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          yr[a][i] = o[a].x;
+          yi[a][i] = o[a].y;
+        }
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {   // the real and imaginary rows are adjacent: one 16-byte write
+        const uint2 r = Act<true>::pack4(yr[a]), i = Act<true>::pack4(yi[a]);
+        *reinterpret_cast<uint4*>(y[u] + 4 * a * cs) = make_uint4(r.x, r.y, i.x, i.y);
+      }
+    }
+  }
+}
+
+// Radix-4 stage of the factored synthesis from a token-grouped tile: an item reads the four tokens
+// of column a' row b (real and imaginary parts, one 8-byte read each) and writes out = s x
+// (+ beta out) for those of its tokens below nt.
+__device__ __forceinline__ void radix4_synthesis_g4(const FrameDev& f, const float2* tw, int nt, const u16* src,
+                                                    int ldt, int ldb, u16* dst, long ld, float s, float beta) {
+  const int k2 = f.k2, W = f.W, cs = f.cs;
+  const int per_tg = f.nblk * k2, items = (nt + 3) / 4 * per_tg;
+  const float inv_pt = 1.f / (float)per_tg, inv_k2 = 1.f / (float)k2;
+  for (int it0 = phase_tid(); it0 < items; it0 += kRB4 * blockDim.x) {
+    f32x4 yr[kRB4][4], yi[kRB4][4];
+    float2 w[kRB4][3];
+    int tg[kRB4], blk[kRB4], b[kRB4];
+#pragma unroll
+    for (int u = 0; u < kRB4; ++u) {
+      const int it = min(it0 + u * (int)blockDim.x, items - 1);
+      tg[u] = div_small(it, per_tg, inv_pt);
+      const int r = it - tg[u] * per_tg;
+      blk[u] = div_small(r, k2, inv_k2);
+      b[u] = r - blk[u] * k2;
+      const u16* yp = src + 4 * (tg[u] * ldt + blk[u] * ldb + 2 * b[u]);
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {   // the real and imaginary rows: one 16-byte read
+        const uint4 w = *reinterpret_cast<const uint4*>(yp + 4 * a * cs);
+        yr[u][a] = Act<true>::unpack4(make_uint2(w.x, w.y));
+        yi[u][a] = Act<true>::unpack4(make_uint2(w.z, w.w));
+      }
+#pragma unroll
+      for (int a = 0; a < 3; ++a) w[u][a] = tw[a * k2 + b[u]];
+    }
+#pragma unroll
+    for (int u = 0; u < kRB4; ++u) {
+      if (it0 + u * (int)blockDim.x >= items) break;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = 4 * tg[u] + i;
+        if (t >= nt) break;
+        const float2 y0 = make_float2(yr[u][0][i], yi[u][0][i]);
+        const float2 y1 = cmul(make_float2(yr[u][1][i], yi[u][1][i]), w[u][0]);
+        const float2 y2 = cmul(make_float2(yr[u][2][i], yi[u][2][i]), w[u][1]);
+        const float2 y3 = cmul(make_float2(yr[u][3][i], yi[u][3][i]), w[u][2]);
+        const float2 s02 = cadd(y0, y2), d02 = csub(y0, y2), s13 = cadd(y1, y3), d13 = csub(y1, y3);
+        const float2 xo[4] = {cadd(s02, s13), make_float2(d02.x - d13.y, d02.y + d13.x), csub(s02, s13),
+                              make_float2(d02.x + d13.y, d02.y - d13.x)};
+        u16* out = dst + (long)t * ld + blk[u] * W + 2 * b[u];
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          float2 v = make_float2(s * xo[a].x, s * xo[a].y);
+          if (beta != 0.f) {
+            const float2 old = gld2<true>(out + 2 * a * k2);
+            v.x = fmaf(beta, old.x, v.x);
+            v.y = fmaf(beta, old.y, v.y);
+          }
+          gst2<true>(out + 2 * a * k2, v);
+        }
+      }
+    }
+  }
+}
+
+// The dense DFT of size k/4 applied in place to every (token group, block, radix-4 column) of a
+// factored token-grouped tile (single-stage frames: four columns per block), M^T for analysis and
+// M for synthesis.  Operands are read below W2 only; outputs up to cs are written (M's rows past
+// W2 are zero, so the padding rows receive zeros).
+__device__ __forceinline__ void factored_dft_g4(const FrameDev& f, bool synth, int nt, u16* tile, int ldt, int ldb) {
+  const int cs = f.cs, nsub = 4 * f.nblk, nsq = f.nblk, ngrp = (nt + 3) / 4 * nsq;
+  const int lane = phase_tid() & 63, q = lane >> 4, L = lane & 15;
+  column_apply_g4<false, true>(
+      f, synth, ngrp, nsq, f.W2, [&](int, int, int) -> const u16* { return tile; },
+      [&](int tg, int sq, int c4, int k) -> const u16* {
+        const int sub = min(4 * sq + c4, nsub - 1);
+        return tile + 4 * (tg * ldt + (sub >> 2) * ldb + (sub & 3) * cs + k);
+      },
+      [&](int tg, int sq, int mt, f32x4 v) {
+        const int sub = 4 * sq + q, o = 16 * mt + L;
+        if (o < cs) Act<true>::st4(tile + 4 * (tg * ldt + (sub >> 2) * ldb + (sub & 3) * cs + o), v);
+      });
+}
+
+// z = P^T x into a token-grouped tile: the block directly, or the radix-4 stage and then the DFT
+// of size k/4 in place.
+__device__ __forceinline__ void analysis_lds_g4(const FrameDev& f, const float2* tw, int nt, const u16* src, long ld,
+                                                u16* dst, int ldt, int ldb) {
+  if (f.radix == 1) {
+    analysis_g4(f, nt, src, ld, dst, ldt, ldb);
+    return;
+  }
+  radix4_analysis_g4(f, tw, nt, src, ld, dst, ldt, ldb);
+  __syncthreads();
+  factored_dft_g4(f, false, nt, dst, ldt, ldb);
+}
+
+// out = s P v (+ beta out) from a token-grouped tile (factored frames transform it in place first).
+__device__ __forceinline__ void synthesis_lds_g4(const FrameDev& f, const float2* tw, int nt, u16* src, int ldt,
+                                                 int ldb, u16* dst, long ld, float s, float beta) {
+  if (f.radix == 1) {
+    synthesis_g4(f, nt, src, ldt, ldb, dst, ld, s, beta);
+    return;
+  }
+  factored_dft_g4(f, true, nt, src, ldt, ldb);
+  __syncthreads();
+  radix4_synthesis_g4(f, tw, nt, src, ldt, ldb, dst, ld, s, beta);
+}
+
 // Zero the padding of every column of a factored tile whose coefficients another phase writes
-// (the MFMA reads whole columns of cs elements).
-template <bool BF16>
+// (the MFMA reads whole columns of cs elements).  Token-grouped tiles (G4) need none.
+template <bool BF16, bool G4 = false>
 __device__ __forceinline__ void zero_column_pads(const FrameDev& f, int nt, typename Act<BF16>::E* tile, int ldt,
                                                  int ldb) {
-  if (f.radix == 1 || f.cs == f.W2) return;
+  if (G4 || f.radix == 1 || f.cs == f.W2) return;
   const int padw = f.cs - f.W2, per_tok = f.nblk * f.ncol * padw, items = nt * per_tok;
   for (int it = threadIdx.x; it < items; it += blockDim.x) {
     const int t = it / per_tok, r = it - t * per_tok, col = r / padw, e = r - col * padw;
@@ -736,12 +953,18 @@ __device__ __forceinline__ void zero_column_pads(const FrameDev& f, int nt, type
 // z = P^T x for a tile: token rows at src (global) -> coefficients in the LDS tile.
 // MS: the frame may be applied in several radix-4 stages (nst >= 2); only the kernels built for
 // such frames carry that code, so the others keep their register allocation.
-template <bool BF16, bool MS = false>
+// G4: into a token-grouped tile.
+template <bool BF16, bool MS = false, bool G4 = false>
 __device__ __forceinline__ void analysis_to_lds(const FrameDev& f, const float2* tw, int nt,
                                                 const typename Act<BF16>::E* src, long ld, typename Act<BF16>::E* dst,
                                                 int ldt, int ldb) {
   using A = Act<BF16>;
   using E = typename A::E;
+  if constexpr (G4) {
+    static_assert(BF16 && !MS, "token-grouped tiles: bf16, frames in at most one radix-4 stage");
+    analysis_lds_g4(f, tw, nt, src, ld, dst, ldt, ldb);
+    return;
+  }
   const int nblk = f.nblk;
   if (f.radix == 1) {
     const int W = f.W;
@@ -782,12 +1005,18 @@ __device__ __forceinline__ void analysis_to_lds(const FrameDev& f, const float2*
 
 // out = s P q (+ beta out) for a tile: coefficients in the LDS tile at src -> token rows at dst.
 // Factored frames transform the tile in place first, so src is overwritten.
-template <bool BF16, bool MS = false>
+// G4: from a token-grouped tile.
+template <bool BF16, bool MS = false, bool G4 = false>
 __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const float2* tw, int nt,
                                                    typename Act<BF16>::E* src, int ldt, int ldb,
                                                    typename Act<BF16>::E* dst, long ld, float s, float beta) {
   using A = Act<BF16>;
   using E = typename A::E;
+  if constexpr (G4) {
+    static_assert(BF16 && !MS, "token-grouped tiles: bf16, frames in at most one radix-4 stage");
+    synthesis_lds_g4(f, tw, nt, src, ldt, ldb, dst, ld, s, beta);
+    return;
+  }
   const int nblk = f.nblk;
   if (f.radix == 1) {
     const int W = f.W;
@@ -827,47 +1056,6 @@ __device__ __forceinline__ void synthesis_from_lds(const FrameDev& f, const floa
     else
       msr_synthesis<BF16, 3>(f, nt, src, ldt, ldb, dst, ld, s, beta);
   }
-}
-
-// z = P^T x for a tile into a token-grouped LDS tile (frames applied directly): every token slot
-// of the tile's groups is written, those past nt with zeros.
-__device__ __forceinline__ void analysis_g4(const FrameDev& f, int nt, const u16* src, long ld, u16* dst, int ldt,
-                                            int ldb) {
-  const int nblk = f.nblk, W = f.W, nsq = (nblk + 3) / 4, ngrp = (nt + 3) / 4 * nsq;
-  const int lane = threadIdx.x & 63, q = lane >> 4, L = lane & 15;
-  column_apply_g4<true>(
-      f, false, ngrp, nsq,
-      [&](int tg, int sq, int c) -> const u16* {
-        const int t = 4 * tg + (c & 3), b = 4 * sq + (c >> 2);
-        return t < nt && b < nblk ? src + (long)t * ld + b * W : nullptr;
-      },
-      [&](int, int, int, int) -> const u16* { return dst; },
-      [&](int tg, int sq, int mt, f32x4 v) {
-        const int b = 4 * sq + q, o = 16 * mt + L;
-        if (b < nblk && o < W) Act<true>::st4(dst + 4 * (tg * ldt + b * ldb + o), v);
-      });
-}
-
-// out = s P v (+ beta out) for a tile from a token-grouped LDS tile (frames applied directly).
-__device__ __forceinline__ void synthesis_g4(const FrameDev& f, int nt, const u16* src, int ldt, int ldb, u16* dst,
-                                             long ld, float s, float beta) {
-  const int nblk = f.nblk, W = f.W, nsq = (nblk + 3) / 4, ngrp = (nt + 3) / 4 * nsq;
-  const int lane = threadIdx.x & 63, q = lane >> 4, L = lane & 15;
-  column_apply_g4<false>(
-      f, true, ngrp, nsq, [&](int, int, int) -> const u16* { return src; },
-      [&](int tg, int sq, int c4, int k) -> const u16* {
-        const int b = min(4 * sq + c4, nblk - 1);
-        return src + 4 * (tg * ldt + b * ldb + k);
-      },
-      [&](int tg, int sq, int mt, f32x4 v) {
-        const int t = 4 * tg + (L & 3), b = 4 * sq + (L >> 2), o = 16 * mt + 4 * q;
-        if (t < nt && b < nblk && o < W) {
-          u16* p = dst + (long)t * ld + b * W + o;
-          f32x4 r = v * s;
-          if (beta != 0.f) r += beta * Act<true>::gld4(p);
-          Act<true>::gst4(p, r);
-        }
-      });
 }
 
 // Sparse products over a generic stream (GenStream).  Each wave walks its run of stream rows
@@ -1005,31 +1193,6 @@ __device__ __forceinline__ void stream_pass(const GenStream& S, const float* __r
   }
 }
 
-// All tokens of a tile, kTGWide at a time while that many remain, then kTG, each pass reading
-// only as many token rows as it needs.
-// `add` (MAY_ADD only): backward, add to the dC partial row (as do the tile's later passes);
-// forward, add the sums to the destination (the input side's later chunks).
-template <bool BF16, bool BWD, bool MAY_ADD = BWD>
-__device__ __forceinline__ void stream_all(const GenStream& S, const float* __restrict__ cv,
-                                           const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
-                                           int ld_dst, int nt, bool write_dst, float* part, bool add = false) {
-  for (int tg = 0; tg < nt;) {
-    const int ntg = nt - tg >= kTGWide ? kTGWide : min(kTG, nt - tg);
-    const bool add_now = MAY_ADD && (add || (BWD && tg > 0));
-    if (ntg == kTGWide) {
-      if (add_now)
-        stream_products<BF16, BWD, MAY_ADD, kTGWide>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-      else
-        stream_products<BF16, BWD, false, kTGWide>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    } else if (add_now) {
-      stream_pass<BF16, BWD, MAY_ADD>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    } else {
-      stream_pass<BF16, BWD, false>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
-    }
-    tg += ntg;
-  }
-}
-
 // The sparse products on token-grouped tiles: the same walk, each table row reading NG groups of
 // four tokens (one 8-byte LDS read each) for the pass's tokens tg0 .. tg0 + 4 NG - 1 (tg0 a
 // multiple of 4) and writing whole groups at a slab's end.  Token slots past ntg hold zeros in the
@@ -1040,7 +1203,7 @@ __device__ __forceinline__ void stream_products_g4(const GenStream& S, const flo
                                                    bool write_dst, float* part) {
   using A = Act<true>;
   constexpr int NT = 4 * NG;
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = phase_tid() & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r0 = S.wave_row[wave], r1 = S.wave_row[wave + 1];
   if (r0 >= r1) return;
   const int2* ent = (S.ent);
@@ -1140,17 +1303,49 @@ __device__ __forceinline__ void stream_pass_g4(const GenStream& S, const float* 
   }
 }
 
-// All tokens of a token-grouped tile, 16 at a time, the last pass reading only the groups it needs.
-template <bool BWD>
+// All tokens of a token-grouped tile, 16 at a time, the last pass reading only the groups it
+// needs; `add` as for stream_all.
+template <bool BWD, bool MAY_ADD>
 __device__ __forceinline__ void stream_all_g4(const GenStream& S, const float* __restrict__ cv, const u16* src,
                                               int ld_src, u16* dst, int ld_dst, int nt, bool write_dst, float* part,
-                                              bool add = false) {
+                                              bool add) {
   for (int tg = 0; tg < nt; tg += 16) {
     const int ntg = min(16, nt - tg);
-    if (BWD && (add || tg > 0))
-      stream_pass_g4<BWD, BWD>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    if (MAY_ADD && (add || (BWD && tg > 0)))
+      stream_pass_g4<BWD, MAY_ADD>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
     else
       stream_pass_g4<BWD, false>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+  }
+}
+
+// All tokens of a tile, kTGWide at a time while that many remain, then kTG, each pass reading
+// only as many token rows as it needs.
+// `add` (MAY_ADD only): backward, add to the dC partial row (as do the tile's later passes);
+// forward, add the sums to the destination (the input side's later chunks).
+// G4: on token-grouped tiles.
+template <bool BF16, bool BWD, bool MAY_ADD = BWD, bool G4 = false>
+__device__ __forceinline__ void stream_all(const GenStream& S, const float* __restrict__ cv,
+                                           const typename Act<BF16>::E* src, int ld_src, typename Act<BF16>::E* dst,
+                                           int ld_dst, int nt, bool write_dst, float* part, bool add = false) {
+  if constexpr (G4) {
+    static_assert(BF16, "token-grouped tiles hold bf16");
+    stream_all_g4<BWD, MAY_ADD>(S, cv, src, ld_src, dst, ld_dst, nt, write_dst, part, add);
+    return;
+  }
+  for (int tg = 0; tg < nt;) {
+    const int ntg = nt - tg >= kTGWide ? kTGWide : min(kTG, nt - tg);
+    const bool add_now = MAY_ADD && (add || (BWD && tg > 0));
+    if (ntg == kTGWide) {
+      if (add_now)
+        stream_products<BF16, BWD, MAY_ADD, kTGWide>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+      else
+        stream_products<BF16, BWD, false, kTGWide>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    } else if (add_now) {
+      stream_pass<BF16, BWD, MAY_ADD>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    } else {
+      stream_pass<BF16, BWD, false>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    }
+    tg += ntg;
   }
 }
 
@@ -1211,16 +1406,6 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   X += (long)t0 * a.ldx;
   Y += (long)t0 * a.ldy;
 
-  if constexpr (G4) {
-    static_assert(BF16 && !CHUNKED && !MS, "token-grouped tiles: bf16, whole input side, direct frames");
-    analysis_g4(a.fin, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
-    __syncthreads();
-    stream_all_g4<false>(st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
-    __syncthreads();
-    synthesis_g4(a.fout, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, a.scale, a.beta);
-    return;
-  }
-
   // twiddle factors of factored frames after the tiles
   float2* tw_in = reinterpret_cast<float2*>(vt + (size_t)cap * a.ldt_out);
   float2* tw_out = tw_in + kTwLdsBytes / 16;
@@ -1228,14 +1413,14 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
   stage_twiddles(a.fout, tw_out);
   if (a.fin.radix != 1 || a.fout.radix != 1) __syncthreads();
 
-  zero_column_pads<BF16>(a.fout, nt, vt, a.ldt_out, a.ldb_out);
+  zero_column_pads<BF16, G4>(a.fout, nt, vt, a.ldt_out, a.ldb_out);
   if constexpr (!CHUNKED) {
     // analysis: z = P_in^T x for every (token, input block)
-    analysis_to_lds<BF16, MS>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
+    analysis_to_lds<BF16, MS, G4>(a.fin, tw_in, nt, X, a.ldx, zt, a.ldt_in, a.ldb_in);
     __syncthreads();
 
     // coefficients: v[a] = sum_{e in row a} c_e z[b_e]
-    stream_all<BF16, false>(st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
+    stream_all<BF16, false, false, G4>(st, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr);
   } else {
     for (int ch = 0; ch < a.nch; ++ch) {
       // the chunk's blocks as a frame of their own, at column b0 W of the token rows
@@ -1243,19 +1428,19 @@ __global__ void __launch_bounds__(kFusedThreads) fwd_kernel(FwdArgs a) {
       FrameDev fc = a.fin;
       fc.nblk = a.chunk_blk[ch + 1] - b0;
       if (ch > 0) __syncthreads();   // the previous chunk's products are done reading z
-      analysis_to_lds<BF16, MS>(fc, tw_in, nt, X + (long)b0 * a.fin.W, a.ldx, zt, a.ldt_in, a.ldb_in);
+      analysis_to_lds<BF16, MS, G4>(fc, tw_in, nt, X + (long)b0 * a.fin.W, a.ldx, zt, a.ldt_in, a.ldb_in);
       __syncthreads();
 
       // v[a] (+)= sum over the chunk's entries of row a of c_e z[b_e]
       GenStream sc = st;
       sc.wave_row += ch * (kGenWaves + 1);
-      stream_all<BF16, false, true>(sc, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr, ch > 0);
+      stream_all<BF16, false, true, G4>(sc, cv, zt, a.ldt_in, vt, a.ldt_out, nt, true, nullptr, ch > 0);
     }
   }
   __syncthreads();
 
   // synthesis and epilogue: y = beta y + s P_out v
-  synthesis_from_lds<BF16, MS>(a.fout, tw_out, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, a.scale, a.beta);
+  synthesis_from_lds<BF16, MS, G4>(a.fout, tw_out, nt, vt, a.ldt_out, a.ldb_out, Y, a.ldy, a.scale, a.beta);
 }
 
 struct BwdArgs {
@@ -1328,34 +1513,23 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
     const int nt = (int)min((long)a.tt, (long)Tb - t0);
     if (tile != blockIdx.x) __syncthreads();   // the previous tile's LDS reads are done
 
-    if constexpr (G4) {
-      static_assert(BF16 && !CHUNKED && !MS, "token-grouped tiles: bf16, whole input side, direct frames");
-      analysis_g4(a.fout, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
-      if (a.want_dc) analysis_g4(a.fin, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
-      __syncthreads();
-      stream_all_g4<true>(st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
-      if (!a.want_dx) continue;
-      __syncthreads();
-      synthesis_g4(a.fin, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale, a.beta);
-      continue;
-    }
     if constexpr (!CHUNKED) {
       // q is written over z and then synthesized from whole columns: their padding must be zero
-      zero_column_pads<BF16>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
-      analysis_to_lds<BF16, MS>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
-      if (a.want_dc) analysis_to_lds<BF16, MS>(a.fin, tw_in, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
+      zero_column_pads<BF16, G4>(a.fin, nt, zt, a.ldt_in, a.ldb_in);
+      analysis_to_lds<BF16, MS, G4>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
+      if (a.want_dc) analysis_to_lds<BF16, MS, G4>(a.fin, tw_in, nt, X0 + t0 * a.ldx, a.ldx, zt, a.ldt_in, a.ldb_in);
       __syncthreads();
 
       // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
-      stream_all<BF16, true>(st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
+      stream_all<BF16, true, true, G4>(st, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
       if (!a.want_dx) continue;
       __syncthreads();
 
-      synthesis_from_lds<BF16, MS>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale,
+      synthesis_from_lds<BF16, MS, G4>(a.fin, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx, a.lddx, a.scale,
                                a.beta);
       continue;
     }
-    analysis_to_lds<BF16, MS>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
+    analysis_to_lds<BF16, MS, G4>(a.fout, tw_out, nt, G0 + t0 * a.ldg, a.ldg, ut, a.ldt_out, a.ldb_out);
     for (int ch = 0; ch < a.nch; ++ch) {
       // the chunk's blocks as a frame of their own, at column b0 W of the token rows
       const int b0 = a.chunk_blk[ch];
@@ -1364,18 +1538,18 @@ __global__ void __launch_bounds__(kFusedThreads) bwd_kernel(BwdArgs a) {
       const long col0 = (long)b0 * a.fin.W;
       if (ch > 0) __syncthreads();   // the previous chunk is done with the z / q tile
       // q is written over z and then synthesized from whole columns: their padding must be zero
-      zero_column_pads<BF16>(fc, nt, zt, a.ldt_in, a.ldb_in);
-      if (a.want_dc) analysis_to_lds<BF16, MS>(fc, tw_in, nt, X0 + t0 * a.ldx + col0, a.ldx, zt, a.ldt_in, a.ldb_in);
+      zero_column_pads<BF16, G4>(fc, nt, zt, a.ldt_in, a.ldb_in);
+      if (a.want_dc) analysis_to_lds<BF16, MS, G4>(fc, tw_in, nt, X0 + t0 * a.ldx + col0, a.ldx, zt, a.ldt_in, a.ldb_in);
       __syncthreads();
 
       // q[b] = sum_{e in column b} c_e u[a_e] (written over z) and this tile's dC partial sums
       GenStream sc = st;
       sc.wave_row += ch * (kGenWaves + 1);
-      stream_all<BF16, true>(sc, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
+      stream_all<BF16, true, true, G4>(sc, cv, ut, a.ldt_out, zt, a.ldt_in, nt, a.want_dx, part, tile != blockIdx.x);
       if (!a.want_dx) continue;
       __syncthreads();
 
-      synthesis_from_lds<BF16, MS>(fc, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx + col0, a.lddx, a.scale,
+      synthesis_from_lds<BF16, MS, G4>(fc, tw_in, nt, zt, a.ldt_in, a.ldb_in, dX0 + t0 * a.lddx + col0, a.lddx, a.scale,
                                a.beta);
     }
   }

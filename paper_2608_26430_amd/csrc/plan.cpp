@@ -347,10 +347,12 @@ extern "C" ff_status ff_plan_create(const ff_frame* f_in, const ff_frame* f_out,
     p->gen_nch = nch;
     for (int c = 0; c <= nch; ++c) p->gen_chunk_blk[c] = (int)((int64_t)c * FI.nblk / nch);
     // bf16 token-grouped tiles (gen_kernels.h): every table row of the sparse phases reads four
-    // tokens per LDS access; they need whole groups of four tokens and the dense block apply
-    const bool direct = FI.radix == 1 && FO.radix == 1 && FI.nst == 0 && FO.nst == 0 && FI.W <= 128 &&
-                        FO.W <= 128;
-    p->gen_g4 = direct && nch == 1 && !f_in->lifted && !f_out->lifted && chunk_tokens(nch, FF_BF16) >= 4;
+    // tokens per LDS access; they need whole groups of four tokens, and frames whose blocks are
+    // applied directly (up to 128 wide) or in one radix-4 stage
+    auto grouped_ok = [](const ff::FrameDev& f) {
+      return (f.radix == 1 && f.nst == 0 && f.W <= 128) || (f.radix == 4 && f.nst == 1 && f.W2 <= 128);
+    };
+    p->gen_g4 = grouped_ok(FI) && grouped_ok(FO) && !f_in->lifted && !f_out->lifted && chunk_tokens(nch, FF_BF16) >= 4;
     for (int dt = 0; dt < 2; ++dt) {
       const int esz = dt == FF_BF16 ? 2 : 4;
       p->gen_ldt_in[dt] = token_stride((FI.nblk + nch - 1) / nch, p->ldb_in, esz);

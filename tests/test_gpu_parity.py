@@ -63,6 +63,9 @@ SHAPES = [
     # tokens than a tile, and a single token
     (8192, 64, 2048, 64, 42000, 5),
     (8192, 64, 2048, 64, 42000, 1),
+    # an output side too wide for four tokens per tile (factored 448-wide blocks): bf16 tiles stay
+    # token-major
+    (256, 16, 28672, 128, 5000, 7),
 ]
 
 
@@ -111,11 +114,13 @@ def test_small_parity(dev, shape, dtype):
     assert plan.radix == (4 if 2 * k_in > 128 else 1, 4 if 2 * k_out > 128 else 1)
     # the generic kernels chunk the input side only for the wide, dense-support shapes
     assert (plan.gen_chunks > 1) == (n == 8192)
-    # bf16 tiles keep four tokens per coefficient together where both blocks are applied directly
-    # (whole multiples of four tokens per tile)
-    assert plan.gen_token_groups == (plan.radix == (1, 1) and plan.gen_chunks == 1)
+    # bf16 tiles keep four tokens per coefficient together (whole multiples of four tokens per
+    # tile) unless not even four tokens fit
+    assert plan.gen_token_groups == (m != 28672)
     if plan.gen_token_groups:
         assert plan.gen_tile_tokens("bf16") % 4 == 0 and plan.gen_tile_tokens("bf16") >= 4
+    else:
+        assert plan.gen_tile_tokens("bf16") < 4
     pad = 8 if dtype == "bf16" else 4
     xbuf, Xd = guarded(T, n, n + pad, dtype, dev, X)
     gbuf, Gd = guarded(T, m, m + 2 * pad, dtype, dev, G)
@@ -273,7 +278,7 @@ def test_generic_backward_many_tiles_per_workgroup(dev, dtype, shape):
     G = inputs.gaussian(g, (T, m), dtype=dtype)
     plan = ff.plan_create(f_in, f_out, rows, cols, max_tokens=T)
     assert plan.radix == ((4, 1) if n == 2752 else (1, 1)) and not plan.fast128
-    assert plan.gen_token_groups == (n == 768)
+    assert plan.gen_token_groups
     Xd, Gd = torch_act(X, dtype, dev), torch_act(G, dtype, dev)
     c = plan_c(plan, vals, dev)
     s = -0.7

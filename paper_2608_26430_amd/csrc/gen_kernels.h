@@ -91,6 +91,15 @@ struct Act<false> {
 // lane l holds column l % 16 and contraction elements 8 (l / 16) .. +7 of each step (4 for fp32).
 // Inputs at or past `lim` (the column's storage length) are taken as zero; M is zero there too.
 
+// threadIdx.x, opaque to the optimizer: what a phase derives from it is computed in that phase
+// instead of being hoisted out of the backward's tile loop, where it would stay live (and, with
+// every phase's share together, spill) through all the other phases.
+__device__ __forceinline__ int phase_tid() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
 template <bool BF16>
 struct Mfma;
 
@@ -135,7 +144,7 @@ template <bool BF16, bool GSRC, int MT, int KT, class Col, class Epi>
 __device__ __forceinline__ void column_apply_reg(const void* frag, int ncols, int lim, Col col, Epi epi) {
   using M = Mfma<BF16>;
   using V = typename M::V;
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
+  const int lane = phase_tid() & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
             q = lane >> 4;
   const int ngrp = (ncols + 15) / 16;
   if (wave >= ngrp) return;
@@ -192,7 +201,7 @@ __device__ __forceinline__ void column_apply_mem(const void* frag, int MT, int K
   using M = Mfma<BF16>;
   using V = typename M::V;
   constexpr int kC = 4, kPre = 8;
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
+  const int lane = phase_tid() & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), nw = blockDim.x >> 6,
             q = lane >> 4;
   const int ngrp = (ncols + 15) / 16;
   const V* fr = reinterpret_cast<const V*>(frag);
@@ -275,14 +284,6 @@ __device__ __forceinline__ void column_apply(const FrameDev& f, bool synth, int 
 
 typedef short g4_i16x4 __attribute__((ext_vector_type(4)));
 
-// threadIdx.x, opaque to the optimizer: what a phase derives from it is computed in that phase
-// instead of being hoisted out of the backward's tile loop, where it would stay live (and, with
-// every phase's share together, spill) through all the other phases.
-__device__ __forceinline__ int phase_tid() {
-  int t = threadIdx.x;
-  asm volatile("" : "+v"(t));
-  return t;
-}
 
 // Contraction elements 32 ks + 8 q .. + 7 of column L of a group from a token-grouped LDS tile,
 // by two transposed reads: within each 16 lanes the 8-byte chunks form 4 rows of 16 values and
@@ -458,7 +459,7 @@ __device__ __forceinline__ void radix4_analysis(const FrameDev& f, const float2*
   const int k2 = f.k2, W = f.W, cs = f.cs, W2 = f.W2;
   const int per_tok = f.nblk * k2, items = nt * per_tok;
   const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
-  for (int it0 = threadIdx.x; it0 < items; it0 += kRB * blockDim.x) {
+  for (int it0 = phase_tid(); it0 < items; it0 += kRB * blockDim.x) {
     float2 x[kRB][4], w[kRB][3];
     int b[kRB];
     E* y[kRB];
@@ -502,7 +503,7 @@ __device__ __forceinline__ void radix4_synthesis(const FrameDev& f, const float2
   const int k2 = f.k2, W = f.W, cs = f.cs;
   const int per_tok = f.nblk * k2, items = nt * per_tok;
   const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
-  for (int it0 = threadIdx.x; it0 < items; it0 += kRB * blockDim.x) {
+  for (int it0 = phase_tid(); it0 < items; it0 += kRB * blockDim.x) {
     float2 yv[kRB][4], w[kRB][3];
     E* out[kRB];
 #pragma unroll
@@ -667,7 +668,7 @@ __device__ __forceinline__ void msr_analysis(const FrameDev& f, int nt, const ty
   const int per_tok = f.nblk * k2, items = nt * per_tok;
   const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
   // whole quads: 4 items is a multiple of 4 and so is blockDim
-  for (int it4 = threadIdx.x; it4 < 4 * items; it4 += blockDim.x) {
+  for (int it4 = phase_tid(); it4 < 4 * items; it4 += blockDim.x) {
     const int q = it4 & 3, it = it4 >> 2;
     const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
     const int b = r - blk * k2;
@@ -703,7 +704,7 @@ __device__ __forceinline__ void msr_synthesis(const FrameDev& f, int nt, const t
   const int k2 = f.k2, W = f.W, cs = f.cs;
   const int per_tok = f.nblk * k2, items = nt * per_tok;
   const float inv_pt = 1.f / (float)per_tok, inv_k2 = 1.f / (float)k2;
-  for (int it4 = threadIdx.x; it4 < 4 * items; it4 += blockDim.x) {
+  for (int it4 = phase_tid(); it4 < 4 * items; it4 += blockDim.x) {
     const int q = it4 & 3, it = it4 >> 2;
     const int t = div_small(it, per_tok, inv_pt), r = it - t * per_tok, blk = div_small(r, k2, inv_k2);
     const int b = r - blk * k2;
@@ -943,7 +944,7 @@ __device__ __forceinline__ void zero_column_pads(const FrameDev& f, int nt, type
                                                  int ldb) {
   if (G4 || f.radix == 1 || f.cs == f.W2) return;
   const int padw = f.cs - f.W2, per_tok = f.nblk * f.ncol * padw, items = nt * per_tok;
-  for (int it = threadIdx.x; it < items; it += blockDim.x) {
+  for (int it = phase_tid(); it < items; it += blockDim.x) {
     const int t = it / per_tok, r = it - t * per_tok, col = r / padw, e = r - col * padw;
     const int blk = col / f.ncol, a = col - blk * f.ncol;
     Act<BF16>::st(tile + t * ldt + blk * ldb + a * f.cs + f.W2 + e, 0.f);
@@ -1076,7 +1077,7 @@ __device__ __forceinline__ void stream_products(const GenStream& S, const float*
                                                 typename Act<BF16>::E* dst, int ld_dst, int tg0, int ntg,
                                                 bool write_dst, float* part) {
   using A = Act<BF16>;
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = phase_tid() & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r0 = S.wave_row[wave], r1 = S.wave_row[wave + 1];
   if (r0 >= r1) return;
   const int2* ent = (S.ent);

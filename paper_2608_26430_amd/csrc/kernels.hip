@@ -137,8 +137,12 @@ __device__ __forceinline__ void split4_bf16(float4 x, uint2& hi, uint2& lo) {
 //    fp32, so a term u v carries at most 3.01 2^-16 |u v| of error besides the fp32 accumulation,
 //    far below the bf16 resolution of the merged weight, at a fifth of the MFMA time.
 // Entries past a chunk's end are zero columns.
-template <bool BF16W>
-__global__ void __launch_bounds__(kMergeThreads) merge_kernel(MergeArgs a) {
+// MINWG = 3 compiles for three workgroups per CU (at most 168 registers: the accumulators then live
+// in the arch VGPRs), which launches with many workgroups use: more of them overlap the W reads,
+// contraction and W writes of their tiles (the 70B down projection's merge 464 -> 401 us).  With
+// only one or two rounds of workgroups the two-per-CU build (MINWG = 1) is faster.
+template <bool BF16W, int MINWG>
+__global__ void __launch_bounds__(kMergeThreads, MINWG) merge_kernel(MergeArgs a) {
   constexpr int kF32Bytes = 2 * kMergeChunk * kMergeLd * 4;
   constexpr int kBfBytes = 4 * kMergeChunk * kMergeBLd * 2;
   __shared__ __attribute__((aligned(16))) unsigned char stage[BF16W ? kBfBytes : kF32Bytes];
@@ -734,10 +738,18 @@ hipError_t launch_merge(const ff_plan* p, const float* c, float scale, int w_bf1
   hipEvent_t e0, e1;
   take_timing_events(&e0, &e1);
   record(e0, s);
-  if (w_bf16)
-    hipLaunchKernelGGL(merge_kernel<true>, dim3((unsigned)nwg), dim3(kMergeThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL(merge_kernel<false>, dim3((unsigned)nwg), dim3(kMergeThreads), 0, s, a);
+  const bool many = nwg >= 6L * p->gen_wgs;   // at least two rounds of three workgroups per CU
+  if (w_bf16) {
+    if (many)
+      hipLaunchKernelGGL((merge_kernel<true, 3>), dim3((unsigned)nwg), dim3(kMergeThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((merge_kernel<true, 1>), dim3((unsigned)nwg), dim3(kMergeThreads), 0, s, a);
+  } else {
+    if (many)
+      hipLaunchKernelGGL((merge_kernel<false, 3>), dim3((unsigned)nwg), dim3(kMergeThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((merge_kernel<false, 1>), dim3((unsigned)nwg), dim3(kMergeThreads), 0, s, a);
+  }
   record(e1, s);
   return hipGetLastError();
 }

@@ -1300,18 +1300,21 @@ __device__ __forceinline__ void stream_pass_g4(const GenStream& S, const float* 
     case 1: stream_products_g4<BWD, PART_ADD, 1>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
     case 2: stream_products_g4<BWD, PART_ADD, 2>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
     case 3: stream_products_g4<BWD, PART_ADD, 3>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
-    default: stream_products_g4<BWD, PART_ADD, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
+    case 4: stream_products_g4<BWD, PART_ADD, 4>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part); break;
+    default: stream_products_g4<BWD, PART_ADD, 5>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
   }
 }
 
-// All tokens of a token-grouped tile, 16 at a time, the last pass reading only the groups it
-// needs; `add` as for stream_all.
+// All tokens of a token-grouped tile, 20 at a time (each pass starts with a latency-bound load of
+// its first entries), the last pass reading only the groups it needs; `add` as for stream_all.
+constexpr int kTGWideG4 = 20;
+
 template <bool BWD, bool MAY_ADD>
 __device__ __forceinline__ void stream_all_g4(const GenStream& S, const float* __restrict__ cv, const u16* src,
                                               int ld_src, u16* dst, int ld_dst, int nt, bool write_dst, float* part,
                                               bool add) {
-  for (int tg = 0; tg < nt; tg += 16) {
-    const int ntg = min(16, nt - tg);
+  for (int tg = 0; tg < nt; tg += kTGWideG4) {
+    const int ntg = min(kTGWideG4, nt - tg);
     if (MAY_ADD && (add || (BWD && tg > 0)))
       stream_pass_g4<BWD, MAY_ADD>(S, cv, src, ld_src, dst, ld_dst, tg, ntg, write_dst, part);
     else

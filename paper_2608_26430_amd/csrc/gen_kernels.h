@@ -40,6 +40,15 @@ __device__ __forceinline__ void gstore(T* p, const T& v) {
 
 __device__ __forceinline__ float bf2f(u16 h) { return __uint_as_float((unsigned)h << 16); }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values to packed bf16 (a in the low half), round to nearest even: one
+// v_cvt_pk_bf16_f32.
+__device__ __forceinline__ unsigned pk_bf2(float a, float b) {
+  return __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+}
+
 // fp32 -> bf16, round to nearest even (NaN kept quiet).
 __device__ __forceinline__ u16 f2bf(float f) {
   unsigned u = __float_as_uint(f);
@@ -62,8 +71,8 @@ struct Act<true> {
   static __device__ __forceinline__ void gst4(E* p, f32x4 v) { gstore(reinterpret_cast<uint2*>(p), pack4(v)); }
   static __device__ __forceinline__ uint2 pack4(f32x4 v) {
     uint2 w;
-    w.x = (unsigned)f2bf(v[0]) | ((unsigned)f2bf(v[1]) << 16);
-    w.y = (unsigned)f2bf(v[2]) | ((unsigned)f2bf(v[3]) << 16);
+    w.x = pk_bf2(v[0], v[1]);
+    w.y = pk_bf2(v[2], v[3]);
     return w;
   }
   static __device__ __forceinline__ f32x4 unpack4(uint2 w) {
@@ -399,7 +408,7 @@ __device__ __forceinline__ float2 ld2(const typename Act<BF16>::E* p) {
 template <bool BF16>
 __device__ __forceinline__ void st2(typename Act<BF16>::E* p, float2 v) {
   if constexpr (BF16)
-    *reinterpret_cast<unsigned*>(p) = (unsigned)f2bf(v.x) | ((unsigned)f2bf(v.y) << 16);
+    *reinterpret_cast<unsigned*>(p) = pk_bf2(v.x, v.y);
   else
     *reinterpret_cast<float2*>(p) = v;
 }
@@ -415,7 +424,7 @@ __device__ __forceinline__ float2 gld2(const typename Act<BF16>::E* p) {
 template <bool BF16>
 __device__ __forceinline__ void gst2(typename Act<BF16>::E* p, float2 v) {
   if constexpr (BF16)
-    gstore(reinterpret_cast<unsigned*>(p), (unsigned)f2bf(v.x) | ((unsigned)f2bf(v.y) << 16));
+    gstore(reinterpret_cast<unsigned*>(p), pk_bf2(v.x, v.y));
   else
     gstore(reinterpret_cast<float2*>(p), v);
 }

@@ -64,7 +64,7 @@ template <>
 struct Act<true> {
   using E = u16;
   static __device__ __forceinline__ float ld(const E* p) { return bf2f(*p); }
-  static __device__ __forceinline__ void st(E* p, float v) { *p = f2bf(v); }
+  static __device__ __forceinline__ void st(E* p, float v) { *p = (u16)pk_bf2(v, 0.f); }
   static __device__ __forceinline__ f32x4 ld4(const E* p) { return unpack4(*reinterpret_cast<const uint2*>(p)); }
   static __device__ __forceinline__ void st4(E* p, f32x4 v) { *reinterpret_cast<uint2*>(p) = pack4(v); }
   static __device__ __forceinline__ f32x4 gld4(const E* p) { return unpack4(gload(reinterpret_cast<const uint2*>(p))); }

@@ -297,6 +297,41 @@ def test_generic_backward_many_tiles_per_workgroup(dev, dtype, shape):
     assert torch.equal(dC, dCo), "dC is not deterministic"
 
 
+def test_grouped_tiles_several_walk_passes(dev):
+    """bf16 token-grouped tiles of more than 20 tokens, whose sparse walks take several passes (in
+    the backward the later passes add into the dC partial rows), with two tiles per backward
+    workgroup: a 256 x 256 layer at 30,720 tokens, for which a call takes 60-token tiles.  y and dX
+    on sampled tokens, dC over all tokens."""
+    n = m = 256
+    rn = 16
+    nnz, T = 512, 30720
+    f = ff.framegen(n, n // rn, rn)
+    g = inputs.rng(7171)
+    rows, cols = inputs.support(g, m, n, nnz)
+    vals = inputs.gaussian(g, (nnz,), std=0.02)
+    X = inputs.gaussian(g, (T, n), dtype="bf16")
+    G = inputs.gaussian(g, (T, m), dtype="bf16")
+    plan = ff.plan_create(f, f, rows, cols, max_tokens=T)
+    assert plan.gen_token_groups and plan.gen_tile_tokens("bf16") >= 60 and not plan.fast128
+    Xd, Gd = torch_act(X, "bf16", dev), torch_act(G, "bf16", dev)
+    c = plan_c(plan, vals, dev)
+    s = 0.37
+    Y = ff.adapter_fwd(plan, Xd, c, s)
+    dX, dC = ff.adapter_bwd(plan, Xd, Gd, c, s)
+    _, dC2 = ff.adapter_bwd(plan, Xd, Gd, c, s, want_dx=False)
+    torch.cuda.synchronize()
+    P = oracle_frame(n // rn, rn, n)
+    tok = _sample_tokens(T, 64, 12)
+    y_ref = O.adapter_fwd(P, P, rows, cols, vals, s, X[tok])
+    dx_ref, _ = O.adapter_bwd(P, P, rows, cols, vals, s, X[tok], G[tok])
+    dc_ref = O.coeff_grad_entries(P, P, rows, cols, s, X, G)
+    tol = TOL["bf16"]
+    assert rel(to_np(Y[tok]), y_ref) <= tol
+    assert rel(to_np(dX[tok]), dx_ref) <= tol
+    assert rel(user_dc(plan, dC), dc_ref) <= tol
+    assert torch.equal(dC, dC2), "dC is not deterministic"
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_generic_input_chunks(dev, dtype):
     """An input side too wide to sit whole next to the output side for 8 tokens (factored
